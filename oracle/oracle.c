@@ -1,0 +1,691 @@
+/*
+ * oracle.c -- plain, slow, obviously-correct CPU evaluator of candidate
+ * deployment plans for heterogeneous LLM training (arXiv 2508.05370).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the reference against which the
+ * HIP path is checked.  Only tests/, the smoke entry point and the CPU
+ * baseline leg of the benchmark may load it.  It shares no code, header,
+ * table or constant generator with the HIP library.
+ *
+ * Every quantity is an unsigned integer; time is picoseconds.  Each step
+ * follows the paper's statement of the problem:
+ *   - input description: model, framework (device groups, TP/PP/DP degrees,
+ *     parallelism-to-device-group mapping) and heterogeneous topology
+ *     (Sec. 4.2 "Input Description", Tables 5 and 6);
+ *   - a device group (DG) forms one pipeline replica; the DP group spans all
+ *     replicas (Sec. 3 "Device grouping");
+ *   - non-uniform layer and batch partitioning (Sec. 3 "Non-uniform workload
+ *     partitioning");
+ *   - exposed communication: TP exposed in forward only, PP in both passes,
+ *     DP after the backward pass (Table 1);
+ *   - interconnect delay = jumbo frame bits / unidirectional bandwidth, two
+ *     PCIe trips for inter-node traffic (Sec. 5 "Interconnect configuration");
+ *   - the slowest link or device of a collective sets its time (Sec. 4.1
+ *     [C4], Sec. 5 [Q2]).
+ * Where the paper is silent the reading used is named R1..R30 in comments;
+ * the design notes of the repository list every reading.
+ *
+ * Parity notes: the recurrence, the collective formulas, the interconnect
+ * delays, the parameter counts and the FLOP counts are pinned by tests
+ * (closed forms, Table 5, Table 6, Table 1, a brute-force event simulator).
+ * The per-op byte accounting of the roofline (R6/R8) has no printed value
+ * to compare against: parity unpinned beyond scaling invariants.
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <stdio.h>
+#include <pthread.h>
+
+#define OR_INVALID UINT64_MAX
+#define OR_MAXK 16
+#define OR_MAXS 16
+#define OR_MAXG 4
+
+/* ------------------------------------------------------------------ */
+/* checked integer arithmetic: the oracle never wraps silently         */
+/* ------------------------------------------------------------------ */
+static void or_die(const char* what) {
+  fprintf(stderr, "oracle: arithmetic overflow in %s\n", what);
+  abort();
+}
+static uint64_t add(uint64_t a, uint64_t b) {
+  uint64_t r;
+  if (__builtin_add_overflow(a, b, &r)) or_die("add");
+  return r;
+}
+static uint64_t mul(uint64_t a, uint64_t b) {
+  uint64_t r;
+  if (__builtin_mul_overflow(a, b, &r)) or_die("mul");
+  return r;
+}
+/* R1: every division rounds up. */
+static uint64_t cdiv(uint64_t a, uint64_t b) { return a / b + (a % b != 0); }
+static uint64_t umax(uint64_t a, uint64_t b) { return a > b ? a : b; }
+
+/* ------------------------------------------------------------------ */
+/* inputs                                                              */
+/* ------------------------------------------------------------------ */
+typedef struct {
+  uint64_t L, h, heads, kv_heads, ffn, gated, vocab, learned_pos, seq, e;
+  uint64_t gbs, n_mbs, mbs[4], grad_bytes, param_bytes, E, topk, effn;
+  uint32_t* q; /* [L][E] expert shares in units of 2^-16 */
+} or_model;
+
+typedef struct {
+  uint64_t K;
+  uint64_t n_nodes[OR_MAXK], dpn[OR_MAXK], tflops[OR_MAXK], hbm[OR_MAXK];
+  uint64_t intra[OR_MAXK], pcie[OR_MAXK], nic[OR_MAXK];
+  uint64_t a_intra[OR_MAXK], a_pcie[OR_MAXK], a_nic[OR_MAXK];
+  uint64_t dev_off[OR_MAXK], node_off[OR_MAXK];
+  uint32_t* nic_dev;    /* NULL or per-device NIC MB/s, pool order */
+  uint32_t* intra_node; /* NULL or per-node intra MB/s, pool order */
+} or_cluster;
+
+typedef struct {
+  or_model m;
+  or_cluster c;
+  uint64_t Vp; /* vocabulary padded to a multiple of 128 (R7) */
+  /* memo of per-layer forward/backward times, computed by the plain
+   * per-layer functions below: [k][tpl][mi][epl][l] */
+  uint64_t* lf;
+  uint64_t* lb;
+} or_ctx;
+
+/* ------------------------------------------------------------------ */
+/* R2: roofline time of one op on device type k                        */
+/* ------------------------------------------------------------------ */
+static uint64_t op_time(const or_ctx* x, int k, uint64_t F, uint64_t B) {
+  uint64_t tc = cdiv(F, x->c.tflops[k]);               /* F / (TFLOPS*1e12) s = F/TFLOPS ps */
+  uint64_t tm = cdiv(mul(1000, B), x->c.hbm[k]);       /* B / (GB/s*1e9) s = 1000*B/GBps ps */
+  return umax(tc, tm);
+}
+
+/* an op is (F flops, B bytes); a layer is a list of ops */
+typedef struct { uint64_t F, B; } op;
+typedef struct { op v[16]; int n; } oplist;
+
+static void push(oplist* l, uint64_t F, uint64_t B) { l->v[l->n].F = F; l->v[l->n].B = B; l->n++; }
+/* GEMM [m x k] x [k x n]: 2mkn flops; reads A and B, writes C */
+static void push_gemm(oplist* l, uint64_t m, uint64_t k, uint64_t n, uint64_t e) {
+  push(l, mul(2, mul(m, mul(k, n))), mul(e, add(add(mul(m, k), mul(k, n)), mul(m, n))));
+}
+
+/* forward time of a list; backward evaluates every op with 2F and 2B (R12) */
+static uint64_t list_fwd(const or_ctx* x, int k, const oplist* l) {
+  uint64_t t = 0;
+  for (int i = 0; i < l->n; ++i) t = add(t, op_time(x, k, l->v[i].F, l->v[i].B));
+  return t;
+}
+static uint64_t list_bwd(const or_ctx* x, int k, const oplist* l) {
+  uint64_t t = 0;
+  for (int i = 0; i < l->n; ++i) t = add(t, op_time(x, k, mul(2, l->v[i].F), mul(2, l->v[i].B)));
+  return t;
+}
+
+/* attention + norms + residuals of one transformer layer, per TP rank
+ * (R6/R8).  T = b*s tokens, hq = h/t query width, hkv = kv width per rank. */
+static void attn_ops(const or_ctx* x, uint64_t t, uint64_t b, oplist* l) {
+  const or_model* m = &x->m;
+  uint64_t T = b * m->seq, e = m->e, h = m->h;
+  uint64_t hd = h / m->heads, hq = h / t, hkv = m->kv_heads * hd / t;
+  push(l, 0, mul(2, mul(T, mul(h, e))));                                   /* norm1 */
+  push_gemm(l, T, h, hq + 2 * hkv, e);                                     /* QKV projection */
+  push(l, mul(4, mul(b, mul(m->seq, mul(m->seq, hq)))),                    /* attention core, non-causal count */
+       mul(e, mul(b, mul(m->seq, 2 * hq + 2 * hkv))));                     /* read Q,K,V write O */
+  push_gemm(l, T, hq, h, e);                                               /* output projection */
+  push(l, 0, mul(3, mul(T, mul(h, e))));                                   /* residual add */
+  push(l, 0, mul(2, mul(T, mul(h, e))));                                   /* norm2 */
+}
+/* dense MLP, per TP rank: gated (three matrices) or plain (two) */
+static void mlp_ops(const or_ctx* x, uint64_t t, uint64_t T, uint64_t f, int gated, oplist* l) {
+  uint64_t e = x->m.e, h = x->m.h, ft = f / t;
+  if (gated) {
+    push_gemm(l, T, h, 2 * ft, e);                                         /* up + gate */
+    push(l, 0, mul(3, mul(T, mul(ft, e))));                                /* activation * gate */
+  } else {
+    push_gemm(l, T, h, ft, e);                                             /* up */
+    push(l, 0, mul(2, mul(T, mul(ft, e))));                                /* activation */
+  }
+  push_gemm(l, T, ft, h, e);                                               /* down */
+}
+
+/* R9: expert part of an MoE layer.  EP rank j hosts experts
+ * [j*E/ep, (j+1)*E/ep); expert e receives cdiv(ep*T*topk*q, 2^16) tokens;
+ * the layer waits for the slowest EP rank (Sec. 4.1 [C4]). */
+static uint64_t expert_time(const or_ctx* x, int k, uint64_t t, uint64_t b, uint64_t ep, uint64_t layer, int bwd) {
+  const or_model* m = &x->m;
+  uint64_t T = b * m->seq, per = m->E / ep, worst = 0;
+  for (uint64_t j = 0; j < ep; ++j) {
+    uint64_t sum = 0;
+    for (uint64_t ex = j * per; ex < (j + 1) * per; ++ex) {
+      uint64_t n_e = cdiv(mul(mul(ep, T), mul(m->topk, m->q[layer * m->E + ex])), 65536);
+      oplist l = {{{0, 0}}, 0};
+      mlp_ops(x, t, n_e, m->effn, 1, &l);
+      sum = add(sum, bwd ? list_bwd(x, k, &l) : list_fwd(x, k, &l));
+    }
+    worst = umax(worst, sum);
+  }
+  return worst;
+}
+
+/* time of transformer layer `layer` on type k, TP t, micro-batch b, EP ep */
+static uint64_t layer_time(const or_ctx* x, int k, uint64_t t, uint64_t b, uint64_t ep, uint64_t layer, int bwd) {
+  const or_model* m = &x->m;
+  uint64_t T = b * m->seq;
+  oplist l = {{{0, 0}}, 0};
+  attn_ops(x, t, b, &l);
+  if (m->E == 0) {
+    mlp_ops(x, t, T, m->ffn, (int)m->gated, &l);
+  } else {
+    push_gemm(&l, T, m->h, m->E, m->e);                                    /* router, replicated */
+  }
+  push(&l, 0, mul(3, mul(T, mul(m->h, m->e))));                            /* residual add */
+  uint64_t tt = bwd ? list_bwd(x, k, &l) : list_fwd(x, k, &l);
+  if (m->E) tt = add(tt, expert_time(x, k, t, b, ep, layer, bwd));
+  return tt;
+}
+
+/* input embedding (stage 0): gather rows, plus learned positions if any */
+static uint64_t embed_time(const or_ctx* x, int k, uint64_t b, int bwd) {
+  const or_model* m = &x->m;
+  uint64_t T = b * m->seq;
+  uint64_t B = mul(m->e, mul(T, mul(m->h, 2 + 2 * (m->learned_pos > 0))));
+  return bwd ? op_time(x, k, 0, mul(2, B)) : op_time(x, k, 0, B);
+}
+/* output head (last stage): final norm, vocab-parallel LM head, loss (R13) */
+static uint64_t head_time(const or_ctx* x, int k, uint64_t t, uint64_t b, int bwd) {
+  const or_model* m = &x->m;
+  uint64_t T = b * m->seq, vt = x->Vp / t;
+  oplist l = {{{0, 0}}, 0};
+  push(&l, 0, mul(2, mul(T, mul(m->h, m->e))));
+  push_gemm(&l, T, m->h, vt, m->e);
+  push(&l, 0, mul(2, mul(T, mul(vt, m->e))));
+  return bwd ? list_bwd(x, k, &l) : list_fwd(x, k, &l);
+}
+
+/* parameters held by one TP rank (biases ignored, R13) */
+static uint64_t layer_params_dense(const or_ctx* x, uint64_t t) {
+  const or_model* m = &x->m;
+  uint64_t h = m->h, hd = h / m->heads, hq = h / t, hkv = m->kv_heads * hd / t;
+  uint64_t p = h * (hq + 2 * hkv) + hq * h + 2 * h;                      /* attention + two norms */
+  if (m->E == 0) p += (m->gated ? 3 : 2) * h * (m->ffn / t);
+  else p += h * m->E;                                                    /* router */
+  return p;
+}
+static uint64_t layer_params_expert(const or_ctx* x, uint64_t t, uint64_t ep) {
+  const or_model* m = &x->m;
+  if (m->E == 0) return 0;
+  return (m->E / ep) * 3 * m->h * (m->effn / t);
+}
+static uint64_t embed_params(const or_ctx* x, uint64_t t) { return x->Vp * x->m.h / t + x->m.learned_pos * x->m.h; }
+static uint64_t head_params(const or_ctx* x, uint64_t t) { return x->Vp * x->m.h / t + x->m.h; }
+
+/* ------------------------------------------------------------------ */
+/* links (R3, R4, R5)                                                  */
+/* ------------------------------------------------------------------ */
+/* ps per byte in units of 2^-16; 0 = tier absent */
+static uint64_t beta_q(uint64_t MBps) { return MBps ? cdiv(65536ull * 1000000ull, MBps) : 0; }
+static uint64_t link_time(uint64_t bytes, uint64_t bq) {
+  unsigned __int128 p = (unsigned __int128)bytes * bq;
+  unsigned __int128 r = p / 65536 + (p % 65536 != 0);
+  if (r >> 64) or_die("link_time");
+  return (uint64_t)r;
+}
+static uint64_t nic_bq(const or_ctx* x, int k, uint64_t dev) {
+  return beta_q(x->c.nic_dev ? x->c.nic_dev[x->c.dev_off[k] + dev] : x->c.nic[k]);
+}
+static uint64_t intra_bq(const or_ctx* x, int k, uint64_t node) {
+  return beta_q(x->c.intra_node ? x->c.intra_node[x->c.node_off[k] + node] : x->c.intra[k]);
+}
+/* one endpoint of an inter-node path: GPU->switch->NIC (two PCIe trips)
+ * plus NIC processing (Sec. 5, Table 5) */
+static uint64_t alpha_side(const or_ctx* x, int k) { return add(mul(2, x->c.a_pcie[k]), x->c.a_nic[k]); }
+
+/* worst NIC over devices [lo, lo+n) of pool k */
+static uint64_t nic_max(const or_ctx* x, int k, uint64_t lo, uint64_t n) {
+  uint64_t w = 0;
+  for (uint64_t d = lo; d < lo + n; ++d) w = umax(w, nic_bq(x, k, d));
+  return w;
+}
+/* worst intra-node fabric over the nodes touched by devices [lo, lo+n) */
+static uint64_t intra_max(const or_ctx* x, int k, uint64_t lo, uint64_t n) {
+  uint64_t w = 0;
+  for (uint64_t d = lo; d < lo + n; ++d) w = umax(w, intra_bq(x, k, d / x->c.dpn[k]));
+  return w;
+}
+
+/* ------------------------------------------------------------------ */
+/* pipeline: non-interleaved 1F1B (R24, R25)                           */
+/* ------------------------------------------------------------------ */
+/* Stage s runs, in order: W = min(S-1-s, M) forwards, then M-W pairs
+ * (forward, backward), then the remaining W backwards.  F(s,m) may start
+ * once F(s-1,m) has ended and its activation crossed hop s-1; B(s,m) once
+ * B(s+1,m) has ended and its gradient crossed hop s; on the last stage
+ * B(S-1,m) needs F(S-1,m).  A stage runs one op at a time; sends do not
+ * block the sender.  The result is the longest path of that DAG, so any
+ * evaluation order that respects it gives the same numbers.  This one
+ * sweeps the stages repeatedly, advancing each while its next op is
+ * ready. */
+typedef struct { int isB; uint64_t m; } slot;
+static slot op_at(uint64_t S, uint64_t M, uint64_t s, uint64_t pos) {
+  uint64_t W = (S - 1 - s) < M ? (S - 1 - s) : M;
+  slot r;
+  if (pos < W) { r.isB = 0; r.m = pos; return r; }
+  if (pos < 2 * M - W) {
+    uint64_t i = (pos - W) / 2;
+    if ((pos - W) % 2 == 0) { r.isB = 0; r.m = W + i; } else { r.isB = 1; r.m = i; }
+    return r;
+  }
+  r.isB = 1; r.m = pos - M; /* B(M-W+j) sits at position 2M-W+j */
+  return r;
+}
+
+/* end[s] := end time of stage s's last op.  scratch holds 2*S*M words. */
+static void pipeline(uint64_t S, uint64_t M, const uint64_t* f, const uint64_t* b, const uint64_t* c,
+                     uint64_t* end, uint64_t* scratch) {
+  uint64_t* endF = scratch;          /* [S][M], OR_INVALID = not yet run */
+  uint64_t* endB = scratch + S * M;
+  for (uint64_t i = 0; i < 2 * S * M; ++i) scratch[i] = OR_INVALID;
+  uint64_t pos[OR_MAXS], last[OR_MAXS];
+  for (uint64_t s = 0; s < S; ++s) { pos[s] = 0; last[s] = 0; }
+  int progress = 1;
+  while (progress) {
+    progress = 0;
+    for (uint64_t s = 0; s < S; ++s) {
+      while (pos[s] < 2 * M) {
+        slot o = op_at(S, M, s, pos[s]);
+        uint64_t ready;
+        if (!o.isB) {
+          if (s == 0) ready = 0;
+          else if (endF[(s - 1) * M + o.m] == OR_INVALID) break;
+          else ready = add(endF[(s - 1) * M + o.m], c[s - 1]);
+        } else {
+          if (s == S - 1) {
+            if (endF[s * M + o.m] == OR_INVALID) break;
+            ready = endF[s * M + o.m];
+          } else if (endB[(s + 1) * M + o.m] == OR_INVALID) break;
+          else ready = add(endB[(s + 1) * M + o.m], c[s]);
+        }
+        uint64_t start = umax(last[s], ready);
+        uint64_t e = add(start, o.isB ? b[s] : f[s]);
+        if (o.isB) endB[s * M + o.m] = e; else endF[s * M + o.m] = e;
+        last[s] = e;
+        pos[s]++;
+        progress = 1;
+      }
+    }
+  }
+  for (uint64_t s = 0; s < S; ++s) {
+    if (pos[s] != 2 * M) { fprintf(stderr, "oracle: pipeline deadlock\n"); abort(); }
+    end[s] = last[s];
+  }
+}
+
+/* ------------------------------------------------------------------ */
+/* one plan                                                            */
+/* ------------------------------------------------------------------ */
+typedef struct {
+  uint64_t tp, ep, S, G, zero, mi;
+  uint64_t cut[OR_MAXS];
+  uint64_t reps[OR_MAXG], nmb[OR_MAXG];
+  int type[OR_MAXG][OR_MAXS];
+} or_plan;
+
+/* per-stage quantities of one plan, exposed for tests */
+typedef struct {
+  uint64_t valid, S, G;
+  uint64_t M[OR_MAXG];
+  uint64_t f[OR_MAXG][OR_MAXS], b[OR_MAXG][OR_MAXS], c[OR_MAXG][OR_MAXS];
+  uint64_t tdp[OR_MAXS];
+  uint64_t end[OR_MAXG][OR_MAXS];
+  uint64_t time;
+} or_detail;
+
+static int decode(const or_ctx* x, uint32_t hdr, const uint8_t* cut, const uint32_t* cls,
+                  const uint64_t* types, int64_t stride, int64_t i, or_plan* p) {
+  const or_model* m = &x->m;
+  if (hdr >> 13) return 0;                                   /* V7 reserved bits */
+  p->tp = 1ull << (hdr & 3);
+  p->ep = 1ull << ((hdr >> 2) & 3);
+  p->S = ((hdr >> 4) & 15) + 1;
+  p->G = ((hdr >> 8) & 3) + 1;
+  p->zero = (hdr >> 10) & 1;
+  p->mi = (hdr >> 11) & 3;
+  if (p->mi >= m->n_mbs) return 0;                           /* V8 */
+  uint64_t prev = 0;
+  for (uint64_t s = 0; s < p->S; ++s) {                      /* V2 */
+    p->cut[s] = cut[s * stride + i];
+    if (p->cut[s] <= prev) return 0;
+    prev = p->cut[s];
+  }
+  if (p->cut[p->S - 1] != m->L) return 0;
+  uint64_t batch = 0;
+  for (uint64_t g = 0; g < p->G; ++g) {
+    uint32_t w = cls[g * stride + i];
+    p->reps[g] = w & 0xffff;
+    p->nmb[g] = w >> 16;
+    if (p->reps[g] == 0) return 0;                           /* V1 */
+    if (p->nmb[g] < p->reps[g]) return 0;                    /* V4 every replica gets work */
+    batch += p->nmb[g] * m->mbs[p->mi];
+    uint64_t tv = types[g * stride + i];
+    for (uint64_t s = 0; s < p->S; ++s) {
+      p->type[g][s] = (int)((tv >> (4 * s)) & 15);
+      if ((uint64_t)p->type[g][s] >= x->c.K) return 0;       /* V1 */
+      if (x->c.dpn[p->type[g][s]] % p->tp) return 0;         /* V5 TP stays inside a node */
+    }
+  }
+  if (batch != m->gbs) return 0;                             /* V4 exactly the global batch (R14) */
+  if (m->E == 0) {                                           /* V3 */
+    if (p->ep != 1) return 0;
+  } else {
+    if (p->ep > m->E || m->E % p->ep) return 0;
+    for (uint64_t g = 0; g < p->G; ++g) if (p->reps[g] % p->ep) return 0;
+  }
+  if (m->heads % p->tp || m->kv_heads % p->tp) return 0;     /* V5 */
+  if (m->E == 0 && m->ffn % p->tp) return 0;
+  if (m->E != 0 && m->effn % p->tp) return 0;
+  uint64_t need[OR_MAXK] = {0};                              /* V6 capacity */
+  for (uint64_t g = 0; g < p->G; ++g)
+    for (uint64_t s = 0; s < p->S; ++s) need[p->type[g][s]] += p->reps[g] * p->tp;
+  for (uint64_t k = 0; k < x->c.K; ++k)
+    if (need[k] > x->c.n_nodes[k] * x->c.dpn[k]) return 0;
+  return 1;
+}
+
+static const uint64_t* LF(const or_ctx* x, int k, uint64_t tpl, uint64_t mi, uint64_t epl) {
+  return x->lf + ((((uint64_t)k * 4 + tpl) * 4 + mi) * 4 + epl) * x->m.L;
+}
+static const uint64_t* LB(const or_ctx* x, int k, uint64_t tpl, uint64_t mi, uint64_t epl) {
+  return x->lb + ((((uint64_t)k * 4 + tpl) * 4 + mi) * 4 + epl) * x->m.L;
+}
+static uint64_t log2u(uint64_t v) { uint64_t r = 0; while ((1ull << r) < v) ++r; return r; }
+
+/* one DP ring phase: `steps` transfers of `chunk` bytes each (R23) */
+static uint64_t ring(uint64_t steps, uint64_t chunk, uint64_t alpha, uint64_t bq) {
+  return add(mul(steps, alpha), link_time(mul(steps, chunk), bq));
+}
+/* gradient sync of one stage over a p-member ring (R11, R26, R27) */
+static uint64_t dp_sync(uint64_t p, uint64_t zero, uint64_t grads, uint64_t params, uint64_t alpha, uint64_t bq) {
+  if (p <= 1) return 0;
+  if (!zero) return ring(2 * (p - 1), cdiv(grads, p), alpha, bq);          /* ring all-reduce */
+  return add(ring(p - 1, cdiv(grads, p), alpha, bq),                       /* reduce-scatter of gradients */
+             ring(p - 1, cdiv(params, p), alpha, bq));                     /* all-gather of parameters */
+}
+
+static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t* scratch) {
+  const or_model* m = &x->m;
+  const or_cluster* cl = &x->c;
+  uint64_t S = p->S, G = p->G, tp = p->tp, ep = p->ep;
+  uint64_t tpl = log2u(tp), epl = log2u(ep);
+  uint64_t b = m->mbs[p->mi];
+  uint64_t T = b * m->seq;
+  uint64_t act = mul(T, mul(m->h, m->e));                      /* one micro-batch activation (Table 1, R10) */
+  d->valid = 1; d->S = S; d->G = G;
+
+  /* R18 canonical packing: per pool, a bump pointer in (class, stage) order */
+  uint64_t ptr[OR_MAXK] = {0}, base[OR_MAXG][OR_MAXS];
+  for (uint64_t g = 0; g < G; ++g)
+    for (uint64_t s = 0; s < S; ++s) {
+      base[g][s] = ptr[p->type[g][s]];
+      ptr[p->type[g][s]] += p->reps[g] * tp;
+    }
+
+  for (uint64_t g = 0; g < G; ++g) {
+    uint64_t n = p->reps[g] * tp;                              /* devices of one (class, stage) */
+    d->M[g] = cdiv(p->nmb[g], p->reps[g]);                     /* R16 */
+    for (uint64_t s = 0; s < S; ++s) {
+      int k = p->type[g][s];
+      uint64_t lo = s ? p->cut[s - 1] : 0, hi = p->cut[s], ns = hi - lo;
+      /* compute: sum of this stage's layers (Sec. 3 non-uniform layer split) */
+      uint64_t Fc = 0, Bc = 0;
+      for (uint64_t l = lo; l < hi; ++l) {
+        Fc = add(Fc, LF(x, k, tpl, p->mi, epl)[l]);
+        Bc = add(Bc, LB(x, k, tpl, p->mi, epl)[l]);
+      }
+      if (s == 0) { Fc = add(Fc, embed_time(x, k, b, 0)); Bc = add(Bc, embed_time(x, k, b, 1)); }
+      if (s == S - 1) { Fc = add(Fc, head_time(x, k, tp, b, 0)); Bc = add(Bc, head_time(x, k, tp, b, 1)); }
+      /* TP all-reduce, exposed in forward only (Table 1, R22) */
+      uint64_t tpf = 0;
+      if (tp > 1) {
+        uint64_t nar = 2 * ns + (s == 0);
+        uint64_t steps = nar * 2 * (tp - 1);
+        tpf = add(mul(steps, cl->a_intra[k]), link_time(mul(steps, cdiv(act, tp)), intra_max(x, k, base[g][s], n)));
+      }
+      /* MoE all-to-all, dispatch + combine per layer in each pass (R20) */
+      uint64_t epc = 0;
+      if (m->E && ep > 1) {
+        int intra = 1;
+        for (uint64_t grp = 0; grp < p->reps[g] / ep; ++grp) {
+          uint64_t first = base[g][s] + grp * ep * tp, last = first + ep * tp - 1;
+          if (first / cl->dpn[k] != last / cl->dpn[k]) intra = 0;
+        }
+        uint64_t alpha, bq;
+        if (intra) { alpha = cl->a_intra[k]; bq = intra_max(x, k, base[g][s], n); }
+        else { alpha = mul(2, alpha_side(x, k)); bq = umax(nic_max(x, k, base[g][s], n), beta_q(cl->pcie[k])); }
+        uint64_t bytes = 0;
+        for (uint64_t l = lo; l < hi; ++l) {
+          uint64_t per = m->E / ep, wmax = 0;
+          for (uint64_t j = 0; j < ep; ++j) {
+            uint64_t w = 0;
+            for (uint64_t ex = j * per; ex < (j + 1) * per; ++ex) w += m->q[l * m->E + ex];
+            wmax = umax(wmax, w);
+          }
+          bytes = add(bytes, cdiv(mul(mul(ep - 1, T), mul(m->topk, mul(wmax, mul(m->h, m->e)))), 65536));
+        }
+        epc = add(mul(ns * 2 * (ep - 1), alpha), link_time(mul(2, bytes), bq));
+      }
+      d->f[g][s] = add(add(Fc, tpf), epc);
+      d->b[g][s] = add(Bc, epc);
+      /* PP hop s -> s+1: activation forward, gradient backward (Table 1) */
+      d->c[g][s] = 0;
+      if (s + 1 < S) {
+        int k2 = p->type[g][s + 1];
+        int intra = (k == k2);
+        for (uint64_t r = 0; intra && r < p->reps[g]; ++r)
+          if ((base[g][s] + r * tp) / cl->dpn[k] != (base[g][s + 1] + r * tp) / cl->dpn[k]) intra = 0;
+        uint64_t alpha, bq;
+        if (intra) {
+          alpha = cl->a_intra[k];
+          bq = umax(intra_max(x, k, base[g][s], n), intra_max(x, k, base[g][s + 1], n));
+        } else {
+          alpha = add(alpha_side(x, k), alpha_side(x, k2));
+          bq = umax(umax(nic_max(x, k, base[g][s], n), nic_max(x, k2, base[g][s + 1], n)),
+                    umax(beta_q(cl->pcie[k]), beta_q(cl->pcie[k2])));
+        }
+        d->c[g][s] = add(alpha, link_time(act, bq));
+      }
+    }
+  }
+
+  /* DP sync per stage across all classes (Sec. 3: DP group = all replicas) */
+  uint64_t p_all = 0;
+  for (uint64_t g = 0; g < G; ++g) p_all += p->reps[g];
+  for (uint64_t s = 0; s < S; ++s) {
+    int k0 = p->type[0][s], same = 1;
+    uint64_t nlo = UINT64_MAX, nhi = 0;
+    for (uint64_t g = 0; g < G; ++g) {
+      if (p->type[g][s] != k0) same = 0;
+      uint64_t n = p->reps[g] * tp;
+      for (uint64_t dv = base[g][s]; dv < base[g][s] + n; ++dv) {
+        uint64_t node = dv / cl->dpn[p->type[g][s]];
+        if (node < nlo) nlo = node;
+        if (node > nhi) nhi = node;
+      }
+    }
+    uint64_t alpha, bq;
+    if (same && nlo == nhi) { alpha = cl->a_intra[k0]; bq = intra_bq(x, k0, nlo); }
+    else {
+      alpha = 0; bq = 0;
+      for (uint64_t g = 0; g < G; ++g) {
+        int k = p->type[g][s];
+        alpha = umax(alpha, mul(2, alpha_side(x, k)));                    /* R21 */
+        bq = umax(bq, umax(nic_max(x, k, base[g][s], p->reps[g] * tp), beta_q(cl->pcie[k])));
+      }
+    }
+    uint64_t lo = s ? p->cut[s - 1] : 0, hi = p->cut[s];
+    uint64_t pd = (hi - lo) * layer_params_dense(x, tp), pe = (hi - lo) * layer_params_expert(x, tp, ep);
+    if (s == 0) pd += embed_params(x, tp);
+    if (s == S - 1) pd += head_params(x, tp);
+    uint64_t t = dp_sync(p_all, p->zero, mul(m->grad_bytes, pd), mul(m->param_bytes, pd), alpha, bq);
+    if (m->E) t = add(t, dp_sync(p_all / ep, p->zero, mul(m->grad_bytes, pe), mul(m->param_bytes, pe), alpha, bq));
+    d->tdp[s] = t;
+  }
+
+  /* per class pipeline, then T = max over stages (R27, R28) */
+  uint64_t T_iter = 0;
+  for (uint64_t g = 0; g < G; ++g) {
+    pipeline(S, d->M[g], d->f[g], d->b[g], d->c[g], d->end[g], scratch);
+    for (uint64_t s = 0; s < S; ++s) T_iter = umax(T_iter, add(d->end[g][s], d->tdp[s]));
+  }
+  d->time = T_iter;
+}
+
+/* ------------------------------------------------------------------ */
+/* context                                                             */
+/* ------------------------------------------------------------------ */
+/* mp: L h heads kv_heads ffn gated vocab learned_pos seq e gbs n_mbs mbs0..3
+ *     grad_bytes param_bytes E topk effn  (21 words)
+ * cp: K, then for each type k: n_nodes dpn tflops hbm intra pcie nic
+ *     a_intra a_pcie a_nic  (1 + 10K words) */
+or_ctx* oracle_new(const uint64_t* mp, const uint32_t* q, const uint64_t* cp,
+                   const uint32_t* nic_dev, const uint32_t* intra_node) {
+  or_ctx* x = (or_ctx*)calloc(1, sizeof(or_ctx));
+  or_model* m = &x->m;
+  m->L = mp[0]; m->h = mp[1]; m->heads = mp[2]; m->kv_heads = mp[3]; m->ffn = mp[4]; m->gated = mp[5];
+  m->vocab = mp[6]; m->learned_pos = mp[7]; m->seq = mp[8]; m->e = mp[9]; m->gbs = mp[10]; m->n_mbs = mp[11];
+  for (int i = 0; i < 4; ++i) m->mbs[i] = mp[12 + i];
+  m->grad_bytes = mp[16]; m->param_bytes = mp[17]; m->E = mp[18]; m->topk = mp[19]; m->effn = mp[20];
+  if (m->E) {
+    m->q = (uint32_t*)malloc(sizeof(uint32_t) * m->L * m->E);
+    memcpy(m->q, q, sizeof(uint32_t) * m->L * m->E);
+  }
+  or_cluster* c = &x->c;
+  c->K = cp[0];
+  uint64_t dsum = 0, nsum = 0;
+  for (uint64_t k = 0; k < c->K; ++k) {
+    const uint64_t* r = cp + 1 + 10 * k;
+    c->n_nodes[k] = r[0]; c->dpn[k] = r[1]; c->tflops[k] = r[2]; c->hbm[k] = r[3];
+    c->intra[k] = r[4]; c->pcie[k] = r[5]; c->nic[k] = r[6];
+    c->a_intra[k] = r[7]; c->a_pcie[k] = r[8]; c->a_nic[k] = r[9];
+    c->dev_off[k] = dsum; c->node_off[k] = nsum;
+    dsum += r[0] * r[1]; nsum += r[0];
+  }
+  if (nic_dev) { c->nic_dev = (uint32_t*)malloc(4 * dsum); memcpy(c->nic_dev, nic_dev, 4 * dsum); }
+  if (intra_node) { c->intra_node = (uint32_t*)malloc(4 * nsum); memcpy(c->intra_node, intra_node, 4 * nsum); }
+  x->Vp = cdiv(m->vocab, 128) * 128;
+  /* per-layer memo, filled by the per-layer definitions above for every
+   * (type, TP, micro-batch size, EP) whose divisibility holds */
+  uint64_t cells = c->K * 4 * 4 * 4 * m->L;
+  x->lf = (uint64_t*)calloc(cells, 8);
+  x->lb = (uint64_t*)calloc(cells, 8);
+  for (uint64_t k = 0; k < c->K; ++k)
+    for (uint64_t tpl = 0; tpl < 4; ++tpl) {
+      uint64_t t = 1ull << tpl;
+      if (m->heads % t || m->kv_heads % t) continue;
+      if (m->E == 0 && m->ffn % t) continue;
+      if (m->E && m->effn % t) continue;
+      for (uint64_t mi = 0; mi < m->n_mbs; ++mi)
+        for (uint64_t epl = 0; epl < 4; ++epl) {
+          uint64_t ep = 1ull << epl;
+          if (m->E == 0 && ep > 1) continue;
+          if (m->E && (ep > m->E || m->E % ep)) continue;
+          uint64_t* f = x->lf + (((k * 4 + tpl) * 4 + mi) * 4 + epl) * m->L;
+          uint64_t* b = x->lb + (((k * 4 + tpl) * 4 + mi) * 4 + epl) * m->L;
+          for (uint64_t l = 0; l < m->L; ++l) {
+            f[l] = layer_time(x, (int)k, t, m->mbs[mi], ep, l, 0);
+            b[l] = layer_time(x, (int)k, t, m->mbs[mi], ep, l, 1);
+          }
+        }
+    }
+  return x;
+}
+
+void oracle_free(or_ctx* x) {
+  if (!x) return;
+  free(x->m.q); free(x->c.nic_dev); free(x->c.intra_node); free(x->lf); free(x->lb); free(x);
+}
+
+typedef struct {
+  const or_ctx* x;
+  const uint32_t* hdr; const uint8_t* cut; const uint32_t* cls; const uint64_t* types;
+  int64_t stride, lo, hi;
+  uint64_t* out;
+} or_job;
+
+static void* worker(void* arg) {
+  or_job* j = (or_job*)arg;
+  uint64_t Mmax = j->x->m.gbs;                 /* nmb <= global batch, so M <= global batch */
+  uint64_t* scratch = (uint64_t*)malloc(8 * 2 * OR_MAXS * (Mmax + 1));
+  or_detail d;
+  for (int64_t i = j->lo; i < j->hi; ++i) {
+    or_plan p;
+    if (!decode(j->x, j->hdr[i], j->cut, j->cls, j->types, j->stride, i, &p)) { j->out[i] = OR_INVALID; continue; }
+    eval_plan(j->x, &p, &d, scratch);
+    j->out[i] = d.time;
+  }
+  free(scratch);
+  return NULL;
+}
+
+/* Evaluate plans [0, n) of SoA planes with plane stride `stride`. */
+void oracle_eval(const or_ctx* x, const uint32_t* hdr, const uint8_t* cut, const uint32_t* cls,
+                 const uint64_t* types, int64_t stride, int64_t n, uint64_t* out, int nthreads) {
+  if (nthreads < 1) nthreads = 1;
+  if (nthreads > 256) nthreads = 256;
+  pthread_t th[256];
+  or_job jobs[256];
+  for (int t = 0; t < nthreads; ++t) {
+    jobs[t].x = x; jobs[t].hdr = hdr; jobs[t].cut = cut; jobs[t].cls = cls; jobs[t].types = types;
+    jobs[t].stride = stride; jobs[t].out = out;
+    jobs[t].lo = n * t / nthreads; jobs[t].hi = n * (t + 1) / nthreads;
+  }
+  for (int t = 1; t < nthreads; ++t) pthread_create(&th[t], NULL, worker, &jobs[t]);
+  worker(&jobs[0]);
+  for (int t = 1; t < nthreads; ++t) pthread_join(th[t], NULL);
+}
+
+/* Stage-level detail of plan i (for tests and debugging). */
+int oracle_detail(const or_ctx* x, const uint32_t* hdr, const uint8_t* cut, const uint32_t* cls,
+                  const uint64_t* types, int64_t stride, int64_t i, or_detail* d) {
+  memset(d, 0, sizeof(*d));
+  or_plan p;
+  if (!decode(x, hdr[i], cut, cls, types, stride, i, &p)) { d->time = OR_INVALID; return 0; }
+  uint64_t* scratch = (uint64_t*)malloc(8 * 2 * OR_MAXS * (x->m.gbs + 1));
+  eval_plan(x, &p, d, scratch);
+  free(scratch);
+  return 1;
+}
+size_t oracle_detail_size(void) { return sizeof(or_detail); }
+
+/* ------------------------------------------------------------------ */
+/* pieces exposed for pinning                                          */
+/* ------------------------------------------------------------------ */
+void oracle_pipeline(uint64_t S, uint64_t M, const uint64_t* f, const uint64_t* b, const uint64_t* c, uint64_t* end) {
+  uint64_t* scratch = (uint64_t*)malloc(8 * 2 * S * M + 8);
+  pipeline(S, M, f, b, c, end, scratch);
+  free(scratch);
+}
+/* Sec. 5: delay = jumbo frame (9200 B) * 8 / unidirectional Gb/s, in ps, rounded up */
+uint64_t oracle_alpha_ps(uint64_t gbps_unidir) { return cdiv(9200ull * 8 * 1000, gbps_unidir); }
+uint64_t oracle_beta_q(uint64_t MBps) { return beta_q(MBps); }
+uint64_t oracle_link_time(uint64_t bytes, uint64_t bq) { return link_time(bytes, bq); }
+uint64_t oracle_dp_sync(uint64_t p, uint64_t zero, uint64_t grads, uint64_t params, uint64_t alpha, uint64_t MBps) {
+  return dp_sync(p, zero, grads, params, alpha, beta_q(MBps));
+}
+uint64_t oracle_layer_time(const or_ctx* x, int k, uint64_t t, uint64_t b, uint64_t ep, uint64_t layer, int bwd) {
+  return layer_time(x, k, t, b, ep, layer, bwd);
+}
+uint64_t oracle_embed_time(const or_ctx* x, int k, uint64_t b, int bwd) { return embed_time(x, k, b, bwd); }
+uint64_t oracle_head_time(const or_ctx* x, int k, uint64_t t, uint64_t b, int bwd) { return head_time(x, k, t, b, bwd); }
+/* total parameters of the model at TP=1, EP=1: layers, embedding, head */
+uint64_t oracle_param_count(const or_ctx* x, int with_head) {
+  uint64_t p = x->m.L * (layer_params_dense(x, 1) + layer_params_expert(x, 1, 1)) + embed_params(x, 1);
+  if (with_head) p += head_params(x, 1);
+  return p;
+}
+/* parameters of the layers [lo, hi) held by one rank at TP t, EP ep */
+uint64_t oracle_rank_params(const or_ctx* x, uint64_t t, uint64_t ep, uint64_t nlayers) {
+  return nlayers * (layer_params_dense(x, t) + layer_params_expert(x, t, ep));
+}
+uint64_t oracle_act_bytes(const or_ctx* x, uint64_t b) { return b * x->m.seq * x->m.h * x->m.e; }

@@ -1,0 +1,146 @@
+/*
+ * plangen.c -- seeded synthetic candidate-plan generator.
+ *
+ * Input generation only: it draws plan descriptors (parallel degrees, a
+ * non-uniform layer split, replica classes with device types and a
+ * non-uniform micro-batch split) and computes no time.  Both the HIP path
+ * and the CPU oracle consume its output.
+ *
+ * Randomness: SplitMix64 (Steele, Lea, Flood, OOPSLA 2014) used
+ * counter-based: draw(seed, c) = mix(seed + (c + 1) * 0x9E3779B97F4A7C15),
+ * with counter c = plan_index * 4096 + draw_number, so every plan is
+ * reproducible on its own and generation parallelises by index.
+ *
+ * Plan layout (structure of arrays, plane stride `stride`):
+ *   hdr[i]            tp_log2:2 | ep_log2:2 | (pp-1):4 | (G-1):2 | zero:1 | mbs_idx:2 | 0:19
+ *   cut[s*stride+i]   cumulative layer end of stage s (u8)
+ *   cls[c*stride+i]   replicas (low 16 bits) | micro-batches (high 16 bits)
+ *   types[c*stride+i] 4-bit device type of stage s in bits [4s, 4s+4)
+ */
+#include <stdint.h>
+#include <string.h>
+#include <pthread.h>
+
+static uint64_t mix(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+uint64_t plangen_draw(uint64_t seed, uint64_t counter) { return mix(seed + (counter + 1) * 0x9E3779B97F4A7C15ull); }
+
+typedef struct { uint64_t seed, i, d; } rng;
+static uint64_t next(rng* r) { return plangen_draw(r->seed, r->i * 4096 + r->d++); }
+/* uniform integer in [lo, hi] */
+static uint64_t uni(rng* r, uint64_t lo, uint64_t hi) { return lo + next(r) % (hi - lo + 1); }
+
+typedef struct {
+  uint64_t seed;
+  uint32_t L;            /* layers */
+  uint32_t K;            /* device types */
+  uint32_t cap[16];      /* devices per type */
+  uint32_t batches;      /* micro-batches per iteration (global batch / micro-batch size) */
+  uint32_t experts;      /* 0 = dense (EP fixed to 1) */
+} pg_params;
+
+static void gen_one(const pg_params* P, uint64_t i, uint32_t* hdr, uint8_t* cut, uint32_t* cls, uint64_t* types,
+                    int64_t stride, int64_t slot) {
+  rng r = {P->seed, i, 0};
+  uint32_t tpl = 0, pp = 1, epl = 0, G = 0, zero = 0;
+  uint32_t reps[4] = {0}, nmb[4] = {0};
+  uint64_t tv[4] = {0};
+  uint32_t sumreps = 0;
+  for (int attempt = 0; attempt < 16 && G == 0; ++attempt) {
+    r.d = (uint64_t)attempt * 256;
+    tpl = (uint32_t)uni(&r, 0, 3);
+    pp = (uint32_t)uni(&r, 1, 16);
+    epl = 0;
+    if (P->experts) {
+      epl = (uint32_t)uni(&r, 0, 3);
+      while ((1u << epl) > P->experts || P->experts % (1u << epl)) --epl;
+    }
+    uint32_t want = (uint32_t)uni(&r, 1, 4);
+    zero = (uint32_t)uni(&r, 0, 1);
+    uint32_t tp = 1u << tpl, ep = 1u << epl;
+    uint32_t left[16];
+    memcpy(left, P->cap, sizeof(left));
+    sumreps = 0;
+    for (uint32_t c = 0; c < want; ++c) {
+      uint32_t cnt[16] = {0};
+      uint64_t t = 0;
+      for (uint32_t s = 0; s < pp; ++s) {
+        uint64_t k = uni(&r, 0, P->K - 1);
+        t |= k << (4 * s);
+        cnt[k]++;
+      }
+      uint32_t maxr = 0xffffffffu;
+      for (uint32_t k = 0; k < P->K; ++k)
+        if (cnt[k]) { uint32_t m = left[k] / (cnt[k] * tp); if (m < maxr) maxr = m; }
+      if (maxr > P->batches - sumreps) maxr = P->batches - sumreps;
+      if (maxr > 0xffff) maxr = 0xffff;
+      maxr = maxr / ep * ep;
+      if (maxr < ep) break;
+      uint32_t rr = ep * (uint32_t)uni(&r, 1, maxr / ep);
+      for (uint32_t k = 0; k < P->K; ++k) left[k] -= rr * cnt[k] * tp;
+      reps[c] = rr; tv[c] = t; sumreps += rr; G = c + 1;
+    }
+    if (G == 0 && attempt == 15) {      /* give up: emit a plan that fails the capacity check */
+      G = 1; reps[0] = ep; tv[0] = 0; sumreps = ep;
+      if (sumreps > P->batches) sumreps = P->batches;
+    }
+  }
+  /* non-uniform layer split: pp-1 distinct cut points in [1, L-1], sorted */
+  uint8_t pts[256];
+  for (uint32_t l = 1; l < P->L; ++l) pts[l - 1] = (uint8_t)l;
+  r.d = 16 * 256;
+  for (uint32_t j = 0; j + 1 < pp; ++j) {
+    uint32_t pick = j + (uint32_t)uni(&r, 0, P->L - 2 - j);
+    uint8_t tmp = pts[j]; pts[j] = pts[pick]; pts[pick] = tmp;
+  }
+  for (uint32_t j = 1; j + 1 < pp; ++j) {         /* insertion sort of the chosen points */
+    uint8_t v = pts[j]; int q = (int)j - 1;
+    while (q >= 0 && pts[q] > v) { pts[q + 1] = pts[q]; --q; }
+    pts[q + 1] = v;
+  }
+  for (uint32_t s = 0; s < 16; ++s) cut[s * stride + slot] = 0;
+  for (uint32_t s = 0; s + 1 < pp; ++s) cut[s * stride + slot] = pts[s];
+  cut[(pp - 1) * stride + slot] = (uint8_t)P->L;
+  /* non-uniform batch split: every replica gets one micro-batch, the rest by random weights */
+  uint32_t extra = P->batches > sumreps ? P->batches - sumreps : 0;
+  uint64_t w[4], W = 0;
+  for (uint32_t c = 0; c < G; ++c) { w[c] = uni(&r, 1, 1000); W += w[c]; }
+  uint32_t given = 0;
+  for (uint32_t c = 1; c < G; ++c) { uint32_t x = (uint32_t)((uint64_t)extra * w[c] / W); nmb[c] = reps[c] + x; given += x; }
+  nmb[0] = reps[0] + (extra - given);
+  for (uint32_t c = 0; c < 4; ++c) {
+    cls[c * stride + slot] = c < G ? (reps[c] & 0xffff) | ((nmb[c] & 0xffff) << 16) : 0;
+    types[c * stride + slot] = c < G ? tv[c] : 0;
+  }
+  hdr[slot] = tpl | (epl << 2) | ((pp - 1) << 4) | ((G - 1) << 8) | (zero << 10);
+}
+
+typedef struct {
+  const pg_params* P; uint64_t first; int64_t lo, hi, stride;
+  uint32_t* hdr; uint8_t* cut; uint32_t* cls; uint64_t* types;
+} pg_job;
+
+static void* run(void* a) {
+  pg_job* j = (pg_job*)a;
+  for (int64_t s = j->lo; s < j->hi; ++s) gen_one(j->P, j->first + (uint64_t)s, j->hdr, j->cut, j->cls, j->types, j->stride, s);
+  return 0;
+}
+
+/* Plans first .. first+n-1 into slots 0 .. n-1 of the given planes. */
+void plangen_random(const pg_params* P, uint64_t first, int64_t n, uint32_t* hdr, uint8_t* cut, uint32_t* cls,
+                    uint64_t* types, int64_t stride, int nthreads) {
+  if (nthreads < 1) nthreads = 1;
+  if (nthreads > 64) nthreads = 64;
+  pthread_t th[64];
+  pg_job jobs[64];
+  for (int t = 0; t < nthreads; ++t) {
+    pg_job j = {P, first, n * t / nthreads, n * (t + 1) / nthreads, stride, hdr, cut, cls, types};
+    jobs[t] = j;
+  }
+  for (int t = 1; t < nthreads; ++t) pthread_create(&th[t], 0, run, &jobs[t]);
+  run(&jobs[0]);
+  for (int t = 1; t < nthreads; ++t) pthread_join(th[t], 0);
+}
