@@ -1,0 +1,153 @@
+"""Throughput of batched plan evaluation on one MI355X.
+
+One step = the whole hot path over every plan of the workload: decode and
+validate, place, stage costs, bottleneck links, collectives, the 1F1B pipeline
+of every replica class, the DP sync, and the argmin over all plans.  Plans are
+resident in HBM before timing starts.
+
+Prints one JSON line.  Roofline: the pipeline kernel is bound by VALU issue;
+its algorithmic work is 3 VALU ops (add, max, add) per dependent schedule node
+and 1 per node without a cross-stage input, i.e. sum over classes of
+M * (6 (S - 1) + 2) per plan; the peak is 256 CUs x 64 lanes x 2.4 GHz.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_VALU = 256 * 64 * 2.4e9          # lane-ops per second (fp64 add/max issue at full rate)
+METRIC = "candidate plans evaluated/sec on 1 MI355X; % of binding roofline"
+MAXU = np.uint64(2**64 - 1)
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def pipeline_ops(p, valid):
+    """Algorithmic VALU ops of the pipeline recurrence, per plan."""
+    hdr = p["hdr"]
+    S = (((hdr >> 4) & 15) + 1).astype(np.int64)
+    G = ((hdr >> 8) & 3) + 1
+    ops = np.zeros(hdr.shape[0], dtype=np.int64)
+    for c in range(4):
+        reps = (p["cls"][c] & 0xFFFF).astype(np.int64)
+        nmb = (p["cls"][c] >> 16).astype(np.int64)
+        has = (G > c) & valid & (reps > 0)
+        M = np.where(has, -(-nmb // np.maximum(reps, 1)), 0)
+        ops += M * (6 * (S - 1) + 2)
+    return ops
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=3, help="1..5 (3 = Llama-70B-shaped, 16M plans)")
+    ap.add_argument("--plans", type=int, default=0, help="evaluate only the first N plans (0 = all)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle time budget for the CPU baseline")
+    ap.add_argument("--no-timing", action="store_true", help="no HIP events inside the library")
+    a = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if a.gpus != 1 or world != 1:
+        print("bench.py evaluates on exactly one GPU: plans shard by index across GPUs with one 16-byte "
+              "argmin exchange, which this build does not run; use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2508_05370_amd import binding as B
+    from paper_2508_05370_amd import workloads as W
+
+    assert torch.cuda.is_available(), "no GPU"
+    w = W.workload(a.workload)
+    n = a.plans or w["n_plans"]
+    t0 = time.time()
+    p = W.plans(w, 0, n)
+    log("generated %d plans in %.1f s" % (n, time.time() - t0))
+    sim = B.Sim(w["model"], w["cluster"])
+    dp = B.device_plans(p)
+    out = torch.empty(n, dtype=torch.int64, device="cuda")
+    best = torch.empty(2, dtype=torch.int64, device="cuda")
+
+    def step():
+        sim.eval_plans(dp, out=out)
+        sim.argmin(out, out=best)
+
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+    got = B.times_u64(out)
+    valid = got != MAXU
+    ops = pipeline_ops(p, valid)
+    chunk = 1 << 21
+    launches_per_step = -(-n // chunk)
+
+    sim.set_timing(not a.no_timing)
+    sim.get_timing(0), sim.get_timing(1), sim.get_timing(2)          # clear
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(a.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    sim.set_timing(False)
+    elapsed = t1 - t0
+    value = n * a.steps / elapsed
+    best_t, best_i = B.best_tuple(best)
+
+    roof = None
+    extra = {}
+    if not a.no_timing:
+        pipe_ms, pipe_n = sim.get_timing(0)
+        setup_ms, setup_n = sim.get_timing(1)
+        call_ms, call_n = sim.get_timing(2)
+        avg_ms = pipe_ms / max(pipe_n, 1)
+        ops_per_launch = float(ops.sum()) / launches_per_step
+        achieved = ops_per_launch / (avg_ms * 1e-3) / 1e12
+        roof = {"bound": "alu", "achieved": round(achieved, 3), "peak": round(PEAK_VALU / 1e12, 3),
+                "unit": "TOP/s", "frac": round(achieved * 1e12 / PEAK_VALU, 4), "traffic": None,
+                "kernel": "k_pipe", "avg_launch_ms": round(avg_ms, 4), "launches": pipe_n,
+                "ops_per_launch": ops_per_launch}
+        extra = {"setup_kernel_ms_per_step": round(setup_ms / a.steps, 4),
+                 "pipe_kernel_ms_per_step": round(pipe_ms / a.steps, 4),
+                 "eval_call_ms_per_step": round(call_ms / a.steps, 4)}
+
+    # CPU baseline: the oracle as it stands, on a bounded prefix of the same plans
+    cpu = None
+    if a.cpu_seconds > 0:
+        from oracle import oracle as O
+        o = O.Oracle(w["model"], w["cluster"])
+        threads = min(16, os.cpu_count() or 1)
+        done, spent, mism, blk = 0, 0.0, 0, 100_000
+        while spent < a.cpu_seconds and done < n:
+            m = min(blk, n - done)
+            sub = {k: (v[done:done + m] if k == "hdr" else np.ascontiguousarray(v[:, done:done + m]))
+                   for k, v in p.items()}
+            c0 = time.perf_counter()
+            ref = o.eval(sub, nthreads=threads)
+            spent += time.perf_counter() - c0
+            mism += int(np.count_nonzero(ref != got[done:done + m]))
+            done += m
+        cpu = {"value": round(done / spent, 1), "unit": "plans/s", "cores": threads, "kind": "oracle",
+               "sample": "first %d plans of the workload (%.1f s)" % (done, spent),
+               "parity_mismatches_vs_gpu": mism}
+
+    rec = {"metric": METRIC, "value": round(value, 1), "unit": "plans/s", "n_gpus": 1, "steps": a.steps,
+           "warmup": a.warmup, "ms_per_step": round(elapsed / a.steps * 1e3, 4), "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "u64", "data": "synthetic",
+           "config": {"workload": w["name"], "plans": n, "valid_plans": int(valid.sum()),
+                      "argmin": [best_i, best_t], "mean_pipeline_ops_per_plan": round(float(ops.mean()), 1)},
+           "roofline": roof, "cpu_baseline": cpu}
+    rec.update(extra)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

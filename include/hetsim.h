@@ -1,0 +1,197 @@
+/*
+ * hetsim.h -- C ABI of the MI355X evaluator of heterogeneous LLM-training
+ * deployment plans (arXiv 2508.05370, "Simulating LLM training workloads for
+ * heterogeneous compute and network infrastructure").
+ *
+ * The library estimates the iteration time of many candidate plans at once.
+ * A plan maps one model onto a heterogeneous cluster: TP/PP/DP/EP degrees,
+ * a non-uniform split of the layers into pipeline stages, and up to four
+ * replica classes (a device group composition, Sec. 3 "Device grouping", and
+ * how many replicas of it run), each with its own share of the global batch
+ * (Sec. 3 "Non-uniform workload partitioning").  The inputs follow the
+ * paper's input description: model parameters, framework parameters and a
+ * heterogeneous topology with per-tier bandwidth and latency (Sec. 4.2
+ * "Input Description", Tables 5 and 6).
+ *
+ * All times are unsigned 64-bit picoseconds and every division rounds up,
+ * so results are exact integers, reproducible bit for bit.
+ *
+ * Threading: a context is immutable after sim_create and may be used from
+ * several host threads and HIP streams at once.  Calls that take a stream
+ * are asynchronous: they enqueue work and return; results are valid once
+ * the stream has been synchronised.
+ */
+#ifndef HETSIM_H
+#define HETSIM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* return codes */
+#define SIM_OK 0
+#define SIM_EINVAL (-1)   /* malformed descriptor or argument */
+#define SIM_ERANGE (-2)   /* descriptor could overflow the 64-bit time arithmetic */
+#define SIM_ENOMEM (-3)   /* host or device allocation failed */
+#define SIM_EHIP (-4)     /* a HIP runtime call or kernel launch failed */
+
+/* per-plan result of an invalid or infeasible plan */
+#define SIM_TIME_INVALID UINT64_MAX
+
+typedef struct sim_ctx sim_ctx;
+
+/*
+ * Model (Sec. 4.2 "Model parameters"; Table 6).  Host memory, owned by the
+ * caller, deep-copied by sim_create.  Per-op costs follow a roofline of the
+ * device type: each op takes max(FLOPs / TFLOPS, bytes / HBM bandwidth).
+ */
+typedef struct {
+  uint32_t n_layers;      /* L, 1..255 transformer layers */
+  uint32_t hidden;        /* h */
+  uint32_t heads;         /* query heads; divides hidden */
+  uint32_t kv_heads;      /* key/value heads (grouped-query attention); divides heads */
+  uint32_t ffn;           /* dense MLP width; ignored when experts > 0 */
+  uint32_t gated;         /* 1: gated MLP with three matrices (SwiGLU); 0: two matrices (GELU) */
+  uint32_t vocab;         /* vocabulary; padded up to a multiple of 128 */
+  uint32_t learned_pos;   /* rows of a learned position table; 0 = none (rotary) */
+  uint32_t seq;           /* sequence length, tokens */
+  uint32_t dtype_bytes;   /* bytes per activation/weight element (2 = bf16/fp16) */
+  uint32_t global_batch;  /* sequences per iteration */
+  uint32_t n_mbs;         /* 1..4 micro-batch sizes a plan may pick from */
+  uint32_t mbs[4];        /* micro-batch sizes in sequences, 1..1024 */
+  uint32_t grad_bytes;    /* bytes per gradient element in the DP sync (4 = fp32) */
+  uint32_t param_bytes;   /* bytes per parameter in the ZeRO all-gather (2 = bf16) */
+  uint32_t experts;       /* E: 0 = dense model; else experts per MoE layer (every layer) */
+  uint32_t topk;          /* experts per token, 1..E */
+  uint32_t expert_ffn;    /* width of one (gated) expert MLP */
+  const uint32_t* load_q16; /* [n_layers][experts] token share of each expert in units of
+                               2^-16, rows summing to 65536; NULL iff experts == 0 */
+} sim_model_desc;
+
+/*
+ * Cluster (Sec. 4.2 "Heterogeneous host and cluster topology"; Table 5).
+ * K device types; type k is a pool of n_nodes[k] homogeneous nodes of
+ * dev_per_node[k] devices.  Devices are numbered pool by pool (type-major),
+ * node-major inside a pool.  Links: an intra-node fabric per node, a PCIe
+ * path from device to NIC, one NIC per device.  Bandwidths are MB/s per
+ * direction (0 = tier absent, else >= 16); latencies are ps per message.
+ * All arrays are host memory owned by the caller and deep-copied.
+ */
+typedef struct {
+  uint32_t n_types;                 /* K, 1..16 */
+  const uint32_t* n_nodes;          /* [K] >= 1 */
+  const uint32_t* dev_per_node;     /* [K] power of two, 1..64 */
+  const uint32_t* tflops;           /* [K] dense TFLOP/s, >= 1 */
+  const uint32_t* hbm_GBps;         /* [K] memory bandwidth GB/s, >= 1 */
+  const uint32_t* intra_MBps;       /* [K] intra-node fabric; required when dev_per_node > 1 */
+  const uint32_t* pcie_MBps;        /* [K] device-to-NIC PCIe; 0 = not on the inter-node path */
+  const uint32_t* nic_MBps;         /* [K] per-device NIC, required */
+  const uint64_t* intra_alpha_ps;   /* [K] latency of one intra-node message */
+  const uint64_t* pcie_alpha_ps;    /* [K] latency of one PCIe trip (an inter-node path makes two per side) */
+  const uint64_t* nic_alpha_ps;     /* [K] NIC processing latency per side */
+  const uint32_t* nic_MBps_dev;     /* optional [total devices] per-device NIC rate (overrides nic_MBps) */
+  const uint32_t* intra_MBps_node;  /* optional [total nodes] per-node fabric rate (overrides intra_MBps) */
+} sim_cluster_desc;
+
+/*
+ * Candidate plans, structure of arrays in DEVICE memory (caller-owned),
+ * plane stride `stride` elements (>= n).  Plan i:
+ *   hdr[i]              bits 0-1 log2 TP, 2-3 log2 EP, 4-7 PP-1, 8-9 classes-1,
+ *                       10 ZeRO (reduce-scatter + all-gather instead of
+ *                       all-reduce), 11-12 micro-batch size index, 13-31 zero
+ *   cut[s*stride+i]     u8, last layer (exclusive) of stage s: 1 <= cut[0] <
+ *                       ... < cut[PP-1] = L (the non-uniform layer split)
+ *   cls[c*stride+i]     u32, class c: replicas in bits 0-15, micro-batches in
+ *                       bits 16-31 (the class's share of the global batch)
+ *   types[c*stride+i]   u64, device type of stage s of class c in bits [4s, 4s+4)
+ * Entries past PP stages or past the class count are ignored.
+ * A plan that breaks any rule (ranges, divisibility of heads/widths by TP,
+ * TP within a node, EP dividing every class's replicas, capacity of every
+ * device pool, micro-batches summing to the global batch, at least one
+ * micro-batch per replica) evaluates to SIM_TIME_INVALID; that is not an
+ * error.
+ */
+typedef struct {
+  const uint32_t* hdr;
+  const uint8_t* cut;
+  const uint32_t* cls;
+  const uint64_t* types;
+  int64_t stride;
+} sim_plans;
+
+/* argmin result: lowest time, ties to the lowest plan index */
+typedef struct {
+  uint64_t time_ps;
+  int64_t index;
+} sim_best;
+
+/*
+ * Create a context on the current HIP device: validates the descriptors,
+ * builds the per-device-type roofline cost tables (per layer, forward and
+ * backward, for every TP degree, micro-batch size and EP degree, with layer
+ * prefix sums), the link tables and range-maximum structures, and uploads
+ * them.  Returns SIM_EINVAL for malformed descriptors, SIM_ERANGE when some
+ * plan's time could exceed 2^62 ps or a per-stage quantity 2^52 ps,
+ * SIM_ENOMEM or SIM_EHIP on allocation/copy failure.  *out is NULL on error.
+ */
+int sim_create(const sim_model_desc* model, const sim_cluster_desc* cluster, sim_ctx** out);
+
+/*
+ * Iteration time of plans 0..n-1 into out_time_ps[0..n-1] (device memory,
+ * caller-owned): per-stage compute from the cost tables, alpha-beta times of
+ * the TP all-reduce (exposed in forward), the MoE all-to-all, the pipeline
+ * point-to-point hops (Table 1 exposure) on each group's slowest link (Sec.
+ * 4.1 [C4]), a 1F1B pipeline per class, then the DP gradient sync per stage
+ * across all replicas.  n = 0 is a no-op.  Temporary device memory is taken
+ * from a stream-ordered pool on `stream` (a hipStream_t; NULL = null
+ * stream).  Returns SIM_EINVAL for a NULL pointer, n < 0 or stride < n,
+ * SIM_ENOMEM if the temporary memory cannot be allocated, SIM_EHIP if a
+ * launch fails.
+ */
+int sim_eval_plans(sim_ctx* ctx, const sim_plans* plans, int64_t n, uint64_t* out_time_ps, void* stream);
+
+/*
+ * Per-stage quantities of plans 0..n-1 (device memory, caller-owned):
+ *   out_stage[((i*4 + c)*16 + s)*4 + q], q = 0 forward time of one
+ *   micro-batch on stage s of class c, 1 backward time, 2 pipeline hop
+ *   s -> s+1, 3 DP sync of stage s;
+ *   out_class[i*4 + c] = PP | M << 8 where M is the micro-batches per replica
+ *   of class c (0 for an absent class or an invalid plan).
+ * Entries of absent stages are left untouched.  Same errors as
+ * sim_eval_plans.
+ */
+int sim_eval_stages(sim_ctx* ctx, const sim_plans* plans, int64_t n, uint64_t* out_stage, uint32_t* out_class,
+                    void* stream);
+
+/*
+ * Lexicographic minimum of (time_ps[i], index_base + i) over i < n, written
+ * to *out_best (device memory).  Invalid plans are skipped; if all are
+ * invalid (or n = 0) the result is {SIM_TIME_INVALID, -1}.  Chunks of a
+ * larger sweep may be reduced on different streams into separate slots and
+ * combined with sim_best_reduce; the result does not depend on the order.
+ */
+int sim_argmin(sim_ctx* ctx, const uint64_t* time_ps, int64_t n, int64_t index_base, sim_best* out_best,
+               void* stream);
+
+/* Lexicographic minimum of n argmin slots (device memory) into *out_best. */
+int sim_best_reduce(sim_ctx* ctx, const sim_best* bests, int64_t n, sim_best* out_best, void* stream);
+
+/*
+ * Kernel timing for measurement.  When enabled, sim_eval_plans records a
+ * HIP event pair on its stream around every launch of its pipeline kernel
+ * and of the whole call; sim_get_timing synchronises those events and
+ * returns the accumulated milliseconds and launch counts, then clears them.
+ * kind 0 = pipeline kernel, 1 = setup kernel, 2 = whole sim_eval_plans call.
+ */
+int sim_set_timing(sim_ctx* ctx, int enable);
+int sim_get_timing(sim_ctx* ctx, int kind, double* total_ms, int64_t* launches);
+
+void sim_destroy(sim_ctx* ctx);
+const char* sim_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,237 @@
+// api.cpp -- the C ABI (include/hetsim.h): context lifetime, workspace, launches.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <mutex>
+#include <new>
+#include <vector>
+
+#include "hetsim.h"
+#include "internal.h"
+
+namespace hetsim {
+hipError_t launch_fill32(uint32_t* p, uint32_t n, uint32_t v, hipStream_t s);
+hipError_t launch_setup(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, uint64_t* rec, uint32_t* meta,
+                        uint32_t* hist, hipStream_t s);
+hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* total, hipStream_t s);
+hipError_t launch_scatter(const uint32_t* meta, uint32_t nslots, uint32_t* cursor, uint32_t* ids, hipStream_t s);
+hipError_t launch_pipe(const uint64_t* rec, const uint32_t* meta, const uint32_t* ids, const uint32_t* total,
+                       uint32_t max_tasks, uint64_t* out, hipStream_t s);
+hipError_t launch_argmin(const uint64_t* t, int64_t n, int64_t base, sim_best* b, hipStream_t s);
+hipError_t launch_best_reduce(const sim_best* in, int64_t n, sim_best* out, hipStream_t s);
+}  // namespace hetsim
+
+using namespace hetsim;
+
+namespace {
+// plans per internal chunk: bounds the temporary memory of one call
+constexpr int64_t kChunk = 1 << 21;
+
+struct EventPair {
+  hipEvent_t a, b;
+};
+}  // namespace
+
+struct sim_ctx {
+  Tab tab;
+  int device;
+  void* tables;        // one device allocation holding every table
+  hipMemPool_t pool;   // stream-ordered pool for per-call workspace
+  std::mutex mu;
+  bool timing;
+  std::vector<EventPair> ev[3];
+};
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+extern "C" const char* sim_strerror(int code) {
+  switch (code) {
+    case SIM_OK: return "ok";
+    case SIM_EINVAL: return "invalid argument or descriptor";
+    case SIM_ERANGE: return "descriptor could overflow 64-bit picosecond arithmetic";
+    case SIM_ENOMEM: return "out of memory";
+    case SIM_EHIP: return "HIP runtime error";
+    default: return "unknown error";
+  }
+}
+
+extern "C" int sim_create(const sim_model_desc* model, const sim_cluster_desc* cluster, sim_ctx** out) {
+  if (!out) return SIM_EINVAL;
+  *out = nullptr;
+  HostTables* ht = new (std::nothrow) HostTables();
+  if (!ht) return SIM_ENOMEM;
+  int rc = build_tables(model, cluster, ht);
+  if (rc != SIM_OK) { delete ht; return rc; }
+  sim_ctx* c = new (std::nothrow) sim_ctx();
+  if (!c) { delete ht; return SIM_ENOMEM; }
+  c->tab = ht->tab;
+  c->timing = false;
+  c->tables = nullptr;
+  c->pool = nullptr;
+  if (hipGetDevice(&c->device) != hipSuccess) { delete ht; delete c; return SIM_EHIP; }
+  struct Part {
+    const void* src;
+    size_t bytes;
+    size_t off;
+  };
+  Part parts[7] = {{ht->pf.data(), ht->pf.size() * 8, 0},         {ht->pb.data(), ht->pb.size() * 8, 0},
+                   {ht->emb.data(), ht->emb.size() * 8, 0},       {ht->head.data(), ht->head.size() * 8, 0},
+                   {ht->pa.data(), ht->pa.size() * 8, 0},         {ht->rm_nic.data(), ht->rm_nic.size() * 4, 0},
+                   {ht->rm_intra.data(), ht->rm_intra.size() * 4, 0}};
+  size_t total = 0;
+  for (auto& p : parts) { p.off = total; total += align256(p.bytes); }
+  if (hipMalloc(&c->tables, total) != hipSuccess) { delete ht; delete c; return SIM_ENOMEM; }
+  for (auto& p : parts)
+    if (p.bytes && hipMemcpy((char*)c->tables + p.off, p.src, p.bytes, hipMemcpyHostToDevice) != hipSuccess) {
+      (void)hipFree(c->tables); delete ht; delete c; return SIM_EHIP;
+    }
+  char* b = (char*)c->tables;
+  c->tab.pf = (const uint64_t*)(b + parts[0].off);
+  c->tab.pb = (const uint64_t*)(b + parts[1].off);
+  c->tab.emb = (const uint64_t*)(b + parts[2].off);
+  c->tab.head = (const uint64_t*)(b + parts[3].off);
+  c->tab.pa = (const uint64_t*)(b + parts[4].off);
+  c->tab.rm_nic = (const uint32_t*)(b + parts[5].off);
+  c->tab.rm_intra = (const uint32_t*)(b + parts[6].off);
+  delete ht;
+  hipMemPoolProps props;
+  memset(&props, 0, sizeof(props));
+  props.allocType = hipMemAllocationTypePinned;
+  props.location.type = hipMemLocationTypeDevice;
+  props.location.id = c->device;
+  if (hipMemPoolCreate(&c->pool, &props) != hipSuccess) { (void)hipFree(c->tables); delete c; return SIM_EHIP; }
+  uint64_t keep = UINT64_MAX;   // keep workspace memory cached between calls
+  (void)hipMemPoolSetAttribute(c->pool, hipMemPoolAttrReleaseThreshold, &keep);
+  *out = c;
+  return SIM_OK;
+}
+
+extern "C" void sim_destroy(sim_ctx* c) {
+  if (!c) return;
+  for (auto& v : c->ev)
+    for (auto& e : v) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }
+  (void)hipDeviceSynchronize();
+  if (c->pool) (void)hipMemPoolDestroy(c->pool);
+  if (c->tables) (void)hipFree(c->tables);
+  delete c;
+}
+
+static bool plans_ok(const sim_plans* p, int64_t n) {
+  return p && p->hdr && p->cut && p->cls && p->types && p->stride >= n && n >= 0;
+}
+
+static bool begin_event(sim_ctx* c, int kind, hipStream_t s, EventPair* e) {
+  if (!c->timing) return false;
+  if (hipEventCreate(&e->a) != hipSuccess) return false;
+  if (hipEventCreate(&e->b) != hipSuccess) { (void)hipEventDestroy(e->a); return false; }
+  (void)hipEventRecord(e->a, s);
+  (void)kind;
+  return true;
+}
+static void end_event(sim_ctx* c, int kind, hipStream_t s, EventPair* e) {
+  (void)hipEventRecord(e->b, s);
+  std::lock_guard<std::mutex> g(c->mu);
+  c->ev[kind].push_back(*e);
+}
+
+// Workspace of one chunk: per-plan records, pipeline metadata and ids, bucket
+// counts, cursors and the pipeline count.
+struct Work {
+  uint64_t* rec;
+  uint32_t *meta, *ids, *hist, *cursor, *total;
+};
+static size_t work_bytes(int64_t ch) {
+  return align256((size_t)ch * kPlanWords * 8) + 2 * align256((size_t)ch * 4 * 4) + 2 * align256(kBuckets * 4) +
+         align256(4);
+}
+static Work carve(void* base, int64_t ch) {
+  Work w;
+  char* p = (char*)base;
+  w.rec = (uint64_t*)p; p += align256((size_t)ch * kPlanWords * 8);
+  w.meta = (uint32_t*)p; p += align256((size_t)ch * 16);
+  w.ids = (uint32_t*)p; p += align256((size_t)ch * 16);
+  w.hist = (uint32_t*)p; p += align256(kBuckets * 4);
+  w.cursor = (uint32_t*)p; p += align256(kBuckets * 4);
+  w.total = (uint32_t*)p;
+  return w;
+}
+
+extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uint64_t* out, void* stream) {
+  if (!c || !plans_ok(plans, n) || (n > 0 && !out)) return SIM_EINVAL;
+  if (n == 0) return SIM_OK;
+  hipStream_t s = (hipStream_t)stream;
+  if (hipSetDevice(c->device) != hipSuccess) return SIM_EHIP;
+  const int64_t ch = n < kChunk ? n : kChunk;
+  void* ws = nullptr;
+  if (hipMallocFromPoolAsync(&ws, work_bytes(ch), c->pool, s) != hipSuccess) return SIM_ENOMEM;
+  Work w = carve(ws, ch);
+  EventPair call, ev;
+  bool tcall = begin_event(c, 2, s, &call);
+  hipError_t e = hipSuccess;
+  for (int64_t off = 0; off < n && e == hipSuccess; off += ch) {
+    const int64_t cn = n - off < ch ? n - off : ch;
+    sim_plans p = *plans;
+    p.hdr += off; p.cut += off; p.cls += off; p.types += off;
+    e = launch_fill32(w.hist, kBuckets, 0, s);
+    bool t1 = e == hipSuccess && begin_event(c, 1, s, &ev);
+    if (e == hipSuccess) e = launch_setup(c->tab, p, cn, out + off, w.rec, w.meta, w.hist, s);
+    if (t1) end_event(c, 1, s, &ev);
+    if (e == hipSuccess) e = launch_scan(w.hist, w.cursor, w.total, s);
+    if (e == hipSuccess) e = launch_scatter(w.meta, (uint32_t)(cn * 4), w.cursor, w.ids, s);
+    bool t0 = e == hipSuccess && begin_event(c, 0, s, &ev);
+    if (e == hipSuccess) e = launch_pipe(w.rec, w.meta, w.ids, w.total, (uint32_t)(cn * 4), out + off, s);
+    if (t0) end_event(c, 0, s, &ev);
+  }
+  if (tcall) end_event(c, 2, s, &call);
+  (void)hipFreeAsync(ws, s);
+  return e == hipSuccess ? SIM_OK : SIM_EHIP;
+}
+
+extern "C" int sim_eval_stages(sim_ctx* c, const sim_plans* plans, int64_t n, uint64_t* out_stage,
+                               uint32_t* out_class, void* stream) {
+  if (!c || !plans_ok(plans, n) || (n > 0 && (!out_stage || !out_class))) return SIM_EINVAL;
+  if (n == 0) return SIM_OK;
+  if (hipSetDevice(c->device) != hipSuccess) return SIM_EHIP;
+  hipError_t e = launch_setup(c->tab, *plans, n, nullptr, out_stage, out_class, nullptr, (hipStream_t)stream);
+  return e == hipSuccess ? SIM_OK : SIM_EHIP;
+}
+
+extern "C" int sim_argmin(sim_ctx* c, const uint64_t* t, int64_t n, int64_t base, sim_best* out, void* stream) {
+  if (!c || !out || n < 0 || (n > 0 && !t)) return SIM_EINVAL;
+  if (hipSetDevice(c->device) != hipSuccess) return SIM_EHIP;
+  return launch_argmin(t, n, base, out, (hipStream_t)stream) == hipSuccess ? SIM_OK : SIM_EHIP;
+}
+
+extern "C" int sim_best_reduce(sim_ctx* c, const sim_best* in, int64_t n, sim_best* out, void* stream) {
+  if (!c || !out || n < 0 || (n > 0 && !in)) return SIM_EINVAL;
+  if (hipSetDevice(c->device) != hipSuccess) return SIM_EHIP;
+  return launch_best_reduce(in, n, out, (hipStream_t)stream) == hipSuccess ? SIM_OK : SIM_EHIP;
+}
+
+extern "C" int sim_set_timing(sim_ctx* c, int enable) {
+  if (!c) return SIM_EINVAL;
+  c->timing = enable != 0;
+  return SIM_OK;
+}
+
+extern "C" int sim_get_timing(sim_ctx* c, int kind, double* total_ms, int64_t* launches) {
+  if (!c || kind < 0 || kind > 2 || !total_ms || !launches) return SIM_EINVAL;
+  std::vector<EventPair> v;
+  {
+    std::lock_guard<std::mutex> g(c->mu);
+    v.swap(c->ev[kind]);
+  }
+  double sum = 0;
+  int rc = SIM_OK;
+  for (auto& e : v) {
+    float ms = 0;
+    if (hipEventSynchronize(e.b) != hipSuccess || hipEventElapsedTime(&ms, e.a, e.b) != hipSuccess) rc = SIM_EHIP;
+    sum += ms;
+    (void)hipEventDestroy(e.a);
+    (void)hipEventDestroy(e.b);
+  }
+  *total_ms = sum;
+  *launches = (int64_t)v.size();
+  return rc;
+}

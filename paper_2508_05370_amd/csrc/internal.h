@@ -1,0 +1,58 @@
+// internal.h -- context tables shared by the host builder and the gfx950 kernels.
+#pragma once
+#include <stdint.h>
+#include <vector>
+
+#include "hetsim.h"
+
+namespace hetsim {
+
+constexpr int kMaxTypes = 16;
+constexpr int kMaxStages = 16;
+constexpr int kMaxClasses = 4;
+constexpr int kRecWords = 4;                    // per (plan, class, stage): fwd, bwd, hop, dp
+constexpr int kPlanWords = kMaxClasses * kMaxStages * kRecWords;
+constexpr int kBucketsM = 256;                  // micro-batch-count buckets per stage count
+constexpr int kBuckets = kMaxStages * kBucketsM;
+
+// Everything a kernel needs about one (model, cluster) pair.  Scalars travel
+// by value in the kernel argument block; tables live in device memory.
+struct Tab {
+  uint32_t L, K, E, n_mbs, gbs;
+  uint32_t mbs[4];
+  uint32_t tp_ok;                 // bit j: TP 2^j divides heads, kv heads and MLP widths
+  uint32_t ep_ok;                 // bit j: EP 2^j allowed (dense models: EP 1 only)
+  uint32_t D, N;                  // total devices, total nodes
+  uint32_t lvl_dev, lvl_node;     // levels of the range-max tables
+  uint32_t dpn_log2[kMaxTypes];
+  uint32_t cap[kMaxTypes];        // devices per pool
+  uint32_t dev_off[kMaxTypes];    // first global device of pool k
+  uint32_t node_off[kMaxTypes];   // first global node of pool k
+  uint32_t bq_pcie[kMaxTypes];    // PCIe ps/byte in 2^-16 units, 0 = absent
+  uint64_t a_intra[kMaxTypes];    // intra-node message latency
+  uint64_t a_side[kMaxTypes];     // one end of an inter-node path: two PCIe trips + NIC
+  uint64_t act[4];                // bytes of one micro-batch activation per mbs index
+  uint64_t grad_bytes, param_bytes;
+  uint64_t par_layer[4];          // non-expert parameters of one layer on one TP rank, by log2 TP
+  uint64_t par_expert[4][4];      // expert parameters of one layer per rank [log2 TP][log2 EP]
+  uint64_t par_embed[4], par_head[4];
+  const uint64_t* pf;             // forward layer prefix sums [K][4][n_mbs][4][L+1]
+  const uint64_t* pb;             // backward prefix sums, same shape
+  const uint64_t* emb;            // [K][n_mbs][2] embedding fwd, bwd
+  const uint64_t* head;           // [K][4][n_mbs][2] head fwd, bwd
+  const uint64_t* pa;             // all-to-all bytes prefix [4][n_mbs][L+1]
+  const uint32_t* rm_nic;         // range-max table of NIC rates per device [lvl_dev][D]
+  const uint32_t* rm_intra;       // range-max table of fabric rates per node [lvl_node][N]
+};
+
+// Host side: validate descriptors and build the tables (host copies).
+struct HostTables {
+  Tab tab;
+  std::vector<uint64_t> pf, pb, emb, head, pa;
+  std::vector<uint32_t> rm_nic, rm_intra;
+};
+
+// Returns 0 (SIM_OK), SIM_EINVAL or SIM_ERANGE.
+int build_tables(const sim_model_desc* model, const sim_cluster_desc* cluster, HostTables* out);
+
+}  // namespace hetsim

@@ -1,0 +1,223 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Integer picoseconds: every comparison is bit-exact.  Small cases compare every
+plan; the full-size sweeps are launched exactly as the benchmark launches them
+and compared on a sample of plans (plus every plan whose time reaches 2^53 ps,
+which takes the u64 path) that the oracle evaluates one by one.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+MAXU = np.uint64(2**64 - 1)
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as T
+    if not T.cuda.is_available():
+        pytest.skip("no GPU")
+    return T
+
+
+@pytest.fixture(scope="module")
+def B():
+    from paper_2508_05370_amd import binding
+    return binding
+
+
+def _sub(p, idx):
+    return dict(hdr=np.ascontiguousarray(p["hdr"][idx]), cut=np.ascontiguousarray(p["cut"][:, idx]),
+                cls=np.ascontiguousarray(p["cls"][:, idx]), types=np.ascontiguousarray(p["types"][:, idx]))
+
+
+def _gpu_times(B, sim, p):
+    dp = B.device_plans(p)
+    return B.times_u64(sim.eval_plans(dp))
+
+
+def _assert_equal(got, want, what):
+    bad = np.nonzero(got != want)[0]
+    assert bad.size == 0, "%s: %d mismatches, first %s: gpu %d oracle %d" % (
+        what, bad.size, bad[:5], int(got[bad[0]]), int(want[bad[0]]))
+
+
+def test_exhaustive_two_type_cluster(torch, B, oracle_mod, workloads):
+    w = workloads.workload(1)
+    p = workloads.plans(w)
+    say("case: exhaustive 8-device, %d plans" % len(p["hdr"]))
+    sim = B.Sim(w["model"], w["cluster"])
+    got = _gpu_times(B, sim, p)
+    want = oracle_mod.Oracle(w["model"], w["cluster"]).eval(p)
+    _assert_equal(got, want, "exhaustive")
+    t = torch.from_numpy(got.view(np.int64)).cuda()
+    bt, bi = B.best_tuple(sim.argmin(t))
+    assert (bt, bi) == (int(want.min()), int(np.argmin(want)))
+
+
+@pytest.mark.parametrize("idx", [2, 3, 4, 5])
+def test_random_prefix(torch, B, oracle_mod, workloads, idx):
+    w = workloads.workload(idx)
+    n = 40_000 + 37                                   # several tiles and a ragged tail
+    p = workloads.plans(w, 0, n)
+    say("case: workload %d prefix %d" % (idx, n))
+    got = _gpu_times(B, B.Sim(w["model"], w["cluster"]), p)
+    want = oracle_mod.Oracle(w["model"], w["cluster"]).eval(p)
+    _assert_equal(got, want, "workload %d" % idx)
+    assert np.count_nonzero(want != MAXU) > n // 2
+
+
+@pytest.mark.parametrize("idx", [1, 2, 3, 4, 5])
+def test_stage_records(torch, B, oracle_mod, workloads, idx):
+    """Per (class, stage) forward/backward/hop/DP times and micro-batch counts."""
+    w = workloads.workload(idx)
+    p = workloads.plans(w, 0, 1500)
+    say("case: stage records workload %d" % idx)
+    sim = B.Sim(w["model"], w["cluster"])
+    st, cl = sim.eval_stages(B.device_plans(p))
+    st = st.cpu().numpy().view(np.uint64)
+    cl = cl.cpu().numpy().view(np.uint32)
+    o = oracle_mod.Oracle(w["model"], w["cluster"])
+    for i in range(0, 1500, 3):
+        d = o.detail(p, i)
+        if d is None:
+            assert np.all(cl[i] == 0)
+            continue
+        S, G = d["S"], d["G"]
+        for g in range(4):
+            if g >= G:
+                assert cl[i, g] == 0
+                continue
+            assert cl[i, g] == S | (d["M"][g] << 8), (i, g)
+            for s in range(S):
+                rec = [int(v) for v in st[i, g, s]]
+                want = [d["f"][g][s], d["b"][g][s], d["c"][g][s], d["tdp"][s]]
+                assert rec == want, (idx, i, g, s, rec, want)
+
+
+def _plan(n):
+    return dict(hdr=np.zeros(n, np.uint32), cut=np.zeros((16, n), np.uint8), cls=np.zeros((4, n), np.uint32),
+                types=np.zeros((4, n), np.uint64))
+
+
+def _set(p, i, tp=1, ep=1, cuts=(12,), classes=((1, 1, 0),), zero=0, mi=0):
+    pp, G = len(cuts), len(classes)
+    p["hdr"][i] = (tp.bit_length() - 1) | ((ep.bit_length() - 1) << 2) | ((pp - 1) << 4) | ((G - 1) << 8) | (
+        zero << 10) | (mi << 11)
+    for s, v in enumerate(cuts):
+        p["cut"][s, i] = v
+    for g, (reps, nmb, tv) in enumerate(classes):
+        p["cls"][g, i] = reps | (nmb << 16)
+        p["types"][g, i] = tv
+
+
+def test_invalid_plans(torch, B, oracle_mod, workloads):
+    w = workloads.workload(1)
+    p = _plan(13)
+    ok = dict(cuts=(6, 12), classes=((4, 8, 0x10),))
+    _set(p, 0, **ok)
+    _set(p, 1, tp=8, cuts=(6, 12), classes=((1, 8, 0x10),))
+    _set(p, 2, cuts=(6, 11), classes=((4, 8, 0x10),))
+    _set(p, 3, cuts=(6, 6), classes=((4, 8, 0x10),))
+    _set(p, 4, cuts=(6, 12), classes=((4, 7, 0x10),))
+    _set(p, 5, cuts=(6, 12), classes=((4, 3, 0x10),))
+    _set(p, 6, cuts=(6, 12), classes=((5, 8, 0x10),))
+    _set(p, 7, cuts=(6, 12), classes=((4, 8, 0x20),))
+    _set(p, 8, ep=2, cuts=(6, 12), classes=((4, 8, 0x10),))
+    _set(p, 9, cuts=(6, 12), classes=((4, 8, 0x10),), mi=1)
+    _set(p, 10, **ok)
+    p["hdr"][10] |= 1 << 20
+    _set(p, 11, cuts=(0, 12), classes=((4, 8, 0x10),))
+    _set(p, 12, tp=4, cuts=(12,), classes=((1, 4, 0x0), (1, 4, 0x1)))   # valid, TP 4 fills each node
+    say("case: invalid plans")
+    got = _gpu_times(B, B.Sim(w["model"], w["cluster"]), p)
+    want = oracle_mod.Oracle(w["model"], w["cluster"]).eval(p)
+    _assert_equal(got, want, "invalid")
+    assert got[0] != MAXU and got[12] != MAXU and np.all(got[1:12] == MAXU)
+
+
+def test_sizes_and_strides(torch, B, oracle_mod, workloads):
+    w = workloads.workload(2)
+    p = workloads.plans(w, 0, 3000)
+    want = oracle_mod.Oracle(w["model"], w["cluster"]).eval(p)
+    sim = B.Sim(w["model"], w["cluster"])
+    dp = B.device_plans(p)
+    say("case: sizes and strides")
+    for n in (1, 2, 63, 64, 65, 255, 257, 1000):
+        got = B.times_u64(sim.eval_plans(dp, n=n))
+        _assert_equal(got, want[:n], "n=%d" % n)
+    # a window in the middle of the arrays (plane stride 3000, offset 1234)
+    got = B.times_u64(sim.eval_plans(dp, n=777, offset=1234))
+    _assert_equal(got, want[1234:2011], "window")
+    empty = torch.zeros(0, dtype=torch.int64, device="cuda")
+    sim.eval_plans(dp, n=0, out=empty)
+
+
+def test_determinism(torch, B, workloads):
+    w = workloads.workload(3)
+    p = workloads.plans(w, 0, 300_000)
+    sim = B.Sim(w["model"], w["cluster"])
+    dp = B.device_plans(p)
+    say("case: determinism")
+    a = B.times_u64(sim.eval_plans(dp)).copy()
+    b = B.times_u64(sim.eval_plans(dp))
+    assert np.array_equal(a, b)
+
+
+def test_argmin_semantics(torch, B, workloads):
+    w = workloads.workload(1)
+    sim = B.Sim(w["model"], w["cluster"])
+    say("case: argmin")
+    inv = np.full(1000, MAXU, dtype=np.uint64)
+    t = torch.from_numpy(inv.view(np.int64)).cuda()
+    assert B.best_tuple(sim.argmin(t)) == (2**64 - 1, -1)
+    assert B.best_tuple(sim.argmin(t, n=0)) == (2**64 - 1, -1)
+    v = np.arange(5000, dtype=np.uint64)[::-1].copy() + np.uint64(7)
+    v[[100, 2000, 4000]] = 3                                     # ties: lowest index wins
+    v[50] = MAXU
+    t = torch.from_numpy(v.view(np.int64)).cuda()
+    assert B.best_tuple(sim.argmin(t, index_base=10**9)) == (3, 10**9 + 100)
+    # chunks on two streams, then one reduction
+    slots = torch.empty(8, dtype=torch.int64, device="cuda")
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    for j in range(4):
+        with torch.cuda.stream(streams[j % 2]):
+            sim.argmin(t[j * 1250:(j + 1) * 1250], index_base=j * 1250, out=slots[2 * j:2 * j + 2],
+                       stream=streams[j % 2])
+    torch.cuda.synchronize()
+    assert B.best_tuple(sim.best_reduce(slots)) == (3, 100)
+    allinv = torch.from_numpy(np.array([-1, -1] * 3, dtype=np.int64)).cuda()   # {MAX, -1} slots
+    assert B.best_tuple(sim.best_reduce(allinv)) == (2**64 - 1, -1)
+
+
+@pytest.mark.parametrize("idx", [2, 3, 4])
+def test_full_size_sampled(torch, B, oracle_mod, workloads, idx):
+    """Whole workload in one call (the benchmark's launch), checked on samples."""
+    w = workloads.workload(idx)
+    n = w["n_plans"]
+    say("case: full workload %d, %d plans: generating" % (idx, n))
+    p = workloads.plans(w)
+    sim = B.Sim(w["model"], w["cluster"])
+    dp = B.device_plans(p)
+    say("case: full workload %d: evaluating on GPU" % idx)
+    out = sim.eval_plans(dp)
+    best = B.best_tuple(sim.argmin(out))
+    got = B.times_u64(out)
+    rng = np.random.default_rng(idx)
+    sample = np.unique(np.concatenate([rng.integers(0, n, 20_000), np.nonzero((got >= 2**53) & (got != MAXU))[0],
+                                       [0, n - 1, best[1]]]))
+    say("case: full workload %d: oracle on %d sampled plans (%d at or above 2^53)" % (
+        idx, sample.size, int(np.count_nonzero((got >= 2**53) & (got != MAXU)))))
+    want = oracle_mod.Oracle(w["model"], w["cluster"]).eval(_sub(p, sample))
+    _assert_equal(got[sample], want, "full workload %d" % idx)
+    valid = got != MAXU
+    assert best[0] == int(got[valid].min()) and best[1] == int(np.argmax(got == got[valid].min()))
