@@ -54,6 +54,8 @@ def main():
     ap.add_argument("--plans", type=int, default=0, help="evaluate only the first N plans (0 = all)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle time budget for the CPU baseline")
     ap.add_argument("--no-timing", action="store_true", help="no HIP events inside the library")
+    ap.add_argument("--copy-calibrate", type=int, default=0, metavar="BYTES",
+                    help="only run a device-to-device copy of BYTES (reference for HBM byte counters)")
     a = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if a.gpus != 1 or world != 1:
@@ -66,6 +68,14 @@ def main():
     from paper_2508_05370_amd import workloads as W
 
     assert torch.cuda.is_available(), "no GPU"
+    if a.copy_calibrate:
+        src = torch.ones(a.copy_calibrate // 4, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": a.copy_calibrate, "launches": 3}), flush=True)
+        return
     w = W.workload(a.workload)
     n = a.plans or w["n_plans"]
     t0 = time.time()

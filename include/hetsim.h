@@ -157,10 +157,11 @@ int sim_eval_plans(sim_ctx* ctx, const sim_plans* plans, int64_t n, uint64_t* ou
  *   out_stage[((i*4 + c)*16 + s)*4 + q], q = 0 forward time of one
  *   micro-batch on stage s of class c, 1 backward time, 2 pipeline hop
  *   s -> s+1, 3 DP sync of stage s;
- *   out_class[i*4 + c] = PP | M << 8 where M is the micro-batches per replica
- *   of class c (0 for an absent class or an invalid plan).
- * Entries of absent stages are left untouched.  Same errors as
- * sim_eval_plans.
+ *   out_class[i*4 + c] = PP | classes << 5 | M << 8 where M is the
+ *   micro-batches per replica of class c (0 for an absent class or an
+ *   invalid plan).
+ * Entries of absent stages are left untouched.  n is at most 2^21 per call.
+ * Same errors as sim_eval_plans.
  */
 int sim_eval_stages(sim_ctx* ctx, const sim_plans* plans, int64_t n, uint64_t* out_stage, uint32_t* out_class,
                     void* stream);
@@ -180,10 +181,11 @@ int sim_best_reduce(sim_ctx* ctx, const sim_best* bests, int64_t n, sim_best* ou
 
 /*
  * Kernel timing for measurement.  When enabled, sim_eval_plans records a
- * HIP event pair on its stream around every launch of its pipeline kernel
- * and of the whole call; sim_get_timing synchronises those events and
+ * HIP event pair on its stream around every launch of its evaluation and
+ * plan-check kernels and around the whole call; sim_get_timing synchronises those events and
  * returns the accumulated milliseconds and launch counts, then clears them.
- * kind 0 = pipeline kernel, 1 = setup kernel, 2 = whole sim_eval_plans call.
+ * kind 0 = evaluation kernel (per-pipeline setup and 1F1B recurrence),
+ * 1 = plan check/pack kernel, 2 = whole sim_eval_plans call.
  */
 int sim_set_timing(sim_ctx* ctx, int enable);
 int sim_get_timing(sim_ctx* ctx, int kind, double* total_ms, int64_t* launches);

@@ -12,12 +12,14 @@
 
 namespace hetsim {
 hipError_t launch_fill32(uint32_t* p, uint32_t n, uint32_t v, hipStream_t s);
-hipError_t launch_setup(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, uint64_t* rec, uint32_t* meta,
-                        uint32_t* hist, hipStream_t s);
+hipError_t launch_prep(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, PackedPlan* packed,
+                       uint32_t* meta, uint32_t* hist, hipStream_t s);
+hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint32_t* meta, int64_t n, uint64_t* out_stage,
+                         hipStream_t s);
 hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* total, hipStream_t s);
 hipError_t launch_scatter(const uint32_t* meta, uint32_t nslots, uint32_t* cursor, uint32_t* ids, hipStream_t s);
-hipError_t launch_pipe(const uint64_t* rec, const uint32_t* meta, const uint32_t* ids, const uint32_t* total,
-                       uint32_t max_tasks, uint64_t* out, hipStream_t s);
+hipError_t launch_eval(const Tab& t, const PackedPlan* packed, const uint32_t* meta, const uint32_t* ids,
+                       const uint32_t* total, uint32_t max_tasks, uint64_t* out, hipStream_t s);
 hipError_t launch_argmin(const uint64_t* t, int64_t n, int64_t base, sim_best* b, hipStream_t s);
 hipError_t launch_best_reduce(const sim_best* in, int64_t n, sim_best* out, hipStream_t s);
 }  // namespace hetsim
@@ -135,20 +137,20 @@ static void end_event(sim_ctx* c, int kind, hipStream_t s, EventPair* e) {
   c->ev[kind].push_back(*e);
 }
 
-// Workspace of one chunk: per-plan records, pipeline metadata and ids, bucket
+// Workspace of one chunk: packed plans, pipeline metadata and ids, bucket
 // counts, cursors and the pipeline count.
 struct Work {
-  uint64_t* rec;
+  PackedPlan* packed;
   uint32_t *meta, *ids, *hist, *cursor, *total;
 };
 static size_t work_bytes(int64_t ch) {
-  return align256((size_t)ch * kPlanWords * 8) + 2 * align256((size_t)ch * 4 * 4) + 2 * align256(kBuckets * 4) +
-         align256(4);
+  return align256((size_t)ch * sizeof(PackedPlan)) + 2 * align256((size_t)ch * 4 * 4) +
+         2 * align256(kBuckets * 4) + align256(4);
 }
 static Work carve(void* base, int64_t ch) {
   Work w;
   char* p = (char*)base;
-  w.rec = (uint64_t*)p; p += align256((size_t)ch * kPlanWords * 8);
+  w.packed = (PackedPlan*)p; p += align256((size_t)ch * sizeof(PackedPlan));
   w.meta = (uint32_t*)p; p += align256((size_t)ch * 16);
   w.ids = (uint32_t*)p; p += align256((size_t)ch * 16);
   w.hist = (uint32_t*)p; p += align256(kBuckets * 4);
@@ -175,12 +177,13 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
     p.hdr += off; p.cut += off; p.cls += off; p.types += off;
     e = launch_fill32(w.hist, kBuckets, 0, s);
     bool t1 = e == hipSuccess && begin_event(c, 1, s, &ev);
-    if (e == hipSuccess) e = launch_setup(c->tab, p, cn, out + off, w.rec, w.meta, w.hist, s);
+    if (e == hipSuccess) e = launch_prep(c->tab, p, cn, out + off, w.packed, w.meta, w.hist, s);
     if (t1) end_event(c, 1, s, &ev);
     if (e == hipSuccess) e = launch_scan(w.hist, w.cursor, w.total, s);
     if (e == hipSuccess) e = launch_scatter(w.meta, (uint32_t)(cn * 4), w.cursor, w.ids, s);
     bool t0 = e == hipSuccess && begin_event(c, 0, s, &ev);
-    if (e == hipSuccess) e = launch_pipe(w.rec, w.meta, w.ids, w.total, (uint32_t)(cn * 4), out + off, s);
+    if (e == hipSuccess)
+      e = launch_eval(c->tab, w.packed, w.meta, w.ids, w.total, (uint32_t)(cn * 4), out + off, s);
     if (t0) end_event(c, 0, s, &ev);
   }
   if (tcall) end_event(c, 2, s, &call);
@@ -192,8 +195,16 @@ extern "C" int sim_eval_stages(sim_ctx* c, const sim_plans* plans, int64_t n, ui
                                uint32_t* out_class, void* stream) {
   if (!c || !plans_ok(plans, n) || (n > 0 && (!out_stage || !out_class))) return SIM_EINVAL;
   if (n == 0) return SIM_OK;
+  if (n > kChunk) return SIM_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
   if (hipSetDevice(c->device) != hipSuccess) return SIM_EHIP;
-  hipError_t e = launch_setup(c->tab, *plans, n, nullptr, out_stage, out_class, nullptr, (hipStream_t)stream);
+  void* ws = nullptr;
+  if (hipMallocFromPoolAsync(&ws, align256((size_t)n * sizeof(PackedPlan)), c->pool, s) != hipSuccess)
+    return SIM_ENOMEM;
+  PackedPlan* packed = (PackedPlan*)ws;
+  hipError_t e = launch_prep(c->tab, *plans, n, nullptr, packed, out_class, nullptr, s);
+  if (e == hipSuccess) e = launch_stages(c->tab, packed, out_class, n, out_stage, s);
+  (void)hipFreeAsync(ws, s);
   return e == hipSuccess ? SIM_OK : SIM_EHIP;
 }
 

@@ -12,8 +12,17 @@ constexpr int kMaxStages = 16;
 constexpr int kMaxClasses = 4;
 constexpr int kRecWords = 4;                    // per (plan, class, stage): fwd, bwd, hop, dp
 constexpr int kPlanWords = kMaxClasses * kMaxStages * kRecWords;
-constexpr int kBucketsM = 256;                  // micro-batch-count buckets per stage count
-constexpr int kBuckets = kMaxStages * kBucketsM;
+constexpr int kBucketsM = 128;                  // micro-batch-count buckets per (stages, classes)
+constexpr int kBuckets = kMaxStages * kMaxClasses * kBucketsM;
+
+// A validated plan packed into 80 contiguous bytes, so that the pipelines of
+// one plan gather it with five 16-byte loads.
+struct __attribute__((aligned(16))) PackedPlan {
+  uint32_t hdr, psum, pad0, pad1;   // header; replicas summed over classes
+  uint8_t cut[16];
+  uint32_t cls[4];
+  uint64_t types[4];
+};
 
 // Everything a kernel needs about one (model, cluster) pair.  Scalars travel
 // by value in the kernel argument block; tables live in device memory.

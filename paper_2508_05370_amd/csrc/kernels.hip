@@ -1,18 +1,19 @@
 // kernels.hip -- gfx950 kernels of the plan evaluator.
 //
 // Data flow of one chunk of plans (all in HBM):
-//   k_setup    one plan per lane: decode and validate the plan, place every
-//              (class, stage) on its device pool, read stage compute from the
-//              layer prefix tables, find each group's slowest link with
-//              range-max tables, and write per (class, stage) the forward and
-//              backward time of one micro-batch, the pipeline hop and the DP
-//              sync; counts pipelines per (stages, micro-batches) bucket.
+//   k_prep     one plan per lane: decode and check the plan, pack it into 80
+//              contiguous bytes, and count its pipelines (one per replica
+//              class) per (stages, classes, micro-batches) bucket.
 //   k_scan     one block: bucket offsets, longest pipelines first.
-//   k_scatter  groups pipeline ids by bucket, so a wavefront runs pipelines of
-//              one stage count and similar micro-batch counts.
-//   k_pipe     one pipeline per lane: the 1F1B recurrence, unrolled per stage
-//              count so that all per-stage state stays in VGPRs; times are
-//              integers carried exactly in fp64 (3 VALU ops per schedule
+//   k_scatter  groups pipeline ids by bucket, so that a wavefront runs
+//              pipelines of one stage count, one class count and similar
+//              micro-batch counts.
+//   k_eval     one pipeline per lane.  Setup: place the class on its device
+//              pools, read stage compute from the layer prefix tables, find
+//              each group's slowest link with range-max tables, and cost the
+//              TP/EP/PP/DP collectives.  Then the 1F1B recurrence, unrolled per
+//              stage count so that all per-stage state stays in VGPRs; times
+//              are integers carried exactly in fp64 (3 VALU ops per schedule
 //              node); a pipeline whose time reaches 2^53 ps is redone in u64.
 //              The plan's time is the max over its classes (atomic max).
 #include <hip/hip_runtime.h>
@@ -72,191 +73,122 @@ __device__ __forceinline__ uint64_t ring_sync(uint32_t p, double rp, uint32_t ze
   return 2 * steps * alpha + link_ps(steps * g, bq) + link_ps(steps * div_up(params, p, rp), bq);
 }
 
-__device__ __host__ __forceinline__ uint32_t m_bucket(uint32_t M) {
-  if (M <= 128) return M - 1;
-  if (M <= 1152) return 128 + (M - 129) / 16;
-  uint32_t b = 192 + (M - 1153) / 256;
-  return b > 255 ? 255 : b;
+// micro-batch counts: exact up to 64, then steps of 16 up to 1088
+__device__ __forceinline__ uint32_t m_bucket(uint32_t M) {
+  if (M <= 64) return M - 1;
+  const uint32_t b = 64 + (M - 65) / 16;
+  return b < kBucketsM - 1 ? b : kBucketsM - 1;
 }
-// ascending key: more stages first, then more micro-batches first
-__device__ __forceinline__ uint32_t bucket_key(uint32_t S, uint32_t M) {
-  return (kMaxStages - S) * kBucketsM + (kBucketsM - 1 - m_bucket(M));
+// ascending key: more stages first, then more classes, then more micro-batches
+__device__ __forceinline__ uint32_t bucket_key(uint32_t S, uint32_t G, uint32_t M) {
+  return ((kMaxStages - S) * kMaxClasses + (kMaxClasses - G)) * kBucketsM + (kBucketsM - 1 - m_bucket(M));
 }
 
-// ---------------------------------------------------------------- setup
-__device__ void setup_plan(const Tab& t, const sim_plans& pl, int64_t i, uint64_t* __restrict__ out,
-                           uint64_t* __restrict__ rec, uint32_t* __restrict__ meta, uint32_t* lh) {
-  const int64_t st = pl.stride;
-  const uint32_t hdr = pl.hdr[i];
-  const uint32_t tpl = hdr & 3, epl = (hdr >> 2) & 3, S = ((hdr >> 4) & 15) + 1, G = ((hdr >> 8) & 3) + 1;
-  const uint32_t zero = (hdr >> 10) & 1, mi = (hdr >> 11) & 3;
-  const uint32_t tp = 1u << tpl, ep = 1u << epl;
-  bool ok = (hdr >> 13) == 0 && mi < t.n_mbs && ((t.tp_ok >> tpl) & 1) && ((t.ep_ok >> epl) & 1);
-
-  uint32_t prev = 0;
-  for (uint32_t s = 0; s < S; ++s) {
-    uint32_t c = pl.cut[s * st + i];
-    ok = ok && c > prev;
-    prev = c;
-  }
-  ok = ok && prev == t.L;
-
-  const uint64_t sel = S == 16 ? ~0ull : ((1ull << (4 * S)) - 1);
+// ---------------------------------------------------------------- plan validation
+// Decoded plan fields used by every pipeline of the plan.
+struct Plan {
+  uint32_t tpl, epl, S, G, zero, mi, tp, ep, psum;
+  uint32_t cut[4];          // cut bytes, four per word
   uint32_t reps[4], nmb[4];
-  uint64_t tv[4];
-  uint32_t batch = 0, psum = 0;
-#pragma unroll
-  for (uint32_t c = 0; c < 4; ++c) {
-    reps[c] = 0; nmb[c] = 0; tv[c] = 0;
-    if (c < G) {
-      uint32_t w = pl.cls[c * st + i];
-      reps[c] = w & 0xffff;
-      nmb[c] = w >> 16;
-      tv[c] = pl.types[c * st + i] & sel;
-      ok = ok && reps[c] >= 1 && nmb[c] >= reps[c] && (reps[c] & (ep - 1)) == 0;
-      batch += nmb[c] * t.mbs[mi];
-      psum += reps[c];
-      for (uint32_t s = 0; s < S; ++s) {
-        uint32_t k = (uint32_t)(tv[c] >> (4 * s)) & 15;
-        ok = ok && k < t.K && t.dpn_log2[k] >= tpl;
-      }
-    }
-  }
-  ok = ok && batch == t.gbs;
-  for (uint32_t k = 0; ok && k < t.K; ++k) {
-    uint32_t need = 0;
-#pragma unroll
-    for (uint32_t c = 0; c < 4; ++c)
-      if (c < G) need += reps[c] * count_type(tv[c], k, sel);
-    ok = need * tp <= t.cap[k];
-  }
-  if (!ok) {
-    if (out) out[i] = kInvalid;
-    if (meta)
-#pragma unroll
-      for (uint32_t c = 0; c < 4; ++c) meta[i * 4 + c] = 0;
-    return;
-  }
-  if (out) out[i] = 0;
+  uint64_t tv[4];           // stage types, nibbles past S cleared
+};
 
-  const uint64_t act = t.act[mi], act_tp = (act + tp - 1) >> tpl;
-  const double rp = 1.0 / (double)psum, rpe = 1.0 / (double)(psum >> epl);
-  const size_t L1 = t.L + 1;
-  uint64_t* R = rec + (size_t)i * kPlanWords;
-  uint32_t pk[4] = {0, 0, 0, 0}, pbase[4] = {0, 0, 0, 0}, pnic[4] = {0, 0, 0, 0}, pin[4] = {0, 0, 0, 0};
-  uint32_t lo = 0;
-  for (uint32_t s = 0; s < S; ++s) {
-    const uint32_t hi = pl.cut[s * st + i], ns = hi - lo;
-    bool same = true;
-    uint32_t k0 = 0, nmin = 0xffffffffu, nmax = 0, bq_dp = 0;
-    uint64_t a_dp = 0;
-#pragma unroll
-    for (uint32_t c = 0; c < 4; ++c) {
-      if (c >= G) continue;
-      const uint32_t k = (uint32_t)(tv[c] >> (4 * s)) & 15;
-      // canonical packing: this (class, stage) follows everything placed before it in pool k
-      uint32_t below = reps[c] * count_type(tv[c], k, (1ull << (4 * s)) - 1);
-#pragma unroll
-      for (uint32_t c2 = 0; c2 < c; ++c2) below += reps[c2] * count_type(tv[c2], k, sel);
-      const uint32_t base = below * tp, nd = reps[c] * tp, dpl = t.dpn_log2[k];
-      const uint32_t gnl = t.node_off[k] + (base >> dpl), gnh = t.node_off[k] + ((base + nd - 1) >> dpl);
-      const uint32_t bq_in = range_max(t.rm_intra, t.N, gnl, gnh);
-      const uint32_t dlo = t.dev_off[k] + base;
-      const uint32_t bq_nic = range_max(t.rm_nic, t.D, dlo, dlo + nd - 1);
-      const size_t tb = ((((size_t)k * 4 + tpl) * t.n_mbs + mi) * 4 + epl) * L1;
-      uint64_t fc = t.pf[tb + hi] - t.pf[tb + lo];
-      uint64_t bc = t.pb[tb + hi] - t.pb[tb + lo];
-      if (s == 0) {
-        fc += t.emb[((size_t)k * t.n_mbs + mi) * 2];
-        bc += t.emb[((size_t)k * t.n_mbs + mi) * 2 + 1];
-      }
-      if (s == S - 1) {
-        const size_t hb = (((size_t)k * 4 + tpl) * t.n_mbs + mi) * 2;
-        fc += t.head[hb];
-        bc += t.head[hb + 1];
-      }
-      if (tp > 1) {  // TP all-reduces of this stage, exposed in the forward pass
-        const uint64_t steps = (uint64_t)(2 * ns + (s == 0)) * 2 * (tp - 1);
-        fc += steps * t.a_intra[k] + link_ps(steps * act_tp, bq_in);
-      }
-      if (t.E && ep > 1) {  // dispatch + combine all-to-all in each pass
-        // EP groups are aligned blocks of ep*tp devices: inside a node iff they fit one
-        const bool intra = ep * tp <= (1u << dpl);
-        const uint64_t alpha = intra ? t.a_intra[k] : 2 * t.a_side[k];
-        const uint32_t bq = intra ? bq_in : (bq_nic > t.bq_pcie[k] ? bq_nic : t.bq_pcie[k]);
-        const size_t pb = ((size_t)epl * t.n_mbs + mi) * L1;
-        const uint64_t e = (uint64_t)ns * 2 * (ep - 1) * alpha + link_ps(2 * (t.pa[pb + hi] - t.pa[pb + lo]), bq);
-        fc += e;
-        bc += e;
-      }
-      uint64_t* r = R + (c * kMaxStages + s) * kRecWords;
-      r[0] = fc;
-      r[1] = bc;
-      if (s > 0) {  // hop (s-1) -> s of this class
-        // same pool means the two ranges are adjacent: intra iff the pair spans one node
-        const bool intra = pk[c] == k && (pbase[c] >> dpl) == ((pbase[c] + (2 * reps[c] - 1) * tp) >> dpl);
-        const uint64_t alpha = intra ? t.a_intra[k] : t.a_side[pk[c]] + t.a_side[k];
-        uint32_t bq;
-        if (intra) {
-          bq = pin[c] > bq_in ? pin[c] : bq_in;
-        } else {
-          uint32_t a = pnic[c] > bq_nic ? pnic[c] : bq_nic;
-          uint32_t b = t.bq_pcie[pk[c]] > t.bq_pcie[k] ? t.bq_pcie[pk[c]] : t.bq_pcie[k];
-          bq = a > b ? a : b;
-        }
-        R[(c * kMaxStages + s - 1) * kRecWords + 2] = alpha + link_ps(act, bq);
-      }
-      pk[c] = k; pbase[c] = base; pnic[c] = bq_nic; pin[c] = bq_in;
-      if (c == 0) k0 = k; else same = same && k == k0;
-      nmin = gnl < nmin ? gnl : nmin;
-      nmax = gnh > nmax ? gnh : nmax;
-      const uint32_t bx = bq_nic > t.bq_pcie[k] ? bq_nic : t.bq_pcie[k];
-      bq_dp = bx > bq_dp ? bx : bq_dp;
-      a_dp = 2 * t.a_side[k] > a_dp ? 2 * t.a_side[k] : a_dp;
-    }
-    // DP sync of this stage over every replica of every class
-    uint64_t tdp = 0;
-    if (psum > 1) {
-      const bool intra = same && nmin == nmax;
-      const uint64_t alpha = intra ? t.a_intra[k0] : a_dp;
-      const uint32_t bq = intra ? t.rm_intra[nmin] : bq_dp;
-      const uint64_t pd = (uint64_t)ns * t.par_layer[tpl] + (s == 0 ? t.par_embed[tpl] : 0) +
-                          (s == S - 1 ? t.par_head[tpl] : 0);
-      tdp = ring_sync(psum, rp, zero, t.grad_bytes * pd, t.param_bytes * pd, alpha, bq);
-      const uint32_t pe = psum >> epl;
-      if (t.E && pe > 1) {
-        const uint64_t px = (uint64_t)ns * t.par_expert[tpl][epl];
-        tdp += ring_sync(pe, rpe, zero, t.grad_bytes * px, t.param_bytes * px, alpha, bq);
-      }
-    }
-#pragma unroll
-    for (uint32_t c = 0; c < 4; ++c)
-      if (c < G) R[(c * kMaxStages + s) * kRecWords + 3] = tdp;
-    lo = hi;
-  }
-#pragma unroll
-  for (uint32_t c = 0; c < 4; ++c) {
-    uint32_t m = 0;
-    if (c < G) {
-      R[(c * kMaxStages + S - 1) * kRecWords + 2] = 0;
-      const uint32_t M = (nmb[c] + reps[c] - 1) / reps[c];
-      m = S | (M << 8);
-      if (lh) atomicAdd(&lh[bucket_key(S, M)], 1u);
-    }
-    if (meta) meta[i * 4 + c] = m;
-  }
+__device__ __forceinline__ uint32_t cut_at(const Plan& p, uint32_t s) {
+  const uint32_t w = s < 8 ? (s < 4 ? p.cut[0] : p.cut[1]) : (s < 12 ? p.cut[2] : p.cut[3]);
+  return (w >> (8 * (s & 3))) & 0xff;
 }
 
-__global__ void __launch_bounds__(256) k_setup(Tab t, sim_plans pl, int64_t n, uint64_t* __restrict__ out,
-                                               uint64_t* __restrict__ rec, uint32_t* __restrict__ meta,
-                                               uint32_t* __restrict__ hist) {
+__device__ __forceinline__ Plan unpack(const PackedPlan& q) {
+  Plan p;
+  const uint32_t hdr = q.hdr;
+  p.tpl = hdr & 3; p.epl = (hdr >> 2) & 3; p.S = ((hdr >> 4) & 15) + 1; p.G = ((hdr >> 8) & 3) + 1;
+  p.zero = (hdr >> 10) & 1; p.mi = (hdr >> 11) & 3; p.tp = 1u << p.tpl; p.ep = 1u << p.epl; p.psum = q.psum;
+  const uint32_t* cw = reinterpret_cast<const uint32_t*>(q.cut);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    p.cut[j] = cw[j];
+    p.reps[j] = q.cls[j] & 0xffff;
+    p.nmb[j] = q.cls[j] >> 16;
+    p.tv[j] = q.types[j];
+  }
+  return p;
+}
+
+// Decode and check plan i (every rule of the plan layout); on success pack it.
+// Writes out[i] (0 = valid, to be raised by the pipelines; else invalid) and
+// the per-pipeline metadata S | G << 5 | M << 8 (0 = no pipeline).
+__global__ void __launch_bounds__(256) k_prep(Tab t, sim_plans pl, int64_t n, uint64_t* __restrict__ out,
+                                              PackedPlan* __restrict__ packed, uint32_t* __restrict__ meta,
+                                              uint32_t* __restrict__ hist) {
   __shared__ uint32_t lh[kBuckets];
   if (hist) {
     for (uint32_t j = threadIdx.x; j < kBuckets; j += blockDim.x) lh[j] = 0;
     __syncthreads();
   }
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) setup_plan(t, pl, i, out, rec, meta, hist ? lh : nullptr);
+  if (i < n) {
+    const int64_t st = pl.stride;
+    const uint32_t hdr = pl.hdr[i];
+    const uint32_t tpl = hdr & 3, epl = (hdr >> 2) & 3, S = ((hdr >> 4) & 15) + 1, G = ((hdr >> 8) & 3) + 1;
+    const uint32_t mi = (hdr >> 11) & 3;
+    const uint32_t tp = 1u << tpl, ep = 1u << epl;
+    bool ok = (hdr >> 13) == 0 && mi < t.n_mbs && ((t.tp_ok >> tpl) & 1) && ((t.ep_ok >> epl) & 1);
+    uint32_t cw[4] = {0, 0, 0, 0}, prev = 0;
+    for (uint32_t s = 0; s < S; ++s) {
+      const uint32_t c = pl.cut[s * st + i];
+      ok = ok && c > prev;
+      prev = c;
+      cw[s >> 2] |= c << (8 * (s & 3));
+    }
+    ok = ok && prev == t.L;
+    const uint64_t sel = S == 16 ? ~0ull : ((1ull << (4 * S)) - 1);
+    uint32_t cls[4];
+    uint64_t tv[4];
+    uint32_t batch = 0, psum = 0;
+#pragma unroll
+    for (uint32_t c = 0; c < 4; ++c) {
+      cls[c] = 0; tv[c] = 0;
+      if (c < G) {
+        cls[c] = pl.cls[c * st + i];
+        tv[c] = pl.types[c * st + i] & sel;
+        const uint32_t reps = cls[c] & 0xffff, nmb = cls[c] >> 16;
+        ok = ok && reps >= 1 && nmb >= reps && (reps & (ep - 1)) == 0;
+        batch += nmb * t.mbs[mi];
+        psum += reps;
+        for (uint32_t s = 0; s < S; ++s) {
+          const uint32_t k = (uint32_t)(tv[c] >> (4 * s)) & 15;
+          ok = ok && k < t.K && t.dpn_log2[k] >= tpl;
+        }
+      }
+    }
+    ok = ok && batch == t.gbs;
+    for (uint32_t k = 0; ok && k < t.K; ++k) {
+      uint32_t need = 0;
+#pragma unroll
+      for (uint32_t c = 0; c < 4; ++c)
+        if (c < G) need += (cls[c] & 0xffff) * count_type(tv[c], k, sel);
+      ok = need * tp <= t.cap[k];
+    }
+    if (out) out[i] = ok ? 0 : kInvalid;
+    if (ok) {
+      PackedPlan q;
+      q.hdr = hdr; q.psum = psum; q.pad0 = 0; q.pad1 = 0;
+      uint32_t* qc = reinterpret_cast<uint32_t*>(q.cut);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) { qc[j] = cw[j]; q.cls[j] = cls[j]; q.types[j] = tv[j]; }
+      packed[i] = q;
+    }
+#pragma unroll
+    for (uint32_t c = 0; c < 4; ++c) {
+      uint32_t m = 0;
+      if (ok && c < G) {
+        const uint32_t reps = cls[c] & 0xffff, M = ((cls[c] >> 16) + reps - 1) / reps;
+        m = S | (G << 5) | (M << 8);
+        if (hist) atomicAdd(&lh[bucket_key(S, G, M)], 1u);
+      }
+      meta[i * 4 + c] = m;
+    }
+  }
   if (hist) {
     __syncthreads();
     for (uint32_t j = threadIdx.x; j < kBuckets; j += blockDim.x)
@@ -264,6 +196,139 @@ __global__ void __launch_bounds__(256) k_setup(Tab t, sim_plans pl, int64_t n, u
   }
 }
 
+// ---------------------------------------------------------------- per-pipeline setup
+// Stage quantities of class c of a valid plan: rec[s] = {forward and backward
+// time of one micro-batch on stage s, hop s -> s+1, DP sync of stage s}.
+//
+// Placement: every pool is filled in (class, stage) order, reps*tp devices per
+// (class, stage), so a (class, stage) of type k starts after the devices of
+// type k used by earlier classes and by earlier stages of its own class.
+__device__ __forceinline__ uint32_t placed_before(const Plan& p, uint32_t c, uint32_t s, uint32_t k) {
+  const uint64_t sel = p.S == 16 ? ~0ull : ((1ull << (4 * p.S)) - 1);
+  uint32_t below = 0;
+#pragma unroll
+  for (uint32_t c2 = 0; c2 < 4; ++c2)
+    if (c2 < c) below += p.reps[c2] * count_type(p.tv[c2], k, sel);
+  const uint32_t rc = c == 0 ? p.reps[0] : c == 1 ? p.reps[1] : c == 2 ? p.reps[2] : p.reps[3];
+  const uint64_t tc = c == 0 ? p.tv[0] : c == 1 ? p.tv[1] : c == 2 ? p.tv[2] : p.tv[3];
+  return below + rc * count_type(tc, k, (1ull << (4 * s)) - 1);
+}
+
+__device__ void class_setup(const Tab& t, const Plan& p, uint32_t c, uint64_t (&rec)[kMaxStages][kRecWords]) {
+  const uint32_t S = p.S, G = p.G, tp = p.tp, ep = p.ep, tpl = p.tpl, epl = p.epl, mi = p.mi;
+  const uint64_t act = t.act[mi], act_tp = (act + tp - 1) >> tpl;
+  const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> epl);
+  const size_t L1 = t.L + 1;
+  const uint32_t reps = c == 0 ? p.reps[0] : c == 1 ? p.reps[1] : c == 2 ? p.reps[2] : p.reps[3];
+  const uint64_t tvc = c == 0 ? p.tv[0] : c == 1 ? p.tv[1] : c == 2 ? p.tv[2] : p.tv[3];
+  uint32_t pk = 0, pbase = 0, pnic = 0, pin = 0, lo = 0;
+  for (uint32_t s = 0; s < S; ++s) {
+    const uint32_t hi = cut_at(p, s), ns = hi - lo;
+    // ---- this class: compute, TP, EP, hop from the previous stage
+    const uint32_t k = (uint32_t)(tvc >> (4 * s)) & 15;
+    const uint32_t base = placed_before(p, c, s, k) * tp, nd = reps * tp, dpl = t.dpn_log2[k];
+    const uint32_t gnl = t.node_off[k] + (base >> dpl), gnh = t.node_off[k] + ((base + nd - 1) >> dpl);
+    const uint32_t bq_in = range_max(t.rm_intra, t.N, gnl, gnh);
+    const uint32_t dlo = t.dev_off[k] + base;
+    const uint32_t bq_nic = range_max(t.rm_nic, t.D, dlo, dlo + nd - 1);
+    const size_t tb = ((((size_t)k * 4 + tpl) * t.n_mbs + mi) * 4 + epl) * L1;
+    uint64_t fc = t.pf[tb + hi] - t.pf[tb + lo];
+    uint64_t bc = t.pb[tb + hi] - t.pb[tb + lo];
+    if (s == 0) {
+      fc += t.emb[((size_t)k * t.n_mbs + mi) * 2];
+      bc += t.emb[((size_t)k * t.n_mbs + mi) * 2 + 1];
+    }
+    if (s == S - 1) {
+      const size_t hb = (((size_t)k * 4 + tpl) * t.n_mbs + mi) * 2;
+      fc += t.head[hb];
+      bc += t.head[hb + 1];
+    }
+    if (tp > 1) {  // TP all-reduces of this stage, exposed in the forward pass
+      const uint64_t steps = (uint64_t)(2 * ns + (s == 0)) * 2 * (tp - 1);
+      fc += steps * t.a_intra[k] + link_ps(steps * act_tp, bq_in);
+    }
+    if (t.E && ep > 1) {  // dispatch + combine all-to-all in each pass
+      // EP groups are aligned blocks of ep*tp devices: inside a node iff they fit one
+      const bool intra = ep * tp <= (1u << dpl);
+      const uint64_t alpha = intra ? t.a_intra[k] : 2 * t.a_side[k];
+      const uint32_t bq = intra ? bq_in : (bq_nic > t.bq_pcie[k] ? bq_nic : t.bq_pcie[k]);
+      const size_t pa = ((size_t)epl * t.n_mbs + mi) * L1;
+      const uint64_t e = (uint64_t)ns * 2 * (ep - 1) * alpha + link_ps(2 * (t.pa[pa + hi] - t.pa[pa + lo]), bq);
+      fc += e;
+      bc += e;
+    }
+    rec[s][0] = fc;
+    rec[s][1] = bc;
+    if (s > 0) {  // hop (s-1) -> s
+      // same pool means the two ranges are adjacent: intra iff the pair spans one node
+      const bool intra = pk == k && (pbase >> dpl) == ((pbase + (2 * reps - 1) * tp) >> dpl);
+      const uint64_t alpha = intra ? t.a_intra[k] : t.a_side[pk] + t.a_side[k];
+      uint32_t bq;
+      if (intra) {
+        bq = pin > bq_in ? pin : bq_in;
+      } else {
+        const uint32_t a = pnic > bq_nic ? pnic : bq_nic;
+        const uint32_t b = t.bq_pcie[pk] > t.bq_pcie[k] ? t.bq_pcie[pk] : t.bq_pcie[k];
+        bq = a > b ? a : b;
+      }
+      rec[s - 1][2] = alpha + link_ps(act, bq);
+    }
+    pk = k; pbase = base; pnic = bq_nic; pin = bq_in;
+    // ---- DP sync of this stage over every replica of every class
+    uint64_t tdp = 0;
+    if (p.psum > 1) {
+      bool same = true;
+      uint32_t k0 = 0, nmin = 0xffffffffu, nmax = 0, bq_dp = 0;
+      uint64_t a_dp = 0;
+#pragma unroll
+      for (uint32_t c2 = 0; c2 < 4; ++c2) {
+        if (c2 >= G) continue;
+        const uint32_t k2 = (uint32_t)(p.tv[c2] >> (4 * s)) & 15;
+        const uint32_t b2 = placed_before(p, c2, s, k2) * tp, n2 = p.reps[c2] * tp, d2 = t.dpn_log2[k2];
+        const uint32_t l2 = t.node_off[k2] + (b2 >> d2), h2 = t.node_off[k2] + ((b2 + n2 - 1) >> d2);
+        const uint32_t dl2 = t.dev_off[k2] + b2;
+        const uint32_t nic2 = range_max(t.rm_nic, t.D, dl2, dl2 + n2 - 1);
+        if (c2 == 0) k0 = k2; else same = same && k2 == k0;
+        nmin = l2 < nmin ? l2 : nmin;
+        nmax = h2 > nmax ? h2 : nmax;
+        const uint32_t bx = nic2 > t.bq_pcie[k2] ? nic2 : t.bq_pcie[k2];
+        bq_dp = bx > bq_dp ? bx : bq_dp;
+        a_dp = 2 * t.a_side[k2] > a_dp ? 2 * t.a_side[k2] : a_dp;
+      }
+      const bool intra = same && nmin == nmax;
+      const uint64_t alpha = intra ? t.a_intra[k0] : a_dp;
+      const uint32_t bq = intra ? t.rm_intra[nmin] : bq_dp;
+      const uint64_t pd = (uint64_t)ns * t.par_layer[tpl] + (s == 0 ? t.par_embed[tpl] : 0) +
+                          (s == S - 1 ? t.par_head[tpl] : 0);
+      tdp = ring_sync(p.psum, rp, p.zero, t.grad_bytes * pd, t.param_bytes * pd, alpha, bq);
+      const uint32_t pe = p.psum >> epl;
+      if (t.E && pe > 1) {
+        const uint64_t px = (uint64_t)ns * t.par_expert[tpl][epl];
+        tdp += ring_sync(pe, rpe, p.zero, t.grad_bytes * px, t.param_bytes * px, alpha, bq);
+      }
+    }
+    rec[s][3] = tdp;
+    lo = hi;
+  }
+  rec[S - 1][2] = 0;
+}
+
+// per (class, stage) quantities of every plan, in plan order
+__global__ void __launch_bounds__(256) k_stages(Tab t, const PackedPlan* __restrict__ packed,
+                                                const uint32_t* __restrict__ meta, int64_t n,
+                                                uint64_t* __restrict__ out_stage) {
+  const int64_t slot = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (slot >= n * 4 || meta[slot] == 0) return;
+  const Plan p = unpack(packed[slot >> 2]);
+  uint64_t rec[kMaxStages][kRecWords];
+  class_setup(t, p, (uint32_t)(slot & 3), rec);
+  uint64_t* o = out_stage + slot * (kMaxStages * kRecWords);
+  for (uint32_t s = 0; s < p.S; ++s)
+#pragma unroll
+    for (int q = 0; q < kRecWords; ++q) o[s * kRecWords + q] = rec[s][q];
+}
+
+// ---------------------------------------------------------------- bucketing
 __global__ void k_fill32(uint32_t* p, uint32_t n, uint32_t v) {
   for (uint32_t j = blockIdx.x * blockDim.x + threadIdx.x; j < n; j += gridDim.x * blockDim.x) p[j] = v;
 }
@@ -272,6 +337,7 @@ __global__ void k_fill32(uint32_t* p, uint32_t n, uint32_t v) {
 __global__ void __launch_bounds__(1024) k_scan(const uint32_t* __restrict__ hist, uint32_t* __restrict__ cursor,
                                                uint32_t* __restrict__ total) {
   constexpr int kPer = kBuckets / 1024;
+  static_assert(kBuckets % 1024 == 0, "bucket count");
   __shared__ uint32_t part[1024];
   uint32_t v[kPer], sum = 0;
   const uint32_t tid = threadIdx.x;
@@ -280,7 +346,7 @@ __global__ void __launch_bounds__(1024) k_scan(const uint32_t* __restrict__ hist
   part[tid] = sum;
   __syncthreads();
   for (uint32_t off = 1; off < 1024; off <<= 1) {
-    uint32_t x = tid >= off ? part[tid - off] : 0;
+    const uint32_t x = tid >= off ? part[tid - off] : 0;
     __syncthreads();
     part[tid] += x;
     __syncthreads();
@@ -304,10 +370,11 @@ __global__ void __launch_bounds__(256) k_scatter(const uint32_t* __restrict__ me
   for (int j = 0; j < kPer; ++j) {
     const uint32_t slot = first + j * blockDim.x;
     key[j] = 0xffffffffu;
+    rank[j] = 0;
     if (slot < nslots) {
       const uint32_t m = meta[slot];
       if (m) {
-        key[j] = bucket_key(m & 255, m >> 8);
+        key[j] = bucket_key(m & 31, (m >> 5) & 7, m >> 8);
         rank[j] = atomicAdd(&lc[key[j]], 1u);
       }
     }
@@ -333,14 +400,16 @@ __global__ void __launch_bounds__(256) k_scatter(const uint32_t* __restrict__ me
 // forward form the steady loop; the last min(S-1, M) iterations, where the
 // upper stages have run out of forwards, are unrolled.
 //   out_f[s] end of the latest forward on stage s, last[s] end of its latest op.
+typedef uint64_t StageRec[kMaxStages][kRecWords];
+
 template <int S>
-__device__ __forceinline__ uint64_t pipe_fp64(const uint64_t* __restrict__ R, uint32_t M) {
+__device__ __forceinline__ uint64_t pipe_fp64(const StageRec& R, uint32_t M) {
   double f[S], b[S], c[S], out_f[S], last[S];
 #pragma unroll
   for (int s = 0; s < S; ++s) {
-    f[s] = (double)R[s * kRecWords + 0];
-    b[s] = (double)R[s * kRecWords + 1];
-    c[s] = (double)R[s * kRecWords + 2];
+    f[s] = (double)R[s][0];
+    b[s] = (double)R[s][1];
+    c[s] = (double)R[s][2];
     out_f[s] = 0.0;
     last[s] = 0.0;
   }
@@ -384,27 +453,27 @@ __device__ __forceinline__ uint64_t pipe_fp64(const uint64_t* __restrict__ R, ui
   }
   double T = 0.0;
 #pragma unroll
-  for (int s = 0; s < S; ++s) T = __builtin_fmax(T, last[s] + (double)R[s * kRecWords + 3]);
+  for (int s = 0; s < S; ++s) T = __builtin_fmax(T, last[s] + (double)R[s][3]);
   // integers below 2^53 are exact in fp64; if no value ever reached 2^53 every
   // add was exact, and the result bounds every intermediate value
   return T < 9007199254740992.0 ? (uint64_t)T : kInvalid;
 }
 
 // same schedule in u64, for pipelines whose time reaches 2^53 ps
-__device__ __noinline__ uint64_t pipe_u64(const uint64_t* __restrict__ R, int S, uint32_t M) {
+__device__ __noinline__ uint64_t pipe_u64(const StageRec& R, int S, uint32_t M) {
   uint64_t out_f[kMaxStages], last[kMaxStages];
   for (int s = 0; s < S; ++s) { out_f[s] = 0; last[s] = 0; }
   const int m_ = (int)M;
   auto fwd = [&](int s) {
     uint64_t st = last[s];
-    if (s > 0) { uint64_t r = out_f[s - 1] + R[(s - 1) * kRecWords + 2]; st = st > r ? st : r; }
-    out_f[s] = st + R[s * kRecWords + 0];
+    if (s > 0) { uint64_t r = out_f[s - 1] + R[s - 1][2]; st = st > r ? st : r; }
+    out_f[s] = st + R[s][0];
     last[s] = out_f[s];
   };
   auto bwd = [&](int s) {
     uint64_t st = last[s];
-    if (s < S - 1) { uint64_t r = last[s + 1] + R[s * kRecWords + 2]; st = st > r ? st : r; }
-    last[s] = st + R[s * kRecWords + 1];
+    if (s < S - 1) { uint64_t r = last[s + 1] + R[s][2]; st = st > r ? st : r; }
+    last[s] = st + R[s][1];
   };
   for (int m = 0; m < S - 1 && m < m_; ++m)
     for (int s = 0; s < S - 1 - m; ++s) fwd(s);
@@ -417,35 +486,37 @@ __device__ __noinline__ uint64_t pipe_u64(const uint64_t* __restrict__ R, int S,
     }
   uint64_t T = 0;
   for (int s = 0; s < S; ++s) {
-    uint64_t v = last[s] + R[s * kRecWords + 3];
+    uint64_t v = last[s] + R[s][3];
     T = T > v ? T : v;
   }
   return T;
 }
 
 template <int S>
-__device__ __forceinline__ uint64_t run_pipe(const uint64_t* R, uint32_t M) {
+__device__ __forceinline__ uint64_t run_pipe(const StageRec& R, uint32_t M) {
   uint64_t r = pipe_fp64<S>(R, M);
   return r != kInvalid ? r : pipe_u64(R, S, M);
 }
 
-__global__ void __launch_bounds__(64) k_pipe(const uint64_t* __restrict__ rec, const uint32_t* __restrict__ meta,
-                                             const uint32_t* __restrict__ ids, const uint32_t* __restrict__ total,
-                                             uint64_t* __restrict__ out) {
+__global__ void __launch_bounds__(64) k_eval(Tab t, const PackedPlan* __restrict__ packed,
+                                             const uint32_t* __restrict__ meta, const uint32_t* __restrict__ ids,
+                                             const uint32_t* __restrict__ total, uint64_t* __restrict__ out) {
   const uint32_t tot = *total;
   if (blockIdx.x * 64u >= tot) return;
   const uint32_t pos = blockIdx.x * 64u + threadIdx.x;
   bool pending = pos < tot;
   const uint32_t slot = pending ? ids[pos] : 0;
   const uint32_t m = pending ? meta[slot] : 0;
-  const uint32_t S = m & 255, M = m >> 8;
-  const uint64_t* R = rec + (size_t)(slot >> 2) * kPlanWords + (slot & 3) * (kMaxStages * kRecWords);
+  const uint32_t S = m & 31, M = m >> 8;
   // one pass per distinct stage count present in the wavefront (usually one)
   while (true) {
     const uint64_t live = __ballot(pending);
     if (!live) break;
     const uint32_t S0 = __builtin_amdgcn_readfirstlane(__shfl(S, __ffsll((unsigned long long)live) - 1));
     if (pending && S == S0) {
+      const Plan p = unpack(packed[slot >> 2]);
+      StageRec R;
+      class_setup(t, p, slot & 3, R);
       uint64_t r;
       switch (S0) {
         case 1: r = run_pipe<1>(R, M); break;
@@ -552,9 +623,14 @@ hipError_t launch_fill32(uint32_t* p, uint32_t n, uint32_t v, hipStream_t s) {
   k_fill32<<<blocks_for(n, 256) < 1024 ? blocks_for(n, 256) : 1024, 256, 0, s>>>(p, n, v);
   return hipGetLastError();
 }
-hipError_t launch_setup(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, uint64_t* rec, uint32_t* meta,
-                        uint32_t* hist, hipStream_t s) {
-  k_setup<<<blocks_for(n, 256), 256, 0, s>>>(t, p, n, out, rec, meta, hist);
+hipError_t launch_prep(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, PackedPlan* packed,
+                       uint32_t* meta, uint32_t* hist, hipStream_t s) {
+  k_prep<<<blocks_for(n, 256), 256, 0, s>>>(t, p, n, out, packed, meta, hist);
+  return hipGetLastError();
+}
+hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint32_t* meta, int64_t n, uint64_t* out_stage,
+                         hipStream_t s) {
+  k_stages<<<blocks_for(n * 4, 256), 256, 0, s>>>(t, packed, meta, n, out_stage);
   return hipGetLastError();
 }
 hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* total, hipStream_t s) {
@@ -565,9 +641,9 @@ hipError_t launch_scatter(const uint32_t* meta, uint32_t nslots, uint32_t* curso
   k_scatter<<<blocks_for(nslots, 256 * 4), 256, 0, s>>>(meta, nslots, cursor, ids);
   return hipGetLastError();
 }
-hipError_t launch_pipe(const uint64_t* rec, const uint32_t* meta, const uint32_t* ids, const uint32_t* total,
-                       uint32_t max_tasks, uint64_t* out, hipStream_t s) {
-  k_pipe<<<blocks_for(max_tasks, 64), 64, 0, s>>>(rec, meta, ids, total, out);
+hipError_t launch_eval(const Tab& t, const PackedPlan* packed, const uint32_t* meta, const uint32_t* ids,
+                       const uint32_t* total, uint32_t max_tasks, uint64_t* out, hipStream_t s) {
+  k_eval<<<blocks_for(max_tasks, 64), 64, 0, s>>>(t, packed, meta, ids, total, out);
   return hipGetLastError();
 }
 hipError_t launch_argmin(const uint64_t* t, int64_t n, int64_t base, sim_best* b, hipStream_t s) {

@@ -96,7 +96,7 @@ def test_stage_records(torch, B, oracle_mod, workloads, idx):
             if g >= G:
                 assert cl[i, g] == 0
                 continue
-            assert cl[i, g] == S | (d["M"][g] << 8), (i, g)
+            assert cl[i, g] == S | (G << 5) | (d["M"][g] << 8), (i, g)
             for s in range(S):
                 rec = [int(v) for v in st[i, g, s]]
                 want = [d["f"][g][s], d["b"][g][s], d["c"][g][s], d["tdp"][s]]
