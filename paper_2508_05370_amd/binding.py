@@ -47,11 +47,13 @@ EXPORTS = ("sim_create", "sim_eval_plans", "sim_eval_stages", "sim_argmin", "sim
 
 
 def lib():
+    """Load libhetsim.so (built in-tree; HETSIM_LIB may name another build of it)."""
     global _lib
     if _lib is None:
-        if not os.path.exists(_build.LIB):
+        path = os.environ.get("HETSIM_LIB") or _build.LIB
+        if path == _build.LIB and not os.path.exists(path):
             _build.build(force=False)
-        L = C.CDLL(_build.LIB)
+        L = C.CDLL(path)
         P, I64 = C.c_void_p, C.c_int64
         L.sim_create.argtypes = [C.POINTER(ModelDesc), C.POINTER(ClusterDesc), C.POINTER(P)]
         L.sim_create.restype = C.c_int

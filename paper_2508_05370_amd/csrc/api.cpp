@@ -16,10 +16,10 @@ hipError_t launch_prep(const Tab& t, const sim_plans& p, int64_t n, uint64_t* ou
                        uint32_t* meta, uint32_t* hist, hipStream_t s);
 hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint32_t* meta, int64_t n, uint64_t* out_stage,
                          hipStream_t s);
-hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* total, hipStream_t s);
+hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* gstart, hipStream_t s);
 hipError_t launch_scatter(const uint32_t* meta, uint32_t nslots, uint32_t* cursor, uint32_t* ids, hipStream_t s);
 hipError_t launch_eval(const Tab& t, const PackedPlan* packed, const uint32_t* meta, const uint32_t* ids,
-                       const uint32_t* total, uint32_t max_tasks, uint64_t* out, hipStream_t s);
+                       const uint32_t* gstart, uint32_t max_tasks, uint64_t* out, uint32_t* ovf, hipStream_t s);
 hipError_t launch_argmin(const uint64_t* t, int64_t n, int64_t base, sim_best* b, hipStream_t s);
 hipError_t launch_best_reduce(const sim_best* in, int64_t n, sim_best* out, hipStream_t s);
 }  // namespace hetsim
@@ -138,14 +138,17 @@ static void end_event(sim_ctx* c, int kind, hipStream_t s, EventPair* e) {
 }
 
 // Workspace of one chunk: packed plans, pipeline metadata and ids, bucket
-// counts, cursors and the pipeline count.
+// counts followed by the overflow list (count, then pipeline ids; cleared
+// together with the counts), bucket cursors, and the start of each
+// stage-count group.
+constexpr uint32_t kCounters = kBuckets + 8;
 struct Work {
   PackedPlan* packed;
-  uint32_t *meta, *ids, *hist, *cursor, *total;
+  uint32_t *meta, *ids, *hist, *ovf, *cursor, *gstart;
 };
 static size_t work_bytes(int64_t ch) {
   return align256((size_t)ch * sizeof(PackedPlan)) + 2 * align256((size_t)ch * 4 * 4) +
-         2 * align256(kBuckets * 4) + align256(4);
+         align256(kCounters * 4 + (size_t)ch * 4 * 4) + align256(kBuckets * 4) + align256(8 * 4);
 }
 static Work carve(void* base, int64_t ch) {
   Work w;
@@ -153,9 +156,9 @@ static Work carve(void* base, int64_t ch) {
   w.packed = (PackedPlan*)p; p += align256((size_t)ch * sizeof(PackedPlan));
   w.meta = (uint32_t*)p; p += align256((size_t)ch * 16);
   w.ids = (uint32_t*)p; p += align256((size_t)ch * 16);
-  w.hist = (uint32_t*)p; p += align256(kBuckets * 4);
+  w.hist = (uint32_t*)p; w.ovf = w.hist + kBuckets; p += align256(kCounters * 4 + (size_t)ch * 16);
   w.cursor = (uint32_t*)p; p += align256(kBuckets * 4);
-  w.total = (uint32_t*)p;
+  w.gstart = (uint32_t*)p;
   return w;
 }
 
@@ -175,15 +178,15 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
     const int64_t cn = n - off < ch ? n - off : ch;
     sim_plans p = *plans;
     p.hdr += off; p.cut += off; p.cls += off; p.types += off;
-    e = launch_fill32(w.hist, kBuckets, 0, s);
+    e = launch_fill32(w.hist, kCounters, 0, s);
     bool t1 = e == hipSuccess && begin_event(c, 1, s, &ev);
     if (e == hipSuccess) e = launch_prep(c->tab, p, cn, out + off, w.packed, w.meta, w.hist, s);
     if (t1) end_event(c, 1, s, &ev);
-    if (e == hipSuccess) e = launch_scan(w.hist, w.cursor, w.total, s);
+    if (e == hipSuccess) e = launch_scan(w.hist, w.cursor, w.gstart, s);
     if (e == hipSuccess) e = launch_scatter(w.meta, (uint32_t)(cn * 4), w.cursor, w.ids, s);
     bool t0 = e == hipSuccess && begin_event(c, 0, s, &ev);
     if (e == hipSuccess)
-      e = launch_eval(c->tab, w.packed, w.meta, w.ids, w.total, (uint32_t)(cn * 4), out + off, s);
+      e = launch_eval(c->tab, w.packed, w.meta, w.ids, w.gstart, (uint32_t)(cn * 4), out + off, w.ovf, s);
     if (t0) end_event(c, 0, s, &ev);
   }
   if (tcall) end_event(c, 2, s, &call);

@@ -31,6 +31,7 @@ struct Tab {
   uint32_t mbs[4];
   uint32_t tp_ok;                 // bit j: TP 2^j divides heads, kv heads and MLP widths
   uint32_t ep_ok;                 // bit j: EP 2^j allowed (dense models: EP 1 only)
+  uint32_t type_ok[4];            // [log2 TP] bit k: type k exists and TP 2^j divides its node size
   uint32_t D, N;                  // total devices, total nodes
   uint32_t lvl_dev, lvl_node;     // levels of the range-max tables
   uint32_t dpn_log2[kMaxTypes];

@@ -114,6 +114,8 @@ __device__ __forceinline__ Plan unpack(const PackedPlan& q) {
   return p;
 }
 
+constexpr int kPrepPerThread = 4;
+
 // Decode and check plan i (every rule of the plan layout); on success pack it.
 // Writes out[i] (0 = valid, to be raised by the pipelines; else invalid) and
 // the per-pipeline metadata S | G << 5 | M << 8 (0 = no pipeline).
@@ -125,40 +127,52 @@ __global__ void __launch_bounds__(256) k_prep(Tab t, sim_plans pl, int64_t n, ui
     for (uint32_t j = threadIdx.x; j < kBuckets; j += blockDim.x) lh[j] = 0;
     __syncthreads();
   }
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) {
+  for (int rep = 0; rep < kPrepPerThread; ++rep) {
+    const int64_t i = ((int64_t)blockIdx.x * kPrepPerThread + rep) * blockDim.x + threadIdx.x;
+    if (i >= n) break;
     const int64_t st = pl.stride;
+    // all 16 cut planes and 4 class planes exist: load them before any use
     const uint32_t hdr = pl.hdr[i];
+    uint32_t cb[16];
+#pragma unroll
+    for (int s = 0; s < 16; ++s) cb[s] = pl.cut[s * st + i];
+    uint32_t cls[4];
+    uint64_t tv[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      cls[c] = pl.cls[c * st + i];
+      tv[c] = pl.types[c * st + i];
+    }
     const uint32_t tpl = hdr & 3, epl = (hdr >> 2) & 3, S = ((hdr >> 4) & 15) + 1, G = ((hdr >> 8) & 3) + 1;
     const uint32_t mi = (hdr >> 11) & 3;
     const uint32_t tp = 1u << tpl, ep = 1u << epl;
     bool ok = (hdr >> 13) == 0 && mi < t.n_mbs && ((t.tp_ok >> tpl) & 1) && ((t.ep_ok >> epl) & 1);
     uint32_t cw[4] = {0, 0, 0, 0}, prev = 0;
-    for (uint32_t s = 0; s < S; ++s) {
-      const uint32_t c = pl.cut[s * st + i];
-      ok = ok && c > prev;
-      prev = c;
-      cw[s >> 2] |= c << (8 * (s & 3));
+#pragma unroll
+    for (uint32_t s = 0; s < 16; ++s) {
+      if (s < S) {
+        ok = ok && cb[s] > prev;
+        prev = cb[s];
+        cw[s >> 2] |= cb[s] << (8 * (s & 3));
+      }
     }
     ok = ok && prev == t.L;
     const uint64_t sel = S == 16 ? ~0ull : ((1ull << (4 * S)) - 1);
-    uint32_t cls[4];
-    uint64_t tv[4];
     uint32_t batch = 0, psum = 0;
 #pragma unroll
     for (uint32_t c = 0; c < 4; ++c) {
-      cls[c] = 0; tv[c] = 0;
       if (c < G) {
-        cls[c] = pl.cls[c * st + i];
-        tv[c] = pl.types[c * st + i] & sel;
+        tv[c] &= sel;
         const uint32_t reps = cls[c] & 0xffff, nmb = cls[c] >> 16;
         ok = ok && reps >= 1 && nmb >= reps && (reps & (ep - 1)) == 0;
         batch += nmb * t.mbs[mi];
         psum += reps;
-        for (uint32_t s = 0; s < S; ++s) {
-          const uint32_t k = (uint32_t)(tv[c] >> (4 * s)) & 15;
-          ok = ok && k < t.K && t.dpn_log2[k] >= tpl;
-        }
+        // every stage's type exists and holds whole TP groups in a node
+        const uint32_t okm = t.type_ok[tpl];
+        for (uint32_t s = 0; s < S; ++s) ok = ok && ((okm >> ((uint32_t)(tv[c] >> (4 * s)) & 15)) & 1);
+      } else {
+        cls[c] = 0;
+        tv[c] = 0;
       }
     }
     ok = ok && batch == t.gbs;
@@ -333,9 +347,10 @@ __global__ void k_fill32(uint32_t* p, uint32_t n, uint32_t v) {
   for (uint32_t j = blockIdx.x * blockDim.x + threadIdx.x; j < n; j += gridDim.x * blockDim.x) p[j] = v;
 }
 
-// exclusive scan of the bucket counts; total pipelines into *total
+// exclusive scan of the bucket counts; gstart[g] = first id of stage-count
+// group g (g = 0..3), gstart[4] = number of pipelines
 __global__ void __launch_bounds__(1024) k_scan(const uint32_t* __restrict__ hist, uint32_t* __restrict__ cursor,
-                                               uint32_t* __restrict__ total) {
+                                               uint32_t* __restrict__ gstart) {
   constexpr int kPer = kBuckets / 1024;
   static_assert(kBuckets % 1024 == 0, "bucket count");
   __shared__ uint32_t part[1024];
@@ -352,15 +367,18 @@ __global__ void __launch_bounds__(1024) k_scan(const uint32_t* __restrict__ hist
     __syncthreads();
   }
   uint32_t run = part[tid] - sum;
+  // group g of stage counts starts at bucket g * kBuckets / 4
+  if ((tid * kPer) % (kBuckets / 4) == 0) gstart[(tid * kPer) / (kBuckets / 4)] = run;
 #pragma unroll
   for (int j = 0; j < kPer; ++j) { cursor[tid * kPer + j] = run; run += v[j]; }
-  if (tid == 1023) *total = part[1023];
+  if (tid == 1023) gstart[4] = part[1023];
 }
 
 // place every pipeline id at its bucket's next free position
+constexpr int kScatterPer = 16;
 __global__ void __launch_bounds__(256) k_scatter(const uint32_t* __restrict__ meta, uint32_t nslots,
                                                  uint32_t* __restrict__ cursor, uint32_t* __restrict__ ids) {
-  constexpr int kPer = 4;
+  constexpr int kPer = kScatterPer;
   __shared__ uint32_t lc[kBuckets];
   for (uint32_t j = threadIdx.x; j < kBuckets; j += blockDim.x) lc[j] = 0;
   __syncthreads();
@@ -400,18 +418,24 @@ __global__ void __launch_bounds__(256) k_scatter(const uint32_t* __restrict__ me
 // forward form the steady loop; the last min(S-1, M) iterations, where the
 // upper stages have run out of forwards, are unrolled.
 //   out_f[s] end of the latest forward on stage s, last[s] end of its latest op.
+// Each schedule node is end = max(previous end on the stage, input end + hop)
+// + duration: 3 VALU ops in fp64, 5 in u64 (64-bit add is one v_lshl_add_u64,
+// max is a compare and two selects).
 typedef uint64_t StageRec[kMaxStages][kRecWords];
 
-template <int S>
-__device__ __forceinline__ uint64_t pipe_fp64(const StageRec& R, uint32_t M) {
-  double f[S], b[S], c[S], out_f[S], last[S];
+__device__ __forceinline__ double vmax(double a, double b) { return __builtin_fmax(a, b); }
+__device__ __forceinline__ uint64_t vmax(uint64_t a, uint64_t b) { return a > b ? a : b; }
+
+template <int S, typename V>
+__device__ __forceinline__ V pipe(const StageRec& R, uint32_t M) {
+  V f[S], b[S], c[S], out_f[S], last[S];
 #pragma unroll
   for (int s = 0; s < S; ++s) {
-    f[s] = (double)R[s][0];
-    b[s] = (double)R[s][1];
-    c[s] = (double)R[s][2];
-    out_f[s] = 0.0;
-    last[s] = 0.0;
+    f[s] = (V)R[s][0];
+    b[s] = (V)R[s][1];
+    c[s] = (V)R[s][2];
+    out_f[s] = 0;
+    last[s] = 0;
   }
   const int m_ = (int)M;
 #pragma unroll
@@ -419,7 +443,7 @@ __device__ __forceinline__ uint64_t pipe_fp64(const StageRec& R, uint32_t M) {
     if (m < m_) {
 #pragma unroll
       for (int s = 0; s < S - 1 - m; ++s) {
-        const double st = s == 0 ? last[0] : __builtin_fmax(last[s], out_f[s - 1] + c[s - 1]);
+        const V st = s == 0 ? last[0] : vmax(last[s], out_f[s - 1] + c[s - 1]);
         out_f[s] = st + f[s];
         last[s] = out_f[s];
       }
@@ -429,9 +453,9 @@ __device__ __forceinline__ uint64_t pipe_fp64(const StageRec& R, uint32_t M) {
   for (int i = 0; i < steady; ++i) {
 #pragma unroll
     for (int s = S - 1; s >= 0; --s) {
-      const double st = s == 0 ? last[0] : __builtin_fmax(last[s], out_f[s - 1] + c[s - 1]);
+      const V st = s == 0 ? last[0] : vmax(last[s], out_f[s - 1] + c[s - 1]);
       out_f[s] = st + f[s];
-      const double sb = s == S - 1 ? out_f[s] : __builtin_fmax(out_f[s], last[s + 1] + c[s]);
+      const V sb = s == S - 1 ? out_f[s] : vmax(out_f[s], last[s + 1] + c[s]);
       last[s] = sb + b[s];
     }
   }
@@ -441,70 +465,58 @@ __device__ __forceinline__ uint64_t pipe_fp64(const StageRec& R, uint32_t M) {
 #pragma unroll
       for (int s = S - 1; s >= 0; --s) {
         if (s > tr) {
-          const double st = __builtin_fmax(last[s], out_f[s - 1] + c[s - 1]);
+          const V st = vmax(last[s], out_f[s - 1] + c[s - 1]);
           out_f[s] = st + f[s];
-          const double sb = s == S - 1 ? out_f[s] : __builtin_fmax(out_f[s], last[s + 1] + c[s]);
+          const V sb = s == S - 1 ? out_f[s] : vmax(out_f[s], last[s + 1] + c[s]);
           last[s] = sb + b[s];
         } else {
-          last[s] = (s == S - 1 ? last[s] : __builtin_fmax(last[s], last[s + 1] + c[s])) + b[s];
+          last[s] = (s == S - 1 ? last[s] : vmax(last[s], last[s + 1] + c[s])) + b[s];
         }
       }
     }
   }
-  double T = 0.0;
+  V T = 0;
 #pragma unroll
-  for (int s = 0; s < S; ++s) T = __builtin_fmax(T, last[s] + (double)R[s][3]);
-  // integers below 2^53 are exact in fp64; if no value ever reached 2^53 every
-  // add was exact, and the result bounds every intermediate value
-  return T < 9007199254740992.0 ? (uint64_t)T : kInvalid;
-}
-
-// same schedule in u64, for pipelines whose time reaches 2^53 ps
-__device__ __noinline__ uint64_t pipe_u64(const StageRec& R, int S, uint32_t M) {
-  uint64_t out_f[kMaxStages], last[kMaxStages];
-  for (int s = 0; s < S; ++s) { out_f[s] = 0; last[s] = 0; }
-  const int m_ = (int)M;
-  auto fwd = [&](int s) {
-    uint64_t st = last[s];
-    if (s > 0) { uint64_t r = out_f[s - 1] + R[s - 1][2]; st = st > r ? st : r; }
-    out_f[s] = st + R[s][0];
-    last[s] = out_f[s];
-  };
-  auto bwd = [&](int s) {
-    uint64_t st = last[s];
-    if (s < S - 1) { uint64_t r = last[s + 1] + R[s][2]; st = st > r ? st : r; }
-    last[s] = st + R[s][1];
-  };
-  for (int m = 0; m < S - 1 && m < m_; ++m)
-    for (int s = 0; s < S - 1 - m; ++s) fwd(s);
-  for (int i = 0; i < m_ - (S - 1); ++i)
-    for (int s = S - 1; s >= 0; --s) { fwd(s); bwd(s); }
-  for (int tr = (S - 1 - m_ > 0 ? S - 1 - m_ : 0); tr < S - 1; ++tr)
-    for (int s = S - 1; s >= 0; --s) {
-      if (s > tr) fwd(s);
-      bwd(s);
-    }
-  uint64_t T = 0;
-  for (int s = 0; s < S; ++s) {
-    uint64_t v = last[s] + R[s][3];
-    T = T > v ? T : v;
-  }
+  for (int s = 0; s < S; ++s) T = vmax(T, last[s] + (V)R[s][3]);
   return T;
 }
 
+// Integers below 2^53 are exact in fp64.  Every value the fp64 pass computes
+// is at most the end of some op, which is at most T, so if T < 2^53 no
+// rounding ever happened.  Otherwise the pipeline goes on an overflow list
+// and k_redo_u64 evaluates it again in u64, outside the hot kernels.
+constexpr double kExact = 9007199254740992.0;
+
+// Pipelines are sorted by stage count (descending), so each group of four
+// stage counts is a contiguous range of ids; one kernel per group keeps the
+// register footprint, and so the occupancy, of small pipelines independent of
+// the 16-stage code.  Block b of group g runs the g-th range's pipelines
+// [64b, 64b + 64); blocks past the range return at once.
 template <int S>
-__device__ __forceinline__ uint64_t run_pipe(const StageRec& R, uint32_t M) {
-  uint64_t r = pipe_fp64<S>(R, M);
-  return r != kInvalid ? r : pipe_u64(R, S, M);
+__device__ __forceinline__ void eval_one(const Tab& t, const PackedPlan* __restrict__ packed, uint32_t slot,
+                                         uint32_t M, uint64_t* __restrict__ out, uint32_t* __restrict__ ovf) {
+  const Plan p = unpack(packed[slot >> 2]);
+  StageRec R;
+  class_setup(t, p, slot & 3, R);
+  const double T = pipe<S, double>(R, M);
+  if (T < kExact) {
+    atomicMax((unsigned long long*)&out[slot >> 2], (unsigned long long)T);
+  } else {
+    ovf[1 + atomicAdd(&ovf[0], 1u)] = slot;
+  }
 }
 
+template <int GRP>
 __global__ void __launch_bounds__(64) k_eval(Tab t, const PackedPlan* __restrict__ packed,
                                              const uint32_t* __restrict__ meta, const uint32_t* __restrict__ ids,
-                                             const uint32_t* __restrict__ total, uint64_t* __restrict__ out) {
-  const uint32_t tot = *total;
-  if (blockIdx.x * 64u >= tot) return;
-  const uint32_t pos = blockIdx.x * 64u + threadIdx.x;
-  bool pending = pos < tot;
+                                             const uint32_t* __restrict__ gstart, uint64_t* __restrict__ out,
+                                             uint32_t* __restrict__ ovf) {
+  constexpr int kTop = kMaxStages - 4 * GRP;   // stage counts kTop-3 .. kTop
+  const uint32_t lo = gstart[GRP], hi = gstart[GRP + 1];
+  const uint32_t base = lo + blockIdx.x * 64u;
+  if (base >= hi) return;
+  const uint32_t pos = base + threadIdx.x;
+  bool pending = pos < hi;
   const uint32_t slot = pending ? ids[pos] : 0;
   const uint32_t m = pending ? meta[slot] : 0;
   const uint32_t S = m & 31, M = m >> 8;
@@ -514,31 +526,51 @@ __global__ void __launch_bounds__(64) k_eval(Tab t, const PackedPlan* __restrict
     if (!live) break;
     const uint32_t S0 = __builtin_amdgcn_readfirstlane(__shfl(S, __ffsll((unsigned long long)live) - 1));
     if (pending && S == S0) {
-      const Plan p = unpack(packed[slot >> 2]);
-      StageRec R;
-      class_setup(t, p, slot & 3, R);
-      uint64_t r;
-      switch (S0) {
-        case 1: r = run_pipe<1>(R, M); break;
-        case 2: r = run_pipe<2>(R, M); break;
-        case 3: r = run_pipe<3>(R, M); break;
-        case 4: r = run_pipe<4>(R, M); break;
-        case 5: r = run_pipe<5>(R, M); break;
-        case 6: r = run_pipe<6>(R, M); break;
-        case 7: r = run_pipe<7>(R, M); break;
-        case 8: r = run_pipe<8>(R, M); break;
-        case 9: r = run_pipe<9>(R, M); break;
-        case 10: r = run_pipe<10>(R, M); break;
-        case 11: r = run_pipe<11>(R, M); break;
-        case 12: r = run_pipe<12>(R, M); break;
-        case 13: r = run_pipe<13>(R, M); break;
-        case 14: r = run_pipe<14>(R, M); break;
-        case 15: r = run_pipe<15>(R, M); break;
-        default: r = run_pipe<16>(R, M); break;
-      }
-      atomicMax((unsigned long long*)&out[slot >> 2], (unsigned long long)r);
+      if (S0 == kTop) eval_one<kTop>(t, packed, slot, M, out, ovf);
+      else if (S0 == kTop - 1) eval_one<kTop - 1>(t, packed, slot, M, out, ovf);
+      else if (S0 == kTop - 2) eval_one<kTop - 2>(t, packed, slot, M, out, ovf);
+      else eval_one<kTop - 3>(t, packed, slot, M, out, ovf);
       pending = false;
     }
+  }
+}
+
+// Pipelines whose fp64 time reached 2^53 ps, again in u64 (exact below 2^64).
+template <int S>
+__device__ __forceinline__ uint64_t redo_one(const StageRec& R, uint32_t M) {
+  return pipe<S, uint64_t>(R, M);
+}
+
+__global__ void __launch_bounds__(64) k_redo_u64(Tab t, const PackedPlan* __restrict__ packed,
+                                                 const uint32_t* __restrict__ meta, const uint32_t* __restrict__ ovf,
+                                                 uint64_t* __restrict__ out) {
+  const uint32_t n = ovf[0];
+  for (uint32_t j = blockIdx.x * 64u + threadIdx.x; j < n; j += gridDim.x * 64u) {
+    const uint32_t slot = ovf[1 + j];
+    const uint32_t m = meta[slot], S = m & 31, M = m >> 8;
+    const Plan p = unpack(packed[slot >> 2]);
+    StageRec R;
+    class_setup(t, p, slot & 3, R);
+    uint64_t r;
+    switch (S) {
+      case 1: r = redo_one<1>(R, M); break;
+      case 2: r = redo_one<2>(R, M); break;
+      case 3: r = redo_one<3>(R, M); break;
+      case 4: r = redo_one<4>(R, M); break;
+      case 5: r = redo_one<5>(R, M); break;
+      case 6: r = redo_one<6>(R, M); break;
+      case 7: r = redo_one<7>(R, M); break;
+      case 8: r = redo_one<8>(R, M); break;
+      case 9: r = redo_one<9>(R, M); break;
+      case 10: r = redo_one<10>(R, M); break;
+      case 11: r = redo_one<11>(R, M); break;
+      case 12: r = redo_one<12>(R, M); break;
+      case 13: r = redo_one<13>(R, M); break;
+      case 14: r = redo_one<14>(R, M); break;
+      case 15: r = redo_one<15>(R, M); break;
+      default: r = redo_one<16>(R, M); break;
+    }
+    atomicMax((unsigned long long*)&out[slot >> 2], (unsigned long long)r);
   }
 }
 
@@ -625,7 +657,7 @@ hipError_t launch_fill32(uint32_t* p, uint32_t n, uint32_t v, hipStream_t s) {
 }
 hipError_t launch_prep(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, PackedPlan* packed,
                        uint32_t* meta, uint32_t* hist, hipStream_t s) {
-  k_prep<<<blocks_for(n, 256), 256, 0, s>>>(t, p, n, out, packed, meta, hist);
+  k_prep<<<blocks_for(n, 256 * kPrepPerThread), 256, 0, s>>>(t, p, n, out, packed, meta, hist);
   return hipGetLastError();
 }
 hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint32_t* meta, int64_t n, uint64_t* out_stage,
@@ -633,17 +665,22 @@ hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint32_t*
   k_stages<<<blocks_for(n * 4, 256), 256, 0, s>>>(t, packed, meta, n, out_stage);
   return hipGetLastError();
 }
-hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* total, hipStream_t s) {
-  k_scan<<<1, 1024, 0, s>>>(hist, cursor, total);
+hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* gstart, hipStream_t s) {
+  k_scan<<<1, 1024, 0, s>>>(hist, cursor, gstart);
   return hipGetLastError();
 }
 hipError_t launch_scatter(const uint32_t* meta, uint32_t nslots, uint32_t* cursor, uint32_t* ids, hipStream_t s) {
-  k_scatter<<<blocks_for(nslots, 256 * 4), 256, 0, s>>>(meta, nslots, cursor, ids);
+  k_scatter<<<blocks_for(nslots, 256 * kScatterPer), 256, 0, s>>>(meta, nslots, cursor, ids);
   return hipGetLastError();
 }
 hipError_t launch_eval(const Tab& t, const PackedPlan* packed, const uint32_t* meta, const uint32_t* ids,
-                       const uint32_t* total, uint32_t max_tasks, uint64_t* out, hipStream_t s) {
-  k_eval<<<blocks_for(max_tasks, 64), 64, 0, s>>>(t, packed, meta, ids, total, out);
+                       const uint32_t* gstart, uint32_t max_tasks, uint64_t* out, uint32_t* ovf, hipStream_t s) {
+  const int g = blocks_for(max_tasks, 64) > 0 ? blocks_for(max_tasks, 64) : 1;
+  k_eval<0><<<g, 64, 0, s>>>(t, packed, meta, ids, gstart, out, ovf);
+  k_eval<1><<<g, 64, 0, s>>>(t, packed, meta, ids, gstart, out, ovf);
+  k_eval<2><<<g, 64, 0, s>>>(t, packed, meta, ids, gstart, out, ovf);
+  k_eval<3><<<g, 64, 0, s>>>(t, packed, meta, ids, gstart, out, ovf);
+  k_redo_u64<<<32, 64, 0, s>>>(t, packed, meta, ovf, out);
   return hipGetLastError();
 }
 hipError_t launch_argmin(const uint64_t* t, int64_t n, int64_t base, sim_best* b, hipStream_t s) {

@@ -224,6 +224,9 @@ int build_tables(const sim_model_desc* md, const sim_cluster_desc* cd, HostTable
     d0 += t.cap[k];
     n0 += cd->n_nodes[k];
   }
+  for (uint32_t j = 0; j < 4; ++j)
+    for (uint32_t k = 0; k < K; ++k)
+      if (t.dpn_log2[k] >= j) t.type_ok[j] |= 1u << k;
   build_rmax(nic, &out->rm_nic, &t.lvl_dev);
   build_rmax(intra, &out->rm_intra, &t.lvl_node);
 
