@@ -221,3 +221,31 @@ def test_full_size_sampled(torch, B, oracle_mod, workloads, idx):
     _assert_equal(got[sample], want, "full workload %d" % idx)
     valid = got != MAXU
     assert best[0] == int(got[valid].min()) and best[1] == int(np.argmax(got == got[valid].min()))
+
+
+def test_chunked_streams_argmin(torch, B, oracle_mod, workloads):
+    """A sweep in chunks on 1, 2 and 4 streams, one argmin slot per chunk reduced on the device,
+    gives the single-call result; the best plan's time matches the oracle."""
+    w = workloads.workload(5)
+    n, chunk = 3_000_000, 700_001
+    say("case: chunked sweep of workload 5, %d plans" % n)
+    p = workloads.plans(w, 0, n)
+    sim = B.Sim(w["model"], w["cluster"])
+    dp = B.device_plans(p)
+    full = sim.eval_plans(dp)
+    ref = B.best_tuple(sim.argmin(full))
+    chunks = [(o, min(chunk, n - o)) for o in range(0, n, chunk)]
+    for ns in (1, 2, 4):
+        out = torch.empty(n, dtype=torch.int64, device="cuda")
+        slots = torch.empty(2 * len(chunks), dtype=torch.int64, device="cuda")
+        streams = [torch.cuda.Stream() for _ in range(ns)]
+        torch.cuda.synchronize()
+        for j, (o, m) in enumerate(chunks):
+            st = streams[j % ns]
+            sim.eval_plans(dp, n=m, offset=o, out=out[o:o + m], stream=st)
+            sim.argmin(out[o:o + m], index_base=o, out=slots[2 * j:2 * j + 2], stream=st)
+        torch.cuda.synchronize()
+        assert B.best_tuple(sim.best_reduce(slots)) == ref, ns
+        assert torch.equal(out, full)
+    want = oracle_mod.Oracle(w["model"], w["cluster"]).eval(_sub(p, np.array([ref[1]])))
+    assert int(want[0]) == ref[0]
