@@ -77,10 +77,11 @@ extern "C" int sim_create(const sim_model_desc* model, const sim_cluster_desc* c
     size_t bytes;
     size_t off;
   };
-  Part parts[7] = {{ht->pf.data(), ht->pf.size() * 8, 0},         {ht->pb.data(), ht->pb.size() * 8, 0},
+  Part parts[8] = {{ht->pf.data(), ht->pf.size() * 8, 0},         {ht->pb.data(), ht->pb.size() * 8, 0},
                    {ht->emb.data(), ht->emb.size() * 8, 0},       {ht->head.data(), ht->head.size() * 8, 0},
                    {ht->pa.data(), ht->pa.size() * 8, 0},         {ht->rm_nic.data(), ht->rm_nic.size() * 4, 0},
-                   {ht->rm_intra.data(), ht->rm_intra.size() * 4, 0}};
+                   {ht->rm_intra.data(), ht->rm_intra.size() * 4, 0},
+                   {ht->ty.data(), ht->ty.size() * sizeof(TypeInfo), 0}};
   size_t total = 0;
   for (auto& p : parts) { p.off = total; total += align256(p.bytes); }
   if (hipMalloc(&c->tables, total) != hipSuccess) { delete ht; delete c; return SIM_ENOMEM; }
@@ -96,6 +97,7 @@ extern "C" int sim_create(const sim_model_desc* model, const sim_cluster_desc* c
   c->tab.pa = (const uint64_t*)(b + parts[4].off);
   c->tab.rm_nic = (const uint32_t*)(b + parts[5].off);
   c->tab.rm_intra = (const uint32_t*)(b + parts[6].off);
+  c->tab.ty = (const TypeInfo*)(b + parts[7].off);
   delete ht;
   hipMemPoolProps props;
   memset(&props, 0, sizeof(props));

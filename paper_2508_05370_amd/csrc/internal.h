@@ -24,6 +24,15 @@ struct __attribute__((aligned(16))) PackedPlan {
   uint64_t types[4];
 };
 
+// Per-device-type fields a kernel reads together (32 bytes, two loads).
+struct TypeInfo {
+  uint32_t node_off, dev_off;     // first global node / device of the pool
+  uint32_t dpl;                   // log2 devices per node
+  uint32_t bq_pcie;               // PCIe ps/byte in 2^-16 units, 0 = absent
+  uint64_t a_intra;               // intra-node message latency
+  uint64_t a_side;                // one end of an inter-node path: two PCIe trips + NIC
+};
+
 // Everything a kernel needs about one (model, cluster) pair.  Scalars travel
 // by value in the kernel argument block; tables live in device memory.
 struct Tab {
@@ -53,6 +62,7 @@ struct Tab {
   const uint64_t* pa;             // all-to-all bytes prefix [4][n_mbs][L+1]
   const uint32_t* rm_nic;         // range-max table of NIC rates per device [lvl_dev][D]
   const uint32_t* rm_intra;       // range-max table of fabric rates per node [lvl_node][N]
+  const TypeInfo* ty;             // [K]
 };
 
 // Host side: validate descriptors and build the tables (host copies).
@@ -60,6 +70,7 @@ struct HostTables {
   Tab tab;
   std::vector<uint64_t> pf, pb, emb, head, pa;
   std::vector<uint32_t> rm_nic, rm_intra;
+  std::vector<TypeInfo> ty;
 };
 
 // Returns 0 (SIM_OK), SIM_EINVAL or SIM_ERANGE.

@@ -236,14 +236,16 @@ __device__ void class_setup(const Tab& t, const Plan& p, uint32_t c, uint64_t (&
   const uint32_t reps = c == 0 ? p.reps[0] : c == 1 ? p.reps[1] : c == 2 ? p.reps[2] : p.reps[3];
   const uint64_t tvc = c == 0 ? p.tv[0] : c == 1 ? p.tv[1] : c == 2 ? p.tv[2] : p.tv[3];
   uint32_t pk = 0, pbase = 0, pnic = 0, pin = 0, lo = 0;
+  TypeInfo pti = {};
   for (uint32_t s = 0; s < S; ++s) {
     const uint32_t hi = cut_at(p, s), ns = hi - lo;
     // ---- this class: compute, TP, EP, hop from the previous stage
     const uint32_t k = (uint32_t)(tvc >> (4 * s)) & 15;
-    const uint32_t base = placed_before(p, c, s, k) * tp, nd = reps * tp, dpl = t.dpn_log2[k];
-    const uint32_t gnl = t.node_off[k] + (base >> dpl), gnh = t.node_off[k] + ((base + nd - 1) >> dpl);
+    const TypeInfo ti = t.ty[k];
+    const uint32_t base = placed_before(p, c, s, k) * tp, nd = reps * tp, dpl = ti.dpl;
+    const uint32_t gnl = ti.node_off + (base >> dpl), gnh = ti.node_off + ((base + nd - 1) >> dpl);
     const uint32_t bq_in = range_max(t.rm_intra, t.N, gnl, gnh);
-    const uint32_t dlo = t.dev_off[k] + base;
+    const uint32_t dlo = ti.dev_off + base;
     const uint32_t bq_nic = range_max(t.rm_nic, t.D, dlo, dlo + nd - 1);
     const size_t tb = ((((size_t)k * 4 + tpl) * t.n_mbs + mi) * 4 + epl) * L1;
     uint64_t fc = t.pf[tb + hi] - t.pf[tb + lo];
@@ -259,13 +261,13 @@ __device__ void class_setup(const Tab& t, const Plan& p, uint32_t c, uint64_t (&
     }
     if (tp > 1) {  // TP all-reduces of this stage, exposed in the forward pass
       const uint64_t steps = (uint64_t)(2 * ns + (s == 0)) * 2 * (tp - 1);
-      fc += steps * t.a_intra[k] + link_ps(steps * act_tp, bq_in);
+      fc += steps * ti.a_intra + link_ps(steps * act_tp, bq_in);
     }
     if (t.E && ep > 1) {  // dispatch + combine all-to-all in each pass
       // EP groups are aligned blocks of ep*tp devices: inside a node iff they fit one
       const bool intra = ep * tp <= (1u << dpl);
-      const uint64_t alpha = intra ? t.a_intra[k] : 2 * t.a_side[k];
-      const uint32_t bq = intra ? bq_in : (bq_nic > t.bq_pcie[k] ? bq_nic : t.bq_pcie[k]);
+      const uint64_t alpha = intra ? ti.a_intra : 2 * ti.a_side;
+      const uint32_t bq = intra ? bq_in : (bq_nic > ti.bq_pcie ? bq_nic : ti.bq_pcie);
       const size_t pa = ((size_t)epl * t.n_mbs + mi) * L1;
       const uint64_t e = (uint64_t)ns * 2 * (ep - 1) * alpha + link_ps(2 * (t.pa[pa + hi] - t.pa[pa + lo]), bq);
       fc += e;
@@ -276,18 +278,18 @@ __device__ void class_setup(const Tab& t, const Plan& p, uint32_t c, uint64_t (&
     if (s > 0) {  // hop (s-1) -> s
       // same pool means the two ranges are adjacent: intra iff the pair spans one node
       const bool intra = pk == k && (pbase >> dpl) == ((pbase + (2 * reps - 1) * tp) >> dpl);
-      const uint64_t alpha = intra ? t.a_intra[k] : t.a_side[pk] + t.a_side[k];
+      const uint64_t alpha = intra ? ti.a_intra : pti.a_side + ti.a_side;
       uint32_t bq;
       if (intra) {
         bq = pin > bq_in ? pin : bq_in;
       } else {
         const uint32_t a = pnic > bq_nic ? pnic : bq_nic;
-        const uint32_t b = t.bq_pcie[pk] > t.bq_pcie[k] ? t.bq_pcie[pk] : t.bq_pcie[k];
+        const uint32_t b = pti.bq_pcie > ti.bq_pcie ? pti.bq_pcie : ti.bq_pcie;
         bq = a > b ? a : b;
       }
       rec[s - 1][2] = alpha + link_ps(act, bq);
     }
-    pk = k; pbase = base; pnic = bq_nic; pin = bq_in;
+    pk = k; pbase = base; pnic = bq_nic; pin = bq_in; pti = ti;
     // ---- DP sync of this stage over every replica of every class
     uint64_t tdp = 0;
     if (p.psum > 1) {
@@ -298,19 +300,20 @@ __device__ void class_setup(const Tab& t, const Plan& p, uint32_t c, uint64_t (&
       for (uint32_t c2 = 0; c2 < 4; ++c2) {
         if (c2 >= G) continue;
         const uint32_t k2 = (uint32_t)(p.tv[c2] >> (4 * s)) & 15;
-        const uint32_t b2 = placed_before(p, c2, s, k2) * tp, n2 = p.reps[c2] * tp, d2 = t.dpn_log2[k2];
-        const uint32_t l2 = t.node_off[k2] + (b2 >> d2), h2 = t.node_off[k2] + ((b2 + n2 - 1) >> d2);
-        const uint32_t dl2 = t.dev_off[k2] + b2;
+        const TypeInfo t2 = t.ty[k2];
+        const uint32_t b2 = placed_before(p, c2, s, k2) * tp, n2 = p.reps[c2] * tp, d2 = t2.dpl;
+        const uint32_t l2 = t2.node_off + (b2 >> d2), h2 = t2.node_off + ((b2 + n2 - 1) >> d2);
+        const uint32_t dl2 = t2.dev_off + b2;
         const uint32_t nic2 = range_max(t.rm_nic, t.D, dl2, dl2 + n2 - 1);
         if (c2 == 0) k0 = k2; else same = same && k2 == k0;
         nmin = l2 < nmin ? l2 : nmin;
         nmax = h2 > nmax ? h2 : nmax;
-        const uint32_t bx = nic2 > t.bq_pcie[k2] ? nic2 : t.bq_pcie[k2];
+        const uint32_t bx = nic2 > t2.bq_pcie ? nic2 : t2.bq_pcie;
         bq_dp = bx > bq_dp ? bx : bq_dp;
-        a_dp = 2 * t.a_side[k2] > a_dp ? 2 * t.a_side[k2] : a_dp;
+        a_dp = 2 * t2.a_side > a_dp ? 2 * t2.a_side : a_dp;
       }
       const bool intra = same && nmin == nmax;
-      const uint64_t alpha = intra ? t.a_intra[k0] : a_dp;
+      const uint64_t alpha = intra ? t.ty[k0].a_intra : a_dp;
       const uint32_t bq = intra ? t.rm_intra[nmin] : bq_dp;
       const uint64_t pd = (uint64_t)ns * t.par_layer[tpl] + (s == 0 ? t.par_embed[tpl] : 0) +
                           (s == S - 1 ? t.par_head[tpl] : 0);
@@ -450,6 +453,9 @@ __device__ __forceinline__ V pipe(const StageRec& R, uint32_t M) {
     }
   }
   const int steady = m_ - (S - 1);
+  // two iterations per trip: the next iteration's upper stages overlap this
+  // one's backward chain
+#pragma unroll 2
   for (int i = 0; i < steady; ++i) {
 #pragma unroll
     for (int s = S - 1; s >= 0; --s) {

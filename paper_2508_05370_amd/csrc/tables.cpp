@@ -227,6 +227,9 @@ int build_tables(const sim_model_desc* md, const sim_cluster_desc* cd, HostTable
   for (uint32_t j = 0; j < 4; ++j)
     for (uint32_t k = 0; k < K; ++k)
       if (t.dpn_log2[k] >= j) t.type_ok[j] |= 1u << k;
+  out->ty.assign(K, TypeInfo{});
+  for (uint32_t k = 0; k < K; ++k)
+    out->ty[k] = TypeInfo{t.node_off[k], t.dev_off[k], t.dpn_log2[k], t.bq_pcie[k], t.a_intra[k], t.a_side[k]};
   build_rmax(nic, &out->rm_nic, &t.lvl_dev);
   build_rmax(intra, &out->rm_intra, &t.lvl_node);
 
