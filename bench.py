@@ -45,6 +45,27 @@ def pipeline_ops(p, valid):
     return ops
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "eval_llama70b_16M_hbm_traffic.txt")
+
+
+def measured_traffic(workload, chunk):
+    """HBM bytes per evaluation launch from the committed FETCH_SIZE/WRITE_SIZE
+    summary; None unless it was taken on this workload, in 2M-plan chunks, with
+    the kernel source as it is now (sha256 recorded in the summary)."""
+    import hashlib
+    if workload != 3 or chunk not in (0, 1 << 21) or not os.path.exists(TRAFFIC_FILE):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_FILE):
+        if "=" in line and not line.startswith("#"):
+            k, v = line.split("=", 1)
+            kv[k.strip()] = v.strip()
+    src = os.path.join(ROOT, "paper_2508_05370_amd", "csrc", "kernels.hip")
+    if kv.get("kernels_sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest():
+        return None
+    return int(kv["traffic_bytes_per_launch"])
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -147,7 +168,8 @@ def main():
         ops_per_launch = float(ops.sum()) / launches_per_step
         achieved = ops_per_launch / (avg_ms * 1e-3) / 1e12
         roof = {"bound": "alu", "achieved": round(achieved, 3), "peak": round(PEAK_VALU / 1e12, 3),
-                "unit": "TOP/s", "frac": round(achieved * 1e12 / PEAK_VALU, 4), "traffic": None,
+                "unit": "TOP/s", "frac": round(achieved * 1e12 / PEAK_VALU, 4),
+                "traffic": None if a.plans else measured_traffic(a.workload, a.chunk),
                 "kernel": "k_eval (4 stage-count groups + u64 redo, per 2M-plan chunk)",
                 "avg_launch_ms": round(avg_ms, 4), "launches": pipe_n, "ops_per_launch": ops_per_launch}
         extra = {"prep_ms_per_step": round(setup_ms / a.steps, 4),

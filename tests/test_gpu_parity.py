@@ -199,7 +199,7 @@ def test_argmin_semantics(torch, B, workloads):
     assert B.best_tuple(sim.best_reduce(allinv)) == (2**64 - 1, -1)
 
 
-@pytest.mark.parametrize("idx", [2, 3, 4])
+@pytest.mark.parametrize("idx", [2, 3, 4, 5])
 def test_full_size_sampled(torch, B, oracle_mod, workloads, idx):
     """Whole workload in one call (the benchmark's launch), checked on samples."""
     w = workloads.workload(idx)
