@@ -190,6 +190,21 @@ int sim_best_reduce(sim_ctx* ctx, const sim_best* bests, int64_t n, sim_best* ou
 int sim_set_timing(sim_ctx* ctx, int enable);
 int sim_get_timing(sim_ctx* ctx, int kind, double* total_ms, int64_t* launches);
 
+/*
+ * Work measure of the periodic shortcut.  After its warm-up a 1F1B schedule
+ * usually becomes periodic: one steady iteration advances every stage's
+ * state by the same amount, and so does every later one (the recurrence is
+ * a max of sums, Table 1's per-op costs being constants per stage), so the
+ * remaining steady iterations are added in one step.  While timing is
+ * enabled sim_eval_plans sums, on the device, the recurrence work this
+ * skipped: s skipped iterations of an S-stage pipeline count
+ * s * (6 (S - 1) + 2) VALU ops, the cost of S forward and S backward nodes
+ * at 3 ops per node (1 for a node without a cross-stage input).
+ * sim_get_skipped_ops synchronises the device, writes the sum to *ops (host
+ * memory) and clears it; enabling timing also clears it.
+ */
+int sim_get_skipped_ops(sim_ctx* ctx, uint64_t* ops);
+
 void sim_destroy(sim_ctx* ctx);
 const char* sim_strerror(int code);
 

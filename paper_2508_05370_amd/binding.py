@@ -43,7 +43,7 @@ class Best(C.Structure):
 
 
 EXPORTS = ("sim_create", "sim_eval_plans", "sim_eval_stages", "sim_argmin", "sim_best_reduce", "sim_set_timing",
-           "sim_get_timing", "sim_destroy", "sim_strerror")
+           "sim_get_timing", "sim_get_skipped_ops", "sim_destroy", "sim_strerror")
 
 
 def lib():
@@ -69,6 +69,8 @@ def lib():
         L.sim_set_timing.restype = C.c_int
         L.sim_get_timing.argtypes = [P, C.c_int, C.POINTER(C.c_double), C.POINTER(I64)]
         L.sim_get_timing.restype = C.c_int
+        L.sim_get_skipped_ops.argtypes = [P, C.POINTER(C.c_uint64)]
+        L.sim_get_skipped_ops.restype = C.c_int
         L.sim_destroy.argtypes = [P]
         L.sim_destroy.restype = None
         L.sim_strerror.argtypes = [C.c_int]
@@ -240,6 +242,11 @@ class Sim:
         ms, cnt = C.c_double(), C.c_int64()
         _check(lib().sim_get_timing(self.h, kind, C.byref(ms), C.byref(cnt)), "sim_get_timing")
         return ms.value, cnt.value
+
+    def get_skipped_ops(self):
+        v = C.c_uint64()
+        _check(lib().sim_get_skipped_ops(self.h, C.byref(v)), "sim_get_skipped_ops")
+        return v.value
 
 
 def best_tuple(slot_tensor):

@@ -16,10 +16,9 @@ hipError_t launch_prep(const Tab& t, const sim_plans& p, int64_t n, uint64_t* ou
                        uint32_t* meta, uint32_t* hist, hipStream_t s);
 hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint32_t* meta, int64_t n, uint64_t* out_stage,
                          hipStream_t s);
-hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* gstart, hipStream_t s);
+hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* sstart, hipStream_t s);
 hipError_t launch_scatter(const uint32_t* meta, uint32_t nslots, uint32_t* cursor, uint32_t* ids, hipStream_t s);
-hipError_t launch_eval(const Tab& t, const PackedPlan* packed, const uint32_t* meta, const uint32_t* ids,
-                       const uint32_t* gstart, uint32_t max_tasks, uint64_t* out, uint32_t* ovf, hipStream_t s);
+hipError_t launch_eval(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s);
 hipError_t launch_argmin(const uint64_t* t, int64_t n, int64_t base, sim_best* b, hipStream_t s);
 hipError_t launch_best_reduce(const sim_best* in, int64_t n, sim_best* out, hipStream_t s);
 }  // namespace hetsim
@@ -43,6 +42,7 @@ struct sim_ctx {
   std::mutex mu;
   bool timing;
   std::vector<EventPair> ev[3];
+  uint64_t* skipped_ops;   // device counter, inside `tables`
 };
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -77,11 +77,12 @@ extern "C" int sim_create(const sim_model_desc* model, const sim_cluster_desc* c
     size_t bytes;
     size_t off;
   };
-  Part parts[8] = {{ht->pf.data(), ht->pf.size() * 8, 0},         {ht->pb.data(), ht->pb.size() * 8, 0},
+  const uint64_t zero = 0;
+  Part parts[9] = {{ht->pf.data(), ht->pf.size() * 8, 0},         {ht->pb.data(), ht->pb.size() * 8, 0},
                    {ht->emb.data(), ht->emb.size() * 8, 0},       {ht->head.data(), ht->head.size() * 8, 0},
                    {ht->pa.data(), ht->pa.size() * 8, 0},         {ht->rm_nic.data(), ht->rm_nic.size() * 4, 0},
                    {ht->rm_intra.data(), ht->rm_intra.size() * 4, 0},
-                   {ht->ty.data(), ht->ty.size() * sizeof(TypeInfo), 0}};
+                   {ht->ty.data(), ht->ty.size() * sizeof(TypeInfo), 0}, {&zero, 8, 0}};
   size_t total = 0;
   for (auto& p : parts) { p.off = total; total += align256(p.bytes); }
   if (hipMalloc(&c->tables, total) != hipSuccess) { delete ht; delete c; return SIM_ENOMEM; }
@@ -98,6 +99,7 @@ extern "C" int sim_create(const sim_model_desc* model, const sim_cluster_desc* c
   c->tab.rm_nic = (const uint32_t*)(b + parts[5].off);
   c->tab.rm_intra = (const uint32_t*)(b + parts[6].off);
   c->tab.ty = (const TypeInfo*)(b + parts[7].off);
+  c->skipped_ops = (uint64_t*)(b + parts[8].off);
   delete ht;
   hipMemPoolProps props;
   memset(&props, 0, sizeof(props));
@@ -139,18 +141,18 @@ static void end_event(sim_ctx* c, int kind, hipStream_t s, EventPair* e) {
   c->ev[kind].push_back(*e);
 }
 
-// Workspace of one chunk: packed plans, pipeline metadata and ids, bucket
-// counts followed by the overflow list (count, then pipeline ids; cleared
-// together with the counts), bucket cursors, and the start of each
-// stage-count group.
-constexpr uint32_t kCounters = kBuckets + 8;
+// Workspace of one chunk: packed plans, pipeline metadata, pipeline ids and
+// the deferred lists, bucket counts followed by the evaluation counters and
+// the overflow list (counts and counters cleared together), bucket cursors,
+// and the start of each stage count's pipelines.
+constexpr uint32_t kCounters = kBuckets + kEvalCounters;
 struct Work {
   PackedPlan* packed;
-  uint32_t *meta, *ids, *hist, *ovf, *cursor, *gstart;
+  uint32_t *meta, *ids, *deferred, *hist, *ctr, *cursor, *sstart;
 };
 static size_t work_bytes(int64_t ch) {
-  return align256((size_t)ch * sizeof(PackedPlan)) + 2 * align256((size_t)ch * 4 * 4) +
-         align256(kCounters * 4 + (size_t)ch * 4 * 4) + align256(kBuckets * 4) + align256(8 * 4);
+  return align256((size_t)ch * sizeof(PackedPlan)) + 3 * align256((size_t)ch * 4 * 4) +
+         align256(kCounters * 4 + (size_t)ch * 4 * 4) + align256(kBuckets * 4) + align256((kMaxStages + 1) * 4);
 }
 static Work carve(void* base, int64_t ch) {
   Work w;
@@ -158,9 +160,10 @@ static Work carve(void* base, int64_t ch) {
   w.packed = (PackedPlan*)p; p += align256((size_t)ch * sizeof(PackedPlan));
   w.meta = (uint32_t*)p; p += align256((size_t)ch * 16);
   w.ids = (uint32_t*)p; p += align256((size_t)ch * 16);
-  w.hist = (uint32_t*)p; w.ovf = w.hist + kBuckets; p += align256(kCounters * 4 + (size_t)ch * 16);
+  w.deferred = (uint32_t*)p; p += align256((size_t)ch * 16);
+  w.hist = (uint32_t*)p; w.ctr = w.hist + kBuckets; p += align256(kCounters * 4 + (size_t)ch * 16);
   w.cursor = (uint32_t*)p; p += align256(kBuckets * 4);
-  w.gstart = (uint32_t*)p;
+  w.sstart = (uint32_t*)p;
   return w;
 }
 
@@ -184,11 +187,14 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
     bool t1 = e == hipSuccess && begin_event(c, 1, s, &ev);
     if (e == hipSuccess) e = launch_prep(c->tab, p, cn, out + off, w.packed, w.meta, w.hist, s);
     if (t1) end_event(c, 1, s, &ev);
-    if (e == hipSuccess) e = launch_scan(w.hist, w.cursor, w.gstart, s);
+    if (e == hipSuccess) e = launch_scan(w.hist, w.cursor, w.sstart, s);
     if (e == hipSuccess) e = launch_scatter(w.meta, (uint32_t)(cn * 4), w.cursor, w.ids, s);
     bool t0 = e == hipSuccess && begin_event(c, 0, s, &ev);
-    if (e == hipSuccess)
-      e = launch_eval(c->tab, w.packed, w.meta, w.ids, w.gstart, (uint32_t)(cn * 4), out + off, w.ovf, s);
+    if (e == hipSuccess) {
+      const EvalArgs a = {w.packed, w.meta, w.ids, w.sstart, out + off, w.ctr, w.deferred,
+                          c->timing ? c->skipped_ops : nullptr};
+      e = launch_eval(c->tab, a, (uint32_t)(cn * 4), s);
+    }
     if (t0) end_event(c, 0, s, &ev);
   }
   if (tcall) end_event(c, 2, s, &call);
@@ -227,7 +233,20 @@ extern "C" int sim_best_reduce(sim_ctx* c, const sim_best* in, int64_t n, sim_be
 
 extern "C" int sim_set_timing(sim_ctx* c, int enable) {
   if (!c) return SIM_EINVAL;
+  if (enable && !c->timing) {
+    if (hipSetDevice(c->device) != hipSuccess || hipMemset(c->skipped_ops, 0, 8) != hipSuccess)
+      return SIM_EHIP;
+  }
   c->timing = enable != 0;
+  return SIM_OK;
+}
+
+extern "C" int sim_get_skipped_ops(sim_ctx* c, uint64_t* ops) {
+  if (!c || !ops) return SIM_EINVAL;
+  if (hipSetDevice(c->device) != hipSuccess || hipDeviceSynchronize() != hipSuccess ||
+      hipMemcpy(ops, c->skipped_ops, 8, hipMemcpyDeviceToHost) != hipSuccess ||
+      hipMemset(c->skipped_ops, 0, 8) != hipSuccess)
+    return SIM_EHIP;
   return SIM_OK;
 }
 

@@ -65,6 +65,23 @@ struct Tab {
   const TypeInfo* ty;             // [K]
 };
 
+// Device buffers of one evaluation pass over a chunk, as the host hands them
+// to the launcher.  sstart[16 - S] is the first sorted id of the S-stage
+// pipelines, sstart[16] their total.  ctr[0] counts overflowed pipelines,
+// ctr[1 + 16 - S] the S-stage pipelines deferred to the full-loop pass; the
+// overflow list follows the counters at ctr + kEvalCounters.
+constexpr uint32_t kEvalCounters = 32;
+struct EvalArgs {
+  const PackedPlan* packed;
+  const uint32_t* meta;
+  const uint32_t* ids;
+  const uint32_t* sstart;
+  uint64_t* out;
+  uint32_t* ctr;
+  uint32_t* deferred;          // as long as ids
+  uint64_t* skipped_ops;       // optional
+};
+
 // Host side: validate descriptors and build the tables (host copies).
 struct HostTables {
   Tab tab;

@@ -8,13 +8,19 @@
 //   k_scatter  groups pipeline ids by bucket, so that a wavefront runs
 //              pipelines of one stage count, one class count and similar
 //              micro-batch counts.
-//   k_eval     one pipeline per lane.  Setup: place the class on its device
-//              pools, read stage compute from the layer prefix tables, find
-//              each group's slowest link with range-max tables, and cost the
-//              TP/EP/PP/DP collectives.  Then the 1F1B recurrence, unrolled per
-//              stage count so that all per-stage state stays in VGPRs; times
-//              are integers carried exactly in fp64 (3 VALU ops per schedule
-//              node); a pipeline whose time reaches 2^53 ps is redone in u64.
+//   k_eval     one pipeline per lane, one launch per group of four stage
+//              counts.  Setup: place the class on its device pools, read
+//              stage compute from the layer prefix tables, find each group's
+//              slowest link with range-max tables, and cost the TP/EP/PP/DP
+//              collectives.  Then the 1F1B recurrence, unrolled per stage
+//              count so that all per-stage state stays in VGPRs; times are
+//              integers carried exactly in fp64 (3 VALU ops per schedule
+//              node).  Once a steady iteration advances the whole schedule
+//              state by one constant, the remaining steady iterations are
+//              added in one step (periodic shortcut); lanes still aperiodic
+//              after a fixed budget are deferred.
+//   k_deferred the deferred pipelines of all stage counts, full steady loop.
+//   k_redo_u64 pipelines whose time reached 2^53 ps, again in u64.
 //              The plan's time is the max over its classes (atomic max).
 #include <hip/hip_runtime.h>
 
@@ -350,10 +356,10 @@ __global__ void k_fill32(uint32_t* p, uint32_t n, uint32_t v) {
   for (uint32_t j = blockIdx.x * blockDim.x + threadIdx.x; j < n; j += gridDim.x * blockDim.x) p[j] = v;
 }
 
-// exclusive scan of the bucket counts; gstart[g] = first id of stage-count
-// group g (g = 0..3), gstart[4] = number of pipelines
+// exclusive scan of the bucket counts; sstart[16 - S] = first id of the
+// S-stage pipelines, sstart[16] = number of pipelines
 __global__ void __launch_bounds__(1024) k_scan(const uint32_t* __restrict__ hist, uint32_t* __restrict__ cursor,
-                                               uint32_t* __restrict__ gstart) {
+                                               uint32_t* __restrict__ sstart) {
   constexpr int kPer = kBuckets / 1024;
   static_assert(kBuckets % 1024 == 0, "bucket count");
   __shared__ uint32_t part[1024];
@@ -370,11 +376,11 @@ __global__ void __launch_bounds__(1024) k_scan(const uint32_t* __restrict__ hist
     __syncthreads();
   }
   uint32_t run = part[tid] - sum;
-  // group g of stage counts starts at bucket g * kBuckets / 4
-  if ((tid * kPer) % (kBuckets / 4) == 0) gstart[(tid * kPer) / (kBuckets / 4)] = run;
+  // pipelines of S stages start at bucket (16 - S) * kBuckets / 16
+  if ((tid * kPer) % (kBuckets / kMaxStages) == 0) sstart[(tid * kPer) / (kBuckets / kMaxStages)] = run;
 #pragma unroll
   for (int j = 0; j < kPer; ++j) { cursor[tid * kPer + j] = run; run += v[j]; }
-  if (tid == 1023) gstart[4] = part[1023];
+  if (tid == 1023) sstart[kMaxStages] = part[1023];
 }
 
 // place every pipeline id at its bucket's next free position
@@ -429,8 +435,35 @@ typedef uint64_t StageRec[kMaxStages][kRecWords];
 __device__ __forceinline__ double vmax(double a, double b) { return __builtin_fmax(a, b); }
 __device__ __forceinline__ uint64_t vmax(uint64_t a, uint64_t b) { return a > b ? a : b; }
 
+// Periodic regime.  One steady iteration maps the state x = (out_f[0..S-2],
+// last[0..S-1]) to a max of (component + constant) terms, so adding a constant
+// lam to every component of x adds lam to every component of the result.
+// Hence once an iteration advances every component by the same lam, every
+// later one does too, and the remaining r steady iterations collapse into
+// x += r * lam, exactly (in fp64 every value stays below 2^53 or the pipeline
+// is redone in u64).  On the workloads here most schedules reach that regime
+// within a few iterations after the warm-up, against a hundred or more
+// micro-batches.  A wave waits at most kPeriodicBudget steady iterations for
+// its lanes; a lane still aperiodic by then is deferred to a full-loop pass,
+// so one aperiodic schedule does not hold 63 periodic ones.
+constexpr int kPeriodicBudget = 32;
+
 template <int S, typename V>
-__device__ __forceinline__ V pipe(const StageRec& R, uint32_t M) {
+__device__ __forceinline__ void steady_iter(const V (&f)[S], const V (&b)[S], const V (&c)[S], V (&out_f)[S],
+                                            V (&last)[S]) {
+#pragma unroll
+  for (int s = S - 1; s >= 0; --s) {
+    const V st = s == 0 ? last[0] : vmax(last[s], out_f[s - 1] + c[s - 1]);
+    out_f[s] = st + f[s];
+    const V sb = s == S - 1 ? out_f[s] : vmax(out_f[s], last[s + 1] + c[s]);
+    last[s] = sb + b[s];
+  }
+}
+
+// kJump: take the periodic shortcut; then `skipped` returns the steady
+// iterations it skipped, or -1 if the lane is deferred (result not computed).
+template <int S, typename V, bool kJump>
+__device__ __forceinline__ V pipe(const StageRec& R, uint32_t M, int& skipped) {
   V f[S], b[S], c[S], out_f[S], last[S];
 #pragma unroll
   for (int s = 0; s < S; ++s) {
@@ -452,18 +485,52 @@ __device__ __forceinline__ V pipe(const StageRec& R, uint32_t M) {
       }
     }
   }
-  const int steady = m_ - (S - 1);
-  // two iterations per trip: the next iteration's upper stages overlap this
-  // one's backward chain
-#pragma unroll 2
-  for (int i = 0; i < steady; ++i) {
+  int left = m_ - (S - 1);
+  skipped = 0;
+  if (kJump) {
+    int budget = kPeriodicBudget;
+    while (left >= 2 && budget > 0) {
+      steady_iter<S, V>(f, b, c, out_f, last);
+      // second iteration of the pair: does every state value advance by lam?
+      bool same = true;
+      V lam = 0;
 #pragma unroll
-    for (int s = S - 1; s >= 0; --s) {
-      const V st = s == 0 ? last[0] : vmax(last[s], out_f[s - 1] + c[s - 1]);
-      out_f[s] = st + f[s];
-      const V sb = s == S - 1 ? out_f[s] : vmax(out_f[s], last[s + 1] + c[s]);
-      last[s] = sb + b[s];
+      for (int s = S - 1; s >= 0; --s) {
+        const V st = s == 0 ? last[0] : vmax(last[s], out_f[s - 1] + c[s - 1]);
+        const V nf = st + f[s];
+        if (s < S - 1) same = same && nf - out_f[s] == lam;
+        out_f[s] = nf;
+        const V nl = (s == S - 1 ? nf : vmax(nf, last[s + 1] + c[s])) + b[s];
+        if (s == S - 1) lam = nl - last[s];
+        else same = same && nl - last[s] == lam;
+        last[s] = nl;
+      }
+      left -= 2;
+      budget -= 2;
+      if (same) {
+        const V k = (V)left * lam;
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+          out_f[s] += k;
+          last[s] += k;
+        }
+        skipped = left;
+        left = 0;
+      }
     }
+    if (left == 1) {
+      steady_iter<S, V>(f, b, c, out_f, last);
+      left = 0;
+    }
+    if (left > 0) {
+      skipped = -1;
+      return 0;
+    }
+  } else {
+    // two iterations per trip: the next iteration's upper stages overlap
+    // this one's backward chain
+#pragma unroll 2
+    for (int i = 0; i < left; ++i) steady_iter<S, V>(f, b, c, out_f, last);
   }
 #pragma unroll
   for (int tr = 0; tr < S - 1; ++tr) {
@@ -493,38 +560,56 @@ __device__ __forceinline__ V pipe(const StageRec& R, uint32_t M) {
 // and k_redo_u64 evaluates it again in u64, outside the hot kernels.
 constexpr double kExact = 9007199254740992.0;
 
+// Device buffers of one evaluation pass over a chunk.
+struct EvalBufs {
+  const PackedPlan* packed;
+  const uint32_t* meta;
+  const uint32_t* ids;      // pipeline ids sorted by bucket
+  const uint32_t* sstart;   // [16 - S]: start of the S-stage pipelines in ids; [16] = total
+  uint64_t* out;
+  uint32_t* ctr;            // [0] overflow count, [1 + 16 - S] deferred S-stage pipelines
+  uint32_t* ovf;            // overflow list (fp64 result reached 2^53)
+  uint32_t* deferred;       // deferred S-stage pipelines at [sstart[16 - S], ...)
+  unsigned long long* skipped_ops;   // optional: recurrence ops skipped by the shortcut
+};
+
 // Pipelines are sorted by stage count (descending), so each group of four
 // stage counts is a contiguous range of ids; one kernel per group keeps the
 // register footprint, and so the occupancy, of small pipelines independent of
 // the 16-stage code.  Block b of group g runs the g-th range's pipelines
-// [64b, 64b + 64); blocks past the range return at once.
-template <int S>
-__device__ __forceinline__ void eval_one(const Tab& t, const PackedPlan* __restrict__ packed, uint32_t slot,
-                                         uint32_t M, uint64_t* __restrict__ out, uint32_t* __restrict__ ovf) {
-  const Plan p = unpack(packed[slot >> 2]);
+// [64b, 64b + 64); blocks past the range return at once.  This first pass
+// takes the periodic shortcut and defers the lanes still aperiodic after the
+// budget; k_deferred runs those through the whole steady loop.
+template <int S, bool kFull>
+__device__ __forceinline__ void eval_one(const Tab& t, const EvalBufs& e, uint32_t slot, uint32_t M) {
+  const Plan p = unpack(e.packed[slot >> 2]);
   StageRec R;
   class_setup(t, p, slot & 3, R);
-  const double T = pipe<S, double>(R, M);
-  if (T < kExact) {
-    atomicMax((unsigned long long*)&out[slot >> 2], (unsigned long long)T);
-  } else {
-    ovf[1 + atomicAdd(&ovf[0], 1u)] = slot;
+  int skipped;
+  const double T = pipe<S, double, !kFull>(R, M, skipped);
+  if (skipped < 0) {
+    e.deferred[e.sstart[kMaxStages - S] + atomicAdd(&e.ctr[1 + kMaxStages - S], 1u)] = slot;
+    return;
   }
+  if (T < kExact) {
+    atomicMax((unsigned long long*)&e.out[slot >> 2], (unsigned long long)T);
+  } else {
+    e.ovf[atomicAdd(&e.ctr[0], 1u)] = slot;
+  }
+  if (e.skipped_ops && skipped > 0)
+    atomicAdd(e.skipped_ops, (unsigned long long)skipped * (unsigned long long)(6 * (S - 1) + 2));
 }
 
 template <int GRP>
-__global__ void __launch_bounds__(64) k_eval(Tab t, const PackedPlan* __restrict__ packed,
-                                             const uint32_t* __restrict__ meta, const uint32_t* __restrict__ ids,
-                                             const uint32_t* __restrict__ gstart, uint64_t* __restrict__ out,
-                                             uint32_t* __restrict__ ovf) {
+__global__ void __launch_bounds__(64) k_eval(Tab t, EvalBufs e) {
   constexpr int kTop = kMaxStages - 4 * GRP;   // stage counts kTop-3 .. kTop
-  const uint32_t lo = gstart[GRP], hi = gstart[GRP + 1];
+  const uint32_t lo = e.sstart[4 * GRP], hi = e.sstart[4 * GRP + 4];
   const uint32_t base = lo + blockIdx.x * 64u;
   if (base >= hi) return;
   const uint32_t pos = base + threadIdx.x;
   bool pending = pos < hi;
-  const uint32_t slot = pending ? ids[pos] : 0;
-  const uint32_t m = pending ? meta[slot] : 0;
+  const uint32_t slot = pending ? e.ids[pos] : 0;
+  const uint32_t m = pending ? e.meta[slot] : 0;
   const uint32_t S = m & 31, M = m >> 8;
   // one pass per distinct stage count present in the wavefront (usually one)
   while (true) {
@@ -532,11 +617,50 @@ __global__ void __launch_bounds__(64) k_eval(Tab t, const PackedPlan* __restrict
     if (!live) break;
     const uint32_t S0 = __builtin_amdgcn_readfirstlane(__shfl(S, __ffsll((unsigned long long)live) - 1));
     if (pending && S == S0) {
-      if (S0 == kTop) eval_one<kTop>(t, packed, slot, M, out, ovf);
-      else if (S0 == kTop - 1) eval_one<kTop - 1>(t, packed, slot, M, out, ovf);
-      else if (S0 == kTop - 2) eval_one<kTop - 2>(t, packed, slot, M, out, ovf);
-      else eval_one<kTop - 3>(t, packed, slot, M, out, ovf);
+      if (S0 == kTop) eval_one<kTop, false>(t, e, slot, M);
+      else if (S0 == kTop - 1) eval_one<kTop - 1, false>(t, e, slot, M);
+      else if (S0 == kTop - 2) eval_one<kTop - 2, false>(t, e, slot, M);
+      else eval_one<kTop - 3, false>(t, e, slot, M);
       pending = false;
+    }
+  }
+}
+
+// Deferred pipelines of every stage count in one launch, so that the long
+// serial chains of the different stage counts overlap.  Deferred S-stage
+// pipelines sit at [sstart[16 - S], + ctr[1 + 16 - S]); tile q of 64 is
+// located by walking the sixteen list lengths (16 stages first), and tiles
+// are dealt round-robin to the blocks of the grid.
+__global__ void __launch_bounds__(64) k_deferred(Tab t, EvalBufs e) {
+  for (uint32_t q = blockIdx.x;; q += gridDim.x) {
+    uint32_t j = 0, before = 0, nt = 0;
+    for (; j < kMaxStages; ++j) {
+      nt = (e.ctr[1 + j] + 63) >> 6;
+      if (q < before + nt) break;
+      before += nt;
+    }
+    if (j == kMaxStages) return;
+    const uint32_t off = (q - before) * 64u + threadIdx.x;
+    if (off >= e.ctr[1 + j]) continue;
+    const uint32_t slot = e.deferred[e.sstart[j] + off];
+    const uint32_t M = e.meta[slot] >> 8;
+    switch (kMaxStages - j) {
+      case 1: eval_one<1, true>(t, e, slot, M); break;
+      case 2: eval_one<2, true>(t, e, slot, M); break;
+      case 3: eval_one<3, true>(t, e, slot, M); break;
+      case 4: eval_one<4, true>(t, e, slot, M); break;
+      case 5: eval_one<5, true>(t, e, slot, M); break;
+      case 6: eval_one<6, true>(t, e, slot, M); break;
+      case 7: eval_one<7, true>(t, e, slot, M); break;
+      case 8: eval_one<8, true>(t, e, slot, M); break;
+      case 9: eval_one<9, true>(t, e, slot, M); break;
+      case 10: eval_one<10, true>(t, e, slot, M); break;
+      case 11: eval_one<11, true>(t, e, slot, M); break;
+      case 12: eval_one<12, true>(t, e, slot, M); break;
+      case 13: eval_one<13, true>(t, e, slot, M); break;
+      case 14: eval_one<14, true>(t, e, slot, M); break;
+      case 15: eval_one<15, true>(t, e, slot, M); break;
+      default: eval_one<16, true>(t, e, slot, M); break;
     }
   }
 }
@@ -544,17 +668,16 @@ __global__ void __launch_bounds__(64) k_eval(Tab t, const PackedPlan* __restrict
 // Pipelines whose fp64 time reached 2^53 ps, again in u64 (exact below 2^64).
 template <int S>
 __device__ __forceinline__ uint64_t redo_one(const StageRec& R, uint32_t M) {
-  return pipe<S, uint64_t>(R, M);
+  int skipped;
+  return pipe<S, uint64_t, false>(R, M, skipped);
 }
 
-__global__ void __launch_bounds__(64) k_redo_u64(Tab t, const PackedPlan* __restrict__ packed,
-                                                 const uint32_t* __restrict__ meta, const uint32_t* __restrict__ ovf,
-                                                 uint64_t* __restrict__ out) {
-  const uint32_t n = ovf[0];
+__global__ void __launch_bounds__(64) k_redo_u64(Tab t, EvalBufs e) {
+  const uint32_t n = e.ctr[0];
   for (uint32_t j = blockIdx.x * 64u + threadIdx.x; j < n; j += gridDim.x * 64u) {
-    const uint32_t slot = ovf[1 + j];
-    const uint32_t m = meta[slot], S = m & 31, M = m >> 8;
-    const Plan p = unpack(packed[slot >> 2]);
+    const uint32_t slot = e.ovf[j];
+    const uint32_t m = e.meta[slot], S = m & 31, M = m >> 8;
+    const Plan p = unpack(e.packed[slot >> 2]);
     StageRec R;
     class_setup(t, p, slot & 3, R);
     uint64_t r;
@@ -576,7 +699,7 @@ __global__ void __launch_bounds__(64) k_redo_u64(Tab t, const PackedPlan* __rest
       case 15: r = redo_one<15>(R, M); break;
       default: r = redo_one<16>(R, M); break;
     }
-    atomicMax((unsigned long long*)&out[slot >> 2], (unsigned long long)r);
+    atomicMax((unsigned long long*)&e.out[slot >> 2], (unsigned long long)r);
   }
 }
 
@@ -671,22 +794,27 @@ hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint32_t*
   k_stages<<<blocks_for(n * 4, 256), 256, 0, s>>>(t, packed, meta, n, out_stage);
   return hipGetLastError();
 }
-hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* gstart, hipStream_t s) {
-  k_scan<<<1, 1024, 0, s>>>(hist, cursor, gstart);
+hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* sstart, hipStream_t s) {
+  k_scan<<<1, 1024, 0, s>>>(hist, cursor, sstart);
   return hipGetLastError();
 }
 hipError_t launch_scatter(const uint32_t* meta, uint32_t nslots, uint32_t* cursor, uint32_t* ids, hipStream_t s) {
   k_scatter<<<blocks_for(nslots, 256 * kScatterPer), 256, 0, s>>>(meta, nslots, cursor, ids);
   return hipGetLastError();
 }
-hipError_t launch_eval(const Tab& t, const PackedPlan* packed, const uint32_t* meta, const uint32_t* ids,
-                       const uint32_t* gstart, uint32_t max_tasks, uint64_t* out, uint32_t* ovf, hipStream_t s) {
+// two waves per SIMD of the 16-stage code
+constexpr int kDeferredBlocks = 2048;
+
+hipError_t launch_eval(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s) {
   const int g = blocks_for(max_tasks, 64) > 0 ? blocks_for(max_tasks, 64) : 1;
-  k_eval<0><<<g, 64, 0, s>>>(t, packed, meta, ids, gstart, out, ovf);
-  k_eval<1><<<g, 64, 0, s>>>(t, packed, meta, ids, gstart, out, ovf);
-  k_eval<2><<<g, 64, 0, s>>>(t, packed, meta, ids, gstart, out, ovf);
-  k_eval<3><<<g, 64, 0, s>>>(t, packed, meta, ids, gstart, out, ovf);
-  k_redo_u64<<<32, 64, 0, s>>>(t, packed, meta, ovf, out);
+  const EvalBufs e = {a.packed, a.meta, a.ids, a.sstart, a.out, a.ctr, a.ctr + kEvalCounters, a.deferred,
+                      (unsigned long long*)a.skipped_ops};
+  k_eval<0><<<g, 64, 0, s>>>(t, e);
+  k_eval<1><<<g, 64, 0, s>>>(t, e);
+  k_eval<2><<<g, 64, 0, s>>>(t, e);
+  k_eval<3><<<g, 64, 0, s>>>(t, e);
+  k_deferred<<<g < kDeferredBlocks ? g : kDeferredBlocks, 64, 0, s>>>(t, e);
+  k_redo_u64<<<32, 64, 0, s>>>(t, e);
   return hipGetLastError();
 }
 hipError_t launch_argmin(const uint64_t* t, int64_t n, int64_t base, sim_best* b, hipStream_t s) {

@@ -249,3 +249,59 @@ def test_chunked_streams_argmin(torch, B, oracle_mod, workloads):
         assert torch.equal(out, full)
     want = oracle_mod.Oracle(w["model"], w["cluster"]).eval(_sub(p, np.array([ref[1]])))
     assert int(want[0]) == ref[0]
+
+
+def _steady_periodic_at(S, M, f, b, c, limit):
+    """First steady iteration (0-based) after which the 1F1B state has advanced
+    by one constant in every component, or None within `limit` iterations."""
+    out_f, last = [0] * S, [0] * S
+    for m in range(min(S - 1, M)):
+        for s in range(S - 1 - m):
+            st = last[0] if s == 0 else max(last[s], out_f[s - 1] + c[s - 1])
+            out_f[s] = st + f[s]
+            last[s] = out_f[s]
+    prev = None
+    for i in range(min(M - (S - 1), limit)):
+        for s in range(S - 1, -1, -1):
+            st = last[0] if s == 0 else max(last[s], out_f[s - 1] + c[s - 1])
+            out_f[s] = st + f[s]
+            last[s] = (out_f[s] if s == S - 1 else max(out_f[s], last[s + 1] + c[s])) + b[s]
+        x = out_f[:S - 1] + last
+        if prev is not None and len({u - v for u, v in zip(x, prev)}) == 1:
+            return i
+        prev = x
+    return None
+
+
+@pytest.mark.parametrize("slow", [1, 40, 200])
+def test_link_bound_schedules(torch, B, oracle_mod, workloads, slow):
+    """Plans whose pipeline hops dominate (NICs and fabrics slowed `slow` times):
+    many schedules never settle into a one-iteration period, so the evaluator's
+    deferred full-loop pass carries a large share of the pipelines."""
+    import copy
+    w = workloads.workload(2)
+    c = copy.deepcopy(w["cluster"])
+    for t in c["types"]:
+        t["nic_MBps"] = max(16, t["nic_MBps"] // slow)
+        t["intra_MBps"] = max(16, t["intra_MBps"] // slow)
+    n = 30_011
+    p = workloads.random_plans(w["model"], c, 0x5107 + slow, 0, n)
+    say("case: workload 2 model, links slowed %dx, %d plans" % (slow, n))
+    got = _gpu_times(B, B.Sim(w["model"], c), p)
+    o = oracle_mod.Oracle(w["model"], c)
+    want = o.eval(p)
+    _assert_equal(got, want, "links slowed %dx" % slow)
+    assert np.count_nonzero(want != MAXU) > n // 2
+    if slow == 200:
+        # the case does reach pipelines that stay aperiodic past the shortcut's budget
+        aperiodic = 0
+        for i in range(300):
+            d = o.detail(p, i)
+            if d is None:
+                continue
+            for g in range(d["G"]):
+                if d["M"][g] - (d["S"] - 1) > 40 and _steady_periodic_at(
+                        d["S"], d["M"][g], d["f"][g], d["b"][g], d["c"][g], 34) is None:
+                    aperiodic += 1
+        say("  aperiodic pipelines in the first 300 plans: %d" % aperiodic)
+        assert aperiodic > 0
