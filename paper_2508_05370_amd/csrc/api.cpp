@@ -72,34 +72,16 @@ extern "C" int sim_create(const sim_model_desc* model, const sim_cluster_desc* c
   c->tables = nullptr;
   c->pool = nullptr;
   if (hipGetDevice(&c->device) != hipSuccess) { delete ht; delete c; return SIM_EHIP; }
-  struct Part {
-    const void* src;
-    size_t bytes;
-    size_t off;
-  };
+  // the table image, then the skipped-work counter
+  const size_t img = align256(ht->img.size());
+  if (hipMalloc(&c->tables, img + 256) != hipSuccess) { delete ht; delete c; return SIM_ENOMEM; }
   const uint64_t zero = 0;
-  Part parts[9] = {{ht->pf.data(), ht->pf.size() * 8, 0},         {ht->pb.data(), ht->pb.size() * 8, 0},
-                   {ht->emb.data(), ht->emb.size() * 8, 0},       {ht->head.data(), ht->head.size() * 8, 0},
-                   {ht->pa.data(), ht->pa.size() * 8, 0},         {ht->rm_nic.data(), ht->rm_nic.size() * 4, 0},
-                   {ht->rm_intra.data(), ht->rm_intra.size() * 4, 0},
-                   {ht->ty.data(), ht->ty.size() * sizeof(TypeInfo), 0}, {&zero, 8, 0}};
-  size_t total = 0;
-  for (auto& p : parts) { p.off = total; total += align256(p.bytes); }
-  if (hipMalloc(&c->tables, total) != hipSuccess) { delete ht; delete c; return SIM_ENOMEM; }
-  for (auto& p : parts)
-    if (p.bytes && hipMemcpy((char*)c->tables + p.off, p.src, p.bytes, hipMemcpyHostToDevice) != hipSuccess) {
-      (void)hipFree(c->tables); delete ht; delete c; return SIM_EHIP;
-    }
-  char* b = (char*)c->tables;
-  c->tab.pf = (const uint64_t*)(b + parts[0].off);
-  c->tab.pb = (const uint64_t*)(b + parts[1].off);
-  c->tab.emb = (const uint64_t*)(b + parts[2].off);
-  c->tab.head = (const uint64_t*)(b + parts[3].off);
-  c->tab.pa = (const uint64_t*)(b + parts[4].off);
-  c->tab.rm_nic = (const uint32_t*)(b + parts[5].off);
-  c->tab.rm_intra = (const uint32_t*)(b + parts[6].off);
-  c->tab.ty = (const TypeInfo*)(b + parts[7].off);
-  c->skipped_ops = (uint64_t*)(b + parts[8].off);
+  if (hipMemcpy(c->tables, ht->img.data(), ht->img.size(), hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy((char*)c->tables + img, &zero, 8, hipMemcpyHostToDevice) != hipSuccess) {
+    (void)hipFree(c->tables); delete ht; delete c; return SIM_EHIP;
+  }
+  c->tab.img = c->tables;
+  c->skipped_ops = (uint64_t*)((char*)c->tables + img);
   delete ht;
   hipMemPoolProps props;
   memset(&props, 0, sizeof(props));

@@ -33,6 +33,19 @@ struct TypeInfo {
   uint64_t a_side;                // one end of an inter-node path: two PCIe trips + NIC
 };
 
+// The tables of the per-pipeline setup form one byte image in device memory
+// that the evaluation kernels copy into LDS, where lanes gather from it at
+// LDS rather than vector-cache rates.  Sections, each 16-byte aligned:
+//   TypeInfo [K]; {forward, backward} layer prefix sums
+//   [K][4 log2 TP][n_mbs][nep][L+1] (nep = 4 EP slots for MoE models, 1 for
+//   dense ones); {fwd, bwd} embedding [K][n_mbs]; {fwd, bwd} head
+//   [K][4][n_mbs]; all-to-all bytes prefix [4][n_mbs][L+1] (MoE only);
+//   range-max rows of the node fabric rates [lvl_node][N]; range-max rows
+//   of the device NIC rates [lvl_dev][D] (last, the largest).
+// mode 0: the whole image fits the LDS budget; 1: all but the device rows
+// fit; 2: nothing is copied and every table is read from device memory.
+constexpr uint32_t kLdsBudget = 64 * 1024;
+
 // Everything a kernel needs about one (model, cluster) pair.  Scalars travel
 // by value in the kernel argument block; tables live in device memory.
 struct Tab {
@@ -55,14 +68,12 @@ struct Tab {
   uint64_t par_layer[4];          // non-expert parameters of one layer on one TP rank, by log2 TP
   uint64_t par_expert[4][4];      // expert parameters of one layer per rank [log2 TP][log2 EP]
   uint64_t par_embed[4], par_head[4];
-  const uint64_t* pf;             // forward layer prefix sums [K][4][n_mbs][4][L+1]
-  const uint64_t* pb;             // backward prefix sums, same shape
-  const uint64_t* emb;            // [K][n_mbs][2] embedding fwd, bwd
-  const uint64_t* head;           // [K][4][n_mbs][2] head fwd, bwd
-  const uint64_t* pa;             // all-to-all bytes prefix [4][n_mbs][L+1]
-  const uint32_t* rm_nic;         // range-max table of NIC rates per device [lvl_dev][D]
-  const uint32_t* rm_intra;       // range-max table of fabric rates per node [lvl_node][N]
-  const TypeInfo* ty;             // [K]
+  uint32_t nep;                   // EP slots of the prefix tables
+  uint32_t o_pfb, o_emb, o_head, o_pa, o_rmi, o_rmn;   // section byte offsets (TypeInfo at 0)
+  uint32_t img_bytes;             // whole image
+  uint32_t lds_bytes;             // prefix copied to LDS: img_bytes, o_rmn or 0 by mode
+  uint32_t mode;
+  const void* img;                // the image in device memory (16-byte aligned)
 };
 
 // Device buffers of one evaluation pass over a chunk, as the host hands them
@@ -85,9 +96,11 @@ struct EvalArgs {
 // Host side: validate descriptors and build the tables (host copies).
 struct HostTables {
   Tab tab;
+  // pf, pb [K][4][n_mbs][4][L+1]; emb [K][n_mbs][2]; head [K][4][n_mbs][2]; pa [4][n_mbs][L+1]
   std::vector<uint64_t> pf, pb, emb, head, pa;
   std::vector<uint32_t> rm_nic, rm_intra;
   std::vector<TypeInfo> ty;
+  std::vector<uint8_t> img;       // the device image built from the above
 };
 
 // Returns 0 (SIM_OK), SIM_EINVAL or SIM_ERANGE.

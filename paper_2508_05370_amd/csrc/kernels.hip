@@ -41,7 +41,7 @@ __device__ __forceinline__ uint64_t link_ps(uint64_t bytes, uint32_t bq) {
 // max over [lo, hi] of a range-max table with row length n
 __device__ __forceinline__ uint32_t range_max(const uint32_t* __restrict__ tb, uint32_t n, uint32_t lo, uint32_t hi) {
   uint32_t j = 31u - __clz(hi - lo + 1);
-  uint32_t a = tb[(size_t)j * n + lo], b = tb[(size_t)j * n + hi + 1 - (1u << j)];
+  uint32_t a = tb[j * n + lo], b = tb[j * n + hi + 1 - (1u << j)];
   return a > b ? a : b;
 }
 
@@ -216,6 +216,47 @@ __global__ void __launch_bounds__(256) k_prep(Tab t, sim_plans pl, int64_t n, ui
   }
 }
 
+// ---------------------------------------------------------------- table image
+// Reads of the setup tables (the image described with Tab).  kMode 0: the
+// whole image is in LDS; 1: all but the device range-max rows; 2: all in
+// device memory.
+template <int kMode>
+struct Hot {
+  const uint8_t* b;       // image base for every section but the device rows
+  const uint32_t* rmn;    // device range-max rows
+  const Tab& t;
+  __device__ __forceinline__ Hot(const Tab& tab, const uint4* lds)
+      : b(kMode < 2 ? (const uint8_t*)lds : (const uint8_t*)tab.img),
+        rmn((const uint32_t*)((kMode == 0 ? (const uint8_t*)lds : (const uint8_t*)tab.img) + tab.o_rmn)),
+        t(tab) {}
+  __device__ __forceinline__ TypeInfo type(uint32_t k) const {
+    const uint4* q = (const uint4*)(b + k * sizeof(TypeInfo));
+    const uint4 x = q[0], y = q[1];
+    TypeInfo r;
+    r.node_off = x.x; r.dev_off = x.y; r.dpl = x.z; r.bq_pcie = x.w;
+    r.a_intra = (uint64_t)y.y << 32 | y.x;
+    r.a_side = (uint64_t)y.w << 32 | y.z;
+    return r;
+  }
+  // {forward, backward} prefix entry
+  __device__ __forceinline__ ulonglong2 pfb(uint32_t i) const { return ((const ulonglong2*)(b + t.o_pfb))[i]; }
+  __device__ __forceinline__ ulonglong2 emb(uint32_t i) const { return ((const ulonglong2*)(b + t.o_emb))[i]; }
+  __device__ __forceinline__ ulonglong2 head(uint32_t i) const { return ((const ulonglong2*)(b + t.o_head))[i]; }
+  __device__ __forceinline__ uint64_t pa(uint32_t i) const { return ((const uint64_t*)(b + t.o_pa))[i]; }
+  __device__ __forceinline__ const uint32_t* rmi() const { return (const uint32_t*)(b + t.o_rmi); }
+};
+
+// Copy the LDS part of the image (every thread of the block takes part).
+template <int kMode>
+__device__ __forceinline__ void fill_lds(const Tab& t, uint4* lds) {
+  if (kMode < 2) {
+    const uint32_t n = t.lds_bytes >> 4;
+    const uint4* img = (const uint4*)t.img;
+    for (uint32_t i = threadIdx.x; i < n; i += blockDim.x) lds[i] = img[i];
+    __syncthreads();
+  }
+}
+
 // ---------------------------------------------------------------- per-pipeline setup
 // Stage quantities of class c of a valid plan: rec[s] = {forward and backward
 // time of one micro-batch on stage s, hop s -> s+1, DP sync of stage s}.
@@ -234,11 +275,13 @@ __device__ __forceinline__ uint32_t placed_before(const Plan& p, uint32_t c, uin
   return below + rc * count_type(tc, k, (1ull << (4 * s)) - 1);
 }
 
-__device__ void class_setup(const Tab& t, const Plan& p, uint32_t c, uint64_t (&rec)[kMaxStages][kRecWords]) {
+template <int kMode>
+__device__ void class_setup(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t c,
+                            uint64_t (&rec)[kMaxStages][kRecWords]) {
   const uint32_t S = p.S, G = p.G, tp = p.tp, ep = p.ep, tpl = p.tpl, epl = p.epl, mi = p.mi;
   const uint64_t act = t.act[mi], act_tp = (act + tp - 1) >> tpl;
   const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> epl);
-  const size_t L1 = t.L + 1;
+  const uint32_t L1 = t.L + 1, epq = t.E ? p.epl : 0;
   const uint32_t reps = c == 0 ? p.reps[0] : c == 1 ? p.reps[1] : c == 2 ? p.reps[2] : p.reps[3];
   const uint64_t tvc = c == 0 ? p.tv[0] : c == 1 ? p.tv[1] : c == 2 ? p.tv[2] : p.tv[3];
   uint32_t pk = 0, pbase = 0, pnic = 0, pin = 0, lo = 0;
@@ -247,23 +290,25 @@ __device__ void class_setup(const Tab& t, const Plan& p, uint32_t c, uint64_t (&
     const uint32_t hi = cut_at(p, s), ns = hi - lo;
     // ---- this class: compute, TP, EP, hop from the previous stage
     const uint32_t k = (uint32_t)(tvc >> (4 * s)) & 15;
-    const TypeInfo ti = t.ty[k];
+    const TypeInfo ti = h.type(k);
     const uint32_t base = placed_before(p, c, s, k) * tp, nd = reps * tp, dpl = ti.dpl;
     const uint32_t gnl = ti.node_off + (base >> dpl), gnh = ti.node_off + ((base + nd - 1) >> dpl);
-    const uint32_t bq_in = range_max(t.rm_intra, t.N, gnl, gnh);
+    const uint32_t bq_in = range_max(h.rmi(), t.N, gnl, gnh);
     const uint32_t dlo = ti.dev_off + base;
-    const uint32_t bq_nic = range_max(t.rm_nic, t.D, dlo, dlo + nd - 1);
-    const size_t tb = ((((size_t)k * 4 + tpl) * t.n_mbs + mi) * 4 + epl) * L1;
-    uint64_t fc = t.pf[tb + hi] - t.pf[tb + lo];
-    uint64_t bc = t.pb[tb + hi] - t.pb[tb + lo];
+    const uint32_t bq_nic = range_max(h.rmn, t.D, dlo, dlo + nd - 1);
+    const uint32_t tb = (((k * 4 + tpl) * t.n_mbs + mi) * t.nep + epq) * L1;
+    const ulonglong2 ph = h.pfb(tb + hi), pl = h.pfb(tb + lo);
+    uint64_t fc = ph.x - pl.x;
+    uint64_t bc = ph.y - pl.y;
     if (s == 0) {
-      fc += t.emb[((size_t)k * t.n_mbs + mi) * 2];
-      bc += t.emb[((size_t)k * t.n_mbs + mi) * 2 + 1];
+      const ulonglong2 em = h.emb(k * t.n_mbs + mi);
+      fc += em.x;
+      bc += em.y;
     }
     if (s == S - 1) {
-      const size_t hb = (((size_t)k * 4 + tpl) * t.n_mbs + mi) * 2;
-      fc += t.head[hb];
-      bc += t.head[hb + 1];
+      const ulonglong2 hd = h.head((k * 4 + tpl) * t.n_mbs + mi);
+      fc += hd.x;
+      bc += hd.y;
     }
     if (tp > 1) {  // TP all-reduces of this stage, exposed in the forward pass
       const uint64_t steps = (uint64_t)(2 * ns + (s == 0)) * 2 * (tp - 1);
@@ -274,8 +319,8 @@ __device__ void class_setup(const Tab& t, const Plan& p, uint32_t c, uint64_t (&
       const bool intra = ep * tp <= (1u << dpl);
       const uint64_t alpha = intra ? ti.a_intra : 2 * ti.a_side;
       const uint32_t bq = intra ? bq_in : (bq_nic > ti.bq_pcie ? bq_nic : ti.bq_pcie);
-      const size_t pa = ((size_t)epl * t.n_mbs + mi) * L1;
-      const uint64_t e = (uint64_t)ns * 2 * (ep - 1) * alpha + link_ps(2 * (t.pa[pa + hi] - t.pa[pa + lo]), bq);
+      const uint32_t pa = (epl * t.n_mbs + mi) * L1;
+      const uint64_t e = (uint64_t)ns * 2 * (ep - 1) * alpha + link_ps(2 * (h.pa(pa + hi) - h.pa(pa + lo)), bq);
       fc += e;
       bc += e;
     }
@@ -306,11 +351,11 @@ __device__ void class_setup(const Tab& t, const Plan& p, uint32_t c, uint64_t (&
       for (uint32_t c2 = 0; c2 < 4; ++c2) {
         if (c2 >= G) continue;
         const uint32_t k2 = (uint32_t)(p.tv[c2] >> (4 * s)) & 15;
-        const TypeInfo t2 = t.ty[k2];
+        const TypeInfo t2 = h.type(k2);
         const uint32_t b2 = placed_before(p, c2, s, k2) * tp, n2 = p.reps[c2] * tp, d2 = t2.dpl;
         const uint32_t l2 = t2.node_off + (b2 >> d2), h2 = t2.node_off + ((b2 + n2 - 1) >> d2);
         const uint32_t dl2 = t2.dev_off + b2;
-        const uint32_t nic2 = range_max(t.rm_nic, t.D, dl2, dl2 + n2 - 1);
+        const uint32_t nic2 = range_max(h.rmn, t.D, dl2, dl2 + n2 - 1);
         if (c2 == 0) k0 = k2; else same = same && k2 == k0;
         nmin = l2 < nmin ? l2 : nmin;
         nmax = h2 > nmax ? h2 : nmax;
@@ -319,8 +364,8 @@ __device__ void class_setup(const Tab& t, const Plan& p, uint32_t c, uint64_t (&
         a_dp = 2 * t2.a_side > a_dp ? 2 * t2.a_side : a_dp;
       }
       const bool intra = same && nmin == nmax;
-      const uint64_t alpha = intra ? t.ty[k0].a_intra : a_dp;
-      const uint32_t bq = intra ? t.rm_intra[nmin] : bq_dp;
+      const uint64_t alpha = intra ? h.type(k0).a_intra : a_dp;
+      const uint32_t bq = intra ? h.rmi()[nmin] : bq_dp;
       const uint64_t pd = (uint64_t)ns * t.par_layer[tpl] + (s == 0 ? t.par_embed[tpl] : 0) +
                           (s == S - 1 ? t.par_head[tpl] : 0);
       tdp = ring_sync(p.psum, rp, p.zero, t.grad_bytes * pd, t.param_bytes * pd, alpha, bq);
@@ -344,7 +389,8 @@ __global__ void __launch_bounds__(256) k_stages(Tab t, const PackedPlan* __restr
   if (slot >= n * 4 || meta[slot] == 0) return;
   const Plan p = unpack(packed[slot >> 2]);
   uint64_t rec[kMaxStages][kRecWords];
-  class_setup(t, p, (uint32_t)(slot & 3), rec);
+  const Hot<2> h(t, nullptr);
+  class_setup(t, h, p, (uint32_t)(slot & 3), rec);
   uint64_t* o = out_stage + slot * (kMaxStages * kRecWords);
   for (uint32_t s = 0; s < p.S; ++s)
 #pragma unroll
@@ -580,11 +626,12 @@ struct EvalBufs {
 // [64b, 64b + 64); blocks past the range return at once.  This first pass
 // takes the periodic shortcut and defers the lanes still aperiodic after the
 // budget; k_deferred runs those through the whole steady loop.
-template <int S, bool kFull>
-__device__ __forceinline__ void eval_one(const Tab& t, const EvalBufs& e, uint32_t slot, uint32_t M) {
+template <int S, bool kFull, int kMode>
+__device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot,
+                                         uint32_t M) {
   const Plan p = unpack(e.packed[slot >> 2]);
   StageRec R;
-  class_setup(t, p, slot & 3, R);
+  class_setup(t, h, p, slot & 3, R);
   int skipped;
   const double T = pipe<S, double, !kFull>(R, M, skipped);
   if (skipped < 0) {
@@ -600,13 +647,20 @@ __device__ __forceinline__ void eval_one(const Tab& t, const EvalBufs& e, uint32
     atomicAdd(e.skipped_ops, (unsigned long long)skipped * (unsigned long long)(6 * (S - 1) + 2));
 }
 
-template <int GRP>
-__global__ void __launch_bounds__(64) k_eval(Tab t, EvalBufs e) {
+// Blocks of four waves share one LDS copy of the table image.
+constexpr uint32_t kEvalThreads = 256;
+
+template <int GRP, int kMode>
+__global__ void __launch_bounds__(kEvalThreads) k_eval(Tab t, EvalBufs e) {
   constexpr int kTop = kMaxStages - 4 * GRP;   // stage counts kTop-3 .. kTop
+  extern __shared__ uint4 lds[];
   const uint32_t lo = e.sstart[4 * GRP], hi = e.sstart[4 * GRP + 4];
-  const uint32_t base = lo + blockIdx.x * 64u;
-  if (base >= hi) return;
-  const uint32_t pos = base + threadIdx.x;
+  const uint32_t first = lo + blockIdx.x * kEvalThreads;
+  if (first >= hi) return;   // the whole block, before any barrier
+  fill_lds<kMode>(t, lds);
+  const Hot<kMode> h(t, lds);
+  const uint32_t pos = first + threadIdx.x;
+  if (first + (threadIdx.x & ~63u) >= hi) return;
   bool pending = pos < hi;
   const uint32_t slot = pending ? e.ids[pos] : 0;
   const uint32_t m = pending ? e.meta[slot] : 0;
@@ -617,10 +671,10 @@ __global__ void __launch_bounds__(64) k_eval(Tab t, EvalBufs e) {
     if (!live) break;
     const uint32_t S0 = __builtin_amdgcn_readfirstlane(__shfl(S, __ffsll((unsigned long long)live) - 1));
     if (pending && S == S0) {
-      if (S0 == kTop) eval_one<kTop, false>(t, e, slot, M);
-      else if (S0 == kTop - 1) eval_one<kTop - 1, false>(t, e, slot, M);
-      else if (S0 == kTop - 2) eval_one<kTop - 2, false>(t, e, slot, M);
-      else eval_one<kTop - 3, false>(t, e, slot, M);
+      if (S0 == kTop) eval_one<kTop, false>(t, h, e, slot, M);
+      else if (S0 == kTop - 1) eval_one<kTop - 1, false>(t, h, e, slot, M);
+      else if (S0 == kTop - 2) eval_one<kTop - 2, false>(t, h, e, slot, M);
+      else eval_one<kTop - 3, false>(t, h, e, slot, M);
       pending = false;
     }
   }
@@ -630,9 +684,14 @@ __global__ void __launch_bounds__(64) k_eval(Tab t, EvalBufs e) {
 // serial chains of the different stage counts overlap.  Deferred S-stage
 // pipelines sit at [sstart[16 - S], + ctr[1 + 16 - S]); tile q of 64 is
 // located by walking the sixteen list lengths (16 stages first), and tiles
-// are dealt round-robin to the blocks of the grid.
-__global__ void __launch_bounds__(64) k_deferred(Tab t, EvalBufs e) {
-  for (uint32_t q = blockIdx.x;; q += gridDim.x) {
+// are dealt round-robin to the waves of the grid.
+template <int kMode>
+__global__ void __launch_bounds__(kEvalThreads) k_deferred(Tab t, EvalBufs e) {
+  extern __shared__ uint4 lds[];
+  fill_lds<kMode>(t, lds);
+  const Hot<kMode> h(t, lds);
+  const uint32_t waves = gridDim.x * (kEvalThreads / 64);
+  for (uint32_t q = blockIdx.x * (kEvalThreads / 64) + (threadIdx.x >> 6);; q += waves) {
     uint32_t j = 0, before = 0, nt = 0;
     for (; j < kMaxStages; ++j) {
       nt = (e.ctr[1 + j] + 63) >> 6;
@@ -640,27 +699,27 @@ __global__ void __launch_bounds__(64) k_deferred(Tab t, EvalBufs e) {
       before += nt;
     }
     if (j == kMaxStages) return;
-    const uint32_t off = (q - before) * 64u + threadIdx.x;
+    const uint32_t off = (q - before) * 64u + (threadIdx.x & 63u);
     if (off >= e.ctr[1 + j]) continue;
     const uint32_t slot = e.deferred[e.sstart[j] + off];
     const uint32_t M = e.meta[slot] >> 8;
     switch (kMaxStages - j) {
-      case 1: eval_one<1, true>(t, e, slot, M); break;
-      case 2: eval_one<2, true>(t, e, slot, M); break;
-      case 3: eval_one<3, true>(t, e, slot, M); break;
-      case 4: eval_one<4, true>(t, e, slot, M); break;
-      case 5: eval_one<5, true>(t, e, slot, M); break;
-      case 6: eval_one<6, true>(t, e, slot, M); break;
-      case 7: eval_one<7, true>(t, e, slot, M); break;
-      case 8: eval_one<8, true>(t, e, slot, M); break;
-      case 9: eval_one<9, true>(t, e, slot, M); break;
-      case 10: eval_one<10, true>(t, e, slot, M); break;
-      case 11: eval_one<11, true>(t, e, slot, M); break;
-      case 12: eval_one<12, true>(t, e, slot, M); break;
-      case 13: eval_one<13, true>(t, e, slot, M); break;
-      case 14: eval_one<14, true>(t, e, slot, M); break;
-      case 15: eval_one<15, true>(t, e, slot, M); break;
-      default: eval_one<16, true>(t, e, slot, M); break;
+      case 1: eval_one<1, true>(t, h, e, slot, M); break;
+      case 2: eval_one<2, true>(t, h, e, slot, M); break;
+      case 3: eval_one<3, true>(t, h, e, slot, M); break;
+      case 4: eval_one<4, true>(t, h, e, slot, M); break;
+      case 5: eval_one<5, true>(t, h, e, slot, M); break;
+      case 6: eval_one<6, true>(t, h, e, slot, M); break;
+      case 7: eval_one<7, true>(t, h, e, slot, M); break;
+      case 8: eval_one<8, true>(t, h, e, slot, M); break;
+      case 9: eval_one<9, true>(t, h, e, slot, M); break;
+      case 10: eval_one<10, true>(t, h, e, slot, M); break;
+      case 11: eval_one<11, true>(t, h, e, slot, M); break;
+      case 12: eval_one<12, true>(t, h, e, slot, M); break;
+      case 13: eval_one<13, true>(t, h, e, slot, M); break;
+      case 14: eval_one<14, true>(t, h, e, slot, M); break;
+      case 15: eval_one<15, true>(t, h, e, slot, M); break;
+      default: eval_one<16, true>(t, h, e, slot, M); break;
     }
   }
 }
@@ -679,7 +738,8 @@ __global__ void __launch_bounds__(64) k_redo_u64(Tab t, EvalBufs e) {
     const uint32_t m = e.meta[slot], S = m & 31, M = m >> 8;
     const Plan p = unpack(e.packed[slot >> 2]);
     StageRec R;
-    class_setup(t, p, slot & 3, R);
+    const Hot<2> h(t, nullptr);
+    class_setup(t, h, p, slot & 3, R);
     uint64_t r;
     switch (S) {
       case 1: r = redo_one<1>(R, M); break;
@@ -803,17 +863,25 @@ hipError_t launch_scatter(const uint32_t* meta, uint32_t nslots, uint32_t* curso
   return hipGetLastError();
 }
 // two waves per SIMD of the 16-stage code
-constexpr int kDeferredBlocks = 2048;
+constexpr int kDeferredBlocks = 512;
+
+template <int kMode>
+void launch_eval_mode(const Tab& t, const EvalBufs& e, uint32_t max_tasks, hipStream_t s) {
+  const int g = blocks_for(max_tasks, kEvalThreads) > 0 ? blocks_for(max_tasks, kEvalThreads) : 1;
+  const size_t lds = kMode < 2 ? t.lds_bytes : 0;
+  k_eval<0, kMode><<<g, kEvalThreads, lds, s>>>(t, e);
+  k_eval<1, kMode><<<g, kEvalThreads, lds, s>>>(t, e);
+  k_eval<2, kMode><<<g, kEvalThreads, lds, s>>>(t, e);
+  k_eval<3, kMode><<<g, kEvalThreads, lds, s>>>(t, e);
+  k_deferred<kMode><<<g < kDeferredBlocks ? g : kDeferredBlocks, kEvalThreads, lds, s>>>(t, e);
+}
 
 hipError_t launch_eval(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s) {
-  const int g = blocks_for(max_tasks, 64) > 0 ? blocks_for(max_tasks, 64) : 1;
   const EvalBufs e = {a.packed, a.meta, a.ids, a.sstart, a.out, a.ctr, a.ctr + kEvalCounters, a.deferred,
                       (unsigned long long*)a.skipped_ops};
-  k_eval<0><<<g, 64, 0, s>>>(t, e);
-  k_eval<1><<<g, 64, 0, s>>>(t, e);
-  k_eval<2><<<g, 64, 0, s>>>(t, e);
-  k_eval<3><<<g, 64, 0, s>>>(t, e);
-  k_deferred<<<g < kDeferredBlocks ? g : kDeferredBlocks, 64, 0, s>>>(t, e);
+  if (t.mode == 0) launch_eval_mode<0>(t, e, max_tasks, s);
+  else if (t.mode == 1) launch_eval_mode<1>(t, e, max_tasks, s);
+  else launch_eval_mode<2>(t, e, max_tasks, s);
   k_redo_u64<<<32, 64, 0, s>>>(t, e);
   return hipGetLastError();
 }

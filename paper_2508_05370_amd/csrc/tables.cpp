@@ -113,6 +113,43 @@ void build_rmax(const std::vector<uint32_t>& v, std::vector<uint32_t>* out, uint
   *levels = lv;
 }
 
+// Lay the setup tables out as the device image (see Tab).
+void build_image(HostTables* h) {
+  Tab& t = h->tab;
+  const uint32_t K = t.K, nm = t.n_mbs, L1 = t.L + 1;
+  t.nep = t.E ? 4 : 1;
+  auto a16 = [](size_t x) { return (uint32_t)((x + 15) & ~(size_t)15); };
+  const uint32_t n_pfb = K * 4 * nm * t.nep * L1;
+  t.o_pfb = a16((size_t)K * sizeof(TypeInfo));
+  t.o_emb = t.o_pfb + n_pfb * 16;
+  t.o_head = t.o_emb + K * nm * 16;
+  t.o_pa = t.o_head + K * 4 * nm * 16;
+  t.o_rmi = t.o_pa + a16(t.E ? (size_t)4 * nm * L1 * 8 : 0);
+  t.o_rmn = t.o_rmi + a16(h->rm_intra.size() * 4);
+  t.img_bytes = t.o_rmn + a16(h->rm_nic.size() * 4);
+  t.mode = t.img_bytes <= kLdsBudget ? 0 : t.o_rmn <= kLdsBudget ? 1 : 2;
+  t.lds_bytes = t.mode == 0 ? t.img_bytes : t.mode == 1 ? t.o_rmn : 0;
+  h->img.assign(t.img_bytes, 0);
+  uint8_t* b = h->img.data();
+  memcpy(b, h->ty.data(), K * sizeof(TypeInfo));
+  uint64_t* pfb = (uint64_t*)(b + t.o_pfb);
+  for (uint32_t k = 0; k < K; ++k)
+    for (uint32_t j = 0; j < 4; ++j)
+      for (uint32_t mi = 0; mi < nm; ++mi)
+        for (uint32_t g = 0; g < t.nep; ++g)
+          for (uint32_t l = 0; l < L1; ++l) {
+            const size_t src = ((((size_t)k * 4 + j) * nm + mi) * 4 + g) * L1 + l;
+            const size_t dst = ((((size_t)k * 4 + j) * nm + mi) * t.nep + g) * L1 + l;
+            pfb[2 * dst] = h->pf[src];
+            pfb[2 * dst + 1] = h->pb[src];
+          }
+  memcpy(b + t.o_emb, h->emb.data(), h->emb.size() * 8);
+  memcpy(b + t.o_head, h->head.data(), h->head.size() * 8);
+  if (t.E) memcpy(b + t.o_pa, h->pa.data(), h->pa.size() * 8);
+  memcpy(b + t.o_rmi, h->rm_intra.data(), h->rm_intra.size() * 4);
+  memcpy(b + t.o_rmn, h->rm_nic.data(), h->rm_nic.size() * 4);
+}
+
 }  // namespace
 
 int build_tables(const sim_model_desc* md, const sim_cluster_desc* cd, HostTables* out) {
@@ -354,6 +391,7 @@ int build_tables(const sim_model_desc* md, const sim_cluster_desc* cd, HostTable
   if (node_max >= ((u128)1 << 52) || dp_max >= ((u128)1 << 52)) return RNG;
   u128 total = (u128)md->global_batch * kMaxStages * node_max + dp_max;
   if (total >= kLimit) return RNG;
+  build_image(out);
   return SIM_OK;
 }
 
