@@ -181,11 +181,16 @@ int sim_best_reduce(sim_ctx* ctx, const sim_best* bests, int64_t n, sim_best* ou
 
 /*
  * Kernel timing for measurement.  When enabled, sim_eval_plans records a
- * HIP event pair on its stream around every launch of its evaluation and
- * plan-check kernels and around the whole call; sim_get_timing synchronises those events and
- * returns the accumulated milliseconds and launch counts, then clears them.
- * kind 0 = evaluation kernel (per-pipeline setup and 1F1B recurrence),
- * 1 = plan check/pack kernel, 2 = whole sim_eval_plans call.
+ * HIP event pair around each chunk's kernels of one kind and around the
+ * whole call; sim_get_timing synchronises those events and returns the
+ * accumulated milliseconds and pair counts, then clears them.
+ * kind 0 = first evaluation pass (per-pipeline setup and 1F1B recurrence
+ * with the periodic shortcut), 1 = plan check/pack kernel, 2 = whole
+ * sim_eval_plans call, 3 = deferred pass (full-loop pipelines and the u64
+ * redo).  A call of more than 2^21 plans works in chunks of 2^21 and runs
+ * each chunk's deferred pass on a second stream of the context, overlapped
+ * with the next chunk; the call's stream waits for it before the call's
+ * work is complete, so kinds 0 and 3 may overlap in time.
  */
 int sim_set_timing(sim_ctx* ctx, int enable);
 int sim_get_timing(sim_ctx* ctx, int kind, double* total_ms, int64_t* launches);

@@ -18,7 +18,8 @@ hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint32_t*
                          hipStream_t s);
 hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* sstart, hipStream_t s);
 hipError_t launch_scatter(const uint32_t* meta, uint32_t nslots, uint32_t* cursor, uint32_t* ids, hipStream_t s);
-hipError_t launch_eval(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s);
+hipError_t launch_first(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s);
+hipError_t launch_deferred(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s);
 hipError_t launch_argmin(const uint64_t* t, int64_t n, int64_t base, sim_best* b, hipStream_t s);
 hipError_t launch_best_reduce(const sim_best* in, int64_t n, sim_best* out, hipStream_t s);
 }  // namespace hetsim
@@ -41,8 +42,9 @@ struct sim_ctx {
   hipMemPool_t pool;   // stream-ordered pool for per-call workspace
   std::mutex mu;
   bool timing;
-  std::vector<EventPair> ev[3];
+  std::vector<EventPair> ev[4];
   uint64_t* skipped_ops;   // device counter, inside `tables`
+  hipStream_t aux;         // deferred passes of multi-chunk calls, created on first use
 };
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -71,6 +73,7 @@ extern "C" int sim_create(const sim_model_desc* model, const sim_cluster_desc* c
   c->timing = false;
   c->tables = nullptr;
   c->pool = nullptr;
+  c->aux = nullptr;
   if (hipGetDevice(&c->device) != hipSuccess) { delete ht; delete c; return SIM_EHIP; }
   // the table image, then the skipped-work counter
   const size_t img = align256(ht->img.size());
@@ -100,6 +103,7 @@ extern "C" void sim_destroy(sim_ctx* c) {
   for (auto& v : c->ev)
     for (auto& e : v) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }
   (void)hipDeviceSynchronize();
+  if (c->aux) (void)hipStreamDestroy(c->aux);
   if (c->pool) (void)hipMemPoolDestroy(c->pool);
   if (c->tables) (void)hipFree(c->tables);
   delete c;
@@ -149,38 +153,91 @@ static Work carve(void* base, int64_t ch) {
   return w;
 }
 
+static hipStream_t aux_stream(sim_ctx* c) {
+  std::lock_guard<std::mutex> g(c->mu);
+  if (!c->aux && hipStreamCreateWithFlags(&c->aux, hipStreamNonBlocking) != hipSuccess) c->aux = nullptr;
+  return c->aux;
+}
+
+// Chunks of kChunk plans.  With more than one chunk, the deferred pass of
+// chunk i runs on the context's second stream while the main stream packs
+// and evaluates chunk i + 1; the two workspaces alternate, and the main
+// stream waits for the deferred pass of chunk i before reusing its
+// workspace for chunk i + 2 and, at the end, for the last one.
 extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uint64_t* out, void* stream) {
   if (!c || !plans_ok(plans, n) || (n > 0 && !out)) return SIM_EINVAL;
   if (n == 0) return SIM_OK;
   hipStream_t s = (hipStream_t)stream;
   if (hipSetDevice(c->device) != hipSuccess) return SIM_EHIP;
   const int64_t ch = n < kChunk ? n : kChunk;
+  const int nbuf = n > ch ? 2 : 1;
+  hipStream_t aux = s;
+  hipEvent_t ready[2] = {nullptr, nullptr}, done[2] = {nullptr, nullptr};
+  if (nbuf == 2) {
+    aux = aux_stream(c);
+    if (!aux) return SIM_EHIP;
+    for (int j = 0; j < 2; ++j)
+      if (hipEventCreateWithFlags(&ready[j], hipEventDisableTiming) != hipSuccess ||
+          hipEventCreateWithFlags(&done[j], hipEventDisableTiming) != hipSuccess) {
+        for (int q = 0; q < 2; ++q) {
+          if (ready[q]) (void)hipEventDestroy(ready[q]);
+          if (done[q]) (void)hipEventDestroy(done[q]);
+        }
+        return SIM_EHIP;
+      }
+  }
   void* ws = nullptr;
-  if (hipMallocFromPoolAsync(&ws, work_bytes(ch), c->pool, s) != hipSuccess) return SIM_ENOMEM;
-  Work w = carve(ws, ch);
+  hipError_t e = hipMallocFromPoolAsync(&ws, nbuf * work_bytes(ch), c->pool, s);
+  if (e != hipSuccess) ws = nullptr;
+  Work w[2];
+  for (int j = 0; ws && j < nbuf; ++j) w[j] = carve((char*)ws + j * work_bytes(ch), ch);
   EventPair call, ev;
-  bool tcall = begin_event(c, 2, s, &call);
-  hipError_t e = hipSuccess;
-  for (int64_t off = 0; off < n && e == hipSuccess; off += ch) {
+  bool tcall = ws && begin_event(c, 2, s, &call);
+  bool joined = true;
+  int64_t i = 0;
+  for (int64_t off = 0; ws && off < n && e == hipSuccess; off += ch, ++i) {
     const int64_t cn = n - off < ch ? n - off : ch;
+    const Work& W = w[i % nbuf];
     sim_plans p = *plans;
     p.hdr += off; p.cut += off; p.cls += off; p.types += off;
-    e = launch_fill32(w.hist, kCounters, 0, s);
+    if (i >= 2) e = hipStreamWaitEvent(s, done[i % 2], 0);
+    if (e == hipSuccess) e = launch_fill32(W.hist, kCounters, 0, s);
     bool t1 = e == hipSuccess && begin_event(c, 1, s, &ev);
-    if (e == hipSuccess) e = launch_prep(c->tab, p, cn, out + off, w.packed, w.meta, w.hist, s);
+    if (e == hipSuccess) e = launch_prep(c->tab, p, cn, out + off, W.packed, W.meta, W.hist, s);
     if (t1) end_event(c, 1, s, &ev);
-    if (e == hipSuccess) e = launch_scan(w.hist, w.cursor, w.sstart, s);
-    if (e == hipSuccess) e = launch_scatter(w.meta, (uint32_t)(cn * 4), w.cursor, w.ids, s);
+    if (e == hipSuccess) e = launch_scan(W.hist, W.cursor, W.sstart, s);
+    if (e == hipSuccess) e = launch_scatter(W.meta, (uint32_t)(cn * 4), W.cursor, W.ids, s);
+    const EvalArgs a = {W.packed, W.meta, W.ids, W.sstart, out + off, W.ctr, W.deferred,
+                        c->timing ? c->skipped_ops : nullptr};
     bool t0 = e == hipSuccess && begin_event(c, 0, s, &ev);
-    if (e == hipSuccess) {
-      const EvalArgs a = {w.packed, w.meta, w.ids, w.sstart, out + off, w.ctr, w.deferred,
-                          c->timing ? c->skipped_ops : nullptr};
-      e = launch_eval(c->tab, a, (uint32_t)(cn * 4), s);
-    }
+    if (e == hipSuccess) e = launch_first(c->tab, a, (uint32_t)(cn * 4), s);
     if (t0) end_event(c, 0, s, &ev);
+    if (e == hipSuccess && nbuf == 2) {
+      e = hipEventRecord(ready[i % 2], s);
+      if (e == hipSuccess) e = hipStreamWaitEvent(aux, ready[i % 2], 0);
+    }
+    if (e != hipSuccess) break;
+    joined = nbuf == 1;
+    bool t3 = begin_event(c, 3, aux, &ev);
+    e = launch_deferred(c->tab, a, (uint32_t)(cn * 4), aux);
+    if (t3) end_event(c, 3, aux, &ev);
+    if (nbuf == 2) {
+      const hipError_t r = hipEventRecord(done[i % 2], aux);
+      if (e == hipSuccess) e = r;
+    }
+  }
+  // the main stream takes over everything the second stream was given
+  if (!joined) {
+    const hipError_t r = hipStreamWaitEvent(s, done[(i - 1) % 2], 0);
+    if (e == hipSuccess) e = r;
   }
   if (tcall) end_event(c, 2, s, &call);
-  (void)hipFreeAsync(ws, s);
+  if (ws) (void)hipFreeAsync(ws, s);
+  for (int j = 0; j < 2; ++j) {
+    if (ready[j]) (void)hipEventDestroy(ready[j]);
+    if (done[j]) (void)hipEventDestroy(done[j]);
+  }
+  if (!ws) return SIM_ENOMEM;
   return e == hipSuccess ? SIM_OK : SIM_EHIP;
 }
 
@@ -233,7 +290,7 @@ extern "C" int sim_get_skipped_ops(sim_ctx* c, uint64_t* ops) {
 }
 
 extern "C" int sim_get_timing(sim_ctx* c, int kind, double* total_ms, int64_t* launches) {
-  if (!c || kind < 0 || kind > 2 || !total_ms || !launches) return SIM_EINVAL;
+  if (!c || kind < 0 || kind > 3 || !total_ms || !launches) return SIM_EINVAL;
   std::vector<EventPair> v;
   {
     std::lock_guard<std::mutex> g(c->mu);

@@ -866,22 +866,38 @@ hipError_t launch_scatter(const uint32_t* meta, uint32_t nslots, uint32_t* curso
 constexpr int kDeferredBlocks = 512;
 
 template <int kMode>
-void launch_eval_mode(const Tab& t, const EvalBufs& e, uint32_t max_tasks, hipStream_t s) {
+void launch_first_mode(const Tab& t, const EvalBufs& e, uint32_t max_tasks, hipStream_t s) {
   const int g = blocks_for(max_tasks, kEvalThreads) > 0 ? blocks_for(max_tasks, kEvalThreads) : 1;
   const size_t lds = kMode < 2 ? t.lds_bytes : 0;
   k_eval<0, kMode><<<g, kEvalThreads, lds, s>>>(t, e);
   k_eval<1, kMode><<<g, kEvalThreads, lds, s>>>(t, e);
   k_eval<2, kMode><<<g, kEvalThreads, lds, s>>>(t, e);
   k_eval<3, kMode><<<g, kEvalThreads, lds, s>>>(t, e);
-  k_deferred<kMode><<<g < kDeferredBlocks ? g : kDeferredBlocks, kEvalThreads, lds, s>>>(t, e);
 }
 
-hipError_t launch_eval(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s) {
-  const EvalBufs e = {a.packed, a.meta, a.ids, a.sstart, a.out, a.ctr, a.ctr + kEvalCounters, a.deferred,
-                      (unsigned long long*)a.skipped_ops};
-  if (t.mode == 0) launch_eval_mode<0>(t, e, max_tasks, s);
-  else if (t.mode == 1) launch_eval_mode<1>(t, e, max_tasks, s);
-  else launch_eval_mode<2>(t, e, max_tasks, s);
+static EvalBufs bufs(const EvalArgs& a) {
+  return {a.packed, a.meta, a.ids, a.sstart, a.out, a.ctr, a.ctr + kEvalCounters, a.deferred,
+          (unsigned long long*)a.skipped_ops};
+}
+
+// first pass over a chunk: k_eval of each stage-count group
+hipError_t launch_first(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s) {
+  const EvalBufs e = bufs(a);
+  if (t.mode == 0) launch_first_mode<0>(t, e, max_tasks, s);
+  else if (t.mode == 1) launch_first_mode<1>(t, e, max_tasks, s);
+  else launch_first_mode<2>(t, e, max_tasks, s);
+  return hipGetLastError();
+}
+
+// then the deferred pipelines and the u64 redo of the overflowed ones
+hipError_t launch_deferred(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s) {
+  const EvalBufs e = bufs(a);
+  int g = blocks_for(max_tasks, kEvalThreads);
+  g = g < 1 ? 1 : (g > kDeferredBlocks ? kDeferredBlocks : g);
+  const size_t lds = t.mode < 2 ? t.lds_bytes : 0;
+  if (t.mode == 0) k_deferred<0><<<g, kEvalThreads, lds, s>>>(t, e);
+  else if (t.mode == 1) k_deferred<1><<<g, kEvalThreads, lds, s>>>(t, e);
+  else k_deferred<2><<<g, kEvalThreads, 0, s>>>(t, e);
   k_redo_u64<<<32, 64, 0, s>>>(t, e);
   return hipGetLastError();
 }

@@ -305,3 +305,24 @@ def test_link_bound_schedules(torch, B, oracle_mod, workloads, slow):
                     aperiodic += 1
         say("  aperiodic pipelines in the first 300 plans: %d" % aperiodic)
         assert aperiodic > 0
+
+
+def test_concurrent_multichunk_calls(torch, B, workloads):
+    """Calls of several internal chunks (their deferred passes overlap on the
+    context's second stream) issued concurrently on two streams of one
+    context give the results of the same calls made one at a time."""
+    w = workloads.workload(3)
+    n = 4_500_001                                     # three internal chunks, the last ragged
+    p = workloads.plans(w, 1_000_000, n)
+    sim = B.Sim(w["model"], w["cluster"])
+    dp = B.device_plans(p)
+    say("case: workload 3, two concurrent calls of %d plans" % n)
+    ref = sim.eval_plans(dp)
+    torch.cuda.synchronize()
+    outs = [torch.empty(n, dtype=torch.int64, device="cuda") for _ in range(2)]
+    streams = [torch.cuda.Stream() for _ in range(2)]
+    for k in range(2):
+        sim.eval_plans(dp, out=outs[k], stream=streams[k])
+    torch.cuda.synchronize()
+    for k in range(2):
+        assert torch.equal(outs[k], ref), k
