@@ -206,7 +206,7 @@ int sim_get_timing(sim_ctx* ctx, int kind, double* total_ms, int64_t* launches);
  * s * (6 (S - 1) + 2) VALU ops, the cost of S forward and S backward nodes
  * at 3 ops per node (1 for a node without a cross-stage input).
  * sim_get_skipped_ops synchronises the device, writes the sum to *ops (host
- * memory) and clears it; enabling timing also clears it.
+ * memory) and clears it (it starts at zero).
  */
 int sim_get_skipped_ops(sim_ctx* ctx, uint64_t* ops);
 

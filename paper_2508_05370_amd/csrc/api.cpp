@@ -48,6 +48,7 @@ struct sim_ctx {
 };
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+constexpr size_t kSkipBytes = (size_t)kSkipSlots * kSkipStride * 8;
 
 extern "C" const char* sim_strerror(int code) {
   switch (code) {
@@ -75,12 +76,11 @@ extern "C" int sim_create(const sim_model_desc* model, const sim_cluster_desc* c
   c->pool = nullptr;
   c->aux = nullptr;
   if (hipGetDevice(&c->device) != hipSuccess) { delete ht; delete c; return SIM_EHIP; }
-  // the table image, then the skipped-work counter
+  // the table image, then the skipped-work counter slots
   const size_t img = align256(ht->img.size());
-  if (hipMalloc(&c->tables, img + 256) != hipSuccess) { delete ht; delete c; return SIM_ENOMEM; }
-  const uint64_t zero = 0;
+  if (hipMalloc(&c->tables, img + kSkipBytes) != hipSuccess) { delete ht; delete c; return SIM_ENOMEM; }
   if (hipMemcpy(c->tables, ht->img.data(), ht->img.size(), hipMemcpyHostToDevice) != hipSuccess ||
-      hipMemcpy((char*)c->tables + img, &zero, 8, hipMemcpyHostToDevice) != hipSuccess) {
+      hipMemset((char*)c->tables + img, 0, kSkipBytes) != hipSuccess) {
     (void)hipFree(c->tables); delete ht; delete c; return SIM_EHIP;
   }
   c->tab.img = c->tables;
@@ -272,20 +272,20 @@ extern "C" int sim_best_reduce(sim_ctx* c, const sim_best* in, int64_t n, sim_be
 
 extern "C" int sim_set_timing(sim_ctx* c, int enable) {
   if (!c) return SIM_EINVAL;
-  if (enable && !c->timing) {
-    if (hipSetDevice(c->device) != hipSuccess || hipMemset(c->skipped_ops, 0, 8) != hipSuccess)
-      return SIM_EHIP;
-  }
   c->timing = enable != 0;
   return SIM_OK;
 }
 
 extern "C" int sim_get_skipped_ops(sim_ctx* c, uint64_t* ops) {
   if (!c || !ops) return SIM_EINVAL;
+  std::vector<uint64_t> v((size_t)kSkipSlots * kSkipStride);
   if (hipSetDevice(c->device) != hipSuccess || hipDeviceSynchronize() != hipSuccess ||
-      hipMemcpy(ops, c->skipped_ops, 8, hipMemcpyDeviceToHost) != hipSuccess ||
-      hipMemset(c->skipped_ops, 0, 8) != hipSuccess)
+      hipMemcpy(v.data(), c->skipped_ops, kSkipBytes, hipMemcpyDeviceToHost) != hipSuccess ||
+      hipMemset(c->skipped_ops, 0, kSkipBytes) != hipSuccess)
     return SIM_EHIP;
+  uint64_t sum = 0;
+  for (uint32_t j = 0; j < kSkipSlots; ++j) sum += v[(size_t)j * kSkipStride];
+  *ops = sum;
   return SIM_OK;
 }
 

@@ -82,6 +82,9 @@ struct Tab {
 // ctr[1 + 16 - S] the S-stage pipelines deferred to the full-loop pass; the
 // overflow list follows the counters at ctr + kEvalCounters.
 constexpr uint32_t kEvalCounters = 32;
+// The skipped-work counter is spread over slots on separate cache lines so
+// that the waves of a launch do not serialise on one address.
+constexpr uint32_t kSkipSlots = 512, kSkipStride = 16;
 struct EvalArgs {
   const PackedPlan* packed;
   const uint32_t* meta;
@@ -90,7 +93,7 @@ struct EvalArgs {
   uint64_t* out;
   uint32_t* ctr;
   uint32_t* deferred;          // as long as ids
-  uint64_t* skipped_ops;       // optional
+  uint64_t* skipped_ops;       // optional: kSkipSlots counters, kSkipStride words apart
 };
 
 // Host side: validate descriptors and build the tables (host copies).

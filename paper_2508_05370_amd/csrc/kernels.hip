@@ -644,7 +644,8 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
     e.ovf[atomicAdd(&e.ctr[0], 1u)] = slot;
   }
   if (e.skipped_ops && skipped > 0)
-    atomicAdd(e.skipped_ops, (unsigned long long)skipped * (unsigned long long)(6 * (S - 1) + 2));
+    atomicAdd(e.skipped_ops + ((blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) % kSkipSlots) * kSkipStride,
+              (unsigned long long)skipped * (unsigned long long)(6 * (S - 1) + 2));
 }
 
 // Blocks of four waves share one LDS copy of the table image.
