@@ -84,6 +84,7 @@ extern "C" int sim_create(const sim_model_desc* model, const sim_cluster_desc* c
     (void)hipFree(c->tables); delete ht; delete c; return SIM_EHIP;
   }
   c->tab.img = c->tables;
+  if (eval_grids(&c->tab) != 0) { (void)hipFree(c->tables); delete ht; delete c; return SIM_EHIP; }
   c->skipped_ops = (uint64_t*)((char*)c->tables + img);
   delete ht;
   hipMemPoolProps props;

@@ -74,6 +74,8 @@ struct Tab {
   uint32_t lds_bytes;             // prefix copied to LDS: img_bytes, o_rmn or 0 by mode
   uint32_t mode;
   const void* img;                // the image in device memory (16-byte aligned)
+  uint32_t grid_eval[4];          // blocks of each first-pass kernel that fit the device at once
+  uint32_t grid_deferred;
 };
 
 // Device buffers of one evaluation pass over a chunk, as the host hands them
@@ -105,6 +107,10 @@ struct HostTables {
   std::vector<TypeInfo> ty;
   std::vector<uint8_t> img;       // the device image built from the above
 };
+
+// Blocks of each evaluation kernel that fit the current device at once (they
+// size the capped grids).  Returns a HIP error code.
+int eval_grids(Tab* t);
 
 // Returns 0 (SIM_OK), SIM_EINVAL or SIM_ERANGE.
 int build_tables(const sim_model_desc* model, const sim_cluster_desc* cluster, HostTables* out);

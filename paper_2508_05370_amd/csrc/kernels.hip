@@ -651,32 +651,37 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
 // Blocks of four waves share one LDS copy of the table image.
 constexpr uint32_t kEvalThreads = 256;
 
+// The grid is capped at a few times the blocks that fit at once (a launch
+// over the whole chunk would mostly start blocks past the group's range,
+// each holding a full LDS allocation); the waves of the grid take the
+// group's 64-pipeline tiles in a fixed stride, heaviest tiles first.
 template <int GRP, int kMode>
 __global__ void __launch_bounds__(kEvalThreads) k_eval(Tab t, EvalBufs e) {
   constexpr int kTop = kMaxStages - 4 * GRP;   // stage counts kTop-3 .. kTop
   extern __shared__ uint4 lds[];
   const uint32_t lo = e.sstart[4 * GRP], hi = e.sstart[4 * GRP + 4];
-  const uint32_t first = lo + blockIdx.x * kEvalThreads;
-  if (first >= hi) return;   // the whole block, before any barrier
+  if (lo + blockIdx.x * kEvalThreads >= hi) return;   // the whole block, before any barrier
   fill_lds<kMode>(t, lds);
   const Hot<kMode> h(t, lds);
-  const uint32_t pos = first + threadIdx.x;
-  if (first + (threadIdx.x & ~63u) >= hi) return;
-  bool pending = pos < hi;
-  const uint32_t slot = pending ? e.ids[pos] : 0;
-  const uint32_t m = pending ? e.meta[slot] : 0;
-  const uint32_t S = m & 31, M = m >> 8;
-  // one pass per distinct stage count present in the wavefront (usually one)
-  while (true) {
-    const uint64_t live = __ballot(pending);
-    if (!live) break;
-    const uint32_t S0 = __builtin_amdgcn_readfirstlane(__shfl(S, __ffsll((unsigned long long)live) - 1));
-    if (pending && S == S0) {
-      if (S0 == kTop) eval_one<kTop, false>(t, h, e, slot, M);
-      else if (S0 == kTop - 1) eval_one<kTop - 1, false>(t, h, e, slot, M);
-      else if (S0 == kTop - 2) eval_one<kTop - 2, false>(t, h, e, slot, M);
-      else eval_one<kTop - 3, false>(t, h, e, slot, M);
-      pending = false;
+  const uint32_t stride = gridDim.x * kEvalThreads;
+  for (uint32_t base = lo + blockIdx.x * kEvalThreads + (threadIdx.x & ~63u); base < hi; base += stride) {
+    const uint32_t pos = base + (threadIdx.x & 63u);
+    bool pending = pos < hi;
+    const uint32_t slot = pending ? e.ids[pos] : 0;
+    const uint32_t m = pending ? e.meta[slot] : 0;
+    const uint32_t S = m & 31, M = m >> 8;
+    // one pass per distinct stage count present in the wavefront (usually one)
+    while (true) {
+      const uint64_t live = __ballot(pending);
+      if (!live) break;
+      const uint32_t S0 = __builtin_amdgcn_readfirstlane(__shfl(S, __ffsll((unsigned long long)live) - 1));
+      if (pending && S == S0) {
+        if (S0 == kTop) eval_one<kTop, false>(t, h, e, slot, M);
+        else if (S0 == kTop - 1) eval_one<kTop - 1, false>(t, h, e, slot, M);
+        else if (S0 == kTop - 2) eval_one<kTop - 2, false>(t, h, e, slot, M);
+        else eval_one<kTop - 3, false>(t, h, e, slot, M);
+        pending = false;
+      }
     }
   }
 }
@@ -863,17 +868,41 @@ hipError_t launch_scatter(const uint32_t* meta, uint32_t nslots, uint32_t* curso
   k_scatter<<<blocks_for(nslots, 256 * kScatterPer), 256, 0, s>>>(meta, nslots, cursor, ids);
   return hipGetLastError();
 }
-// two waves per SIMD of the 16-stage code
-constexpr int kDeferredBlocks = 512;
-
 template <int kMode>
 void launch_first_mode(const Tab& t, const EvalBufs& e, uint32_t max_tasks, hipStream_t s) {
-  const int g = blocks_for(max_tasks, kEvalThreads) > 0 ? blocks_for(max_tasks, kEvalThreads) : 1;
+  const int nb = blocks_for(max_tasks, kEvalThreads);
+  const uint32_t need = nb > 0 ? (uint32_t)nb : 1;
   const size_t lds = kMode < 2 ? t.lds_bytes : 0;
-  k_eval<0, kMode><<<g, kEvalThreads, lds, s>>>(t, e);
-  k_eval<1, kMode><<<g, kEvalThreads, lds, s>>>(t, e);
-  k_eval<2, kMode><<<g, kEvalThreads, lds, s>>>(t, e);
-  k_eval<3, kMode><<<g, kEvalThreads, lds, s>>>(t, e);
+  auto grid = [&](int g) { return 4 * t.grid_eval[g] < need ? 4 * t.grid_eval[g] : need; };
+  k_eval<0, kMode><<<grid(0), kEvalThreads, lds, s>>>(t, e);
+  k_eval<1, kMode><<<grid(1), kEvalThreads, lds, s>>>(t, e);
+  k_eval<2, kMode><<<grid(2), kEvalThreads, lds, s>>>(t, e);
+  k_eval<3, kMode><<<grid(3), kEvalThreads, lds, s>>>(t, e);
+}
+
+template <int kMode>
+static int grids_mode(Tab* t) {
+  int cus = 0, dev = 0;
+  hipError_t r = hipGetDevice(&dev);
+  if (r == hipSuccess) r = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (r != hipSuccess) return (int)r;
+  const size_t lds = kMode < 2 ? t->lds_bytes : 0;
+  const void* k[5] = {(const void*)k_eval<0, kMode>, (const void*)k_eval<1, kMode>, (const void*)k_eval<2, kMode>,
+                      (const void*)k_eval<3, kMode>, (const void*)k_deferred<kMode>};
+  uint32_t g[5];
+  for (int i = 0; i < 5; ++i) {
+    int nb = 0;
+    r = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k[i], kEvalThreads, lds);
+    if (r != hipSuccess) return (int)r;
+    g[i] = (uint32_t)((nb > 0 ? nb : 1) * cus);
+  }
+  for (int i = 0; i < 4; ++i) t->grid_eval[i] = g[i];
+  t->grid_deferred = g[4];
+  return 0;
+}
+
+int eval_grids(Tab* t) {
+  return t->mode == 0 ? grids_mode<0>(t) : t->mode == 1 ? grids_mode<1>(t) : grids_mode<2>(t);
 }
 
 static EvalBufs bufs(const EvalArgs& a) {
@@ -894,7 +923,7 @@ hipError_t launch_first(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hip
 hipError_t launch_deferred(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s) {
   const EvalBufs e = bufs(a);
   int g = blocks_for(max_tasks, kEvalThreads);
-  g = g < 1 ? 1 : (g > kDeferredBlocks ? kDeferredBlocks : g);
+  g = g < 1 ? 1 : (g > (int)t.grid_deferred ? (int)t.grid_deferred : g);
   const size_t lds = t.mode < 2 ? t.lds_bytes : 0;
   if (t.mode == 0) k_deferred<0><<<g, kEvalThreads, lds, s>>>(t, e);
   else if (t.mode == 1) k_deferred<1><<<g, kEvalThreads, lds, s>>>(t, e);
