@@ -275,9 +275,52 @@ __device__ __forceinline__ uint32_t placed_before(const Plan& p, uint32_t c, uin
   return below + rc * count_type(tc, k, (1ull << (4 * s)) - 1);
 }
 
+// DP sync of stage s (layers [lo, hi), ns = hi - lo) over every replica of
+// every class: one ring across all replicas on the slowest NIC of the
+// participating devices, or inside one node when every replica of the stage
+// sits in the same node; MoE models add the expert ring over the EP-sized
+// groups.  The same for every class of the plan.
 template <int kMode>
-__device__ void class_setup(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t c,
-                            uint64_t (&rec)[kMaxStages][kRecWords]) {
+__device__ __forceinline__ uint64_t stage_dp(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t s,
+                                             uint32_t ns, double rp, double rpe) {
+  if (p.psum <= 1) return 0;
+  const uint32_t G = p.G, tp = p.tp, tpl = p.tpl, epl = p.epl, S = p.S;
+  bool same = true;
+  uint32_t k0 = 0, nmin = 0xffffffffu, nmax = 0, bq_dp = 0;
+  uint64_t a_dp = 0;
+#pragma unroll
+  for (uint32_t c2 = 0; c2 < 4; ++c2) {
+    if (c2 >= G) continue;
+    const uint32_t k2 = (uint32_t)(p.tv[c2] >> (4 * s)) & 15;
+    const TypeInfo t2 = h.type(k2);
+    const uint32_t b2 = placed_before(p, c2, s, k2) * tp, n2 = p.reps[c2] * tp, d2 = t2.dpl;
+    const uint32_t l2 = t2.node_off + (b2 >> d2), h2 = t2.node_off + ((b2 + n2 - 1) >> d2);
+    const uint32_t dl2 = t2.dev_off + b2;
+    const uint32_t nic2 = range_max(h.rmn, t.D, dl2, dl2 + n2 - 1);
+    if (c2 == 0) k0 = k2; else same = same && k2 == k0;
+    nmin = l2 < nmin ? l2 : nmin;
+    nmax = h2 > nmax ? h2 : nmax;
+    const uint32_t bx = nic2 > t2.bq_pcie ? nic2 : t2.bq_pcie;
+    bq_dp = bx > bq_dp ? bx : bq_dp;
+    a_dp = 2 * t2.a_side > a_dp ? 2 * t2.a_side : a_dp;
+  }
+  const bool intra = same && nmin == nmax;
+  const uint64_t alpha = intra ? h.type(k0).a_intra : a_dp;
+  const uint32_t bq = intra ? h.rmi()[nmin] : bq_dp;
+  const uint64_t pd = (uint64_t)ns * t.par_layer[tpl] + (s == 0 ? t.par_embed[tpl] : 0) +
+                      (s == S - 1 ? t.par_head[tpl] : 0);
+  uint64_t tdp = ring_sync(p.psum, rp, p.zero, t.grad_bytes * pd, t.param_bytes * pd, alpha, bq);
+  const uint32_t pe = p.psum >> epl;
+  if (t.E && pe > 1) {
+    const uint64_t px = (uint64_t)ns * t.par_expert[tpl][epl];
+    tdp += ring_sync(pe, rpe, p.zero, t.grad_bytes * px, t.param_bytes * px, alpha, bq);
+  }
+  return tdp;
+}
+
+template <int kMode, typename Sink>
+__device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t c,
+                                            Sink& sink) {
   const uint32_t S = p.S, G = p.G, tp = p.tp, ep = p.ep, tpl = p.tpl, epl = p.epl, mi = p.mi;
   const uint64_t act = t.act[mi], act_tp = (act + tp - 1) >> tpl;
   const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> epl);
@@ -324,8 +367,7 @@ __device__ void class_setup(const Tab& t, const Hot<kMode>& h, const Plan& p, ui
       fc += e;
       bc += e;
     }
-    rec[s][0] = fc;
-    rec[s][1] = bc;
+    uint64_t hop = 0;
     if (s > 0) {  // hop (s-1) -> s
       // same pool means the two ranges are adjacent: intra iff the pair spans one node
       const bool intra = pk == k && (pbase >> dpl) == ((pbase + (2 * reps - 1) * tp) >> dpl);
@@ -338,47 +380,74 @@ __device__ void class_setup(const Tab& t, const Hot<kMode>& h, const Plan& p, ui
         const uint32_t b = pti.bq_pcie > ti.bq_pcie ? pti.bq_pcie : ti.bq_pcie;
         bq = a > b ? a : b;
       }
-      rec[s - 1][2] = alpha + link_ps(act, bq);
+      hop = alpha + link_ps(act, bq);
     }
     pk = k; pbase = base; pnic = bq_nic; pin = bq_in; pti = ti;
-    // ---- DP sync of this stage over every replica of every class
-    uint64_t tdp = 0;
-    if (p.psum > 1) {
-      bool same = true;
-      uint32_t k0 = 0, nmin = 0xffffffffu, nmax = 0, bq_dp = 0;
-      uint64_t a_dp = 0;
-#pragma unroll
-      for (uint32_t c2 = 0; c2 < 4; ++c2) {
-        if (c2 >= G) continue;
-        const uint32_t k2 = (uint32_t)(p.tv[c2] >> (4 * s)) & 15;
-        const TypeInfo t2 = h.type(k2);
-        const uint32_t b2 = placed_before(p, c2, s, k2) * tp, n2 = p.reps[c2] * tp, d2 = t2.dpl;
-        const uint32_t l2 = t2.node_off + (b2 >> d2), h2 = t2.node_off + ((b2 + n2 - 1) >> d2);
-        const uint32_t dl2 = t2.dev_off + b2;
-        const uint32_t nic2 = range_max(h.rmn, t.D, dl2, dl2 + n2 - 1);
-        if (c2 == 0) k0 = k2; else same = same && k2 == k0;
-        nmin = l2 < nmin ? l2 : nmin;
-        nmax = h2 > nmax ? h2 : nmax;
-        const uint32_t bx = nic2 > t2.bq_pcie ? nic2 : t2.bq_pcie;
-        bq_dp = bx > bq_dp ? bx : bq_dp;
-        a_dp = 2 * t2.a_side > a_dp ? 2 * t2.a_side : a_dp;
-      }
-      const bool intra = same && nmin == nmax;
-      const uint64_t alpha = intra ? h.type(k0).a_intra : a_dp;
-      const uint32_t bq = intra ? h.rmi()[nmin] : bq_dp;
-      const uint64_t pd = (uint64_t)ns * t.par_layer[tpl] + (s == 0 ? t.par_embed[tpl] : 0) +
-                          (s == S - 1 ? t.par_head[tpl] : 0);
-      tdp = ring_sync(p.psum, rp, p.zero, t.grad_bytes * pd, t.param_bytes * pd, alpha, bq);
-      const uint32_t pe = p.psum >> epl;
-      if (t.E && pe > 1) {
-        const uint64_t px = (uint64_t)ns * t.par_expert[tpl][epl];
-        tdp += ring_sync(pe, rpe, p.zero, t.grad_bytes * px, t.param_bytes * px, alpha, bq);
-      }
-    }
-    rec[s][3] = tdp;
+    // ---- DP sync of this stage (the sink may leave it for later)
+    const uint64_t tdp = Sink::kDp ? stage_dp(t, h, p, s, ns, rp, rpe) : 0;
+    sink.put(s, fc, bc, hop, tdp);
     lo = hi;
   }
-  rec[S - 1][2] = 0;
+}
+
+// Sinks of class_setup.  RecSink stores whole stage records in memory order
+// (the hop of the last stage is 0).
+struct RecSink {
+  static constexpr bool kDp = true;
+  uint64_t (&rec)[kMaxStages][kRecWords];
+  __device__ __forceinline__ void put(uint32_t s, uint64_t fc, uint64_t bc, uint64_t hop, uint64_t tdp) {
+    rec[s][0] = fc;
+    rec[s][1] = bc;
+    rec[s][2] = 0;
+    rec[s][3] = tdp;
+    if (s > 0) rec[s - 1][2] = hop;
+  }
+};
+
+// RegSink keeps forward, backward and hop times of an S-stage pipeline in
+// registers as fp64 (every stage quantity is below 2^52, so exact): each
+// stage shifts the arrays down by one and appends, so after S stages stage s
+// sits at index s; a runtime-indexed array would go through private memory.
+// The DP sync is left to dp_tail, after the recurrence.
+template <int S>
+struct RegSink {
+  static constexpr bool kDp = false;
+  double f[S], b[S], c[S];
+  __device__ __forceinline__ RegSink() {
+#pragma unroll
+    for (int i = 0; i < S; ++i) f[i] = b[i] = c[i] = 0;
+  }
+  __device__ __forceinline__ void put(uint32_t s, uint64_t fc, uint64_t bc, uint64_t hop, uint64_t) {
+#pragma unroll
+    for (int i = 0; i + 1 < S; ++i) {
+      f[i] = f[i + 1];
+      b[i] = b[i + 1];
+      c[i] = c[i + 1];
+    }
+    f[S - 1] = (double)fc;
+    b[S - 1] = (double)bc;
+    c[S - 1] = 0;
+    if (S > 1 && s > 0) c[S - 2] = (double)hop;
+  }
+};
+
+// Iteration time from the end of each stage's last op: the max over stages
+// of that end plus the stage's DP sync, walking the stages with the same
+// shift so that no array is indexed at run time.
+template <int S, int kMode>
+__device__ __forceinline__ double dp_tail(const Tab& t, const Hot<kMode>& h, const Plan& p, double (&last)[S]) {
+  const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> p.epl);
+  double T = 0;
+  uint32_t lo = 0;
+  for (uint32_t s = 0; s < (uint32_t)S; ++s) {
+    const uint32_t hi = cut_at(p, s);
+    const double e = last[0] + (double)stage_dp(t, h, p, s, hi - lo, rp, rpe);
+    T = e > T ? e : T;
+#pragma unroll
+    for (int i = 0; i + 1 < S; ++i) last[i] = last[i + 1];
+    lo = hi;
+  }
+  return T;
 }
 
 // per (class, stage) quantities of every plan, in plan order
@@ -390,7 +459,8 @@ __global__ void __launch_bounds__(256) k_stages(Tab t, const PackedPlan* __restr
   const Plan p = unpack(packed[slot >> 2]);
   uint64_t rec[kMaxStages][kRecWords];
   const Hot<2> h(t, nullptr);
-  class_setup(t, h, p, (uint32_t)(slot & 3), rec);
+  RecSink sink{rec};
+  class_setup(t, h, p, (uint32_t)(slot & 3), sink);
   uint64_t* o = out_stage + slot * (kMaxStages * kRecWords);
   for (uint32_t s = 0; s < p.S; ++s)
 #pragma unroll
@@ -508,14 +578,13 @@ __device__ __forceinline__ void steady_iter(const V (&f)[S], const V (&b)[S], co
 
 // kJump: take the periodic shortcut; then `skipped` returns the steady
 // iterations it skipped, or -1 if the lane is deferred (result not computed).
+// Returns false for a deferred lane; else last[s] = end of stage s's last op.
 template <int S, typename V, bool kJump>
-__device__ __forceinline__ V pipe(const StageRec& R, uint32_t M, int& skipped) {
-  V f[S], b[S], c[S], out_f[S], last[S];
+__device__ __forceinline__ bool pipe(const V (&f)[S], const V (&b)[S], const V (&c)[S], uint32_t M, int& skipped,
+                                     V (&last)[S]) {
+  V out_f[S];
 #pragma unroll
   for (int s = 0; s < S; ++s) {
-    f[s] = (V)R[s][0];
-    b[s] = (V)R[s][1];
-    c[s] = (V)R[s][2];
     out_f[s] = 0;
     last[s] = 0;
   }
@@ -570,7 +639,7 @@ __device__ __forceinline__ V pipe(const StageRec& R, uint32_t M, int& skipped) {
     }
     if (left > 0) {
       skipped = -1;
-      return 0;
+      return false;
     }
   } else {
     // two iterations per trip: the next iteration's upper stages overlap
@@ -594,10 +663,7 @@ __device__ __forceinline__ V pipe(const StageRec& R, uint32_t M, int& skipped) {
       }
     }
   }
-  V T = 0;
-#pragma unroll
-  for (int s = 0; s < S; ++s) T = vmax(T, last[s] + (V)R[s][3]);
-  return T;
+  return true;
 }
 
 // Integers below 2^53 are exact in fp64.  Every value the fp64 pass computes
@@ -630,11 +696,13 @@ template <int S, bool kFull, int kMode>
 __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot,
                                          uint32_t M) {
   const Plan p = unpack(e.packed[slot >> 2]);
-  StageRec R;
-  class_setup(t, h, p, slot & 3, R);
+  RegSink<S> r;
+  class_setup(t, h, p, slot & 3, r);
   int skipped;
-  const double T = pipe<S, double, !kFull>(R, M, skipped);
-  if (skipped < 0) {
+  double last[S];
+  const bool done = pipe<S, double, !kFull>(r.f, r.b, r.c, M, skipped, last);
+  const double T = done ? dp_tail(t, h, p, last) : 0;
+  if (!done) {
     e.deferred[e.sstart[kMaxStages - S] + atomicAdd(&e.ctr[1 + kMaxStages - S], 1u)] = slot;
     return;
   }
@@ -733,8 +801,19 @@ __global__ void __launch_bounds__(kEvalThreads) k_deferred(Tab t, EvalBufs e) {
 // Pipelines whose fp64 time reached 2^53 ps, again in u64 (exact below 2^64).
 template <int S>
 __device__ __forceinline__ uint64_t redo_one(const StageRec& R, uint32_t M) {
+  uint64_t f[S], b[S], c[S], last[S];
+#pragma unroll
+  for (int s = 0; s < S; ++s) {
+    f[s] = R[s][0];
+    b[s] = R[s][1];
+    c[s] = R[s][2];
+  }
   int skipped;
-  return pipe<S, uint64_t, false>(R, M, skipped);
+  pipe<S, uint64_t, false>(f, b, c, M, skipped, last);
+  uint64_t T = 0;
+#pragma unroll
+  for (int s = 0; s < S; ++s) T = vmax(T, last[s] + R[s][3]);
+  return T;
 }
 
 __global__ void __launch_bounds__(64) k_redo_u64(Tab t, EvalBufs e) {
@@ -745,7 +824,8 @@ __global__ void __launch_bounds__(64) k_redo_u64(Tab t, EvalBufs e) {
     const Plan p = unpack(e.packed[slot >> 2]);
     StageRec R;
     const Hot<2> h(t, nullptr);
-    class_setup(t, h, p, slot & 3, R);
+    RecSink sink{R};
+    class_setup(t, h, p, slot & 3, sink);
     uint64_t r;
     switch (S) {
       case 1: r = redo_one<1>(R, M); break;
