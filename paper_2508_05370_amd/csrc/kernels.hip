@@ -120,6 +120,13 @@ __device__ __forceinline__ Plan unpack(const PackedPlan& q) {
   return p;
 }
 
+// micro-batches per replica of class c (the pipeline's M)
+__device__ __forceinline__ uint32_t class_mb(const Plan& p, uint32_t c) {
+  const uint32_t r = c == 0 ? p.reps[0] : c == 1 ? p.reps[1] : c == 2 ? p.reps[2] : p.reps[3];
+  const uint32_t n = c == 0 ? p.nmb[0] : c == 1 ? p.nmb[1] : c == 2 ? p.nmb[2] : p.nmb[3];
+  return (n + r - 1) / r;
+}
+
 constexpr int kPrepPerThread = 4;
 
 // Decode and check plan i (every rule of the plan layout); on success pack it.
@@ -693,9 +700,9 @@ struct EvalBufs {
 // takes the periodic shortcut and defers the lanes still aperiodic after the
 // budget; k_deferred runs those through the whole steady loop.
 template <int S, bool kFull, int kMode>
-__device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot,
-                                         uint32_t M) {
+__device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot) {
   const Plan p = unpack(e.packed[slot >> 2]);
+  const uint32_t M = class_mb(p, slot & 3);
   RegSink<S> r;
   class_setup(t, h, p, slot & 3, r);
   int skipped;
@@ -736,18 +743,17 @@ __global__ void __launch_bounds__(kEvalThreads) k_eval(Tab t, EvalBufs e) {
     const uint32_t pos = base + (threadIdx.x & 63u);
     bool pending = pos < hi;
     const uint32_t slot = pending ? e.ids[pos] : 0;
-    const uint32_t m = pending ? e.meta[slot] : 0;
-    const uint32_t S = m & 31, M = m >> 8;
+    const uint32_t S = pending ? ((e.packed[slot >> 2].hdr >> 4) & 15) + 1 : 0;
     // one pass per distinct stage count present in the wavefront (usually one)
     while (true) {
       const uint64_t live = __ballot(pending);
       if (!live) break;
       const uint32_t S0 = __builtin_amdgcn_readfirstlane(__shfl(S, __ffsll((unsigned long long)live) - 1));
       if (pending && S == S0) {
-        if (S0 == kTop) eval_one<kTop, false>(t, h, e, slot, M);
-        else if (S0 == kTop - 1) eval_one<kTop - 1, false>(t, h, e, slot, M);
-        else if (S0 == kTop - 2) eval_one<kTop - 2, false>(t, h, e, slot, M);
-        else eval_one<kTop - 3, false>(t, h, e, slot, M);
+        if (S0 == kTop) eval_one<kTop, false>(t, h, e, slot);
+        else if (S0 == kTop - 1) eval_one<kTop - 1, false>(t, h, e, slot);
+        else if (S0 == kTop - 2) eval_one<kTop - 2, false>(t, h, e, slot);
+        else eval_one<kTop - 3, false>(t, h, e, slot);
         pending = false;
       }
     }
@@ -776,24 +782,23 @@ __global__ void __launch_bounds__(kEvalThreads) k_deferred(Tab t, EvalBufs e) {
     const uint32_t off = (q - before) * 64u + (threadIdx.x & 63u);
     if (off >= e.ctr[1 + j]) continue;
     const uint32_t slot = e.deferred[e.sstart[j] + off];
-    const uint32_t M = e.meta[slot] >> 8;
     switch (kMaxStages - j) {
-      case 1: eval_one<1, true>(t, h, e, slot, M); break;
-      case 2: eval_one<2, true>(t, h, e, slot, M); break;
-      case 3: eval_one<3, true>(t, h, e, slot, M); break;
-      case 4: eval_one<4, true>(t, h, e, slot, M); break;
-      case 5: eval_one<5, true>(t, h, e, slot, M); break;
-      case 6: eval_one<6, true>(t, h, e, slot, M); break;
-      case 7: eval_one<7, true>(t, h, e, slot, M); break;
-      case 8: eval_one<8, true>(t, h, e, slot, M); break;
-      case 9: eval_one<9, true>(t, h, e, slot, M); break;
-      case 10: eval_one<10, true>(t, h, e, slot, M); break;
-      case 11: eval_one<11, true>(t, h, e, slot, M); break;
-      case 12: eval_one<12, true>(t, h, e, slot, M); break;
-      case 13: eval_one<13, true>(t, h, e, slot, M); break;
-      case 14: eval_one<14, true>(t, h, e, slot, M); break;
-      case 15: eval_one<15, true>(t, h, e, slot, M); break;
-      default: eval_one<16, true>(t, h, e, slot, M); break;
+      case 1: eval_one<1, true>(t, h, e, slot); break;
+      case 2: eval_one<2, true>(t, h, e, slot); break;
+      case 3: eval_one<3, true>(t, h, e, slot); break;
+      case 4: eval_one<4, true>(t, h, e, slot); break;
+      case 5: eval_one<5, true>(t, h, e, slot); break;
+      case 6: eval_one<6, true>(t, h, e, slot); break;
+      case 7: eval_one<7, true>(t, h, e, slot); break;
+      case 8: eval_one<8, true>(t, h, e, slot); break;
+      case 9: eval_one<9, true>(t, h, e, slot); break;
+      case 10: eval_one<10, true>(t, h, e, slot); break;
+      case 11: eval_one<11, true>(t, h, e, slot); break;
+      case 12: eval_one<12, true>(t, h, e, slot); break;
+      case 13: eval_one<13, true>(t, h, e, slot); break;
+      case 14: eval_one<14, true>(t, h, e, slot); break;
+      case 15: eval_one<15, true>(t, h, e, slot); break;
+      default: eval_one<16, true>(t, h, e, slot); break;
     }
   }
 }
@@ -820,8 +825,8 @@ __global__ void __launch_bounds__(64) k_redo_u64(Tab t, EvalBufs e) {
   const uint32_t n = e.ctr[0];
   for (uint32_t j = blockIdx.x * 64u + threadIdx.x; j < n; j += gridDim.x * 64u) {
     const uint32_t slot = e.ovf[j];
-    const uint32_t m = e.meta[slot], S = m & 31, M = m >> 8;
     const Plan p = unpack(e.packed[slot >> 2]);
+    const uint32_t S = p.S, M = class_mb(p, slot & 3);
     StageRec R;
     const Hot<2> h(t, nullptr);
     RecSink sink{R};

@@ -326,3 +326,19 @@ def test_concurrent_multichunk_calls(torch, B, workloads):
     torch.cuda.synchronize()
     for k in range(2):
         assert torch.equal(outs[k], ref), k
+
+
+def test_tables_in_device_memory(torch, B, oracle_mod, workloads):
+    """A context whose setup tables exceed the LDS budget (16 device types,
+    200 layers, 4 micro-batch sizes: 0.8 MB of layer prefix sums) reads them
+    from device memory; every plan still matches the oracle."""
+    m = dict(workloads.workload(2)["model"])
+    m["L"], m["mbs"] = 200, [1, 2, 4, 8]
+    c = workloads.cluster_random(9, [2] * 16, dpn=8, jitter=True)
+    n = 20_011
+    p = workloads.random_plans(m, c, 0x7AB1E, 0, n)
+    say("case: 16 types, 200 layers, tables in device memory, %d plans" % n)
+    got = _gpu_times(B, B.Sim(m, c), p)
+    want = oracle_mod.Oracle(m, c).eval(p)
+    _assert_equal(got, want, "tables in device memory")
+    assert np.count_nonzero(want != MAXU) > n // 2
