@@ -5,13 +5,14 @@ validate, place, stage costs, bottleneck links, collectives, the 1F1B pipeline
 of every replica class, the DP sync, and the argmin over all plans.  Plans are
 resident in HBM before timing starts.
 
-Prints one JSON line.  Roofline: the evaluation kernels are bound by VALU
-issue.  The 1F1B recurrence costs 3 VALU ops (add, max, add) per dependent
-schedule node and 1 per node without a cross-stage input, i.e. sum over
-classes of M * (6 (S - 1) + 2) per plan; the library skips the steady
-iterations that follow a periodic one (counted on the device while timing is
-on), and the algorithmic work reported is the recurrence work that remains.
-The peak is 256 CUs x 64 lanes x 2.4 GHz.
+Prints one JSON line.  Roofline: the evaluation is bound by VALU issue.  The
+1F1B recurrence costs 3 VALU ops (add, max, add) per dependent schedule node
+and 1 per node without a cross-stage input, i.e. sum over classes of
+M * (6 (S - 1) + 2) per plan; the library skips the steady iterations that
+follow a periodic one (counted on the device while timing is on), and the
+algorithmic work reported is the recurrence work that remains, per
+sim_eval_plans call, over the call's duration.  The peak is 256 CUs x 64
+lanes x 2.4 GHz.
 """
 import argparse
 import json
@@ -51,20 +52,27 @@ def pipeline_ops(p, valid):
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "eval_llama70b_16M_hbm_traffic.txt")
 
 
-def measured_traffic(workload, chunk):
-    """HBM bytes per evaluation launch from the committed FETCH_SIZE/WRITE_SIZE
-    summary; None unless it was taken on this workload, in 2M-plan chunks, with
-    the kernel source as it is now (sha256 recorded in the summary)."""
+def source_hash():
+    """sha256 of the kernel and launch sources (kernels.hip, then api.cpp)."""
     import hashlib
-    if workload != 3 or chunk not in (0, 1 << 21) or not os.path.exists(TRAFFIC_FILE):
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "api.cpp"):
+        h.update(open(os.path.join(ROOT, "paper_2508_05370_amd", "csrc", f), "rb").read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload, chunk):
+    """HBM bytes per evaluation call (the whole 16M-plan workload in one call)
+    from the committed FETCH_SIZE/WRITE_SIZE summary; None unless it was taken
+    on this workload with the sources as they are now (hash recorded there)."""
+    if workload != 3 or chunk != 0 or not os.path.exists(TRAFFIC_FILE):
         return None
     kv = {}
     for line in open(TRAFFIC_FILE):
         if "=" in line and not line.startswith("#"):
             k, v = line.split("=", 1)
             kv[k.strip()] = v.strip()
-    src = os.path.join(ROOT, "paper_2508_05370_amd", "csrc", "kernels.hip")
-    if kv.get("kernels_sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest():
+    if kv.get("sources_sha256") != source_hash():
         return None
     return int(kv["traffic_bytes_per_launch"])
 
@@ -142,11 +150,7 @@ def main():
     got = B.times_u64(out)
     valid = got != MAXU
     ops = pipeline_ops(p, valid)
-    lib_chunk = 1 << 21
-    if a.chunk:
-        launches_per_step = sum(-(-min(a.chunk, n - o) // lib_chunk) for o in range(0, n, a.chunk))
-    else:
-        launches_per_step = -(-n // lib_chunk)
+    calls_per_step = len(range(0, n, a.chunk)) if a.chunk else 1
 
     [sim.get_timing(k) for k in range(4)]          # clear
     sim.get_skipped_ops()
@@ -174,24 +178,24 @@ def main():
         setup_ms, setup_n = sim.get_timing(1)
         call_ms, call_n = sim.get_timing(2)
         defer_ms, defer_n = sim.get_timing(3)
-        # one launch = a chunk's first pass plus its deferred pass; their busy
-        # times are added (the overlap of a deferred pass with the next
-        # chunk's first pass is not credited)
-        avg_ms = pipe_ms / max(pipe_n, 1) + defer_ms / max(defer_n, 1)
-        full_per_launch = float(ops.sum()) / launches_per_step
-        ops_per_launch = full_per_launch - skipped / timed / launches_per_step
+        # one launch = one sim_eval_plans call (all its kernels, on all its
+        # streams), timed by the library's events on the call's stream
+        avg_ms = call_ms / max(call_n, 1)
+        full_per_launch = float(ops.sum()) / calls_per_step
+        ops_per_launch = full_per_launch - skipped / timed / calls_per_step
         achieved = ops_per_launch / (avg_ms * 1e-3) / 1e12
         roof = {"bound": "alu", "achieved": round(achieved, 3), "peak": round(PEAK_VALU / 1e12, 3),
                 "unit": "TOP/s", "frac": round(achieved * 1e12 / PEAK_VALU, 4),
                 "traffic": None if a.plans else measured_traffic(a.workload, a.chunk),
-                "kernel": "k_eval x4 stage-count groups + k_deferred + k_redo_u64, per 2M-plan chunk",
-                "avg_launch_ms": round(avg_ms, 4), "launches": pipe_n, "ops_per_launch": ops_per_launch,
+                "kernel": "sim_eval_plans call: k_prep, k_scan, k_scatter, k_eval x4 groups, k_deferred, "
+                          "k_redo_u64 per 2M-plan chunk",
+                "avg_launch_ms": round(avg_ms, 4), "launches": call_n, "ops_per_launch": ops_per_launch,
                 "full_recurrence_ops_per_launch": full_per_launch,
                 "skipped_by_periodic_shortcut": round(1 - ops_per_launch / full_per_launch, 4)}
         extra = {"timed_steps_with_kernel_events": timed,
                  "prep_ms_per_step": round(setup_ms / timed, 4),
-                 "eval_kernels_ms_per_step": round(pipe_ms / timed, 4),
-                 "deferred_kernels_ms_per_step": round(defer_ms / timed, 4),
+                 "first_pass_span_ms_per_step": round(pipe_ms / timed, 4),
+                 "deferred_pass_ms_per_step": round(defer_ms / timed, 4),
                  "eval_call_ms_per_step": round(call_ms / timed, 4)}
 
     # CPU baseline: the oracle as it stands, on a bounded prefix of the same plans

@@ -19,6 +19,7 @@ hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint32_t*
 hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* sstart, hipStream_t s);
 hipError_t launch_scatter(const uint32_t* meta, uint32_t nslots, uint32_t* cursor, uint32_t* ids, hipStream_t s);
 hipError_t launch_first(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s);
+hipError_t launch_group(const Tab& t, const EvalArgs& a, uint32_t max_tasks, int g, hipStream_t s);
 hipError_t launch_deferred(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s);
 hipError_t launch_argmin(const uint64_t* t, int64_t n, int64_t base, sim_best* b, hipStream_t s);
 hipError_t launch_best_reduce(const sim_best* in, int64_t n, sim_best* out, hipStream_t s);
@@ -45,6 +46,7 @@ struct sim_ctx {
   std::vector<EventPair> ev[4];
   uint64_t* skipped_ops;   // device counter, inside `tables`
   hipStream_t aux;         // deferred passes of multi-chunk calls, created on first use
+  hipStream_t grp[4];      // first-pass groups of multi-chunk calls, created on first use
 };
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -75,6 +77,7 @@ extern "C" int sim_create(const sim_model_desc* model, const sim_cluster_desc* c
   c->tables = nullptr;
   c->pool = nullptr;
   c->aux = nullptr;
+  for (auto& g : c->grp) g = nullptr;
   if (hipGetDevice(&c->device) != hipSuccess) { delete ht; delete c; return SIM_EHIP; }
   // the table image, then the skipped-work counter slots
   const size_t img = align256(ht->img.size());
@@ -105,6 +108,8 @@ extern "C" void sim_destroy(sim_ctx* c) {
     for (auto& e : v) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }
   (void)hipDeviceSynchronize();
   if (c->aux) (void)hipStreamDestroy(c->aux);
+  for (auto& g : c->grp)
+    if (g) (void)hipStreamDestroy(g);
   if (c->pool) (void)hipMemPoolDestroy(c->pool);
   if (c->tables) (void)hipFree(c->tables);
   delete c;
@@ -154,17 +159,22 @@ static Work carve(void* base, int64_t ch) {
   return w;
 }
 
-static hipStream_t aux_stream(sim_ctx* c) {
+static bool side_streams(sim_ctx* c) {
   std::lock_guard<std::mutex> g(c->mu);
   if (!c->aux && hipStreamCreateWithFlags(&c->aux, hipStreamNonBlocking) != hipSuccess) c->aux = nullptr;
-  return c->aux;
+  for (auto& q : c->grp)
+    if (!q && hipStreamCreateWithFlags(&q, hipStreamNonBlocking) != hipSuccess) q = nullptr;
+  bool ok = c->aux != nullptr;
+  for (auto q : c->grp) ok = ok && q;
+  return ok;
 }
 
-// Chunks of kChunk plans.  With more than one chunk, the deferred pass of
-// chunk i runs on the context's second stream while the main stream packs
-// and evaluates chunk i + 1; the two workspaces alternate, and the main
-// stream waits for the deferred pass of chunk i before reusing its
-// workspace for chunk i + 2 and, at the end, for the last one.
+// Chunks of kChunk plans.  With more than one chunk, the four stage-count
+// groups of chunk i's first pass run on four streams of the context, and its
+// deferred pass on a fifth that waits for the four, while the call's stream
+// packs and sorts chunk i + 1.  The two workspaces alternate; the call's
+// stream waits for chunk i's deferred pass before reusing its workspace for
+// chunk i + 2 and, at the end, for the last one.
 extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uint64_t* out, void* stream) {
   if (!c || !plans_ok(plans, n) || (n > 0 && !out)) return SIM_EINVAL;
   if (n == 0) return SIM_OK;
@@ -173,17 +183,18 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
   const int64_t ch = n < kChunk ? n : kChunk;
   const int nbuf = n > ch ? 2 : 1;
   hipStream_t aux = s;
-  hipEvent_t ready[2] = {nullptr, nullptr}, done[2] = {nullptr, nullptr};
+  constexpr int kEv = 2 * 6;   // per buffer: sorted, four group ends, deferred end
+  hipEvent_t evs[kEv] = {};
+  auto sorted = [&](int b) { return evs[b * 6]; };
+  auto fin = [&](int b, int g) { return evs[b * 6 + 1 + g]; };
+  auto done = [&](int b) { return evs[b * 6 + 5]; };
   if (nbuf == 2) {
-    aux = aux_stream(c);
-    if (!aux) return SIM_EHIP;
-    for (int j = 0; j < 2; ++j)
-      if (hipEventCreateWithFlags(&ready[j], hipEventDisableTiming) != hipSuccess ||
-          hipEventCreateWithFlags(&done[j], hipEventDisableTiming) != hipSuccess) {
-        for (int q = 0; q < 2; ++q) {
-          if (ready[q]) (void)hipEventDestroy(ready[q]);
-          if (done[q]) (void)hipEventDestroy(done[q]);
-        }
+    if (!side_streams(c)) return SIM_EHIP;
+    aux = c->aux;
+    for (int j = 0; j < kEv; ++j)
+      if (hipEventCreateWithFlags(&evs[j], hipEventDisableTiming) != hipSuccess) {
+        for (auto& x : evs)
+          if (x) (void)hipEventDestroy(x);
         return SIM_EHIP;
       }
   }
@@ -198,10 +209,11 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
   int64_t i = 0;
   for (int64_t off = 0; ws && off < n && e == hipSuccess; off += ch, ++i) {
     const int64_t cn = n - off < ch ? n - off : ch;
-    const Work& W = w[i % nbuf];
+    const int b = (int)(i % nbuf);
+    const Work& W = w[b];
     sim_plans p = *plans;
     p.hdr += off; p.cut += off; p.cls += off; p.types += off;
-    if (i >= 2) e = hipStreamWaitEvent(s, done[i % 2], 0);
+    if (i >= 2) e = hipStreamWaitEvent(s, done(b), 0);
     if (e == hipSuccess) e = launch_fill32(W.hist, kCounters, 0, s);
     bool t1 = e == hipSuccess && begin_event(c, 1, s, &ev);
     if (e == hipSuccess) e = launch_prep(c->tab, p, cn, out + off, W.packed, W.meta, W.hist, s);
@@ -210,34 +222,49 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
     if (e == hipSuccess) e = launch_scatter(W.meta, (uint32_t)(cn * 4), W.cursor, W.ids, s);
     const EvalArgs a = {W.packed, W.meta, W.ids, W.sstart, out + off, W.ctr, W.deferred,
                         c->timing ? c->skipped_ops : nullptr};
-    bool t0 = e == hipSuccess && begin_event(c, 0, s, &ev);
-    if (e == hipSuccess) e = launch_first(c->tab, a, (uint32_t)(cn * 4), s);
-    if (t0) end_event(c, 0, s, &ev);
-    if (e == hipSuccess && nbuf == 2) {
-      e = hipEventRecord(ready[i % 2], s);
-      if (e == hipSuccess) e = hipStreamWaitEvent(aux, ready[i % 2], 0);
+    EventPair e0;
+    bool t0 = e == hipSuccess && begin_event(c, 0, s, &e0);
+    if (nbuf == 1) {
+      if (e == hipSuccess) e = launch_first(c->tab, a, (uint32_t)(cn * 4), s);
+      if (t0) end_event(c, 0, s, &e0);
+      if (e != hipSuccess) break;
+    } else {
+      if (e == hipSuccess) e = hipEventRecord(sorted(b), s);
+      joined = false;
+      for (int g = 0; g < 4 && e == hipSuccess; ++g) {
+        e = hipStreamWaitEvent(c->grp[g], sorted(b), 0);
+        if (e == hipSuccess) e = launch_group(c->tab, a, (uint32_t)(cn * 4), g, c->grp[g]);
+        if (e == hipSuccess) e = hipEventRecord(fin(b, g), c->grp[g]);
+        if (e == hipSuccess) e = hipStreamWaitEvent(aux, fin(b, g), 0);
+      }
+      if (t0) end_event(c, 0, aux, &e0);
+      if (e != hipSuccess) break;
     }
-    if (e != hipSuccess) break;
-    joined = nbuf == 1;
     bool t3 = begin_event(c, 3, aux, &ev);
     e = launch_deferred(c->tab, a, (uint32_t)(cn * 4), aux);
     if (t3) end_event(c, 3, aux, &ev);
     if (nbuf == 2) {
-      const hipError_t r = hipEventRecord(done[i % 2], aux);
+      const hipError_t r = hipEventRecord(done(b), aux);
       if (e == hipSuccess) e = r;
     }
   }
-  // the main stream takes over everything the second stream was given
-  if (!joined) {
-    const hipError_t r = hipStreamWaitEvent(s, done[(i - 1) % 2], 0);
+  // the call's stream takes over everything the side streams were given (after
+  // a failed launch, drain them before the workspace is released)
+  if (nbuf == 2 && e != hipSuccess) {
+    for (auto q : c->grp) (void)hipStreamSynchronize(q);
+    (void)hipStreamSynchronize(aux);
+  } else if (!joined) {
+    for (int g = 0; g < 4; ++g) {
+      const hipError_t r = hipStreamWaitEvent(s, fin((int)((i - 1) % 2), g), 0);
+      if (e == hipSuccess) e = r;
+    }
+    const hipError_t r = hipStreamWaitEvent(s, done((int)((i - 1) % 2)), 0);
     if (e == hipSuccess) e = r;
   }
   if (tcall) end_event(c, 2, s, &call);
   if (ws) (void)hipFreeAsync(ws, s);
-  for (int j = 0; j < 2; ++j) {
-    if (ready[j]) (void)hipEventDestroy(ready[j]);
-    if (done[j]) (void)hipEventDestroy(done[j]);
-  }
+  for (auto& x : evs)
+    if (x) (void)hipEventDestroy(x);
   if (!ws) return SIM_ENOMEM;
   return e == hipSuccess ? SIM_OK : SIM_EHIP;
 }

@@ -995,6 +995,26 @@ static EvalBufs bufs(const EvalArgs& a) {
           (unsigned long long*)a.skipped_ops};
 }
 
+// first pass of one stage-count group (g = 0..3) over a chunk
+template <int kMode>
+static void launch_group_mode(const Tab& t, const EvalBufs& e, uint32_t max_tasks, int g, hipStream_t s) {
+  const int nb = blocks_for(max_tasks, kEvalThreads);
+  const uint32_t need = nb > 0 ? (uint32_t)nb : 1, grid = 4 * t.grid_eval[g] < need ? 4 * t.grid_eval[g] : need;
+  const size_t lds = kMode < 2 ? t.lds_bytes : 0;
+  if (g == 0) k_eval<0, kMode><<<grid, kEvalThreads, lds, s>>>(t, e);
+  else if (g == 1) k_eval<1, kMode><<<grid, kEvalThreads, lds, s>>>(t, e);
+  else if (g == 2) k_eval<2, kMode><<<grid, kEvalThreads, lds, s>>>(t, e);
+  else k_eval<3, kMode><<<grid, kEvalThreads, lds, s>>>(t, e);
+}
+
+hipError_t launch_group(const Tab& t, const EvalArgs& a, uint32_t max_tasks, int g, hipStream_t s) {
+  const EvalBufs e = bufs(a);
+  if (t.mode == 0) launch_group_mode<0>(t, e, max_tasks, g, s);
+  else if (t.mode == 1) launch_group_mode<1>(t, e, max_tasks, g, s);
+  else launch_group_mode<2>(t, e, max_tasks, g, s);
+  return hipGetLastError();
+}
+
 // first pass over a chunk: k_eval of each stage-count group
 hipError_t launch_first(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s) {
   const EvalBufs e = bufs(a);
