@@ -38,7 +38,9 @@ struct TypeInfo {
 // LDS rather than vector-cache rates.  Sections, each 16-byte aligned:
 //   TypeInfo [K]; {forward, backward} layer prefix sums
 //   [K][4 log2 TP][n_mbs][nep][L+1] (nep = 4 EP slots for MoE models, 1 for
-//   dense ones); {fwd, bwd} embedding [K][n_mbs]; {fwd, bwd} head
+//   dense ones), or, when every layer costs the same (dense models), one
+//   {forward, backward} layer cost [K][4][n_mbs] (uniform_layers);
+//   {fwd, bwd} embedding [K][n_mbs]; {fwd, bwd} head
 //   [K][4][n_mbs]; all-to-all bytes prefix [4][n_mbs][L+1] (MoE only);
 //   range-max rows of the node fabric rates [lvl_node][N]; range-max rows
 //   of the device NIC rates [lvl_dev][D] (last, the largest).
@@ -69,6 +71,7 @@ struct Tab {
   uint64_t par_expert[4][4];      // expert parameters of one layer per rank [log2 TP][log2 EP]
   uint64_t par_embed[4], par_head[4];
   uint32_t nep;                   // EP slots of the prefix tables
+  uint32_t uniform_layers;        // 1: the layer table holds one layer's cost per row
   uint32_t o_pfb, o_emb, o_head, o_pa, o_rmi, o_rmn;   // section byte offsets (TypeInfo at 0)
   uint32_t img_bytes;             // whole image
   uint32_t lds_bytes;             // prefix copied to LDS: img_bytes, o_rmn or 0 by mode

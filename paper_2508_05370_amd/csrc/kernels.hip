@@ -94,25 +94,41 @@ __device__ __forceinline__ uint32_t bucket_key(uint32_t S, uint32_t G, uint32_t 
 // Decoded plan fields used by every pipeline of the plan.
 struct Plan {
   uint32_t tpl, epl, S, G, zero, mi, tp, ep, psum;
-  uint32_t cut[4];          // cut bytes, four per word
+  uint64_t cut_lo, cut_hi;  // cut bytes of stages 0-7 and 8-15, eight per word
   uint32_t reps[4], nmb[4];
   uint64_t tv[4];           // stage types, nibbles past S cleared
+  // the class a pipeline evaluates: index, replicas, micro-batches, types.
+  // Read here, from the packed plan in memory, so that no per-lane class
+  // index ever selects among the fields above (that would put them in
+  // private memory).
+  uint32_t c, rc, nc;
+  uint64_t tc;
 };
 
+// cut of stage s (a run-time index): mask arithmetic rather than a select,
+// which the compiler may turn into an indexed load of the plan in private
+// memory
 __device__ __forceinline__ uint32_t cut_at(const Plan& p, uint32_t s) {
-  const uint32_t w = s < 8 ? (s < 4 ? p.cut[0] : p.cut[1]) : (s < 12 ? p.cut[2] : p.cut[3]);
-  return (w >> (8 * (s & 3))) & 0xff;
+  const uint64_t m = 0ull - (uint64_t)(s >> 3);
+  const uint64_t w = (p.cut_lo & ~m) | (p.cut_hi & m);
+  return (uint32_t)(w >> (8 * (s & 7))) & 0xff;
 }
 
-__device__ __forceinline__ Plan unpack(const PackedPlan& q) {
+__device__ __forceinline__ Plan unpack(const PackedPlan& q, uint32_t c = 0) {
   Plan p;
+  p.c = c;
+  const uint32_t cc = q.cls[c];
+  p.rc = cc & 0xffff;
+  p.nc = cc >> 16;
+  p.tc = q.types[c];
   const uint32_t hdr = q.hdr;
   p.tpl = hdr & 3; p.epl = (hdr >> 2) & 3; p.S = ((hdr >> 4) & 15) + 1; p.G = ((hdr >> 8) & 3) + 1;
   p.zero = (hdr >> 10) & 1; p.mi = (hdr >> 11) & 3; p.tp = 1u << p.tpl; p.ep = 1u << p.epl; p.psum = q.psum;
-  const uint32_t* cw = reinterpret_cast<const uint32_t*>(q.cut);
+  const uint64_t* cw = reinterpret_cast<const uint64_t*>(q.cut);
+  p.cut_lo = cw[0];
+  p.cut_hi = cw[1];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    p.cut[j] = cw[j];
     p.reps[j] = q.cls[j] & 0xffff;
     p.nmb[j] = q.cls[j] >> 16;
     p.tv[j] = q.types[j];
@@ -120,12 +136,8 @@ __device__ __forceinline__ Plan unpack(const PackedPlan& q) {
   return p;
 }
 
-// micro-batches per replica of class c (the pipeline's M)
-__device__ __forceinline__ uint32_t class_mb(const Plan& p, uint32_t c) {
-  const uint32_t r = c == 0 ? p.reps[0] : c == 1 ? p.reps[1] : c == 2 ? p.reps[2] : p.reps[3];
-  const uint32_t n = c == 0 ? p.nmb[0] : c == 1 ? p.nmb[1] : c == 2 ? p.nmb[2] : p.nmb[3];
-  return (n + r - 1) / r;
-}
+// micro-batches per replica of the pipeline's class (its M)
+__device__ __forceinline__ uint32_t class_mb(const Plan& p) { return (p.nc + p.rc - 1) / p.rc; }
 
 constexpr int kPrepPerThread = 4;
 
@@ -271,15 +283,25 @@ __device__ __forceinline__ void fill_lds(const Tab& t, uint4* lds) {
 // Placement: every pool is filled in (class, stage) order, reps*tp devices per
 // (class, stage), so a (class, stage) of type k starts after the devices of
 // type k used by earlier classes and by earlier stages of its own class.
-__device__ __forceinline__ uint32_t placed_before(const Plan& p, uint32_t c, uint32_t s, uint32_t k) {
+// Devices of type k taken before (class c2, stage s) for a class index c2
+// that is a compile-time constant once the callers' class loops unroll.
+__device__ __forceinline__ uint32_t placed_before(const Plan& p, uint32_t c2, uint32_t s, uint32_t k) {
   const uint64_t sel = p.S == 16 ? ~0ull : ((1ull << (4 * p.S)) - 1);
   uint32_t below = 0;
 #pragma unroll
-  for (uint32_t c2 = 0; c2 < 4; ++c2)
-    if (c2 < c) below += p.reps[c2] * count_type(p.tv[c2], k, sel);
-  const uint32_t rc = c == 0 ? p.reps[0] : c == 1 ? p.reps[1] : c == 2 ? p.reps[2] : p.reps[3];
-  const uint64_t tc = c == 0 ? p.tv[0] : c == 1 ? p.tv[1] : c == 2 ? p.tv[2] : p.tv[3];
-  return below + rc * count_type(tc, k, (1ull << (4 * s)) - 1);
+  for (uint32_t c3 = 0; c3 < 4; ++c3)
+    if (c3 < c2) below += p.reps[c3] * count_type(p.tv[c3], k, sel);
+  return below + p.reps[c2] * count_type(p.tv[c2], k, (1ull << (4 * s)) - 1);
+}
+
+// The same for the pipeline's own class (a per-lane index).
+__device__ __forceinline__ uint32_t placed_before_own(const Plan& p, uint32_t s, uint32_t k) {
+  const uint64_t sel = p.S == 16 ? ~0ull : ((1ull << (4 * p.S)) - 1);
+  uint32_t below = 0;
+#pragma unroll
+  for (uint32_t c3 = 0; c3 < 4; ++c3)
+    if (c3 < p.c) below += p.reps[c3] * count_type(p.tv[c3], k, sel);
+  return below + p.rc * count_type(p.tc, k, (1ull << (4 * s)) - 1);
 }
 
 // DP sync of stage s (layers [lo, hi), ns = hi - lo) over every replica of
@@ -332,8 +354,8 @@ __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, c
   const uint64_t act = t.act[mi], act_tp = (act + tp - 1) >> tpl;
   const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> epl);
   const uint32_t L1 = t.L + 1, epq = t.E ? p.epl : 0;
-  const uint32_t reps = c == 0 ? p.reps[0] : c == 1 ? p.reps[1] : c == 2 ? p.reps[2] : p.reps[3];
-  const uint64_t tvc = c == 0 ? p.tv[0] : c == 1 ? p.tv[1] : c == 2 ? p.tv[2] : p.tv[3];
+  const uint32_t reps = p.rc;
+  const uint64_t tvc = p.tc;
   uint32_t pk = 0, pbase = 0, pnic = 0, pin = 0, lo = 0;
   TypeInfo pti = {};
   for (uint32_t s = 0; s < S; ++s) {
@@ -341,15 +363,22 @@ __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, c
     // ---- this class: compute, TP, EP, hop from the previous stage
     const uint32_t k = (uint32_t)(tvc >> (4 * s)) & 15;
     const TypeInfo ti = h.type(k);
-    const uint32_t base = placed_before(p, c, s, k) * tp, nd = reps * tp, dpl = ti.dpl;
+    const uint32_t base = placed_before_own(p, s, k) * tp, nd = reps * tp, dpl = ti.dpl;
     const uint32_t gnl = ti.node_off + (base >> dpl), gnh = ti.node_off + ((base + nd - 1) >> dpl);
     const uint32_t bq_in = range_max(h.rmi(), t.N, gnl, gnh);
     const uint32_t dlo = ti.dev_off + base;
     const uint32_t bq_nic = range_max(h.rmn, t.D, dlo, dlo + nd - 1);
-    const uint32_t tb = (((k * 4 + tpl) * t.n_mbs + mi) * t.nep + epq) * L1;
-    const ulonglong2 ph = h.pfb(tb + hi), pl = h.pfb(tb + lo);
-    uint64_t fc = ph.x - pl.x;
-    uint64_t bc = ph.y - pl.y;
+    const uint32_t row = ((k * 4 + tpl) * t.n_mbs + mi) * t.nep + epq;
+    uint64_t fc, bc;
+    if (t.uniform_layers) {
+      const ulonglong2 lc = h.pfb(row);
+      fc = lc.x * ns;
+      bc = lc.y * ns;
+    } else {
+      const ulonglong2 ph = h.pfb(row * L1 + hi), pl = h.pfb(row * L1 + lo);
+      fc = ph.x - pl.x;
+      bc = ph.y - pl.y;
+    }
     if (s == 0) {
       const ulonglong2 em = h.emb(k * t.n_mbs + mi);
       fc += em.x;
@@ -463,7 +492,7 @@ __global__ void __launch_bounds__(256) k_stages(Tab t, const PackedPlan* __restr
                                                 uint64_t* __restrict__ out_stage) {
   const int64_t slot = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (slot >= n * 4 || meta[slot] == 0) return;
-  const Plan p = unpack(packed[slot >> 2]);
+  const Plan p = unpack(packed[slot >> 2], (uint32_t)(slot & 3));
   uint64_t rec[kMaxStages][kRecWords];
   const Hot<2> h(t, nullptr);
   RecSink sink{rec};
@@ -701,14 +730,22 @@ struct EvalBufs {
 // budget; k_deferred runs those through the whole steady loop.
 template <int S, bool kFull, int kMode>
 __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot) {
-  const Plan p = unpack(e.packed[slot >> 2]);
-  const uint32_t M = class_mb(p, slot & 3);
   RegSink<S> r;
-  class_setup(t, h, p, slot & 3, r);
+  uint32_t M;
+  {
+    const Plan p = unpack(e.packed[slot >> 2], slot & 3);
+    M = class_mb(p);
+    class_setup(t, h, p, slot & 3, r);
+  }
   int skipped;
   double last[S];
   const bool done = pipe<S, double, !kFull>(r.f, r.b, r.c, M, skipped, last);
-  const double T = done ? dp_tail(t, h, p, last) : 0;
+  // the DP tail reads the plan again (an L2 hit) rather than keeping it in
+  // registers through the recurrence; the lane's own slot passed through a
+  // shuffle is opaque to the compiler, which would otherwise reuse the
+  // first load
+  const uint32_t slot2 = __shfl(slot, (int)(threadIdx.x & 63u));
+  const double T = done ? dp_tail(t, h, unpack(e.packed[slot2 >> 2], slot2 & 3), last) : 0;
   if (!done) {
     e.deferred[e.sstart[kMaxStages - S] + atomicAdd(&e.ctr[1 + kMaxStages - S], 1u)] = slot;
     return;
@@ -825,8 +862,8 @@ __global__ void __launch_bounds__(64) k_redo_u64(Tab t, EvalBufs e) {
   const uint32_t n = e.ctr[0];
   for (uint32_t j = blockIdx.x * 64u + threadIdx.x; j < n; j += gridDim.x * 64u) {
     const uint32_t slot = e.ovf[j];
-    const Plan p = unpack(e.packed[slot >> 2]);
-    const uint32_t S = p.S, M = class_mb(p, slot & 3);
+    const Plan p = unpack(e.packed[slot >> 2], slot & 3);
+    const uint32_t S = p.S, M = class_mb(p);
     StageRec R;
     const Hot<2> h(t, nullptr);
     RecSink sink{R};

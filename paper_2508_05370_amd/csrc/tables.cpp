@@ -118,8 +118,20 @@ void build_image(HostTables* h) {
   Tab& t = h->tab;
   const uint32_t K = t.K, nm = t.n_mbs, L1 = t.L + 1;
   t.nep = t.E ? 4 : 1;
+  // every layer of a dense model costs the same on a given (type, TP,
+  // micro-batch size): then one {fwd, bwd} entry per table row replaces the
+  // L+1 prefix sums, and a stage costs ns times it (the same integers)
+  bool uniform = t.E == 0;
+  for (size_t r = 0; uniform && r < h->pf.size() / L1; ++r)
+    for (uint32_t l = 1; uniform && l < t.L; ++l) {
+      const size_t b = r * L1;
+      uniform = h->pf[b + l + 1] - h->pf[b + l] == h->pf[b + 1] - h->pf[b] &&
+                h->pb[b + l + 1] - h->pb[b + l] == h->pb[b + 1] - h->pb[b];
+    }
+  t.uniform_layers = uniform ? 1 : 0;
+  const uint32_t row = uniform ? 1 : L1;   // entries per (type, TP, mbs, EP slot)
   auto a16 = [](size_t x) { return (uint32_t)((x + 15) & ~(size_t)15); };
-  const uint32_t n_pfb = K * 4 * nm * t.nep * L1;
+  const uint32_t n_pfb = K * 4 * nm * t.nep * row;
   t.o_pfb = a16((size_t)K * sizeof(TypeInfo));
   t.o_emb = t.o_pfb + n_pfb * 16;
   t.o_head = t.o_emb + K * nm * 16;
@@ -137,10 +149,10 @@ void build_image(HostTables* h) {
     for (uint32_t j = 0; j < 4; ++j)
       for (uint32_t mi = 0; mi < nm; ++mi)
         for (uint32_t g = 0; g < t.nep; ++g)
-          for (uint32_t l = 0; l < L1; ++l) {
-            const size_t src = ((((size_t)k * 4 + j) * nm + mi) * 4 + g) * L1 + l;
-            const size_t dst = ((((size_t)k * 4 + j) * nm + mi) * t.nep + g) * L1 + l;
-            pfb[2 * dst] = h->pf[src];
+          for (uint32_t l = 0; l < row; ++l) {
+            const size_t src = ((((size_t)k * 4 + j) * nm + mi) * 4 + g) * L1 + l + (uniform ? 1 : 0);
+            const size_t dst = ((((size_t)k * 4 + j) * nm + mi) * t.nep + g) * row + l;
+            pfb[2 * dst] = h->pf[src];        // uniform: pf[1] - pf[0] = the layer's cost
             pfb[2 * dst + 1] = h->pb[src];
           }
   memcpy(b + t.o_emb, h->emb.data(), h->emb.size() * 8);
