@@ -536,7 +536,7 @@ __global__ void __launch_bounds__(1024) k_scan(const uint32_t* __restrict__ hist
 }
 
 // place every pipeline id at its bucket's next free position
-constexpr int kScatterPer = 16;
+constexpr int kScatterPer = 64;
 __global__ void __launch_bounds__(256) k_scatter(const uint32_t* __restrict__ meta, uint32_t nslots,
                                                  uint32_t* __restrict__ cursor, uint32_t* __restrict__ ids) {
   constexpr int kPer = kScatterPer;
