@@ -21,7 +21,10 @@
  *   - interconnect delay = jumbo frame bits / unidirectional bandwidth, two
  *     PCIe trips for inter-node traffic (Sec. 5 "Interconnect configuration");
  *   - the slowest link or device of a collective sets its time (Sec. 4.1
- *     [C4], Sec. 5 [Q2]).
+ *     [C4], Sec. 5 [Q2]);
+ *   - parallelism exists to fit the model within device memory (Sec. 2),
+ *     and device types differ in capacity (Sec. 3 example, Table 5: A100
+ *     40 GB, H100 80 GB): a plan that overflows a device is infeasible.
  * Where the paper is silent the reading used is named R1..R30 in comments;
  * the design notes of the repository list every reading.
  *
@@ -29,7 +32,10 @@
  * delays, the parameter counts and the FLOP counts are pinned by tests
  * (closed forms, Table 5, Table 6, Table 1, a brute-force event simulator).
  * The per-op byte accounting of the roofline (R6/R8) has no printed value
- * to compare against: parity unpinned beyond scaling invariants.
+ * to compare against: parity unpinned beyond scaling invariants.  The
+ * stored-activation count (R32) is pinned for GPT-shaped layers to
+ * Korthikanti et al. 2022; its gated-MLP and MoE terms are parity unpinned
+ * beyond the reduction of a one-expert top-1 MoE layer to a gated dense one.
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -69,6 +75,7 @@ static uint64_t umax(uint64_t a, uint64_t b) { return a > b ? a : b; }
 typedef struct {
   uint64_t L, h, heads, kv_heads, ffn, gated, vocab, learned_pos, seq, e;
   uint64_t gbs, n_mbs, mbs[4], grad_bytes, param_bytes, E, topk, effn;
+  uint64_t opt_bytes; /* optimizer-state bytes per parameter (R31) */
   uint32_t* q; /* [L][E] expert shares in units of 2^-16 */
 } or_model;
 
@@ -78,6 +85,8 @@ typedef struct {
   uint64_t intra[OR_MAXK], pcie[OR_MAXK], nic[OR_MAXK];
   uint64_t a_intra[OR_MAXK], a_pcie[OR_MAXK], a_nic[OR_MAXK];
   uint64_t dev_off[OR_MAXK], node_off[OR_MAXK];
+  uint64_t mem[OR_MAXK]; /* device memory capacity in bytes (R34) */
+  int mem_check;         /* 0: capacities not given, memory not checked */
   uint32_t* nic_dev;    /* NULL or per-device NIC MB/s, pool order */
   uint32_t* intra_node; /* NULL or per-node intra MB/s, pool order */
 } or_cluster;
@@ -221,6 +230,38 @@ static uint64_t layer_params_expert(const or_ctx* x, uint64_t t, uint64_t ep) {
 static uint64_t embed_params(const or_ctx* x, uint64_t t) { return x->Vp * x->m.h / t + x->m.learned_pos * x->m.h; }
 static uint64_t head_params(const or_ctx* x, uint64_t t) { return x->Vp * x->m.h / t + x->m.h; }
 
+/* R32: bytes one TP rank keeps from the forward pass of one transformer
+ * layer for its backward pass, for a micro-batch of b sequences: the inputs
+ * of the layer's ops (the stored-activation count of Korthikanti et al.
+ * 2022, "Reducing Activation Recomputation in Large Transformer Models",
+ * without dropout masks and without the s x s attention scores, which a
+ * fused attention kernel recomputes).  No sequence parallelism: the inputs
+ * of the norms and of the first projections are full width on every rank.
+ * Counted per token, in elements: */
+static uint64_t layer_act_bytes(const or_ctx* x, uint64_t t, uint64_t b) {
+  const or_model* m = &x->m;
+  uint64_t h = m->h, hd = h / m->heads, hq = h / t, hkv = m->kv_heads * hd / t;
+  uint64_t w = 0;
+  w += h;                          /* input of the first norm */
+  w += h;                          /* normed input of the QKV projection */
+  w += hq + 2 * hkv;               /* Q, K and V, inputs of the attention core */
+  w += hq;                         /* attention output, input of the output projection */
+  w += h;                          /* input of the second norm */
+  if (m->E == 0) {
+    uint64_t ft = m->ffn / t;
+    w += h;                        /* normed input of the up (and gate) projection */
+    w += m->gated ? 2 * ft : ft;   /* up (and gate) outputs, inputs of the activation */
+    w += ft;                       /* activation output, input of the down projection */
+  } else {
+    uint64_t ft = m->effn / t;
+    w += h;                        /* normed input of the router */
+    /* each token goes to topk experts (balanced, R32); per routed copy: the
+     * expert's input, its up and gate outputs, its down projection's input */
+    w += m->topk * (h + 3 * ft);
+  }
+  return mul(m->e, mul(b * m->seq, w));
+}
+
 /* ------------------------------------------------------------------ */
 /* links (R3, R4, R5)                                                  */
 /* ------------------------------------------------------------------ */
@@ -342,7 +383,7 @@ typedef struct {
   uint64_t time;
 } or_detail;
 
-static int decode(const or_ctx* x, uint32_t hdr, const uint8_t* cut, const uint32_t* cls,
+static int decode_rules(const or_ctx* x, uint32_t hdr, const uint8_t* cut, const uint32_t* cls,
                   const uint64_t* types, int64_t stride, int64_t i, or_plan* p) {
   const or_model* m = &x->m;
   if (hdr >> 13) return 0;                                   /* V7 reserved bits */
@@ -390,6 +431,50 @@ static int decode(const or_ctx* x, uint32_t hdr, const uint8_t* cut, const uint3
     for (uint64_t s = 0; s < p->S; ++s) need[p->type[g][s]] += p->reps[g] * p->tp;
   for (uint64_t k = 0; k < x->c.K; ++k)
     if (need[k] > x->c.n_nodes[k] * x->c.dpn[k]) return 0;
+  return 1;
+}
+
+/* R33: micro-batches whose activations stage s holds at once under 1F1B.
+ * The stage runs W = min(S-1-s, M) forwards before its first backward,
+ * then alternates forward and backward, so right after each of those
+ * forwards it holds W+1 of them (all M when M <= W). */
+static uint64_t in_flight(uint64_t S, uint64_t M, uint64_t s) {
+  uint64_t W = (S - 1 - s) < M ? (S - 1 - s) : M;
+  return W + 1 < M ? W + 1 : M;
+}
+
+/* R31: peak bytes on one device of stage s of class g.  Every replica keeps
+ * the weights and gradients of the parameters its TP rank holds; the
+ * optimizer state is kept whole, or, with ZeRO, split over the stage's DP
+ * group (the same groups the gradient sync uses: all replicas for the
+ * non-expert parameters, replicas/EP for the experts), rounded up; the
+ * activations of the in-flight micro-batches come on top (R32, R33). */
+static uint64_t stage_mem(const or_ctx* x, const or_plan* p, uint64_t g, uint64_t s) {
+  const or_model* m = &x->m;
+  uint64_t tp = p->tp, ep = p->ep;
+  uint64_t lo = s ? p->cut[s - 1] : 0, ns = p->cut[s] - lo;
+  uint64_t pd = mul(ns, layer_params_dense(x, tp)), pe = mul(ns, layer_params_expert(x, tp, ep));
+  if (s == 0) pd = add(pd, embed_params(x, tp));
+  if (s == p->S - 1) pd = add(pd, head_params(x, tp));
+  uint64_t p_all = 0;
+  for (uint64_t c = 0; c < p->G; ++c) p_all += p->reps[c];
+  uint64_t wg = mul(add(m->param_bytes, m->grad_bytes), add(pd, pe));
+  uint64_t opt;
+  if (p->zero) opt = add(cdiv(mul(m->opt_bytes, pd), p_all), cdiv(mul(m->opt_bytes, pe), p_all / ep));
+  else opt = mul(m->opt_bytes, add(pd, pe));
+  uint64_t M = cdiv(p->nmb[g], p->reps[g]);
+  uint64_t act = mul(mul(ns, layer_act_bytes(x, tp, m->mbs[p->mi])), in_flight(p->S, M, s));
+  return add(add(wg, opt), act);
+}
+
+/* V9 (R34): when capacities are given, every device of the plan fits. */
+static int decode(const or_ctx* x, uint32_t hdr, const uint8_t* cut, const uint32_t* cls,
+                  const uint64_t* types, int64_t stride, int64_t i, or_plan* p) {
+  if (!decode_rules(x, hdr, cut, cls, types, stride, i, p)) return 0;
+  if (!x->c.mem_check) return 1;
+  for (uint64_t g = 0; g < p->G; ++g)
+    for (uint64_t s = 0; s < p->S; ++s)
+      if (stage_mem(x, p, g, s) > x->c.mem[p->type[g][s]]) return 0;
   return 1;
 }
 
@@ -545,9 +630,10 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
 /* context                                                             */
 /* ------------------------------------------------------------------ */
 /* mp: L h heads kv_heads ffn gated vocab learned_pos seq e gbs n_mbs mbs0..3
- *     grad_bytes param_bytes E topk effn  (21 words)
+ *     grad_bytes param_bytes E topk effn opt_bytes  (22 words)
  * cp: K, then for each type k: n_nodes dpn tflops hbm intra pcie nic
- *     a_intra a_pcie a_nic  (1 + 10K words) */
+ *     a_intra a_pcie a_nic mem  (1 + 11K words; mem = device memory in
+ *     bytes, 0 for every type = memory not checked) */
 or_ctx* oracle_new(const uint64_t* mp, const uint32_t* q, const uint64_t* cp,
                    const uint32_t* nic_dev, const uint32_t* intra_node) {
   or_ctx* x = (or_ctx*)calloc(1, sizeof(or_ctx));
@@ -556,6 +642,7 @@ or_ctx* oracle_new(const uint64_t* mp, const uint32_t* q, const uint64_t* cp,
   m->vocab = mp[6]; m->learned_pos = mp[7]; m->seq = mp[8]; m->e = mp[9]; m->gbs = mp[10]; m->n_mbs = mp[11];
   for (int i = 0; i < 4; ++i) m->mbs[i] = mp[12 + i];
   m->grad_bytes = mp[16]; m->param_bytes = mp[17]; m->E = mp[18]; m->topk = mp[19]; m->effn = mp[20];
+  m->opt_bytes = mp[21];
   if (m->E) {
     m->q = (uint32_t*)malloc(sizeof(uint32_t) * m->L * m->E);
     memcpy(m->q, q, sizeof(uint32_t) * m->L * m->E);
@@ -564,10 +651,12 @@ or_ctx* oracle_new(const uint64_t* mp, const uint32_t* q, const uint64_t* cp,
   c->K = cp[0];
   uint64_t dsum = 0, nsum = 0;
   for (uint64_t k = 0; k < c->K; ++k) {
-    const uint64_t* r = cp + 1 + 10 * k;
+    const uint64_t* r = cp + 1 + 11 * k;
     c->n_nodes[k] = r[0]; c->dpn[k] = r[1]; c->tflops[k] = r[2]; c->hbm[k] = r[3];
     c->intra[k] = r[4]; c->pcie[k] = r[5]; c->nic[k] = r[6];
     c->a_intra[k] = r[7]; c->a_pcie[k] = r[8]; c->a_nic[k] = r[9];
+    c->mem[k] = r[10];
+    if (r[10]) c->mem_check = 1;
     c->dev_off[k] = dsum; c->node_off[k] = nsum;
     dsum += r[0] * r[1]; nsum += r[0];
   }
@@ -689,3 +778,17 @@ uint64_t oracle_rank_params(const or_ctx* x, uint64_t t, uint64_t ep, uint64_t n
   return nlayers * (layer_params_dense(x, t) + layer_params_expert(x, t, ep));
 }
 uint64_t oracle_act_bytes(const or_ctx* x, uint64_t b) { return b * x->m.seq * x->m.h * x->m.e; }
+uint64_t oracle_layer_act_bytes(const or_ctx* x, uint64_t t, uint64_t b) { return layer_act_bytes(x, t, b); }
+uint64_t oracle_in_flight(uint64_t S, uint64_t M, uint64_t s) { return in_flight(S, M, s); }
+/* Peak memory of every (class, stage) device of plan i into mem[c*16 + s]
+ * (entries of absent classes and stages 0).  Returns 0 if the plan breaks
+ * a rule other than the memory check (mem then all 0), else 1. */
+int oracle_stage_mem(const or_ctx* x, const uint32_t* hdr, const uint8_t* cut, const uint32_t* cls,
+                     const uint64_t* types, int64_t stride, int64_t i, uint64_t* mem) {
+  memset(mem, 0, 8 * OR_MAXG * OR_MAXS);
+  or_plan p;
+  if (!decode_rules(x, hdr[i], cut, cls, types, stride, i, &p)) return 0;
+  for (uint64_t g = 0; g < p.G; ++g)
+    for (uint64_t s = 0; s < p.S; ++s) mem[g * OR_MAXS + s] = stage_mem(x, &p, g, s);
+  return 1;
+}

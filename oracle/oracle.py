@@ -63,6 +63,12 @@ def lib():
         L.oracle_rank_params.restype = u64
         L.oracle_act_bytes.argtypes = [P, u64]
         L.oracle_act_bytes.restype = u64
+        L.oracle_layer_act_bytes.argtypes = [P, u64, u64]
+        L.oracle_layer_act_bytes.restype = u64
+        L.oracle_in_flight.argtypes = [u64, u64, u64]
+        L.oracle_in_flight.restype = u64
+        L.oracle_stage_mem.argtypes = [P, P, P, P, P, C.c_int64, C.c_int64, P]
+        L.oracle_stage_mem.restype = C.c_int
         assert L.oracle_detail_size() == C.sizeof(_Detail)
         _lib = L
     return _lib
@@ -80,7 +86,7 @@ def _model_words(m):
     mbs = list(m["mbs"]) + [0] * (4 - len(m["mbs"]))
     w = [m[k] for k in MODEL_KEYS] + [len(m["mbs"])] + mbs + [
         m.get("grad_bytes", 4), m.get("param_bytes", 2), m.get("experts", 0), m.get("topk", 0),
-        m.get("expert_ffn", 0)]
+        m.get("expert_ffn", 0), m.get("opt_bytes", 12)]
     return np.array(w, dtype=np.uint64)
 
 
@@ -91,7 +97,7 @@ TYPE_KEYS = ("n_nodes", "dev_per_node", "tflops", "hbm_GBps", "intra_MBps", "pci
 def _cluster_words(c):
     w = [len(c["types"])]
     for t in c["types"]:
-        w += [t[k] for k in TYPE_KEYS]
+        w += [t[k] for k in TYPE_KEYS] + [t.get("mem_bytes") or 0]
     return np.array(w, dtype=np.uint64)
 
 
@@ -168,6 +174,21 @@ class Oracle:
     def act_bytes(self, b):
         return lib().oracle_act_bytes(self.h, b)
 
+    def layer_act_bytes(self, t, b):
+        return lib().oracle_layer_act_bytes(self.h, t, b)
+
+    def stage_mem(self, plans, i):
+        """[4][16] peak bytes per (class, stage) device of plan i, or None if a rule other than
+        the memory check rejects the plan."""
+        hdr = np.ascontiguousarray(plans["hdr"], dtype=np.uint32)
+        cut = np.ascontiguousarray(plans["cut"], dtype=np.uint8)
+        cls = np.ascontiguousarray(plans["cls"], dtype=np.uint32)
+        typ = np.ascontiguousarray(plans["types"], dtype=np.uint64)
+        mem = np.zeros((4, 16), dtype=np.uint64)
+        ok = lib().oracle_stage_mem(self.h, _ptr(hdr), _ptr(cut), _ptr(cls), _ptr(typ), cut.shape[1], int(i),
+                                    _ptr(mem))
+        return mem if ok else None
+
 
 def pipeline(S, M, f, b, c):
     """End time of each stage's last op for one 1F1B pipeline (c has S-1 hops)."""
@@ -177,6 +198,10 @@ def pipeline(S, M, f, b, c):
     end = np.zeros(S, dtype=np.uint64)
     lib().oracle_pipeline(S, M, _ptr(fa), _ptr(ba), _ptr(ca), _ptr(end))
     return [int(v) for v in end]
+
+
+def in_flight(S, M, s):
+    return lib().oracle_in_flight(S, M, s)
 
 
 def alpha_ps(gbps_unidir):

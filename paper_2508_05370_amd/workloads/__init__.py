@@ -8,7 +8,7 @@ and interconnect delays from the jumbo-frame formula of Sec. 5.
 
 Randomness is SplitMix64 used counter-based (see plangen.c); cluster seeds are
 0xC1A50000 + config, plan seeds 0x91A70000 + config, expert-load seed
-0xD1210004.
+0xD1210004, device-memory seeds 0xC1A60000 + config.
 """
 import ctypes as C
 import itertools
@@ -110,7 +110,7 @@ MODELS = {
 
 
 def model(name, **over):
-    m = dict(grad_bytes=4, param_bytes=2, experts=0, topk=0, expert_ffn=0, load_q16=None)
+    m = dict(grad_bytes=4, param_bytes=2, opt_bytes=12, experts=0, topk=0, expert_ffn=0, load_q16=None)
     m.update(MODELS[name])
     m.update(over)
     return m
@@ -176,6 +176,23 @@ def cluster_random(cfg, nodes, dpn=8, nic_choices=(100, 200, 400), pcie=True, ji
         c["nic_MBps_dev"] = np.array(dev, dtype=np.uint32)
         c["intra_MBps_node"] = np.array(node, dtype=np.uint32)
     return c
+
+
+# device memory sizes of accelerators of the last generations, GiB (Table 5's
+# A100 40 GB and H100 80 GB among them)
+MEM_GIB = (16, 24, 32, 40, 48, 64, 80, 96, 128, 141, 192, 288)
+
+
+def with_memory(w, gib=None):
+    """Copy of workload w whose device types have a memory capacity: `gib` per type, or drawn per type
+    from MEM_GIB with the seed 0xC1A60000 + the workload's index."""
+    types = [dict(t) for t in w["cluster"]["types"]]
+    if gib is None:
+        st = Stream(0xC1A60000 + w["index"])
+        gib = [MEM_GIB[st.uni(0, len(MEM_GIB) - 1)] for _ in types]
+    for t, g in zip(types, gib):
+        t["mem_bytes"] = int(g) << 30
+    return dict(w, name=w["name"] + "/mem", cluster=dict(w["cluster"], types=types))
 
 
 # ---------------------------------------------------------------- plans
@@ -251,22 +268,22 @@ def enumerate_two_type_8(L=12, n_dev=8, per_type=4, batches=8):
 def workload(idx):
     """Workload idx in 1..5: dict(name, model, cluster, n_plans, seed)."""
     if idx == 1:
-        return dict(name="gpt2-small/8dev-2type/exhaustive", model=model("gpt2-small"), cluster=cluster_two_type_8(),
-                    n_plans=29470, seed=None)
+        return dict(index=1, name="gpt2-small/8dev-2type/exhaustive", model=model("gpt2-small"),
+                    cluster=cluster_two_type_8(), n_plans=29470, seed=None)
     if idx == 2:
-        return dict(name="llama-7b/64dev-3type/1M", model=model("llama-7b"),
+        return dict(index=2, name="llama-7b/64dev-3type/1M", model=model("llama-7b"),
                     cluster=cluster_random(2, [3, 3, 2]), n_plans=1 << 20, seed=0x91A70002)
     if idx == 3:
-        return dict(name="llama-70b/512dev-4type-jitter/16M", model=model("llama-70b"),
+        return dict(index=3, name="llama-70b/512dev-4type-jitter/16M", model=model("llama-70b"),
                     cluster=cluster_random(3, [16, 16, 16, 16], nic_choices=(200, 400), pcie=False, jitter=True),
                     n_plans=1 << 24, seed=0x91A70003)
     if idx == 4:
         m = model("mixtral-8x7b")
         m["load_q16"] = dirichlet_q16(m["L"], m["experts"])
-        return dict(name="mixtral-8x7b/256dev-3type/4M", model=m, cluster=cluster_random(4, [11, 11, 10]),
+        return dict(index=4, name="mixtral-8x7b/256dev-3type/4M", model=m, cluster=cluster_random(4, [11, 11, 10]),
                     n_plans=1 << 22, seed=0x91A70004)
     if idx == 5:
-        return dict(name="gpt3-175b/4096dev-6type-3tier/64M", model=model("gpt3-175b"),
+        return dict(index=5, name="gpt3-175b/4096dev-6type-3tier/64M", model=model("gpt3-175b"),
                     cluster=cluster_random(5, [86, 86, 85, 85, 85, 85], pcie_only_types=(4, 5), alpha_mult=True),
                     n_plans=1 << 26, seed=0x91A70005)
     raise ValueError(idx)
