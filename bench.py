@@ -90,6 +90,8 @@ def main():
                     help="evaluate in chunks of this many plans on --streams streams, one argmin slot per chunk "
                          "reduced on the device (0 = one call over all plans)")
     ap.add_argument("--streams", type=int, default=2)
+    ap.add_argument("--mem-steps", type=int, default=5,
+                    help="also time the same plans with per-type device memory checked (0 = skip)")
     ap.add_argument("--copy-calibrate", type=int, default=0, metavar="BYTES",
                     help="only run a device-to-device copy of BYTES (reference for HBM byte counters)")
     a = ap.parse_args()
@@ -198,6 +200,28 @@ def main():
                  "deferred_pass_ms_per_step": round(defer_ms / timed, 4),
                  "eval_call_ms_per_step": round(call_ms / timed, 4)}
 
+    # The same sweep with device memory capacities: plans that do not fit become invalid
+    mem = None
+    if a.mem_steps > 0 and not a.chunk:
+        wm = W.with_memory(w)
+        simm = B.Sim(wm["model"], wm["cluster"])
+        simm.eval_plans(dp, out=out)
+        simm.argmin(out, out=best)
+        torch.cuda.synchronize()
+        m0 = time.perf_counter()
+        for _ in range(a.mem_steps):
+            simm.eval_plans(dp, out=out)
+            simm.argmin(out, out=best)
+        torch.cuda.synchronize()
+        m1 = time.perf_counter()
+        fit = int(np.count_nonzero(B.times_u64(out) != MAXU))
+        mb_t, mb_i = B.best_tuple(best)
+        mem = {"workload": wm["name"], "memory_GiB": [t["mem_bytes"] >> 30 for t in wm["cluster"]["types"]],
+               "plans_per_s": round(n * a.mem_steps / (m1 - m0), 1), "steps": a.mem_steps,
+               "ms_per_step": round((m1 - m0) / a.mem_steps * 1e3, 4), "feasible_plans": fit,
+               "argmin": [mb_i, mb_t]}
+        simm.close()
+
     # CPU baseline: the oracle as it stands, on a bounded prefix of the same plans
     cpu = None
     if a.cpu_seconds > 0:
@@ -226,6 +250,7 @@ def main():
                       "argmin": [best_i, best_t], "mean_pipeline_ops_per_plan": round(float(ops.mean()), 1)},
            "roofline": roof, "cpu_baseline": cpu}
     rec.update(extra)
+    rec["memory_check"] = mem
     print(json.dumps(rec), flush=True)
 
 

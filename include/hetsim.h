@@ -68,6 +68,8 @@ typedef struct {
   uint32_t expert_ffn;    /* width of one (gated) expert MLP */
   const uint32_t* load_q16; /* [n_layers][experts] token share of each expert in units of
                                2^-16, rows summing to 65536; NULL iff experts == 0 */
+  uint32_t opt_bytes;     /* optimizer-state bytes per parameter, 0..64 (12 = fp32 master
+                             weights and two Adam moments); used by the memory check only */
 } sim_model_desc;
 
 /*
@@ -93,6 +95,8 @@ typedef struct {
   const uint64_t* nic_alpha_ps;     /* [K] NIC processing latency per side */
   const uint32_t* nic_MBps_dev;     /* optional [total devices] per-device NIC rate (overrides nic_MBps) */
   const uint32_t* intra_MBps_node;  /* optional [total nodes] per-node fabric rate (overrides intra_MBps) */
+  const uint64_t* mem_bytes;        /* optional [K] device memory in bytes, each >= 1 (Table 5 names
+                                       A100 40 GB and H100 80 GB); NULL = memory not checked */
 } sim_cluster_desc;
 
 /*
@@ -110,8 +114,9 @@ typedef struct {
  * A plan that breaks any rule (ranges, divisibility of heads/widths by TP,
  * TP within a node, EP dividing every class's replicas, capacity of every
  * device pool, micro-batches summing to the global batch, at least one
- * micro-batch per replica) evaluates to SIM_TIME_INVALID; that is not an
- * error.
+ * micro-batch per replica, and, when the cluster gives mem_bytes, the peak
+ * memory of every device as sim_eval_memory defines it) evaluates to
+ * SIM_TIME_INVALID; that is not an error.
  */
 typedef struct {
   const uint32_t* hdr;
@@ -165,6 +170,30 @@ int sim_eval_plans(sim_ctx* ctx, const sim_plans* plans, int64_t n, uint64_t* ou
  */
 int sim_eval_stages(sim_ctx* ctx, const sim_plans* plans, int64_t n, uint64_t* out_stage, uint32_t* out_class,
                     void* stream);
+
+/*
+ * Peak device memory of plans 0..n-1: out_mem[(i*4 + c)*16 + s] (device
+ * memory, caller-owned) = bytes one device of stage s of class c holds at
+ * once.  Parallelism exists to fit the model in device memory (Sec. 2) and
+ * device types differ in it (Sec. 3 example, Table 5), so with mem_bytes
+ * given a plan is feasible only if every device fits.  The bytes are
+ *   (param_bytes + grad_bytes) * P                 weights and gradients
+ * + opt_bytes * P, or with ZeRO ceil(opt_bytes * P_dense / replicas)
+ *   + ceil(opt_bytes * P_expert / (replicas / EP)) optimizer state, split
+ *   over the stage's DP group as its gradient sync is
+ * + layers * A * min(PP - s, M)                    stored activations
+ * where P is the parameters the device's TP rank holds for the stage's
+ * layers (and the embedding on the first stage, the head on the last), A
+ * the bytes one layer keeps for its backward pass per micro-batch (the
+ * inputs of its ops: the stored-activation count of Korthikanti et al.
+ * 2022 without dropout masks and attention scores; routed MoE tokens
+ * counted at the balanced top-k share) and min(PP - s, M) the micro-batches
+ * stage s holds at once under 1F1B.  Entries of absent classes and stages
+ * are 0; all 64 entries of a plan that breaks another rule are
+ * SIM_TIME_INVALID.  The memory check itself does not affect this output.
+ * n is at most 2^21 per call.  Errors as sim_eval_plans.
+ */
+int sim_eval_memory(sim_ctx* ctx, const sim_plans* plans, int64_t n, uint64_t* out_mem, void* stream);
 
 /*
  * Lexicographic minimum of (time_ps[i], index_base + i) over i < n, written

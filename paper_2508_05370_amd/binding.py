@@ -24,13 +24,13 @@ class ModelDesc(C.Structure):
                 ("seq", C.c_uint32), ("dtype_bytes", C.c_uint32), ("global_batch", C.c_uint32),
                 ("n_mbs", C.c_uint32), ("mbs", C.c_uint32 * 4), ("grad_bytes", C.c_uint32),
                 ("param_bytes", C.c_uint32), ("experts", C.c_uint32), ("topk", C.c_uint32),
-                ("expert_ffn", C.c_uint32), ("load_q16", C.c_void_p)]
+                ("expert_ffn", C.c_uint32), ("load_q16", C.c_void_p), ("opt_bytes", C.c_uint32)]
 
 
 class ClusterDesc(C.Structure):
     _fields_ = [("n_types", C.c_uint32)] + [(k, C.c_void_p) for k in (
         "n_nodes", "dev_per_node", "tflops", "hbm_GBps", "intra_MBps", "pcie_MBps", "nic_MBps", "intra_alpha_ps",
-        "pcie_alpha_ps", "nic_alpha_ps", "nic_MBps_dev", "intra_MBps_node")]
+        "pcie_alpha_ps", "nic_alpha_ps", "nic_MBps_dev", "intra_MBps_node", "mem_bytes")]
 
 
 class Plans(C.Structure):
@@ -42,7 +42,7 @@ class Best(C.Structure):
     _fields_ = [("time_ps", C.c_uint64), ("index", C.c_int64)]
 
 
-EXPORTS = ("sim_create", "sim_eval_plans", "sim_eval_stages", "sim_argmin", "sim_best_reduce", "sim_set_timing",
+EXPORTS = ("sim_create", "sim_eval_plans", "sim_eval_stages", "sim_eval_memory", "sim_argmin", "sim_best_reduce", "sim_set_timing",
            "sim_get_timing", "sim_get_skipped_ops", "sim_destroy", "sim_strerror")
 
 
@@ -61,6 +61,8 @@ def lib():
         L.sim_eval_plans.restype = C.c_int
         L.sim_eval_stages.argtypes = [P, C.POINTER(Plans), I64, P, P, P]
         L.sim_eval_stages.restype = C.c_int
+        L.sim_eval_memory.argtypes = [P, C.POINTER(Plans), I64, P, P]
+        L.sim_eval_memory.restype = C.c_int
         L.sim_argmin.argtypes = [P, P, I64, I64, P, P]
         L.sim_argmin.restype = C.c_int
         L.sim_best_reduce.argtypes = [P, P, I64, P, P]
@@ -109,6 +111,7 @@ def model_desc(m):
         d.mbs[i] = v
     d.grad_bytes, d.param_bytes = m.get("grad_bytes", 4), m.get("param_bytes", 2)
     d.experts, d.topk, d.expert_ffn = m.get("experts", 0), m.get("topk", 0), m.get("expert_ffn", 0)
+    d.opt_bytes = m.get("opt_bytes", 12)
     keep = []
     q = m.get("load_q16")
     if q is not None:
@@ -137,6 +140,11 @@ def cluster_desc(c):
             a = _u32(c[key])
             keep.append(a)
             setattr(d, key, a.ctypes.data)
+    mem = [t.get("mem_bytes") for t in c["types"]]
+    if any(v is not None for v in mem):
+        a = _u64([v or 0 for v in mem])
+        keep.append(a)
+        d.mem_bytes = a.ctypes.data
     return d, keep
 
 
@@ -214,6 +222,16 @@ class Sim:
         _check(lib().sim_eval_stages(self.h, C.byref(ps), n, st.data_ptr(), cl.data_ptr(), _stream(stream)),
                "sim_eval_stages")
         return st, cl
+
+    def eval_memory(self, dp, n=None, stream=None):
+        """Peak bytes per (class, stage) device: int64 tensor [n, 4, 16] (uint64 bits)."""
+        import torch
+        if n is None:
+            n = dp["hdr"].shape[0]
+        mem = torch.empty((n, 4, 16), dtype=torch.int64, device=dp["hdr"].device)
+        ps = plans_struct(dp)
+        _check(lib().sim_eval_memory(self.h, C.byref(ps), n, mem.data_ptr(), _stream(stream)), "sim_eval_memory")
+        return mem
 
     def argmin(self, times, n=None, index_base=0, out=None, stream=None):
         """Lexicographic (time, index) minimum into a 2-word int64 tensor slot."""

@@ -14,6 +14,7 @@ namespace hetsim {
 hipError_t launch_fill32(uint32_t* p, uint32_t n, uint32_t v, hipStream_t s);
 hipError_t launch_prep(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, PackedPlan* packed,
                        uint32_t* meta, uint32_t* hist, hipStream_t s);
+hipError_t launch_memory(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, hipStream_t s);
 hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint32_t* meta, int64_t n, uint64_t* out_stage,
                          hipStream_t s);
 hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* sstart, hipStream_t s);
@@ -284,6 +285,14 @@ extern "C" int sim_eval_stages(sim_ctx* c, const sim_plans* plans, int64_t n, ui
   if (e == hipSuccess) e = launch_stages(c->tab, packed, out_class, n, out_stage, s);
   (void)hipFreeAsync(ws, s);
   return e == hipSuccess ? SIM_OK : SIM_EHIP;
+}
+
+extern "C" int sim_eval_memory(sim_ctx* c, const sim_plans* plans, int64_t n, uint64_t* out_mem, void* stream) {
+  if (!c || !plans_ok(plans, n) || (n > 0 && !out_mem)) return SIM_EINVAL;
+  if (n == 0) return SIM_OK;
+  if (n > kChunk) return SIM_EINVAL;
+  if (hipSetDevice(c->device) != hipSuccess) return SIM_EHIP;
+  return launch_memory(c->tab, *plans, n, out_mem, (hipStream_t)stream) == hipSuccess ? SIM_OK : SIM_EHIP;
 }
 
 extern "C" int sim_argmin(sim_ctx* c, const uint64_t* t, int64_t n, int64_t base, sim_best* out, void* stream) {

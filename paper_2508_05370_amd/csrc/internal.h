@@ -70,6 +70,10 @@ struct Tab {
   uint64_t par_layer[4];          // non-expert parameters of one layer on one TP rank, by log2 TP
   uint64_t par_expert[4][4];      // expert parameters of one layer per rank [log2 TP][log2 EP]
   uint64_t par_embed[4], par_head[4];
+  uint32_t mem_check;             // 1: device memory capacities given; plans must fit them
+  uint64_t mem_cap[kMaxTypes];    // device memory of type k, bytes
+  uint64_t opt_bytes;             // optimizer-state bytes per parameter
+  uint64_t act_layer[4][4];       // bytes one layer stores for backward per micro-batch [log2 TP][mbs index]
   uint32_t nep;                   // EP slots of the prefix tables
   uint32_t uniform_layers;        // 1: the layer table holds one layer's cost per row
   uint32_t o_pfb, o_emb, o_head, o_pa, o_rmi, o_rmn;   // section byte offsets (TypeInfo at 0)

@@ -141,6 +141,129 @@ __device__ __forceinline__ uint32_t class_mb(const Plan& p) { return (p.nc + p.r
 
 constexpr int kPrepPerThread = 4;
 
+// Plan i as loaded and checked by one lane: every rule of the plan layout
+// except the memory check.
+struct Checked {
+  bool ok;
+  uint32_t hdr, psum;
+  uint32_t cw[4];          // cut bytes, four per word
+  uint32_t cls[4];         // 0 past the class count
+  uint64_t tv[4];          // stage types, nibbles past PP cleared; 0 past the class count
+};
+
+__device__ __forceinline__ Checked check_plan(const Tab& t, const sim_plans& pl, int64_t i) {
+  Checked r;
+  const int64_t st = pl.stride;
+  // all 16 cut planes and 4 class planes exist: load them before any use
+  const uint32_t hdr = pl.hdr[i];
+  uint32_t cb[16];
+#pragma unroll
+  for (int s = 0; s < 16; ++s) cb[s] = pl.cut[s * st + i];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    r.cls[c] = pl.cls[c * st + i];
+    r.tv[c] = pl.types[c * st + i];
+  }
+  const uint32_t tpl = hdr & 3, epl = (hdr >> 2) & 3, S = ((hdr >> 4) & 15) + 1, G = ((hdr >> 8) & 3) + 1;
+  const uint32_t mi = (hdr >> 11) & 3;
+  const uint32_t tp = 1u << tpl, ep = 1u << epl;
+  bool ok = (hdr >> 13) == 0 && mi < t.n_mbs && ((t.tp_ok >> tpl) & 1) && ((t.ep_ok >> epl) & 1);
+  uint32_t prev = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) r.cw[j] = 0;
+#pragma unroll
+  for (uint32_t s = 0; s < 16; ++s) {
+    if (s < S) {
+      ok = ok && cb[s] > prev;
+      prev = cb[s];
+      r.cw[s >> 2] |= cb[s] << (8 * (s & 3));
+    }
+  }
+  ok = ok && prev == t.L;
+  const uint64_t sel = S == 16 ? ~0ull : ((1ull << (4 * S)) - 1);
+  uint32_t batch = 0, psum = 0;
+#pragma unroll
+  for (uint32_t c = 0; c < 4; ++c) {
+    if (c < G) {
+      r.tv[c] &= sel;
+      const uint32_t reps = r.cls[c] & 0xffff, nmb = r.cls[c] >> 16;
+      ok = ok && reps >= 1 && nmb >= reps && (reps & (ep - 1)) == 0;
+      batch += nmb * t.mbs[mi];
+      psum += reps;
+      // every stage's type exists and holds whole TP groups in a node
+      const uint32_t okm = t.type_ok[tpl];
+      for (uint32_t s = 0; s < S; ++s) ok = ok && ((okm >> ((uint32_t)(r.tv[c] >> (4 * s)) & 15)) & 1);
+    } else {
+      r.cls[c] = 0;
+      r.tv[c] = 0;
+    }
+  }
+  ok = ok && batch == t.gbs;
+  for (uint32_t k = 0; ok && k < t.K; ++k) {
+    uint32_t need = 0;
+#pragma unroll
+    for (uint32_t c = 0; c < 4; ++c)
+      if (c < G) need += (r.cls[c] & 0xffff) * count_type(r.tv[c], k, sel);
+    ok = need * tp <= t.cap[k];
+  }
+  r.ok = ok;
+  r.hdr = hdr;
+  r.psum = psum;
+  return r;
+}
+
+// Peak bytes of one device of stage s (layers lo..hi) apart from its stored
+// activations: weights and gradients of the parameters its TP rank holds,
+// and the optimizer state, split with ZeRO over the stage's DP group (all
+// replicas for the non-expert parameters, replicas / EP for the experts).
+__device__ __forceinline__ uint64_t state_bytes(const Tab& t, uint32_t hdr, uint32_t psum, uint32_t s, uint32_t ns) {
+  const uint32_t tpl = hdr & 3, epl = (hdr >> 2) & 3, S = ((hdr >> 4) & 15) + 1, zero = (hdr >> 10) & 1;
+  uint64_t pd = (uint64_t)ns * t.par_layer[tpl];
+  if (s == 0) pd += t.par_embed[tpl];
+  if (s == S - 1) pd += t.par_head[tpl];
+  const uint64_t pe = (uint64_t)ns * t.par_expert[tpl][epl];
+  uint64_t od = t.opt_bytes * pd, oe = t.opt_bytes * pe;
+  if (zero) {
+    const uint32_t pdx = psum >> epl;
+    od = (od + psum - 1) / psum;
+    oe = (oe + pdx - 1) / pdx;
+  }
+  return (t.param_bytes + t.grad_bytes) * (pd + pe) + od + oe;
+}
+
+// Peak bytes of the devices of stage s of every class: state plus the
+// activations of the min(PP - s, M) micro-batches 1F1B keeps in flight there.
+__device__ __forceinline__ uint64_t class_stage_bytes(const Tab& t, const Checked& r, uint32_t c, uint32_t s,
+                                                      uint32_t ns, uint64_t state) {
+  const uint32_t tpl = r.hdr & 3, S = ((r.hdr >> 4) & 15) + 1, mi = (r.hdr >> 11) & 3;
+  const uint32_t reps = r.cls[c] & 0xffff, M = ((r.cls[c] >> 16) + reps - 1) / reps;
+  const uint32_t fly = S - s < M ? S - s : M;
+  return state + (uint64_t)ns * fly * t.act_layer[tpl][mi];
+}
+
+// cut byte of stage s (run-time index) of a checked plan
+__device__ __forceinline__ uint32_t checked_cut(const Checked& r, uint32_t s) {
+  const uint64_t lo = (uint64_t)r.cw[0] | ((uint64_t)r.cw[1] << 32), hi = (uint64_t)r.cw[2] | ((uint64_t)r.cw[3] << 32);
+  const uint64_t m = 0ull - (uint64_t)(s >> 3);
+  return (uint32_t)(((lo & ~m) | (hi & m)) >> (8 * (s & 7))) & 0xff;
+}
+
+// Every device of a checked plan fits its type's memory.
+__device__ __forceinline__ bool fits_memory(const Tab& t, const Checked& r) {
+  const uint32_t S = ((r.hdr >> 4) & 15) + 1, G = ((r.hdr >> 8) & 3) + 1;
+  bool ok = true;
+  uint32_t prev = 0;
+  for (uint32_t s = 0; s < S; ++s) {
+    const uint32_t cut = checked_cut(r, s), ns = cut - prev;
+    prev = cut;
+    const uint64_t state = state_bytes(t, r.hdr, r.psum, s, ns);
+#pragma unroll
+    for (uint32_t c = 0; c < 4; ++c)
+      if (c < G) ok = ok && class_stage_bytes(t, r, c, s, ns, state) <= t.mem_cap[(uint32_t)(r.tv[c] >> (4 * s)) & 15];
+  }
+  return ok;
+}
+
 // Decode and check plan i (every rule of the plan layout); on success pack it.
 // Writes out[i] (0 = valid, to be raised by the pipelines; else invalid) and
 // the per-pipeline metadata S | G << 5 | M << 8 (0 = no pipeline).
@@ -155,73 +278,23 @@ __global__ void __launch_bounds__(256) k_prep(Tab t, sim_plans pl, int64_t n, ui
   for (int rep = 0; rep < kPrepPerThread; ++rep) {
     const int64_t i = ((int64_t)blockIdx.x * kPrepPerThread + rep) * blockDim.x + threadIdx.x;
     if (i >= n) break;
-    const int64_t st = pl.stride;
-    // all 16 cut planes and 4 class planes exist: load them before any use
-    const uint32_t hdr = pl.hdr[i];
-    uint32_t cb[16];
-#pragma unroll
-    for (int s = 0; s < 16; ++s) cb[s] = pl.cut[s * st + i];
-    uint32_t cls[4];
-    uint64_t tv[4];
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      cls[c] = pl.cls[c * st + i];
-      tv[c] = pl.types[c * st + i];
-    }
-    const uint32_t tpl = hdr & 3, epl = (hdr >> 2) & 3, S = ((hdr >> 4) & 15) + 1, G = ((hdr >> 8) & 3) + 1;
-    const uint32_t mi = (hdr >> 11) & 3;
-    const uint32_t tp = 1u << tpl, ep = 1u << epl;
-    bool ok = (hdr >> 13) == 0 && mi < t.n_mbs && ((t.tp_ok >> tpl) & 1) && ((t.ep_ok >> epl) & 1);
-    uint32_t cw[4] = {0, 0, 0, 0}, prev = 0;
-#pragma unroll
-    for (uint32_t s = 0; s < 16; ++s) {
-      if (s < S) {
-        ok = ok && cb[s] > prev;
-        prev = cb[s];
-        cw[s >> 2] |= cb[s] << (8 * (s & 3));
-      }
-    }
-    ok = ok && prev == t.L;
-    const uint64_t sel = S == 16 ? ~0ull : ((1ull << (4 * S)) - 1);
-    uint32_t batch = 0, psum = 0;
-#pragma unroll
-    for (uint32_t c = 0; c < 4; ++c) {
-      if (c < G) {
-        tv[c] &= sel;
-        const uint32_t reps = cls[c] & 0xffff, nmb = cls[c] >> 16;
-        ok = ok && reps >= 1 && nmb >= reps && (reps & (ep - 1)) == 0;
-        batch += nmb * t.mbs[mi];
-        psum += reps;
-        // every stage's type exists and holds whole TP groups in a node
-        const uint32_t okm = t.type_ok[tpl];
-        for (uint32_t s = 0; s < S; ++s) ok = ok && ((okm >> ((uint32_t)(tv[c] >> (4 * s)) & 15)) & 1);
-      } else {
-        cls[c] = 0;
-        tv[c] = 0;
-      }
-    }
-    ok = ok && batch == t.gbs;
-    for (uint32_t k = 0; ok && k < t.K; ++k) {
-      uint32_t need = 0;
-#pragma unroll
-      for (uint32_t c = 0; c < 4; ++c)
-        if (c < G) need += (cls[c] & 0xffff) * count_type(tv[c], k, sel);
-      ok = need * tp <= t.cap[k];
-    }
+    const Checked r = check_plan(t, pl, i);
+    const bool ok = r.ok && (!t.mem_check || fits_memory(t, r));
+    const uint32_t S = ((r.hdr >> 4) & 15) + 1, G = ((r.hdr >> 8) & 3) + 1;
     if (out) out[i] = ok ? 0 : kInvalid;
     if (ok) {
       PackedPlan q;
-      q.hdr = hdr; q.psum = psum; q.pad0 = 0; q.pad1 = 0;
+      q.hdr = r.hdr; q.psum = r.psum; q.pad0 = 0; q.pad1 = 0;
       uint32_t* qc = reinterpret_cast<uint32_t*>(q.cut);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) { qc[j] = cw[j]; q.cls[j] = cls[j]; q.types[j] = tv[j]; }
+      for (int j = 0; j < 4; ++j) { qc[j] = r.cw[j]; q.cls[j] = r.cls[j]; q.types[j] = r.tv[j]; }
       packed[i] = q;
     }
 #pragma unroll
     for (uint32_t c = 0; c < 4; ++c) {
       uint32_t m = 0;
       if (ok && c < G) {
-        const uint32_t reps = cls[c] & 0xffff, M = ((cls[c] >> 16) + reps - 1) / reps;
+        const uint32_t reps = r.cls[c] & 0xffff, M = ((r.cls[c] >> 16) + reps - 1) / reps;
         m = S | (G << 5) | (M << 8);
         if (hist) atomicAdd(&lh[bucket_key(S, G, M)], 1u);
       }
@@ -232,6 +305,27 @@ __global__ void __launch_bounds__(256) k_prep(Tab t, sim_plans pl, int64_t n, ui
     __syncthreads();
     for (uint32_t j = threadIdx.x; j < kBuckets; j += blockDim.x)
       if (lh[j]) atomicAdd(&hist[j], lh[j]);
+  }
+}
+
+// Peak memory of every (class, stage) device of plan i (one plan per lane).
+__global__ void __launch_bounds__(256) k_memory(Tab t, sim_plans pl, int64_t n, uint64_t* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const Checked r = check_plan(t, pl, i);
+  const uint32_t S = ((r.hdr >> 4) & 15) + 1, G = ((r.hdr >> 8) & 3) + 1;
+  uint64_t* o = out + i * (kMaxClasses * kMaxStages);
+  uint32_t prev = 0;
+  for (uint32_t s = 0; s < (uint32_t)kMaxStages; ++s) {
+    const uint32_t cut = s < S ? checked_cut(r, s) : prev, ns = cut - prev;
+    prev = cut;
+    const uint64_t state = r.ok && s < S ? state_bytes(t, r.hdr, r.psum, s, ns) : 0;
+#pragma unroll
+    for (uint32_t c = 0; c < 4; ++c) {
+      uint64_t v = kInvalid;
+      if (r.ok) v = c < G && s < S ? class_stage_bytes(t, r, c, s, ns, state) : 0;
+      o[c * kMaxStages + s] = v;
+    }
   }
 }
 
@@ -350,7 +444,7 @@ __device__ __forceinline__ uint64_t stage_dp(const Tab& t, const Hot<kMode>& h, 
 template <int kMode, typename Sink>
 __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t c,
                                             Sink& sink) {
-  const uint32_t S = p.S, G = p.G, tp = p.tp, ep = p.ep, tpl = p.tpl, epl = p.epl, mi = p.mi;
+  const uint32_t S = p.S, tp = p.tp, ep = p.ep, tpl = p.tpl, epl = p.epl, mi = p.mi;
   const uint64_t act = t.act[mi], act_tp = (act + tp - 1) >> tpl;
   const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> epl);
   const uint32_t L1 = t.L + 1, epq = t.E ? p.epl : 0;
@@ -977,6 +1071,11 @@ hipError_t launch_prep(const Tab& t, const sim_plans& p, int64_t n, uint64_t* ou
   k_prep<<<blocks_for(n, 256 * kPrepPerThread), 256, 0, s>>>(t, p, n, out, packed, meta, hist);
   return hipGetLastError();
 }
+hipError_t launch_memory(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, hipStream_t s) {
+  k_memory<<<blocks_for(n, 256), 256, 0, s>>>(t, p, n, out);
+  return hipGetLastError();
+}
+
 hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint32_t* meta, int64_t n, uint64_t* out_stage,
                          hipStream_t s) {
   k_stages<<<blocks_for(n * 4, 256), 256, 0, s>>>(t, packed, meta, n, out_stage);

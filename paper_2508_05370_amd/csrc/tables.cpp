@@ -182,6 +182,7 @@ int build_tables(const sim_model_desc* md, const sim_cluster_desc* cd, HostTable
   for (uint32_t i = 0; i < md->n_mbs; ++i)
     if (md->mbs[i] < 1 || md->mbs[i] > 1024) return INV;
   if (md->grad_bytes < 1 || md->grad_bytes > 16 || md->param_bytes < 1 || md->param_bytes > 16) return INV;
+  if (md->opt_bytes > 64) return INV;
   if (md->experts > 256) return INV;
   if (md->experts == 0) {
     if (md->ffn < 1 || md->ffn > (1u << 20)) return INV;
@@ -212,6 +213,7 @@ int build_tables(const sim_model_desc* md, const sim_cluster_desc* cd, HostTable
     if (cd->nic_MBps[k] < 16) return INV;
     if (cd->intra_alpha_ps[k] > kMaxAlpha || cd->pcie_alpha_ps[k] > kMaxAlpha || cd->nic_alpha_ps[k] > kMaxAlpha)
       return INV;
+    if (cd->mem_bytes && cd->mem_bytes[k] < 1) return INV;
     D += (uint64_t)cd->n_nodes[k] * cd->dev_per_node[k];
     N += cd->n_nodes[k];
   }
@@ -296,6 +298,36 @@ int build_tables(const sim_model_desc* md, const sim_cluster_desc* cd, HostTable
       if (s.E && (t.ep_ok >> g & 1)) t.par_expert[j][g] = (uint64_t)((s.E >> g) * 3 * s.h * (s.effn / tp));
   }
   for (uint32_t mi = 0; mi < md->n_mbs; ++mi) t.act[mi] = (uint64_t)((u128)md->mbs[mi] * s.seq * s.h * s.e);
+
+  // Memory check: capacities, optimizer bytes, and the activations one layer
+  // keeps for its backward pass on one TP rank: the inputs of its ops (no
+  // dropout masks; attention scores are recomputed by a fused kernel), per
+  // token: norm input, QKV input, Q/K/V, attention output, second norm
+  // input, then the MLP's input, its activation input(s) and the down
+  // projection's input -- or, for MoE layers, the router input and per
+  // routed token copy (top-k of them, balanced) the same three MLP tensors.
+  u128 mem_max = 0;
+  if (cd->mem_bytes) {
+    t.mem_check = 1;
+    for (uint32_t k = 0; k < K; ++k) t.mem_cap[k] = cd->mem_bytes[k];
+    t.opt_bytes = md->opt_bytes;
+    for (uint32_t j = 0; j < 4; ++j) {
+      if (!(t.tp_ok >> j & 1)) continue;
+      u128 tp = (u128)1 << j, hd = s.h / s.heads, q = s.h / tp, kv = s.kv * hd / tp;
+      u128 per_tok = 3 * s.h + q + 2 * kv + q;
+      if (s.E) per_tok += s.h + s.topk * (s.h + 3 * (s.effn / tp));
+      else per_tok += s.h + (s.gated ? 3 : 2) * (s.ffn / tp);
+      for (uint32_t mi = 0; mi < md->n_mbs; ++mi) {
+        u128 a = per_tok * md->mbs[mi] * s.seq * s.e;
+        t.act_layer[j][mi] = (uint64_t)a;
+        u128 par = (u128)t.par_layer[j] * s.L + t.par_embed[j] + t.par_head[j] + (u128)t.par_expert[j][0] * s.L;
+        mem_max = std::max(mem_max, par * (md->param_bytes + md->grad_bytes + md->opt_bytes) +
+                                        a * s.L * kMaxStages);
+      }
+    }
+    // a device's bytes are summed in 64 bits
+    if (mem_max >= ((u128)1 << 63)) return RNG;
+  }
 
   // per-layer roofline times and their prefix sums
   const uint64_t L1 = s.L + 1, nm = md->n_mbs;
