@@ -34,8 +34,10 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def pipeline_ops(p, valid):
-    """Algorithmic VALU ops of the pipeline recurrence, per plan."""
+def pipeline_ops(p, valid, per_node=3, first=1):
+    """VALU ops of the whole pipeline recurrence, per plan: `per_node` per schedule node with a
+    cross-stage input, `first` per node without one (3 and 1 in fp64 as the kernels run it; the
+    int32 count of the same nodes is 7 and 2)."""
     hdr = p["hdr"]
     S = (((hdr >> 4) & 15) + 1).astype(np.int64)
     G = ((hdr >> 8) & 3) + 1
@@ -45,7 +47,7 @@ def pipeline_ops(p, valid):
         nmb = (p["cls"][c] >> 16).astype(np.int64)
         has = (G > c) & valid & (reps > 0)
         M = np.where(has, -(-nmb // np.maximum(reps, 1)), 0)
-        ops += M * (6 * (S - 1) + 2)
+        ops += 2 * M * (per_node * (S - 1) + first)
     return ops
 
 
@@ -184,6 +186,7 @@ def main():
         # streams), timed by the library's events on the call's stream
         avg_ms = call_ms / max(call_n, 1)
         full_per_launch = float(ops.sum()) / calls_per_step
+        int32_per_launch = float(pipeline_ops(p, valid, 7, 2).sum()) / calls_per_step
         ops_per_launch = full_per_launch - skipped / timed / calls_per_step
         achieved = ops_per_launch / (avg_ms * 1e-3) / 1e12
         roof = {"bound": "alu", "achieved": round(achieved, 3), "peak": round(PEAK_VALU / 1e12, 3),
@@ -193,7 +196,11 @@ def main():
                           "k_redo_u64 per 2M-plan chunk",
                 "avg_launch_ms": round(avg_ms, 4), "launches": call_n, "ops_per_launch": ops_per_launch,
                 "full_recurrence_ops_per_launch": full_per_launch,
-                "skipped_by_periodic_shortcut": round(1 - ops_per_launch / full_per_launch, 4)}
+                "skipped_by_periodic_shortcut": round(1 - ops_per_launch / full_per_launch, 4),
+                # the int32 count of every node (7 ops with a cross-stage input, 2 without), shortcut or
+                # not: what the evaluation would cost without the shortcut, in 32-bit integer ops
+                "int32_all_nodes_ops_per_launch": int32_per_launch,
+                "int32_all_nodes_rate_frac": round(int32_per_launch / (avg_ms * 1e-3) / PEAK_VALU, 4)}
         extra = {"timed_steps_with_kernel_events": timed,
                  "prep_ms_per_step": round(setup_ms / timed, 4),
                  "first_pass_span_ms_per_step": round(pipe_ms / timed, 4),

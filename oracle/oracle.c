@@ -24,7 +24,10 @@
  *     [C4], Sec. 5 [Q2]);
  *   - parallelism exists to fit the model within device memory (Sec. 2),
  *     and device types differ in capacity (Sec. 3 example, Table 5: A100
- *     40 GB, H100 80 GB): a plan that overflows a device is infeasible.
+ *     40 GB, H100 80 GB): a plan that overflows a device is infeasible;
+ *   - device groups may differ in TP degree and layer split (Sec. 3); then
+ *     the gradient sync is preceded by resharding (Sec. 3 "Resharding",
+ *     Sec. 4.1 [C2]).
  * Where the paper is silent the reading used is named R1..R30 in comments;
  * the design notes of the repository list every reading.
  *
@@ -33,6 +36,9 @@
  * (closed forms, Table 5, Table 6, Table 1, a brute-force event simulator).
  * The per-op byte accounting of the roofline (R6/R8) has no printed value
  * to compare against: parity unpinned beyond scaling invariants.  The
+ * per-class layout (R35-R37) is pinned by its encoding of a shared layout,
+ * by classes that do not interact without links, and by the ring closed
+ * forms of its segment syncs and its resharding all-gather.  The
  * stored-activation count (R32) is pinned for GPT-shaped layers to
  * Korthikanti et al. 2022; its gated-MLP and MoE terms are parity unpinned
  * beyond the reduction of a one-expert top-1 MoE layer to a gated dense one.
@@ -366,55 +372,98 @@ static void pipeline(uint64_t S, uint64_t M, const uint64_t* f, const uint64_t* 
 /* ------------------------------------------------------------------ */
 /* one plan                                                            */
 /* ------------------------------------------------------------------ */
+/* A plan's replica classes either share one TP degree, pipeline depth and
+ * layer split (the header and the cut planes say which), or, with the
+ * per-class layout, each class has its own (Sec. 3: more layers to faster
+ * devices, TP degrees that follow each device group's size; R35). */
 typedef struct {
-  uint64_t tp, ep, S, G, zero, mi;
-  uint64_t cut[OR_MAXS];
+  uint64_t ep, G, zero, mi;
+  uint64_t tp[OR_MAXG], S[OR_MAXG];
+  uint64_t cut[OR_MAXG][OR_MAXS];
   uint64_t reps[OR_MAXG], nmb[OR_MAXG];
   int type[OR_MAXG][OR_MAXS];
 } or_plan;
 
-/* per-stage quantities of one plan, exposed for tests */
+/* per-stage quantities of one plan, exposed for tests; tdp[g][s] is the
+ * longest layer-segment sync (resharding included) that waits for stage s
+ * of class g */
 typedef struct {
-  uint64_t valid, S, G;
+  uint64_t valid, G;
+  uint64_t S[OR_MAXG];
   uint64_t M[OR_MAXG];
   uint64_t f[OR_MAXG][OR_MAXS], b[OR_MAXG][OR_MAXS], c[OR_MAXG][OR_MAXS];
-  uint64_t tdp[OR_MAXS];
+  uint64_t tdp[OR_MAXG][OR_MAXS];
   uint64_t end[OR_MAXG][OR_MAXS];
   uint64_t time;
 } or_detail;
 
-static int decode_rules(const or_ctx* x, uint32_t hdr, const uint8_t* cut, const uint32_t* cls,
-                  const uint64_t* types, int64_t stride, int64_t i, or_plan* p) {
+/* the input planes of a batch of plans */
+typedef struct {
+  const uint32_t* hdr;
+  const uint8_t* cut;    /* [16][stride]; unused with the per-class layout */
+  const uint32_t* cls;   /* [4][stride] */
+  const uint64_t* types; /* [4][stride] */
+  const uint32_t* chdr;  /* NULL, or [stride]: per-class layout, byte c = log2 TP | (PP-1) << 2 */
+  const uint8_t* ccut;   /* with chdr: [4*16][stride], cut of stage s of class c at row c*16+s */
+  int64_t stride;
+} or_planes;
+
+static int heads_split(const or_model* m, uint64_t tp) {
+  if (m->heads % tp || m->kv_heads % tp) return 0;
+  if (m->E == 0 && m->ffn % tp) return 0;
+  if (m->E != 0 && m->effn % tp) return 0;
+  return 1;
+}
+
+static int decode_rules(const or_ctx* x, const or_planes* q, int64_t i, or_plan* p) {
   const or_model* m = &x->m;
+  const int64_t stride = q->stride;
+  const uint32_t hdr = q->hdr[i];
   if (hdr >> 13) return 0;                                   /* V7 reserved bits */
-  p->tp = 1ull << (hdr & 3);
   p->ep = 1ull << ((hdr >> 2) & 3);
-  p->S = ((hdr >> 4) & 15) + 1;
   p->G = ((hdr >> 8) & 3) + 1;
   p->zero = (hdr >> 10) & 1;
   p->mi = (hdr >> 11) & 3;
   if (p->mi >= m->n_mbs) return 0;                           /* V8 */
-  uint64_t prev = 0;
-  for (uint64_t s = 0; s < p->S; ++s) {                      /* V2 */
-    p->cut[s] = cut[s * stride + i];
-    if (p->cut[s] <= prev) return 0;
-    prev = p->cut[s];
+  if (q->chdr) {
+    if (hdr & 0xf3) return 0;                                /* V10 the header's TP and PP are unused (0) */
+    uint32_t w = q->chdr[i];
+    for (uint64_t g = 0; g < p->G; ++g) {
+      uint32_t bt = (w >> (8 * g)) & 0xff;
+      if (bt >> 6) return 0;                                 /* V10 reserved class bits */
+      p->tp[g] = 1ull << (bt & 3);
+      p->S[g] = ((bt >> 2) & 15) + 1;
+    }
+  } else {
+    for (uint64_t g = 0; g < p->G; ++g) {
+      p->tp[g] = 1ull << (hdr & 3);
+      p->S[g] = ((hdr >> 4) & 15) + 1;
+    }
   }
-  if (p->cut[p->S - 1] != m->L) return 0;
+  for (uint64_t g = 0; g < p->G; ++g) {                      /* V2, per class */
+    uint64_t prev = 0;
+    for (uint64_t s = 0; s < p->S[g]; ++s) {
+      p->cut[g][s] = q->chdr ? q->ccut[(g * OR_MAXS + s) * stride + i] : q->cut[s * stride + i];
+      if (p->cut[g][s] <= prev) return 0;
+      prev = p->cut[g][s];
+    }
+    if (prev != m->L) return 0;
+  }
   uint64_t batch = 0;
   for (uint64_t g = 0; g < p->G; ++g) {
-    uint32_t w = cls[g * stride + i];
+    uint32_t w = q->cls[g * stride + i];
     p->reps[g] = w & 0xffff;
     p->nmb[g] = w >> 16;
     if (p->reps[g] == 0) return 0;                           /* V1 */
     if (p->nmb[g] < p->reps[g]) return 0;                    /* V4 every replica gets work */
     batch += p->nmb[g] * m->mbs[p->mi];
-    uint64_t tv = types[g * stride + i];
-    for (uint64_t s = 0; s < p->S; ++s) {
+    uint64_t tv = q->types[g * stride + i];
+    for (uint64_t s = 0; s < p->S[g]; ++s) {
       p->type[g][s] = (int)((tv >> (4 * s)) & 15);
       if ((uint64_t)p->type[g][s] >= x->c.K) return 0;       /* V1 */
-      if (x->c.dpn[p->type[g][s]] % p->tp) return 0;         /* V5 TP stays inside a node */
+      if (x->c.dpn[p->type[g][s]] % p->tp[g]) return 0;      /* V5 TP stays inside a node */
     }
+    if (!heads_split(m, p->tp[g])) return 0;                 /* V5 */
   }
   if (batch != m->gbs) return 0;                             /* V4 exactly the global batch (R14) */
   if (m->E == 0) {                                           /* V3 */
@@ -423,12 +472,9 @@ static int decode_rules(const or_ctx* x, uint32_t hdr, const uint8_t* cut, const
     if (p->ep > m->E || m->E % p->ep) return 0;
     for (uint64_t g = 0; g < p->G; ++g) if (p->reps[g] % p->ep) return 0;
   }
-  if (m->heads % p->tp || m->kv_heads % p->tp) return 0;     /* V5 */
-  if (m->E == 0 && m->ffn % p->tp) return 0;
-  if (m->E != 0 && m->effn % p->tp) return 0;
   uint64_t need[OR_MAXK] = {0};                              /* V6 capacity */
   for (uint64_t g = 0; g < p->G; ++g)
-    for (uint64_t s = 0; s < p->S; ++s) need[p->type[g][s]] += p->reps[g] * p->tp;
+    for (uint64_t s = 0; s < p->S[g]; ++s) need[p->type[g][s]] += p->reps[g] * p->tp[g];
   for (uint64_t k = 0; k < x->c.K; ++k)
     if (need[k] > x->c.n_nodes[k] * x->c.dpn[k]) return 0;
   return 1;
@@ -445,17 +491,17 @@ static uint64_t in_flight(uint64_t S, uint64_t M, uint64_t s) {
 
 /* R31: peak bytes on one device of stage s of class g.  Every replica keeps
  * the weights and gradients of the parameters its TP rank holds; the
- * optimizer state is kept whole, or, with ZeRO, split over the stage's DP
- * group (the same groups the gradient sync uses: all replicas for the
- * non-expert parameters, replicas/EP for the experts), rounded up; the
- * activations of the in-flight micro-batches come on top (R32, R33). */
+ * optimizer state is kept whole, or, with ZeRO, split over the DP group
+ * (all replicas for the non-expert parameters, replicas/EP for the
+ * experts), rounded up; the activations of the in-flight micro-batches come
+ * on top (R32, R33). */
 static uint64_t stage_mem(const or_ctx* x, const or_plan* p, uint64_t g, uint64_t s) {
   const or_model* m = &x->m;
-  uint64_t tp = p->tp, ep = p->ep;
-  uint64_t lo = s ? p->cut[s - 1] : 0, ns = p->cut[s] - lo;
+  uint64_t tp = p->tp[g], ep = p->ep;
+  uint64_t lo = s ? p->cut[g][s - 1] : 0, ns = p->cut[g][s] - lo;
   uint64_t pd = mul(ns, layer_params_dense(x, tp)), pe = mul(ns, layer_params_expert(x, tp, ep));
   if (s == 0) pd = add(pd, embed_params(x, tp));
-  if (s == p->S - 1) pd = add(pd, head_params(x, tp));
+  if (s == p->S[g] - 1) pd = add(pd, head_params(x, tp));
   uint64_t p_all = 0;
   for (uint64_t c = 0; c < p->G; ++c) p_all += p->reps[c];
   uint64_t wg = mul(add(m->param_bytes, m->grad_bytes), add(pd, pe));
@@ -463,17 +509,16 @@ static uint64_t stage_mem(const or_ctx* x, const or_plan* p, uint64_t g, uint64_
   if (p->zero) opt = add(cdiv(mul(m->opt_bytes, pd), p_all), cdiv(mul(m->opt_bytes, pe), p_all / ep));
   else opt = mul(m->opt_bytes, add(pd, pe));
   uint64_t M = cdiv(p->nmb[g], p->reps[g]);
-  uint64_t act = mul(mul(ns, layer_act_bytes(x, tp, m->mbs[p->mi])), in_flight(p->S, M, s));
+  uint64_t act = mul(mul(ns, layer_act_bytes(x, tp, m->mbs[p->mi])), in_flight(p->S[g], M, s));
   return add(add(wg, opt), act);
 }
 
 /* V9 (R34): when capacities are given, every device of the plan fits. */
-static int decode(const or_ctx* x, uint32_t hdr, const uint8_t* cut, const uint32_t* cls,
-                  const uint64_t* types, int64_t stride, int64_t i, or_plan* p) {
-  if (!decode_rules(x, hdr, cut, cls, types, stride, i, p)) return 0;
+static int decode(const or_ctx* x, const or_planes* q, int64_t i, or_plan* p) {
+  if (!decode_rules(x, q, i, p)) return 0;
   if (!x->c.mem_check) return 1;
   for (uint64_t g = 0; g < p->G; ++g)
-    for (uint64_t s = 0; s < p->S; ++s)
+    for (uint64_t s = 0; s < p->S[g]; ++s)
       if (stage_mem(x, p, g, s) > x->c.mem[p->type[g][s]]) return 0;
   return 1;
 }
@@ -498,30 +543,41 @@ static uint64_t dp_sync(uint64_t p, uint64_t zero, uint64_t grads, uint64_t para
              ring(p - 1, cdiv(params, p), alpha, bq));                     /* all-gather of parameters */
 }
 
+/* parameters of layers [a, b) held by one rank at TP t, EP ep: non-expert
+ * part (with the embedding if a = 0 and the head if b = L) and expert part */
+static void span_params(const or_ctx* x, uint64_t a, uint64_t b, uint64_t t, uint64_t ep, uint64_t* pd,
+                        uint64_t* pe) {
+  *pd = mul(b - a, layer_params_dense(x, t));
+  if (a == 0) *pd = add(*pd, embed_params(x, t));
+  if (b == x->m.L) *pd = add(*pd, head_params(x, t));
+  *pe = mul(b - a, layer_params_expert(x, t, ep));
+}
+
 static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t* scratch) {
   const or_model* m = &x->m;
   const or_cluster* cl = &x->c;
-  uint64_t S = p->S, G = p->G, tp = p->tp, ep = p->ep;
-  uint64_t tpl = log2u(tp), epl = log2u(ep);
+  uint64_t G = p->G, ep = p->ep, epl = log2u(ep);
   uint64_t b = m->mbs[p->mi];
   uint64_t T = b * m->seq;
   uint64_t act = mul(T, mul(m->h, m->e));                      /* one micro-batch activation (Table 1, R10) */
-  d->valid = 1; d->S = S; d->G = G;
+  d->valid = 1; d->G = G;
 
   /* R18 canonical packing: per pool, a bump pointer in (class, stage) order */
   uint64_t ptr[OR_MAXK] = {0}, base[OR_MAXG][OR_MAXS];
   for (uint64_t g = 0; g < G; ++g)
-    for (uint64_t s = 0; s < S; ++s) {
+    for (uint64_t s = 0; s < p->S[g]; ++s) {
       base[g][s] = ptr[p->type[g][s]];
-      ptr[p->type[g][s]] += p->reps[g] * tp;
+      ptr[p->type[g][s]] += p->reps[g] * p->tp[g];
     }
 
   for (uint64_t g = 0; g < G; ++g) {
+    uint64_t S = p->S[g], tp = p->tp[g], tpl = log2u(tp);
     uint64_t n = p->reps[g] * tp;                              /* devices of one (class, stage) */
+    d->S[g] = S;
     d->M[g] = cdiv(p->nmb[g], p->reps[g]);                     /* R16 */
     for (uint64_t s = 0; s < S; ++s) {
       int k = p->type[g][s];
-      uint64_t lo = s ? p->cut[s - 1] : 0, hi = p->cut[s], ns = hi - lo;
+      uint64_t lo = s ? p->cut[g][s - 1] : 0, hi = p->cut[g][s], ns = hi - lo;
       /* compute: sum of this stage's layers (Sec. 3 non-uniform layer split) */
       uint64_t Fc = 0, Bc = 0;
       for (uint64_t l = lo; l < hi; ++l) {
@@ -583,17 +639,41 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
     }
   }
 
-  /* DP sync per stage across all classes (Sec. 3: DP group = all replicas) */
-  uint64_t p_all = 0;
-  for (uint64_t g = 0; g < G; ++g) p_all += p->reps[g];
-  for (uint64_t s = 0; s < S; ++s) {
-    int k0 = p->type[0][s], same = 1;
+  /* DP sync per layer segment across all classes (Sec. 3: DP group = all
+   * replicas; R35-R37).  The segments are the layer ranges between
+   * consecutive cuts of any class, so each lies inside one stage of every
+   * class; with one layout for all classes they are the stages. */
+  uint64_t p_all = 0, tp_min = 8;
+  for (uint64_t g = 0; g < G; ++g) { p_all += p->reps[g]; if (p->tp[g] < tp_min) tp_min = p->tp[g]; }
+  uint64_t bnd[OR_MAXG * OR_MAXS + 1], nb = 0;
+  bnd[nb++] = 0;
+  for (uint64_t g = 0; g < G; ++g)
+    for (uint64_t s = 0; s < p->S[g]; ++s) {
+      uint64_t v = p->cut[g][s], j = nb;
+      int seen = 0;
+      for (uint64_t t = 0; t < nb; ++t) if (bnd[t] == v) seen = 1;
+      if (seen) continue;
+      while (j > 0 && bnd[j - 1] > v) { bnd[j] = bnd[j - 1]; --j; }   /* insertion sort */
+      bnd[j] = v;
+      ++nb;
+    }
+  for (uint64_t g = 0; g < G; ++g) for (uint64_t s = 0; s < OR_MAXS; ++s) d->tdp[g][s] = 0;
+  for (uint64_t j = 0; j + 1 < nb; ++j) {
+    uint64_t a = bnd[j], e = bnd[j + 1];
+    uint64_t sg[OR_MAXG];
+    for (uint64_t g = 0; g < G; ++g) {                          /* the stage of class g holding [a, e) */
+      uint64_t s = 0;
+      while (p->cut[g][s] <= a) ++s;
+      sg[g] = s;
+    }
+    int k0 = p->type[0][sg[0]], same = 1;
     uint64_t nlo = UINT64_MAX, nhi = 0;
     for (uint64_t g = 0; g < G; ++g) {
-      if (p->type[g][s] != k0) same = 0;
-      uint64_t n = p->reps[g] * tp;
-      for (uint64_t dv = base[g][s]; dv < base[g][s] + n; ++dv) {
-        uint64_t node = dv / cl->dpn[p->type[g][s]];
+      int k = p->type[g][sg[g]];
+      if (k != k0) same = 0;
+      uint64_t n = p->reps[g] * p->tp[g];
+      for (uint64_t dv = base[g][sg[g]]; dv < base[g][sg[g]] + n; ++dv) {
+        uint64_t node = dv / cl->dpn[k];
         if (node < nlo) nlo = node;
         if (node > nhi) nhi = node;
       }
@@ -603,25 +683,40 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
     else {
       alpha = 0; bq = 0;
       for (uint64_t g = 0; g < G; ++g) {
-        int k = p->type[g][s];
-        alpha = umax(alpha, mul(2, alpha_side(x, k)));                    /* R21 */
-        bq = umax(bq, umax(nic_max(x, k, base[g][s], p->reps[g] * tp), beta_q(cl->pcie[k])));
+        int k = p->type[g][sg[g]];
+        alpha = umax(alpha, mul(2, alpha_side(x, k)));                  /* R21 */
+        bq = umax(bq, umax(nic_max(x, k, base[g][sg[g]], p->reps[g] * p->tp[g]), beta_q(cl->pcie[k])));
       }
     }
-    uint64_t lo = s ? p->cut[s - 1] : 0, hi = p->cut[s];
-    uint64_t pd = (hi - lo) * layer_params_dense(x, tp), pe = (hi - lo) * layer_params_expert(x, tp, ep);
-    if (s == 0) pd += embed_params(x, tp);
-    if (s == S - 1) pd += head_params(x, tp);
+    /* R36: the ring runs on the coarsest TP layout among the classes */
+    uint64_t pd, pe;
+    span_params(x, a, e, tp_min, ep, &pd, &pe);
     uint64_t t = dp_sync(p_all, p->zero, mul(m->grad_bytes, pd), mul(m->param_bytes, pd), alpha, bq);
     if (m->E) t = add(t, dp_sync(p_all / ep, p->zero, mul(m->grad_bytes, pe), mul(m->param_bytes, pe), alpha, bq));
-    d->tdp[s] = t;
+    /* R36: classes with finer shards first gather the coarse shard inside
+     * each TP group: a ring all-gather over tp/tp_min members of the
+     * class's own gradient shard, on the group's node fabric; classes
+     * reshard at the same time, so the slowest counts */
+    uint64_t rs = 0;
+    for (uint64_t g = 0; g < G; ++g) {
+      if (p->tp[g] == tp_min) continue;
+      uint64_t qd, qe;
+      span_params(x, a, e, p->tp[g], ep, &qd, &qe);
+      int k = p->type[g][sg[g]];
+      uint64_t r = ring(p->tp[g] / tp_min - 1, mul(m->grad_bytes, add(qd, qe)), cl->a_intra[k],
+                        intra_max(x, k, base[g][sg[g]], p->reps[g] * p->tp[g]));
+      rs = umax(rs, r);
+    }
+    t = add(t, rs);
+    for (uint64_t g = 0; g < G; ++g) d->tdp[g][sg[g]] = umax(d->tdp[g][sg[g]], t);
   }
 
-  /* per class pipeline, then T = max over stages (R27, R28) */
+  /* per class pipeline; a segment's sync starts when every stage holding it
+   * has finished, so T = max over classes and stages (R27, R28) */
   uint64_t T_iter = 0;
   for (uint64_t g = 0; g < G; ++g) {
-    pipeline(S, d->M[g], d->f[g], d->b[g], d->c[g], d->end[g], scratch);
-    for (uint64_t s = 0; s < S; ++s) T_iter = umax(T_iter, add(d->end[g][s], d->tdp[s]));
+    pipeline(p->S[g], d->M[g], d->f[g], d->b[g], d->c[g], d->end[g], scratch);
+    for (uint64_t s = 0; s < p->S[g]; ++s) T_iter = umax(T_iter, add(d->end[g][s], d->tdp[g][s]));
   }
   d->time = T_iter;
 }
@@ -697,10 +792,16 @@ void oracle_free(or_ctx* x) {
 
 typedef struct {
   const or_ctx* x;
-  const uint32_t* hdr; const uint8_t* cut; const uint32_t* cls; const uint64_t* types;
-  int64_t stride, lo, hi;
+  or_planes q;
+  int64_t lo, hi;
   uint64_t* out;
 } or_job;
+
+static or_planes planes(const uint32_t* hdr, const uint8_t* cut, const uint32_t* cls, const uint64_t* types,
+                        const uint32_t* chdr, const uint8_t* ccut, int64_t stride) {
+  or_planes q = {hdr, cut, cls, types, chdr, ccut, stride};
+  return q;
+}
 
 static void* worker(void* arg) {
   or_job* j = (or_job*)arg;
@@ -709,7 +810,7 @@ static void* worker(void* arg) {
   or_detail d;
   for (int64_t i = j->lo; i < j->hi; ++i) {
     or_plan p;
-    if (!decode(j->x, j->hdr[i], j->cut, j->cls, j->types, j->stride, i, &p)) { j->out[i] = OR_INVALID; continue; }
+    if (!decode(j->x, &j->q, i, &p)) { j->out[i] = OR_INVALID; continue; }
     eval_plan(j->x, &p, &d, scratch);
     j->out[i] = d.time;
   }
@@ -717,16 +818,17 @@ static void* worker(void* arg) {
   return NULL;
 }
 
-/* Evaluate plans [0, n) of SoA planes with plane stride `stride`. */
+/* Evaluate plans [0, n) of SoA planes with plane stride `stride` (chdr and
+ * ccut NULL unless the plans use the per-class layout). */
 void oracle_eval(const or_ctx* x, const uint32_t* hdr, const uint8_t* cut, const uint32_t* cls,
-                 const uint64_t* types, int64_t stride, int64_t n, uint64_t* out, int nthreads) {
+                 const uint64_t* types, const uint32_t* chdr, const uint8_t* ccut, int64_t stride, int64_t n,
+                 uint64_t* out, int nthreads) {
   if (nthreads < 1) nthreads = 1;
   if (nthreads > 256) nthreads = 256;
   pthread_t th[256];
   or_job jobs[256];
   for (int t = 0; t < nthreads; ++t) {
-    jobs[t].x = x; jobs[t].hdr = hdr; jobs[t].cut = cut; jobs[t].cls = cls; jobs[t].types = types;
-    jobs[t].stride = stride; jobs[t].out = out;
+    jobs[t].x = x; jobs[t].q = planes(hdr, cut, cls, types, chdr, ccut, stride); jobs[t].out = out;
     jobs[t].lo = n * t / nthreads; jobs[t].hi = n * (t + 1) / nthreads;
   }
   for (int t = 1; t < nthreads; ++t) pthread_create(&th[t], NULL, worker, &jobs[t]);
@@ -736,10 +838,12 @@ void oracle_eval(const or_ctx* x, const uint32_t* hdr, const uint8_t* cut, const
 
 /* Stage-level detail of plan i (for tests and debugging). */
 int oracle_detail(const or_ctx* x, const uint32_t* hdr, const uint8_t* cut, const uint32_t* cls,
-                  const uint64_t* types, int64_t stride, int64_t i, or_detail* d) {
+                  const uint64_t* types, const uint32_t* chdr, const uint8_t* ccut, int64_t stride, int64_t i,
+                  or_detail* d) {
   memset(d, 0, sizeof(*d));
   or_plan p;
-  if (!decode(x, hdr[i], cut, cls, types, stride, i, &p)) { d->time = OR_INVALID; return 0; }
+  or_planes q = planes(hdr, cut, cls, types, chdr, ccut, stride);
+  if (!decode(x, &q, i, &p)) { d->time = OR_INVALID; return 0; }
   uint64_t* scratch = (uint64_t*)malloc(8 * 2 * OR_MAXS * (x->m.gbs + 1));
   eval_plan(x, &p, d, scratch);
   free(scratch);
@@ -784,11 +888,13 @@ uint64_t oracle_in_flight(uint64_t S, uint64_t M, uint64_t s) { return in_flight
  * (entries of absent classes and stages 0).  Returns 0 if the plan breaks
  * a rule other than the memory check (mem then all 0), else 1. */
 int oracle_stage_mem(const or_ctx* x, const uint32_t* hdr, const uint8_t* cut, const uint32_t* cls,
-                     const uint64_t* types, int64_t stride, int64_t i, uint64_t* mem) {
+                     const uint64_t* types, const uint32_t* chdr, const uint8_t* ccut, int64_t stride, int64_t i,
+                     uint64_t* mem) {
   memset(mem, 0, 8 * OR_MAXG * OR_MAXS);
   or_plan p;
-  if (!decode_rules(x, hdr[i], cut, cls, types, stride, i, &p)) return 0;
+  or_planes q = planes(hdr, cut, cls, types, chdr, ccut, stride);
+  if (!decode_rules(x, &q, i, &p)) return 0;
   for (uint64_t g = 0; g < p.G; ++g)
-    for (uint64_t s = 0; s < p.S; ++s) mem[g * OR_MAXS + s] = stage_mem(x, &p, g, s);
+    for (uint64_t s = 0; s < p.S[g]; ++s) mem[g * OR_MAXS + s] = stage_mem(x, &p, g, s);
   return 1;
 }

@@ -17,12 +17,13 @@ OR_MAXG, OR_MAXS = 4, 16
 
 
 class _Detail(C.Structure):
-    _fields_ = [("valid", C.c_uint64), ("S", C.c_uint64), ("G", C.c_uint64),
+    _fields_ = [("valid", C.c_uint64), ("G", C.c_uint64),
+                ("S", C.c_uint64 * OR_MAXG),
                 ("M", C.c_uint64 * OR_MAXG),
                 ("f", (C.c_uint64 * OR_MAXS) * OR_MAXG),
                 ("b", (C.c_uint64 * OR_MAXS) * OR_MAXG),
                 ("c", (C.c_uint64 * OR_MAXS) * OR_MAXG),
-                ("tdp", C.c_uint64 * OR_MAXS),
+                ("tdp", (C.c_uint64 * OR_MAXS) * OR_MAXG),
                 ("end", (C.c_uint64 * OR_MAXS) * OR_MAXG),
                 ("time", C.c_uint64)]
 
@@ -39,8 +40,8 @@ def lib():
         L.oracle_new.restype = P
         L.oracle_new.argtypes = [P, P, P, P, P]
         L.oracle_free.argtypes = [P]
-        L.oracle_eval.argtypes = [P, P, P, P, P, C.c_int64, C.c_int64, P, C.c_int]
-        L.oracle_detail.argtypes = [P, P, P, P, P, C.c_int64, C.c_int64, C.POINTER(_Detail)]
+        L.oracle_eval.argtypes = [P, P, P, P, P, P, P, C.c_int64, C.c_int64, P, C.c_int]
+        L.oracle_detail.argtypes = [P, P, P, P, P, P, P, C.c_int64, C.c_int64, C.POINTER(_Detail)]
         L.oracle_detail.restype = C.c_int
         L.oracle_detail_size.restype = C.c_size_t
         L.oracle_pipeline.argtypes = [u64, u64, P, P, P, P]
@@ -67,7 +68,7 @@ def lib():
         L.oracle_layer_act_bytes.restype = u64
         L.oracle_in_flight.argtypes = [u64, u64, u64]
         L.oracle_in_flight.restype = u64
-        L.oracle_stage_mem.argtypes = [P, P, P, P, P, C.c_int64, C.c_int64, P]
+        L.oracle_stage_mem.argtypes = [P, P, P, P, P, P, P, C.c_int64, C.c_int64, P]
         L.oracle_stage_mem.restype = C.c_int
         assert L.oracle_detail_size() == C.sizeof(_Detail)
         _lib = L
@@ -121,37 +122,51 @@ class Oracle:
             _lib.oracle_free(self.h)
             self.h = None
 
-    def eval(self, plans, nthreads=None, n=None):
-        """plans: dict with hdr u32[n], cut u8[16, stride], cls u32[4, stride], types u64[4, stride]."""
+    @staticmethod
+    def _planes(plans):
+        """The plan planes as contiguous arrays; chdr/ccut only for the per-class layout."""
         hdr = np.ascontiguousarray(plans["hdr"], dtype=np.uint32)
-        cut = np.ascontiguousarray(plans["cut"], dtype=np.uint8)
         cls = np.ascontiguousarray(plans["cls"], dtype=np.uint32)
         typ = np.ascontiguousarray(plans["types"], dtype=np.uint64)
-        stride = cut.shape[1]
-        n = hdr.shape[0] if n is None else n
+        stride = cls.shape[1]
+        cut = plans.get("cut")
+        cut = np.ascontiguousarray(cut, dtype=np.uint8) if cut is not None else None
+        chdr = plans.get("chdr")
+        ccut = plans.get("ccut")
+        chdr = np.ascontiguousarray(chdr, dtype=np.uint32) if chdr is not None else None
+        ccut = np.ascontiguousarray(ccut, dtype=np.uint8) if ccut is not None else None
+        if cut is not None:
+            assert cut.shape[1] == stride
+        if ccut is not None:
+            assert ccut.shape == (64, stride)
+        return (hdr, cut, cls, typ, chdr, ccut), stride
+
+    def eval(self, plans, nthreads=None, n=None):
+        """plans: dict with hdr u32[n], cut u8[16, stride], cls u32[4, stride], types u64[4, stride], and for
+        the per-class layout chdr u32[n] and ccut u8[64, stride] (cut may then be absent)."""
+        arrs, stride = self._planes(plans)
+        n = arrs[0].shape[0] if n is None else n
         out = np.empty(n, dtype=np.uint64)
         if nthreads is None:
             nthreads = os.cpu_count() or 1
-        lib().oracle_eval(self.h, _ptr(hdr), _ptr(cut), _ptr(cls), _ptr(typ), stride, n, _ptr(out), int(nthreads))
+        lib().oracle_eval(self.h, *[_ptr(a) for a in arrs], stride, n, _ptr(out), int(nthreads))
         return out
 
     def detail(self, plans, i):
-        hdr = np.ascontiguousarray(plans["hdr"], dtype=np.uint32)
-        cut = np.ascontiguousarray(plans["cut"], dtype=np.uint8)
-        cls = np.ascontiguousarray(plans["cls"], dtype=np.uint32)
-        typ = np.ascontiguousarray(plans["types"], dtype=np.uint64)
+        arrs, stride = self._planes(plans)
         d = _Detail()
-        ok = lib().oracle_detail(self.h, _ptr(hdr), _ptr(cut), _ptr(cls), _ptr(typ), cut.shape[1], int(i), C.byref(d))
+        ok = lib().oracle_detail(self.h, *[_ptr(a) for a in arrs], stride, int(i), C.byref(d))
         if not ok:
             return None
-        S, G = d.S, d.G
+        G = d.G
+        S = [d.S[g] for g in range(G)]
         return {
-            "S": S, "G": G, "M": [d.M[g] for g in range(G)],
-            "f": [[d.f[g][s] for s in range(S)] for g in range(G)],
-            "b": [[d.b[g][s] for s in range(S)] for g in range(G)],
-            "c": [[d.c[g][s] for s in range(S)] for g in range(G)],
-            "tdp": [d.tdp[s] for s in range(S)],
-            "end": [[d.end[g][s] for s in range(S)] for g in range(G)],
+            "S": S[0] if len(set(S)) == 1 else None, "S_class": S, "G": G, "M": [d.M[g] for g in range(G)],
+            "f": [[d.f[g][s] for s in range(S[g])] for g in range(G)],
+            "b": [[d.b[g][s] for s in range(S[g])] for g in range(G)],
+            "c": [[d.c[g][s] for s in range(S[g])] for g in range(G)],
+            "tdp": [[d.tdp[g][s] for s in range(S[g])] for g in range(G)],
+            "end": [[d.end[g][s] for s in range(S[g])] for g in range(G)],
             "time": d.time,
         }
 
@@ -180,13 +195,9 @@ class Oracle:
     def stage_mem(self, plans, i):
         """[4][16] peak bytes per (class, stage) device of plan i, or None if a rule other than
         the memory check rejects the plan."""
-        hdr = np.ascontiguousarray(plans["hdr"], dtype=np.uint32)
-        cut = np.ascontiguousarray(plans["cut"], dtype=np.uint8)
-        cls = np.ascontiguousarray(plans["cls"], dtype=np.uint32)
-        typ = np.ascontiguousarray(plans["types"], dtype=np.uint64)
+        arrs, stride = self._planes(plans)
         mem = np.zeros((4, 16), dtype=np.uint64)
-        ok = lib().oracle_stage_mem(self.h, _ptr(hdr), _ptr(cut), _ptr(cls), _ptr(typ), cut.shape[1], int(i),
-                                    _ptr(mem))
+        ok = lib().oracle_stage_mem(self.h, *[_ptr(a) for a in arrs], stride, int(i), _ptr(mem))
         return mem if ok else None
 
 

@@ -49,6 +49,8 @@ def _load():
         L = C.CDLL(_LIB)
         L.plangen_random.argtypes = [C.POINTER(_Params), C.c_uint64, C.c_int64, C.c_void_p, C.c_void_p,
                                      C.c_void_p, C.c_void_p, C.c_int64, C.c_int]
+        L.plangen_random_het.argtypes = [C.POINTER(_Params), C.c_uint64, C.c_int64, C.c_void_p, C.c_void_p,
+                                         C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64, C.c_int]
         L.plangen_draw.argtypes = [C.c_uint64, C.c_uint64]
         L.plangen_draw.restype = C.c_uint64
         _lib = L
@@ -219,6 +221,35 @@ def random_plans(m, c, seed, first, n, nthreads=None, out=None):
     L.plangen_random(C.byref(P), first, n, p["hdr"].ctypes.data, p["cut"].ctypes.data, p["cls"].ctypes.data,
                      p["types"].ctypes.data, stride, nthreads)
     return p
+
+
+def random_plans_het(m, c, seed, first, n, nthreads=None):
+    """Per-class-layout plans first..first+n-1 (every class its own TP degree, pipeline depth and layer
+    split; see plangen.c): dict with hdr, cls, types, chdr (u32 [n]) and ccut (u8 [64, n])."""
+    L = _load()
+    P = _Params()
+    P.seed = seed
+    P.L = m["L"]
+    P.K = len(c["types"])
+    for k, t in enumerate(c["types"]):
+        P.cap[k] = t["n_nodes"] * t["dev_per_node"]
+    P.batches = m["global_batch"] // m["mbs"][0]
+    P.experts = m.get("experts", 0)
+    p = dict(hdr=np.zeros(n, np.uint32), cls=np.zeros((4, n), np.uint32), types=np.zeros((4, n), np.uint64),
+             chdr=np.zeros(n, np.uint32), ccut=np.zeros((64, n), np.uint8))
+    if nthreads is None:
+        nthreads = min(16, os.cpu_count() or 1)
+    L.plangen_random_het(C.byref(P), first, n, p["hdr"].ctypes.data, p["ccut"].ctypes.data, p["cls"].ctypes.data,
+                         p["types"].ctypes.data, p["chdr"].ctypes.data, n, nthreads)
+    return p
+
+
+def het_plans(w, first=0, n=None, nthreads=None):
+    """Per-class-layout plans of workload w (its own seed + 0x100)."""
+    if n is None:
+        n = w["n_plans"] - first
+    seed = (w["seed"] if w["seed"] is not None else 0x91A70001) + 0x100
+    return random_plans_het(w["model"], w["cluster"], seed, first, n, nthreads)
 
 
 def enumerate_two_type_8(L=12, n_dev=8, per_type=4, batches=8):

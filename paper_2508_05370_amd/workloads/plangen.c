@@ -144,3 +144,120 @@ void plangen_random(const pg_params* P, uint64_t first, int64_t n, uint32_t* hdr
   run(&jobs[0]);
   for (int t = 1; t < nthreads; ++t) pthread_join(th[t], 0);
 }
+
+/* ------------------------------------------------------------------ */
+/* plans with a per-class layout: every replica class draws its own TP
+ * degree, pipeline depth and layer split (per-class planes):
+ *   chdr[i]                    byte c = tp_log2:2 | (pp_c-1):4 | 0:2
+ *   ccut[(c*16+s)*stride+i]    cumulative layer end of stage s of class c
+ * and hdr carries only ep_log2, G-1, zero (TP and PP fields 0). */
+static void gen_one_het(const pg_params* P, uint64_t i, uint32_t* hdr, uint8_t* ccut, uint32_t* cls,
+                        uint64_t* types, uint32_t* chdr, int64_t stride, int64_t slot) {
+  rng r = {P->seed, i, 0};
+  uint32_t tpl[4] = {0}, pp[4] = {1, 1, 1, 1}, epl = 0, G = 0, zero = 0;
+  uint32_t reps[4] = {0}, nmb[4] = {0};
+  uint64_t tv[4] = {0};
+  uint32_t sumreps = 0;
+  for (int attempt = 0; attempt < 16 && G == 0; ++attempt) {
+    r.d = (uint64_t)attempt * 256;
+    epl = 0;
+    if (P->experts) {
+      epl = (uint32_t)uni(&r, 0, 3);
+      while ((1u << epl) > P->experts || P->experts % (1u << epl)) --epl;
+    }
+    uint32_t want = (uint32_t)uni(&r, 1, 4);
+    zero = (uint32_t)uni(&r, 0, 1);
+    uint32_t ep = 1u << epl;
+    uint32_t left[16];
+    memcpy(left, P->cap, sizeof(left));
+    sumreps = 0;
+    for (uint32_t c = 0; c < want; ++c) {
+      tpl[c] = (uint32_t)uni(&r, 0, 3);
+      pp[c] = (uint32_t)uni(&r, 1, 16);
+      uint32_t tp = 1u << tpl[c];
+      uint32_t cnt[16] = {0};
+      uint64_t t = 0;
+      for (uint32_t s = 0; s < pp[c]; ++s) {
+        uint64_t k = uni(&r, 0, P->K - 1);
+        t |= k << (4 * s);
+        cnt[k]++;
+      }
+      uint32_t maxr = 0xffffffffu;
+      for (uint32_t k = 0; k < P->K; ++k)
+        if (cnt[k]) { uint32_t m = left[k] / (cnt[k] * tp); if (m < maxr) maxr = m; }
+      if (maxr > P->batches - sumreps) maxr = P->batches - sumreps;
+      if (maxr > 0xffff) maxr = 0xffff;
+      maxr = maxr / ep * ep;
+      if (maxr < ep) break;
+      uint32_t rr = ep * (uint32_t)uni(&r, 1, maxr / ep);
+      for (uint32_t k = 0; k < P->K; ++k) left[k] -= rr * cnt[k] * tp;
+      reps[c] = rr; tv[c] = t; sumreps += rr; G = c + 1;
+    }
+    if (G == 0 && attempt == 15) {      /* give up: emit a plan that fails the capacity check */
+      G = 1; reps[0] = ep; tv[0] = 0; sumreps = ep; tpl[0] = 0; pp[0] = 1;
+      if (sumreps > P->batches) sumreps = P->batches;
+    }
+  }
+  for (uint32_t c = 0; c < 4; ++c) {
+    for (uint32_t s = 0; s < 16; ++s) ccut[(c * 16 + s) * stride + slot] = 0;
+    if (c >= G) continue;
+    /* this class's layer split: pp-1 distinct cut points in [1, L-1], sorted */
+    uint8_t pts[256];
+    for (uint32_t l = 1; l < P->L; ++l) pts[l - 1] = (uint8_t)l;
+    r.d = 16 * 256 + c * 64;
+    for (uint32_t j = 0; j + 1 < pp[c]; ++j) {
+      uint32_t pick = j + (uint32_t)uni(&r, 0, P->L - 2 - j);
+      uint8_t tmp = pts[j]; pts[j] = pts[pick]; pts[pick] = tmp;
+    }
+    for (uint32_t j = 1; j + 1 < pp[c]; ++j) {
+      uint8_t v = pts[j]; int q = (int)j - 1;
+      while (q >= 0 && pts[q] > v) { pts[q + 1] = pts[q]; --q; }
+      pts[q + 1] = v;
+    }
+    for (uint32_t s = 0; s + 1 < pp[c]; ++s) ccut[(c * 16 + s) * stride + slot] = pts[s];
+    ccut[(c * 16 + pp[c] - 1) * stride + slot] = (uint8_t)P->L;
+  }
+  r.d = 16 * 256 + 4 * 64;
+  uint32_t extra = P->batches > sumreps ? P->batches - sumreps : 0;
+  uint64_t w[4], W = 0;
+  for (uint32_t c = 0; c < G; ++c) { w[c] = uni(&r, 1, 1000); W += w[c]; }
+  uint32_t given = 0;
+  for (uint32_t c = 1; c < G; ++c) { uint32_t x = (uint32_t)((uint64_t)extra * w[c] / W); nmb[c] = reps[c] + x; given += x; }
+  nmb[0] = reps[0] + (extra - given);
+  uint32_t ch = 0;
+  for (uint32_t c = 0; c < 4; ++c) {
+    cls[c * stride + slot] = c < G ? (reps[c] & 0xffff) | ((nmb[c] & 0xffff) << 16) : 0;
+    types[c * stride + slot] = c < G ? tv[c] : 0;
+    if (c < G) ch |= (tpl[c] | ((pp[c] - 1) << 2)) << (8 * c);
+  }
+  chdr[slot] = ch;
+  hdr[slot] = (epl << 2) | ((G - 1) << 8) | (zero << 10);
+}
+
+typedef struct {
+  const pg_params* P; uint64_t first; int64_t lo, hi, stride;
+  uint32_t* hdr; uint8_t* ccut; uint32_t* cls; uint64_t* types; uint32_t* chdr;
+} pg_job_het;
+
+static void* run_het(void* a) {
+  pg_job_het* j = (pg_job_het*)a;
+  for (int64_t s = j->lo; s < j->hi; ++s)
+    gen_one_het(j->P, j->first + (uint64_t)s, j->hdr, j->ccut, j->cls, j->types, j->chdr, j->stride, s);
+  return 0;
+}
+
+/* Per-class-layout plans first .. first+n-1 into slots 0 .. n-1. */
+void plangen_random_het(const pg_params* P, uint64_t first, int64_t n, uint32_t* hdr, uint8_t* ccut, uint32_t* cls,
+                        uint64_t* types, uint32_t* chdr, int64_t stride, int nthreads) {
+  if (nthreads < 1) nthreads = 1;
+  if (nthreads > 64) nthreads = 64;
+  pthread_t th[64];
+  pg_job_het jobs[64];
+  for (int t = 0; t < nthreads; ++t) {
+    pg_job_het j = {P, first, n * t / nthreads, n * (t + 1) / nthreads, stride, hdr, ccut, cls, types, chdr};
+    jobs[t] = j;
+  }
+  for (int t = 1; t < nthreads; ++t) pthread_create(&th[t], 0, run_het, &jobs[t]);
+  run_het(&jobs[0]);
+  for (int t = 1; t < nthreads; ++t) pthread_join(th[t], 0);
+}

@@ -99,7 +99,7 @@ def test_stage_records(torch, B, oracle_mod, workloads, idx):
             assert cl[i, g] == S | (G << 5) | (d["M"][g] << 8), (i, g)
             for s in range(S):
                 rec = [int(v) for v in st[i, g, s]]
-                want = [d["f"][g][s], d["b"][g][s], d["c"][g][s], d["tdp"][s]]
+                want = [d["f"][g][s], d["b"][g][s], d["c"][g][s], d["tdp"][g][s]]
                 assert rec == want, (idx, i, g, s, rec, want)
 
 
