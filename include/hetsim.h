@@ -101,7 +101,8 @@ typedef struct {
 
 /*
  * Candidate plans, structure of arrays in DEVICE memory (caller-owned),
- * plane stride `stride` elements (>= n).  Plan i:
+ * plane stride `stride` elements (>= n).  Plan i, shared layout (every
+ * replica class runs the same TP degree, pipeline depth and layer split):
  *   hdr[i]              bits 0-1 log2 TP, 2-3 log2 EP, 4-7 PP-1, 8-9 classes-1,
  *                       10 ZeRO (reduce-scatter + all-gather instead of
  *                       all-reduce), 11-12 micro-batch size index, 13-31 zero
@@ -111,6 +112,22 @@ typedef struct {
  *                       bits 16-31 (the class's share of the global batch)
  *   types[c*stride+i]   u64, device type of stage s of class c in bits [4s, 4s+4)
  * Entries past PP stages or past the class count are ignored.
+ *
+ * Per-class layout (chdr != NULL): device groups may differ in TP degree and
+ * in how many layers each stage takes (Sec. 3 "Non-uniform workload
+ * partitioning": TP=1 next to TP=3 groups, more layers on faster devices).
+ * Then hdr's TP and PP fields must be 0, `cut` is not read (may be NULL),
+ * and
+ *   chdr[i]                 byte c (class c): bits 0-1 log2 TP, 2-5 PP-1,
+ *                           6-7 zero
+ *   ccut[(c*16+s)*stride+i] u8, last layer (exclusive) of stage s of class
+ *                           c: 1 <= ... < ccut[(c*16+PP_c-1)*stride+i] = L
+ * The gradient sync of the layers between two consecutive cuts of any
+ * class runs as one ring over every replica on the coarsest TP layout among
+ * the classes, after the classes with finer shards gather it inside their
+ * TP groups (resharding, Sec. 3 "Resharding", Sec. 4.1 [C2]); a stage's
+ * sync waits for its own backward passes and those of the other classes'
+ * stages that hold the same layers.  The rules above apply per class.
  * A plan that breaks any rule (ranges, divisibility of heads/widths by TP,
  * TP within a node, EP dividing every class's replicas, capacity of every
  * device pool, micro-batches summing to the global batch, at least one
@@ -124,6 +141,8 @@ typedef struct {
   const uint32_t* cls;
   const uint64_t* types;
   int64_t stride;
+  const uint32_t* chdr;   /* NULL = shared layout */
+  const uint8_t* ccut;    /* with chdr: [64][stride] */
 } sim_plans;
 
 /* argmin result: lowest time, ties to the lowest plan index */
@@ -161,8 +180,10 @@ int sim_eval_plans(sim_ctx* ctx, const sim_plans* plans, int64_t n, uint64_t* ou
  * Per-stage quantities of plans 0..n-1 (device memory, caller-owned):
  *   out_stage[((i*4 + c)*16 + s)*4 + q], q = 0 forward time of one
  *   micro-batch on stage s of class c, 1 backward time, 2 pipeline hop
- *   s -> s+1, 3 DP sync of stage s;
- *   out_class[i*4 + c] = PP | classes << 5 | M << 8 where M is the
+ *   s -> s+1, 3 DP sync that waits for stage s of class c (with the
+ *   per-class layout: the longest of the syncs of the layer segments the
+ *   stage holds, resharding included);
+ *   out_class[i*4 + c] = PP of the class | classes << 5 | M << 8 where M is the
  *   micro-batches per replica of class c (0 for an absent class or an
  *   invalid plan).
  * Entries of absent stages are left untouched.  n is at most 2^21 per call.

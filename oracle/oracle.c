@@ -472,9 +472,12 @@ static int decode_rules(const or_ctx* x, const or_planes* q, int64_t i, or_plan*
     if (p->ep > m->E || m->E % p->ep) return 0;
     for (uint64_t g = 0; g < p->G; ++g) if (p->reps[g] % p->ep) return 0;
   }
-  uint64_t need[OR_MAXK] = {0};                              /* V6 capacity */
+  uint64_t need[OR_MAXK] = {0};                              /* V6 capacity of the packing (R18) */
   for (uint64_t g = 0; g < p->G; ++g)
-    for (uint64_t s = 0; s < p->S[g]; ++s) need[p->type[g][s]] += p->reps[g] * p->tp[g];
+    for (uint64_t s = 0; s < p->S[g]; ++s) {
+      int k = p->type[g][s];
+      need[k] = cdiv(need[k], p->tp[g]) * p->tp[g] + p->reps[g] * p->tp[g];
+    }
   for (uint64_t k = 0; k < x->c.K; ++k)
     if (need[k] > x->c.n_nodes[k] * x->c.dpn[k]) return 0;
   return 1;
@@ -562,12 +565,16 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
   uint64_t act = mul(T, mul(m->h, m->e));                      /* one micro-batch activation (Table 1, R10) */
   d->valid = 1; d->G = G;
 
-  /* R18 canonical packing: per pool, a bump pointer in (class, stage) order */
+  /* R18 canonical packing: per pool, a bump pointer in (class, stage) order;
+   * a block starts at a multiple of its class's TP degree so that no TP
+   * group spans two nodes (with one TP degree for all classes every block
+   * already does) */
   uint64_t ptr[OR_MAXK] = {0}, base[OR_MAXG][OR_MAXS];
   for (uint64_t g = 0; g < G; ++g)
     for (uint64_t s = 0; s < p->S[g]; ++s) {
-      base[g][s] = ptr[p->type[g][s]];
-      ptr[p->type[g][s]] += p->reps[g] * p->tp[g];
+      int k = p->type[g][s];
+      base[g][s] = cdiv(ptr[k], p->tp[g]) * p->tp[g];
+      ptr[k] = base[g][s] + p->reps[g] * p->tp[g];
     }
 
   for (uint64_t g = 0; g < G; ++g) {

@@ -35,7 +35,7 @@ class ClusterDesc(C.Structure):
 
 class Plans(C.Structure):
     _fields_ = [("hdr", C.c_void_p), ("cut", C.c_void_p), ("cls", C.c_void_p), ("types", C.c_void_p),
-                ("stride", C.c_int64)]
+                ("stride", C.c_int64), ("chdr", C.c_void_p), ("ccut", C.c_void_p)]
 
 
 class Best(C.Structure):
@@ -156,25 +156,37 @@ def _stream(stream):
 
 
 def device_plans(p, device="cuda"):
-    """Copy a host plan dict (numpy) to device tensors (bit-preserving int views)."""
+    """Copy a host plan dict (numpy) to device tensors (bit-preserving int views).  A dict with
+    chdr and ccut is a per-class-layout batch (its cut plane, if any, is not used)."""
     import torch
-    return dict(
+    d = dict(
         hdr=torch.from_numpy(np.ascontiguousarray(p["hdr"]).view(np.int32)).to(device),
-        cut=torch.from_numpy(np.ascontiguousarray(p["cut"])).to(device),
         cls=torch.from_numpy(np.ascontiguousarray(p["cls"]).view(np.int32)).to(device),
         types=torch.from_numpy(np.ascontiguousarray(p["types"]).view(np.int64)).to(device),
     )
+    if p.get("chdr") is not None:
+        d["chdr"] = torch.from_numpy(np.ascontiguousarray(p["chdr"]).view(np.int32)).to(device)
+        d["ccut"] = torch.from_numpy(np.ascontiguousarray(p["ccut"])).to(device)
+    else:
+        d["cut"] = torch.from_numpy(np.ascontiguousarray(p["cut"])).to(device)
+    return d
 
 
 def plans_struct(dp, offset=0):
     """sim_plans view of device plan tensors, starting at plan `offset`."""
     s = Plans()
-    stride = dp["cut"].shape[1]
+    stride = dp["cls"].shape[1]
     s.hdr = dp["hdr"].data_ptr() + 4 * offset
-    s.cut = dp["cut"].data_ptr() + offset
     s.cls = dp["cls"].data_ptr() + 4 * offset
     s.types = dp["types"].data_ptr() + 8 * offset
     s.stride = stride
+    if "chdr" in dp:
+        assert dp["ccut"].shape == (64, stride)
+        s.chdr = dp["chdr"].data_ptr() + 4 * offset
+        s.ccut = dp["ccut"].data_ptr() + offset
+    else:
+        assert dp["cut"].shape == (16, stride)
+        s.cut = dp["cut"].data_ptr() + offset
     return s
 
 

@@ -12,11 +12,11 @@
 
 namespace hetsim {
 hipError_t launch_fill32(uint32_t* p, uint32_t n, uint32_t v, hipStream_t s);
-hipError_t launch_prep(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, PackedPlan* packed,
+hipError_t launch_prep(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, PackedPlan* packed, uint4* pcut,
                        uint32_t* meta, uint32_t* hist, hipStream_t s);
 hipError_t launch_memory(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, hipStream_t s);
-hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint32_t* meta, int64_t n, uint64_t* out_stage,
-                         hipStream_t s);
+hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint4* pcut, const uint32_t* meta, int64_t n,
+                         uint64_t* out_stage, hipStream_t s);
 hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* sstart, hipStream_t s);
 hipError_t launch_scatter(const uint32_t* meta, uint32_t nslots, uint32_t* cursor, uint32_t* ids, hipStream_t s);
 hipError_t launch_first(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s);
@@ -117,7 +117,8 @@ extern "C" void sim_destroy(sim_ctx* c) {
 }
 
 static bool plans_ok(const sim_plans* p, int64_t n) {
-  return p && p->hdr && p->cut && p->cls && p->types && p->stride >= n && n >= 0;
+  return p && p->hdr && (p->chdr ? p->ccut != nullptr : p->cut != nullptr) && p->cls && p->types &&
+         p->stride >= n && n >= 0;
 }
 
 static bool begin_event(sim_ctx* c, int kind, hipStream_t s, EventPair* e) {
@@ -137,19 +138,24 @@ static void end_event(sim_ctx* c, int kind, hipStream_t s, EventPair* e) {
 // Workspace of one chunk: packed plans, pipeline metadata, pipeline ids and
 // the deferred lists, bucket counts followed by the evaluation counters and
 // the overflow list (counts and counters cleared together), bucket cursors,
-// and the start of each stage count's pipelines.
+// the start of each stage count's pipelines, and with the per-class layout
+// the plans' class cut rows (64 bytes per plan).
 constexpr uint32_t kCounters = kBuckets + kEvalCounters;
 struct Work {
   PackedPlan* packed;
+  uint4* pcut;
   uint32_t *meta, *ids, *deferred, *hist, *ctr, *cursor, *sstart;
 };
-static size_t work_bytes(int64_t ch) {
+static size_t cut_rows_bytes(int64_t ch, bool het) { return het ? align256((size_t)ch * 64) : 0; }
+static size_t work_bytes(int64_t ch, bool het) {
   return align256((size_t)ch * sizeof(PackedPlan)) + 3 * align256((size_t)ch * 4 * 4) +
-         align256(kCounters * 4 + (size_t)ch * 4 * 4) + align256(kBuckets * 4) + align256((kMaxStages + 1) * 4);
+         align256(kCounters * 4 + (size_t)ch * 4 * 4) + align256(kBuckets * 4) + align256((kMaxStages + 1) * 4) +
+         cut_rows_bytes(ch, het);
 }
-static Work carve(void* base, int64_t ch) {
+static Work carve(void* base, int64_t ch, bool het) {
   Work w;
   char* p = (char*)base;
+  w.pcut = het ? (uint4*)p : nullptr; p += cut_rows_bytes(ch, het);
   w.packed = (PackedPlan*)p; p += align256((size_t)ch * sizeof(PackedPlan));
   w.meta = (uint32_t*)p; p += align256((size_t)ch * 16);
   w.ids = (uint32_t*)p; p += align256((size_t)ch * 16);
@@ -200,10 +206,11 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
       }
   }
   void* ws = nullptr;
-  hipError_t e = hipMallocFromPoolAsync(&ws, nbuf * work_bytes(ch), c->pool, s);
+  const bool het = plans->chdr != nullptr;
+  hipError_t e = hipMallocFromPoolAsync(&ws, nbuf * work_bytes(ch, het), c->pool, s);
   if (e != hipSuccess) ws = nullptr;
   Work w[2];
-  for (int j = 0; ws && j < nbuf; ++j) w[j] = carve((char*)ws + j * work_bytes(ch), ch);
+  for (int j = 0; ws && j < nbuf; ++j) w[j] = carve((char*)ws + j * work_bytes(ch, het), ch, het);
   EventPair call, ev;
   bool tcall = ws && begin_event(c, 2, s, &call);
   bool joined = true;
@@ -213,15 +220,17 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
     const int b = (int)(i % nbuf);
     const Work& W = w[b];
     sim_plans p = *plans;
-    p.hdr += off; p.cut += off; p.cls += off; p.types += off;
+    p.hdr += off; p.cls += off; p.types += off;
+    if (p.cut) p.cut += off;
+    if (het) { p.chdr += off; p.ccut += off; }
     if (i >= 2) e = hipStreamWaitEvent(s, done(b), 0);
     if (e == hipSuccess) e = launch_fill32(W.hist, kCounters, 0, s);
     bool t1 = e == hipSuccess && begin_event(c, 1, s, &ev);
-    if (e == hipSuccess) e = launch_prep(c->tab, p, cn, out + off, W.packed, W.meta, W.hist, s);
+    if (e == hipSuccess) e = launch_prep(c->tab, p, cn, out + off, W.packed, W.pcut, W.meta, W.hist, s);
     if (t1) end_event(c, 1, s, &ev);
     if (e == hipSuccess) e = launch_scan(W.hist, W.cursor, W.sstart, s);
     if (e == hipSuccess) e = launch_scatter(W.meta, (uint32_t)(cn * 4), W.cursor, W.ids, s);
-    const EvalArgs a = {W.packed, W.meta, W.ids, W.sstart, out + off, W.ctr, W.deferred,
+    const EvalArgs a = {W.packed, W.pcut, W.meta, W.ids, W.sstart, out + off, W.ctr, W.deferred,
                         c->timing ? c->skipped_ops : nullptr};
     EventPair e0;
     bool t0 = e == hipSuccess && begin_event(c, 0, s, &e0);
@@ -278,11 +287,14 @@ extern "C" int sim_eval_stages(sim_ctx* c, const sim_plans* plans, int64_t n, ui
   hipStream_t s = (hipStream_t)stream;
   if (hipSetDevice(c->device) != hipSuccess) return SIM_EHIP;
   void* ws = nullptr;
-  if (hipMallocFromPoolAsync(&ws, align256((size_t)n * sizeof(PackedPlan)), c->pool, s) != hipSuccess)
+  const bool het = plans->chdr != nullptr;
+  if (hipMallocFromPoolAsync(&ws, align256((size_t)n * sizeof(PackedPlan)) + cut_rows_bytes(n, het), c->pool, s) !=
+      hipSuccess)
     return SIM_ENOMEM;
   PackedPlan* packed = (PackedPlan*)ws;
-  hipError_t e = launch_prep(c->tab, *plans, n, nullptr, packed, out_class, nullptr, s);
-  if (e == hipSuccess) e = launch_stages(c->tab, packed, out_class, n, out_stage, s);
+  uint4* pcut = het ? (uint4*)((char*)ws + align256((size_t)n * sizeof(PackedPlan))) : nullptr;
+  hipError_t e = launch_prep(c->tab, *plans, n, nullptr, packed, pcut, out_class, nullptr, s);
+  if (e == hipSuccess) e = launch_stages(c->tab, packed, pcut, out_class, n, out_stage, s);
   (void)hipFreeAsync(ws, s);
   return e == hipSuccess ? SIM_OK : SIM_EHIP;
 }

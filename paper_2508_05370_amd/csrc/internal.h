@@ -96,6 +96,7 @@ constexpr uint32_t kEvalCounters = 32;
 constexpr uint32_t kSkipSlots = 512, kSkipStride = 16;
 struct EvalArgs {
   const PackedPlan* packed;
+  const void* pcut;            // per-class layout: four 16-byte cut rows per plan; nullptr for the shared layout
   const uint32_t* meta;
   const uint32_t* ids;
   const uint32_t* sstart;

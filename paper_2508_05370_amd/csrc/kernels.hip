@@ -103,7 +103,15 @@ struct Plan {
   // private memory).
   uint32_t c, rc, nc;
   uint64_t tc;
+  // per-class layout: byte c = log2 TP | (PP - 1) << 2 of class c (0 with
+  // the shared layout, where tpl, S and the cuts above hold for every class;
+  // with the per-class layout they are the pipeline's own class's)
+  uint32_t chdr;
 };
+
+__device__ __forceinline__ uint32_t cls_tpl(uint32_t chdr, uint32_t c) { return (chdr >> (8 * c)) & 3; }
+__device__ __forceinline__ uint32_t cls_S(uint32_t chdr, uint32_t c) { return ((chdr >> (8 * c + 2)) & 15) + 1; }
+__device__ __forceinline__ uint64_t stage_sel(uint32_t S) { return S == 16 ? ~0ull : ((1ull << (4 * S)) - 1); }
 
 // cut of stage s (a run-time index): mask arithmetic rather than a select,
 // which the compiler may turn into an indexed load of the plan in private
@@ -124,6 +132,7 @@ __device__ __forceinline__ Plan unpack(const PackedPlan& q, uint32_t c = 0) {
   const uint32_t hdr = q.hdr;
   p.tpl = hdr & 3; p.epl = (hdr >> 2) & 3; p.S = ((hdr >> 4) & 15) + 1; p.G = ((hdr >> 8) & 3) + 1;
   p.zero = (hdr >> 10) & 1; p.mi = (hdr >> 11) & 3; p.tp = 1u << p.tpl; p.ep = 1u << p.epl; p.psum = q.psum;
+  p.chdr = q.pad0;
   const uint64_t* cw = reinterpret_cast<const uint64_t*>(q.cut);
   p.cut_lo = cw[0];
   p.cut_hi = cw[1];
@@ -136,56 +145,83 @@ __device__ __forceinline__ Plan unpack(const PackedPlan& q, uint32_t c = 0) {
   return p;
 }
 
+// The plan of pipeline `slot` (plan slot / 4, class slot % 4).  With the
+// per-class layout the own class's TP degree, depth and cuts replace the
+// header's; its cut row is row `slot` of the per-class cut array.
+template <bool kHet>
+__device__ __forceinline__ Plan load_plan(const PackedPlan* packed, const uint4* pcut, uint32_t slot) {
+  Plan p = unpack(packed[slot >> 2], slot & 3);
+  if (kHet) {
+    p.tpl = cls_tpl(p.chdr, p.c);
+    p.tp = 1u << p.tpl;
+    p.S = cls_S(p.chdr, p.c);
+    const uint4 r = pcut[slot];
+    p.cut_lo = (uint64_t)r.y << 32 | r.x;
+    p.cut_hi = (uint64_t)r.w << 32 | r.z;
+  }
+  return p;
+}
+
 // micro-batches per replica of the pipeline's class (its M)
 __device__ __forceinline__ uint32_t class_mb(const Plan& p) { return (p.nc + p.rc - 1) / p.rc; }
 
 constexpr int kPrepPerThread = 4;
 
 // Plan i as loaded and checked by one lane: every rule of the plan layout
-// except the memory check.
+// except the memory check.  Per-class quantities are kept per class; with
+// the shared layout every class has the header's.
 struct Checked {
   bool ok;
-  uint32_t hdr, psum;
-  uint32_t cw[4];          // cut bytes, four per word
+  uint32_t hdr, psum, chdr;
+  uint32_t tpl[4], S[4];   // per class
+  uint32_t cw[4][4];       // per class: cut bytes, four per word, 0 past the class's stages
   uint32_t cls[4];         // 0 past the class count
-  uint64_t tv[4];          // stage types, nibbles past PP cleared; 0 past the class count
+  uint64_t tv[4];          // stage types, nibbles past the class's stages cleared; 0 past the class count
 };
 
+template <bool kHet>
 __device__ __forceinline__ Checked check_plan(const Tab& t, const sim_plans& pl, int64_t i) {
   Checked r;
   const int64_t st = pl.stride;
-  // all 16 cut planes and 4 class planes exist: load them before any use
+  // every plane exists: load before any use
   const uint32_t hdr = pl.hdr[i];
-  uint32_t cb[16];
+  uint32_t cb[kHet ? 64 : 16];
 #pragma unroll
-  for (int s = 0; s < 16; ++s) cb[s] = pl.cut[s * st + i];
+  for (int s = 0; s < (kHet ? 64 : 16); ++s) cb[s] = kHet ? pl.ccut[s * st + i] : pl.cut[s * st + i];
+  const uint32_t chdr = kHet ? pl.chdr[i] : 0;
 #pragma unroll
   for (int c = 0; c < 4; ++c) {
     r.cls[c] = pl.cls[c * st + i];
     r.tv[c] = pl.types[c * st + i];
   }
-  const uint32_t tpl = hdr & 3, epl = (hdr >> 2) & 3, S = ((hdr >> 4) & 15) + 1, G = ((hdr >> 8) & 3) + 1;
-  const uint32_t mi = (hdr >> 11) & 3;
-  const uint32_t tp = 1u << tpl, ep = 1u << epl;
-  bool ok = (hdr >> 13) == 0 && mi < t.n_mbs && ((t.tp_ok >> tpl) & 1) && ((t.ep_ok >> epl) & 1);
-  uint32_t prev = 0;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) r.cw[j] = 0;
-#pragma unroll
-  for (uint32_t s = 0; s < 16; ++s) {
-    if (s < S) {
-      ok = ok && cb[s] > prev;
-      prev = cb[s];
-      r.cw[s >> 2] |= cb[s] << (8 * (s & 3));
-    }
-  }
-  ok = ok && prev == t.L;
-  const uint64_t sel = S == 16 ? ~0ull : ((1ull << (4 * S)) - 1);
+  const uint32_t epl = (hdr >> 2) & 3, G = ((hdr >> 8) & 3) + 1, mi = (hdr >> 11) & 3;
+  const uint32_t ep = 1u << epl;
+  bool ok = (hdr >> 13) == 0 && mi < t.n_mbs && ((t.ep_ok >> epl) & 1);
+  if (kHet) ok = ok && (hdr & 0xf3) == 0;     // the header's TP and PP fields are unused
   uint32_t batch = 0, psum = 0;
 #pragma unroll
   for (uint32_t c = 0; c < 4; ++c) {
+    const uint32_t lay = kHet ? (chdr >> (8 * c)) & 0xff : (hdr & 3) | (((hdr >> 4) & 15) << 2);
+    const uint32_t tpl = lay & 3, S = ((lay >> 2) & 15) + 1;
+    r.tpl[c] = tpl;
+    r.S[c] = S;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) r.cw[c][j] = 0;
     if (c < G) {
-      r.tv[c] &= sel;
+      if (kHet) ok = ok && (lay >> 6) == 0;
+      ok = ok && ((t.tp_ok >> tpl) & 1);
+      uint32_t prev = 0;
+#pragma unroll
+      for (uint32_t s = 0; s < 16; ++s) {
+        if (s < S) {
+          const uint32_t v = cb[(kHet ? 16 * c : 0) + s];
+          ok = ok && v > prev;
+          prev = v;
+          r.cw[c][s >> 2] |= v << (8 * (s & 3));
+        }
+      }
+      ok = ok && prev == t.L;
+      r.tv[c] &= stage_sel(S);
       const uint32_t reps = r.cls[c] & 0xffff, nmb = r.cls[c] >> 16;
       ok = ok && reps >= 1 && nmb >= reps && (reps & (ep - 1)) == 0;
       batch += nmb * t.mbs[mi];
@@ -199,28 +235,33 @@ __device__ __forceinline__ Checked check_plan(const Tab& t, const sim_plans& pl,
     }
   }
   ok = ok && batch == t.gbs;
+  // capacity of every pool under the packing (blocks aligned to their TP degree)
   for (uint32_t k = 0; ok && k < t.K; ++k) {
     uint32_t need = 0;
 #pragma unroll
-    for (uint32_t c = 0; c < 4; ++c)
-      if (c < G) need += (r.cls[c] & 0xffff) * count_type(r.tv[c], k, sel);
-    ok = need * tp <= t.cap[k];
+    for (uint32_t c = 0; c < 4; ++c) {
+      const uint32_t nk = c < G ? count_type(r.tv[c], k, stage_sel(r.S[c])) : 0;
+      if (nk) need = ((need + (1u << r.tpl[c]) - 1) >> r.tpl[c] << r.tpl[c]) + (((r.cls[c] & 0xffff) * nk) << r.tpl[c]);
+    }
+    ok = need <= t.cap[k];
   }
   r.ok = ok;
   r.hdr = hdr;
   r.psum = psum;
+  r.chdr = chdr;
   return r;
 }
 
-// Peak bytes of one device of stage s (layers lo..hi) apart from its stored
-// activations: weights and gradients of the parameters its TP rank holds,
-// and the optimizer state, split with ZeRO over the stage's DP group (all
-// replicas for the non-expert parameters, replicas / EP for the experts).
-__device__ __forceinline__ uint64_t state_bytes(const Tab& t, uint32_t hdr, uint32_t psum, uint32_t s, uint32_t ns) {
-  const uint32_t tpl = hdr & 3, epl = (hdr >> 2) & 3, S = ((hdr >> 4) & 15) + 1, zero = (hdr >> 10) & 1;
+// Peak bytes of one device of a stage of ns layers at TP 2^tpl apart from
+// its stored activations: weights and gradients of the parameters its TP
+// rank holds, and the optimizer state, split with ZeRO over the DP group
+// (all replicas for the non-expert parameters, replicas / EP for the
+// experts).
+__device__ __forceinline__ uint64_t state_bytes(const Tab& t, uint32_t tpl, uint32_t epl, uint32_t zero,
+                                                uint32_t psum, bool first, bool last, uint32_t ns) {
   uint64_t pd = (uint64_t)ns * t.par_layer[tpl];
-  if (s == 0) pd += t.par_embed[tpl];
-  if (s == S - 1) pd += t.par_head[tpl];
+  if (first) pd += t.par_embed[tpl];
+  if (last) pd += t.par_head[tpl];
   const uint64_t pe = (uint64_t)ns * t.par_expert[tpl][epl];
   uint64_t od = t.opt_bytes * pd, oe = t.opt_bytes * pe;
   if (zero) {
@@ -231,45 +272,51 @@ __device__ __forceinline__ uint64_t state_bytes(const Tab& t, uint32_t hdr, uint
   return (t.param_bytes + t.grad_bytes) * (pd + pe) + od + oe;
 }
 
-// Peak bytes of the devices of stage s of every class: state plus the
-// activations of the min(PP - s, M) micro-batches 1F1B keeps in flight there.
-__device__ __forceinline__ uint64_t class_stage_bytes(const Tab& t, const Checked& r, uint32_t c, uint32_t s,
-                                                      uint32_t ns, uint64_t state) {
-  const uint32_t tpl = r.hdr & 3, S = ((r.hdr >> 4) & 15) + 1, mi = (r.hdr >> 11) & 3;
-  const uint32_t reps = r.cls[c] & 0xffff, M = ((r.cls[c] >> 16) + reps - 1) / reps;
-  const uint32_t fly = S - s < M ? S - s : M;
-  return state + (uint64_t)ns * fly * t.act_layer[tpl][mi];
-}
-
-// cut byte of stage s (run-time index) of a checked plan
-__device__ __forceinline__ uint32_t checked_cut(const Checked& r, uint32_t s) {
-  const uint64_t lo = (uint64_t)r.cw[0] | ((uint64_t)r.cw[1] << 32), hi = (uint64_t)r.cw[2] | ((uint64_t)r.cw[3] << 32);
+// cut byte of stage s (run-time index) of class c (a compile-time index) of a checked plan
+__device__ __forceinline__ uint32_t checked_cut(const Checked& r, uint32_t c, uint32_t s) {
+  const uint64_t lo = (uint64_t)r.cw[c][0] | ((uint64_t)r.cw[c][1] << 32);
+  const uint64_t hi = (uint64_t)r.cw[c][2] | ((uint64_t)r.cw[c][3] << 32);
   const uint64_t m = 0ull - (uint64_t)(s >> 3);
   return (uint32_t)(((lo & ~m) | (hi & m)) >> (8 * (s & 7))) & 0xff;
 }
 
+// Peak bytes of the devices of stage s (ns layers) of class c: state plus the
+// activations of the min(PP - s, M) micro-batches 1F1B keeps in flight there.
+__device__ __forceinline__ uint64_t class_stage_bytes(const Tab& t, const Checked& r, uint32_t c, uint32_t s,
+                                                      uint32_t ns) {
+  const uint32_t epl = (r.hdr >> 2) & 3, zero = (r.hdr >> 10) & 1, mi = (r.hdr >> 11) & 3;
+  const uint32_t S = r.S[c], tpl = r.tpl[c];
+  const uint32_t reps = r.cls[c] & 0xffff, M = ((r.cls[c] >> 16) + reps - 1) / reps;
+  const uint32_t fly = S - s < M ? S - s : M;
+  return state_bytes(t, tpl, epl, zero, r.psum, s == 0, s == S - 1, ns) + (uint64_t)ns * fly * t.act_layer[tpl][mi];
+}
+
 // Every device of a checked plan fits its type's memory.
 __device__ __forceinline__ bool fits_memory(const Tab& t, const Checked& r) {
-  const uint32_t S = ((r.hdr >> 4) & 15) + 1, G = ((r.hdr >> 8) & 3) + 1;
+  const uint32_t G = ((r.hdr >> 8) & 3) + 1;
   bool ok = true;
-  uint32_t prev = 0;
-  for (uint32_t s = 0; s < S; ++s) {
-    const uint32_t cut = checked_cut(r, s), ns = cut - prev;
-    prev = cut;
-    const uint64_t state = state_bytes(t, r.hdr, r.psum, s, ns);
 #pragma unroll
-    for (uint32_t c = 0; c < 4; ++c)
-      if (c < G) ok = ok && class_stage_bytes(t, r, c, s, ns, state) <= t.mem_cap[(uint32_t)(r.tv[c] >> (4 * s)) & 15];
+  for (uint32_t c = 0; c < 4; ++c) {
+    if (c >= G) continue;
+    uint32_t prev = 0;
+    for (uint32_t s = 0; s < r.S[c]; ++s) {
+      const uint32_t cut = checked_cut(r, c, s), ns = cut - prev;
+      prev = cut;
+      ok = ok && class_stage_bytes(t, r, c, s, ns) <= t.mem_cap[(uint32_t)(r.tv[c] >> (4 * s)) & 15];
+    }
   }
   return ok;
 }
 
-// Decode and check plan i (every rule of the plan layout); on success pack it.
-// Writes out[i] (0 = valid, to be raised by the pipelines; else invalid) and
-// the per-pipeline metadata S | G << 5 | M << 8 (0 = no pipeline).
+// Decode and check plan i (every rule of the plan layout); on success pack it
+// (with the per-class layout, the class header word goes to pad0 and each
+// class's cut row to pcut[4 i + c]).  Writes out[i] (0 = valid, to be raised
+// by the pipelines; else invalid) and the per-pipeline metadata
+// S | G << 5 | M << 8 with the class's own S (0 = no pipeline).
+template <bool kHet>
 __global__ void __launch_bounds__(256) k_prep(Tab t, sim_plans pl, int64_t n, uint64_t* __restrict__ out,
-                                              PackedPlan* __restrict__ packed, uint32_t* __restrict__ meta,
-                                              uint32_t* __restrict__ hist) {
+                                              PackedPlan* __restrict__ packed, uint4* __restrict__ pcut,
+                                              uint32_t* __restrict__ meta, uint32_t* __restrict__ hist) {
   __shared__ uint32_t lh[kBuckets];
   if (hist) {
     for (uint32_t j = threadIdx.x; j < kBuckets; j += blockDim.x) lh[j] = 0;
@@ -278,25 +325,29 @@ __global__ void __launch_bounds__(256) k_prep(Tab t, sim_plans pl, int64_t n, ui
   for (int rep = 0; rep < kPrepPerThread; ++rep) {
     const int64_t i = ((int64_t)blockIdx.x * kPrepPerThread + rep) * blockDim.x + threadIdx.x;
     if (i >= n) break;
-    const Checked r = check_plan(t, pl, i);
+    const Checked r = check_plan<kHet>(t, pl, i);
     const bool ok = r.ok && (!t.mem_check || fits_memory(t, r));
-    const uint32_t S = ((r.hdr >> 4) & 15) + 1, G = ((r.hdr >> 8) & 3) + 1;
+    const uint32_t G = ((r.hdr >> 8) & 3) + 1;
     if (out) out[i] = ok ? 0 : kInvalid;
     if (ok) {
       PackedPlan q;
-      q.hdr = r.hdr; q.psum = r.psum; q.pad0 = 0; q.pad1 = 0;
+      q.hdr = r.hdr; q.psum = r.psum; q.pad0 = r.chdr; q.pad1 = 0;
       uint32_t* qc = reinterpret_cast<uint32_t*>(q.cut);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) { qc[j] = r.cw[j]; q.cls[j] = r.cls[j]; q.types[j] = r.tv[j]; }
+      for (int j = 0; j < 4; ++j) { qc[j] = r.cw[0][j]; q.cls[j] = r.cls[j]; q.types[j] = r.tv[j]; }
       packed[i] = q;
+      if (kHet) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) pcut[4 * i + c] = make_uint4(r.cw[c][0], r.cw[c][1], r.cw[c][2], r.cw[c][3]);
+      }
     }
 #pragma unroll
     for (uint32_t c = 0; c < 4; ++c) {
       uint32_t m = 0;
       if (ok && c < G) {
         const uint32_t reps = r.cls[c] & 0xffff, M = ((r.cls[c] >> 16) + reps - 1) / reps;
-        m = S | (G << 5) | (M << 8);
-        if (hist) atomicAdd(&lh[bucket_key(S, G, M)], 1u);
+        m = r.S[c] | (G << 5) | (M << 8);
+        if (hist) atomicAdd(&lh[bucket_key(r.S[c], G, M)], 1u);
       }
       meta[i * 4 + c] = m;
     }
@@ -309,21 +360,26 @@ __global__ void __launch_bounds__(256) k_prep(Tab t, sim_plans pl, int64_t n, ui
 }
 
 // Peak memory of every (class, stage) device of plan i (one plan per lane).
+template <bool kHet>
 __global__ void __launch_bounds__(256) k_memory(Tab t, sim_plans pl, int64_t n, uint64_t* __restrict__ out) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
-  const Checked r = check_plan(t, pl, i);
-  const uint32_t S = ((r.hdr >> 4) & 15) + 1, G = ((r.hdr >> 8) & 3) + 1;
+  const Checked r = check_plan<kHet>(t, pl, i);
+  const uint32_t G = ((r.hdr >> 8) & 3) + 1;
   uint64_t* o = out + i * (kMaxClasses * kMaxStages);
-  uint32_t prev = 0;
-  for (uint32_t s = 0; s < (uint32_t)kMaxStages; ++s) {
-    const uint32_t cut = s < S ? checked_cut(r, s) : prev, ns = cut - prev;
-    prev = cut;
-    const uint64_t state = r.ok && s < S ? state_bytes(t, r.hdr, r.psum, s, ns) : 0;
 #pragma unroll
-    for (uint32_t c = 0; c < 4; ++c) {
+  for (uint32_t c = 0; c < 4; ++c) {
+    uint32_t prev = 0;
+    for (uint32_t s = 0; s < (uint32_t)kMaxStages; ++s) {
       uint64_t v = kInvalid;
-      if (r.ok) v = c < G && s < S ? class_stage_bytes(t, r, c, s, ns, state) : 0;
+      if (r.ok) {
+        v = 0;
+        if (c < G && s < r.S[c]) {
+          const uint32_t cut = checked_cut(r, c, s);
+          v = class_stage_bytes(t, r, c, s, cut - prev);
+          prev = cut;
+        }
+      }
       o[c * kMaxStages + s] = v;
     }
   }
@@ -398,6 +454,41 @@ __device__ __forceinline__ uint32_t placed_before_own(const Plan& p, uint32_t s,
   return below + p.rc * count_type(p.tc, k, (1ull << (4 * s)) - 1);
 }
 
+// Devices of type k taken before (class c2, stage s), and the same for the
+// pipeline's own class, under either layout.  With the per-class layout each
+// class takes reps * its own TP degree devices per stage, and its blocks
+// start at a multiple of that degree (so no TP group spans two nodes): a
+// class's blocks in a pool are contiguous after its first one is aligned.
+__device__ __forceinline__ uint32_t align_up(uint32_t x, uint32_t tpl) { return ((x + (1u << tpl) - 1) >> tpl) << tpl; }
+
+template <bool kHet>
+__device__ __forceinline__ uint32_t dev_before(const Plan& p, uint32_t c2, uint32_t s, uint32_t k) {
+  if (!kHet) return placed_before(p, c2, s, k) * p.tp;
+  uint32_t ptr = 0;
+#pragma unroll
+  for (uint32_t c3 = 0; c3 < 4; ++c3) {
+    if (c3 < c2) {
+      const uint32_t tl = cls_tpl(p.chdr, c3), nk = count_type(p.tv[c3], k, stage_sel(cls_S(p.chdr, c3)));
+      if (nk) ptr = align_up(ptr, tl) + ((p.reps[c3] * nk) << tl);
+    }
+  }
+  const uint32_t tl = cls_tpl(p.chdr, c2);
+  return align_up(ptr, tl) + ((p.reps[c2] * count_type(p.tv[c2], k, (1ull << (4 * s)) - 1)) << tl);
+}
+template <bool kHet>
+__device__ __forceinline__ uint32_t dev_before_own(const Plan& p, uint32_t s, uint32_t k) {
+  if (!kHet) return placed_before_own(p, s, k) * p.tp;
+  uint32_t ptr = 0;
+#pragma unroll
+  for (uint32_t c3 = 0; c3 < 4; ++c3) {
+    if (c3 < p.c) {
+      const uint32_t tl = cls_tpl(p.chdr, c3), nk = count_type(p.tv[c3], k, stage_sel(cls_S(p.chdr, c3)));
+      if (nk) ptr = align_up(ptr, tl) + ((p.reps[c3] * nk) << tl);
+    }
+  }
+  return align_up(ptr, p.tpl) + ((p.rc * count_type(p.tc, k, (1ull << (4 * s)) - 1)) << p.tpl);
+}
+
 // DP sync of stage s (layers [lo, hi), ns = hi - lo) over every replica of
 // every class: one ring across all replicas on the slowest NIC of the
 // participating devices, or inside one node when every replica of the stage
@@ -441,9 +532,114 @@ __device__ __forceinline__ uint64_t stage_dp(const Tab& t, const Hot<kMode>& h, 
   return tdp;
 }
 
-template <int kMode, typename Sink>
+// Per-class layout.  The gradients of layers [a, e) -- a segment between
+// consecutive cuts of any class, so inside one stage of every class -- sync
+// in one ring over every replica, on the coarsest TP layout among the
+// classes; before it, each class with finer shards gathers the coarse shard
+// inside its TP groups (ring all-gather over 2^(tpl - tpl_min) members of
+// the class's own shard, on the node fabric; classes at the same time, so
+// the slowest counts).  rows: the plan's four class cut rows.
+__device__ __forceinline__ uint32_t row_word(const uint4 (&rows)[4], uint32_t c, uint32_t j) {
+  const uint4 v = rows[c];
+  return j == 0 ? v.x : j == 1 ? v.y : j == 2 ? v.z : v.w;
+}
+
+template <int kMode>
+__device__ __forceinline__ uint64_t seg_dp(const Tab& t, const Hot<kMode>& h, const Plan& p, const uint4 (&rows)[4],
+                                           uint32_t a, uint32_t e, double rp, double rpe) {
+  const uint32_t G = p.G, epl = p.epl, ns = e - a;
+  uint32_t tmin = 3;
+#pragma unroll
+  for (uint32_t c2 = 0; c2 < 4; ++c2)
+    if (c2 < G) tmin = cls_tpl(p.chdr, c2) < tmin ? cls_tpl(p.chdr, c2) : tmin;
+  bool same = true;
+  uint32_t k0 = 0, nmin = 0xffffffffu, nmax = 0, bq_dp = 0;
+  uint64_t a_dp = 0, rs = 0;
+#pragma unroll
+  for (uint32_t c2 = 0; c2 < 4; ++c2) {
+    if (c2 >= G) continue;
+    const uint32_t tpl2 = cls_tpl(p.chdr, c2);
+    // the stage of class c2 holding layer a: its cuts in (0, a] (bytes past its stages are 0)
+    uint32_t s2 = 0;
+#pragma unroll
+    for (uint32_t j = 0; j < 4; ++j) {
+      const uint32_t w = row_word(rows, c2, j);
+#pragma unroll
+      for (uint32_t q = 0; q < 4; ++q) {
+        const uint32_t v = (w >> (8 * q)) & 0xff;
+        s2 += (v != 0 && v <= a) ? 1u : 0u;
+      }
+    }
+    const uint32_t k2 = (uint32_t)(p.tv[c2] >> (4 * s2)) & 15;
+    const TypeInfo t2 = h.type(k2);
+    const uint32_t b2 = dev_before<true>(p, c2, s2, k2), n2 = p.reps[c2] << tpl2, d2 = t2.dpl;
+    const uint32_t l2 = t2.node_off + (b2 >> d2), h2 = t2.node_off + ((b2 + n2 - 1) >> d2);
+    const uint32_t dl2 = t2.dev_off + b2;
+    const uint32_t nic2 = range_max(h.rmn, t.D, dl2, dl2 + n2 - 1);
+    if (c2 == 0) k0 = k2; else same = same && k2 == k0;
+    nmin = l2 < nmin ? l2 : nmin;
+    nmax = h2 > nmax ? h2 : nmax;
+    const uint32_t bx = nic2 > t2.bq_pcie ? nic2 : t2.bq_pcie;
+    bq_dp = bx > bq_dp ? bx : bq_dp;
+    a_dp = 2 * t2.a_side > a_dp ? 2 * t2.a_side : a_dp;
+    if (tpl2 > tmin) {
+      const uint64_t g1 = (1u << (tpl2 - tmin)) - 1;
+      const uint64_t sh = (uint64_t)ns * (t.par_layer[tpl2] + t.par_expert[tpl2][epl]) +
+                          (a == 0 ? t.par_embed[tpl2] : 0) + (e == t.L ? t.par_head[tpl2] : 0);
+      const uint32_t bq_in = range_max(h.rmi(), t.N, l2, h2);
+      const uint64_t r = g1 * t2.a_intra + link_ps(g1 * t.grad_bytes * sh, bq_in);
+      rs = r > rs ? r : rs;
+    }
+  }
+  const bool intra = same && nmin == nmax;
+  const uint64_t alpha = intra ? h.type(k0).a_intra : a_dp;
+  const uint32_t bq = intra ? h.rmi()[nmin] : bq_dp;
+  const uint64_t pd = (uint64_t)ns * t.par_layer[tmin] + (a == 0 ? t.par_embed[tmin] : 0) +
+                      (e == t.L ? t.par_head[tmin] : 0);
+  uint64_t tdp = p.psum <= 1 ? 0 : ring_sync(p.psum, rp, p.zero, t.grad_bytes * pd, t.param_bytes * pd, alpha, bq);
+  const uint32_t pe = p.psum >> epl;
+  if (t.E && pe > 1) {
+    const uint64_t px = (uint64_t)ns * t.par_expert[tmin][epl];
+    tdp += ring_sync(pe, rpe, p.zero, t.grad_bytes * px, t.param_bytes * px, alpha, bq);
+  }
+  return tdp + rs;
+}
+
+// The sync a stage [lo, hi) of the pipeline's class waits for: the longest
+// of the segments inside it.
+template <int kMode>
+__device__ __forceinline__ uint64_t het_stage_dp(const Tab& t, const Hot<kMode>& h, const Plan& p,
+                                                 const uint4 (&rows)[4], uint32_t lo, uint32_t hi, double rp,
+                                                 double rpe) {
+  uint64_t best = 0;
+  for (uint32_t a = lo; a < hi;) {
+    uint32_t e = hi;   // the next cut of any class above a
+#pragma unroll
+    for (uint32_t c2 = 0; c2 < 4; ++c2)
+#pragma unroll
+      for (uint32_t j = 0; j < 4; ++j) {
+        const uint32_t w = row_word(rows, c2, j);
+#pragma unroll
+        for (uint32_t q = 0; q < 4; ++q) {
+          const uint32_t v = (w >> (8 * q)) & 0xff;
+          e = (v > a && v < e) ? v : e;
+        }
+      }
+    const uint64_t x = seg_dp(t, h, p, rows, a, e, rp, rpe);
+    best = x > best ? x : best;
+    a = e;
+  }
+  return best;
+}
+
+__device__ __forceinline__ void load_rows(const uint4* prow, uint4 (&rows)[4]) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) rows[c] = prow[c];
+}
+
+template <int kMode, bool kHet, typename Sink>
 __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t c,
-                                            Sink& sink) {
+                                            Sink& sink, const uint4* prow) {
   const uint32_t S = p.S, tp = p.tp, ep = p.ep, tpl = p.tpl, epl = p.epl, mi = p.mi;
   const uint64_t act = t.act[mi], act_tp = (act + tp - 1) >> tpl;
   const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> epl);
@@ -457,7 +653,7 @@ __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, c
     // ---- this class: compute, TP, EP, hop from the previous stage
     const uint32_t k = (uint32_t)(tvc >> (4 * s)) & 15;
     const TypeInfo ti = h.type(k);
-    const uint32_t base = placed_before_own(p, s, k) * tp, nd = reps * tp, dpl = ti.dpl;
+    const uint32_t base = dev_before_own<kHet>(p, s, k), nd = reps * tp, dpl = ti.dpl;
     const uint32_t gnl = ti.node_off + (base >> dpl), gnh = ti.node_off + ((base + nd - 1) >> dpl);
     const uint32_t bq_in = range_max(h.rmi(), t.N, gnl, gnh);
     const uint32_t dlo = ti.dev_off + base;
@@ -488,8 +684,19 @@ __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, c
       fc += steps * ti.a_intra + link_ps(steps * act_tp, bq_in);
     }
     if (t.E && ep > 1) {  // dispatch + combine all-to-all in each pass
-      // EP groups are aligned blocks of ep*tp devices: inside a node iff they fit one
-      const bool intra = ep * tp <= (1u << dpl);
+      // EP groups are blocks of ep*tp devices from base on.  With one TP
+      // degree for all classes base is a multiple of ep*tp, and the groups
+      // are inside nodes iff one fits a node.  With per-class degrees, a
+      // group of E = ep*tp <= node size starting at offset r in its node
+      // fits iff r <= node - E; the offsets of the successive groups are
+      // base's in-node offset plus multiples of E, so with b = base mod E
+      // != 0 the first group to cross is number node/E - 1 - (in-node offset div E).
+      const uint32_t E = ep * tp;
+      bool intra = E <= (1u << dpl);
+      if (kHet && intra && (base & (E - 1)) != 0) {
+        const uint32_t q = (base & ((1u << dpl) - 1)) / E;
+        intra = reps / ep <= (1u << dpl) / E - 1 - q;
+      }
       const uint64_t alpha = intra ? ti.a_intra : 2 * ti.a_side;
       const uint32_t bq = intra ? bq_in : (bq_nic > ti.bq_pcie ? bq_nic : ti.bq_pcie);
       const uint32_t pa = (epl * t.n_mbs + mi) * L1;
@@ -514,7 +721,16 @@ __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, c
     }
     pk = k; pbase = base; pnic = bq_nic; pin = bq_in; pti = ti;
     // ---- DP sync of this stage (the sink may leave it for later)
-    const uint64_t tdp = Sink::kDp ? stage_dp(t, h, p, s, ns, rp, rpe) : 0;
+    uint64_t tdp = 0;
+    if (Sink::kDp) {
+      if (kHet) {
+        uint4 rows[4];
+        load_rows(prow, rows);
+        tdp = het_stage_dp(t, h, p, rows, lo, hi, rp, rpe);
+      } else {
+        tdp = stage_dp(t, h, p, s, ns, rp, rpe);
+      }
+    }
     sink.put(s, fc, bc, hop, tdp);
     lo = hi;
   }
@@ -564,14 +780,18 @@ struct RegSink {
 // Iteration time from the end of each stage's last op: the max over stages
 // of that end plus the stage's DP sync, walking the stages with the same
 // shift so that no array is indexed at run time.
-template <int S, int kMode>
-__device__ __forceinline__ double dp_tail(const Tab& t, const Hot<kMode>& h, const Plan& p, double (&last)[S]) {
+template <int S, int kMode, bool kHet>
+__device__ __forceinline__ double dp_tail(const Tab& t, const Hot<kMode>& h, const Plan& p, double (&last)[S],
+                                          const uint4* prow) {
   const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> p.epl);
+  uint4 rows[4];
+  if (kHet) load_rows(prow, rows);
   double T = 0;
   uint32_t lo = 0;
   for (uint32_t s = 0; s < (uint32_t)S; ++s) {
     const uint32_t hi = cut_at(p, s);
-    const double e = last[0] + (double)stage_dp(t, h, p, s, hi - lo, rp, rpe);
+    const uint64_t d = kHet ? het_stage_dp(t, h, p, rows, lo, hi, rp, rpe) : stage_dp(t, h, p, s, hi - lo, rp, rpe);
+    const double e = last[0] + (double)d;
     T = e > T ? e : T;
 #pragma unroll
     for (int i = 0; i + 1 < S; ++i) last[i] = last[i + 1];
@@ -581,16 +801,17 @@ __device__ __forceinline__ double dp_tail(const Tab& t, const Hot<kMode>& h, con
 }
 
 // per (class, stage) quantities of every plan, in plan order
+template <bool kHet>
 __global__ void __launch_bounds__(256) k_stages(Tab t, const PackedPlan* __restrict__ packed,
-                                                const uint32_t* __restrict__ meta, int64_t n,
-                                                uint64_t* __restrict__ out_stage) {
+                                                const uint4* __restrict__ pcut, const uint32_t* __restrict__ meta,
+                                                int64_t n, uint64_t* __restrict__ out_stage) {
   const int64_t slot = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (slot >= n * 4 || meta[slot] == 0) return;
-  const Plan p = unpack(packed[slot >> 2], (uint32_t)(slot & 3));
+  const Plan p = load_plan<kHet>(packed, pcut, (uint32_t)slot);
   uint64_t rec[kMaxStages][kRecWords];
   const Hot<2> h(t, nullptr);
   RecSink sink{rec};
-  class_setup(t, h, p, (uint32_t)(slot & 3), sink);
+  class_setup<2, kHet>(t, h, p, (uint32_t)(slot & 3), sink, kHet ? pcut + (slot & ~3ll) : nullptr);
   uint64_t* o = out_stage + slot * (kMaxStages * kRecWords);
   for (uint32_t s = 0; s < p.S; ++s)
 #pragma unroll
@@ -805,6 +1026,7 @@ constexpr double kExact = 9007199254740992.0;
 // Device buffers of one evaluation pass over a chunk.
 struct EvalBufs {
   const PackedPlan* packed;
+  const uint4* pcut;        // per-class layout: cut row of pipeline slot at [slot]
   const uint32_t* meta;
   const uint32_t* ids;      // pipeline ids sorted by bucket
   const uint32_t* sstart;   // [16 - S]: start of the S-stage pipelines in ids; [16] = total
@@ -822,14 +1044,14 @@ struct EvalBufs {
 // [64b, 64b + 64); blocks past the range return at once.  This first pass
 // takes the periodic shortcut and defers the lanes still aperiodic after the
 // budget; k_deferred runs those through the whole steady loop.
-template <int S, bool kFull, int kMode>
+template <int S, bool kFull, int kMode, bool kHet>
 __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot) {
   RegSink<S> r;
   uint32_t M;
   {
-    const Plan p = unpack(e.packed[slot >> 2], slot & 3);
+    const Plan p = load_plan<kHet>(e.packed, e.pcut, slot);
     M = class_mb(p);
-    class_setup(t, h, p, slot & 3, r);
+    class_setup<kMode, kHet>(t, h, p, slot & 3, r, nullptr);
   }
   int skipped;
   double last[S];
@@ -839,7 +1061,9 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
   // shuffle is opaque to the compiler, which would otherwise reuse the
   // first load
   const uint32_t slot2 = __shfl(slot, (int)(threadIdx.x & 63u));
-  const double T = done ? dp_tail(t, h, unpack(e.packed[slot2 >> 2], slot2 & 3), last) : 0;
+  const double T = done ? dp_tail<S, kMode, kHet>(t, h, load_plan<kHet>(e.packed, e.pcut, slot2), last,
+                                                   kHet ? e.pcut + (slot2 & ~3u) : nullptr)
+                         : 0;
   if (!done) {
     e.deferred[e.sstart[kMaxStages - S] + atomicAdd(&e.ctr[1 + kMaxStages - S], 1u)] = slot;
     return;
@@ -861,7 +1085,7 @@ constexpr uint32_t kEvalThreads = 256;
 // over the whole chunk would mostly start blocks past the group's range,
 // each holding a full LDS allocation); the waves of the grid take the
 // group's 64-pipeline tiles in a fixed stride, heaviest tiles first.
-template <int GRP, int kMode>
+template <int GRP, int kMode, bool kHet>
 __global__ void __launch_bounds__(kEvalThreads) k_eval(Tab t, EvalBufs e) {
   constexpr int kTop = kMaxStages - 4 * GRP;   // stage counts kTop-3 .. kTop
   extern __shared__ uint4 lds[];
@@ -874,17 +1098,17 @@ __global__ void __launch_bounds__(kEvalThreads) k_eval(Tab t, EvalBufs e) {
     const uint32_t pos = base + (threadIdx.x & 63u);
     bool pending = pos < hi;
     const uint32_t slot = pending ? e.ids[pos] : 0;
-    const uint32_t S = pending ? ((e.packed[slot >> 2].hdr >> 4) & 15) + 1 : 0;
+    const uint32_t S = !pending ? 0 : kHet ? e.meta[slot] & 31 : ((e.packed[slot >> 2].hdr >> 4) & 15) + 1;
     // one pass per distinct stage count present in the wavefront (usually one)
     while (true) {
       const uint64_t live = __ballot(pending);
       if (!live) break;
       const uint32_t S0 = __builtin_amdgcn_readfirstlane(__shfl(S, __ffsll((unsigned long long)live) - 1));
       if (pending && S == S0) {
-        if (S0 == kTop) eval_one<kTop, false>(t, h, e, slot);
-        else if (S0 == kTop - 1) eval_one<kTop - 1, false>(t, h, e, slot);
-        else if (S0 == kTop - 2) eval_one<kTop - 2, false>(t, h, e, slot);
-        else eval_one<kTop - 3, false>(t, h, e, slot);
+        if (S0 == kTop) eval_one<kTop, false, kMode, kHet>(t, h, e, slot);
+        else if (S0 == kTop - 1) eval_one<kTop - 1, false, kMode, kHet>(t, h, e, slot);
+        else if (S0 == kTop - 2) eval_one<kTop - 2, false, kMode, kHet>(t, h, e, slot);
+        else eval_one<kTop - 3, false, kMode, kHet>(t, h, e, slot);
         pending = false;
       }
     }
@@ -896,7 +1120,7 @@ __global__ void __launch_bounds__(kEvalThreads) k_eval(Tab t, EvalBufs e) {
 // pipelines sit at [sstart[16 - S], + ctr[1 + 16 - S]); tile q of 64 is
 // located by walking the sixteen list lengths (16 stages first), and tiles
 // are dealt round-robin to the waves of the grid.
-template <int kMode>
+template <int kMode, bool kHet>
 __global__ void __launch_bounds__(kEvalThreads) k_deferred(Tab t, EvalBufs e) {
   extern __shared__ uint4 lds[];
   fill_lds<kMode>(t, lds);
@@ -914,22 +1138,22 @@ __global__ void __launch_bounds__(kEvalThreads) k_deferred(Tab t, EvalBufs e) {
     if (off >= e.ctr[1 + j]) continue;
     const uint32_t slot = e.deferred[e.sstart[j] + off];
     switch (kMaxStages - j) {
-      case 1: eval_one<1, true>(t, h, e, slot); break;
-      case 2: eval_one<2, true>(t, h, e, slot); break;
-      case 3: eval_one<3, true>(t, h, e, slot); break;
-      case 4: eval_one<4, true>(t, h, e, slot); break;
-      case 5: eval_one<5, true>(t, h, e, slot); break;
-      case 6: eval_one<6, true>(t, h, e, slot); break;
-      case 7: eval_one<7, true>(t, h, e, slot); break;
-      case 8: eval_one<8, true>(t, h, e, slot); break;
-      case 9: eval_one<9, true>(t, h, e, slot); break;
-      case 10: eval_one<10, true>(t, h, e, slot); break;
-      case 11: eval_one<11, true>(t, h, e, slot); break;
-      case 12: eval_one<12, true>(t, h, e, slot); break;
-      case 13: eval_one<13, true>(t, h, e, slot); break;
-      case 14: eval_one<14, true>(t, h, e, slot); break;
-      case 15: eval_one<15, true>(t, h, e, slot); break;
-      default: eval_one<16, true>(t, h, e, slot); break;
+      case 1: eval_one<1, true, kMode, kHet>(t, h, e, slot); break;
+      case 2: eval_one<2, true, kMode, kHet>(t, h, e, slot); break;
+      case 3: eval_one<3, true, kMode, kHet>(t, h, e, slot); break;
+      case 4: eval_one<4, true, kMode, kHet>(t, h, e, slot); break;
+      case 5: eval_one<5, true, kMode, kHet>(t, h, e, slot); break;
+      case 6: eval_one<6, true, kMode, kHet>(t, h, e, slot); break;
+      case 7: eval_one<7, true, kMode, kHet>(t, h, e, slot); break;
+      case 8: eval_one<8, true, kMode, kHet>(t, h, e, slot); break;
+      case 9: eval_one<9, true, kMode, kHet>(t, h, e, slot); break;
+      case 10: eval_one<10, true, kMode, kHet>(t, h, e, slot); break;
+      case 11: eval_one<11, true, kMode, kHet>(t, h, e, slot); break;
+      case 12: eval_one<12, true, kMode, kHet>(t, h, e, slot); break;
+      case 13: eval_one<13, true, kMode, kHet>(t, h, e, slot); break;
+      case 14: eval_one<14, true, kMode, kHet>(t, h, e, slot); break;
+      case 15: eval_one<15, true, kMode, kHet>(t, h, e, slot); break;
+      default: eval_one<16, true, kMode, kHet>(t, h, e, slot); break;
     }
   }
 }
@@ -952,16 +1176,17 @@ __device__ __forceinline__ uint64_t redo_one(const StageRec& R, uint32_t M) {
   return T;
 }
 
+template <bool kHet>
 __global__ void __launch_bounds__(64) k_redo_u64(Tab t, EvalBufs e) {
   const uint32_t n = e.ctr[0];
   for (uint32_t j = blockIdx.x * 64u + threadIdx.x; j < n; j += gridDim.x * 64u) {
     const uint32_t slot = e.ovf[j];
-    const Plan p = unpack(e.packed[slot >> 2], slot & 3);
+    const Plan p = load_plan<kHet>(e.packed, e.pcut, slot);
     const uint32_t S = p.S, M = class_mb(p);
     StageRec R;
     const Hot<2> h(t, nullptr);
     RecSink sink{R};
-    class_setup(t, h, p, slot & 3, sink);
+    class_setup<2, kHet>(t, h, p, slot & 3, sink, kHet ? e.pcut + (slot & ~3u) : nullptr);
     uint64_t r;
     switch (S) {
       case 1: r = redo_one<1>(R, M); break;
@@ -1066,19 +1291,22 @@ hipError_t launch_fill32(uint32_t* p, uint32_t n, uint32_t v, hipStream_t s) {
   k_fill32<<<blocks_for(n, 256) < 1024 ? blocks_for(n, 256) : 1024, 256, 0, s>>>(p, n, v);
   return hipGetLastError();
 }
-hipError_t launch_prep(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, PackedPlan* packed,
+hipError_t launch_prep(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, PackedPlan* packed, uint4* pcut,
                        uint32_t* meta, uint32_t* hist, hipStream_t s) {
-  k_prep<<<blocks_for(n, 256 * kPrepPerThread), 256, 0, s>>>(t, p, n, out, packed, meta, hist);
+  if (p.chdr) k_prep<true><<<blocks_for(n, 256 * kPrepPerThread), 256, 0, s>>>(t, p, n, out, packed, pcut, meta, hist);
+  else k_prep<false><<<blocks_for(n, 256 * kPrepPerThread), 256, 0, s>>>(t, p, n, out, packed, pcut, meta, hist);
   return hipGetLastError();
 }
 hipError_t launch_memory(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, hipStream_t s) {
-  k_memory<<<blocks_for(n, 256), 256, 0, s>>>(t, p, n, out);
+  if (p.chdr) k_memory<true><<<blocks_for(n, 256), 256, 0, s>>>(t, p, n, out);
+  else k_memory<false><<<blocks_for(n, 256), 256, 0, s>>>(t, p, n, out);
   return hipGetLastError();
 }
 
-hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint32_t* meta, int64_t n, uint64_t* out_stage,
-                         hipStream_t s) {
-  k_stages<<<blocks_for(n * 4, 256), 256, 0, s>>>(t, packed, meta, n, out_stage);
+hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint4* pcut, const uint32_t* meta, int64_t n,
+                         uint64_t* out_stage, hipStream_t s) {
+  if (pcut) k_stages<true><<<blocks_for(n * 4, 256), 256, 0, s>>>(t, packed, pcut, meta, n, out_stage);
+  else k_stages<false><<<blocks_for(n * 4, 256), 256, 0, s>>>(t, packed, pcut, meta, n, out_stage);
   return hipGetLastError();
 }
 hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* sstart, hipStream_t s) {
@@ -1089,18 +1317,20 @@ hipError_t launch_scatter(const uint32_t* meta, uint32_t nslots, uint32_t* curso
   k_scatter<<<blocks_for(nslots, 256 * kScatterPer), 256, 0, s>>>(meta, nslots, cursor, ids);
   return hipGetLastError();
 }
-template <int kMode>
+template <int kMode, bool kHet>
 void launch_first_mode(const Tab& t, const EvalBufs& e, uint32_t max_tasks, hipStream_t s) {
   const int nb = blocks_for(max_tasks, kEvalThreads);
   const uint32_t need = nb > 0 ? (uint32_t)nb : 1;
   const size_t lds = kMode < 2 ? t.lds_bytes : 0;
   auto grid = [&](int g) { return 4 * t.grid_eval[g] < need ? 4 * t.grid_eval[g] : need; };
-  k_eval<0, kMode><<<grid(0), kEvalThreads, lds, s>>>(t, e);
-  k_eval<1, kMode><<<grid(1), kEvalThreads, lds, s>>>(t, e);
-  k_eval<2, kMode><<<grid(2), kEvalThreads, lds, s>>>(t, e);
-  k_eval<3, kMode><<<grid(3), kEvalThreads, lds, s>>>(t, e);
+  k_eval<0, kMode, kHet><<<grid(0), kEvalThreads, lds, s>>>(t, e);
+  k_eval<1, kMode, kHet><<<grid(1), kEvalThreads, lds, s>>>(t, e);
+  k_eval<2, kMode, kHet><<<grid(2), kEvalThreads, lds, s>>>(t, e);
+  k_eval<3, kMode, kHet><<<grid(3), kEvalThreads, lds, s>>>(t, e);
 }
 
+// Grid sizes come from the shared-layout kernels; the per-class-layout ones
+// take the same caps (their fixed-stride loops cover any grid).
 template <int kMode>
 static int grids_mode(Tab* t) {
   int cus = 0, dev = 0;
@@ -1108,8 +1338,9 @@ static int grids_mode(Tab* t) {
   if (r == hipSuccess) r = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (r != hipSuccess) return (int)r;
   const size_t lds = kMode < 2 ? t->lds_bytes : 0;
-  const void* k[5] = {(const void*)k_eval<0, kMode>, (const void*)k_eval<1, kMode>, (const void*)k_eval<2, kMode>,
-                      (const void*)k_eval<3, kMode>, (const void*)k_deferred<kMode>};
+  const void* k[5] = {(const void*)k_eval<0, kMode, false>, (const void*)k_eval<1, kMode, false>,
+                      (const void*)k_eval<2, kMode, false>, (const void*)k_eval<3, kMode, false>,
+                      (const void*)k_deferred<kMode, false>};
   uint32_t g[5];
   for (int i = 0; i < 5; ++i) {
     int nb = 0;
@@ -1127,49 +1358,67 @@ int eval_grids(Tab* t) {
 }
 
 static EvalBufs bufs(const EvalArgs& a) {
-  return {a.packed, a.meta, a.ids, a.sstart, a.out, a.ctr, a.ctr + kEvalCounters, a.deferred,
+  return {a.packed, (const uint4*)a.pcut, a.meta, a.ids, a.sstart, a.out, a.ctr, a.ctr + kEvalCounters, a.deferred,
           (unsigned long long*)a.skipped_ops};
 }
 
 // first pass of one stage-count group (g = 0..3) over a chunk
-template <int kMode>
+template <int kMode, bool kHet>
 static void launch_group_mode(const Tab& t, const EvalBufs& e, uint32_t max_tasks, int g, hipStream_t s) {
   const int nb = blocks_for(max_tasks, kEvalThreads);
   const uint32_t need = nb > 0 ? (uint32_t)nb : 1, grid = 4 * t.grid_eval[g] < need ? 4 * t.grid_eval[g] : need;
   const size_t lds = kMode < 2 ? t.lds_bytes : 0;
-  if (g == 0) k_eval<0, kMode><<<grid, kEvalThreads, lds, s>>>(t, e);
-  else if (g == 1) k_eval<1, kMode><<<grid, kEvalThreads, lds, s>>>(t, e);
-  else if (g == 2) k_eval<2, kMode><<<grid, kEvalThreads, lds, s>>>(t, e);
-  else k_eval<3, kMode><<<grid, kEvalThreads, lds, s>>>(t, e);
+  if (g == 0) k_eval<0, kMode, kHet><<<grid, kEvalThreads, lds, s>>>(t, e);
+  else if (g == 1) k_eval<1, kMode, kHet><<<grid, kEvalThreads, lds, s>>>(t, e);
+  else if (g == 2) k_eval<2, kMode, kHet><<<grid, kEvalThreads, lds, s>>>(t, e);
+  else k_eval<3, kMode, kHet><<<grid, kEvalThreads, lds, s>>>(t, e);
+}
+
+template <bool kHet>
+static void launch_group_het(const Tab& t, const EvalBufs& e, uint32_t max_tasks, int g, hipStream_t s) {
+  if (t.mode == 0) launch_group_mode<0, kHet>(t, e, max_tasks, g, s);
+  else if (t.mode == 1) launch_group_mode<1, kHet>(t, e, max_tasks, g, s);
+  else launch_group_mode<2, kHet>(t, e, max_tasks, g, s);
 }
 
 hipError_t launch_group(const Tab& t, const EvalArgs& a, uint32_t max_tasks, int g, hipStream_t s) {
   const EvalBufs e = bufs(a);
-  if (t.mode == 0) launch_group_mode<0>(t, e, max_tasks, g, s);
-  else if (t.mode == 1) launch_group_mode<1>(t, e, max_tasks, g, s);
-  else launch_group_mode<2>(t, e, max_tasks, g, s);
+  if (a.pcut) launch_group_het<true>(t, e, max_tasks, g, s);
+  else launch_group_het<false>(t, e, max_tasks, g, s);
   return hipGetLastError();
 }
 
 // first pass over a chunk: k_eval of each stage-count group
+template <bool kHet>
+static void launch_first_het(const Tab& t, const EvalBufs& e, uint32_t max_tasks, hipStream_t s) {
+  if (t.mode == 0) launch_first_mode<0, kHet>(t, e, max_tasks, s);
+  else if (t.mode == 1) launch_first_mode<1, kHet>(t, e, max_tasks, s);
+  else launch_first_mode<2, kHet>(t, e, max_tasks, s);
+}
+
 hipError_t launch_first(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s) {
   const EvalBufs e = bufs(a);
-  if (t.mode == 0) launch_first_mode<0>(t, e, max_tasks, s);
-  else if (t.mode == 1) launch_first_mode<1>(t, e, max_tasks, s);
-  else launch_first_mode<2>(t, e, max_tasks, s);
+  if (a.pcut) launch_first_het<true>(t, e, max_tasks, s);
+  else launch_first_het<false>(t, e, max_tasks, s);
   return hipGetLastError();
 }
 
 // then the deferred pipelines and the u64 redo of the overflowed ones
-hipError_t launch_deferred(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s) {
-  const EvalBufs e = bufs(a);
+template <bool kHet>
+static void launch_deferred_het(const Tab& t, const EvalBufs& e, uint32_t max_tasks, hipStream_t s) {
   int g = blocks_for(max_tasks, kEvalThreads);
   g = g < 1 ? 1 : (g > (int)t.grid_deferred ? (int)t.grid_deferred : g);
   const size_t lds = t.mode < 2 ? t.lds_bytes : 0;
-  if (t.mode == 0) k_deferred<0><<<g, kEvalThreads, lds, s>>>(t, e);
-  else if (t.mode == 1) k_deferred<1><<<g, kEvalThreads, lds, s>>>(t, e);
-  else k_deferred<2><<<g, kEvalThreads, 0, s>>>(t, e);
-  k_redo_u64<<<32, 64, 0, s>>>(t, e);
+  if (t.mode == 0) k_deferred<0, kHet><<<g, kEvalThreads, lds, s>>>(t, e);
+  else if (t.mode == 1) k_deferred<1, kHet><<<g, kEvalThreads, lds, s>>>(t, e);
+  else k_deferred<2, kHet><<<g, kEvalThreads, 0, s>>>(t, e);
+  k_redo_u64<kHet><<<32, 64, 0, s>>>(t, e);
+}
+
+hipError_t launch_deferred(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s) {
+  const EvalBufs e = bufs(a);
+  if (a.pcut) launch_deferred_het<true>(t, e, max_tasks, s);
+  else launch_deferred_het<false>(t, e, max_tasks, s);
   return hipGetLastError();
 }
 hipError_t launch_argmin(const uint64_t* t, int64_t n, int64_t base, sim_best* b, hipStream_t s) {

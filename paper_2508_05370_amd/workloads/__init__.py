@@ -244,6 +244,24 @@ def random_plans_het(m, c, seed, first, n, nthreads=None):
     return p
 
 
+def as_per_class(p):
+    """The per-class-layout encoding of shared-layout plans: every class gets the plan's TP degree, depth and
+    cuts (header TP and PP fields cleared)."""
+    n = p["hdr"].shape[0]
+    hdr = p["hdr"].astype(np.uint32)
+    tpl = hdr & 3
+    pp1 = (hdr >> 4) & 15
+    G = ((hdr >> 8) & 3) + 1
+    chdr = np.zeros(n, np.uint32)
+    ccut = np.zeros((64, n), np.uint8)
+    for c in range(4):
+        has = G > c
+        chdr |= np.where(has, (tpl | (pp1 << 2)) << (8 * c), 0).astype(np.uint32)
+        ccut[c * 16:(c + 1) * 16] = np.where(has[None, :], p["cut"][:, :n], 0)
+    return dict(hdr=hdr & ~np.uint32(0xF3), cls=np.ascontiguousarray(p["cls"][:, :n]),
+                types=np.ascontiguousarray(p["types"][:, :n]), chdr=chdr, ccut=ccut)
+
+
 def het_plans(w, first=0, n=None, nthreads=None):
     """Per-class-layout plans of workload w (its own seed + 0x100)."""
     if n is None:

@@ -1,0 +1,123 @@
+"""Parity of the per-class layout (each replica class with its own TP degree, pipeline depth
+and layer split, resharding before the gradient sync) between the HIP path, through the C
+ABI, and the oracle.  Integer picoseconds: every comparison is bit-exact."""
+import sys
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+MAXU = np.uint64(2**64 - 1)
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as T
+    if not T.cuda.is_available():
+        pytest.skip("no GPU")
+    return T
+
+
+@pytest.fixture(scope="module")
+def B():
+    from paper_2508_05370_amd import binding
+    return binding
+
+
+def _equal(got, want, what):
+    bad = np.nonzero(got != want)[0]
+    assert bad.size == 0, "%s: %d mismatches, first %s: gpu %d oracle %d" % (
+        what, bad.size, bad[:5], int(got[bad[0]]), int(want[bad[0]]))
+
+
+@pytest.mark.parametrize("idx", [1, 2, 3, 4, 5])
+def test_per_class_plans(torch, B, oracle_mod, workloads, idx):
+    w = workloads.workload(idx)
+    n = 40_000 + 37
+    p = workloads.het_plans(w, 0, n)
+    say("case: per-class layout, workload %d, %d plans" % (idx, n))
+    got = B.times_u64(B.Sim(w["model"], w["cluster"]).eval_plans(B.device_plans(p)))
+    want = oracle_mod.Oracle(w["model"], w["cluster"]).eval(p)
+    _equal(got, want, "per-class workload %d" % idx)
+    assert np.count_nonzero(want != MAXU) > n // 4
+
+
+@pytest.mark.parametrize("idx", [2, 3])
+def test_per_class_encoding_of_shared_plans(torch, B, workloads, idx):
+    w = workloads.workload(idx)
+    n = 20_011
+    p = workloads.plans(w, 0, n)
+    say("case: shared plans in the per-class encoding, workload %d" % idx)
+    sim = B.Sim(w["model"], w["cluster"])
+    a = B.times_u64(sim.eval_plans(B.device_plans(p)))
+    b = B.times_u64(sim.eval_plans(B.device_plans(workloads.as_per_class(p))))
+    _equal(b, a, "per-class encoding")
+
+
+@pytest.mark.parametrize("idx", [2, 3, 4, 5])
+def test_per_class_stage_records(torch, B, oracle_mod, workloads, idx):
+    """Per (class, stage) forward/backward/hop times and the sync each stage waits for."""
+    w = workloads.workload(idx)
+    n = 1500
+    p = workloads.het_plans(w, 0, n)
+    say("case: per-class stage records workload %d" % idx)
+    sim = B.Sim(w["model"], w["cluster"])
+    st, cl = sim.eval_stages(B.device_plans(p))
+    st = st.cpu().numpy().view(np.uint64)
+    cl = cl.cpu().numpy().view(np.uint32)
+    o = oracle_mod.Oracle(w["model"], w["cluster"])
+    for i in range(0, n, 3):
+        d = o.detail(p, i)
+        if d is None:
+            assert np.all(cl[i] == 0)
+            continue
+        G = d["G"]
+        for g in range(4):
+            if g >= G:
+                assert cl[i, g] == 0
+                continue
+            S = d["S_class"][g]
+            assert cl[i, g] == S | (G << 5) | (d["M"][g] << 8), (i, g)
+            for s in range(S):
+                rec = [int(v) for v in st[i, g, s]]
+                want = [d["f"][g][s], d["b"][g][s], d["c"][g][s], d["tdp"][g][s]]
+                assert rec == want, (idx, i, g, s, rec, want)
+
+
+@pytest.mark.parametrize("idx", [3, 4])
+def test_per_class_memory(torch, B, oracle_mod, workloads, idx):
+    w = workloads.with_memory(workloads.workload(idx))
+    n = 20_011
+    p = workloads.het_plans(w, 0, n)
+    say("case: per-class layout with device memory, workload %d" % idx)
+    sim, o = B.Sim(w["model"], w["cluster"]), oracle_mod.Oracle(w["model"], w["cluster"])
+    got = B.times_u64(sim.eval_plans(B.device_plans(p)))
+    want = o.eval(p)
+    _equal(got, want, "per-class with memory, workload %d" % idx)
+    assert 0 < np.count_nonzero(want != MAXU) < n
+    m = 1500
+    mem = sim.eval_memory(B.device_plans({k: np.ascontiguousarray(v[..., :m]) for k, v in p.items()}), m)
+    mem = mem.cpu().numpy().view(np.uint64)
+    for i in range(m):
+        ref = o.stage_mem(p, i)
+        if ref is None:
+            assert np.all(mem[i] == MAXU), i
+        else:
+            assert np.array_equal(mem[i], ref), i
+
+
+def test_per_class_chunks_and_streams(torch, B, oracle_mod, workloads):
+    """More than one 2M-plan chunk: the per-class cut rows follow every chunk's offset."""
+    w = workloads.workload(3)
+    n = (1 << 21) + 40_013
+    p = workloads.het_plans(w, 0, n)
+    say("case: per-class layout, %d plans in two chunks" % n)
+    got = B.times_u64(B.Sim(w["model"], w["cluster"]).eval_plans(B.device_plans(p)))
+    want = oracle_mod.Oracle(w["model"], w["cluster"]).eval(p)
+    _equal(got, want, "per-class multi-chunk")

@@ -13,28 +13,12 @@ import pytest
 MAXU = np.uint64(2**64 - 1)
 
 
-def _het_from_shared(p):
-    """The per-class encoding of shared-layout plans: every class gets the plan's TP, PP and cuts."""
-    n = p["hdr"].shape[0]
-    hdr = p["hdr"].astype(np.uint32)
-    tpl = hdr & 3
-    pp1 = (hdr >> 4) & 15
-    G = ((hdr >> 8) & 3) + 1
-    chdr = np.zeros(n, np.uint32)
-    ccut = np.zeros((64, n), np.uint8)
-    for c in range(4):
-        has = G > c
-        chdr |= np.where(has, (tpl | (pp1 << 2)) << (8 * c), 0).astype(np.uint32)
-        ccut[c * 16:(c + 1) * 16] = np.where(has[None, :], p["cut"], 0)
-    return dict(hdr=hdr & ~np.uint32(0xF3), cls=p["cls"], types=p["types"], chdr=chdr, ccut=ccut)
-
-
 @pytest.mark.parametrize("idx", [1, 2, 3, 4, 5])
 def test_per_class_encoding_of_a_shared_layout(oracle_mod, workloads, idx):
     w = workloads.with_memory(workloads.workload(idx), {1: [2, 1], 2: [24, 40, 16]}.get(idx))
     n = min(5000, w["n_plans"])
     p = workloads.plans(w, 0, n)
-    h = _het_from_shared(p)
+    h = workloads.as_per_class(p)
     o = oracle_mod.Oracle(w["model"], w["cluster"])
     assert np.array_equal(o.eval(p), o.eval(h))
     for i in range(0, n, 97):
@@ -168,3 +152,16 @@ def test_invalid_per_class_plans(oracle_mod, workloads):
     t = o.eval(p)
     assert t[0] != MAXU
     assert all(t[i] == MAXU for i in range(1, 7)), t
+
+
+def test_tp_groups_stay_in_a_node(oracle_mod, workloads):
+    """Blocks of a pool start at a multiple of their class's TP degree (no TP group spans two
+    nodes), so three classes of TP 1, 2 and 1 with one replica each need 5 devices of one
+    4-device node -- one more than their sum -- and do not fit; the first two do."""
+    w = workloads.workload(1)
+    o = oracle_mod.Oracle(w["model"], w["cluster"])
+    p = _plan(2)
+    _set(p, 0, [(1, (12,), 1, 3, 0x0), (2, (12,), 1, 3, 0x0), (1, (12,), 1, 2, 0x0)])
+    _set(p, 1, [(1, (12,), 1, 3, 0x0), (2, (12,), 1, 3, 0x0), (1, (12,), 1, 2, 0x1)])
+    t = o.eval(p)
+    assert t[0] == MAXU and t[1] != MAXU
