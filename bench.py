@@ -94,6 +94,8 @@ def main():
     ap.add_argument("--streams", type=int, default=2)
     ap.add_argument("--mem-steps", type=int, default=5,
                     help="also time the same plans with per-type device memory checked (0 = skip)")
+    ap.add_argument("--layout-steps", type=int, default=5,
+                    help="also time as many per-class-layout plans of the workload (0 = skip)")
     ap.add_argument("--copy-calibrate", type=int, default=0, metavar="BYTES",
                     help="only run a device-to-device copy of BYTES (reference for HBM byte counters)")
     a = ap.parse_args()
@@ -229,6 +231,29 @@ def main():
                "argmin": [mb_i, mb_t]}
         simm.close()
 
+    # Plans with a per-class layout (each replica class its own TP degree, depth and layer split)
+    lay = None
+    if a.layout_steps > 0 and not a.chunk:
+        t0 = time.time()
+        ph = W.het_plans(w, 0, n)
+        log("generated %d per-class-layout plans in %.1f s" % (n, time.time() - t0))
+        dh = B.device_plans(ph)
+        del ph
+        sim.eval_plans(dh, out=out)
+        sim.argmin(out, out=best)
+        torch.cuda.synchronize()
+        h0 = time.perf_counter()
+        for _ in range(a.layout_steps):
+            sim.eval_plans(dh, out=out)
+            sim.argmin(out, out=best)
+        torch.cuda.synchronize()
+        h1 = time.perf_counter()
+        hb_t, hb_i = B.best_tuple(best)
+        lay = {"workload": w["name"] + "/per-class-layout", "plans_per_s": round(n * a.layout_steps / (h1 - h0), 1),
+               "steps": a.layout_steps, "ms_per_step": round((h1 - h0) / a.layout_steps * 1e3, 4),
+               "valid_plans": int(np.count_nonzero(B.times_u64(out) != MAXU)), "argmin": [hb_i, hb_t]}
+        del dh
+
     # CPU baseline: the oracle as it stands, on a bounded prefix of the same plans
     cpu = None
     if a.cpu_seconds > 0:
@@ -258,6 +283,7 @@ def main():
            "roofline": roof, "cpu_baseline": cpu}
     rec.update(extra)
     rec["memory_check"] = mem
+    rec["per_class_layout"] = lay
     print(json.dumps(rec), flush=True)
 
 

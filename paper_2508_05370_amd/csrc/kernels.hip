@@ -209,18 +209,23 @@ __device__ __forceinline__ Checked check_plan(const Tab& t, const sim_plans& pl,
     for (int j = 0; j < 4; ++j) r.cw[c][j] = 0;
     if (c < G) {
       if (kHet) ok = ok && (lay >> 6) == 0;
-      ok = ok && ((t.tp_ok >> tpl) & 1);
-      uint32_t prev = 0;
+      if (kHet || c == 0) {   // the shared layout's cuts are checked once
+        ok = ok && ((t.tp_ok >> tpl) & 1);
+        uint32_t prev = 0;
 #pragma unroll
-      for (uint32_t s = 0; s < 16; ++s) {
-        if (s < S) {
-          const uint32_t v = cb[(kHet ? 16 * c : 0) + s];
-          ok = ok && v > prev;
-          prev = v;
-          r.cw[c][s >> 2] |= v << (8 * (s & 3));
+        for (uint32_t s = 0; s < 16; ++s) {
+          if (s < S) {
+            const uint32_t v = cb[(kHet ? 16 * c : 0) + s];
+            ok = ok && v > prev;
+            prev = v;
+            r.cw[c][s >> 2] |= v << (8 * (s & 3));
+          }
         }
+        ok = ok && prev == t.L;
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) r.cw[c][j] = r.cw[0][j];
       }
-      ok = ok && prev == t.L;
       r.tv[c] &= stage_sel(S);
       const uint32_t reps = r.cls[c] & 0xffff, nmb = r.cls[c] >> 16;
       ok = ok && reps >= 1 && nmb >= reps && (reps & (ep - 1)) == 0;
@@ -280,21 +285,42 @@ __device__ __forceinline__ uint32_t checked_cut(const Checked& r, uint32_t c, ui
   return (uint32_t)(((lo & ~m) | (hi & m)) >> (8 * (s & 7))) & 0xff;
 }
 
-// Peak bytes of the devices of stage s (ns layers) of class c: state plus the
-// activations of the min(PP - s, M) micro-batches 1F1B keeps in flight there.
-__device__ __forceinline__ uint64_t class_stage_bytes(const Tab& t, const Checked& r, uint32_t c, uint32_t s,
+// State bytes of stage s (ns layers) of class c of a checked plan.
+__device__ __forceinline__ uint64_t class_state_bytes(const Tab& t, const Checked& r, uint32_t c, uint32_t s,
                                                       uint32_t ns) {
-  const uint32_t epl = (r.hdr >> 2) & 3, zero = (r.hdr >> 10) & 1, mi = (r.hdr >> 11) & 3;
-  const uint32_t S = r.S[c], tpl = r.tpl[c];
-  const uint32_t reps = r.cls[c] & 0xffff, M = ((r.cls[c] >> 16) + reps - 1) / reps;
-  const uint32_t fly = S - s < M ? S - s : M;
-  return state_bytes(t, tpl, epl, zero, r.psum, s == 0, s == S - 1, ns) + (uint64_t)ns * fly * t.act_layer[tpl][mi];
+  const uint32_t epl = (r.hdr >> 2) & 3, zero = (r.hdr >> 10) & 1;
+  return state_bytes(t, r.tpl[c], epl, zero, r.psum, s == 0, s == r.S[c] - 1, ns);
 }
 
-// Every device of a checked plan fits its type's memory.
+// Peak bytes of the devices of stage s (ns layers) of class c: its state plus
+// the activations of the min(PP - s, M) micro-batches 1F1B keeps in flight there.
+__device__ __forceinline__ uint64_t class_stage_bytes(const Tab& t, const Checked& r, uint32_t c, uint32_t s,
+                                                      uint32_t ns, uint64_t state) {
+  const uint32_t mi = (r.hdr >> 11) & 3, S = r.S[c];
+  const uint32_t reps = r.cls[c] & 0xffff, M = ((r.cls[c] >> 16) + reps - 1) / reps;
+  const uint32_t fly = S - s < M ? S - s : M;
+  return state + (uint64_t)ns * fly * t.act_layer[r.tpl[c]][mi];
+}
+
+// Every device of a checked plan fits its type's memory.  With one layout
+// for all classes a stage's state is the same for every class: computed once.
+template <bool kHet>
 __device__ __forceinline__ bool fits_memory(const Tab& t, const Checked& r) {
   const uint32_t G = ((r.hdr >> 8) & 3) + 1;
   bool ok = true;
+  if (!kHet) {
+    uint32_t prev = 0;
+    for (uint32_t s = 0; s < r.S[0]; ++s) {
+      const uint32_t cut = checked_cut(r, 0, s), ns = cut - prev;
+      prev = cut;
+      const uint64_t state = class_state_bytes(t, r, 0, s, ns);
+#pragma unroll
+      for (uint32_t c = 0; c < 4; ++c)
+        if (c < G)
+          ok = ok && class_stage_bytes(t, r, c, s, ns, state) <= t.mem_cap[(uint32_t)(r.tv[c] >> (4 * s)) & 15];
+    }
+    return ok;
+  }
 #pragma unroll
   for (uint32_t c = 0; c < 4; ++c) {
     if (c >= G) continue;
@@ -302,7 +328,8 @@ __device__ __forceinline__ bool fits_memory(const Tab& t, const Checked& r) {
     for (uint32_t s = 0; s < r.S[c]; ++s) {
       const uint32_t cut = checked_cut(r, c, s), ns = cut - prev;
       prev = cut;
-      ok = ok && class_stage_bytes(t, r, c, s, ns) <= t.mem_cap[(uint32_t)(r.tv[c] >> (4 * s)) & 15];
+      const uint64_t v = class_stage_bytes(t, r, c, s, ns, class_state_bytes(t, r, c, s, ns));
+      ok = ok && v <= t.mem_cap[(uint32_t)(r.tv[c] >> (4 * s)) & 15];
     }
   }
   return ok;
@@ -326,7 +353,7 @@ __global__ void __launch_bounds__(256) k_prep(Tab t, sim_plans pl, int64_t n, ui
     const int64_t i = ((int64_t)blockIdx.x * kPrepPerThread + rep) * blockDim.x + threadIdx.x;
     if (i >= n) break;
     const Checked r = check_plan<kHet>(t, pl, i);
-    const bool ok = r.ok && (!t.mem_check || fits_memory(t, r));
+    const bool ok = r.ok && (!t.mem_check || fits_memory<kHet>(t, r));
     const uint32_t G = ((r.hdr >> 8) & 3) + 1;
     if (out) out[i] = ok ? 0 : kInvalid;
     if (ok) {
@@ -376,7 +403,7 @@ __global__ void __launch_bounds__(256) k_memory(Tab t, sim_plans pl, int64_t n, 
         v = 0;
         if (c < G && s < r.S[c]) {
           const uint32_t cut = checked_cut(r, c, s);
-          v = class_stage_bytes(t, r, c, s, cut - prev);
+          v = class_stage_bytes(t, r, c, s, cut - prev, class_state_bytes(t, r, c, s, cut - prev));
           prev = cut;
         }
       }
