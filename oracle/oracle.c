@@ -378,6 +378,7 @@ static void pipeline(uint64_t S, uint64_t M, const uint64_t* f, const uint64_t* 
  * devices, TP degrees that follow each device group's size; R35). */
 typedef struct {
   uint64_t ep, G, zero, mi;
+  uint64_t overlap;      /* 1: gradient sync overlapped with the last backward pass (R38) */
   uint64_t tp[OR_MAXG], S[OR_MAXG];
   uint64_t cut[OR_MAXG][OR_MAXS];
   uint64_t reps[OR_MAXG], nmb[OR_MAXG];
@@ -419,7 +420,8 @@ static int decode_rules(const or_ctx* x, const or_planes* q, int64_t i, or_plan*
   const or_model* m = &x->m;
   const int64_t stride = q->stride;
   const uint32_t hdr = q->hdr[i];
-  if (hdr >> 13) return 0;                                   /* V7 reserved bits */
+  if (hdr >> 14) return 0;                                   /* V7 reserved bits */
+  p->overlap = (hdr >> 13) & 1;
   p->ep = 1ull << ((hdr >> 2) & 3);
   p->G = ((hdr >> 8) & 3) + 1;
   p->zero = (hdr >> 10) & 1;
@@ -427,6 +429,7 @@ static int decode_rules(const or_ctx* x, const or_planes* q, int64_t i, or_plan*
   if (p->mi >= m->n_mbs) return 0;                           /* V8 */
   if (q->chdr) {
     if (hdr & 0xf3) return 0;                                /* V10 the header's TP and PP are unused (0) */
+    if (p->overlap) return 0;                                /* V11 overlap needs the shared layout */
     uint32_t w = q->chdr[i];
     for (uint64_t g = 0; g < p->G; ++g) {
       uint32_t bt = (w >> (8 * g)) & 0xff;
@@ -665,6 +668,7 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
       ++nb;
     }
   for (uint64_t g = 0; g < G; ++g) for (uint64_t s = 0; s < OR_MAXS; ++s) d->tdp[g][s] = 0;
+  uint64_t seg_alpha[OR_MAXG * OR_MAXS], seg_bq[OR_MAXG * OR_MAXS];
   for (uint64_t j = 0; j + 1 < nb; ++j) {
     uint64_t a = bnd[j], e = bnd[j + 1];
     uint64_t sg[OR_MAXG];
@@ -695,6 +699,8 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
         bq = umax(bq, umax(nic_max(x, k, base[g][sg[g]], p->reps[g] * p->tp[g]), beta_q(cl->pcie[k])));
       }
     }
+    seg_alpha[j] = alpha;
+    seg_bq[j] = bq;
     /* R36: the ring runs on the coarsest TP layout among the classes */
     uint64_t pd, pe;
     span_params(x, a, e, tp_min, ep, &pd, &pe);
@@ -723,7 +729,50 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
   uint64_t T_iter = 0;
   for (uint64_t g = 0; g < G; ++g) {
     pipeline(p->S[g], d->M[g], d->f[g], d->b[g], d->c[g], d->end[g], scratch);
-    for (uint64_t s = 0; s < p->S[g]; ++s) T_iter = umax(T_iter, add(d->end[g][s], d->tdp[g][s]));
+    if (!p->overlap)
+      for (uint64_t s = 0; s < p->S[g]; ++s) T_iter = umax(T_iter, add(d->end[g][s], d->tdp[g][s]));
+  }
+  if (p->overlap) {
+    /* R38-R40 (shared layout: segment s is stage s).  The last backward pass
+     * of stage s (it ends the stage's schedule) first runs the stage's MoE
+     * all-to-all share, then the head (last stage), layers hi-1 .. lo and
+     * the embedding (first stage); each of these is a gradient bucket whose
+     * sync may start once its backward is done and the stage's previous
+     * bucket has synced (one queue per stage and class) */
+    uint64_t S = p->S[0], tp = p->tp[0], tpl = log2u(tp);
+    for (uint64_t g = 0; g < G; ++g)
+      for (uint64_t s = 0; s < S; ++s) {
+        int k = p->type[g][s];
+        uint64_t lo = s ? p->cut[g][s - 1] : 0, hi = p->cut[g][s];
+        uint64_t comp[OR_MAXS * 16 + 2], pd[OR_MAXS * 16 + 2], pe[OR_MAXS * 16 + 2], nbk = 0, bsum = 0;
+        if (s == S - 1) {
+          comp[nbk] = head_time(x, k, tp, b, 1); pd[nbk] = head_params(x, tp); pe[nbk] = 0; ++nbk;
+        }
+        for (uint64_t l = hi; l-- > lo;) {
+          comp[nbk] = LB(x, k, tpl, p->mi, epl)[l];
+          pd[nbk] = layer_params_dense(x, tp);
+          pe[nbk] = layer_params_expert(x, tp, ep);
+          ++nbk;
+        }
+        if (s == 0) {
+          comp[nbk] = embed_time(x, k, b, 1); pd[nbk] = embed_params(x, tp); pe[nbk] = 0; ++nbk;
+        }
+        for (uint64_t j = 0; j < nbk; ++j) bsum = add(bsum, comp[j]);
+        /* the last backward starts at end - b; the all-to-all share b - bsum comes first */
+        uint64_t ready = d->end[g][s] - bsum, c = 0, total = 0;
+        for (uint64_t j = 0; j < nbk; ++j) {
+          ready = add(ready, comp[j]);
+          uint64_t dj = dp_sync(p_all, p->zero, mul(m->grad_bytes, pd[j]), mul(m->param_bytes, pd[j]),
+                                seg_alpha[s], seg_bq[s]);
+          if (m->E && pe[j])
+            dj = add(dj, dp_sync(p_all / ep, p->zero, mul(m->grad_bytes, pe[j]), mul(m->param_bytes, pe[j]),
+                                 seg_alpha[s], seg_bq[s]));
+          c = add(umax(c, ready), dj);
+          total = add(total, dj);
+        }
+        d->tdp[g][s] = total;
+        T_iter = umax(T_iter, c);
+      }
   }
   d->time = T_iter;
 }
