@@ -94,6 +94,8 @@ def main():
     ap.add_argument("--streams", type=int, default=2)
     ap.add_argument("--mem-steps", type=int, default=5,
                     help="also time the same plans with per-type device memory checked (0 = skip)")
+    ap.add_argument("--overlap-steps", type=int, default=5,
+                    help="also time the same plans with the gradient sync overlapped with the last backward (0 = skip)")
     ap.add_argument("--layout-steps", type=int, default=5,
                     help="also time as many per-class-layout plans of the workload (0 = skip)")
     ap.add_argument("--copy-calibrate", type=int, default=0, metavar="BYTES",
@@ -231,6 +233,25 @@ def main():
                "argmin": [mb_i, mb_t]}
         simm.close()
 
+    # The same plans with the gradient sync overlapped with each stage's last backward pass
+    ovl = None
+    if a.overlap_steps > 0 and not a.chunk:
+        dov = dict(dp, hdr=dp["hdr"] | (1 << 13))
+        sim.eval_plans(dov, out=out)
+        sim.argmin(out, out=best)
+        torch.cuda.synchronize()
+        o0 = time.perf_counter()
+        for _ in range(a.overlap_steps):
+            sim.eval_plans(dov, out=out)
+            sim.argmin(out, out=best)
+        torch.cuda.synchronize()
+        o1 = time.perf_counter()
+        ob_t, ob_i = B.best_tuple(best)
+        ovl = {"workload": w["name"] + "/overlap", "plans_per_s": round(n * a.overlap_steps / (o1 - o0), 1),
+               "steps": a.overlap_steps, "ms_per_step": round((o1 - o0) / a.overlap_steps * 1e3, 4),
+               "argmin": [ob_i, ob_t]}
+        del dov
+
     # Plans with a per-class layout (each replica class its own TP degree, depth and layer split)
     lay = None
     if a.layout_steps > 0 and not a.chunk:
@@ -283,6 +304,7 @@ def main():
            "roofline": roof, "cpu_baseline": cpu}
     rec.update(extra)
     rec["memory_check"] = mem
+    rec["dp_overlap"] = ovl
     rec["per_class_layout"] = lay
     print(json.dumps(rec), flush=True)
 

@@ -105,7 +105,13 @@ typedef struct {
  * replica class runs the same TP degree, pipeline depth and layer split):
  *   hdr[i]              bits 0-1 log2 TP, 2-3 log2 EP, 4-7 PP-1, 8-9 classes-1,
  *                       10 ZeRO (reduce-scatter + all-gather instead of
- *                       all-reduce), 11-12 micro-batch size index, 13-31 zero
+ *                       all-reduce), 11-12 micro-batch size index,
+ *                       13 overlap: each stage's gradient sync runs in
+ *                       buckets (head, every layer, embedding) that start as
+ *                       soon as their part of the stage's last backward pass
+ *                       is done, one after another on the stage's ring
+ *                       (Sec. 6 on overlapping communication with
+ *                       computation; shared layout only), 14-31 zero
  *   cut[s*stride+i]     u8, last layer (exclusive) of stage s: 1 <= cut[0] <
  *                       ... < cut[PP-1] = L (the non-uniform layer split)
  *   cls[c*stride+i]     u32, class c: replicas in bits 0-15, micro-batches in

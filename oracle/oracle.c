@@ -387,7 +387,8 @@ typedef struct {
 
 /* per-stage quantities of one plan, exposed for tests; tdp[g][s] is the
  * longest layer-segment sync (resharding included) that waits for stage s
- * of class g */
+ * of class g, or with overlap the part of the stage's bucket syncs left
+ * after its last backward ends */
 typedef struct {
   uint64_t valid, G;
   uint64_t S[OR_MAXG];
@@ -759,7 +760,7 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
         }
         for (uint64_t j = 0; j < nbk; ++j) bsum = add(bsum, comp[j]);
         /* the last backward starts at end - b; the all-to-all share b - bsum comes first */
-        uint64_t ready = d->end[g][s] - bsum, c = 0, total = 0;
+        uint64_t ready = d->end[g][s] - bsum, c = 0;
         for (uint64_t j = 0; j < nbk; ++j) {
           ready = add(ready, comp[j]);
           uint64_t dj = dp_sync(p_all, p->zero, mul(m->grad_bytes, pd[j]), mul(m->param_bytes, pd[j]),
@@ -768,9 +769,8 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
             dj = add(dj, dp_sync(p_all / ep, p->zero, mul(m->grad_bytes, pe[j]), mul(m->param_bytes, pe[j]),
                                  seg_alpha[s], seg_bq[s]));
           c = add(umax(c, ready), dj);
-          total = add(total, dj);
         }
-        d->tdp[g][s] = total;
+        d->tdp[g][s] = c - d->end[g][s];        /* the sync time left after the stage's end */
         T_iter = umax(T_iter, c);
       }
   }

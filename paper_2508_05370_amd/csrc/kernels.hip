@@ -94,6 +94,7 @@ __device__ __forceinline__ uint32_t bucket_key(uint32_t S, uint32_t G, uint32_t 
 // Decoded plan fields used by every pipeline of the plan.
 struct Plan {
   uint32_t tpl, epl, S, G, zero, mi, tp, ep, psum;
+  uint32_t overlap;         // gradient sync overlapped with the last backward pass
   uint64_t cut_lo, cut_hi;  // cut bytes of stages 0-7 and 8-15, eight per word
   uint32_t reps[4], nmb[4];
   uint64_t tv[4];           // stage types, nibbles past S cleared
@@ -132,6 +133,7 @@ __device__ __forceinline__ Plan unpack(const PackedPlan& q, uint32_t c = 0) {
   const uint32_t hdr = q.hdr;
   p.tpl = hdr & 3; p.epl = (hdr >> 2) & 3; p.S = ((hdr >> 4) & 15) + 1; p.G = ((hdr >> 8) & 3) + 1;
   p.zero = (hdr >> 10) & 1; p.mi = (hdr >> 11) & 3; p.tp = 1u << p.tpl; p.ep = 1u << p.epl; p.psum = q.psum;
+  p.overlap = (hdr >> 13) & 1;
   p.chdr = q.pad0;
   const uint64_t* cw = reinterpret_cast<const uint64_t*>(q.cut);
   p.cut_lo = cw[0];
@@ -196,8 +198,9 @@ __device__ __forceinline__ Checked check_plan(const Tab& t, const sim_plans& pl,
   }
   const uint32_t epl = (hdr >> 2) & 3, G = ((hdr >> 8) & 3) + 1, mi = (hdr >> 11) & 3;
   const uint32_t ep = 1u << epl;
-  bool ok = (hdr >> 13) == 0 && mi < t.n_mbs && ((t.ep_ok >> epl) & 1);
-  if (kHet) ok = ok && (hdr & 0xf3) == 0;     // the header's TP and PP fields are unused
+  bool ok = (hdr >> 14) == 0 && mi < t.n_mbs && ((t.ep_ok >> epl) & 1);
+  // the per-class layout leaves the header's TP and PP fields unused (0) and has no overlap
+  if (kHet) ok = ok && (hdr & 0x20f3) == 0;
   uint32_t batch = 0, psum = 0;
 #pragma unroll
   for (uint32_t c = 0; c < 4; ++c) {
@@ -522,10 +525,9 @@ __device__ __forceinline__ uint32_t dev_before_own(const Plan& p, uint32_t s, ui
 // sits in the same node; MoE models add the expert ring over the EP-sized
 // groups.  The same for every class of the plan.
 template <int kMode>
-__device__ __forceinline__ uint64_t stage_dp(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t s,
-                                             uint32_t ns, double rp, double rpe) {
-  if (p.psum <= 1) return 0;
-  const uint32_t G = p.G, tp = p.tp, tpl = p.tpl, epl = p.epl, S = p.S;
+__device__ __forceinline__ void stage_link(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t s,
+                                           uint64_t& alpha, uint32_t& bq) {
+  const uint32_t G = p.G, tp = p.tp;
   bool same = true;
   uint32_t k0 = 0, nmin = 0xffffffffu, nmax = 0, bq_dp = 0;
   uint64_t a_dp = 0;
@@ -546,8 +548,18 @@ __device__ __forceinline__ uint64_t stage_dp(const Tab& t, const Hot<kMode>& h, 
     a_dp = 2 * t2.a_side > a_dp ? 2 * t2.a_side : a_dp;
   }
   const bool intra = same && nmin == nmax;
-  const uint64_t alpha = intra ? h.type(k0).a_intra : a_dp;
-  const uint32_t bq = intra ? h.rmi()[nmin] : bq_dp;
+  alpha = intra ? h.type(k0).a_intra : a_dp;
+  bq = intra ? h.rmi()[nmin] : bq_dp;
+}
+
+template <int kMode>
+__device__ __forceinline__ uint64_t stage_dp(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t s,
+                                             uint32_t ns, double rp, double rpe) {
+  if (p.psum <= 1) return 0;
+  const uint32_t tpl = p.tpl, epl = p.epl, S = p.S;
+  uint64_t alpha;
+  uint32_t bq;
+  stage_link(t, h, p, s, alpha, bq);
   const uint64_t pd = (uint64_t)ns * t.par_layer[tpl] + (s == 0 ? t.par_embed[tpl] : 0) +
                       (s == S - 1 ? t.par_head[tpl] : 0);
   uint64_t tdp = ring_sync(p.psum, rp, p.zero, t.grad_bytes * pd, t.param_bytes * pd, alpha, bq);
@@ -557,6 +569,57 @@ __device__ __forceinline__ uint64_t stage_dp(const Tab& t, const Hot<kMode>& h, 
     tdp += ring_sync(pe, rpe, p.zero, t.grad_bytes * px, t.param_bytes * px, alpha, bq);
   }
   return tdp;
+}
+
+// Gradient sync overlapped with stage s's last backward pass (shared layout;
+// stage s holds layers [lo, hi) on device type k in the pipeline's class).
+// Buckets -- the head on the last stage, the layers from the top, the
+// embedding on the first stage -- each start once their backward is done,
+// one after another on the stage's ring.  Bucket j is ready at
+// r_j = end - R_j (R_j: backward compute of the buckets after it), so the
+// queue completes at end + max_j (D_j - R_j) (D_j: syncs of bucket j and
+// the later ones); that tail is returned, walked from the last bucket.
+template <int kMode>
+__device__ __forceinline__ uint64_t overlap_tail(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t s,
+                                                 uint32_t lo, uint32_t hi, uint32_t k, double rp, double rpe) {
+  if (p.psum <= 1) return 0;
+  const uint32_t tpl = p.tpl, epl = p.epl, mi = p.mi;
+  uint64_t alpha;
+  uint32_t bq;
+  stage_link(t, h, p, s, alpha, bq);
+  const uint64_t gb = t.grad_bytes, pb = t.param_bytes;
+  uint64_t dl = ring_sync(p.psum, rp, p.zero, gb * t.par_layer[tpl], pb * t.par_layer[tpl], alpha, bq);
+  const uint32_t pe = p.psum >> epl;
+  if (t.E && pe > 1)
+    dl += ring_sync(pe, rpe, p.zero, gb * t.par_expert[tpl][epl], pb * t.par_expert[tpl][epl], alpha, bq);
+  const uint32_t L1 = t.L + 1, epq = t.E ? epl : 0;
+  const uint32_t row = ((k * 4 + tpl) * t.n_mbs + mi) * t.nep + epq;
+  int64_t D = 0, R = 0, X = 0;
+  if (s == 0) {
+    D += (int64_t)ring_sync(p.psum, rp, p.zero, gb * t.par_embed[tpl], pb * t.par_embed[tpl], alpha, bq);
+    X = D;
+    R += (int64_t)h.emb(k * t.n_mbs + mi).y;
+  }
+  for (uint32_t l = lo; l < hi; ++l) {
+    D += (int64_t)dl;
+    X = D - R > X ? D - R : X;
+    R += (int64_t)(t.uniform_layers ? h.pfb(row).y : h.pfb(row * L1 + l + 1).y - h.pfb(row * L1 + l).y);
+  }
+  if (s == p.S - 1) {
+    D += (int64_t)ring_sync(p.psum, rp, p.zero, gb * t.par_head[tpl], pb * t.par_head[tpl], alpha, bq);
+    X = D - R > X ? D - R : X;
+  }
+  return (uint64_t)X;
+}
+
+// The sync that follows stage s of the pipeline's class (shared layout):
+// the stage's whole ring, or with overlap the part of its bucket syncs left
+// after its last backward pass.
+template <int kMode>
+__device__ __forceinline__ uint64_t stage_sync(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t s,
+                                               uint32_t lo, uint32_t hi, double rp, double rpe) {
+  if (p.overlap) return overlap_tail(t, h, p, s, lo, hi, (uint32_t)(p.tc >> (4 * s)) & 15, rp, rpe);
+  return stage_dp(t, h, p, s, hi - lo, rp, rpe);
 }
 
 // Per-class layout.  The gradients of layers [a, e) -- a segment between
@@ -755,7 +818,7 @@ __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, c
         load_rows(prow, rows);
         tdp = het_stage_dp(t, h, p, rows, lo, hi, rp, rpe);
       } else {
-        tdp = stage_dp(t, h, p, s, ns, rp, rpe);
+        tdp = stage_sync(t, h, p, s, lo, hi, rp, rpe);
       }
     }
     sink.put(s, fc, bc, hop, tdp);
@@ -817,7 +880,7 @@ __device__ __forceinline__ double dp_tail(const Tab& t, const Hot<kMode>& h, con
   uint32_t lo = 0;
   for (uint32_t s = 0; s < (uint32_t)S; ++s) {
     const uint32_t hi = cut_at(p, s);
-    const uint64_t d = kHet ? het_stage_dp(t, h, p, rows, lo, hi, rp, rpe) : stage_dp(t, h, p, s, hi - lo, rp, rpe);
+    const uint64_t d = kHet ? het_stage_dp(t, h, p, rows, lo, hi, rp, rpe) : stage_sync(t, h, p, s, lo, hi, rp, rpe);
     const double e = last[0] + (double)d;
     T = e > T ? e : T;
 #pragma unroll

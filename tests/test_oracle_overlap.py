@@ -87,7 +87,7 @@ def test_overlap_event_queue_and_extremes(oracle_mod, workloads):
             jobs = _stage_jobs(oracle_mod, o, m, d, [0, 6, 12], s, s, 4, MBps)
             done = _queue(jobs)
             worst = max(worst, done)
-            assert d["tdp"][0][s] == sum(x for _, x in jobs)
+            assert d["tdp"][0][s] == done - d["end"][0][s]
             assert done >= d["end"][0][s] + jobs[-1][1]
             if MBps == 400:                  # communication-bound: back to back from the first bucket
                 assert done == jobs[0][0] + sum(x for _, x in jobs)
