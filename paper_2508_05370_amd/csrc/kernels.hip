@@ -870,7 +870,7 @@ struct RegSink {
 // Iteration time from the end of each stage's last op: the max over stages
 // of that end plus the stage's DP sync, walking the stages with the same
 // shift so that no array is indexed at run time.
-template <int S, int kMode, bool kHet>
+template <int S, int kMode, bool kHet, bool kOvl>
 __device__ __forceinline__ double dp_tail(const Tab& t, const Hot<kMode>& h, const Plan& p, double (&last)[S],
                                           const uint4* prow) {
   const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> p.epl);
@@ -880,7 +880,9 @@ __device__ __forceinline__ double dp_tail(const Tab& t, const Hot<kMode>& h, con
   uint32_t lo = 0;
   for (uint32_t s = 0; s < (uint32_t)S; ++s) {
     const uint32_t hi = cut_at(p, s);
-    const uint64_t d = kHet ? het_stage_dp(t, h, p, rows, lo, hi, rp, rpe) : stage_sync(t, h, p, s, lo, hi, rp, rpe);
+    const uint64_t d = kHet   ? het_stage_dp(t, h, p, rows, lo, hi, rp, rpe)
+                       : kOvl ? overlap_tail(t, h, p, s, lo, hi, (uint32_t)(p.tc >> (4 * s)) & 15, rp, rpe)
+                              : stage_dp(t, h, p, s, hi - lo, rp, rpe);
     const double e = last[0] + (double)d;
     T = e > T ? e : T;
 #pragma unroll
@@ -1020,7 +1022,7 @@ __device__ __forceinline__ void steady_iter(const V (&f)[S], const V (&b)[S], co
 // kJump: take the periodic shortcut; then `skipped` returns the steady
 // iterations it skipped, or -1 if the lane is deferred (result not computed).
 // Returns false for a deferred lane; else last[s] = end of stage s's last op.
-template <int S, typename V, bool kJump>
+template <int S, typename V, bool kJump, bool kFallback = false>
 __device__ __forceinline__ bool pipe(const V (&f)[S], const V (&b)[S], const V (&c)[S], uint32_t M, int& skipped,
                                      V (&last)[S]) {
   V out_f[S];
@@ -1078,7 +1080,10 @@ __device__ __forceinline__ bool pipe(const V (&f)[S], const V (&b)[S], const V (
       steady_iter<S, V>(f, b, c, out_f, last);
       left = 0;
     }
-    if (left > 0) {
+    if (kFallback) {
+      // still aperiodic after the budget: the rest of the steady loop here
+      for (; left > 0; --left) steady_iter<S, V>(f, b, c, out_f, last);
+    } else if (left > 0) {
       skipped = -1;
       return false;
     }
@@ -1134,26 +1139,36 @@ struct EvalBufs {
 // [64b, 64b + 64); blocks past the range return at once.  This first pass
 // takes the periodic shortcut and defers the lanes still aperiodic after the
 // budget; k_deferred runs those through the whole steady loop.
-template <int S, bool kFull, int kMode, bool kHet>
+// kOvl: the pipeline's plan overlaps its gradient sync with the last
+// backward pass.  The first pass (kFull false) sends such pipelines straight
+// to the deferred lists, so that its kernels carry no overlap code; the
+// deferred pass runs them with the shortcut (the whole loop where they stay
+// aperiodic) and the overlapped sync.
+template <int S, bool kFull, int kMode, bool kHet, bool kOvl = false>
 __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot) {
   RegSink<S> r;
   uint32_t M;
   {
     const Plan p = load_plan<kHet>(e.packed, e.pcut, slot);
+    if (!kFull && !kHet && !kOvl && p.overlap) {
+      e.deferred[e.sstart[kMaxStages - S] + atomicAdd(&e.ctr[1 + kMaxStages - S], 1u)] = slot;
+      return;
+    }
     M = class_mb(p);
     class_setup<kMode, kHet>(t, h, p, slot & 3, r, nullptr);
   }
   int skipped;
   double last[S];
-  const bool done = pipe<S, double, !kFull>(r.f, r.b, r.c, M, skipped, last);
+  const bool done = kOvl ? pipe<S, double, true, true>(r.f, r.b, r.c, M, skipped, last)
+                         : pipe<S, double, !kFull>(r.f, r.b, r.c, M, skipped, last);
   // the DP tail reads the plan again (an L2 hit) rather than keeping it in
   // registers through the recurrence; the lane's own slot passed through a
   // shuffle is opaque to the compiler, which would otherwise reuse the
   // first load
   const uint32_t slot2 = __shfl(slot, (int)(threadIdx.x & 63u));
-  const double T = done ? dp_tail<S, kMode, kHet>(t, h, load_plan<kHet>(e.packed, e.pcut, slot2), last,
-                                                   kHet ? e.pcut + (slot2 & ~3u) : nullptr)
-                         : 0;
+  const double T = done ? dp_tail<S, kMode, kHet, kOvl>(t, h, load_plan<kHet>(e.packed, e.pcut, slot2), last,
+                                                         kHet ? e.pcut + (slot2 & ~3u) : nullptr)
+                        : 0;
   if (!done) {
     e.deferred[e.sstart[kMaxStages - S] + atomicAdd(&e.ctr[1 + kMaxStages - S], 1u)] = slot;
     return;
@@ -1166,6 +1181,14 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
   if (e.skipped_ops && skipped > 0)
     atomicAdd(e.skipped_ops + ((blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) % kSkipSlots) * kSkipStride,
               (unsigned long long)skipped * (unsigned long long)(6 * (S - 1) + 2));
+}
+
+// Deferred pass of one pipeline: the whole loop, or for a plan with
+// overlapped gradient sync the shortcut first (shared layout only).
+template <int S, int kMode, bool kHet>
+__device__ __forceinline__ void eval_deferred(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot) {
+  if (!kHet && ((e.packed[slot >> 2].hdr >> 13) & 1)) eval_one<S, false, kMode, kHet, true>(t, h, e, slot);
+  else eval_one<S, true, kMode, kHet>(t, h, e, slot);
 }
 
 // Blocks of four waves share one LDS copy of the table image.
@@ -1228,22 +1251,22 @@ __global__ void __launch_bounds__(kEvalThreads) k_deferred(Tab t, EvalBufs e) {
     if (off >= e.ctr[1 + j]) continue;
     const uint32_t slot = e.deferred[e.sstart[j] + off];
     switch (kMaxStages - j) {
-      case 1: eval_one<1, true, kMode, kHet>(t, h, e, slot); break;
-      case 2: eval_one<2, true, kMode, kHet>(t, h, e, slot); break;
-      case 3: eval_one<3, true, kMode, kHet>(t, h, e, slot); break;
-      case 4: eval_one<4, true, kMode, kHet>(t, h, e, slot); break;
-      case 5: eval_one<5, true, kMode, kHet>(t, h, e, slot); break;
-      case 6: eval_one<6, true, kMode, kHet>(t, h, e, slot); break;
-      case 7: eval_one<7, true, kMode, kHet>(t, h, e, slot); break;
-      case 8: eval_one<8, true, kMode, kHet>(t, h, e, slot); break;
-      case 9: eval_one<9, true, kMode, kHet>(t, h, e, slot); break;
-      case 10: eval_one<10, true, kMode, kHet>(t, h, e, slot); break;
-      case 11: eval_one<11, true, kMode, kHet>(t, h, e, slot); break;
-      case 12: eval_one<12, true, kMode, kHet>(t, h, e, slot); break;
-      case 13: eval_one<13, true, kMode, kHet>(t, h, e, slot); break;
-      case 14: eval_one<14, true, kMode, kHet>(t, h, e, slot); break;
-      case 15: eval_one<15, true, kMode, kHet>(t, h, e, slot); break;
-      default: eval_one<16, true, kMode, kHet>(t, h, e, slot); break;
+      case 1: eval_deferred<1, kMode, kHet>(t, h, e, slot); break;
+      case 2: eval_deferred<2, kMode, kHet>(t, h, e, slot); break;
+      case 3: eval_deferred<3, kMode, kHet>(t, h, e, slot); break;
+      case 4: eval_deferred<4, kMode, kHet>(t, h, e, slot); break;
+      case 5: eval_deferred<5, kMode, kHet>(t, h, e, slot); break;
+      case 6: eval_deferred<6, kMode, kHet>(t, h, e, slot); break;
+      case 7: eval_deferred<7, kMode, kHet>(t, h, e, slot); break;
+      case 8: eval_deferred<8, kMode, kHet>(t, h, e, slot); break;
+      case 9: eval_deferred<9, kMode, kHet>(t, h, e, slot); break;
+      case 10: eval_deferred<10, kMode, kHet>(t, h, e, slot); break;
+      case 11: eval_deferred<11, kMode, kHet>(t, h, e, slot); break;
+      case 12: eval_deferred<12, kMode, kHet>(t, h, e, slot); break;
+      case 13: eval_deferred<13, kMode, kHet>(t, h, e, slot); break;
+      case 14: eval_deferred<14, kMode, kHet>(t, h, e, slot); break;
+      case 15: eval_deferred<15, kMode, kHet>(t, h, e, slot); break;
+      default: eval_deferred<16, kMode, kHet>(t, h, e, slot); break;
     }
   }
 }
