@@ -727,6 +727,126 @@ __device__ __forceinline__ void load_rows(const uint4* prow, uint4 (&rows)[4]) {
   for (int c = 0; c < 4; ++c) rows[c] = prow[c];
 }
 
+// cut byte of stage s (run-time index) of class c of the plan's cut rows
+__device__ __forceinline__ uint32_t row_cut(const uint4 (&rows)[4], uint32_t c, uint32_t s) {
+  const uint4 r = rows[c];
+  const uint64_t lo = (uint64_t)r.y << 32 | r.x, hi = (uint64_t)r.w << 32 | r.z;
+  const uint64_t m = 0ull - (uint64_t)(s >> 3);
+  return (uint32_t)(((lo & ~m) | (hi & m)) >> (8 * (s & 7))) & 0xff;
+}
+
+// Per-class layout, DP tail of one pipeline: the same syncs as
+// het_stage_dp, found by one walk over the segments of the whole model (the
+// pipeline's own stages cover every layer).  Each class's stage holding the
+// current segment, with its placement and links, is recomputed only when
+// the walk crosses one of that class's cuts.  Returns the max over the own
+// stages s of last[s] plus the longest sync of the segments inside stage s.
+template <int S, int kMode>
+__device__ __forceinline__ double het_dp_tail(const Tab& t, const Hot<kMode>& h, const Plan& p, double (&last)[S],
+                                              const uint4* prow) {
+  uint4 rows[4];
+  load_rows(prow, rows);
+  const uint32_t G = p.G, epl = p.epl;
+  const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> epl);
+  uint32_t tmin = 3;
+#pragma unroll
+  for (uint32_t c2 = 0; c2 < 4; ++c2)
+    if (c2 < G) tmin = cls_tpl(p.chdr, c2) < tmin ? cls_tpl(p.chdr, c2) : tmin;
+  // per class: current stage and its end, and that stage's type, node range,
+  // worst NIC/PCIe rate, inter-node latency, node latency and worst node fabric
+  uint32_t stg[4], nxt[4], kk[4], nl[4], nh[4], bx[4], bin[4];
+  uint64_t as2[4], ain[4];
+#pragma unroll
+  for (uint32_t c2 = 0; c2 < 4; ++c2) {
+    stg[c2] = 0; nxt[c2] = 0xffffffffu; kk[c2] = 0; nl[c2] = 0; nh[c2] = 0; bx[c2] = 0; bin[c2] = 0;
+    as2[c2] = 0; ain[c2] = 0;
+  }
+  auto enter = [&](uint32_t c2) {
+    const uint32_t s2 = stg[c2], tpl2 = cls_tpl(p.chdr, c2);
+    const uint32_t k2 = (uint32_t)(p.tv[c2] >> (4 * s2)) & 15;
+    const TypeInfo t2 = h.type(k2);
+    const uint32_t b2 = dev_before<true>(p, c2, s2, k2), n2 = p.reps[c2] << tpl2, d2 = t2.dpl;
+    const uint32_t l2 = t2.node_off + (b2 >> d2), h2 = t2.node_off + ((b2 + n2 - 1) >> d2);
+    const uint32_t dl2 = t2.dev_off + b2;
+    const uint32_t nic2 = range_max(h.rmn, t.D, dl2, dl2 + n2 - 1);
+    nxt[c2] = row_cut(rows, c2, s2);
+    kk[c2] = k2;
+    nl[c2] = l2;
+    nh[c2] = h2;
+    bx[c2] = nic2 > t2.bq_pcie ? nic2 : t2.bq_pcie;
+    as2[c2] = 2 * t2.a_side;
+    ain[c2] = t2.a_intra;
+    bin[c2] = tpl2 > tmin ? range_max(h.rmi(), t.N, l2, h2) : 0;
+  };
+#pragma unroll
+  for (uint32_t c2 = 0; c2 < 4; ++c2)
+    if (c2 < G) enter(c2);
+  double T = 0;
+  uint64_t best = 0;
+  uint32_t own_hi = cut_at(p, 0), so = 0;
+  for (uint32_t a = 0; a < t.L;) {
+    uint32_t e = t.L;
+#pragma unroll
+    for (uint32_t c2 = 0; c2 < 4; ++c2)
+      if (c2 < G) e = nxt[c2] < e ? nxt[c2] : e;
+    // the sync of layers [a, e)
+    const uint32_t ns = e - a;
+    bool same = true;
+    uint32_t nmin = 0xffffffffu, nmax = 0, bq_dp = 0;
+    uint64_t a_dp = 0, rs = 0;
+#pragma unroll
+    for (uint32_t c2 = 0; c2 < 4; ++c2) {
+      if (c2 >= G) continue;
+      same = same && kk[c2] == kk[0];
+      nmin = nl[c2] < nmin ? nl[c2] : nmin;
+      nmax = nh[c2] > nmax ? nh[c2] : nmax;
+      bq_dp = bx[c2] > bq_dp ? bx[c2] : bq_dp;
+      a_dp = as2[c2] > a_dp ? as2[c2] : a_dp;
+      const uint32_t tpl2 = cls_tpl(p.chdr, c2);
+      if (tpl2 > tmin) {
+        const uint64_t g1 = (1u << (tpl2 - tmin)) - 1;
+        const uint64_t sh = (uint64_t)ns * (t.par_layer[tpl2] + t.par_expert[tpl2][epl]) +
+                            (a == 0 ? t.par_embed[tpl2] : 0) + (e == t.L ? t.par_head[tpl2] : 0);
+        const uint64_t r = g1 * ain[c2] + link_ps(g1 * t.grad_bytes * sh, bin[c2]);
+        rs = r > rs ? r : rs;
+      }
+    }
+    const bool intra = same && nmin == nmax;
+    const uint64_t alpha = intra ? ain[0] : a_dp;
+    const uint32_t bq = intra ? h.rmi()[nmin] : bq_dp;
+    const uint64_t pd = (uint64_t)ns * t.par_layer[tmin] + (a == 0 ? t.par_embed[tmin] : 0) +
+                        (e == t.L ? t.par_head[tmin] : 0);
+    uint64_t x = p.psum <= 1 ? 0 : ring_sync(p.psum, rp, p.zero, t.grad_bytes * pd, t.param_bytes * pd, alpha, bq);
+    const uint32_t pe = p.psum >> epl;
+    if (t.E && pe > 1) {
+      const uint64_t px = (uint64_t)ns * t.par_expert[tmin][epl];
+      x += ring_sync(pe, rpe, p.zero, t.grad_bytes * px, t.param_bytes * px, alpha, bq);
+    }
+    x += rs;
+    best = x > best ? x : best;
+    if (e == own_hi) {   // the pipeline's own stage so ends here
+      const double v = last[0] + (double)best;
+      T = v > T ? v : T;
+#pragma unroll
+      for (int i = 0; i + 1 < S; ++i) last[i] = last[i + 1];
+      best = 0;
+      ++so;
+      own_hi = so < (uint32_t)S ? cut_at(p, so) : t.L + 1;
+    }
+    if (e < t.L) {
+#pragma unroll
+      for (uint32_t c2 = 0; c2 < 4; ++c2) {
+        if (c2 < G && nxt[c2] == e) {
+          ++stg[c2];
+          enter(c2);
+        }
+      }
+    }
+    a = e;
+  }
+  return T;
+}
+
 template <int kMode, bool kHet, typename Sink>
 __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t c,
                                             Sink& sink, const uint4* prow) {
@@ -873,16 +993,14 @@ struct RegSink {
 template <int S, int kMode, bool kHet, bool kOvl>
 __device__ __forceinline__ double dp_tail(const Tab& t, const Hot<kMode>& h, const Plan& p, double (&last)[S],
                                           const uint4* prow) {
+  if constexpr (kHet) return het_dp_tail<S, kMode>(t, h, p, last, prow);
   const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> p.epl);
-  uint4 rows[4];
-  if (kHet) load_rows(prow, rows);
   double T = 0;
   uint32_t lo = 0;
   for (uint32_t s = 0; s < (uint32_t)S; ++s) {
     const uint32_t hi = cut_at(p, s);
-    const uint64_t d = kHet   ? het_stage_dp(t, h, p, rows, lo, hi, rp, rpe)
-                       : kOvl ? overlap_tail(t, h, p, s, lo, hi, (uint32_t)(p.tc >> (4 * s)) & 15, rp, rpe)
-                              : stage_dp(t, h, p, s, hi - lo, rp, rpe);
+    const uint64_t d = kOvl ? overlap_tail(t, h, p, s, lo, hi, (uint32_t)(p.tc >> (4 * s)) & 15, rp, rpe)
+                            : stage_dp(t, h, p, s, hi - lo, rp, rpe);
     const double e = last[0] + (double)d;
     T = e > T ? e : T;
 #pragma unroll

@@ -46,7 +46,7 @@ def _create(B, m, c):
 
 @pytest.mark.parametrize("field,value", [
     ("L", 0), ("L", 256), ("heads", 7), ("kv_heads", 5), ("seq", 0), ("dtype_bytes", 0), ("mbs", []),
-    ("mbs", [1, 2, 3, 4, 5]), ("mbs", [0]), ("gated", 2), ("ffn", 0)])
+    ("mbs", [1, 2, 3, 4, 5]), ("mbs", [0]), ("gated", 2), ("ffn", 0), ("opt_bytes", 65)])
 def test_create_rejects_bad_model(B, workloads, field, value):
     w = workloads.workload(1)
     m = dict(w["model"])
@@ -67,6 +67,14 @@ def test_create_rejects_bad_cluster(B, workloads, field, value):
     c = {**w["cluster"], "types": [dict(t) for t in w["cluster"]["types"]]}
     c["types"][1][field] = value
     rc, h = _create(B, w["model"], c)
+    assert rc == B.SIM_EINVAL and not h.value
+
+
+def test_create_rejects_zero_device_memory(B, workloads):
+    """Device memory is optional for the whole cluster, but a given capacity must be >= 1 byte."""
+    w = workloads.with_memory(workloads.workload(1), [40, 80])
+    w["cluster"]["types"][1]["mem_bytes"] = 0
+    rc, h = _create(B, w["model"], w["cluster"])
     assert rc == B.SIM_EINVAL and not h.value
 
 
@@ -97,6 +105,8 @@ def test_null_arguments(B):
     L = B.lib()
     assert L.sim_create(None, None, None) == B.SIM_EINVAL
     assert L.sim_eval_plans(None, None, 0, None, None) == B.SIM_EINVAL
+    assert L.sim_eval_stages(None, None, 0, None, None, None) == B.SIM_EINVAL
+    assert L.sim_eval_memory(None, None, 0, None, None) == B.SIM_EINVAL
     assert L.sim_argmin(None, None, 0, 0, None, None) == B.SIM_EINVAL
     assert L.sim_best_reduce(None, None, 0, None, None) == B.SIM_EINVAL
     assert L.sim_set_timing(None, 1) == B.SIM_EINVAL

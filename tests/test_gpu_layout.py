@@ -121,3 +121,17 @@ def test_per_class_chunks_and_streams(torch, B, oracle_mod, workloads):
     got = B.times_u64(B.Sim(w["model"], w["cluster"]).eval_plans(B.device_plans(p)))
     want = oracle_mod.Oracle(w["model"], w["cluster"]).eval(p)
     _equal(got, want, "per-class multi-chunk")
+
+
+def test_per_class_layout_needs_its_cut_planes(torch, B, workloads):
+    """A per-class header without the per-class cut planes is an argument error."""
+    import ctypes as C
+    w = workloads.workload(3)
+    p = workloads.het_plans(w, 0, 64)
+    sim = B.Sim(w["model"], w["cluster"])
+    dp = B.device_plans(p)
+    ps = B.plans_struct(dp)
+    ps.ccut = None
+    out = torch.empty(64, dtype=torch.int64, device="cuda")
+    rc = B.lib().sim_eval_plans(sim.h, C.byref(ps), 64, out.data_ptr(), B._stream(None))
+    assert rc == B.SIM_EINVAL
