@@ -15,6 +15,8 @@ hipError_t launch_fill32(uint32_t* p, uint32_t n, uint32_t v, hipStream_t s);
 hipError_t launch_prep(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, PackedPlan* packed, uint4* pcut,
                        uint32_t* meta, uint32_t* hist, hipStream_t s);
 hipError_t launch_memory(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, hipStream_t s);
+hipError_t launch_plan_syncs(const Tab& t, const PackedPlan* packed, const uint4* pcut, const uint32_t* meta,
+                             int64_t n, uint64_t* hdp, hipStream_t s);
 hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint4* pcut, const uint32_t* meta, int64_t n,
                          uint64_t* out_stage, hipStream_t s);
 hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* sstart, hipStream_t s);
@@ -139,23 +141,29 @@ static void end_event(sim_ctx* c, int kind, hipStream_t s, EventPair* e) {
 // the deferred lists, bucket counts followed by the evaluation counters and
 // the overflow list (counts and counters cleared together), bucket cursors,
 // the start of each stage count's pipelines, and with the per-class layout
-// the plans' class cut rows (64 bytes per plan).
+// the plans' class cut rows (64 bytes per plan) and the syncs each pipeline's
+// stages wait for (16 u64 per pipeline slot, 512 bytes per plan).
 constexpr uint32_t kCounters = kBuckets + kEvalCounters;
 struct Work {
   PackedPlan* packed;
   uint4* pcut;
+  uint64_t* hdp;
   uint32_t *meta, *ids, *deferred, *hist, *ctr, *cursor, *sstart;
 };
 static size_t cut_rows_bytes(int64_t ch, bool het) { return het ? align256((size_t)ch * 64) : 0; }
+static size_t het_sync_bytes(int64_t ch, bool het) {
+  return het ? align256((size_t)ch * kMaxClasses * kMaxStages * 8) : 0;
+}
 static size_t work_bytes(int64_t ch, bool het) {
   return align256((size_t)ch * sizeof(PackedPlan)) + 3 * align256((size_t)ch * 4 * 4) +
          align256(kCounters * 4 + (size_t)ch * 4 * 4) + align256(kBuckets * 4) + align256((kMaxStages + 1) * 4) +
-         cut_rows_bytes(ch, het);
+         cut_rows_bytes(ch, het) + het_sync_bytes(ch, het);
 }
 static Work carve(void* base, int64_t ch, bool het) {
   Work w;
   char* p = (char*)base;
   w.pcut = het ? (uint4*)p : nullptr; p += cut_rows_bytes(ch, het);
+  w.hdp = het ? (uint64_t*)p : nullptr; p += het_sync_bytes(ch, het);
   w.packed = (PackedPlan*)p; p += align256((size_t)ch * sizeof(PackedPlan));
   w.meta = (uint32_t*)p; p += align256((size_t)ch * 16);
   w.ids = (uint32_t*)p; p += align256((size_t)ch * 16);
@@ -228,9 +236,10 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
     bool t1 = e == hipSuccess && begin_event(c, 1, s, &ev);
     if (e == hipSuccess) e = launch_prep(c->tab, p, cn, out + off, W.packed, W.pcut, W.meta, W.hist, s);
     if (t1) end_event(c, 1, s, &ev);
+    if (e == hipSuccess && het) e = launch_plan_syncs(c->tab, W.packed, W.pcut, W.meta, cn, W.hdp, s);
     if (e == hipSuccess) e = launch_scan(W.hist, W.cursor, W.sstart, s);
     if (e == hipSuccess) e = launch_scatter(W.meta, (uint32_t)(cn * 4), W.cursor, W.ids, s);
-    const EvalArgs a = {W.packed, W.pcut, W.meta, W.ids, W.sstart, out + off, W.ctr, W.deferred,
+    const EvalArgs a = {W.packed, W.pcut, W.hdp, W.meta, W.ids, W.sstart, out + off, W.ctr, W.deferred,
                         c->timing ? c->skipped_ops : nullptr};
     EventPair e0;
     bool t0 = e == hipSuccess && begin_event(c, 0, s, &e0);

@@ -97,6 +97,7 @@ constexpr uint32_t kSkipSlots = 512, kSkipStride = 16;
 struct EvalArgs {
   const PackedPlan* packed;
   const void* pcut;            // per-class layout: four 16-byte cut rows per plan; nullptr for the shared layout
+  const uint64_t* hdp;         // per-class layout: per pipeline slot, the syncs its 16 stages wait for
   const uint32_t* meta;
   const uint32_t* ids;
   const uint32_t* sstart;

@@ -735,17 +735,15 @@ __device__ __forceinline__ uint32_t row_cut(const uint4 (&rows)[4], uint32_t c, 
   return (uint32_t)(((lo & ~m) | (hi & m)) >> (8 * (s & 7))) & 0xff;
 }
 
-// Per-class layout, DP tail of one pipeline: the same syncs as
-// het_stage_dp, found by one walk over the segments of the whole model (the
-// pipeline's own stages cover every layer).  Each class's stage holding the
-// current segment, with its placement and links, is recomputed only when
-// the walk crosses one of that class's cuts.  Returns the max over the own
-// stages s of last[s] plus the longest sync of the segments inside stage s.
-template <int S, int kMode>
-__device__ __forceinline__ double het_dp_tail(const Tab& t, const Hot<kMode>& h, const Plan& p, double (&last)[S],
-                                              const uint4* prow) {
-  uint4 rows[4];
-  load_rows(prow, rows);
+// Per-class layout: the sync each (class, stage) of a valid plan waits for
+// -- the same values as het_stage_dp -- found by one walk over the segments
+// of the whole model.  Each class's stage holding the current segment, with
+// its placement and links, is recomputed only when the walk crosses one of
+// that class's cuts; a class's running max is stored when it leaves a stage.
+// drow: the plan's four rows of 16 entries (class c, stage s at c*16 + s).
+template <int kMode>
+__device__ __forceinline__ void het_plan_syncs(const Tab& t, const Hot<kMode>& h, const Plan& p,
+                                               const uint4 (&rows)[4], uint64_t* __restrict__ drow) {
   const uint32_t G = p.G, epl = p.epl;
   const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> epl);
   uint32_t tmin = 3;
@@ -753,38 +751,38 @@ __device__ __forceinline__ double het_dp_tail(const Tab& t, const Hot<kMode>& h,
   for (uint32_t c2 = 0; c2 < 4; ++c2)
     if (c2 < G) tmin = cls_tpl(p.chdr, c2) < tmin ? cls_tpl(p.chdr, c2) : tmin;
   // per class: current stage and its end, and that stage's type, node range,
-  // worst NIC/PCIe rate, inter-node latency, node latency and worst node fabric
+  // worst NIC/PCIe rate, inter-node latency, node latency, worst node fabric;
+  // classes enter their first stage at the walk's first step
   uint32_t stg[4], nxt[4], kk[4], nl[4], nh[4], bx[4], bin[4];
-  uint64_t as2[4], ain[4];
+  uint64_t as2[4], ain[4], cur[4];
 #pragma unroll
   for (uint32_t c2 = 0; c2 < 4; ++c2) {
-    stg[c2] = 0; nxt[c2] = 0xffffffffu; kk[c2] = 0; nl[c2] = 0; nh[c2] = 0; bx[c2] = 0; bin[c2] = 0;
-    as2[c2] = 0; ain[c2] = 0;
+    stg[c2] = 0xffffffffu; nxt[c2] = c2 < G ? 0 : 0xffffffffu; kk[c2] = 0; nl[c2] = 0; nh[c2] = 0; bx[c2] = 0;
+    bin[c2] = 0; as2[c2] = 0; ain[c2] = 0; cur[c2] = 0;
   }
-  auto enter = [&](uint32_t c2) {
-    const uint32_t s2 = stg[c2], tpl2 = cls_tpl(p.chdr, c2);
-    const uint32_t k2 = (uint32_t)(p.tv[c2] >> (4 * s2)) & 15;
-    const TypeInfo t2 = h.type(k2);
-    const uint32_t b2 = dev_before<true>(p, c2, s2, k2), n2 = p.reps[c2] << tpl2, d2 = t2.dpl;
-    const uint32_t l2 = t2.node_off + (b2 >> d2), h2 = t2.node_off + ((b2 + n2 - 1) >> d2);
-    const uint32_t dl2 = t2.dev_off + b2;
-    const uint32_t nic2 = range_max(h.rmn, t.D, dl2, dl2 + n2 - 1);
-    nxt[c2] = row_cut(rows, c2, s2);
-    kk[c2] = k2;
-    nl[c2] = l2;
-    nh[c2] = h2;
-    bx[c2] = nic2 > t2.bq_pcie ? nic2 : t2.bq_pcie;
-    as2[c2] = 2 * t2.a_side;
-    ain[c2] = t2.a_intra;
-    bin[c2] = tpl2 > tmin ? range_max(h.rmi(), t.N, l2, h2) : 0;
-  };
-#pragma unroll
-  for (uint32_t c2 = 0; c2 < 4; ++c2)
-    if (c2 < G) enter(c2);
-  double T = 0;
-  uint64_t best = 0;
-  uint32_t own_hi = cut_at(p, 0), so = 0;
   for (uint32_t a = 0; a < t.L;) {
+#pragma unroll
+    for (uint32_t c2 = 0; c2 < 4; ++c2) {
+      if (nxt[c2] == a) {   // the walk crossed one of class c2's cuts (or starts)
+        if (a > 0) drow[c2 * kMaxStages + stg[c2]] = cur[c2];
+        cur[c2] = 0;
+        const uint32_t s2 = ++stg[c2], tpl2 = cls_tpl(p.chdr, c2);
+        const uint32_t k2 = (uint32_t)(p.tv[c2] >> (4 * s2)) & 15;
+        const TypeInfo t2 = h.type(k2);
+        const uint32_t b2 = dev_before<true>(p, c2, s2, k2), n2 = p.reps[c2] << tpl2, d2 = t2.dpl;
+        const uint32_t l2 = t2.node_off + (b2 >> d2), h2 = t2.node_off + ((b2 + n2 - 1) >> d2);
+        const uint32_t dl2 = t2.dev_off + b2;
+        const uint32_t nic2 = range_max(h.rmn, t.D, dl2, dl2 + n2 - 1);
+        nxt[c2] = row_cut(rows, c2, s2);
+        kk[c2] = k2;
+        nl[c2] = l2;
+        nh[c2] = h2;
+        bx[c2] = nic2 > t2.bq_pcie ? nic2 : t2.bq_pcie;
+        as2[c2] = 2 * t2.a_side;
+        ain[c2] = t2.a_intra;
+        bin[c2] = tpl2 > tmin ? range_max(h.rmi(), t.N, l2, h2) : 0;
+      }
+    }
     uint32_t e = t.L;
 #pragma unroll
     for (uint32_t c2 = 0; c2 < 4; ++c2)
@@ -823,28 +821,14 @@ __device__ __forceinline__ double het_dp_tail(const Tab& t, const Hot<kMode>& h,
       x += ring_sync(pe, rpe, p.zero, t.grad_bytes * px, t.param_bytes * px, alpha, bq);
     }
     x += rs;
-    best = x > best ? x : best;
-    if (e == own_hi) {   // the pipeline's own stage so ends here
-      const double v = last[0] + (double)best;
-      T = v > T ? v : T;
 #pragma unroll
-      for (int i = 0; i + 1 < S; ++i) last[i] = last[i + 1];
-      best = 0;
-      ++so;
-      own_hi = so < (uint32_t)S ? cut_at(p, so) : t.L + 1;
-    }
-    if (e < t.L) {
-#pragma unroll
-      for (uint32_t c2 = 0; c2 < 4; ++c2) {
-        if (c2 < G && nxt[c2] == e) {
-          ++stg[c2];
-          enter(c2);
-        }
-      }
-    }
+    for (uint32_t c2 = 0; c2 < 4; ++c2)
+      if (c2 < G) cur[c2] = x > cur[c2] ? x : cur[c2];
     a = e;
   }
-  return T;
+#pragma unroll
+  for (uint32_t c2 = 0; c2 < 4; ++c2)
+    if (c2 < G) drow[c2 * kMaxStages + stg[c2]] = cur[c2];
 }
 
 template <int kMode, bool kHet, typename Sink>
@@ -992,8 +976,17 @@ struct RegSink {
 // shift so that no array is indexed at run time.
 template <int S, int kMode, bool kHet, bool kOvl>
 __device__ __forceinline__ double dp_tail(const Tab& t, const Hot<kMode>& h, const Plan& p, double (&last)[S],
-                                          const uint4* prow) {
-  if constexpr (kHet) return het_dp_tail<S, kMode>(t, h, p, last, prow);
+                                          const uint64_t* drow) {
+  if constexpr (kHet) {
+    // per-class layout: the syncs the plan pass stored for this pipeline's stages
+    double T = 0;
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+      const double e = last[s] + (double)drow[s];
+      T = e > T ? e : T;
+    }
+    return T;
+  }
   const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> p.epl);
   double T = 0;
   uint32_t lo = 0;
@@ -1026,6 +1019,23 @@ __global__ void __launch_bounds__(256) k_stages(Tab t, const PackedPlan* __restr
   for (uint32_t s = 0; s < p.S; ++s)
 #pragma unroll
     for (int q = 0; q < kRecWords; ++q) o[s * kRecWords + q] = rec[s][q];
+}
+
+// Per-class layout: the syncs of every (class, stage) of every valid plan
+// (one plan per lane), once per plan rather than once per pipeline.
+template <int kMode>
+__global__ void __launch_bounds__(256) k_plan_syncs(Tab t, const PackedPlan* __restrict__ packed,
+                                                    const uint4* __restrict__ pcut, const uint32_t* __restrict__ meta,
+                                                    int64_t n, uint64_t* __restrict__ hdp) {
+  extern __shared__ uint4 lds[];
+  fill_lds<kMode>(t, lds);
+  const Hot<kMode> h(t, lds);
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n || meta[4 * i] == 0) return;
+  const Plan p = unpack(packed[i], 0);
+  uint4 rows[4];
+  load_rows(pcut + 4 * i, rows);
+  het_plan_syncs(t, h, p, rows, hdp + (size_t)i * (kMaxClasses * kMaxStages));
 }
 
 // ---------------------------------------------------------------- bucketing
@@ -1240,6 +1250,7 @@ constexpr double kExact = 9007199254740992.0;
 struct EvalBufs {
   const PackedPlan* packed;
   const uint4* pcut;        // per-class layout: cut row of pipeline slot at [slot]
+  const uint64_t* hdp;      // per-class layout: the syncs of pipeline slot's stages at [16 slot, + 16)
   const uint32_t* meta;
   const uint32_t* ids;      // pipeline ids sorted by bucket
   const uint32_t* sstart;   // [16 - S]: start of the S-stage pipelines in ids; [16] = total
@@ -1285,7 +1296,7 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
   // first load
   const uint32_t slot2 = __shfl(slot, (int)(threadIdx.x & 63u));
   const double T = done ? dp_tail<S, kMode, kHet, kOvl>(t, h, load_plan<kHet>(e.packed, e.pcut, slot2), last,
-                                                         kHet ? e.pcut + (slot2 & ~3u) : nullptr)
+                                                         kHet ? e.hdp + (size_t)slot2 * kMaxStages : nullptr)
                         : 0;
   if (!done) {
     e.deferred[e.sstart[kMaxStages - S] + atomicAdd(&e.ctr[1 + kMaxStages - S], 1u)] = slot;
@@ -1534,6 +1545,16 @@ hipError_t launch_memory(const Tab& t, const sim_plans& p, int64_t n, uint64_t* 
   return hipGetLastError();
 }
 
+hipError_t launch_plan_syncs(const Tab& t, const PackedPlan* packed, const uint4* pcut, const uint32_t* meta,
+                             int64_t n, uint64_t* hdp, hipStream_t s) {
+  const int g = blocks_for(n, 256);
+  const size_t lds = t.mode < 2 ? t.lds_bytes : 0;
+  if (t.mode == 0) k_plan_syncs<0><<<g, 256, lds, s>>>(t, packed, pcut, meta, n, hdp);
+  else if (t.mode == 1) k_plan_syncs<1><<<g, 256, lds, s>>>(t, packed, pcut, meta, n, hdp);
+  else k_plan_syncs<2><<<g, 256, 0, s>>>(t, packed, pcut, meta, n, hdp);
+  return hipGetLastError();
+}
+
 hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint4* pcut, const uint32_t* meta, int64_t n,
                          uint64_t* out_stage, hipStream_t s) {
   if (pcut) k_stages<true><<<blocks_for(n * 4, 256), 256, 0, s>>>(t, packed, pcut, meta, n, out_stage);
@@ -1589,7 +1610,7 @@ int eval_grids(Tab* t) {
 }
 
 static EvalBufs bufs(const EvalArgs& a) {
-  return {a.packed, (const uint4*)a.pcut, a.meta, a.ids, a.sstart, a.out, a.ctr, a.ctr + kEvalCounters, a.deferred,
+  return {a.packed, (const uint4*)a.pcut, a.hdp, a.meta, a.ids, a.sstart, a.out, a.ctr, a.ctr + kEvalCounters, a.deferred,
           (unsigned long long*)a.skipped_ops};
 }
 
