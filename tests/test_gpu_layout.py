@@ -135,3 +135,48 @@ def test_per_class_layout_needs_its_cut_planes(torch, B, workloads):
     out = torch.empty(64, dtype=torch.int64, device="cuda")
     rc = B.lib().sim_eval_plans(sim.h, C.byref(ps), 64, out.data_ptr(), B._stream(None))
     assert rc == B.SIM_EINVAL
+
+
+def test_per_class_deep_and_wide_plans(torch, B, oracle_mod, workloads):
+    """Classes of 16 stages (every class its own 16-way split), whole-node TP 8, and single-stage
+    classes next to them, on the 512-device cluster."""
+    w = workloads.workload(3)
+    L = w["model"]["L"]
+    rng = np.random.default_rng(7)
+    n = 4096
+    p = dict(hdr=np.zeros(n, np.uint32), cls=np.zeros((4, n), np.uint32), types=np.zeros((4, n), np.uint64),
+             chdr=np.zeros(n, np.uint32), ccut=np.zeros((64, n), np.uint8))
+    gbs = w["model"]["global_batch"]
+    for i in range(n):
+        G = int(rng.integers(1, 5))
+        reps = [int(rng.integers(1, 3)) for _ in range(G)]
+        left = gbs - sum(reps)
+        nmb = [r for r in reps]
+        nmb[0] += left
+        ch = 0
+        for g in range(G):
+            tpl = int(rng.choice([0, 3])) if g % 2 else int(rng.integers(0, 4))
+            pp = 16 if g % 2 == 0 else int(rng.choice([1, 16]))
+            cuts = np.sort(rng.choice(np.arange(1, L), pp - 1, replace=False)).tolist() + [L]
+            for s, v in enumerate(cuts):
+                p["ccut"][g * 16 + s, i] = v
+            ch |= (tpl | ((pp - 1) << 2)) << (8 * g)
+            p["cls"][g, i] = reps[g] | (nmb[g] << 16)
+            p["types"][g, i] = int(sum(int(rng.integers(0, 4)) << (4 * s) for s in range(pp)))
+        p["chdr"][i] = ch
+        p["hdr"][i] = (G - 1) << 8 | (int(rng.integers(0, 2)) << 10)
+    say("case: per-class layout, 16-stage classes and TP 8, %d plans" % n)
+    got = B.times_u64(B.Sim(w["model"], w["cluster"]).eval_plans(B.device_plans(p)))
+    want = oracle_mod.Oracle(w["model"], w["cluster"]).eval(p)
+    _equal(got, want, "deep and wide per-class plans")
+    assert np.count_nonzero(want != MAXU) > n // 2
+
+
+def test_per_class_empty_call(torch, B, workloads):
+    w = workloads.workload(3)
+    p = workloads.het_plans(w, 0, 16)
+    sim = B.Sim(w["model"], w["cluster"])
+    out = torch.full((16,), 7, dtype=torch.int64, device="cuda")
+    sim.eval_plans(B.device_plans(p), n=0, out=out)
+    torch.cuda.synchronize()
+    assert torch.all(out == 7)

@@ -128,3 +128,17 @@ def test_capacity_edges(torch, B, oracle_mod, workloads):
             say("case: capacity edge plan %d type %d delta %d" % (i, k, delta))
             got = B.times_u64(B.Sim(w["model"], c).eval_plans(B.device_plans(one)))[0]
             assert got == (times[i] if delta == 0 else MAXU), (k, delta)
+
+
+def test_memory_empty_and_oversized_calls(torch, B, workloads):
+    import ctypes as C
+    w = _workload(workloads, 2)
+    sim = B.Sim(w["model"], w["cluster"])
+    p = workloads.plans(w, 0, 8)
+    dp = B.device_plans(p)
+    ps = B.plans_struct(dp)
+    out = torch.empty((8, 4, 16), dtype=torch.int64, device="cuda")
+    L = B.lib()
+    assert L.sim_eval_memory(sim.h, C.byref(ps), 0, out.data_ptr(), B._stream(None)) == B.SIM_OK
+    ps.stride = 1 << 22                      # stride >= n holds; n above 2^21 is rejected
+    assert L.sim_eval_memory(sim.h, C.byref(ps), (1 << 21) + 1, out.data_ptr(), B._stream(None)) == B.SIM_EINVAL

@@ -93,3 +93,27 @@ def test_overlap_rejected_with_per_class_layout(torch, B, workloads):
     p["hdr"] |= OVERLAP
     got = B.times_u64(B.Sim(w["model"], w["cluster"]).eval_plans(B.device_plans(p)))
     assert np.all(got == MAXU)
+
+
+def test_overlap_without_dp(torch, B, oracle_mod, workloads):
+    """One 8-stage replica holding every micro-batch: a DP group of one, no gradient sync, so
+    overlap changes nothing.  Every placement of 4 type-A and 4 type-B stages."""
+    import itertools
+    w = workloads.workload(1)
+    pats = [sum(1 << (4 * s) for s in c) for c in itertools.combinations(range(8), 4)]
+    n = len(pats)
+    q = dict(hdr=np.full(n, 7 << 4, np.uint32), cut=np.zeros((16, n), np.uint8), cls=np.zeros((4, n), np.uint32),
+             types=np.zeros((4, n), np.uint64))
+    q["cls"][0, :] = 1 | (8 << 16)
+    for s, v in enumerate([1, 2, 3, 4, 6, 8, 10, 12]):
+        q["cut"][s, :] = v
+    q["types"][0, :] = np.array(pats, dtype=np.uint64)
+    sim = B.Sim(w["model"], w["cluster"])
+    a = B.times_u64(sim.eval_plans(B.device_plans(q)))
+    q2 = {k: v.copy() for k, v in q.items()}
+    q2["hdr"] |= OVERLAP
+    b = B.times_u64(sim.eval_plans(B.device_plans(q2)))
+    want = oracle_mod.Oracle(w["model"], w["cluster"]).eval(q2)
+    assert np.all(want != MAXU)
+    _equal(b, want, "overlap without DP")
+    _equal(b, a, "overlap without DP equals no overlap")
