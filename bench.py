@@ -52,6 +52,7 @@ def pipeline_ops(p, valid, per_node=3, first=1):
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "eval_llama70b_16M_hbm_traffic.txt")
+SQ_FILE = os.path.join(ROOT, "profiles", "eval_llama70b_16M_sq_counters.txt")
 
 
 def source_hash():
@@ -63,20 +64,29 @@ def source_hash():
     return h.hexdigest()
 
 
-def measured_traffic(workload, chunk):
-    """HBM bytes per evaluation call (the whole 16M-plan workload in one call)
-    from the committed FETCH_SIZE/WRITE_SIZE summary; None unless it was taken
-    on this workload with the sources as they are now (hash recorded there)."""
-    if workload != 3 or chunk != 0 or not os.path.exists(TRAFFIC_FILE):
+def _profile_value(path, key, workload, chunk):
+    """A figure from a committed rocprofv3 summary of the 16M-plan workload in one call; None
+    unless it was taken on this workload with the sources as they are now (hash recorded there)."""
+    if workload != 3 or chunk != 0 or not os.path.exists(path):
         return None
     kv = {}
-    for line in open(TRAFFIC_FILE):
+    for line in open(path):
         if "=" in line and not line.startswith("#"):
             k, v = line.split("=", 1)
             kv[k.strip()] = v.strip()
     if kv.get("sources_sha256") != source_hash():
         return None
-    return int(kv["traffic_bytes_per_launch"])
+    return int(kv[key])
+
+
+def measured_traffic(workload, chunk):
+    """HBM bytes per evaluation call, from the FETCH_SIZE/WRITE_SIZE summary."""
+    return _profile_value(TRAFFIC_FILE, "traffic_bytes_per_launch", workload, chunk)
+
+
+def measured_valu(workload, chunk):
+    """VALU lane-ops executed per evaluation call by the evaluation kernels, from the SQ counter summary."""
+    return _profile_value(SQ_FILE, "valu_lane_ops_per_launch", workload, chunk)
 
 
 def main():
@@ -205,6 +215,10 @@ def main():
                 # not: what the evaluation would cost without the shortcut, in 32-bit integer ops
                 "int32_all_nodes_ops_per_launch": int32_per_launch,
                 "int32_all_nodes_rate_frac": round(int32_per_launch / (avg_ms * 1e-3) / PEAK_VALU, 4)}
+        # every VALU instruction the evaluation kernels execute (setup, recurrence, syncs), from counters
+        valu = None if a.plans else measured_valu(a.workload, a.chunk)
+        roof["valu_lane_ops_per_launch_counters"] = valu
+        roof["valu_issue_frac"] = None if valu is None else round(valu / (avg_ms * 1e-3) / PEAK_VALU, 4)
         extra = {"timed_steps_with_kernel_events": timed,
                  "prep_ms_per_step": round(setup_ms / timed, 4),
                  "first_pass_span_ms_per_step": round(pipe_ms / timed, 4),
