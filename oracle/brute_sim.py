@@ -82,3 +82,91 @@ def simulate(S, M, f, b, c):
     for s in range(S):
         assert nxt[s] == len(lists[s]), "simulation stalled"
     return idle_at, trace
+
+
+# ---------------------------------------------------------------------------
+# Interleaved 1F1B (several model chunks per device, as in Megatron-LM):
+# device s holds chunks j = 0..v-1, virtual stage j*S + s.
+
+
+def interleaved_op_list(S, v, M, s):
+    """Device s's ops as (kind, virtual stage, micro-batch), in the order it runs them:
+    warm-up forwards, then one forward and one backward at a time, then the remaining
+    backwards.  Forwards visit micro-batches in groups of S, chunk by chunk; backwards the
+    same groups with the chunks in reverse."""
+    n = M * v
+    warm = min(n, 2 * (S - 1 - s) + (v - 1) * S)
+
+    def fwd(k):
+        g, r = divmod(k, S * v)
+        return ("F", (r // S) * S + s, g * S + r % S)
+
+    def bwd(k):
+        g, r = divmod(k, S * v)
+        return ("B", (v - 1 - r // S) * S + s, g * S + r % S)
+    ops = [fwd(k) for k in range(warm)]
+    for i in range(n - warm):
+        ops.append(fwd(warm + i))
+        ops.append(bwd(i))
+    ops += [bwd(k) for k in range(n - warm, n)]
+    return ops
+
+
+def simulate_interleaved(S, v, M, f, b, c, cw):
+    """Event-driven replay: f, b per virtual stage; c[s] the hop between devices s and s+1;
+    cw the hop from the last device to the first (between chunks).  Returns the end time of
+    each device's last op."""
+    V = S * v
+    lists = [interleaved_op_list(S, v, M, s) for s in range(S)]
+    nxt = [0] * S
+    busy = [False] * S
+    idle_at = [0] * S
+    arrived = set()                      # (kind, vs, m) inputs present at the device of vs
+    for m in range(M):
+        arrived.add(("F", 0, m))
+    events = []
+    seq = 0
+
+    def push(t, kind, data):
+        nonlocal seq
+        heapq.heappush(events, (t, seq, kind, data))
+        seq += 1
+
+    def hop(vs_from, vs_to):
+        """Forward hops go vs -> vs + 1, backward ones vs -> vs - 1; the one between the
+        last device and the first (either way) is cw."""
+        lo = min(vs_from, vs_to) % S
+        return c[lo] if lo < S - 1 else cw
+
+    def try_start(s, now):
+        if busy[s] or nxt[s] >= len(lists[s]):
+            return
+        kind, vs, m = lists[s][nxt[s]]
+        if (kind, vs, m) not in arrived:
+            return
+        busy[s] = True
+        push(now + (f[vs] if kind == "F" else b[vs]), "done", (s, kind, vs, m))
+
+    for s in range(S):
+        try_start(s, 0)
+    while events:
+        now, _, kind, data = heapq.heappop(events)
+        if kind == "done":
+            s, k, vs, m = data
+            busy[s] = False
+            idle_at[s] = now
+            nxt[s] += 1
+            if k == "F":
+                if vs + 1 < V:
+                    push(now + hop(vs, vs + 1), "arrive", ("F", vs + 1, m))
+                else:
+                    arrived.add(("B", vs, m))
+            elif vs > 0:
+                push(now + hop(vs, vs - 1), "arrive", ("B", vs - 1, m))
+            try_start(s, now)
+        else:
+            arrived.add(data)
+            try_start(data[1] % S, now)
+    for s in range(S):
+        assert nxt[s] == len(lists[s]), "simulation stalled"
+    return idle_at

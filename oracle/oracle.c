@@ -28,7 +28,7 @@
  *   - device groups may differ in TP degree and layer split (Sec. 3); then
  *     the gradient sync is preceded by resharding (Sec. 3 "Resharding",
  *     Sec. 4.1 [C2]).
- * Where the paper is silent the reading used is named R1..R30 in comments;
+ * Where the paper is silent the reading used is named R1..R43 in comments;
  * the design notes of the repository list every reading.
  *
  * Parity notes: the recurrence, the collective formulas, the interconnect
@@ -42,6 +42,14 @@
  * stored-activation count (R32) is pinned for GPT-shaped layers to
  * Korthikanti et al. 2022; its gated-MLP and MoE terms are parity unpinned
  * beyond the reduction of a one-expert top-1 MoE layer to a gated dense one.
+ * The gradient-sync overlap (R38-R40) is pinned by an event queue over the
+ * same buckets and by its communication- and compute-bound extremes.
+ * Interleaved 1F1B (R41-R43) is pinned by the bubble closed form of
+ * Narayanan et al. 2021, an event-driven replay of the same op lists, the
+ * per-virtual-stage costs of a plain plan over the same cuts and the ring
+ * closed form of its per-device sync; its in-flight activation count (each
+ * pass counted at the device's largest chunk) is a bound of this reading,
+ * pinned only by its own differences.
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -379,6 +387,7 @@ static void pipeline(uint64_t S, uint64_t M, const uint64_t* f, const uint64_t* 
 typedef struct {
   uint64_t ep, G, zero, mi;
   uint64_t overlap;      /* 1: gradient sync overlapped with the last backward pass (R38) */
+  uint64_t v;            /* model chunks per device: 1 = plain 1F1B, 2..4 interleaved (R41) */
   uint64_t tp[OR_MAXG], S[OR_MAXG];
   uint64_t cut[OR_MAXG][OR_MAXS];
   uint64_t reps[OR_MAXG], nmb[OR_MAXG];
@@ -421,8 +430,9 @@ static int decode_rules(const or_ctx* x, const or_planes* q, int64_t i, or_plan*
   const or_model* m = &x->m;
   const int64_t stride = q->stride;
   const uint32_t hdr = q->hdr[i];
-  if (hdr >> 14) return 0;                                   /* V7 reserved bits */
+  if (hdr >> 16) return 0;                                   /* V7 reserved bits */
   p->overlap = (hdr >> 13) & 1;
+  p->v = ((hdr >> 14) & 3) + 1;
   p->ep = 1ull << ((hdr >> 2) & 3);
   p->G = ((hdr >> 8) & 3) + 1;
   p->zero = (hdr >> 10) & 1;
@@ -431,6 +441,7 @@ static int decode_rules(const or_ctx* x, const or_planes* q, int64_t i, or_plan*
   if (q->chdr) {
     if (hdr & 0xf3) return 0;                                /* V10 the header's TP and PP are unused (0) */
     if (p->overlap) return 0;                                /* V11 overlap needs the shared layout */
+    if (p->v > 1) return 0;                                  /* V12 interleaving needs the shared layout */
     uint32_t w = q->chdr[i];
     for (uint64_t g = 0; g < p->G; ++g) {
       uint32_t bt = (w >> (8 * g)) & 0xff;
@@ -444,9 +455,10 @@ static int decode_rules(const or_ctx* x, const or_planes* q, int64_t i, or_plan*
       p->S[g] = ((hdr >> 4) & 15) + 1;
     }
   }
-  for (uint64_t g = 0; g < p->G; ++g) {                      /* V2, per class */
+  if (p->v > 1 && (p->overlap || p->S[0] < 2 || p->S[0] * p->v > OR_MAXS)) return 0;   /* V12 */
+  for (uint64_t g = 0; g < p->G; ++g) {                      /* V2, per class; S*v virtual stages */
     uint64_t prev = 0;
-    for (uint64_t s = 0; s < p->S[g]; ++s) {
+    for (uint64_t s = 0; s < p->S[g] * p->v; ++s) {
       p->cut[g][s] = q->chdr ? q->ccut[(g * OR_MAXS + s) * stride + i] : q->cut[s * stride + i];
       if (p->cut[g][s] <= prev) return 0;
       prev = p->cut[g][s];
@@ -470,6 +482,11 @@ static int decode_rules(const or_ctx* x, const or_planes* q, int64_t i, or_plan*
     if (!heads_split(m, p->tp[g])) return 0;                 /* V5 */
   }
   if (batch != m->gbs) return 0;                             /* V4 exactly the global batch (R14) */
+  if (p->v > 1)                                              /* V12 (R42) */
+    for (uint64_t g = 0; g < p->G; ++g) {
+      uint64_t M = cdiv(p->nmb[g], p->reps[g]);
+      if (M % p->S[g] || M < 2 * p->S[g]) return 0;
+    }
   if (m->E == 0) {                                           /* V3 */
     if (p->ep != 1) return 0;
   } else {
@@ -496,6 +513,41 @@ static uint64_t in_flight(uint64_t S, uint64_t M, uint64_t s) {
   return W + 1 < M ? W + 1 : M;
 }
 
+/* R41: the warm-up forwards of device s under interleaved 1F1B with S
+ * devices, v chunks and M micro-batches. */
+static uint64_t interleaved_warmup(uint64_t S, uint64_t v, uint64_t M, uint64_t s) {
+  uint64_t w = 2 * (S - 1 - s) + (v - 1) * S;
+  return w < M * v ? w : M * v;
+}
+
+/* R31 for interleaved 1F1B (R43): device s holds the layers of its v chunks
+ * (virtual stages j*S + s), the embedding with virtual stage 0 and the head
+ * with the last one; it keeps at most W_s + 1 chunk forwards in flight, each
+ * counted at its largest chunk (a bound, not the exact mix). */
+static uint64_t stage_mem_interleaved(const or_ctx* x, const or_plan* p, uint64_t g, uint64_t s) {
+  const or_model* m = &x->m;
+  uint64_t tp = p->tp[g], ep = p->ep, S = p->S[g], v = p->v, ns = 0, nmax = 0;
+  for (uint64_t j = 0; j < v; ++j) {
+    uint64_t vs = j * S + s, lo = vs ? p->cut[g][vs - 1] : 0, n = p->cut[g][vs] - lo;
+    ns += n;
+    if (n > nmax) nmax = n;
+  }
+  uint64_t pd = mul(ns, layer_params_dense(x, tp)), pe = mul(ns, layer_params_expert(x, tp, ep));
+  if (s == 0) pd = add(pd, embed_params(x, tp));
+  if (s == S - 1) pd = add(pd, head_params(x, tp));
+  uint64_t p_all = 0;
+  for (uint64_t c = 0; c < p->G; ++c) p_all += p->reps[c];
+  uint64_t wg = mul(add(m->param_bytes, m->grad_bytes), add(pd, pe));
+  uint64_t opt;
+  if (p->zero) opt = add(cdiv(mul(m->opt_bytes, pd), p_all), cdiv(mul(m->opt_bytes, pe), p_all / ep));
+  else opt = mul(m->opt_bytes, add(pd, pe));
+  uint64_t M = cdiv(p->nmb[g], p->reps[g]);
+  uint64_t fly = interleaved_warmup(S, v, M, s) + 1;
+  if (fly > M * v) fly = M * v;
+  uint64_t act = mul(mul(nmax, layer_act_bytes(x, tp, m->mbs[p->mi])), fly);
+  return add(add(wg, opt), act);
+}
+
 /* R31: peak bytes on one device of stage s of class g.  Every replica keeps
  * the weights and gradients of the parameters its TP rank holds; the
  * optimizer state is kept whole, or, with ZeRO, split over the DP group
@@ -505,6 +557,7 @@ static uint64_t in_flight(uint64_t S, uint64_t M, uint64_t s) {
 static uint64_t stage_mem(const or_ctx* x, const or_plan* p, uint64_t g, uint64_t s) {
   const or_model* m = &x->m;
   uint64_t tp = p->tp[g], ep = p->ep;
+  if (p->v > 1) return stage_mem_interleaved(x, p, g, s);
   uint64_t lo = s ? p->cut[g][s - 1] : 0, ns = p->cut[g][s] - lo;
   uint64_t pd = mul(ns, layer_params_dense(x, tp)), pe = mul(ns, layer_params_expert(x, tp, ep));
   if (s == 0) pd = add(pd, embed_params(x, tp));
@@ -560,93 +613,145 @@ static void span_params(const or_ctx* x, uint64_t a, uint64_t b, uint64_t t, uin
   *pe = mul(b - a, layer_params_expert(x, t, ep));
 }
 
-static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t* scratch) {
-  const or_model* m = &x->m;
-  const or_cluster* cl = &x->c;
-  uint64_t G = p->G, ep = p->ep, epl = log2u(ep);
-  uint64_t b = m->mbs[p->mi];
-  uint64_t T = b * m->seq;
-  uint64_t act = mul(T, mul(m->h, m->e));                      /* one micro-batch activation (Table 1, R10) */
-  d->valid = 1; d->G = G;
-
-  /* R18 canonical packing: per pool, a bump pointer in (class, stage) order;
-   * a block starts at a multiple of its class's TP degree so that no TP
-   * group spans two nodes (with one TP degree for all classes every block
-   * already does) */
-  uint64_t ptr[OR_MAXK] = {0}, base[OR_MAXG][OR_MAXS];
-  for (uint64_t g = 0; g < G; ++g)
+/* R18 canonical packing: per pool, a bump pointer in (class, stage) order;
+ * a block starts at a multiple of its class's TP degree so that no TP group
+ * spans two nodes (with one TP degree for all classes every block already
+ * does) */
+static void place(const or_plan* p, uint64_t base[OR_MAXG][OR_MAXS]) {
+  uint64_t ptr[OR_MAXK] = {0};
+  for (uint64_t g = 0; g < p->G; ++g)
     for (uint64_t s = 0; s < p->S[g]; ++s) {
       int k = p->type[g][s];
       base[g][s] = cdiv(ptr[k], p->tp[g]) * p->tp[g];
       ptr[k] = base[g][s] + p->reps[g] * p->tp[g];
     }
+}
+
+/* Forward and backward time of one micro-batch over layers [lo, hi) on the
+ * devices of class g's stage on pool k from device `base` on: the layers
+ * (Sec. 3 non-uniform layer split), the embedding if `first`, the head if
+ * `last`, the TP all-reduces exposed in forward (Table 1, R22) and the MoE
+ * all-to-all in both passes (R20). */
+static void stage_compute(const or_ctx* x, const or_plan* p, uint64_t g, int k, uint64_t base, uint64_t lo,
+                          uint64_t hi, int first, int last, uint64_t* F, uint64_t* B) {
+  const or_model* m = &x->m;
+  const or_cluster* cl = &x->c;
+  uint64_t ep = p->ep, epl = log2u(ep), tp = p->tp[g], tpl = log2u(tp);
+  uint64_t b = m->mbs[p->mi], T = b * m->seq, ns = hi - lo, n = p->reps[g] * tp;
+  uint64_t act = mul(T, mul(m->h, m->e));                      /* one micro-batch activation (Table 1, R10) */
+  uint64_t Fc = 0, Bc = 0;
+  for (uint64_t l = lo; l < hi; ++l) {
+    Fc = add(Fc, LF(x, k, tpl, p->mi, epl)[l]);
+    Bc = add(Bc, LB(x, k, tpl, p->mi, epl)[l]);
+  }
+  if (first) { Fc = add(Fc, embed_time(x, k, b, 0)); Bc = add(Bc, embed_time(x, k, b, 1)); }
+  if (last) { Fc = add(Fc, head_time(x, k, tp, b, 0)); Bc = add(Bc, head_time(x, k, tp, b, 1)); }
+  uint64_t tpf = 0;
+  if (tp > 1) {
+    uint64_t nar = 2 * ns + (first != 0);
+    uint64_t steps = nar * 2 * (tp - 1);
+    tpf = add(mul(steps, cl->a_intra[k]), link_time(mul(steps, cdiv(act, tp)), intra_max(x, k, base, n)));
+  }
+  uint64_t epc = 0;
+  if (m->E && ep > 1) {
+    int intra = 1;
+    for (uint64_t grp = 0; grp < p->reps[g] / ep; ++grp) {
+      uint64_t f0 = base + grp * ep * tp, f1 = f0 + ep * tp - 1;
+      if (f0 / cl->dpn[k] != f1 / cl->dpn[k]) intra = 0;
+    }
+    uint64_t alpha, bq;
+    if (intra) { alpha = cl->a_intra[k]; bq = intra_max(x, k, base, n); }
+    else { alpha = mul(2, alpha_side(x, k)); bq = umax(nic_max(x, k, base, n), beta_q(cl->pcie[k])); }
+    uint64_t bytes = 0;
+    for (uint64_t l = lo; l < hi; ++l) {
+      uint64_t per = m->E / ep, wmax = 0;
+      for (uint64_t j = 0; j < ep; ++j) {
+        uint64_t w = 0;
+        for (uint64_t ex = j * per; ex < (j + 1) * per; ++ex) w += m->q[l * m->E + ex];
+        wmax = umax(wmax, w);
+      }
+      bytes = add(bytes, cdiv(mul(mul(ep - 1, T), mul(m->topk, mul(wmax, mul(m->h, m->e)))), 65536));
+    }
+    epc = add(mul(ns * 2 * (ep - 1), alpha), link_time(mul(2, bytes), bq));
+  }
+  *F = add(add(Fc, tpf), epc);
+  *B = add(Bc, epc);
+}
+
+/* PP hop between class g's stage on pool k (devices from b1 on) and its
+ * stage on pool k2 (from b2 on): activation forward, gradient backward
+ * (Table 1); intra-node iff same pool and every replica's pair of devices
+ * shares a node (R20) */
+static uint64_t hop_cost(const or_ctx* x, const or_plan* p, uint64_t g, int k, uint64_t b1, int k2, uint64_t b2) {
+  const or_model* m = &x->m;
+  const or_cluster* cl = &x->c;
+  uint64_t tp = p->tp[g], n = p->reps[g] * tp;
+  uint64_t act = mul(m->mbs[p->mi] * m->seq, mul(m->h, m->e));
+  int intra = (k == k2);
+  for (uint64_t r = 0; intra && r < p->reps[g]; ++r)
+    if ((b1 + r * tp) / cl->dpn[k] != (b2 + r * tp) / cl->dpn[k]) intra = 0;
+  uint64_t alpha, bq;
+  if (intra) {
+    alpha = cl->a_intra[k];
+    bq = umax(intra_max(x, k, b1, n), intra_max(x, k, b2, n));
+  } else {
+    alpha = add(alpha_side(x, k), alpha_side(x, k2));
+    bq = umax(umax(nic_max(x, k, b1, n), nic_max(x, k2, b2, n)), umax(beta_q(cl->pcie[k]), beta_q(cl->pcie[k2])));
+  }
+  return add(alpha, link_time(act, bq));
+}
+
+/* the DP ring's latency and rate over the devices of stage sg[g] of every
+ * class (R20, R21) */
+static void dp_link(const or_ctx* x, const or_plan* p, uint64_t base[OR_MAXG][OR_MAXS], const uint64_t* sg,
+                    uint64_t* alpha_out, uint64_t* bq_out) {
+  const or_cluster* cl = &x->c;
+  int k0 = p->type[0][sg[0]], same = 1;
+  uint64_t nlo = UINT64_MAX, nhi = 0;
+  for (uint64_t g = 0; g < p->G; ++g) {
+    int k = p->type[g][sg[g]];
+    if (k != k0) same = 0;
+    uint64_t n = p->reps[g] * p->tp[g];
+    for (uint64_t dv = base[g][sg[g]]; dv < base[g][sg[g]] + n; ++dv) {
+      uint64_t node = dv / cl->dpn[k];
+      if (node < nlo) nlo = node;
+      if (node > nhi) nhi = node;
+    }
+  }
+  uint64_t alpha, bq;
+  if (same && nlo == nhi) { alpha = cl->a_intra[k0]; bq = intra_bq(x, k0, nlo); }
+  else {
+    alpha = 0; bq = 0;
+    for (uint64_t g = 0; g < p->G; ++g) {
+      int k = p->type[g][sg[g]];
+      alpha = umax(alpha, mul(2, alpha_side(x, k)));                    /* R21 */
+      bq = umax(bq, umax(nic_max(x, k, base[g][sg[g]], p->reps[g] * p->tp[g]), beta_q(cl->pcie[k])));
+    }
+  }
+  *alpha_out = alpha;
+  *bq_out = bq;
+}
+
+static void eval_plan_interleaved(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t* scratch);
+
+static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t* scratch) {
+  if (p->v > 1) { eval_plan_interleaved(x, p, d, scratch); return; }
+  const or_model* m = &x->m;
+  const or_cluster* cl = &x->c;
+  uint64_t G = p->G, ep = p->ep, epl = log2u(ep), b = m->mbs[p->mi];
+  d->valid = 1; d->G = G;
+  uint64_t base[OR_MAXG][OR_MAXS];
+  place(p, base);
 
   for (uint64_t g = 0; g < G; ++g) {
-    uint64_t S = p->S[g], tp = p->tp[g], tpl = log2u(tp);
-    uint64_t n = p->reps[g] * tp;                              /* devices of one (class, stage) */
+    uint64_t S = p->S[g];
     d->S[g] = S;
     d->M[g] = cdiv(p->nmb[g], p->reps[g]);                     /* R16 */
     for (uint64_t s = 0; s < S; ++s) {
       int k = p->type[g][s];
-      uint64_t lo = s ? p->cut[g][s - 1] : 0, hi = p->cut[g][s], ns = hi - lo;
-      /* compute: sum of this stage's layers (Sec. 3 non-uniform layer split) */
-      uint64_t Fc = 0, Bc = 0;
-      for (uint64_t l = lo; l < hi; ++l) {
-        Fc = add(Fc, LF(x, k, tpl, p->mi, epl)[l]);
-        Bc = add(Bc, LB(x, k, tpl, p->mi, epl)[l]);
-      }
-      if (s == 0) { Fc = add(Fc, embed_time(x, k, b, 0)); Bc = add(Bc, embed_time(x, k, b, 1)); }
-      if (s == S - 1) { Fc = add(Fc, head_time(x, k, tp, b, 0)); Bc = add(Bc, head_time(x, k, tp, b, 1)); }
-      /* TP all-reduce, exposed in forward only (Table 1, R22) */
-      uint64_t tpf = 0;
-      if (tp > 1) {
-        uint64_t nar = 2 * ns + (s == 0);
-        uint64_t steps = nar * 2 * (tp - 1);
-        tpf = add(mul(steps, cl->a_intra[k]), link_time(mul(steps, cdiv(act, tp)), intra_max(x, k, base[g][s], n)));
-      }
-      /* MoE all-to-all, dispatch + combine per layer in each pass (R20) */
-      uint64_t epc = 0;
-      if (m->E && ep > 1) {
-        int intra = 1;
-        for (uint64_t grp = 0; grp < p->reps[g] / ep; ++grp) {
-          uint64_t first = base[g][s] + grp * ep * tp, last = first + ep * tp - 1;
-          if (first / cl->dpn[k] != last / cl->dpn[k]) intra = 0;
-        }
-        uint64_t alpha, bq;
-        if (intra) { alpha = cl->a_intra[k]; bq = intra_max(x, k, base[g][s], n); }
-        else { alpha = mul(2, alpha_side(x, k)); bq = umax(nic_max(x, k, base[g][s], n), beta_q(cl->pcie[k])); }
-        uint64_t bytes = 0;
-        for (uint64_t l = lo; l < hi; ++l) {
-          uint64_t per = m->E / ep, wmax = 0;
-          for (uint64_t j = 0; j < ep; ++j) {
-            uint64_t w = 0;
-            for (uint64_t ex = j * per; ex < (j + 1) * per; ++ex) w += m->q[l * m->E + ex];
-            wmax = umax(wmax, w);
-          }
-          bytes = add(bytes, cdiv(mul(mul(ep - 1, T), mul(m->topk, mul(wmax, mul(m->h, m->e)))), 65536));
-        }
-        epc = add(mul(ns * 2 * (ep - 1), alpha), link_time(mul(2, bytes), bq));
-      }
-      d->f[g][s] = add(add(Fc, tpf), epc);
-      d->b[g][s] = add(Bc, epc);
-      /* PP hop s -> s+1: activation forward, gradient backward (Table 1) */
-      d->c[g][s] = 0;
-      if (s + 1 < S) {
-        int k2 = p->type[g][s + 1];
-        int intra = (k == k2);
-        for (uint64_t r = 0; intra && r < p->reps[g]; ++r)
-          if ((base[g][s] + r * tp) / cl->dpn[k] != (base[g][s + 1] + r * tp) / cl->dpn[k]) intra = 0;
-        uint64_t alpha, bq;
-        if (intra) {
-          alpha = cl->a_intra[k];
-          bq = umax(intra_max(x, k, base[g][s], n), intra_max(x, k, base[g][s + 1], n));
-        } else {
-          alpha = add(alpha_side(x, k), alpha_side(x, k2));
-          bq = umax(umax(nic_max(x, k, base[g][s], n), nic_max(x, k2, base[g][s + 1], n)),
-                    umax(beta_q(cl->pcie[k]), beta_q(cl->pcie[k2])));
-        }
-        d->c[g][s] = add(alpha, link_time(act, bq));
-      }
+      uint64_t lo = s ? p->cut[g][s - 1] : 0, hi = p->cut[g][s];
+      stage_compute(x, p, g, k, base[g][s], lo, hi, s == 0, s == S - 1, &d->f[g][s], &d->b[g][s]);
+      d->c[g][s] = s + 1 < S ? hop_cost(x, p, g, k, base[g][s], p->type[g][s + 1], base[g][s + 1]) : 0;
     }
   }
 
@@ -678,28 +783,8 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
       while (p->cut[g][s] <= a) ++s;
       sg[g] = s;
     }
-    int k0 = p->type[0][sg[0]], same = 1;
-    uint64_t nlo = UINT64_MAX, nhi = 0;
-    for (uint64_t g = 0; g < G; ++g) {
-      int k = p->type[g][sg[g]];
-      if (k != k0) same = 0;
-      uint64_t n = p->reps[g] * p->tp[g];
-      for (uint64_t dv = base[g][sg[g]]; dv < base[g][sg[g]] + n; ++dv) {
-        uint64_t node = dv / cl->dpn[k];
-        if (node < nlo) nlo = node;
-        if (node > nhi) nhi = node;
-      }
-    }
     uint64_t alpha, bq;
-    if (same && nlo == nhi) { alpha = cl->a_intra[k0]; bq = intra_bq(x, k0, nlo); }
-    else {
-      alpha = 0; bq = 0;
-      for (uint64_t g = 0; g < G; ++g) {
-        int k = p->type[g][sg[g]];
-        alpha = umax(alpha, mul(2, alpha_side(x, k)));                  /* R21 */
-        bq = umax(bq, umax(nic_max(x, k, base[g][sg[g]], p->reps[g] * p->tp[g]), beta_q(cl->pcie[k])));
-      }
-    }
+    dp_link(x, p, base, sg, &alpha, &bq);
     seg_alpha[j] = alpha;
     seg_bq[j] = bq;
     /* R36: the ring runs on the coarsest TP layout among the classes */
@@ -773,6 +858,121 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
         d->tdp[g][s] = c - d->end[g][s];        /* the sync time left after the stage's end */
         T_iter = umax(T_iter, c);
       }
+  }
+  d->time = T_iter;
+}
+
+/* R41: interleaved 1F1B (Narayanan et al. 2021, as in Megatron-LM).  Device
+ * s runs chunks j = 0..v-1 of the model, virtual stage vs = j S + s.  Its
+ * ops: W_s forwards, then (forward, backward) pairs, then the remaining
+ * backwards; forward number k runs micro-batch (k / (S v)) S + k mod S of
+ * chunk (k mod S v) / S, backward number k the same micro-batch of chunk
+ * v - 1 - (k mod S v) / S.  A forward of vs waits for vs - 1's forward of
+ * the micro-batch plus the hop between their devices (the wrap hop cw from
+ * the last device to the first between chunks); a backward for vs + 1's
+ * backward plus the hop back, or on the last virtual stage for its own
+ * forward.  Evaluated by sweeping the devices as pipeline() does.
+ * f, b: [S v] per virtual stage; c: [S] hops s -> s+1. */
+static void pipeline_interleaved(uint64_t S, uint64_t v, uint64_t M, const uint64_t* f, const uint64_t* b,
+                                 const uint64_t* c, uint64_t cw, uint64_t* end, uint64_t* scratch) {
+  uint64_t V = S * v, n = M * v;
+  uint64_t* endF = scratch;          /* [V][M] */
+  uint64_t* endB = scratch + V * M;
+  for (uint64_t i = 0; i < 2 * V * M; ++i) scratch[i] = OR_INVALID;
+  uint64_t pos[OR_MAXS], last[OR_MAXS], W[OR_MAXS];
+  for (uint64_t s = 0; s < S; ++s) { pos[s] = 0; last[s] = 0; W[s] = interleaved_warmup(S, v, M, s); }
+  int progress = 1;
+  while (progress) {
+    progress = 0;
+    for (uint64_t s = 0; s < S; ++s) {
+      while (pos[s] < 2 * n) {
+        uint64_t q = pos[s], k;
+        int isB;
+        if (q < W[s]) { isB = 0; k = q; }
+        else if (q < 2 * n - W[s]) {
+          uint64_t i = (q - W[s]) / 2;
+          if ((q - W[s]) % 2 == 0) { isB = 0; k = W[s] + i; } else { isB = 1; k = i; }
+        } else { isB = 1; k = q - n; }
+        uint64_t r = k % V, mb = (k / V) * S + r % S;
+        uint64_t j = isB ? v - 1 - r / S : r / S, vs = j * S + s;
+        uint64_t ready;
+        if (!isB) {
+          if (vs == 0) ready = 0;
+          else if (endF[(vs - 1) * M + mb] == OR_INVALID) break;
+          else ready = add(endF[(vs - 1) * M + mb], s > 0 ? c[s - 1] : cw);
+        } else {
+          if (vs == V - 1) {
+            if (endF[vs * M + mb] == OR_INVALID) break;
+            ready = endF[vs * M + mb];
+          } else if (endB[(vs + 1) * M + mb] == OR_INVALID) break;
+          else ready = add(endB[(vs + 1) * M + mb], s < S - 1 ? c[s] : cw);
+        }
+        uint64_t e = add(umax(last[s], ready), isB ? b[vs] : f[vs]);
+        if (isB) endB[vs * M + mb] = e; else endF[vs * M + mb] = e;
+        last[s] = e;
+        pos[s]++;
+        progress = 1;
+      }
+    }
+  }
+  for (uint64_t s = 0; s < S; ++s) {
+    if (pos[s] != 2 * n) { fprintf(stderr, "oracle: interleaved pipeline deadlock\n"); abort(); }
+    end[s] = last[s];
+  }
+}
+
+/* An interleaved plan (shared layout): per class, virtual stage costs, the
+ * hops between devices (c[g][S-1] holds the wrap hop), the DP sync of each
+ * device over the parameters of all its chunks, and T = max over classes
+ * and devices of the device's last op end plus its sync. */
+static void eval_plan_interleaved(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t* scratch) {
+  const or_model* m = &x->m;
+  uint64_t G = p->G, ep = p->ep, v = p->v;
+  d->valid = 1; d->G = G;
+  uint64_t base[OR_MAXG][OR_MAXS];
+  place(p, base);
+  for (uint64_t g = 0; g < G; ++g) {
+    uint64_t S = p->S[g], V = S * v;
+    d->S[g] = V;
+    d->M[g] = cdiv(p->nmb[g], p->reps[g]);
+    for (uint64_t vs = 0; vs < V; ++vs) {
+      uint64_t s = vs % S;
+      uint64_t lo = vs ? p->cut[g][vs - 1] : 0, hi = p->cut[g][vs];
+      stage_compute(x, p, g, p->type[g][s], base[g][s], lo, hi, vs == 0, vs == V - 1, &d->f[g][vs], &d->b[g][vs]);
+    }
+    for (uint64_t s = 0; s < S; ++s) {
+      uint64_t s2 = s + 1 < S ? s + 1 : 0;
+      d->c[g][s] = hop_cost(x, p, g, p->type[g][s], base[g][s], p->type[g][s2], base[g][s2]);
+    }
+    for (uint64_t s = S; s < OR_MAXS; ++s) d->c[g][s] = 0;
+  }
+  /* DP sync of each device over all its chunks' parameters (R43) */
+  uint64_t p_all = 0, S = p->S[0], tp = p->tp[0];
+  for (uint64_t g = 0; g < G; ++g) p_all += p->reps[g];
+  uint64_t tdp[OR_MAXS];
+  for (uint64_t s = 0; s < S; ++s) {
+    uint64_t sg[OR_MAXG];
+    for (uint64_t g = 0; g < G; ++g) sg[g] = s;
+    uint64_t alpha, bq, ns = 0;
+    dp_link(x, p, base, sg, &alpha, &bq);
+    for (uint64_t j = 0; j < v; ++j) {
+      uint64_t vs = j * S + s;
+      ns += p->cut[0][vs] - (vs ? p->cut[0][vs - 1] : 0);
+    }
+    uint64_t pd = mul(ns, layer_params_dense(x, tp)), pe = mul(ns, layer_params_expert(x, tp, ep));
+    if (s == 0) pd = add(pd, embed_params(x, tp));
+    if (s == S - 1) pd = add(pd, head_params(x, tp));
+    uint64_t t = dp_sync(p_all, p->zero, mul(m->grad_bytes, pd), mul(m->param_bytes, pd), alpha, bq);
+    if (m->E) t = add(t, dp_sync(p_all / ep, p->zero, mul(m->grad_bytes, pe), mul(m->param_bytes, pe), alpha, bq));
+    tdp[s] = t;
+  }
+  uint64_t T_iter = 0;
+  for (uint64_t g = 0; g < G; ++g) {
+    pipeline_interleaved(S, v, d->M[g], d->f[g], d->b[g], d->c[g], d->c[g][S - 1], d->end[g], scratch);
+    for (uint64_t s = 0; s < S; ++s) {
+      d->tdp[g][s] = tdp[s];
+      T_iter = umax(T_iter, add(d->end[g][s], tdp[s]));
+    }
   }
   d->time = T_iter;
 }
@@ -916,6 +1116,12 @@ void oracle_pipeline(uint64_t S, uint64_t M, const uint64_t* f, const uint64_t* 
   free(scratch);
 }
 /* Sec. 5: delay = jumbo frame (9200 B) * 8 / unidirectional Gb/s, in ps, rounded up */
+void oracle_pipeline_interleaved(uint64_t S, uint64_t v, uint64_t M, const uint64_t* f, const uint64_t* b,
+                                 const uint64_t* c, uint64_t cw, uint64_t* end) {
+  uint64_t* scratch = (uint64_t*)malloc(8 * 2 * S * v * M + 8);
+  pipeline_interleaved(S, v, M, f, b, c, cw, end, scratch);
+  free(scratch);
+}
 uint64_t oracle_alpha_ps(uint64_t gbps_unidir) { return cdiv(9200ull * 8 * 1000, gbps_unidir); }
 uint64_t oracle_beta_q(uint64_t MBps) { return beta_q(MBps); }
 uint64_t oracle_link_time(uint64_t bytes, uint64_t bq) { return link_time(bytes, bq); }

@@ -45,6 +45,7 @@ def lib():
         L.oracle_detail.restype = C.c_int
         L.oracle_detail_size.restype = C.c_size_t
         L.oracle_pipeline.argtypes = [u64, u64, P, P, P, P]
+        L.oracle_pipeline_interleaved.argtypes = [u64, u64, u64, P, P, P, u64, P]
         for name in ("oracle_alpha_ps", "oracle_beta_q"):
             getattr(L, name).argtypes = [u64]
             getattr(L, name).restype = u64
@@ -209,6 +210,17 @@ def pipeline(S, M, f, b, c):
     end = np.zeros(S, dtype=np.uint64)
     lib().oracle_pipeline(S, M, _ptr(fa), _ptr(ba), _ptr(ca), _ptr(end))
     return [int(v) for v in end]
+
+
+def pipeline_interleaved(S, v, M, f, b, c, cw):
+    """End time of each device's last op for interleaved 1F1B: f, b per virtual stage (S*v), c the S-1
+    hops between devices, cw the hop from the last device back to the first."""
+    fa = np.array(f, dtype=np.uint64)
+    ba = np.array(b, dtype=np.uint64)
+    ca = np.array(list(c) + [0], dtype=np.uint64)
+    end = np.zeros(S, dtype=np.uint64)
+    lib().oracle_pipeline_interleaved(S, v, M, _ptr(fa), _ptr(ba), _ptr(ca), cw, _ptr(end))
+    return [int(x) for x in end]
 
 
 def in_flight(S, M, s):

@@ -51,6 +51,8 @@ def _load():
                                      C.c_void_p, C.c_void_p, C.c_int64, C.c_int]
         L.plangen_random_het.argtypes = [C.POINTER(_Params), C.c_uint64, C.c_int64, C.c_void_p, C.c_void_p,
                                          C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64, C.c_int]
+        L.plangen_random_interleaved.argtypes = [C.POINTER(_Params), C.c_uint64, C.c_int64, C.c_void_p,
+                                                 C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64, C.c_int]
         L.plangen_draw.argtypes = [C.c_uint64, C.c_uint64]
         L.plangen_draw.restype = C.c_uint64
         _lib = L
@@ -241,6 +243,30 @@ def random_plans_het(m, c, seed, first, n, nthreads=None):
         nthreads = min(16, os.cpu_count() or 1)
     L.plangen_random_het(C.byref(P), first, n, p["hdr"].ctypes.data, p["ccut"].ctypes.data, p["cls"].ctypes.data,
                          p["types"].ctypes.data, p["chdr"].ctypes.data, n, nthreads)
+    return p
+
+
+def interleaved_plans(w, first=0, n=None, nthreads=None):
+    """Interleaved-1F1B plans of workload w (its own seed + 0x200; see plangen.c): v = 2..4 model
+    chunks per device, S devices with S*v <= 16, every class's micro-batches per replica a
+    multiple of S and at least 2S."""
+    if n is None:
+        n = w["n_plans"] - first
+    m, c = w["model"], w["cluster"]
+    L = _load()
+    P = _Params()
+    P.seed = (w["seed"] if w["seed"] is not None else 0x91A70001) + 0x200
+    P.L = m["L"]
+    P.K = len(c["types"])
+    for k, t in enumerate(c["types"]):
+        P.cap[k] = t["n_nodes"] * t["dev_per_node"]
+    P.batches = m["global_batch"] // m["mbs"][0]
+    P.experts = m.get("experts", 0)
+    p = empty_plans(n)
+    if nthreads is None:
+        nthreads = min(16, os.cpu_count() or 1)
+    L.plangen_random_interleaved(C.byref(P), first, n, p["hdr"].ctypes.data, p["cut"].ctypes.data,
+                                 p["cls"].ctypes.data, p["types"].ctypes.data, n, nthreads)
     return p
 
 

@@ -261,3 +261,125 @@ void plangen_random_het(const pg_params* P, uint64_t first, int64_t n, uint32_t*
   run_het(&jobs[0]);
   for (int t = 1; t < nthreads; ++t) pthread_join(th[t], 0);
 }
+
+/* ------------------------------------------------------------------ */
+/* interleaved plans: hdr bits 14-15 = v - 1 (v = 2..4 model chunks per
+ * device), PP = S devices, S*v virtual-stage cuts; every class runs a
+ * micro-batch count per replica M that is a multiple of S and at least 2S. */
+static void gen_one_il(const pg_params* P, uint64_t i, uint32_t* hdr, uint8_t* cut, uint32_t* cls, uint64_t* types,
+                       int64_t stride, int64_t slot) {
+  rng r = {P->seed, i, 0};
+  uint32_t tpl = 0, v = 2, S = 2, epl = 0, G = 0, zero = 0;
+  uint32_t reps[4] = {0}, nmb[4] = {0};
+  uint64_t tv[4] = {0};
+  for (int attempt = 0; attempt < 32 && G == 0; ++attempt) {
+    r.d = (uint64_t)attempt * 256;
+    tpl = (uint32_t)uni(&r, 0, 3);
+    v = (uint32_t)uni(&r, 2, 4);
+    S = (uint32_t)uni(&r, 2, 16 / v);
+    if (S * v > P->L) continue;
+    epl = 0;
+    if (P->experts) {
+      epl = (uint32_t)uni(&r, 0, 3);
+      while ((1u << epl) > P->experts || P->experts % (1u << epl)) --epl;
+    }
+    uint32_t want = (uint32_t)uni(&r, 1, 4);
+    zero = (uint32_t)uni(&r, 0, 1);
+    uint32_t tp = 1u << tpl, ep = 1u << epl;
+    uint32_t left[16];
+    memcpy(left, P->cap, sizeof(left));
+    /* every replica runs at least 2S micro-batches (2S-1 of them can be short) */
+    uint32_t budget = P->batches, g = 0;
+    for (uint32_t c = 0; c < want; ++c) {
+      uint32_t cnt[16] = {0};
+      uint64_t t = 0;
+      for (uint32_t s = 0; s < S; ++s) {
+        uint64_t k = uni(&r, 0, P->K - 1);
+        t |= k << (4 * s);
+        cnt[k]++;
+      }
+      uint32_t maxr = 0xffffffffu;
+      for (uint32_t k = 0; k < P->K; ++k)
+        if (cnt[k]) { uint32_t m = left[k] / (cnt[k] * tp); if (m < maxr) maxr = m; }
+      uint32_t per = 2 * S * 2 - 1;     /* a little more than the minimum per replica */
+      if (maxr > budget / per) maxr = budget / per;
+      maxr = maxr / ep * ep;
+      if (maxr < ep) break;
+      uint32_t rr = ep * (uint32_t)uni(&r, 1, maxr / ep);
+      for (uint32_t k = 0; k < P->K; ++k) left[k] -= rr * cnt[k] * tp;
+      reps[c] = rr; tv[c] = t; budget -= rr * (2 * S - 1) + rr; g = c + 1;
+    }
+    if (g == 0) continue;
+    /* micro-batches: class c runs M_c = S q_c per replica, so it takes between
+     * reps (M_c - 1) + 1 and reps M_c of them; raise q until the windows reach
+     * the global batch, then fill the windows */
+    uint32_t q[4] = {2, 2, 2, 2};
+    uint64_t lo_sum = 0, hi_sum = 0;
+    for (int guard = 0; guard < 100000; ++guard) {
+      lo_sum = hi_sum = 0;
+      for (uint32_t c = 0; c < g; ++c) {
+        lo_sum += (uint64_t)reps[c] * (S * q[c] - 1) + 1;
+        hi_sum += (uint64_t)reps[c] * S * q[c];
+      }
+      if (hi_sum >= P->batches) break;
+      q[uni(&r, 0, g - 1)]++;
+    }
+    if (lo_sum > P->batches || hi_sum < P->batches) continue;
+    uint64_t extra = P->batches - lo_sum;
+    for (uint32_t c = 0; c < g; ++c) {
+      uint64_t lo = (uint64_t)reps[c] * (S * q[c] - 1) + 1, width = reps[c] - 1;
+      uint64_t add = extra < width ? extra : width;
+      nmb[c] = (uint32_t)(lo + add);
+      extra -= add;
+    }
+    if (extra) continue;
+    G = g;
+  }
+  if (G == 0) {        /* give up: a plan that fails the micro-batch rule */
+    G = 1; reps[0] = 1u << epl; tv[0] = 0; nmb[0] = P->batches; S = 2; v = 2;
+  }
+  uint8_t pts[256];
+  for (uint32_t l = 1; l < P->L; ++l) pts[l - 1] = (uint8_t)l;
+  uint32_t V = S * v;
+  r.d = 32 * 256;
+  for (uint32_t j = 0; j + 1 < V; ++j) {
+    uint32_t pick = j + (uint32_t)uni(&r, 0, P->L - 2 - j);
+    uint8_t tmp = pts[j]; pts[j] = pts[pick]; pts[pick] = tmp;
+  }
+  for (uint32_t j = 1; j + 1 < V; ++j) {
+    uint8_t vv = pts[j]; int qq = (int)j - 1;
+    while (qq >= 0 && pts[qq] > vv) { pts[qq + 1] = pts[qq]; --qq; }
+    pts[qq + 1] = vv;
+  }
+  for (uint32_t s = 0; s < 16; ++s) cut[s * stride + slot] = 0;
+  for (uint32_t s = 0; s + 1 < V; ++s) cut[s * stride + slot] = pts[s];
+  cut[(V - 1) * stride + slot] = (uint8_t)P->L;
+  for (uint32_t c = 0; c < 4; ++c) {
+    cls[c * stride + slot] = c < G ? (reps[c] & 0xffff) | ((nmb[c] & 0xffff) << 16) : 0;
+    types[c * stride + slot] = c < G ? tv[c] : 0;
+  }
+  hdr[slot] = tpl | (epl << 2) | ((S - 1) << 4) | ((G - 1) << 8) | (zero << 10) | ((v - 1) << 14);
+}
+
+static void* run_il(void* a) {
+  pg_job* j = (pg_job*)a;
+  for (int64_t s = j->lo; s < j->hi; ++s)
+    gen_one_il(j->P, j->first + (uint64_t)s, j->hdr, j->cut, j->cls, j->types, j->stride, s);
+  return 0;
+}
+
+/* Interleaved plans first .. first+n-1 into slots 0 .. n-1. */
+void plangen_random_interleaved(const pg_params* P, uint64_t first, int64_t n, uint32_t* hdr, uint8_t* cut,
+                                uint32_t* cls, uint64_t* types, int64_t stride, int nthreads) {
+  if (nthreads < 1) nthreads = 1;
+  if (nthreads > 64) nthreads = 64;
+  pthread_t th[64];
+  pg_job jobs[64];
+  for (int t = 0; t < nthreads; ++t) {
+    pg_job j = {P, first, n * t / nthreads, n * (t + 1) / nthreads, stride, hdr, cut, cls, types};
+    jobs[t] = j;
+  }
+  for (int t = 1; t < nthreads; ++t) pthread_create(&th[t], 0, run_il, &jobs[t]);
+  run_il(&jobs[0]);
+  for (int t = 1; t < nthreads; ++t) pthread_join(th[t], 0);
+}
