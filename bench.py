@@ -106,6 +106,8 @@ def main():
                     help="also time the same plans with per-type device memory checked (0 = skip)")
     ap.add_argument("--overlap-steps", type=int, default=5,
                     help="also time the same plans with the gradient sync overlapped with the last backward (0 = skip)")
+    ap.add_argument("--il-steps", type=int, default=3,
+                    help="also time as many interleaved-1F1B plans of the workload (0 = skip)")
     ap.add_argument("--layout-steps", type=int, default=5,
                     help="also time as many per-class-layout plans of the workload (0 = skip)")
     ap.add_argument("--copy-calibrate", type=int, default=0, metavar="BYTES",
@@ -289,6 +291,33 @@ def main():
                "valid_plans": int(np.count_nonzero(B.times_u64(out) != MAXU)), "argmin": [hb_i, hb_t]}
         del dh
 
+    # Interleaved 1F1B plans (v model chunks per device) of the same workload
+    il = None
+    if a.il_steps > 0 and not a.chunk:
+        t0 = time.time()
+        pi = W.interleaved_plans(w, 0, n)
+        log("generated %d interleaved plans in %.1f s" % (n, time.time() - t0))
+        di = B.device_plans(pi)
+        sim.eval_plans(di, out=out)
+        sim.argmin(out, out=best)
+        torch.cuda.synchronize()
+        i0 = time.perf_counter()
+        for _ in range(a.il_steps):
+            sim.eval_plans(di, out=out)
+            sim.argmin(out, out=best)
+        torch.cuda.synchronize()
+        i1 = time.perf_counter()
+        ib_t, ib_i = B.best_tuple(best)
+        ivalid = B.times_u64(out) != MAXU
+        v = (((pi["hdr"] >> 14) & 3) + 1).astype(np.int64)
+        # schedule nodes: every device runs 2 M v ops per class
+        nodes = pipeline_ops(pi, ivalid, per_node=1, first=1) * v
+        il = {"workload": w["name"] + "/interleaved", "plans_per_s": round(n * a.il_steps / (i1 - i0), 1),
+              "steps": a.il_steps, "ms_per_step": round((i1 - i0) / a.il_steps * 1e3, 4),
+              "valid_plans": int(ivalid.sum()), "argmin": [ib_i, ib_t],
+              "schedule_nodes_per_s": round(float(nodes.sum()) * a.il_steps / (i1 - i0), 1)}
+        del di, pi
+
     # CPU baseline: the oracle as it stands, on a bounded prefix of the same plans
     cpu = None
     if a.cpu_seconds > 0:
@@ -320,6 +349,7 @@ def main():
     rec["memory_check"] = mem
     rec["dp_overlap"] = ovl
     rec["per_class_layout"] = lay
+    rec["interleaved"] = il
     print(json.dumps(rec), flush=True)
 
 

@@ -111,9 +111,17 @@ typedef struct {
  *                       soon as their part of the stage's last backward pass
  *                       is done, one after another on the stage's ring
  *                       (Sec. 6 on overlapping communication with
- *                       computation; shared layout only), 14-31 zero
+ *                       computation; shared layout only), 14-15 v-1:
+ *                       with v > 1, interleaved 1F1B (Narayanan et al.
+ *                       2021): each of the PP devices of a replica holds v
+ *                       model chunks, virtual stage j*PP + s on device s
+ *                       (shared layout only, no overlap, PP >= 2,
+ *                       PP*v <= 16, micro-batches per replica of every
+ *                       class a multiple of PP and at least 2 PP),
+ *                       16-31 zero
  *   cut[s*stride+i]     u8, last layer (exclusive) of stage s: 1 <= cut[0] <
- *                       ... < cut[PP-1] = L (the non-uniform layer split)
+ *                       ... < cut[PP-1] = L (the non-uniform layer split);
+ *                       interleaved: PP*v cuts, one per virtual stage
  *   cls[c*stride+i]     u32, class c: replicas in bits 0-15, micro-batches in
  *                       bits 16-31 (the class's share of the global batch)
  *   types[c*stride+i]   u64, device type of stage s of class c in bits [4s, 4s+4)
@@ -173,8 +181,9 @@ int sim_create(const sim_model_desc* model, const sim_cluster_desc* cluster, sim
  * caller-owned): per-stage compute from the cost tables, alpha-beta times of
  * the TP all-reduce (exposed in forward), the MoE all-to-all, the pipeline
  * point-to-point hops (Table 1 exposure) on each group's slowest link (Sec.
- * 4.1 [C4]), a 1F1B pipeline per class, then the DP gradient sync per stage
- * across all replicas.  n = 0 is a no-op.  Temporary device memory is taken
+ * 4.1 [C4]), a 1F1B pipeline per class (interleaved when the header says
+ * so), then the DP gradient sync per stage (per device) across all
+ * replicas.  n = 0 is a no-op.  Temporary device memory is taken
  * from a stream-ordered pool on `stream` (a hipStream_t; NULL = null
  * stream).  Returns SIM_EINVAL for a NULL pointer, n < 0 or stride < n,
  * SIM_ENOMEM if the temporary memory cannot be allocated, SIM_EHIP if a
@@ -189,9 +198,11 @@ int sim_eval_plans(sim_ctx* ctx, const sim_plans* plans, int64_t n, uint64_t* ou
  *   s -> s+1, 3 DP sync that waits for stage s of class c (with the
  *   per-class layout: the longest of the syncs of the layer segments the
  *   stage holds, resharding included);
- *   out_class[i*4 + c] = PP of the class | classes << 5 | M << 8 where M is the
- *   micro-batches per replica of class c (0 for an absent class or an
- *   invalid plan).
+ *   out_class[i*4 + c] = PP of the class | classes << 5 | M << 8 | (v-1) << 24
+ *   where M is the micro-batches per replica of class c (0 for an absent
+ *   class or an invalid plan).  For an interleaved plan s runs over the
+ *   PP*v virtual stages for q = 0, 1; q = 2 and 3 are per device (s < PP;
+ *   the hop of device PP-1 is the one back to device 0) and 0 past PP.
  * Entries of absent stages are left untouched.  n is at most 2^21 per call.
  * Same errors as sim_eval_plans.
  */
@@ -215,7 +226,11 @@ int sim_eval_stages(sim_ctx* ctx, const sim_plans* plans, int64_t n, uint64_t* o
  * inputs of its ops: the stored-activation count of Korthikanti et al.
  * 2022 without dropout masks and attention scores; routed MoE tokens
  * counted at the balanced top-k share) and min(PP - s, M) the micro-batches
- * stage s holds at once under 1F1B.  Entries of absent classes and stages
+ * stage s holds at once under 1F1B.  Interleaved plans: s is the device,
+ * whose layers are those of all its chunks, and the activation term is
+ * nmax * A * min(2 (PP-1-s) + (v-1) PP + 1, M v) with nmax the layers of the
+ * device's largest chunk (its warm-up passes plus one, each counted at that
+ * chunk).  Entries of absent classes and stages
  * are 0; all 64 entries of a plan that breaks another rule are
  * SIM_TIME_INVALID.  The memory check itself does not affect this output.
  * n is at most 2^21 per call.  Errors as sim_eval_plans.

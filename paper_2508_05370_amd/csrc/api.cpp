@@ -13,14 +13,14 @@
 namespace hetsim {
 hipError_t launch_fill32(uint32_t* p, uint32_t n, uint32_t v, hipStream_t s);
 hipError_t launch_prep(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, PackedPlan* packed, uint4* pcut,
-                       uint32_t* meta, uint32_t* hist, hipStream_t s);
+                       uint32_t* meta, uint32_t* hist, uint16_t* keys, hipStream_t s);
 hipError_t launch_memory(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, hipStream_t s);
 hipError_t launch_plan_syncs(const Tab& t, const PackedPlan* packed, const uint4* pcut, const uint32_t* meta,
                              int64_t n, uint64_t* hdp, hipStream_t s);
 hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint4* pcut, const uint32_t* meta, int64_t n,
                          uint64_t* out_stage, hipStream_t s);
 hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* sstart, hipStream_t s);
-hipError_t launch_scatter(const uint32_t* meta, uint32_t nslots, uint32_t* cursor, uint32_t* ids, hipStream_t s);
+hipError_t launch_scatter(const uint16_t* keys, uint32_t nslots, uint32_t* cursor, uint32_t* ids, hipStream_t s);
 hipError_t launch_first(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s);
 hipError_t launch_group(const Tab& t, const EvalArgs& a, uint32_t max_tasks, int g, hipStream_t s);
 hipError_t launch_deferred(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s);
@@ -140,7 +140,9 @@ static void end_event(sim_ctx* c, int kind, hipStream_t s, EventPair* e) {
 // Workspace of one chunk: packed plans, pipeline metadata, pipeline ids and
 // the deferred lists, bucket counts followed by the evaluation counters and
 // the overflow list (counts and counters cleared together), bucket cursors,
-// the start of each stage count's pipelines, and with the per-class layout
+// the start of each stage count's pipelines, each pipeline's bucket key
+// (u16, written with the metadata and read by the scatter), and with the
+// per-class layout
 // the plans' class cut rows (64 bytes per plan) and the syncs each pipeline's
 // stages wait for (16 u64 per pipeline slot, 512 bytes per plan).
 constexpr uint32_t kCounters = kBuckets + kEvalCounters;
@@ -149,6 +151,7 @@ struct Work {
   uint4* pcut;
   uint64_t* hdp;
   uint32_t *meta, *ids, *deferred, *hist, *ctr, *cursor, *sstart;
+  uint16_t* keys;
 };
 static size_t cut_rows_bytes(int64_t ch, bool het) { return het ? align256((size_t)ch * 64) : 0; }
 static size_t het_sync_bytes(int64_t ch, bool het) {
@@ -156,7 +159,8 @@ static size_t het_sync_bytes(int64_t ch, bool het) {
 }
 static size_t work_bytes(int64_t ch, bool het) {
   return align256((size_t)ch * sizeof(PackedPlan)) + 3 * align256((size_t)ch * 4 * 4) +
-         align256(kCounters * 4 + (size_t)ch * 4 * 4) + align256(kBuckets * 4) + align256((kMaxStages + 1) * 4) +
+         align256(kCounters * 4 + (size_t)ch * 4 * 4) + align256(kBuckets * 4) + align256(kSstartWords * 4) +
+         align256((size_t)ch * 4 * 2) +
          cut_rows_bytes(ch, het) + het_sync_bytes(ch, het);
 }
 static Work carve(void* base, int64_t ch, bool het) {
@@ -170,7 +174,8 @@ static Work carve(void* base, int64_t ch, bool het) {
   w.deferred = (uint32_t*)p; p += align256((size_t)ch * 16);
   w.hist = (uint32_t*)p; w.ctr = w.hist + kBuckets; p += align256(kCounters * 4 + (size_t)ch * 16);
   w.cursor = (uint32_t*)p; p += align256(kBuckets * 4);
-  w.sstart = (uint32_t*)p;
+  w.sstart = (uint32_t*)p; p += align256(kSstartWords * 4);
+  w.keys = (uint16_t*)p;
   return w;
 }
 
@@ -234,11 +239,11 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
     if (i >= 2) e = hipStreamWaitEvent(s, done(b), 0);
     if (e == hipSuccess) e = launch_fill32(W.hist, kCounters, 0, s);
     bool t1 = e == hipSuccess && begin_event(c, 1, s, &ev);
-    if (e == hipSuccess) e = launch_prep(c->tab, p, cn, out + off, W.packed, W.pcut, W.meta, W.hist, s);
+    if (e == hipSuccess) e = launch_prep(c->tab, p, cn, out + off, W.packed, W.pcut, W.meta, W.hist, W.keys, s);
     if (t1) end_event(c, 1, s, &ev);
     if (e == hipSuccess && het) e = launch_plan_syncs(c->tab, W.packed, W.pcut, W.meta, cn, W.hdp, s);
     if (e == hipSuccess) e = launch_scan(W.hist, W.cursor, W.sstart, s);
-    if (e == hipSuccess) e = launch_scatter(W.meta, (uint32_t)(cn * 4), W.cursor, W.ids, s);
+    if (e == hipSuccess) e = launch_scatter(W.keys, (uint32_t)(cn * 4), W.cursor, W.ids, s);
     const EvalArgs a = {W.packed, W.pcut, W.hdp, W.meta, W.ids, W.sstart, out + off, W.ctr, W.deferred,
                         c->timing ? c->skipped_ops : nullptr};
     EventPair e0;
@@ -302,7 +307,7 @@ extern "C" int sim_eval_stages(sim_ctx* c, const sim_plans* plans, int64_t n, ui
     return SIM_ENOMEM;
   PackedPlan* packed = (PackedPlan*)ws;
   uint4* pcut = het ? (uint4*)((char*)ws + align256((size_t)n * sizeof(PackedPlan))) : nullptr;
-  hipError_t e = launch_prep(c->tab, *plans, n, nullptr, packed, pcut, out_class, nullptr, s);
+  hipError_t e = launch_prep(c->tab, *plans, n, nullptr, packed, pcut, out_class, nullptr, nullptr, s);
   if (e == hipSuccess) e = launch_stages(c->tab, packed, pcut, out_class, n, out_stage, s);
   (void)hipFreeAsync(ws, s);
   return e == hipSuccess ? SIM_OK : SIM_EHIP;

@@ -13,7 +13,17 @@ constexpr int kMaxClasses = 4;
 constexpr int kRecWords = 4;                    // per (plan, class, stage): fwd, bwd, hop, dp
 constexpr int kPlanWords = kMaxClasses * kMaxStages * kRecWords;
 constexpr int kBucketsM = 128;                  // micro-batch-count buckets per (stages, classes)
-constexpr int kBuckets = kMaxStages * kMaxClasses * kBucketsM;
+constexpr int kPlainBuckets = kMaxStages * kMaxClasses * kBucketsM;
+// Interleaved 1F1B pipelines (S = 2..8 devices, v = 2..4 chunks, S v <= 16)
+// sort after all others, in groups keyed (S - 2) * 3 + (v - 2), each of
+// kIlBucketsQ micro-batch buckets.
+constexpr int kIlGroups = 21;
+constexpr int kIlBucketsQ = 48;
+constexpr int kBuckets = kPlainBuckets + 1024;
+static_assert(kIlGroups * kIlBucketsQ <= 1024, "interleaved buckets");
+// sstart: [16 - S] first sorted id of the S-stage pipelines, [16 + q] first
+// id of interleaved group q, [16 + kIlGroups] the total
+constexpr int kSstartWords = kMaxStages + kIlGroups + 1;
 
 // A validated plan packed into 80 contiguous bytes, so that the pipelines of
 // one plan gather it with five 16-byte loads.
@@ -87,7 +97,8 @@ struct Tab {
 
 // Device buffers of one evaluation pass over a chunk, as the host hands them
 // to the launcher.  sstart[16 - S] is the first sorted id of the S-stage
-// pipelines, sstart[16] their total.  ctr[0] counts overflowed pipelines,
+// pipelines, sstart[16] their total and the first id of the interleaved
+// pipelines (layout above).  ctr[0] counts overflowed pipelines,
 // ctr[1 + 16 - S] the S-stage pipelines deferred to the full-loop pass; the
 // overflow list follows the counters at ctr + kEvalCounters.
 constexpr uint32_t kEvalCounters = 32;

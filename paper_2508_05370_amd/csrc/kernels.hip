@@ -19,7 +19,8 @@
 //              state by one constant, the remaining steady iterations are
 //              added in one step (periodic shortcut); lanes still aperiodic
 //              after a fixed budget are deferred.
-//   k_deferred the deferred pipelines of all stage counts, full steady loop.
+//   k_deferred the interleaved-1F1B pipelines, then the deferred pipelines of
+//              all stage counts (full steady loop).
 //   k_redo_u64 pipelines whose time reached 2^53 ps, again in u64.
 //              The plan's time is the max over its classes (atomic max).
 #include <hip/hip_runtime.h>
@@ -89,13 +90,30 @@ __device__ __forceinline__ uint32_t m_bucket(uint32_t M) {
 __device__ __forceinline__ uint32_t bucket_key(uint32_t S, uint32_t G, uint32_t M) {
   return ((kMaxStages - S) * kMaxClasses + (kMaxClasses - G)) * kBucketsM + (kBucketsM - 1 - m_bucket(M));
 }
+// interleaved pipelines: after all others, one group per (S, v), more
+// micro-batches first (q = M / S exact from 2 to 49).  M is a multiple of S
+// below 2^16, so M times the approximate reciprocal of S rounds to q.
+__device__ __forceinline__ uint32_t il_group(uint32_t S, uint32_t v) { return (S - 2) * 3 + (v - 2); }
+__device__ __forceinline__ uint32_t il_key(uint32_t S, uint32_t v, uint32_t M) {
+  const uint32_t q = (uint32_t)((float)M * __builtin_amdgcn_rcpf((float)S) + 0.5f) - 2;
+  return kPlainBuckets + il_group(S, v) * kIlBucketsQ + (kIlBucketsQ - 1 - (q < kIlBucketsQ - 1 ? q : kIlBucketsQ - 1));
+}
+// (S, v) shapes of interleaved pipelines: S v <= 16 virtual stages
+#define HETSIM_IL_SHAPES(X) \
+  X(2, 2) X(2, 3) X(2, 4) X(3, 2) X(3, 3) X(3, 4) X(4, 2) X(4, 3) X(4, 4) X(5, 2) X(5, 3) X(6, 2) X(7, 2) X(8, 2)
+
+// pipeline metadata word: S | G << 5 | M << 8 | (v - 1) << 24 (0 = no pipeline);
+// bucket keys travel as u16, kNoKey = no pipeline
+constexpr uint32_t kNoKey = 0xffff;
+static_assert(kBuckets < kNoKey, "bucket keys fit 16 bits");
 
 // ---------------------------------------------------------------- plan validation
 // Decoded plan fields used by every pipeline of the plan.
 struct Plan {
   uint32_t tpl, epl, S, G, zero, mi, tp, ep, psum;
   uint32_t overlap;         // gradient sync overlapped with the last backward pass
-  uint64_t cut_lo, cut_hi;  // cut bytes of stages 0-7 and 8-15, eight per word
+  uint32_t v;               // model chunks per device: 1, or 2..4 for interleaved 1F1B
+  uint64_t cut_lo, cut_hi;  // cut bytes of stages 0-7 and 8-15, eight per word (virtual stages when v > 1)
   uint32_t reps[4], nmb[4];
   uint64_t tv[4];           // stage types, nibbles past S cleared
   // the class a pipeline evaluates: index, replicas, micro-batches, types.
@@ -134,6 +152,7 @@ __device__ __forceinline__ Plan unpack(const PackedPlan& q, uint32_t c = 0) {
   p.tpl = hdr & 3; p.epl = (hdr >> 2) & 3; p.S = ((hdr >> 4) & 15) + 1; p.G = ((hdr >> 8) & 3) + 1;
   p.zero = (hdr >> 10) & 1; p.mi = (hdr >> 11) & 3; p.tp = 1u << p.tpl; p.ep = 1u << p.epl; p.psum = q.psum;
   p.overlap = (hdr >> 13) & 1;
+  p.v = ((hdr >> 14) & 3) + 1;
   p.chdr = q.pad0;
   const uint64_t* cw = reinterpret_cast<const uint64_t*>(q.cut);
   p.cut_lo = cw[0];
@@ -175,8 +194,9 @@ constexpr int kPrepPerThread = 4;
 struct Checked {
   bool ok;
   uint32_t hdr, psum, chdr;
-  uint32_t tpl[4], S[4];   // per class
-  uint32_t cw[4][4];       // per class: cut bytes, four per word, 0 past the class's stages
+  uint32_t tpl[4], S[4];   // per class (devices per replica)
+  uint32_t v;              // model chunks per device (interleaved 1F1B when > 1)
+  uint32_t cw[4][4];       // per class: cut bytes, four per word, 0 past the class's (virtual) stages
   uint32_t cls[4];         // 0 past the class count
   uint64_t tv[4];          // stage types, nibbles past the class's stages cleared; 0 past the class count
 };
@@ -197,10 +217,16 @@ __device__ __forceinline__ Checked check_plan(const Tab& t, const sim_plans& pl,
     r.tv[c] = pl.types[c * st + i];
   }
   const uint32_t epl = (hdr >> 2) & 3, G = ((hdr >> 8) & 3) + 1, mi = (hdr >> 11) & 3;
-  const uint32_t ep = 1u << epl;
-  bool ok = (hdr >> 14) == 0 && mi < t.n_mbs && ((t.ep_ok >> epl) & 1);
-  // the per-class layout leaves the header's TP and PP fields unused (0) and has no overlap
-  if (kHet) ok = ok && (hdr & 0x20f3) == 0;
+  const uint32_t ep = 1u << epl, v = ((hdr >> 14) & 3) + 1;
+  bool ok = (hdr >> 16) == 0 && mi < t.n_mbs && ((t.ep_ok >> epl) & 1);
+  // the per-class layout leaves the header's TP and PP fields unused (0) and
+  // has neither overlap nor interleaving
+  if (kHet) ok = ok && (hdr & 0xe0f3) == 0;
+  // interleaving: no overlap, at least two devices, at most 16 virtual stages
+  if (!kHet && v > 1) {
+    const uint32_t S0 = ((hdr >> 4) & 15) + 1;
+    ok = ok && ((hdr >> 13) & 1) == 0 && S0 >= 2 && S0 * v <= (uint32_t)kMaxStages;
+  }
   uint32_t batch = 0, psum = 0;
 #pragma unroll
   for (uint32_t c = 0; c < 4; ++c) {
@@ -214,10 +240,11 @@ __device__ __forceinline__ Checked check_plan(const Tab& t, const sim_plans& pl,
       if (kHet) ok = ok && (lay >> 6) == 0;
       if (kHet || c == 0) {   // the shared layout's cuts are checked once
         ok = ok && ((t.tp_ok >> tpl) & 1);
+        const uint32_t ncut = kHet ? S : S * v;
         uint32_t prev = 0;
 #pragma unroll
         for (uint32_t s = 0; s < 16; ++s) {
-          if (s < S) {
+          if (s < ncut) {
             const uint32_t v = cb[(kHet ? 16 * c : 0) + s];
             ok = ok && v > prev;
             prev = v;
@@ -232,6 +259,10 @@ __device__ __forceinline__ Checked check_plan(const Tab& t, const sim_plans& pl,
       r.tv[c] &= stage_sel(S);
       const uint32_t reps = r.cls[c] & 0xffff, nmb = r.cls[c] >> 16;
       ok = ok && reps >= 1 && nmb >= reps && (reps & (ep - 1)) == 0;
+      if (!kHet && v > 1 && ok) {   // interleaving: M a multiple of S and at least 2 S
+        const uint32_t M = (nmb + reps - 1) / reps;
+        ok = M % S == 0 && M >= 2 * S;
+      }
       batch += nmb * t.mbs[mi];
       psum += reps;
       // every stage's type exists and holds whole TP groups in a node
@@ -257,6 +288,7 @@ __device__ __forceinline__ Checked check_plan(const Tab& t, const sim_plans& pl,
   r.hdr = hdr;
   r.psum = psum;
   r.chdr = chdr;
+  r.v = kHet ? 1 : v;
   return r;
 }
 
@@ -305,12 +337,49 @@ __device__ __forceinline__ uint64_t class_stage_bytes(const Tab& t, const Checke
   return state + (uint64_t)ns * fly * t.act_layer[r.tpl[c]][mi];
 }
 
+// Interleaved 1F1B: device s holds virtual stages j S + s (j < v), so its
+// state covers the layers of all of them (ns; the embedding on device 0, the
+// head on device S - 1), and its activations are those of its
+// 2 (S - 1 - s) + (v - 1) S warm-up passes plus one (at most M v passes),
+// each counted at the device's largest chunk (nmax layers).
+__device__ __forceinline__ void il_device_layers(const Checked& r, uint32_t s, uint32_t& ns, uint32_t& nmax) {
+  const uint32_t S = r.S[0];
+  ns = 0;
+  nmax = 0;
+  for (uint32_t j = 0; j < r.v; ++j) {
+    const uint32_t vs = j * S + s;
+    const uint32_t n = checked_cut(r, 0, vs) - (vs ? checked_cut(r, 0, vs - 1) : 0);
+    ns += n;
+    nmax = n > nmax ? n : nmax;
+  }
+}
+__device__ __forceinline__ uint64_t il_stage_bytes(const Tab& t, const Checked& r, uint32_t c, uint32_t s,
+                                                   uint32_t nmax, uint64_t state) {
+  const uint32_t mi = (r.hdr >> 11) & 3, S = r.S[c], v = r.v;
+  const uint32_t reps = r.cls[c] & 0xffff, M = ((r.cls[c] >> 16) + reps - 1) / reps;
+  const uint32_t w = 2 * (S - 1 - s) + (v - 1) * S + 1;
+  const uint32_t fly = w < M * v ? w : M * v;
+  return state + (uint64_t)nmax * fly * t.act_layer[r.tpl[c]][mi];
+}
+
 // Every device of a checked plan fits its type's memory.  With one layout
 // for all classes a stage's state is the same for every class: computed once.
 template <bool kHet>
 __device__ __forceinline__ bool fits_memory(const Tab& t, const Checked& r) {
   const uint32_t G = ((r.hdr >> 8) & 3) + 1;
   bool ok = true;
+  if (!kHet && r.v > 1) {
+    for (uint32_t s = 0; s < r.S[0]; ++s) {
+      uint32_t ns, nmax;
+      il_device_layers(r, s, ns, nmax);
+      const uint64_t state = class_state_bytes(t, r, 0, s, ns);
+#pragma unroll
+      for (uint32_t c = 0; c < 4; ++c)
+        if (c < G)
+          ok = ok && il_stage_bytes(t, r, c, s, nmax, state) <= t.mem_cap[(uint32_t)(r.tv[c] >> (4 * s)) & 15];
+    }
+    return ok;
+  }
   if (!kHet) {
     uint32_t prev = 0;
     for (uint32_t s = 0; s < r.S[0]; ++s) {
@@ -342,11 +411,13 @@ __device__ __forceinline__ bool fits_memory(const Tab& t, const Checked& r) {
 // (with the per-class layout, the class header word goes to pad0 and each
 // class's cut row to pcut[4 i + c]).  Writes out[i] (0 = valid, to be raised
 // by the pipelines; else invalid) and the per-pipeline metadata
-// S | G << 5 | M << 8 with the class's own S (0 = no pipeline).
+// S | G << 5 | M << 8 | (v - 1) << 24 with the class's own S (0 = no pipeline),
+// and (keys, when given) each pipeline's bucket (kNoKey = no pipeline).
 template <bool kHet>
 __global__ void __launch_bounds__(256) k_prep(Tab t, sim_plans pl, int64_t n, uint64_t* __restrict__ out,
                                               PackedPlan* __restrict__ packed, uint4* __restrict__ pcut,
-                                              uint32_t* __restrict__ meta, uint32_t* __restrict__ hist) {
+                                              uint32_t* __restrict__ meta, uint32_t* __restrict__ hist,
+                                              uint16_t* __restrict__ keys) {
   __shared__ uint32_t lh[kBuckets];
   if (hist) {
     for (uint32_t j = threadIdx.x; j < kBuckets; j += blockDim.x) lh[j] = 0;
@@ -371,16 +442,27 @@ __global__ void __launch_bounds__(256) k_prep(Tab t, sim_plans pl, int64_t n, ui
         for (int c = 0; c < 4; ++c) pcut[4 * i + c] = make_uint4(r.cw[c][0], r.cw[c][1], r.cw[c][2], r.cw[c][3]);
       }
     }
+    uint32_t m[4], key[4];
 #pragma unroll
     for (uint32_t c = 0; c < 4; ++c) {
-      uint32_t m = 0;
+      m[c] = 0;
+      key[c] = kNoKey;
       if (ok && c < G) {
         const uint32_t reps = r.cls[c] & 0xffff, M = ((r.cls[c] >> 16) + reps - 1) / reps;
-        m = r.S[c] | (G << 5) | (M << 8);
-        if (hist) atomicAdd(&lh[bucket_key(r.S[c], G, M)], 1u);
+        m[c] = r.S[c] | (G << 5) | (M << 8) | ((r.v - 1) << 24);
+        key[c] = r.v > 1 ? il_key(r.S[c], r.v, M) : bucket_key(r.S[c], G, M);
+        if (hist) atomicAdd(&lh[key[c]], 1u);
       }
-      meta[i * 4 + c] = m;
     }
+    // one 16-byte and one 8-byte store per plan (the workspace is 256-byte
+    // aligned; a caller's class array may be aligned to 4 bytes only)
+    if (((uintptr_t)meta & 15) == 0) {
+      reinterpret_cast<uint4*>(meta)[i] = make_uint4(m[0], m[1], m[2], m[3]);
+    } else {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) meta[i * 4 + c] = m[c];
+    }
+    if (keys) reinterpret_cast<uint2*>(keys)[i] = make_uint2(key[0] | key[1] << 16, key[2] | key[3] << 16);
   }
   if (hist) {
     __syncthreads();
@@ -404,7 +486,11 @@ __global__ void __launch_bounds__(256) k_memory(Tab t, sim_plans pl, int64_t n, 
       uint64_t v = kInvalid;
       if (r.ok) {
         v = 0;
-        if (c < G && s < r.S[c]) {
+        if (c < G && s < r.S[c] && r.v > 1) {
+          uint32_t ns, nmax;
+          il_device_layers(r, s, ns, nmax);
+          v = il_stage_bytes(t, r, c, s, nmax, class_state_bytes(t, r, c, s, ns));
+        } else if (c < G && s < r.S[c]) {
           const uint32_t cut = checked_cut(r, c, s);
           v = class_stage_bytes(t, r, c, s, cut - prev, class_state_bytes(t, r, c, s, cut - prev));
           prev = cut;
@@ -831,73 +917,101 @@ __device__ __forceinline__ void het_plan_syncs(const Tab& t, const Hot<kMode>& h
     if (c2 < G) drow[c2 * kMaxStages + stg[c2]] = cur[c2];
 }
 
+// Forward and backward time of one micro-batch over layers [lo, hi) on the
+// reps * tp devices of the pipeline's class from `base` on in pool k (type
+// ti; bq_in, bq_nic: slowest node fabric and NIC rates over them): the
+// layers, the embedding if `first`, the head if `last`, the TP all-reduces
+// exposed in the forward pass and the MoE all-to-all in both passes.
+template <int kMode, bool kHet>
+__device__ __forceinline__ void stage_cost(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t k,
+                                           const TypeInfo& ti, uint32_t base, uint32_t bq_in, uint32_t bq_nic,
+                                           uint32_t lo, uint32_t hi, bool first, bool last, uint64_t& fc,
+                                           uint64_t& bc) {
+  const uint32_t tp = p.tp, ep = p.ep, tpl = p.tpl, epl = p.epl, mi = p.mi, ns = hi - lo, dpl = ti.dpl;
+  const uint64_t act = t.act[mi], act_tp = (act + tp - 1) >> tpl;
+  const uint32_t L1 = t.L + 1, epq = t.E ? p.epl : 0;
+  const uint32_t reps = p.rc;
+  const uint32_t row = ((k * 4 + tpl) * t.n_mbs + mi) * t.nep + epq;
+  if (t.uniform_layers) {
+    const ulonglong2 lc = h.pfb(row);
+    fc = lc.x * ns;
+    bc = lc.y * ns;
+  } else {
+    const ulonglong2 ph = h.pfb(row * L1 + hi), pl = h.pfb(row * L1 + lo);
+    fc = ph.x - pl.x;
+    bc = ph.y - pl.y;
+  }
+  if (first) {
+    const ulonglong2 em = h.emb(k * t.n_mbs + mi);
+    fc += em.x;
+    bc += em.y;
+  }
+  if (last) {
+    const ulonglong2 hd = h.head((k * 4 + tpl) * t.n_mbs + mi);
+    fc += hd.x;
+    bc += hd.y;
+  }
+  if (tp > 1) {  // TP all-reduces of this stage, exposed in the forward pass
+    const uint64_t steps = (uint64_t)(2 * ns + first) * 2 * (tp - 1);
+    fc += steps * ti.a_intra + link_ps(steps * act_tp, bq_in);
+  }
+  if (t.E && ep > 1) {  // dispatch + combine all-to-all in each pass
+    // EP groups are blocks of ep*tp devices from base on.  With one TP
+    // degree for all classes base is a multiple of ep*tp, and the groups
+    // are inside nodes iff one fits a node.  With per-class degrees, a
+    // group of E = ep*tp <= node size starting at offset r in its node
+    // fits iff r <= node - E; the offsets of the successive groups are
+    // base's in-node offset plus multiples of E, so with b = base mod E
+    // != 0 the first group to cross is number node/E - 1 - (in-node offset div E).
+    const uint32_t E = ep * tp;
+    bool intra = E <= (1u << dpl);
+    if (kHet && intra && (base & (E - 1)) != 0) {
+      const uint32_t q = (base & ((1u << dpl) - 1)) / E;
+      intra = reps / ep <= (1u << dpl) / E - 1 - q;
+    }
+    const uint64_t alpha = intra ? ti.a_intra : 2 * ti.a_side;
+    const uint32_t bq = intra ? bq_in : (bq_nic > ti.bq_pcie ? bq_nic : ti.bq_pcie);
+    const uint32_t pa = (epl * t.n_mbs + mi) * L1;
+    const uint64_t e = (uint64_t)ns * 2 * (ep - 1) * alpha + link_ps(2 * (h.pa(pa + hi) - h.pa(pa + lo)), bq);
+    fc += e;
+    bc += e;
+  }
+}
+
+// Where the devices of stage s of the pipeline's class sit: type k, its
+// pool's info, the first device in the pool, and the slowest node fabric
+// and NIC rates over the stage's reps * tp devices.
+template <int kMode, bool kHet>
+__device__ __forceinline__ void stage_place(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t s, uint32_t& k,
+                                            TypeInfo& ti, uint32_t& base, uint32_t& bq_in, uint32_t& bq_nic) {
+  k = (uint32_t)(p.tc >> (4 * s)) & 15;
+  ti = h.type(k);
+  base = dev_before_own<kHet>(p, s, k);
+  const uint32_t nd = p.rc * p.tp, dpl = ti.dpl;
+  const uint32_t gnl = ti.node_off + (base >> dpl), gnh = ti.node_off + ((base + nd - 1) >> dpl);
+  bq_in = range_max(h.rmi(), t.N, gnl, gnh);
+  const uint32_t dlo = ti.dev_off + base;
+  bq_nic = range_max(h.rmn, t.D, dlo, dlo + nd - 1);
+}
+
 template <int kMode, bool kHet, typename Sink>
 __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t c,
                                             Sink& sink, const uint4* prow) {
-  const uint32_t S = p.S, tp = p.tp, ep = p.ep, tpl = p.tpl, epl = p.epl, mi = p.mi;
-  const uint64_t act = t.act[mi], act_tp = (act + tp - 1) >> tpl;
+  const uint32_t S = p.S, tp = p.tp, epl = p.epl;
+  const uint64_t act = t.act[p.mi];
   const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> epl);
-  const uint32_t L1 = t.L + 1, epq = t.E ? p.epl : 0;
   const uint32_t reps = p.rc;
-  const uint64_t tvc = p.tc;
   uint32_t pk = 0, pbase = 0, pnic = 0, pin = 0, lo = 0;
   TypeInfo pti = {};
   for (uint32_t s = 0; s < S; ++s) {
-    const uint32_t hi = cut_at(p, s), ns = hi - lo;
+    const uint32_t hi = cut_at(p, s);
     // ---- this class: compute, TP, EP, hop from the previous stage
-    const uint32_t k = (uint32_t)(tvc >> (4 * s)) & 15;
-    const TypeInfo ti = h.type(k);
-    const uint32_t base = dev_before_own<kHet>(p, s, k), nd = reps * tp, dpl = ti.dpl;
-    const uint32_t gnl = ti.node_off + (base >> dpl), gnh = ti.node_off + ((base + nd - 1) >> dpl);
-    const uint32_t bq_in = range_max(h.rmi(), t.N, gnl, gnh);
-    const uint32_t dlo = ti.dev_off + base;
-    const uint32_t bq_nic = range_max(h.rmn, t.D, dlo, dlo + nd - 1);
-    const uint32_t row = ((k * 4 + tpl) * t.n_mbs + mi) * t.nep + epq;
+    uint32_t k, base, bq_in, bq_nic;
+    TypeInfo ti;
+    stage_place<kMode, kHet>(t, h, p, s, k, ti, base, bq_in, bq_nic);
+    const uint32_t dpl = ti.dpl;
     uint64_t fc, bc;
-    if (t.uniform_layers) {
-      const ulonglong2 lc = h.pfb(row);
-      fc = lc.x * ns;
-      bc = lc.y * ns;
-    } else {
-      const ulonglong2 ph = h.pfb(row * L1 + hi), pl = h.pfb(row * L1 + lo);
-      fc = ph.x - pl.x;
-      bc = ph.y - pl.y;
-    }
-    if (s == 0) {
-      const ulonglong2 em = h.emb(k * t.n_mbs + mi);
-      fc += em.x;
-      bc += em.y;
-    }
-    if (s == S - 1) {
-      const ulonglong2 hd = h.head((k * 4 + tpl) * t.n_mbs + mi);
-      fc += hd.x;
-      bc += hd.y;
-    }
-    if (tp > 1) {  // TP all-reduces of this stage, exposed in the forward pass
-      const uint64_t steps = (uint64_t)(2 * ns + (s == 0)) * 2 * (tp - 1);
-      fc += steps * ti.a_intra + link_ps(steps * act_tp, bq_in);
-    }
-    if (t.E && ep > 1) {  // dispatch + combine all-to-all in each pass
-      // EP groups are blocks of ep*tp devices from base on.  With one TP
-      // degree for all classes base is a multiple of ep*tp, and the groups
-      // are inside nodes iff one fits a node.  With per-class degrees, a
-      // group of E = ep*tp <= node size starting at offset r in its node
-      // fits iff r <= node - E; the offsets of the successive groups are
-      // base's in-node offset plus multiples of E, so with b = base mod E
-      // != 0 the first group to cross is number node/E - 1 - (in-node offset div E).
-      const uint32_t E = ep * tp;
-      bool intra = E <= (1u << dpl);
-      if (kHet && intra && (base & (E - 1)) != 0) {
-        const uint32_t q = (base & ((1u << dpl) - 1)) / E;
-        intra = reps / ep <= (1u << dpl) / E - 1 - q;
-      }
-      const uint64_t alpha = intra ? ti.a_intra : 2 * ti.a_side;
-      const uint32_t bq = intra ? bq_in : (bq_nic > ti.bq_pcie ? bq_nic : ti.bq_pcie);
-      const uint32_t pa = (epl * t.n_mbs + mi) * L1;
-      const uint64_t e = (uint64_t)ns * 2 * (ep - 1) * alpha + link_ps(2 * (h.pa(pa + hi) - h.pa(pa + lo)), bq);
-      fc += e;
-      bc += e;
-    }
+    stage_cost<kMode, kHet>(t, h, p, k, ti, base, bq_in, bq_nic, lo, hi, s == 0, s == S - 1, fc, bc);
     uint64_t hop = 0;
     if (s > 0) {  // hop (s-1) -> s
       // same pool means the two ranges are adjacent: intra iff the pair spans one node
@@ -1003,7 +1117,13 @@ __device__ __forceinline__ double dp_tail(const Tab& t, const Hot<kMode>& h, con
   return T;
 }
 
-// per (class, stage) quantities of every plan, in plan order
+template <int S, int v>
+__device__ __forceinline__ void il_records(const Tab& t, const Hot<2>& h, const Plan& p, uint64_t* o);
+__device__ __forceinline__ uint32_t il_shape(uint32_t S, uint32_t v) { return S | (v - 1) << 5; }
+
+// per (class, stage) quantities of every plan, in plan order; for an
+// interleaved pipeline per virtual stage (hops and syncs per device, in the
+// first S records, the last hop being the wrap hop)
 template <bool kHet>
 __global__ void __launch_bounds__(256) k_stages(Tab t, const PackedPlan* __restrict__ packed,
                                                 const uint4* __restrict__ pcut, const uint32_t* __restrict__ meta,
@@ -1011,8 +1131,21 @@ __global__ void __launch_bounds__(256) k_stages(Tab t, const PackedPlan* __restr
   const int64_t slot = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (slot >= n * 4 || meta[slot] == 0) return;
   const Plan p = load_plan<kHet>(packed, pcut, (uint32_t)slot);
-  uint64_t rec[kMaxStages][kRecWords];
   const Hot<2> h(t, nullptr);
+  if (!kHet && p.v > 1) {
+    uint64_t* o = out_stage + slot * (kMaxStages * kRecWords);
+    switch (il_shape(p.S, p.v)) {
+#define X(S_, V_)                        \
+  case S_ | (V_ - 1) << 5:               \
+    il_records<S_, V_>(t, h, p, o);      \
+    break;
+      HETSIM_IL_SHAPES(X)
+#undef X
+      default: break;
+    }
+    return;
+  }
+  uint64_t rec[kMaxStages][kRecWords];
   RecSink sink{rec};
   class_setup<2, kHet>(t, h, p, (uint32_t)(slot & 3), sink, kHet ? pcut + (slot & ~3ll) : nullptr);
   uint64_t* o = out_stage + slot * (kMaxStages * kRecWords);
@@ -1044,35 +1177,42 @@ __global__ void k_fill32(uint32_t* p, uint32_t n, uint32_t v) {
 }
 
 // exclusive scan of the bucket counts; sstart[16 - S] = first id of the
-// S-stage pipelines, sstart[16] = number of pipelines
+// S-stage pipelines, sstart[16 + q] = first id of interleaved group q,
+// sstart[16 + kIlGroups] = number of pipelines.  Thread tid takes plain
+// buckets [8 tid, 8 tid + 8) and interleaved bucket kPlainBuckets + tid; one
+// scan of (plain, interleaved) pairs, the interleaved ones after all plain.
 __global__ void __launch_bounds__(1024) k_scan(const uint32_t* __restrict__ hist, uint32_t* __restrict__ cursor,
                                                uint32_t* __restrict__ sstart) {
-  constexpr int kPer = kBuckets / 1024;
-  static_assert(kBuckets % 1024 == 0, "bucket count");
-  __shared__ uint32_t part[1024];
+  constexpr int kPer = kPlainBuckets / 1024;
+  static_assert(kPlainBuckets % 1024 == 0 && kBuckets - kPlainBuckets == 1024, "bucket count");
+  __shared__ uint2 part[1024];
   uint32_t v[kPer], sum = 0;
   const uint32_t tid = threadIdx.x;
 #pragma unroll
   for (int j = 0; j < kPer; ++j) { v[j] = hist[tid * kPer + j]; sum += v[j]; }
-  part[tid] = sum;
+  const uint32_t vi = hist[kPlainBuckets + tid];
+  part[tid] = make_uint2(sum, vi);
   __syncthreads();
   for (uint32_t off = 1; off < 1024; off <<= 1) {
-    const uint32_t x = tid >= off ? part[tid - off] : 0;
+    const uint2 x = tid >= off ? part[tid - off] : make_uint2(0, 0);
     __syncthreads();
-    part[tid] += x;
+    part[tid].x += x.x;
+    part[tid].y += x.y;
     __syncthreads();
   }
-  uint32_t run = part[tid] - sum;
-  // pipelines of S stages start at bucket (16 - S) * kBuckets / 16
-  if ((tid * kPer) % (kBuckets / kMaxStages) == 0) sstart[(tid * kPer) / (kBuckets / kMaxStages)] = run;
+  uint32_t run = part[tid].x - sum;
+  // pipelines of S stages start at bucket (16 - S) * kPlainBuckets / 16
+  if ((tid * kPer) % (kPlainBuckets / kMaxStages) == 0) sstart[(tid * kPer) / (kPlainBuckets / kMaxStages)] = run;
 #pragma unroll
   for (int j = 0; j < kPer; ++j) { cursor[tid * kPer + j] = run; run += v[j]; }
-  if (tid == 1023) sstart[kMaxStages] = part[1023];
+  const uint32_t irun = part[1023].x + part[tid].y - vi;
+  if (tid % kIlBucketsQ == 0 && tid / kIlBucketsQ <= (uint32_t)kIlGroups) sstart[kMaxStages + tid / kIlBucketsQ] = irun;
+  cursor[kPlainBuckets + tid] = irun;
 }
 
 // place every pipeline id at its bucket's next free position
 constexpr int kScatterPer = 64;
-__global__ void __launch_bounds__(256) k_scatter(const uint32_t* __restrict__ meta, uint32_t nslots,
+__global__ void __launch_bounds__(256) k_scatter(const uint16_t* __restrict__ keys, uint32_t nslots,
                                                  uint32_t* __restrict__ cursor, uint32_t* __restrict__ ids) {
   constexpr int kPer = kScatterPer;
   __shared__ uint32_t lc[kBuckets];
@@ -1086,10 +1226,10 @@ __global__ void __launch_bounds__(256) k_scatter(const uint32_t* __restrict__ me
     key[j] = 0xffffffffu;
     rank[j] = 0;
     if (slot < nslots) {
-      const uint32_t m = meta[slot];
-      if (m) {
-        key[j] = bucket_key(m & 31, (m >> 5) & 7, m >> 8);
-        rank[j] = atomicAdd(&lc[key[j]], 1u);
+      const uint32_t k = keys[slot];
+      if (k != kNoKey) {
+        key[j] = k;
+        rank[j] = atomicAdd(&lc[k], 1u);
       }
     }
   }
@@ -1320,6 +1460,245 @@ __device__ __forceinline__ void eval_deferred(const Tab& t, const Hot<kMode>& h,
   else eval_one<S, true, kMode, kHet>(t, h, e, slot);
 }
 
+// ---------------------------------------------------------------- interleaved 1F1B
+// Schedule (Narayanan et al. 2021): device s of an S-device pipeline holds
+// chunks j = 0..v-1 of the model, virtual stage j S + s.  It runs
+// W_s = 2 (S-1-s) + (v-1) S warm-up forwards, then (forward, backward) pairs,
+// then its last W_s backwards; its k-th forward runs chunk (k mod S v) / S,
+// its k-th backward chunk v-1 - (k mod S v) / S, both on micro-batch
+// (k div S v) S + k mod S.  With M a multiple of S and M >= 2 S the devices
+// advance in lockstep: at step t device s runs forward k = t - s, then
+// backward k = t - s - W_s (each where 0 <= k < M v), and each op's input is
+// an op of a neighbouring device at step t - 1: for a forward on device
+// s > 0 the forward of device s - 1, on device 0 (chunk j > 0) the forward
+// of device S - 1 across the wrap hop; for a backward on device s < S - 1
+// the backward of device s + 1, on device S - 1 (chunk j < v - 1) the
+// backward of device 0 across the wrap hop; the last virtual stage's
+// backward takes its own forward of the same step.  Steps run
+// t = 0 .. M v + W_0 - 1.  Within a trip of S v steps starting at a multiple
+// of S v, the chunk of every op is a compile-time constant, so every
+// duration is a register.
+
+// Hop between the devices of two stages of one class, a placed before b
+// when they share a pool: inside a node iff every replica's pair is, i.e.
+// iff a's first device and b's last one share a node.
+__device__ __forceinline__ uint64_t il_hop(uint32_t ka, const TypeInfo& ta, uint32_t basea, uint32_t ina,
+                                           uint32_t nica, uint32_t kb, const TypeInfo& tb, uint32_t baseb,
+                                           uint32_t inb, uint32_t nicb, uint32_t reps, uint32_t tp, uint64_t act) {
+  const uint32_t dpl = tb.dpl;
+  const bool intra = ka == kb && (basea >> dpl) == ((baseb + (reps - 1) * tp) >> dpl);
+  const uint64_t alpha = intra ? tb.a_intra : ta.a_side + tb.a_side;
+  uint32_t bq;
+  if (intra) {
+    bq = ina > inb ? ina : inb;
+  } else {
+    const uint32_t x = nica > nicb ? nica : nicb;
+    const uint32_t y = ta.bq_pcie > tb.bq_pcie ? ta.bq_pcie : tb.bq_pcie;
+    bq = x > y ? x : y;
+  }
+  return alpha + link_ps(act, bq);
+}
+
+// Per virtual stage forward and backward time (f, b), hops between devices
+// (c[s]: s -> s + 1, c[S - 1]: the wrap hop S - 1 -> 0).
+template <int S, int v, int kMode, typename V>
+__device__ __forceinline__ void il_setup(const Tab& t, const Hot<kMode>& h, const Plan& p, V (&f)[S * v],
+                                         V (&b)[S * v], V (&c)[S]) {
+  constexpr int NV = S * v;
+  const uint64_t act = t.act[p.mi];
+  uint32_t k0 = 0, base0 = 0, in0 = 0, nic0 = 0, pk = 0, pbase = 0, pin = 0, pnic = 0;
+  TypeInfo ti0 = {}, pti = {};
+#pragma unroll
+  for (int s = 0; s < S; ++s) {
+    uint32_t k, base, bq_in, bq_nic;
+    TypeInfo ti;
+    stage_place<kMode, false>(t, h, p, s, k, ti, base, bq_in, bq_nic);
+#pragma unroll
+    for (int j = 0; j < v; ++j) {
+      const int vs = j * S + s;
+      const uint32_t lo = vs ? cut_at(p, vs - 1) : 0, hi = cut_at(p, vs);
+      uint64_t fc, bc;
+      stage_cost<kMode, false>(t, h, p, k, ti, base, bq_in, bq_nic, lo, hi, vs == 0, vs == NV - 1, fc, bc);
+      f[vs] = (V)fc;
+      b[vs] = (V)bc;
+    }
+    if (s > 0) c[s - 1] = (V)il_hop(pk, pti, pbase, pin, pnic, k, ti, base, bq_in, bq_nic, p.rc, p.tp, act);
+    if (s == 0) {
+      k0 = k; ti0 = ti; base0 = base; in0 = bq_in; nic0 = bq_nic;
+    }
+    if (s == S - 1) c[S - 1] = (V)il_hop(k0, ti0, base0, in0, nic0, k, ti, base, bq_in, bq_nic, p.rc, p.tp, act);
+    pk = k; pti = ti; pbase = base; pin = bq_in; pnic = bq_nic;
+  }
+}
+
+// One trip of S v steps from step t0 (a multiple of S v).  kPred: some op of
+// the trip may lie outside its device's schedule (warm-up, cool-down);
+// otherwise every device runs a forward and a backward at every step.
+// F[s], B[s]: end of device s's latest forward / backward; busy[s]: of its
+// latest op.
+template <int S, int v, typename V, bool kPred>
+__device__ __forceinline__ void il_trip(int t0, int n, const V (&f)[S * v], const V (&b)[S * v], const V (&c)[S],
+                                        V (&F)[S], V (&B)[S], V (&busy)[S]) {
+  constexpr int NV = S * v;
+#pragma unroll
+  for (int u = 0; u < NV; ++u) {
+    V nF[S], nB[S];
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+      const int W = 2 * (S - 1 - s) + (v - 1) * S;
+      const int jf = ((u - s) % NV + NV) % NV / S, vf = jf * S + s;
+      const int jb = v - 1 - ((u - s - W) % NV + NV) % NV / S, vb = jb * S + s;
+      V x = busy[s];
+      const V rf = s > 0 ? F[s - 1] + c[s - 1] : jf > 0 ? F[S - 1] + c[S - 1] : (V)0;
+      V ef = vmax(x, rf) + f[vf];
+      if (kPred) {
+        const bool a = (unsigned)(t0 + u - s) < (unsigned)n;
+        ef = a ? ef : F[s];
+        x = a ? ef : x;
+      } else {
+        x = ef;
+      }
+      nF[s] = ef;
+      const V rb = vb == NV - 1 ? ef : s < S - 1 ? B[s + 1] + c[s] : B[0] + c[S - 1];
+      V eb = vmax(x, rb) + b[vb];
+      if (kPred) {
+        const bool a = (unsigned)(t0 + u - s - W) < (unsigned)n;
+        eb = a ? eb : B[s];
+        x = a ? eb : x;
+      } else {
+        x = eb;
+      }
+      nB[s] = eb;
+      busy[s] = x;
+    }
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+      F[s] = nF[s];
+      B[s] = nB[s];
+    }
+  }
+}
+
+// The whole schedule; busy[s] = end of device s's last op.  kJump: a trip
+// in the steady part maps the state (F, B; busy = B there) to a max of
+// (component + constant) terms, so once a steady trip advances every
+// component by one constant lam the later steady trips do too, and they are
+// taken in one step (the argument of the plain pipeline's shortcut).
+template <int S, int v, typename V, bool kJump>
+__device__ __forceinline__ void il_pipe(const V (&f)[S * v], const V (&b)[S * v], const V (&c)[S], uint32_t M,
+                                        V (&busy)[S], int& skipped) {
+  constexpr int NV = S * v, W0 = 2 * (S - 1) + (v - 1) * S;
+  const int n = (int)M * v, steps = n + W0;
+  V F[S], B[S], pF[S], pB[S];
+#pragma unroll
+  for (int s = 0; s < S; ++s) F[s] = B[s] = busy[s] = pF[s] = pB[s] = 0;
+  skipped = 0;
+  bool prev_steady = false;
+  for (int t0 = 0; t0 < steps; t0 += NV) {
+    if (t0 >= W0 && t0 + NV <= n) {
+      if (kJump) {
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+          pF[s] = F[s];
+          pB[s] = B[s];
+        }
+      }
+      il_trip<S, v, V, false>(t0, n, f, b, c, F, B, busy);
+      if (kJump && prev_steady) {
+        const V lam = B[0] - pB[0];
+        bool same = true;
+#pragma unroll
+        for (int s = 0; s < S; ++s) same = same && F[s] - pF[s] == lam && B[s] - pB[s] == lam;
+        const int r = (n - (t0 + NV)) / NV;
+        if (same && r > 0) {
+          const V k = (V)r * lam;
+#pragma unroll
+          for (int s = 0; s < S; ++s) {
+            F[s] += k;
+            B[s] += k;
+            busy[s] += k;
+          }
+          t0 += r * NV;
+          skipped += r;
+        }
+      }
+      prev_steady = true;
+    } else {
+      il_trip<S, v, V, true>(t0, n, f, b, c, F, B, busy);
+      prev_steady = false;
+    }
+  }
+}
+
+// Layers on device s: the sum over its chunks.
+template <int S, int v>
+__device__ __forceinline__ uint32_t il_device_ns(const Plan& p, int s) {
+  uint32_t ns = 0;
+#pragma unroll
+  for (int j = 0; j < v; ++j) {
+    const int vs = j * S + s;
+    ns += cut_at(p, vs) - (vs ? cut_at(p, vs - 1) : 0);
+  }
+  return ns;
+}
+
+// The iteration time of one interleaved pipeline: the latest device end
+// plus that device's DP sync over the parameters of all its chunks.
+template <int S, int v, int kMode, typename V>
+__device__ __forceinline__ V il_tail(const Tab& t, const Hot<kMode>& h, const Plan& p, const V (&busy)[S]) {
+  const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> p.epl);
+  V T = 0;
+#pragma unroll
+  for (int s = 0; s < S; ++s) T = vmax(T, busy[s] + (V)stage_dp(t, h, p, s, il_device_ns<S, v>(p, s), rp, rpe));
+  return T;
+}
+
+template <int S, int v, int kMode, typename V, bool kJump>
+__device__ __forceinline__ V il_time(const Tab& t, const Hot<kMode>& h, const Plan& p, int& skipped) {
+  V f[S * v], b[S * v], c[S], busy[S];
+  il_setup<S, v, kMode, V>(t, h, p, f, b, c);
+  il_pipe<S, v, V, kJump>(f, b, c, class_mb(p), busy, skipped);
+  return il_tail<S, v, kMode, V>(t, h, p, busy);
+}
+
+// Stage records of an interleaved pipeline: {forward, backward, hop, sync}
+// per virtual stage; hop and sync only in the first S records (per device).
+template <int S, int v>
+__device__ __forceinline__ void il_records(const Tab& t, const Hot<2>& h, const Plan& p, uint64_t* o) {
+  uint64_t f[S * v], b[S * v], c[S];
+  il_setup<S, v, 2, uint64_t>(t, h, p, f, b, c);
+  const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> p.epl);
+#pragma unroll
+  for (int vs = 0; vs < S * v; ++vs) {
+    o[vs * kRecWords + 0] = f[vs];
+    o[vs * kRecWords + 1] = b[vs];
+    o[vs * kRecWords + 2] = vs < S ? c[vs < S ? vs : 0] : 0;
+    o[vs * kRecWords + 3] = vs < S ? stage_dp(t, h, p, vs, il_device_ns<S, v>(p, vs < S ? vs : 0), rp, rpe) : 0;
+  }
+}
+
+template <int S, int v, int kMode>
+__device__ __forceinline__ void eval_il(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot) {
+  double busy[S];
+  int skipped;
+  {
+    double f[S * v], b[S * v], c[S];
+    uint32_t M;
+    {
+      const Plan p = load_plan<false>(e.packed, e.pcut, slot);
+      il_setup<S, v, kMode, double>(t, h, p, f, b, c);
+      M = class_mb(p);
+    }
+    il_pipe<S, v, double, true>(f, b, c, M, busy, skipped);
+  }
+  // the tail reads the plan again (as eval_one does) rather than keeping it
+  // in registers through the recurrence
+  const uint32_t slot2 = __shfl(slot, (int)(threadIdx.x & 63u));
+  const double T = il_tail<S, v, kMode, double>(t, h, load_plan<false>(e.packed, e.pcut, slot2), busy);
+  if (T < kExact) atomicMax((unsigned long long*)&e.out[slot >> 2], (unsigned long long)T);
+  else e.ovf[atomicAdd(&e.ctr[0], 1u)] = slot;
+}
+
 // Blocks of four waves share one LDS copy of the table image.
 constexpr uint32_t kEvalThreads = 256;
 
@@ -1357,19 +1736,56 @@ __global__ void __launch_bounds__(kEvalThreads) k_eval(Tab t, EvalBufs e) {
   }
 }
 
+// Interleaved pipelines (shared layout) of one 64-pipeline tile starting at
+// sorted id `base` (ids below hi): one pass per (S, v) present in the tile.
+template <int kMode>
+__device__ __forceinline__ void il_tile(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t base,
+                                        uint32_t hi) {
+  const uint32_t pos = base + (threadIdx.x & 63u);
+  bool pending = pos < hi;
+  const uint32_t slot = pending ? e.ids[pos] : 0;
+  const uint32_t m = pending ? e.meta[slot] : 0;
+  const uint32_t key = il_shape(m & 31, (m >> 24) + 1);
+  while (true) {
+    const uint64_t live = __ballot(pending);
+    if (!live) break;
+    const uint32_t k0 = __builtin_amdgcn_readfirstlane(__shfl(key, __ffsll((unsigned long long)live) - 1));
+    if (pending && key == k0) {
+      switch (k0) {
+#define X(S_, V_)                          \
+  case S_ | (V_ - 1) << 5:                 \
+    eval_il<S_, V_, kMode>(t, h, e, slot); \
+    break;
+        HETSIM_IL_SHAPES(X)
+#undef X
+        default: break;
+      }
+      pending = false;
+    }
+  }
+}
+
 // Deferred pipelines of every stage count in one launch, so that the long
-// serial chains of the different stage counts overlap.  Deferred S-stage
-// pipelines sit at [sstart[16 - S], + ctr[1 + 16 - S]); tile q of 64 is
-// located by walking the sixteen list lengths (16 stages first), and tiles
-// are dealt round-robin to the waves of the grid.
+// serial chains of the different stage counts overlap.  Tiles of 64 are
+// dealt round-robin to the waves of the grid: first the interleaved
+// pipelines (shared layout; sorted ids [sstart[16], sstart[16 + 21]), so a
+// tile mostly holds one (S, v) and one micro-batch count), then the
+// deferred S-stage pipelines at [sstart[16 - S], + ctr[1 + 16 - S]), tile q
+// located by walking the sixteen list lengths (16 stages first).
 template <int kMode, bool kHet>
 __global__ void __launch_bounds__(kEvalThreads) k_deferred(Tab t, EvalBufs e) {
   extern __shared__ uint4 lds[];
   fill_lds<kMode>(t, lds);
   const Hot<kMode> h(t, lds);
   const uint32_t waves = gridDim.x * (kEvalThreads / 64);
+  const uint32_t il_lo = kHet ? 0 : e.sstart[kMaxStages], il_hi = kHet ? 0 : e.sstart[kMaxStages + kIlGroups];
+  const uint32_t il_tiles = (il_hi - il_lo + 63) >> 6;
   for (uint32_t q = blockIdx.x * (kEvalThreads / 64) + (threadIdx.x >> 6);; q += waves) {
-    uint32_t j = 0, before = 0, nt = 0;
+    if (!kHet && q < il_tiles) {
+      il_tile<kMode>(t, h, e, il_lo + q * 64u, il_hi);
+      continue;
+    }
+    uint32_t j = 0, before = il_tiles, nt = 0;
     for (; j < kMaxStages; ++j) {
       nt = (e.ctr[1 + j] + 63) >> 6;
       if (q < before + nt) break;
@@ -1425,8 +1841,23 @@ __global__ void __launch_bounds__(64) k_redo_u64(Tab t, EvalBufs e) {
     const uint32_t slot = e.ovf[j];
     const Plan p = load_plan<kHet>(e.packed, e.pcut, slot);
     const uint32_t S = p.S, M = class_mb(p);
-    StageRec R;
     const Hot<2> h(t, nullptr);
+    if (!kHet && p.v > 1) {
+      uint64_t r = 0;
+      int skipped;
+      switch (il_shape(S, p.v)) {
+#define X(S_, V_)                                                    \
+  case S_ | (V_ - 1) << 5:                                           \
+    r = il_time<S_, V_, 2, uint64_t, false>(t, h, p, skipped);       \
+    break;
+        HETSIM_IL_SHAPES(X)
+#undef X
+        default: break;
+      }
+      atomicMax((unsigned long long*)&e.out[slot >> 2], (unsigned long long)r);
+      continue;
+    }
+    StageRec R;
     RecSink sink{R};
     class_setup<2, kHet>(t, h, p, slot & 3, sink, kHet ? e.pcut + (slot & ~3u) : nullptr);
     uint64_t r;
@@ -1534,9 +1965,10 @@ hipError_t launch_fill32(uint32_t* p, uint32_t n, uint32_t v, hipStream_t s) {
   return hipGetLastError();
 }
 hipError_t launch_prep(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, PackedPlan* packed, uint4* pcut,
-                       uint32_t* meta, uint32_t* hist, hipStream_t s) {
-  if (p.chdr) k_prep<true><<<blocks_for(n, 256 * kPrepPerThread), 256, 0, s>>>(t, p, n, out, packed, pcut, meta, hist);
-  else k_prep<false><<<blocks_for(n, 256 * kPrepPerThread), 256, 0, s>>>(t, p, n, out, packed, pcut, meta, hist);
+                       uint32_t* meta, uint32_t* hist, uint16_t* keys, hipStream_t s) {
+  const int g = blocks_for(n, 256 * kPrepPerThread);
+  if (p.chdr) k_prep<true><<<g, 256, 0, s>>>(t, p, n, out, packed, pcut, meta, hist, keys);
+  else k_prep<false><<<g, 256, 0, s>>>(t, p, n, out, packed, pcut, meta, hist, keys);
   return hipGetLastError();
 }
 hipError_t launch_memory(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, hipStream_t s) {
@@ -1565,8 +1997,8 @@ hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* sstart,
   k_scan<<<1, 1024, 0, s>>>(hist, cursor, sstart);
   return hipGetLastError();
 }
-hipError_t launch_scatter(const uint32_t* meta, uint32_t nslots, uint32_t* cursor, uint32_t* ids, hipStream_t s) {
-  k_scatter<<<blocks_for(nslots, 256 * kScatterPer), 256, 0, s>>>(meta, nslots, cursor, ids);
+hipError_t launch_scatter(const uint16_t* keys, uint32_t nslots, uint32_t* cursor, uint32_t* ids, hipStream_t s) {
+  k_scatter<<<blocks_for(nslots, 256 * kScatterPer), 256, 0, s>>>(keys, nslots, cursor, ids);
   return hipGetLastError();
 }
 template <int kMode, bool kHet>
@@ -1655,12 +2087,13 @@ hipError_t launch_first(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hip
   return hipGetLastError();
 }
 
-// then the deferred pipelines and the u64 redo of the overflowed ones
+// then the interleaved and the deferred pipelines, and the u64 redo of the
+// overflowed ones
 template <bool kHet>
 static void launch_deferred_het(const Tab& t, const EvalBufs& e, uint32_t max_tasks, hipStream_t s) {
   int g = blocks_for(max_tasks, kEvalThreads);
-  g = g < 1 ? 1 : (g > (int)t.grid_deferred ? (int)t.grid_deferred : g);
   const size_t lds = t.mode < 2 ? t.lds_bytes : 0;
+  g = g < 1 ? 1 : (g > (int)t.grid_deferred ? (int)t.grid_deferred : g);
   if (t.mode == 0) k_deferred<0, kHet><<<g, kEvalThreads, lds, s>>>(t, e);
   else if (t.mode == 1) k_deferred<1, kHet><<<g, kEvalThreads, lds, s>>>(t, e);
   else k_deferred<2, kHet><<<g, kEvalThreads, 0, s>>>(t, e);

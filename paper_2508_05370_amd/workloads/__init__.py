@@ -246,16 +246,12 @@ def random_plans_het(m, c, seed, first, n, nthreads=None):
     return p
 
 
-def interleaved_plans(w, first=0, n=None, nthreads=None):
-    """Interleaved-1F1B plans of workload w (its own seed + 0x200; see plangen.c): v = 2..4 model
-    chunks per device, S devices with S*v <= 16, every class's micro-batches per replica a
-    multiple of S and at least 2S."""
-    if n is None:
-        n = w["n_plans"] - first
-    m, c = w["model"], w["cluster"]
+def random_plans_il(m, c, seed, first, n, nthreads=None):
+    """Interleaved-1F1B plans (see plangen.c): v = 2..4 model chunks per device, S devices with
+    S*v <= 16, every class's micro-batches per replica a multiple of S and at least 2S."""
     L = _load()
     P = _Params()
-    P.seed = (w["seed"] if w["seed"] is not None else 0x91A70001) + 0x200
+    P.seed = seed
     P.L = m["L"]
     P.K = len(c["types"])
     for k, t in enumerate(c["types"]):
@@ -268,6 +264,14 @@ def interleaved_plans(w, first=0, n=None, nthreads=None):
     L.plangen_random_interleaved(C.byref(P), first, n, p["hdr"].ctypes.data, p["cut"].ctypes.data,
                                  p["cls"].ctypes.data, p["types"].ctypes.data, n, nthreads)
     return p
+
+
+def interleaved_plans(w, first=0, n=None, nthreads=None):
+    """Interleaved plans of workload w (its own seed + 0x200)."""
+    if n is None:
+        n = w["n_plans"] - first
+    seed = (w["seed"] if w["seed"] is not None else 0x91A70001) + 0x200
+    return random_plans_il(w["model"], w["cluster"], seed, first, n, nthreads)
 
 
 def as_per_class(p):

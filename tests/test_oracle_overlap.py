@@ -113,5 +113,5 @@ def test_overlap_needs_the_shared_layout(oracle_mod, workloads):
     q = _plan(1)
     _set(q, 0, (12,), ((4, 8, 0x0),), overlap=1)
     assert o.eval(q)[0] != MAXU
-    q["hdr"][0] |= np.uint32(1 << 14)                         # reserved
+    q["hdr"][0] |= np.uint32(1 << 14)                         # v = 2: no interleaving with overlap
     assert o.eval(q)[0] == MAXU
