@@ -170,3 +170,78 @@ def simulate_interleaved(S, v, M, f, b, c, cw):
     for s in range(S):
         assert nxt[s] == len(lists[s]), "simulation stalled"
     return idle_at
+
+
+# ---------------------------------------------------------------------------
+# Zero-bubble order (ZB-H1, Qi et al. 2024): the backward pass splits into B
+# (input gradient, sent upstream) and W (weight gradient, local).
+
+
+def zb_op_list(S, M, s):
+    """Stage s's ops: the 1F1B order of forwards and input-gradient passes, with each weight-
+    gradient pass queued behind its B and released s micro-batches later; the queue empties
+    at the end."""
+    warm = min(S - 1 - s, M)
+    ops = [("F", m) for m in range(warm)]
+    queue = []
+    f_next = warm
+    for i in range(M):
+        if f_next < M:
+            ops.append(("F", f_next))
+            f_next += 1
+        ops.append(("B", i))
+        queue.append(i)
+        if len(queue) > s:
+            ops.append(("W", queue.pop(0)))
+    ops += [("W", m) for m in queue]
+    return ops
+
+
+def simulate_zb(S, M, f, bi, w, c):
+    """Event-driven replay; f, bi, w per stage, c[s] the hop between stages s and s+1.  Returns
+    the end time of each stage's last op."""
+    lists = [zb_op_list(S, M, s) for s in range(S)]
+    nxt = [0] * S
+    busy = [False] * S
+    idle_at = [0] * S
+    arrived = {("F", 0, m) for m in range(M)}
+    events = []
+    seq = 0
+
+    def push(t, kind, data):
+        nonlocal seq
+        heapq.heappush(events, (t, seq, kind, data))
+        seq += 1
+
+    def try_start(s, now):
+        if busy[s] or nxt[s] >= len(lists[s]):
+            return
+        kind, m = lists[s][nxt[s]]
+        if kind != "W" and (kind, s, m) not in arrived:
+            return
+        busy[s] = True
+        push(now + {"F": f, "B": bi, "W": w}[kind][s], "done", (s, kind, m))
+
+    for s in range(S):
+        try_start(s, 0)
+    while events:
+        now, _, kind, data = heapq.heappop(events)
+        if kind == "done":
+            s, k, m = data
+            busy[s] = False
+            idle_at[s] = now
+            nxt[s] += 1
+            if k == "F":
+                if s + 1 < S:
+                    push(now + c[s], "arrive", ("F", s + 1, m))
+                else:
+                    arrived.add(("B", s, m))
+            elif k == "B" and s > 0:
+                push(now + c[s - 1], "arrive", ("B", s - 1, m))
+            try_start(s, now)
+        else:
+            arrived.add(data)
+            try_start(data[1], now)
+    for s in range(S):
+        assert nxt[s] == len(lists[s]), "simulation stalled"
+    return idle_at

@@ -388,6 +388,7 @@ typedef struct {
   uint64_t ep, G, zero, mi;
   uint64_t overlap;      /* 1: gradient sync overlapped with the last backward pass (R38) */
   uint64_t v;            /* model chunks per device: 1 = plain 1F1B, 2..4 interleaved (R41) */
+  uint64_t zb;           /* 1: backward split into input and weight gradients, zero-bubble order (R44) */
   uint64_t tp[OR_MAXG], S[OR_MAXG];
   uint64_t cut[OR_MAXG][OR_MAXS];
   uint64_t reps[OR_MAXG], nmb[OR_MAXG];
@@ -403,6 +404,7 @@ typedef struct {
   uint64_t S[OR_MAXG];
   uint64_t M[OR_MAXG];
   uint64_t f[OR_MAXG][OR_MAXS], b[OR_MAXG][OR_MAXS], c[OR_MAXG][OR_MAXS];
+  uint64_t w[OR_MAXG][OR_MAXS];   /* zero-bubble order: the weight-gradient part of b */
   uint64_t tdp[OR_MAXG][OR_MAXS];
   uint64_t end[OR_MAXG][OR_MAXS];
   uint64_t time;
@@ -430,9 +432,11 @@ static int decode_rules(const or_ctx* x, const or_planes* q, int64_t i, or_plan*
   const or_model* m = &x->m;
   const int64_t stride = q->stride;
   const uint32_t hdr = q->hdr[i];
-  if (hdr >> 16) return 0;                                   /* V7 reserved bits */
+  if (hdr >> 17) return 0;                                   /* V7 reserved bits */
   p->overlap = (hdr >> 13) & 1;
   p->v = ((hdr >> 14) & 3) + 1;
+  p->zb = (hdr >> 16) & 1;
+  if (p->zb && (p->overlap || p->v > 1)) return 0;           /* V13 (R45) */
   p->ep = 1ull << ((hdr >> 2) & 3);
   p->G = ((hdr >> 8) & 3) + 1;
   p->zero = (hdr >> 10) & 1;
@@ -442,6 +446,7 @@ static int decode_rules(const or_ctx* x, const or_planes* q, int64_t i, or_plan*
     if (hdr & 0xf3) return 0;                                /* V10 the header's TP and PP are unused (0) */
     if (p->overlap) return 0;                                /* V11 overlap needs the shared layout */
     if (p->v > 1) return 0;                                  /* V12 interleaving needs the shared layout */
+    if (p->zb) return 0;                                     /* V13 so does the zero-bubble order */
     uint32_t w = q->chdr[i];
     for (uint64_t g = 0; g < p->G; ++g) {
       uint32_t bt = (w >> (8 * g)) & 0xff;
@@ -513,6 +518,25 @@ static uint64_t in_flight(uint64_t S, uint64_t M, uint64_t s) {
   return W + 1 < M ? W + 1 : M;
 }
 
+/* R46: micro-batches whose activations stage s holds at once under the
+ * zero-bubble order: a forward's activations stay until the micro-batch's
+ * weight-gradient pass (W) has run.  Counted by walking the stage's ops. */
+static void zb_ops(uint64_t S, uint64_t M, uint64_t s, char* kind, uint64_t* mb);
+static uint64_t in_flight_zb(uint64_t S, uint64_t M, uint64_t s) {
+  char* kind = (char*)malloc(3 * M + 1);
+  uint64_t* mb = (uint64_t*)malloc(8 * (3 * M + 1));
+  if (!kind || !mb) or_die("in_flight_zb: out of memory");
+  zb_ops(S, M, s, kind, mb);
+  uint64_t live = 0, peak = 0;
+  for (uint64_t j = 0; j < 3 * M; ++j) {
+    if (kind[j] == 'F') { ++live; if (live > peak) peak = live; }
+    if (kind[j] == 'W') --live;
+  }
+  free(kind);
+  free(mb);
+  return peak;
+}
+
 /* R41: the warm-up forwards of device s under interleaved 1F1B with S
  * devices, v chunks and M micro-batches. */
 static uint64_t interleaved_warmup(uint64_t S, uint64_t v, uint64_t M, uint64_t s) {
@@ -569,7 +593,8 @@ static uint64_t stage_mem(const or_ctx* x, const or_plan* p, uint64_t g, uint64_
   if (p->zero) opt = add(cdiv(mul(m->opt_bytes, pd), p_all), cdiv(mul(m->opt_bytes, pe), p_all / ep));
   else opt = mul(m->opt_bytes, add(pd, pe));
   uint64_t M = cdiv(p->nmb[g], p->reps[g]);
-  uint64_t act = mul(mul(ns, layer_act_bytes(x, tp, m->mbs[p->mi])), in_flight(p->S[g], M, s));
+  uint64_t fly = p->zb ? in_flight_zb(p->S[g], M, s) : in_flight(p->S[g], M, s);
+  uint64_t act = mul(mul(ns, layer_act_bytes(x, tp, m->mbs[p->mi])), fly);
   return add(add(wg, opt), act);
 }
 
@@ -633,7 +658,7 @@ static void place(const or_plan* p, uint64_t base[OR_MAXG][OR_MAXS]) {
  * `last`, the TP all-reduces exposed in forward (Table 1, R22) and the MoE
  * all-to-all in both passes (R20). */
 static void stage_compute(const or_ctx* x, const or_plan* p, uint64_t g, int k, uint64_t base, uint64_t lo,
-                          uint64_t hi, int first, int last, uint64_t* F, uint64_t* B) {
+                          uint64_t hi, int first, int last, uint64_t* F, uint64_t* B, uint64_t* Wg) {
   const or_model* m = &x->m;
   const or_cluster* cl = &x->c;
   uint64_t ep = p->ep, epl = log2u(ep), tp = p->tp[g], tpl = log2u(tp);
@@ -676,6 +701,7 @@ static void stage_compute(const or_ctx* x, const or_plan* p, uint64_t g, int k, 
   }
   *F = add(add(Fc, tpf), epc);
   *B = add(Bc, epc);
+  if (Wg) *Wg = Bc / 2;                                        /* R44: the weight-gradient half of the compute */
 }
 
 /* PP hop between class g's stage on pool k (devices from b1 on) and its
@@ -734,6 +760,83 @@ static void dp_link(const or_ctx* x, const or_plan* p, uint64_t base[OR_MAXG][OR
 
 static void eval_plan_interleaved(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t* scratch);
 
+/* R44-R46: zero-bubble order (ZB-H1 of Qi et al. 2024, "Zero Bubble
+ * Pipeline Parallelism").  The backward pass of a stage splits into B, the
+ * gradient of its input (what stage s-1 waits for), and W, the gradient of
+ * its weights (needed by nobody downstream).  Stage s runs min(S-1-s, M)
+ * warm-up forwards, then for i = 0..M-1: the next forward if any is left,
+ * B(i), and W(i-s) once i >= s; then its last min(s, M) W passes.  So W of
+ * stage s trails its B by s micro-batches, which fills the cool-down and
+ * keeps at most S micro-batches' activations on any stage. */
+static void zb_ops(uint64_t S, uint64_t M, uint64_t s, char* kind, uint64_t* mb) {
+  uint64_t Wu = (S - 1 - s) < M ? (S - 1 - s) : M, n = 0, nextF = 0, nextW = 0;
+  for (; nextF < Wu; ++nextF) { kind[n] = 'F'; mb[n++] = nextF; }
+  for (uint64_t i = 0; i < M; ++i) {
+    if (nextF < M) { kind[n] = 'F'; mb[n++] = nextF++; }
+    kind[n] = 'B'; mb[n++] = i;
+    if (i >= s) { kind[n] = 'W'; mb[n++] = nextW++; }
+  }
+  while (nextW < M) { kind[n] = 'W'; mb[n++] = nextW++; }
+}
+
+/* end[s] := end of stage s's last op; bi, w: B and W durations per stage.
+ * F and B wait as in 1F1B; W(s,m) needs B(s,m), which precedes it on the
+ * stage.  scratch holds 2 S M words. */
+static void pipeline_zb(uint64_t S, uint64_t M, const uint64_t* f, const uint64_t* bi, const uint64_t* w,
+                        const uint64_t* c, uint64_t* end, uint64_t* scratch) {
+  char* kind[OR_MAXS];
+  uint64_t* mb[OR_MAXS];
+  for (uint64_t s = 0; s < S; ++s) {
+    kind[s] = (char*)malloc(3 * M + 1);
+    mb[s] = (uint64_t*)malloc(8 * (3 * M + 1));
+    if (!kind[s] || !mb[s]) or_die("pipeline_zb: out of memory");
+  }
+  uint64_t* endF = scratch;
+  uint64_t* endB = scratch + S * M;
+  for (uint64_t i = 0; i < 2 * S * M; ++i) scratch[i] = OR_INVALID;
+  uint64_t pos[OR_MAXS], last[OR_MAXS];
+  for (uint64_t s = 0; s < S; ++s) { pos[s] = 0; last[s] = 0; zb_ops(S, M, s, kind[s], mb[s]); }
+  int progress = 1;
+  while (progress) {
+    progress = 0;
+    for (uint64_t s = 0; s < S; ++s) {
+      while (pos[s] < 3 * M) {
+        char k = kind[s][pos[s]];
+        uint64_t m = mb[s][pos[s]], ready, dur;
+        if (k == 'F') {
+          if (s == 0) ready = 0;
+          else if (endF[(s - 1) * M + m] == OR_INVALID) break;
+          else ready = add(endF[(s - 1) * M + m], c[s - 1]);
+          dur = f[s];
+        } else if (k == 'B') {
+          if (s == S - 1) {
+            if (endF[s * M + m] == OR_INVALID) break;
+            ready = endF[s * M + m];
+          } else if (endB[(s + 1) * M + m] == OR_INVALID) break;
+          else ready = add(endB[(s + 1) * M + m], c[s]);
+          dur = bi[s];
+        } else {
+          if (endB[s * M + m] == OR_INVALID) or_die("pipeline_zb: W before its B");
+          ready = endB[s * M + m];
+          dur = w[s];
+        }
+        uint64_t e = add(umax(last[s], ready), dur);
+        if (k == 'F') endF[s * M + m] = e;
+        else if (k == 'B') endB[s * M + m] = e;
+        last[s] = e;
+        pos[s]++;
+        progress = 1;
+      }
+    }
+  }
+  for (uint64_t s = 0; s < S; ++s) {
+    if (pos[s] != 3 * M) or_die("pipeline_zb: deadlock");
+    end[s] = last[s];
+    free(kind[s]);
+    free(mb[s]);
+  }
+}
+
 static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t* scratch) {
   if (p->v > 1) { eval_plan_interleaved(x, p, d, scratch); return; }
   const or_model* m = &x->m;
@@ -750,7 +853,7 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
     for (uint64_t s = 0; s < S; ++s) {
       int k = p->type[g][s];
       uint64_t lo = s ? p->cut[g][s - 1] : 0, hi = p->cut[g][s];
-      stage_compute(x, p, g, k, base[g][s], lo, hi, s == 0, s == S - 1, &d->f[g][s], &d->b[g][s]);
+      stage_compute(x, p, g, k, base[g][s], lo, hi, s == 0, s == S - 1, &d->f[g][s], &d->b[g][s], &d->w[g][s]);
       d->c[g][s] = s + 1 < S ? hop_cost(x, p, g, k, base[g][s], p->type[g][s + 1], base[g][s + 1]) : 0;
     }
   }
@@ -814,7 +917,13 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
    * has finished, so T = max over classes and stages (R27, R28) */
   uint64_t T_iter = 0;
   for (uint64_t g = 0; g < G; ++g) {
-    pipeline(p->S[g], d->M[g], d->f[g], d->b[g], d->c[g], d->end[g], scratch);
+    if (p->zb) {
+      uint64_t bi[OR_MAXS];
+      for (uint64_t s = 0; s < p->S[g]; ++s) bi[s] = d->b[g][s] - d->w[g][s];
+      pipeline_zb(p->S[g], d->M[g], d->f[g], bi, d->w[g], d->c[g], d->end[g], scratch);
+    } else {
+      pipeline(p->S[g], d->M[g], d->f[g], d->b[g], d->c[g], d->end[g], scratch);
+    }
     if (!p->overlap)
       for (uint64_t s = 0; s < p->S[g]; ++s) T_iter = umax(T_iter, add(d->end[g][s], d->tdp[g][s]));
   }
@@ -938,7 +1047,8 @@ static void eval_plan_interleaved(const or_ctx* x, const or_plan* p, or_detail* 
     for (uint64_t vs = 0; vs < V; ++vs) {
       uint64_t s = vs % S;
       uint64_t lo = vs ? p->cut[g][vs - 1] : 0, hi = p->cut[g][vs];
-      stage_compute(x, p, g, p->type[g][s], base[g][s], lo, hi, vs == 0, vs == V - 1, &d->f[g][vs], &d->b[g][vs]);
+      stage_compute(x, p, g, p->type[g][s], base[g][s], lo, hi, vs == 0, vs == V - 1, &d->f[g][vs], &d->b[g][vs],
+                    NULL);
     }
     for (uint64_t s = 0; s < S; ++s) {
       uint64_t s2 = s + 1 < S ? s + 1 : 0;
@@ -1146,6 +1256,13 @@ uint64_t oracle_rank_params(const or_ctx* x, uint64_t t, uint64_t ep, uint64_t n
 uint64_t oracle_act_bytes(const or_ctx* x, uint64_t b) { return b * x->m.seq * x->m.h * x->m.e; }
 uint64_t oracle_layer_act_bytes(const or_ctx* x, uint64_t t, uint64_t b) { return layer_act_bytes(x, t, b); }
 uint64_t oracle_in_flight(uint64_t S, uint64_t M, uint64_t s) { return in_flight(S, M, s); }
+uint64_t oracle_in_flight_zb(uint64_t S, uint64_t M, uint64_t s) { return in_flight_zb(S, M, s); }
+void oracle_pipeline_zb(uint64_t S, uint64_t M, const uint64_t* f, const uint64_t* bi, const uint64_t* w,
+                        const uint64_t* c, uint64_t* end) {
+  uint64_t* scratch = (uint64_t*)malloc(8 * 2 * S * M + 8);
+  pipeline_zb(S, M, f, bi, w, c, end, scratch);
+  free(scratch);
+}
 /* Peak memory of every (class, stage) device of plan i into mem[c*16 + s]
  * (entries of absent classes and stages 0).  Returns 0 if the plan breaks
  * a rule other than the memory check (mem then all 0), else 1. */

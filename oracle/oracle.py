@@ -23,6 +23,7 @@ class _Detail(C.Structure):
                 ("f", (C.c_uint64 * OR_MAXS) * OR_MAXG),
                 ("b", (C.c_uint64 * OR_MAXS) * OR_MAXG),
                 ("c", (C.c_uint64 * OR_MAXS) * OR_MAXG),
+                ("w", (C.c_uint64 * OR_MAXS) * OR_MAXG),
                 ("tdp", (C.c_uint64 * OR_MAXS) * OR_MAXG),
                 ("end", (C.c_uint64 * OR_MAXS) * OR_MAXG),
                 ("time", C.c_uint64)]
@@ -69,6 +70,9 @@ def lib():
         L.oracle_layer_act_bytes.restype = u64
         L.oracle_in_flight.argtypes = [u64, u64, u64]
         L.oracle_in_flight.restype = u64
+        L.oracle_in_flight_zb.argtypes = [u64, u64, u64]
+        L.oracle_in_flight_zb.restype = u64
+        L.oracle_pipeline_zb.argtypes = [u64, u64, P, P, P, P, P]
         L.oracle_stage_mem.argtypes = [P, P, P, P, P, P, P, C.c_int64, C.c_int64, P]
         L.oracle_stage_mem.restype = C.c_int
         assert L.oracle_detail_size() == C.sizeof(_Detail)
@@ -166,6 +170,7 @@ class Oracle:
             "f": [[d.f[g][s] for s in range(S[g])] for g in range(G)],
             "b": [[d.b[g][s] for s in range(S[g])] for g in range(G)],
             "c": [[d.c[g][s] for s in range(S[g])] for g in range(G)],
+            "w": [[d.w[g][s] for s in range(S[g])] for g in range(G)],
             "tdp": [[d.tdp[g][s] for s in range(S[g])] for g in range(G)],
             "end": [[d.end[g][s] for s in range(S[g])] for g in range(G)],
             "time": d.time,
@@ -225,6 +230,20 @@ def pipeline_interleaved(S, v, M, f, b, c, cw):
 
 def in_flight(S, M, s):
     return lib().oracle_in_flight(S, M, s)
+
+
+def in_flight_zb(S, M, s):
+    return lib().oracle_in_flight_zb(S, M, s)
+
+
+def pipeline_zb(S, M, f, bi, w, c):
+    """End time of each stage's last op under the zero-bubble order: f, bi (input-gradient part
+    of the backward) and w (weight-gradient part) per stage; c has S-1 hops."""
+    arrs = [np.array(x, dtype=np.uint64) for x in (f, bi, w)]
+    ca = np.array(list(c) + [0], dtype=np.uint64)
+    end = np.zeros(S, dtype=np.uint64)
+    lib().oracle_pipeline_zb(S, M, *[_ptr(a) for a in arrs], _ptr(ca), _ptr(end))
+    return [int(x) for x in end]
 
 
 def alpha_ps(gbps_unidir):
