@@ -106,6 +106,8 @@ def main():
                     help="also time the same plans with per-type device memory checked (0 = skip)")
     ap.add_argument("--overlap-steps", type=int, default=5,
                     help="also time the same plans with the gradient sync overlapped with the last backward (0 = skip)")
+    ap.add_argument("--zb-steps", type=int, default=3,
+                    help="also time the same plans in the zero-bubble pipeline order (0 = skip)")
     ap.add_argument("--il-steps", type=int, default=3,
                     help="also time as many interleaved-1F1B plans of the workload (0 = skip)")
     ap.add_argument("--layout-steps", type=int, default=5,
@@ -291,6 +293,25 @@ def main():
                "valid_plans": int(np.count_nonzero(B.times_u64(out) != MAXU)), "argmin": [hb_i, hb_t]}
         del dh
 
+    # The same plans in the zero-bubble order (backward split into input and weight gradients)
+    zb = None
+    if a.zb_steps > 0 and not a.chunk:
+        dz = dict(dp, hdr=dp["hdr"] | (1 << 16))
+        sim.eval_plans(dz, out=out)
+        sim.argmin(out, out=best)
+        torch.cuda.synchronize()
+        z0 = time.perf_counter()
+        for _ in range(a.zb_steps):
+            sim.eval_plans(dz, out=out)
+            sim.argmin(out, out=best)
+        torch.cuda.synchronize()
+        z1 = time.perf_counter()
+        zb_t, zb_i = B.best_tuple(best)
+        zb = {"workload": w["name"] + "/zero-bubble", "plans_per_s": round(n * a.zb_steps / (z1 - z0), 1),
+              "steps": a.zb_steps, "ms_per_step": round((z1 - z0) / a.zb_steps * 1e3, 4),
+              "argmin": [zb_i, zb_t]}
+        del dz
+
     # Interleaved 1F1B plans (v model chunks per device) of the same workload
     il = None
     if a.il_steps > 0 and not a.chunk:
@@ -350,6 +371,7 @@ def main():
     rec["dp_overlap"] = ovl
     rec["per_class_layout"] = lay
     rec["interleaved"] = il
+    rec["zero_bubble"] = zb
     print(json.dumps(rec), flush=True)
 
 

@@ -118,7 +118,16 @@ typedef struct {
  *                       (shared layout only, no overlap, PP >= 2,
  *                       PP*v <= 16, micro-batches per replica of every
  *                       class a multiple of PP and at least 2 PP),
- *                       16-31 zero
+ *                       16 zero-bubble order (ZB-H1, Qi et al. 2024): the
+ *                       backward pass splits into an input-gradient part
+ *                       (what the previous stage waits for) and a
+ *                       weight-gradient part, half of the backward compute
+ *                       rounded down; stage s runs 1F1B's order of forwards
+ *                       and input-gradient passes and each weight-gradient
+ *                       pass s micro-batches after its input-gradient pass,
+ *                       the last s at the end (shared layout only, with
+ *                       neither overlap nor interleaving),
+ *                       17-31 zero
  *   cut[s*stride+i]     u8, last layer (exclusive) of stage s: 1 <= cut[0] <
  *                       ... < cut[PP-1] = L (the non-uniform layer split);
  *                       interleaved: PP*v cuts, one per virtual stage
@@ -226,7 +235,9 @@ int sim_eval_stages(sim_ctx* ctx, const sim_plans* plans, int64_t n, uint64_t* o
  * inputs of its ops: the stored-activation count of Korthikanti et al.
  * 2022 without dropout masks and attention scores; routed MoE tokens
  * counted at the balanced top-k share) and min(PP - s, M) the micro-batches
- * stage s holds at once under 1F1B.  Interleaved plans: s is the device,
+ * stage s holds at once under 1F1B (min(PP, M) on every stage under the
+ * zero-bubble order, whose activations stay until the weight-gradient
+ * pass).  Interleaved plans: s is the device,
  * whose layers are those of all its chunks, and the activation term is
  * nmax * A * min(2 (PP-1-s) + (v-1) PP + 1, M v) with nmax the layers of the
  * device's largest chunk (its warm-up passes plus one, each counted at that

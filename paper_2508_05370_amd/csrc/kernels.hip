@@ -113,6 +113,7 @@ struct Plan {
   uint32_t tpl, epl, S, G, zero, mi, tp, ep, psum;
   uint32_t overlap;         // gradient sync overlapped with the last backward pass
   uint32_t v;               // model chunks per device: 1, or 2..4 for interleaved 1F1B
+  uint32_t zb;              // zero-bubble order: backward split into input and weight gradients
   uint64_t cut_lo, cut_hi;  // cut bytes of stages 0-7 and 8-15, eight per word (virtual stages when v > 1)
   uint32_t reps[4], nmb[4];
   uint64_t tv[4];           // stage types, nibbles past S cleared
@@ -153,6 +154,7 @@ __device__ __forceinline__ Plan unpack(const PackedPlan& q, uint32_t c = 0) {
   p.zero = (hdr >> 10) & 1; p.mi = (hdr >> 11) & 3; p.tp = 1u << p.tpl; p.ep = 1u << p.epl; p.psum = q.psum;
   p.overlap = (hdr >> 13) & 1;
   p.v = ((hdr >> 14) & 3) + 1;
+  p.zb = (hdr >> 16) & 1;
   p.chdr = q.pad0;
   const uint64_t* cw = reinterpret_cast<const uint64_t*>(q.cut);
   p.cut_lo = cw[0];
@@ -218,10 +220,12 @@ __device__ __forceinline__ Checked check_plan(const Tab& t, const sim_plans& pl,
   }
   const uint32_t epl = (hdr >> 2) & 3, G = ((hdr >> 8) & 3) + 1, mi = (hdr >> 11) & 3;
   const uint32_t ep = 1u << epl, v = ((hdr >> 14) & 3) + 1;
-  bool ok = (hdr >> 16) == 0 && mi < t.n_mbs && ((t.ep_ok >> epl) & 1);
+  bool ok = (hdr >> 17) == 0 && mi < t.n_mbs && ((t.ep_ok >> epl) & 1);
   // the per-class layout leaves the header's TP and PP fields unused (0) and
-  // has neither overlap nor interleaving
-  if (kHet) ok = ok && (hdr & 0xe0f3) == 0;
+  // has no overlap, interleaving or zero-bubble order
+  if (kHet) ok = ok && (hdr & 0x1e0f3) == 0;
+  // the zero-bubble order goes with neither overlap nor interleaving
+  if (!kHet && ((hdr >> 16) & 1)) ok = ok && (hdr & 0xe000) == 0;
   // interleaving: no overlap, at least two devices, at most 16 virtual stages
   if (!kHet && v > 1) {
     const uint32_t S0 = ((hdr >> 4) & 15) + 1;
@@ -328,12 +332,15 @@ __device__ __forceinline__ uint64_t class_state_bytes(const Tab& t, const Checke
 }
 
 // Peak bytes of the devices of stage s (ns layers) of class c: its state plus
-// the activations of the min(PP - s, M) micro-batches 1F1B keeps in flight there.
+// the activations of the min(PP - s, M) micro-batches 1F1B keeps in flight
+// there (min(PP, M) on every stage under the zero-bubble order, where a
+// micro-batch's activations stay until its weight-gradient pass).
 __device__ __forceinline__ uint64_t class_stage_bytes(const Tab& t, const Checked& r, uint32_t c, uint32_t s,
                                                       uint32_t ns, uint64_t state) {
   const uint32_t mi = (r.hdr >> 11) & 3, S = r.S[c];
   const uint32_t reps = r.cls[c] & 0xffff, M = ((r.cls[c] >> 16) + reps - 1) / reps;
-  const uint32_t fly = S - s < M ? S - s : M;
+  const uint32_t held = ((r.hdr >> 16) & 1) ? S : S - s;
+  const uint32_t fly = held < M ? held : M;
   return state + (uint64_t)ns * fly * t.act_layer[r.tpl[c]][mi];
 }
 
@@ -926,7 +933,7 @@ template <int kMode, bool kHet>
 __device__ __forceinline__ void stage_cost(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t k,
                                            const TypeInfo& ti, uint32_t base, uint32_t bq_in, uint32_t bq_nic,
                                            uint32_t lo, uint32_t hi, bool first, bool last, uint64_t& fc,
-                                           uint64_t& bc) {
+                                           uint64_t& bc, uint64_t& wc) {
   const uint32_t tp = p.tp, ep = p.ep, tpl = p.tpl, epl = p.epl, mi = p.mi, ns = hi - lo, dpl = ti.dpl;
   const uint64_t act = t.act[mi], act_tp = (act + tp - 1) >> tpl;
   const uint32_t L1 = t.L + 1, epq = t.E ? p.epl : 0;
@@ -951,6 +958,7 @@ __device__ __forceinline__ void stage_cost(const Tab& t, const Hot<kMode>& h, co
     fc += hd.x;
     bc += hd.y;
   }
+  wc = bc >> 1;  // weight-gradient half of the backward compute (zero-bubble order)
   if (tp > 1) {  // TP all-reduces of this stage, exposed in the forward pass
     const uint64_t steps = (uint64_t)(2 * ns + first) * 2 * (tp - 1);
     fc += steps * ti.a_intra + link_ps(steps * act_tp, bq_in);
@@ -1010,8 +1018,8 @@ __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, c
     TypeInfo ti;
     stage_place<kMode, kHet>(t, h, p, s, k, ti, base, bq_in, bq_nic);
     const uint32_t dpl = ti.dpl;
-    uint64_t fc, bc;
-    stage_cost<kMode, kHet>(t, h, p, k, ti, base, bq_in, bq_nic, lo, hi, s == 0, s == S - 1, fc, bc);
+    uint64_t fc, bc, wc;
+    stage_cost<kMode, kHet>(t, h, p, k, ti, base, bq_in, bq_nic, lo, hi, s == 0, s == S - 1, fc, bc, wc);
     uint64_t hop = 0;
     if (s > 0) {  // hop (s-1) -> s
       // same pool means the two ranges are adjacent: intra iff the pair spans one node
@@ -1039,22 +1047,25 @@ __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, c
         tdp = stage_sync(t, h, p, s, lo, hi, rp, rpe);
       }
     }
-    sink.put(s, fc, bc, hop, tdp);
+    sink.put(s, fc, bc, hop, tdp, wc);
     lo = hi;
   }
 }
 
 // Sinks of class_setup.  RecSink stores whole stage records in memory order
-// (the hop of the last stage is 0).
+// (the hop of the last stage is 0), and with `w` the weight-gradient parts.
 struct RecSink {
   static constexpr bool kDp = true;
   uint64_t (&rec)[kMaxStages][kRecWords];
-  __device__ __forceinline__ void put(uint32_t s, uint64_t fc, uint64_t bc, uint64_t hop, uint64_t tdp) {
+  uint64_t* w = nullptr;
+  __device__ __forceinline__ void put(uint32_t s, uint64_t fc, uint64_t bc, uint64_t hop, uint64_t tdp,
+                                      uint64_t wc) {
     rec[s][0] = fc;
     rec[s][1] = bc;
     rec[s][2] = 0;
     rec[s][3] = tdp;
     if (s > 0) rec[s - 1][2] = hop;
+    if (w) w[s] = wc;
   }
 };
 
@@ -1062,24 +1073,29 @@ struct RecSink {
 // registers as fp64 (every stage quantity is below 2^52, so exact): each
 // stage shifts the arrays down by one and appends, so after S stages stage s
 // sits at index s; a runtime-indexed array would go through private memory.
-// The DP sync is left to dp_tail, after the recurrence.
-template <int S>
+// The DP sync is left to dp_tail, after the recurrence.  kZb: b holds the
+// input-gradient part of the backward and w the weight-gradient part.
+template <int S, bool kZb = false>
 struct RegSink {
   static constexpr bool kDp = false;
-  double f[S], b[S], c[S];
+  double f[S], b[S], c[S], w[kZb ? S : 1];
   __device__ __forceinline__ RegSink() {
 #pragma unroll
     for (int i = 0; i < S; ++i) f[i] = b[i] = c[i] = 0;
+    w[0] = 0;
   }
-  __device__ __forceinline__ void put(uint32_t s, uint64_t fc, uint64_t bc, uint64_t hop, uint64_t) {
+  __device__ __forceinline__ void put(uint32_t s, uint64_t fc, uint64_t bc, uint64_t hop, uint64_t,
+                                      uint64_t wc) {
 #pragma unroll
     for (int i = 0; i + 1 < S; ++i) {
       f[i] = f[i + 1];
       b[i] = b[i + 1];
       c[i] = c[i + 1];
+      if (kZb) w[i] = w[i + 1];
     }
     f[S - 1] = (double)fc;
-    b[S - 1] = (double)bc;
+    b[S - 1] = (double)(kZb ? bc - wc : bc);
+    if (kZb) w[S - 1] = (double)wc;
     c[S - 1] = 0;
     if (S > 1 && s > 0) c[S - 2] = (double)hop;
   }
@@ -1380,6 +1396,96 @@ __device__ __forceinline__ bool pipe(const V (&f)[S], const V (&b)[S], const V (
   return true;
 }
 
+// Zero-bubble order (ZB-H1, Qi et al. 2024): pipe's evaluation order with the
+// backward split into B, the input gradient stage s-1 waits for (eb[s] = its
+// end), and W, the weight gradient.  After B(s, i) stage s runs W(s, i - s)
+// once i >= s -- a pure delay on the stage, its B having run before -- and
+// its last min(s, M) W passes at the end.  From i = S - 1 on every steady
+// iteration runs every stage's W, so the same map repeats and the periodic
+// shortcut applies as in pipe (state out_f[0..S-2], last[0..S-1]; eb is
+// rewritten before it is read).  kJump: shortcut pairs within the budget,
+// then the whole loop; otherwise the whole loop.
+template <int S, typename V>
+__device__ __forceinline__ void zb_iter(const V (&f)[S], const V (&b)[S], const V (&w)[S], const V (&c)[S], int i,
+                                        int tr, V (&out_f)[S], V (&eb)[S], V (&last)[S]) {
+#pragma unroll
+  for (int s = S - 1; s >= 0; --s) {
+    if (s > tr) {   // the stage still runs a forward in this iteration
+      const V st = s == 0 ? last[0] : vmax(last[s], out_f[s - 1] + c[s - 1]);
+      out_f[s] = st + f[s];
+      const V sb = s == S - 1 ? out_f[s] : vmax(out_f[s], eb[s + 1] + c[s]);
+      eb[s] = sb + b[s];
+    } else {
+      eb[s] = (s == S - 1 ? last[s] : vmax(last[s], eb[s + 1] + c[s])) + b[s];
+    }
+    last[s] = eb[s] + (i >= s ? w[s] : (V)0);
+  }
+}
+
+template <int S, typename V, bool kJump>
+__device__ __forceinline__ void pipe_zb(const V (&f)[S], const V (&b)[S], const V (&w)[S], const V (&c)[S],
+                                        uint32_t M, int& skipped, V (&last)[S]) {
+  V out_f[S], eb[S];
+#pragma unroll
+  for (int s = 0; s < S; ++s) out_f[s] = eb[s] = last[s] = 0;
+  const int m_ = (int)M;
+#pragma unroll
+  for (int m = 0; m < S - 1; ++m) {
+    if (m < m_) {
+#pragma unroll
+      for (int s = 0; s < S - 1 - m; ++s) {
+        const V st = s == 0 ? last[0] : vmax(last[s], out_f[s - 1] + c[s - 1]);
+        out_f[s] = st + f[s];
+        last[s] = out_f[s];
+      }
+    }
+  }
+  const int left = m_ - (S - 1);
+  skipped = 0;
+  int i = 0;
+  for (; i < left && i < S - 1; ++i) zb_iter<S, V>(f, b, w, c, i, -1, out_f, eb, last);
+  int rem = left - i;
+  if (kJump) {
+    int budget = kPeriodicBudget;
+    while (rem >= 2 && budget > 0) {
+      zb_iter<S, V>(f, b, w, c, S, -1, out_f, eb, last);
+      bool same = true;
+      V lam = 0;
+#pragma unroll
+      for (int s = S - 1; s >= 0; --s) {
+        const V st = s == 0 ? last[0] : vmax(last[s], out_f[s - 1] + c[s - 1]);
+        const V nf = st + f[s];
+        if (s < S - 1) same = same && nf - out_f[s] == lam;
+        out_f[s] = nf;
+        const V sb = s == S - 1 ? nf : vmax(nf, eb[s + 1] + c[s]);
+        eb[s] = sb + b[s];
+        const V nl = eb[s] + w[s];
+        if (s == S - 1) lam = nl - last[s];
+        else same = same && nl - last[s] == lam;
+        last[s] = nl;
+      }
+      rem -= 2;
+      budget -= 2;
+      if (same) {
+        const V k = (V)rem * lam;
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+          out_f[s] += k;
+          last[s] += k;
+        }
+        skipped = rem;
+        rem = 0;
+      }
+    }
+  }
+  for (; rem > 0; --rem) zb_iter<S, V>(f, b, w, c, S, -1, out_f, eb, last);
+#pragma unroll
+  for (int tr = 0; tr < S - 1; ++tr)
+    if (tr >= S - 1 - m_) zb_iter<S, V>(f, b, w, c, m_ - S + 1 + tr, tr, out_f, eb, last);
+#pragma unroll
+  for (int s = 0; s < S; ++s) last[s] += (V)(s < m_ ? s : m_) * w[s];
+}
+
 // Integers below 2^53 are exact in fp64.  Every value the fp64 pass computes
 // is at most the end of some op, which is at most T, so if T < 2^53 no
 // rounding ever happened.  Otherwise the pipeline goes on an overflow list
@@ -1413,13 +1519,13 @@ struct EvalBufs {
 // to the deferred lists, so that its kernels carry no overlap code; the
 // deferred pass runs them with the shortcut (the whole loop where they stay
 // aperiodic) and the overlapped sync.
-template <int S, bool kFull, int kMode, bool kHet, bool kOvl = false>
+template <int S, bool kFull, int kMode, bool kHet, bool kOvl = false, bool kZb = false>
 __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot) {
-  RegSink<S> r;
+  RegSink<S, kZb> r;
   uint32_t M;
   {
     const Plan p = load_plan<kHet>(e.packed, e.pcut, slot);
-    if (!kFull && !kHet && !kOvl && p.overlap) {
+    if (!kFull && !kHet && !kOvl && !kZb && (p.overlap | p.zb)) {
       e.deferred[e.sstart[kMaxStages - S] + atomicAdd(&e.ctr[1 + kMaxStages - S], 1u)] = slot;
       return;
     }
@@ -1428,8 +1534,10 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
   }
   int skipped;
   double last[S];
-  const bool done = kOvl ? pipe<S, double, true, true>(r.f, r.b, r.c, M, skipped, last)
-                         : pipe<S, double, !kFull>(r.f, r.b, r.c, M, skipped, last);
+  bool done = true;
+  if constexpr (kZb) pipe_zb<S, double, true>(r.f, r.b, r.w, r.c, M, skipped, last);
+  else if constexpr (kOvl) done = pipe<S, double, true, true>(r.f, r.b, r.c, M, skipped, last);
+  else done = pipe<S, double, !kFull>(r.f, r.b, r.c, M, skipped, last);
   // the DP tail reads the plan again (an L2 hit) rather than keeping it in
   // registers through the recurrence; the lane's own slot passed through a
   // shuffle is opaque to the compiler, which would otherwise reuse the
@@ -1453,10 +1561,14 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
 }
 
 // Deferred pass of one pipeline: the whole loop, or for a plan with
-// overlapped gradient sync the shortcut first (shared layout only).
+// overlapped gradient sync or the zero-bubble order the shortcut first
+// (shared layout only).  The first pass sends both kinds here at once, so
+// that its kernels carry neither.
 template <int S, int kMode, bool kHet>
 __device__ __forceinline__ void eval_deferred(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot) {
-  if (!kHet && ((e.packed[slot >> 2].hdr >> 13) & 1)) eval_one<S, false, kMode, kHet, true>(t, h, e, slot);
+  const uint32_t hdr = kHet ? 0 : e.packed[slot >> 2].hdr;
+  if (!kHet && ((hdr >> 13) & 1)) eval_one<S, false, kMode, kHet, true>(t, h, e, slot);
+  else if (!kHet && ((hdr >> 16) & 1)) eval_one<S, false, kMode, kHet, false, true>(t, h, e, slot);
   else eval_one<S, true, kMode, kHet>(t, h, e, slot);
 }
 
@@ -1517,8 +1629,8 @@ __device__ __forceinline__ void il_setup(const Tab& t, const Hot<kMode>& h, cons
     for (int j = 0; j < v; ++j) {
       const int vs = j * S + s;
       const uint32_t lo = vs ? cut_at(p, vs - 1) : 0, hi = cut_at(p, vs);
-      uint64_t fc, bc;
-      stage_cost<kMode, false>(t, h, p, k, ti, base, bq_in, bq_nic, lo, hi, vs == 0, vs == NV - 1, fc, bc);
+      uint64_t fc, bc, wc;
+      stage_cost<kMode, false>(t, h, p, k, ti, base, bq_in, bq_nic, lo, hi, vs == 0, vs == NV - 1, fc, bc, wc);
       f[vs] = (V)fc;
       b[vs] = (V)bc;
     }
@@ -1817,17 +1929,20 @@ __global__ void __launch_bounds__(kEvalThreads) k_deferred(Tab t, EvalBufs e) {
 }
 
 // Pipelines whose fp64 time reached 2^53 ps, again in u64 (exact below 2^64).
+// wz: the weight-gradient parts of a zero-bubble pipeline, else nullptr.
 template <int S>
-__device__ __forceinline__ uint64_t redo_one(const StageRec& R, uint32_t M) {
-  uint64_t f[S], b[S], c[S], last[S];
+__device__ __forceinline__ uint64_t redo_one(const StageRec& R, const uint64_t* wz, uint32_t M) {
+  uint64_t f[S], b[S], c[S], w[S], last[S];
 #pragma unroll
   for (int s = 0; s < S; ++s) {
     f[s] = R[s][0];
-    b[s] = R[s][1];
+    w[s] = wz ? wz[s] : 0;
+    b[s] = R[s][1] - w[s];
     c[s] = R[s][2];
   }
   int skipped;
-  pipe<S, uint64_t, false>(f, b, c, M, skipped, last);
+  if (wz) pipe_zb<S, uint64_t, false>(f, b, w, c, M, skipped, last);
+  else pipe<S, uint64_t, false>(f, b, c, M, skipped, last);
   uint64_t T = 0;
 #pragma unroll
   for (int s = 0; s < S; ++s) T = vmax(T, last[s] + R[s][3]);
@@ -1858,26 +1973,28 @@ __global__ void __launch_bounds__(64) k_redo_u64(Tab t, EvalBufs e) {
       continue;
     }
     StageRec R;
-    RecSink sink{R};
+    uint64_t wz[kMaxStages];
+    const uint64_t* w = !kHet && p.zb ? wz : nullptr;
+    RecSink sink{R, !kHet && p.zb ? wz : nullptr};
     class_setup<2, kHet>(t, h, p, slot & 3, sink, kHet ? e.pcut + (slot & ~3u) : nullptr);
     uint64_t r;
     switch (S) {
-      case 1: r = redo_one<1>(R, M); break;
-      case 2: r = redo_one<2>(R, M); break;
-      case 3: r = redo_one<3>(R, M); break;
-      case 4: r = redo_one<4>(R, M); break;
-      case 5: r = redo_one<5>(R, M); break;
-      case 6: r = redo_one<6>(R, M); break;
-      case 7: r = redo_one<7>(R, M); break;
-      case 8: r = redo_one<8>(R, M); break;
-      case 9: r = redo_one<9>(R, M); break;
-      case 10: r = redo_one<10>(R, M); break;
-      case 11: r = redo_one<11>(R, M); break;
-      case 12: r = redo_one<12>(R, M); break;
-      case 13: r = redo_one<13>(R, M); break;
-      case 14: r = redo_one<14>(R, M); break;
-      case 15: r = redo_one<15>(R, M); break;
-      default: r = redo_one<16>(R, M); break;
+      case 1: r = redo_one<1>(R, w, M); break;
+      case 2: r = redo_one<2>(R, w, M); break;
+      case 3: r = redo_one<3>(R, w, M); break;
+      case 4: r = redo_one<4>(R, w, M); break;
+      case 5: r = redo_one<5>(R, w, M); break;
+      case 6: r = redo_one<6>(R, w, M); break;
+      case 7: r = redo_one<7>(R, w, M); break;
+      case 8: r = redo_one<8>(R, w, M); break;
+      case 9: r = redo_one<9>(R, w, M); break;
+      case 10: r = redo_one<10>(R, w, M); break;
+      case 11: r = redo_one<11>(R, w, M); break;
+      case 12: r = redo_one<12>(R, w, M); break;
+      case 13: r = redo_one<13>(R, w, M); break;
+      case 14: r = redo_one<14>(R, w, M); break;
+      case 15: r = redo_one<15>(R, w, M); break;
+      default: r = redo_one<16>(R, w, M); break;
     }
     atomicMax((unsigned long long*)&e.out[slot >> 2], (unsigned long long)r);
   }
