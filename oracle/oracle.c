@@ -101,6 +101,7 @@ typedef struct {
   uint64_t dev_off[OR_MAXK], node_off[OR_MAXK];
   uint64_t mem[OR_MAXK]; /* device memory capacity in bytes (R34) */
   int mem_check;         /* 0: capacities not given, memory not checked */
+  int rail_only;         /* 1: rail-only inter-node network (R47) */
   uint32_t* nic_dev;    /* NULL or per-device NIC MB/s, pool order */
   uint32_t* intra_node; /* NULL or per-node intra MB/s, pool order */
 } or_cluster;
@@ -724,7 +725,26 @@ static uint64_t hop_cost(const or_ctx* x, const or_plan* p, uint64_t g, int k, u
     alpha = add(alpha_side(x, k), alpha_side(x, k2));
     bq = umax(umax(nic_max(x, k, b1, n), nic_max(x, k2, b2, n)), umax(beta_q(cl->pcie[k]), beta_q(cl->pcie[k2])));
   }
-  return add(alpha, link_time(act, bq));
+  uint64_t t = add(alpha, link_time(act, bq));
+  if (cl->rail_only) {
+    /* R47 (Fig. 2c): device i of the earlier stage sends to device i of the
+     * later one (i < reps * tp); a pair in two nodes at different local
+     * ranks crosses rails, so its data first crosses a node's fabric to the
+     * receiver's rank: that of the sender's node, or of the receiver's when
+     * the sender's node holds one device */
+    int cross = 0;
+    for (uint64_t i = 0; i < n; ++i) {
+      uint64_t d1 = b1 + i, d2 = b2 + i;
+      int other_node = k != k2 || d1 / cl->dpn[k] != d2 / cl->dpn[k2];
+      if (other_node && d1 % cl->dpn[k] != d2 % cl->dpn[k2]) cross = 1;
+    }
+    if (cross) {
+      int kf = cl->dpn[k] > 1 ? k : k2;
+      uint64_t bf = cl->dpn[k] > 1 ? b1 : b2;
+      t = add(t, add(cl->a_intra[kf], link_time(act, intra_max(x, kf, bf, n))));
+    }
+  }
+  return t;
 }
 
 /* the DP ring's latency and rate over the devices of stage sg[g] of every
@@ -1121,6 +1141,7 @@ or_ctx* oracle_new(const uint64_t* mp, const uint32_t* q, const uint64_t* cp,
     c->dev_off[k] = dsum; c->node_off[k] = nsum;
     dsum += r[0] * r[1]; nsum += r[0];
   }
+  c->rail_only = cp[1 + 11 * c->K] != 0;
   if (nic_dev) { c->nic_dev = (uint32_t*)malloc(4 * dsum); memcpy(c->nic_dev, nic_dev, 4 * dsum); }
   if (intra_node) { c->intra_node = (uint32_t*)malloc(4 * nsum); memcpy(c->intra_node, intra_node, 4 * nsum); }
   x->Vp = cdiv(m->vocab, 128) * 128;

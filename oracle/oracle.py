@@ -104,6 +104,7 @@ def _cluster_words(c):
     w = [len(c["types"])]
     for t in c["types"]:
         w += [t[k] for k in TYPE_KEYS] + [t.get("mem_bytes") or 0]
+    w.append(1 if c.get("rail_only") else 0)
     return np.array(w, dtype=np.uint64)
 
 

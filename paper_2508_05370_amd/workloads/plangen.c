@@ -52,7 +52,7 @@ static void gen_one(const pg_params* P, uint64_t i, uint32_t* hdr, uint8_t* cut,
   for (int attempt = 0; attempt < 16 && G == 0; ++attempt) {
     r.d = (uint64_t)attempt * 256;
     tpl = (uint32_t)uni(&r, 0, 3);
-    pp = (uint32_t)uni(&r, 1, 16);
+    pp = (uint32_t)uni(&r, 1, P->L < 16 ? P->L : 16);   /* at most one stage per layer */
     epl = 0;
     if (P->experts) {
       epl = (uint32_t)uni(&r, 0, 3);
@@ -173,7 +173,7 @@ static void gen_one_het(const pg_params* P, uint64_t i, uint32_t* hdr, uint8_t* 
     sumreps = 0;
     for (uint32_t c = 0; c < want; ++c) {
       tpl[c] = (uint32_t)uni(&r, 0, 3);
-      pp[c] = (uint32_t)uni(&r, 1, 16);
+      pp[c] = (uint32_t)uni(&r, 1, P->L < 16 ? P->L : 16);
       uint32_t tp = 1u << tpl[c];
       uint32_t cnt[16] = {0};
       uint64_t t = 0;
