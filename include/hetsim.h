@@ -97,6 +97,13 @@ typedef struct {
   const uint32_t* intra_MBps_node;  /* optional [total nodes] per-node fabric rate (overrides intra_MBps) */
   const uint64_t* mem_bytes;        /* optional [K] device memory in bytes, each >= 1 (Table 5 names
                                        A100 40 GB and H100 80 GB); NULL = memory not checked */
+  uint32_t rail_only;               /* 1: rail-only inter-node network (Fig. 2): the NIC of local rank r
+                                       of every node joins rail r and rails do not meet, so a pipeline
+                                       hop between nodes whose device pairs sit at different local ranks
+                                       first crosses a node's fabric to the receiver's rank -- the
+                                       sender's node, or the receiver's when the sender's type has one
+                                       device per node -- adding that node's latency and the activation
+                                       at its slowest fabric rate (Fig. 2c); 0: any NIC reaches any */
 } sim_cluster_desc;
 
 /*

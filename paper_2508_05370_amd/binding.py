@@ -30,7 +30,8 @@ class ModelDesc(C.Structure):
 class ClusterDesc(C.Structure):
     _fields_ = [("n_types", C.c_uint32)] + [(k, C.c_void_p) for k in (
         "n_nodes", "dev_per_node", "tflops", "hbm_GBps", "intra_MBps", "pcie_MBps", "nic_MBps", "intra_alpha_ps",
-        "pcie_alpha_ps", "nic_alpha_ps", "nic_MBps_dev", "intra_MBps_node", "mem_bytes")]
+        "pcie_alpha_ps", "nic_alpha_ps", "nic_MBps_dev", "intra_MBps_node", "mem_bytes")] + [
+        ("rail_only", C.c_uint32)]
 
 
 class Plans(C.Structure):
@@ -145,6 +146,7 @@ def cluster_desc(c):
         a = _u64([v or 0 for v in mem])
         keep.append(a)
         d.mem_bytes = a.ctypes.data
+    d.rail_only = 1 if c.get("rail_only") else 0
     return d, keep
 
 

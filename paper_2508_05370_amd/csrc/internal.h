@@ -81,6 +81,7 @@ struct Tab {
   uint64_t par_expert[4][4];      // expert parameters of one layer per rank [log2 TP][log2 EP]
   uint64_t par_embed[4], par_head[4];
   uint32_t mem_check;             // 1: device memory capacities given; plans must fit them
+  uint32_t rail_only;             // 1: rail-only inter-node network (cross-rail hops forwarded in a node)
   uint64_t mem_cap[kMaxTypes];    // device memory of type k, bytes
   uint64_t opt_bytes;             // optimizer-state bytes per parameter
   uint64_t act_layer[4][4];       // bytes one layer stores for backward per micro-batch [log2 TP][mbs index]

@@ -1002,6 +1002,25 @@ __device__ __forceinline__ void stage_place(const Tab& t, const Hot<kMode>& h, c
   bq_nic = range_max(h.rmn, t.D, dlo, dlo + nd - 1);
 }
 
+// Rail-only network (Fig. 2): the NIC of local rank r of every node joins
+// rail r and rails do not meet.  A pipeline hop between nodes pairs device i
+// of the sending stage (from bs on, n = reps * tp devices) with device i of
+// the receiving one (from br on); a pair at different local ranks is
+// forwarded over a node's fabric first -- the sender's, or the receiver's
+// when the sender's nodes hold one device -- which adds that node's latency
+// and the activation at its slowest fabric rate (ins / inr over the
+// stage's nodes).  Offsets os, or in their nodes: every pair shares a rank
+// iff os == or and, with different node sizes, the n pairs do not reach the
+// end of the smaller node (past it one rank wraps and the other does not).
+__device__ __forceinline__ uint64_t rail_extra(uint32_t n, const TypeInfo& ts, uint32_t bs, uint32_t ins,
+                                               const TypeInfo& tr, uint32_t br, uint32_t inr, uint64_t act) {
+  const uint32_t ds = 1u << ts.dpl, dr = 1u << tr.dpl, os = bs & (ds - 1), orr = br & (dr - 1);
+  const bool same = os == orr && (ds == dr || os + n <= (ds < dr ? ds : dr));
+  if (same) return 0;
+  const bool at_s = ts.dpl > 0;
+  return (at_s ? ts.a_intra : tr.a_intra) + link_ps(act, at_s ? ins : inr);
+}
+
 template <int kMode, bool kHet, typename Sink>
 __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t c,
                                             Sink& sink, const uint4* prow) {
@@ -1034,6 +1053,7 @@ __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, c
         bq = a > b ? a : b;
       }
       hop = alpha + link_ps(act, bq);
+      if (t.rail_only && !intra) hop += rail_extra(reps * tp, pti, pbase, pin, ti, base, bq_in, act);
     }
     pk = k; pbase = base; pnic = bq_nic; pin = bq_in; pti = ti;
     // ---- DP sync of this stage (the sink may leave it for later)
@@ -1594,9 +1614,10 @@ __device__ __forceinline__ void eval_deferred(const Tab& t, const Hot<kMode>& h,
 // Hop between the devices of two stages of one class, a placed before b
 // when they share a pool: inside a node iff every replica's pair is, i.e.
 // iff a's first device and b's last one share a node.
-__device__ __forceinline__ uint64_t il_hop(uint32_t ka, const TypeInfo& ta, uint32_t basea, uint32_t ina,
-                                           uint32_t nica, uint32_t kb, const TypeInfo& tb, uint32_t baseb,
-                                           uint32_t inb, uint32_t nicb, uint32_t reps, uint32_t tp, uint64_t act) {
+__device__ __forceinline__ uint64_t il_hop(const Tab& t, uint32_t ka, const TypeInfo& ta, uint32_t basea,
+                                           uint32_t ina, uint32_t nica, uint32_t kb, const TypeInfo& tb,
+                                           uint32_t baseb, uint32_t inb, uint32_t nicb, uint32_t reps, uint32_t tp,
+                                           uint64_t act, bool a_sends) {
   const uint32_t dpl = tb.dpl;
   const bool intra = ka == kb && (basea >> dpl) == ((baseb + (reps - 1) * tp) >> dpl);
   const uint64_t alpha = intra ? tb.a_intra : ta.a_side + tb.a_side;
@@ -1608,7 +1629,11 @@ __device__ __forceinline__ uint64_t il_hop(uint32_t ka, const TypeInfo& ta, uint
     const uint32_t y = ta.bq_pcie > tb.bq_pcie ? ta.bq_pcie : tb.bq_pcie;
     bq = x > y ? x : y;
   }
-  return alpha + link_ps(act, bq);
+  uint64_t hop = alpha + link_ps(act, bq);
+  if (t.rail_only && !intra)
+    hop += a_sends ? rail_extra(reps * tp, ta, basea, ina, tb, baseb, inb, act)
+                   : rail_extra(reps * tp, tb, baseb, inb, ta, basea, ina, act);
+  return hop;
 }
 
 // Per virtual stage forward and backward time (f, b), hops between devices
@@ -1634,11 +1659,12 @@ __device__ __forceinline__ void il_setup(const Tab& t, const Hot<kMode>& h, cons
       f[vs] = (V)fc;
       b[vs] = (V)bc;
     }
-    if (s > 0) c[s - 1] = (V)il_hop(pk, pti, pbase, pin, pnic, k, ti, base, bq_in, bq_nic, p.rc, p.tp, act);
+    if (s > 0) c[s - 1] = (V)il_hop(t, pk, pti, pbase, pin, pnic, k, ti, base, bq_in, bq_nic, p.rc, p.tp, act, true);
     if (s == 0) {
       k0 = k; ti0 = ti; base0 = base; in0 = bq_in; nic0 = bq_nic;
     }
-    if (s == S - 1) c[S - 1] = (V)il_hop(k0, ti0, base0, in0, nic0, k, ti, base, bq_in, bq_nic, p.rc, p.tp, act);
+    if (s == S - 1)   // the wrap hop: device S - 1 sends to device 0, placed before it
+      c[S - 1] = (V)il_hop(t, k0, ti0, base0, in0, nic0, k, ti, base, bq_in, bq_nic, p.rc, p.tp, act, false);
     pk = k; pti = ti; pbase = base; pin = bq_in; pnic = bq_nic;
   }
 }

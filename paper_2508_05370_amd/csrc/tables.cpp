@@ -306,6 +306,7 @@ int build_tables(const sim_model_desc* md, const sim_cluster_desc* cd, HostTable
   // input, then the MLP's input, its activation input(s) and the down
   // projection's input -- or, for MoE layers, the router input and per
   // routed token copy (top-k of them, balanced) the same three MLP tensors.
+  t.rail_only = cd->rail_only != 0;
   u128 mem_max = 0;
   if (cd->mem_bytes) {
     t.mem_check = 1;
@@ -424,6 +425,7 @@ int build_tables(const sim_model_desc* md, const sim_cluster_desc* cd, HostTable
   u128 tp_max = steps_tp * a_max + link_ps(steps_tp * act_max, bq_max);
   u128 ep_max = steps_ep * a_max + link_ps(2 * a2a_max, bq_max);
   u128 hop_max = a_max + link_ps(act_max, bq_max);
+  if (t.rail_only) hop_max *= 2;   // a cross-rail hop adds one intra-node step
   u128 par_max = 0;
   for (uint32_t j = 0; j < 4; ++j)
     par_max = std::max<u128>(par_max, (u128)t.par_layer[j] * s.L + t.par_embed[j] + t.par_head[j] +
