@@ -102,6 +102,7 @@ typedef struct {
   uint64_t mem[OR_MAXK]; /* device memory capacity in bytes (R34) */
   int mem_check;         /* 0: capacities not given, memory not checked */
   int rail_only;         /* 1: rail-only inter-node network (R47) */
+  int ccl_tree;          /* 1: all-reduces take the faster of ring and tree (R48) */
   uint32_t* nic_dev;    /* NULL or per-device NIC MB/s, pool order */
   uint32_t* intra_node; /* NULL or per-node intra MB/s, pool order */
 } or_cluster;
@@ -629,6 +630,26 @@ static uint64_t dp_sync(uint64_t p, uint64_t zero, uint64_t grads, uint64_t para
              ring(p - 1, cdiv(params, p), alpha, bq));                     /* all-gather of parameters */
 }
 
+/* R48: pipelined binary-tree all-reduce over p members (reduce up the tree,
+ * broadcast down it, in chunks): 2 ceil(log2 p) message latencies, and
+ * every member's gradient crosses its busiest link twice. */
+static uint64_t umin(uint64_t a, uint64_t b) { return a < b ? a : b; }
+static uint64_t tree_allreduce(uint64_t p, uint64_t grads, uint64_t alpha, uint64_t bq) {
+  if (p <= 1) return 0;
+  uint64_t lg = 0;
+  while ((1ull << lg) < p) ++lg;
+  return add(mul(2 * lg, alpha), link_time(mul(2, grads), bq));
+}
+/* a stage's DP sync on the cluster's collectives: the ring, or with tree
+ * collectives enabled the faster of ring and tree for an all-reduce (NCCL
+ * picks an algorithm per call); reduce-scatter and all-gather are rings */
+static uint64_t dp_sync_cl(const or_ctx* x, uint64_t p, uint64_t zero, uint64_t grads, uint64_t params, uint64_t alpha,
+                           uint64_t bq) {
+  uint64_t r = dp_sync(p, zero, grads, params, alpha, bq);
+  if (x->c.ccl_tree && !zero && p > 1) r = umin(r, tree_allreduce(p, grads, alpha, bq));
+  return r;
+}
+
 /* parameters of layers [a, b) held by one rank at TP t, EP ep: non-expert
  * part (with the embedding if a = 0 and the head if b = L) and expert part */
 static void span_params(const or_ctx* x, uint64_t a, uint64_t b, uint64_t t, uint64_t ep, uint64_t* pd,
@@ -913,8 +934,8 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
     /* R36: the ring runs on the coarsest TP layout among the classes */
     uint64_t pd, pe;
     span_params(x, a, e, tp_min, ep, &pd, &pe);
-    uint64_t t = dp_sync(p_all, p->zero, mul(m->grad_bytes, pd), mul(m->param_bytes, pd), alpha, bq);
-    if (m->E) t = add(t, dp_sync(p_all / ep, p->zero, mul(m->grad_bytes, pe), mul(m->param_bytes, pe), alpha, bq));
+    uint64_t t = dp_sync_cl(x, p_all, p->zero, mul(m->grad_bytes, pd), mul(m->param_bytes, pd), alpha, bq);
+    if (m->E) t = add(t, dp_sync_cl(x, p_all / ep, p->zero, mul(m->grad_bytes, pe), mul(m->param_bytes, pe), alpha, bq));
     /* R36: classes with finer shards first gather the coarse shard inside
      * each TP group: a ring all-gather over tp/tp_min members of the
      * class's own gradient shard, on the group's node fabric; classes
@@ -977,10 +998,10 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
         uint64_t ready = d->end[g][s] - bsum, c = 0;
         for (uint64_t j = 0; j < nbk; ++j) {
           ready = add(ready, comp[j]);
-          uint64_t dj = dp_sync(p_all, p->zero, mul(m->grad_bytes, pd[j]), mul(m->param_bytes, pd[j]),
+          uint64_t dj = dp_sync_cl(x, p_all, p->zero, mul(m->grad_bytes, pd[j]), mul(m->param_bytes, pd[j]),
                                 seg_alpha[s], seg_bq[s]);
           if (m->E && pe[j])
-            dj = add(dj, dp_sync(p_all / ep, p->zero, mul(m->grad_bytes, pe[j]), mul(m->param_bytes, pe[j]),
+            dj = add(dj, dp_sync_cl(x, p_all / ep, p->zero, mul(m->grad_bytes, pe[j]), mul(m->param_bytes, pe[j]),
                                  seg_alpha[s], seg_bq[s]));
           c = add(umax(c, ready), dj);
         }
@@ -1092,8 +1113,8 @@ static void eval_plan_interleaved(const or_ctx* x, const or_plan* p, or_detail* 
     uint64_t pd = mul(ns, layer_params_dense(x, tp)), pe = mul(ns, layer_params_expert(x, tp, ep));
     if (s == 0) pd = add(pd, embed_params(x, tp));
     if (s == S - 1) pd = add(pd, head_params(x, tp));
-    uint64_t t = dp_sync(p_all, p->zero, mul(m->grad_bytes, pd), mul(m->param_bytes, pd), alpha, bq);
-    if (m->E) t = add(t, dp_sync(p_all / ep, p->zero, mul(m->grad_bytes, pe), mul(m->param_bytes, pe), alpha, bq));
+    uint64_t t = dp_sync_cl(x, p_all, p->zero, mul(m->grad_bytes, pd), mul(m->param_bytes, pd), alpha, bq);
+    if (m->E) t = add(t, dp_sync_cl(x, p_all / ep, p->zero, mul(m->grad_bytes, pe), mul(m->param_bytes, pe), alpha, bq));
     tdp[s] = t;
   }
   uint64_t T_iter = 0;
@@ -1142,6 +1163,7 @@ or_ctx* oracle_new(const uint64_t* mp, const uint32_t* q, const uint64_t* cp,
     dsum += r[0] * r[1]; nsum += r[0];
   }
   c->rail_only = cp[1 + 11 * c->K] != 0;
+  c->ccl_tree = cp[2 + 11 * c->K] != 0;
   if (nic_dev) { c->nic_dev = (uint32_t*)malloc(4 * dsum); memcpy(c->nic_dev, nic_dev, 4 * dsum); }
   if (intra_node) { c->intra_node = (uint32_t*)malloc(4 * nsum); memcpy(c->intra_node, intra_node, 4 * nsum); }
   x->Vp = cdiv(m->vocab, 128) * 128;
@@ -1256,6 +1278,9 @@ void oracle_pipeline_interleaved(uint64_t S, uint64_t v, uint64_t M, const uint6
 uint64_t oracle_alpha_ps(uint64_t gbps_unidir) { return cdiv(9200ull * 8 * 1000, gbps_unidir); }
 uint64_t oracle_beta_q(uint64_t MBps) { return beta_q(MBps); }
 uint64_t oracle_link_time(uint64_t bytes, uint64_t bq) { return link_time(bytes, bq); }
+uint64_t oracle_tree_allreduce(uint64_t p, uint64_t grads, uint64_t alpha, uint64_t MBps) {
+  return tree_allreduce(p, grads, alpha, beta_q(MBps));
+}
 uint64_t oracle_dp_sync(uint64_t p, uint64_t zero, uint64_t grads, uint64_t params, uint64_t alpha, uint64_t MBps) {
   return dp_sync(p, zero, grads, params, alpha, beta_q(MBps));
 }

@@ -53,6 +53,8 @@ def lib():
         L.oracle_link_time.argtypes = [u64, u64]
         L.oracle_link_time.restype = u64
         L.oracle_dp_sync.argtypes = [u64, u64, u64, u64, u64, u64]
+        L.oracle_tree_allreduce.argtypes = [u64, u64, u64, u64]
+        L.oracle_tree_allreduce.restype = u64
         L.oracle_dp_sync.restype = u64
         L.oracle_layer_time.argtypes = [P, C.c_int, u64, u64, u64, u64, C.c_int]
         L.oracle_layer_time.restype = u64
@@ -105,6 +107,7 @@ def _cluster_words(c):
     for t in c["types"]:
         w += [t[k] for k in TYPE_KEYS] + [t.get("mem_bytes") or 0]
     w.append(1 if c.get("rail_only") else 0)
+    w.append(1 if c.get("ccl_tree") else 0)
     return np.array(w, dtype=np.uint64)
 
 
@@ -261,3 +264,7 @@ def link_time(nbytes, bq):
 
 def dp_sync(p, zero, grads, params, alpha, MBps):
     return lib().oracle_dp_sync(p, zero, grads, params, alpha, MBps)
+
+
+def tree_allreduce(p, grads, alpha, MBps):
+    return lib().oracle_tree_allreduce(p, grads, alpha, MBps)
