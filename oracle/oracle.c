@@ -723,7 +723,7 @@ static void stage_compute(const or_ctx* x, const or_plan* p, uint64_t g, int k, 
   }
   *F = add(add(Fc, tpf), epc);
   *B = add(Bc, epc);
-  if (Wg) *Wg = Bc / 2;                                        /* R44: the weight-gradient half of the compute */
+  if (Wg) *Wg = *B / 2;                                        /* R44: the weight-gradient half of the backward */
 }
 
 /* PP hop between class g's stage on pool k (devices from b1 on) and its

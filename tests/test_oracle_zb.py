@@ -3,7 +3,8 @@
 The backward pass splits into B (input gradient, what the previous stage waits for) and W
 (weight gradient, local); stage s runs the 1F1B order of forwards and B passes and releases
 each W s micro-batches after its B (ZB-H1 of Qi et al. 2024, "Zero Bubble Pipeline
-Parallelism").  Pinned: that paper's ZB-H1 bubble (S - 1)(F + B - W) for equal pass costs, an
+Parallelism"), W being half of the stage's backward time.  Pinned: that paper's ZB-H1 bubble
+(S - 1)(F + B - W) for equal pass costs, an
 event-driven replay of the same op lists (independent code), the reduction to 1F1B when W
 costs nothing, the in-flight count (every stage at most S micro-batches, 1F1B's peak) against a
 walk of the op lists, the per-stage split of the backward, and the invalid combinations.
@@ -85,9 +86,9 @@ def _set(p, i, cuts, classes, tp=1, zero=0, zb=1, overlap=0, v=1):
 
 
 def test_plan_split_and_schedule(oracle_mod, workloads):
-    """A dense model: each stage's backward is its compute only, so W is half of it (rounded
-    down) and B the rest; the stage times equal the plain plan's, the ends are the zero-bubble
-    pipeline over them, and the iteration is the latest end plus its sync."""
+    """W is half of each stage's backward time (rounded down) and B the rest; the stage times
+    equal the plain plan's, the ends are the zero-bubble pipeline over them, and the iteration is
+    the latest end plus its sync."""
     m = workloads.model("gpt2-small")
     c = workloads.cluster_two_type_8()
     o = oracle_mod.Oracle(m, c)
