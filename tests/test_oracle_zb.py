@@ -138,3 +138,24 @@ def test_invalid_zero_bubble_plans(oracle_mod, workloads):
     h = workloads.as_per_class(workloads.plans(workloads.workload(1), 0, 16))
     h["hdr"] |= np.uint32(1 << 16)                                        # the per-class layout does not take it
     assert np.all(o.eval(h) == MAXU)
+
+
+def test_split_with_moe_all_to_all(oracle_mod, workloads):
+    """For an MoE model the backward includes the expert all-to-all; W is still half of the
+    whole backward time and the plan's time follows the zero-bubble pipeline over the split."""
+    w = workloads.workload(4)
+    p = workloads.plans(w, 0, 400)
+    p["hdr"] |= np.uint32(1 << 16)
+    o = oracle_mod.Oracle(w["model"], w["cluster"])
+    checked = 0
+    for i in range(0, 400, 7):
+        d = o.detail(p, i)
+        if d is None:
+            continue
+        for g in range(d["G"]):
+            assert d["w"][g] == [x // 2 for x in d["b"][g]]
+            bi = [x - y for x, y in zip(d["b"][g], d["w"][g])]
+            S = d["S"]
+            assert d["end"][g] == oracle_mod.pipeline_zb(S, d["M"][g], d["f"][g], bi, d["w"][g], d["c"][g][:S - 1])
+        checked += 1
+    assert checked > 30
