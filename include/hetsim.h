@@ -104,6 +104,11 @@ typedef struct {
                                        sender's node, or the receiver's when the sender's type has one
                                        device per node -- adding that node's latency and the activation
                                        at its slowest fabric rate (Fig. 2c); 0: any NIC reaches any */
+  uint32_t ccl_tree;                /* 1: every DP all-reduce (not the reduce-scatter and all-gather of
+                                       ZeRO) takes the faster of the ring and a pipelined binary tree,
+                                       2 ceil(log2 p) latencies plus twice the gradient bytes at the
+                                       ring's slowest rate, as a collective library picks an algorithm
+                                       per call (Sec. 4.1 [C3]); 0: rings only */
 } sim_cluster_desc;
 
 /*
@@ -128,7 +133,7 @@ typedef struct {
  *                       16 zero-bubble order (ZB-H1, Qi et al. 2024): the
  *                       backward pass splits into an input-gradient part
  *                       (what the previous stage waits for) and a
- *                       weight-gradient part, half of the backward compute
+ *                       weight-gradient part, half of the backward time
  *                       rounded down; stage s runs 1F1B's order of forwards
  *                       and input-gradient passes and each weight-gradient
  *                       pass s micro-batches after its input-gradient pass,

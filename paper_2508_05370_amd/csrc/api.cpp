@@ -48,6 +48,7 @@ struct sim_ctx {
   bool timing;
   std::vector<EventPair> ev[4];
   uint64_t* skipped_ops;   // device counter, inside `tables`
+  Tab* dtab;               // copy of `tab` in device memory, inside `tables`
   hipStream_t aux;         // deferred passes of multi-chunk calls, created on first use
   hipStream_t grp[4];      // first-pass groups of multi-chunk calls, created on first use
 };
@@ -84,7 +85,9 @@ extern "C" int sim_create(const sim_model_desc* model, const sim_cluster_desc* c
   if (hipGetDevice(&c->device) != hipSuccess) { delete ht; delete c; return SIM_EHIP; }
   // the table image, then the skipped-work counter slots
   const size_t img = align256(ht->img.size());
-  if (hipMalloc(&c->tables, img + kSkipBytes) != hipSuccess) { delete ht; delete c; return SIM_ENOMEM; }
+  if (hipMalloc(&c->tables, img + kSkipBytes + align256(sizeof(Tab))) != hipSuccess) {
+    delete ht; delete c; return SIM_ENOMEM;
+  }
   if (hipMemcpy(c->tables, ht->img.data(), ht->img.size(), hipMemcpyHostToDevice) != hipSuccess ||
       hipMemset((char*)c->tables + img, 0, kSkipBytes) != hipSuccess) {
     (void)hipFree(c->tables); delete ht; delete c; return SIM_EHIP;
@@ -92,6 +95,10 @@ extern "C" int sim_create(const sim_model_desc* model, const sim_cluster_desc* c
   c->tab.img = c->tables;
   if (eval_grids(&c->tab) != 0) { (void)hipFree(c->tables); delete ht; delete c; return SIM_EHIP; }
   c->skipped_ops = (uint64_t*)((char*)c->tables + img);
+  c->dtab = (Tab*)((char*)c->tables + img + kSkipBytes);
+  if (hipMemcpy(c->dtab, &c->tab, sizeof(Tab), hipMemcpyHostToDevice) != hipSuccess) {
+    (void)hipFree(c->tables); delete ht; delete c; return SIM_EHIP;
+  }
   delete ht;
   hipMemPoolProps props;
   memset(&props, 0, sizeof(props));
@@ -245,7 +252,7 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
     if (e == hipSuccess) e = launch_scan(W.hist, W.cursor, W.sstart, s);
     if (e == hipSuccess) e = launch_scatter(W.keys, (uint32_t)(cn * 4), W.cursor, W.ids, s);
     const EvalArgs a = {W.packed, W.pcut, W.hdp, W.meta, W.ids, W.sstart, out + off, W.ctr, W.deferred,
-                        c->timing ? c->skipped_ops : nullptr};
+                        c->timing ? c->skipped_ops : nullptr, c->dtab};
     EventPair e0;
     bool t0 = e == hipSuccess && begin_event(c, 0, s, &e0);
     if (nbuf == 1) {

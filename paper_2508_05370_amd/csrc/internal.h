@@ -82,6 +82,7 @@ struct Tab {
   uint64_t par_embed[4], par_head[4];
   uint32_t mem_check;             // 1: device memory capacities given; plans must fit them
   uint32_t rail_only;             // 1: rail-only inter-node network (cross-rail hops forwarded in a node)
+  uint32_t ccl_tree;              // 1: all-reduces take the faster of ring and tree
   uint64_t mem_cap[kMaxTypes];    // device memory of type k, bytes
   uint64_t opt_bytes;             // optimizer-state bytes per parameter
   uint64_t act_layer[4][4];       // bytes one layer stores for backward per micro-batch [log2 TP][mbs index]
@@ -117,6 +118,7 @@ struct EvalArgs {
   uint32_t* ctr;
   uint32_t* deferred;          // as long as ids
   uint64_t* skipped_ops;       // optional: kSkipSlots counters, kSkipStride words apart
+  const Tab* dtab;             // the context's Tab in device memory (read by the deferred pass)
 };
 
 // Host side: validate descriptors and build the tables (host copies).

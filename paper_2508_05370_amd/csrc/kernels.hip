@@ -68,13 +68,23 @@ __device__ __forceinline__ uint64_t div_up(uint64_t x, uint64_t p, double rp) {
   return q + (r != 0);
 }
 
-// DP gradient sync of one stage over a ring of p members
+// DP gradient sync of one stage over a ring of p members.  tree: an
+// all-reduce takes the faster of the ring and a pipelined binary tree
+// (reduce up, broadcast down: 2 ceil(log2 p) latencies, each member's
+// gradient twice over the slowest link); ZeRO's reduce-scatter and
+// all-gather stay rings.
 __device__ __forceinline__ uint64_t ring_sync(uint32_t p, double rp, uint32_t zero, uint64_t grads, uint64_t params,
-                                              uint64_t alpha, uint32_t bq) {
+                                              uint64_t alpha, uint32_t bq, uint32_t tree) {
   uint64_t g = div_up(grads, p, rp);
   if (!zero) {
     uint64_t steps = 2ull * (p - 1);
-    return steps * alpha + link_ps(steps * g, bq);
+    uint64_t r = steps * alpha + link_ps(steps * g, bq);
+    if (tree && p > 1) {
+      const uint64_t lg = 32 - __builtin_clz(p - 1);
+      const uint64_t tt = 2 * lg * alpha + link_ps(2 * grads, bq);
+      r = tt < r ? tt : r;
+    }
+    return r;
   }
   uint64_t steps = p - 1;
   return 2 * steps * alpha + link_ps(steps * g, bq) + link_ps(steps * div_up(params, p, rp), bq);
@@ -655,11 +665,11 @@ __device__ __forceinline__ uint64_t stage_dp(const Tab& t, const Hot<kMode>& h, 
   stage_link(t, h, p, s, alpha, bq);
   const uint64_t pd = (uint64_t)ns * t.par_layer[tpl] + (s == 0 ? t.par_embed[tpl] : 0) +
                       (s == S - 1 ? t.par_head[tpl] : 0);
-  uint64_t tdp = ring_sync(p.psum, rp, p.zero, t.grad_bytes * pd, t.param_bytes * pd, alpha, bq);
+  uint64_t tdp = ring_sync(p.psum, rp, p.zero, t.grad_bytes * pd, t.param_bytes * pd, alpha, bq, t.ccl_tree);
   const uint32_t pe = p.psum >> epl;
   if (t.E && pe > 1) {
     const uint64_t px = (uint64_t)ns * t.par_expert[tpl][epl];
-    tdp += ring_sync(pe, rpe, p.zero, t.grad_bytes * px, t.param_bytes * px, alpha, bq);
+    tdp += ring_sync(pe, rpe, p.zero, t.grad_bytes * px, t.param_bytes * px, alpha, bq, t.ccl_tree);
   }
   return tdp;
 }
@@ -681,15 +691,15 @@ __device__ __forceinline__ uint64_t overlap_tail(const Tab& t, const Hot<kMode>&
   uint32_t bq;
   stage_link(t, h, p, s, alpha, bq);
   const uint64_t gb = t.grad_bytes, pb = t.param_bytes;
-  uint64_t dl = ring_sync(p.psum, rp, p.zero, gb * t.par_layer[tpl], pb * t.par_layer[tpl], alpha, bq);
+  uint64_t dl = ring_sync(p.psum, rp, p.zero, gb * t.par_layer[tpl], pb * t.par_layer[tpl], alpha, bq, t.ccl_tree);
   const uint32_t pe = p.psum >> epl;
   if (t.E && pe > 1)
-    dl += ring_sync(pe, rpe, p.zero, gb * t.par_expert[tpl][epl], pb * t.par_expert[tpl][epl], alpha, bq);
+    dl += ring_sync(pe, rpe, p.zero, gb * t.par_expert[tpl][epl], pb * t.par_expert[tpl][epl], alpha, bq, t.ccl_tree);
   const uint32_t L1 = t.L + 1, epq = t.E ? epl : 0;
   const uint32_t row = ((k * 4 + tpl) * t.n_mbs + mi) * t.nep + epq;
   int64_t D = 0, R = 0, X = 0;
   if (s == 0) {
-    D += (int64_t)ring_sync(p.psum, rp, p.zero, gb * t.par_embed[tpl], pb * t.par_embed[tpl], alpha, bq);
+    D += (int64_t)ring_sync(p.psum, rp, p.zero, gb * t.par_embed[tpl], pb * t.par_embed[tpl], alpha, bq, t.ccl_tree);
     X = D;
     R += (int64_t)h.emb(k * t.n_mbs + mi).y;
   }
@@ -699,7 +709,7 @@ __device__ __forceinline__ uint64_t overlap_tail(const Tab& t, const Hot<kMode>&
     R += (int64_t)(t.uniform_layers ? h.pfb(row).y : h.pfb(row * L1 + l + 1).y - h.pfb(row * L1 + l).y);
   }
   if (s == p.S - 1) {
-    D += (int64_t)ring_sync(p.psum, rp, p.zero, gb * t.par_head[tpl], pb * t.par_head[tpl], alpha, bq);
+    D += (int64_t)ring_sync(p.psum, rp, p.zero, gb * t.par_head[tpl], pb * t.par_head[tpl], alpha, bq, t.ccl_tree);
     X = D - R > X ? D - R : X;
   }
   return (uint64_t)X;
@@ -779,11 +789,11 @@ __device__ __forceinline__ uint64_t seg_dp(const Tab& t, const Hot<kMode>& h, co
   const uint32_t bq = intra ? h.rmi()[nmin] : bq_dp;
   const uint64_t pd = (uint64_t)ns * t.par_layer[tmin] + (a == 0 ? t.par_embed[tmin] : 0) +
                       (e == t.L ? t.par_head[tmin] : 0);
-  uint64_t tdp = p.psum <= 1 ? 0 : ring_sync(p.psum, rp, p.zero, t.grad_bytes * pd, t.param_bytes * pd, alpha, bq);
+  uint64_t tdp = p.psum <= 1 ? 0 : ring_sync(p.psum, rp, p.zero, t.grad_bytes * pd, t.param_bytes * pd, alpha, bq, t.ccl_tree);
   const uint32_t pe = p.psum >> epl;
   if (t.E && pe > 1) {
     const uint64_t px = (uint64_t)ns * t.par_expert[tmin][epl];
-    tdp += ring_sync(pe, rpe, p.zero, t.grad_bytes * px, t.param_bytes * px, alpha, bq);
+    tdp += ring_sync(pe, rpe, p.zero, t.grad_bytes * px, t.param_bytes * px, alpha, bq, t.ccl_tree);
   }
   return tdp + rs;
 }
@@ -907,11 +917,11 @@ __device__ __forceinline__ void het_plan_syncs(const Tab& t, const Hot<kMode>& h
     const uint32_t bq = intra ? h.rmi()[nmin] : bq_dp;
     const uint64_t pd = (uint64_t)ns * t.par_layer[tmin] + (a == 0 ? t.par_embed[tmin] : 0) +
                         (e == t.L ? t.par_head[tmin] : 0);
-    uint64_t x = p.psum <= 1 ? 0 : ring_sync(p.psum, rp, p.zero, t.grad_bytes * pd, t.param_bytes * pd, alpha, bq);
+    uint64_t x = p.psum <= 1 ? 0 : ring_sync(p.psum, rp, p.zero, t.grad_bytes * pd, t.param_bytes * pd, alpha, bq, t.ccl_tree);
     const uint32_t pe = p.psum >> epl;
     if (t.E && pe > 1) {
       const uint64_t px = (uint64_t)ns * t.par_expert[tmin][epl];
-      x += ring_sync(pe, rpe, p.zero, t.grad_bytes * px, t.param_bytes * px, alpha, bq);
+      x += ring_sync(pe, rpe, p.zero, t.grad_bytes * px, t.param_bytes * px, alpha, bq, t.ccl_tree);
     }
     x += rs;
 #pragma unroll
@@ -933,7 +943,7 @@ template <int kMode, bool kHet>
 __device__ __forceinline__ void stage_cost(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t k,
                                            const TypeInfo& ti, uint32_t base, uint32_t bq_in, uint32_t bq_nic,
                                            uint32_t lo, uint32_t hi, bool first, bool last, uint64_t& fc,
-                                           uint64_t& bc, uint64_t& wc) {
+                                           uint64_t& bc) {
   const uint32_t tp = p.tp, ep = p.ep, tpl = p.tpl, epl = p.epl, mi = p.mi, ns = hi - lo, dpl = ti.dpl;
   const uint64_t act = t.act[mi], act_tp = (act + tp - 1) >> tpl;
   const uint32_t L1 = t.L + 1, epq = t.E ? p.epl : 0;
@@ -958,7 +968,6 @@ __device__ __forceinline__ void stage_cost(const Tab& t, const Hot<kMode>& h, co
     fc += hd.x;
     bc += hd.y;
   }
-  wc = bc >> 1;  // weight-gradient half of the backward compute (zero-bubble order)
   if (tp > 1) {  // TP all-reduces of this stage, exposed in the forward pass
     const uint64_t steps = (uint64_t)(2 * ns + first) * 2 * (tp - 1);
     fc += steps * ti.a_intra + link_ps(steps * act_tp, bq_in);
@@ -1037,8 +1046,8 @@ __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, c
     TypeInfo ti;
     stage_place<kMode, kHet>(t, h, p, s, k, ti, base, bq_in, bq_nic);
     const uint32_t dpl = ti.dpl;
-    uint64_t fc, bc, wc;
-    stage_cost<kMode, kHet>(t, h, p, k, ti, base, bq_in, bq_nic, lo, hi, s == 0, s == S - 1, fc, bc, wc);
+    uint64_t fc, bc;
+    stage_cost<kMode, kHet>(t, h, p, k, ti, base, bq_in, bq_nic, lo, hi, s == 0, s == S - 1, fc, bc);
     uint64_t hop = 0;
     if (s > 0) {  // hop (s-1) -> s
       // same pool means the two ranges are adjacent: intra iff the pair spans one node
@@ -1067,25 +1076,22 @@ __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, c
         tdp = stage_sync(t, h, p, s, lo, hi, rp, rpe);
       }
     }
-    sink.put(s, fc, bc, hop, tdp, wc);
+    sink.put(s, fc, bc, hop, tdp);
     lo = hi;
   }
 }
 
 // Sinks of class_setup.  RecSink stores whole stage records in memory order
-// (the hop of the last stage is 0), and with `w` the weight-gradient parts.
+// (the hop of the last stage is 0).
 struct RecSink {
   static constexpr bool kDp = true;
   uint64_t (&rec)[kMaxStages][kRecWords];
-  uint64_t* w = nullptr;
-  __device__ __forceinline__ void put(uint32_t s, uint64_t fc, uint64_t bc, uint64_t hop, uint64_t tdp,
-                                      uint64_t wc) {
+  __device__ __forceinline__ void put(uint32_t s, uint64_t fc, uint64_t bc, uint64_t hop, uint64_t tdp) {
     rec[s][0] = fc;
     rec[s][1] = bc;
     rec[s][2] = 0;
     rec[s][3] = tdp;
     if (s > 0) rec[s - 1][2] = hop;
-    if (w) w[s] = wc;
   }
 };
 
@@ -1093,29 +1099,24 @@ struct RecSink {
 // registers as fp64 (every stage quantity is below 2^52, so exact): each
 // stage shifts the arrays down by one and appends, so after S stages stage s
 // sits at index s; a runtime-indexed array would go through private memory.
-// The DP sync is left to dp_tail, after the recurrence.  kZb: b holds the
-// input-gradient part of the backward and w the weight-gradient part.
-template <int S, bool kZb = false>
+// The DP sync is left to dp_tail, after the recurrence.
+template <int S>
 struct RegSink {
   static constexpr bool kDp = false;
-  double f[S], b[S], c[S], w[kZb ? S : 1];
+  double f[S], b[S], c[S];
   __device__ __forceinline__ RegSink() {
 #pragma unroll
     for (int i = 0; i < S; ++i) f[i] = b[i] = c[i] = 0;
-    w[0] = 0;
   }
-  __device__ __forceinline__ void put(uint32_t s, uint64_t fc, uint64_t bc, uint64_t hop, uint64_t,
-                                      uint64_t wc) {
+  __device__ __forceinline__ void put(uint32_t s, uint64_t fc, uint64_t bc, uint64_t hop, uint64_t) {
 #pragma unroll
     for (int i = 0; i + 1 < S; ++i) {
       f[i] = f[i + 1];
       b[i] = b[i + 1];
       c[i] = c[i + 1];
-      if (kZb) w[i] = w[i + 1];
     }
     f[S - 1] = (double)fc;
-    b[S - 1] = (double)(kZb ? bc - wc : bc);
-    if (kZb) w[S - 1] = (double)wc;
+    b[S - 1] = (double)bc;
     c[S - 1] = 0;
     if (S > 1 && s > 0) c[S - 2] = (double)hop;
   }
@@ -1416,38 +1417,54 @@ __device__ __forceinline__ bool pipe(const V (&f)[S], const V (&b)[S], const V (
   return true;
 }
 
-// Zero-bubble order (ZB-H1, Qi et al. 2024): pipe's evaluation order with the
-// backward split into B, the input gradient stage s-1 waits for (eb[s] = its
-// end), and W, the weight gradient.  After B(s, i) stage s runs W(s, i - s)
-// once i >= s -- a pure delay on the stage, its B having run before -- and
-// its last min(s, M) W passes at the end.  From i = S - 1 on every steady
-// iteration runs every stage's W, so the same map repeats and the periodic
-// shortcut applies as in pipe (state out_f[0..S-2], last[0..S-1]; eb is
-// rewritten before it is read).  kJump: shortcut pairs within the budget,
-// then the whole loop; otherwise the whole loop.
+// Zero-bubble order (ZB-H1, Qi et al. 2024): pipe's evaluation order with a
+// stage's backward pass b split into W = floor(b / 2), the weight gradient,
+// and B = b - W, the input gradient stage s-1 waits for (eb = its end).
+// After B(s, i) stage s runs W(s, i - s) once i >= s -- a pure delay on the
+// stage, its B having run before -- and its last min(s, M) W passes at the
+// end.  From i = S - 1 on every steady iteration runs every stage's W, so
+// the same map repeats and the periodic shortcut applies as in pipe (state
+// out_f[0..S-2], last[0..S-1]; the B end of stage s + 1 is read only by
+// stage s, right after, in the same iteration, so it is one carried value).
+// W is derived from b where it is used, so the recurrence keeps pipe's five
+// per-stage arrays: the empty asm makes the copy of b opaque, so that the
+// derivation is not hoisted out of the loops into a sixth array.  kJump:
+// shortcut pairs within the budget, then the whole loop; otherwise the
+// whole loop.
+__device__ __forceinline__ double half_down(double b) {
+  asm volatile("" : "+v"(b));
+  return __builtin_floor(b * 0.5);
+}
+__device__ __forceinline__ uint64_t half_down(uint64_t b) {
+  asm volatile("" : "+v"(b));
+  return b >> 1;
+}
+
 template <int S, typename V>
-__device__ __forceinline__ void zb_iter(const V (&f)[S], const V (&b)[S], const V (&w)[S], const V (&c)[S], int i,
-                                        int tr, V (&out_f)[S], V (&eb)[S], V (&last)[S]) {
+__device__ __forceinline__ void zb_iter(const V (&f)[S], const V (&b)[S], const V (&c)[S], int i, int tr,
+                                        V (&out_f)[S], V (&last)[S]) {
+  V eb = 0;
 #pragma unroll
   for (int s = S - 1; s >= 0; --s) {
+    const V w = half_down(b[s]);
     if (s > tr) {   // the stage still runs a forward in this iteration
       const V st = s == 0 ? last[0] : vmax(last[s], out_f[s - 1] + c[s - 1]);
       out_f[s] = st + f[s];
-      const V sb = s == S - 1 ? out_f[s] : vmax(out_f[s], eb[s + 1] + c[s]);
-      eb[s] = sb + b[s];
+      const V sb = s == S - 1 ? out_f[s] : vmax(out_f[s], eb + c[s]);
+      eb = sb + (b[s] - w);
     } else {
-      eb[s] = (s == S - 1 ? last[s] : vmax(last[s], eb[s + 1] + c[s])) + b[s];
+      eb = (s == S - 1 ? last[s] : vmax(last[s], eb + c[s])) + (b[s] - w);
     }
-    last[s] = eb[s] + (i >= s ? w[s] : (V)0);
+    last[s] = i >= s ? eb + w : eb;
   }
 }
 
 template <int S, typename V, bool kJump>
-__device__ __forceinline__ void pipe_zb(const V (&f)[S], const V (&b)[S], const V (&w)[S], const V (&c)[S],
-                                        uint32_t M, int& skipped, V (&last)[S]) {
-  V out_f[S], eb[S];
+__device__ __forceinline__ void pipe_zb(const V (&f)[S], const V (&b)[S], const V (&c)[S], uint32_t M, int& skipped,
+                                        V (&last)[S]) {
+  V out_f[S];
 #pragma unroll
-  for (int s = 0; s < S; ++s) out_f[s] = eb[s] = last[s] = 0;
+  for (int s = 0; s < S; ++s) out_f[s] = last[s] = 0;
   const int m_ = (int)M;
 #pragma unroll
   for (int m = 0; m < S - 1; ++m) {
@@ -1463,23 +1480,24 @@ __device__ __forceinline__ void pipe_zb(const V (&f)[S], const V (&b)[S], const 
   const int left = m_ - (S - 1);
   skipped = 0;
   int i = 0;
-  for (; i < left && i < S - 1; ++i) zb_iter<S, V>(f, b, w, c, i, -1, out_f, eb, last);
+  for (; i < left && i < S - 1; ++i) zb_iter<S, V>(f, b, c, i, -1, out_f, last);
   int rem = left - i;
   if (kJump) {
     int budget = kPeriodicBudget;
     while (rem >= 2 && budget > 0) {
-      zb_iter<S, V>(f, b, w, c, S, -1, out_f, eb, last);
+      zb_iter<S, V>(f, b, c, S, -1, out_f, last);
       bool same = true;
-      V lam = 0;
+      V lam = 0, eb = 0;
 #pragma unroll
       for (int s = S - 1; s >= 0; --s) {
+        const V w = half_down(b[s]);
         const V st = s == 0 ? last[0] : vmax(last[s], out_f[s - 1] + c[s - 1]);
         const V nf = st + f[s];
         if (s < S - 1) same = same && nf - out_f[s] == lam;
         out_f[s] = nf;
-        const V sb = s == S - 1 ? nf : vmax(nf, eb[s + 1] + c[s]);
-        eb[s] = sb + b[s];
-        const V nl = eb[s] + w[s];
+        const V sb = s == S - 1 ? nf : vmax(nf, eb + c[s]);
+        eb = sb + (b[s] - w);
+        const V nl = eb + w;
         if (s == S - 1) lam = nl - last[s];
         else same = same && nl - last[s] == lam;
         last[s] = nl;
@@ -1498,12 +1516,12 @@ __device__ __forceinline__ void pipe_zb(const V (&f)[S], const V (&b)[S], const 
       }
     }
   }
-  for (; rem > 0; --rem) zb_iter<S, V>(f, b, w, c, S, -1, out_f, eb, last);
+  for (; rem > 0; --rem) zb_iter<S, V>(f, b, c, S, -1, out_f, last);
 #pragma unroll
   for (int tr = 0; tr < S - 1; ++tr)
-    if (tr >= S - 1 - m_) zb_iter<S, V>(f, b, w, c, m_ - S + 1 + tr, tr, out_f, eb, last);
+    if (tr >= S - 1 - m_) zb_iter<S, V>(f, b, c, m_ - S + 1 + tr, tr, out_f, last);
 #pragma unroll
-  for (int s = 0; s < S; ++s) last[s] += (V)(s < m_ ? s : m_) * w[s];
+  for (int s = 0; s < S; ++s) last[s] += (V)(s < m_ ? s : m_) * half_down(b[s]);
 }
 
 // Integers below 2^53 are exact in fp64.  Every value the fp64 pass computes
@@ -1525,6 +1543,7 @@ struct EvalBufs {
   uint32_t* ovf;            // overflow list (fp64 result reached 2^53)
   uint32_t* deferred;       // deferred S-stage pipelines at [sstart[16 - S], ...)
   unsigned long long* skipped_ops;   // optional: recurrence ops skipped by the shortcut
+  const Tab* dtab;          // the Tab in device memory
 };
 
 // Pipelines are sorted by stage count (descending), so each group of four
@@ -1541,7 +1560,7 @@ struct EvalBufs {
 // aperiodic) and the overlapped sync.
 template <int S, bool kFull, int kMode, bool kHet, bool kOvl = false, bool kZb = false>
 __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot) {
-  RegSink<S, kZb> r;
+  RegSink<S> r;
   uint32_t M;
   {
     const Plan p = load_plan<kHet>(e.packed, e.pcut, slot);
@@ -1555,7 +1574,7 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
   int skipped;
   double last[S];
   bool done = true;
-  if constexpr (kZb) pipe_zb<S, double, true>(r.f, r.b, r.w, r.c, M, skipped, last);
+  if constexpr (kZb) pipe_zb<S, double, true>(r.f, r.b, r.c, M, skipped, last);
   else if constexpr (kOvl) done = pipe<S, double, true, true>(r.f, r.b, r.c, M, skipped, last);
   else done = pipe<S, double, !kFull>(r.f, r.b, r.c, M, skipped, last);
   // the DP tail reads the plan again (an L2 hit) rather than keeping it in
@@ -1587,9 +1606,13 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
 template <int S, int kMode, bool kHet>
 __device__ __forceinline__ void eval_deferred(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot) {
   const uint32_t hdr = kHet ? 0 : e.packed[slot >> 2].hdr;
-  if (!kHet && ((hdr >> 13) & 1)) eval_one<S, false, kMode, kHet, true>(t, h, e, slot);
-  else if (!kHet && ((hdr >> 16) & 1)) eval_one<S, false, kMode, kHet, false, true>(t, h, e, slot);
-  else eval_one<S, true, kMode, kHet>(t, h, e, slot);
+  if (!kHet && ((hdr >> 13) & 1)) {
+    eval_one<S, false, kMode, kHet, true>(t, h, e, slot);
+  } else if (!kHet && ((hdr >> 16) & 1)) {
+    eval_one<S, false, kMode, kHet, false, true>(t, h, e, slot);
+  } else {
+    eval_one<S, true, kMode, kHet>(t, h, e, slot);
+  }
 }
 
 // ---------------------------------------------------------------- interleaved 1F1B
@@ -1654,8 +1677,8 @@ __device__ __forceinline__ void il_setup(const Tab& t, const Hot<kMode>& h, cons
     for (int j = 0; j < v; ++j) {
       const int vs = j * S + s;
       const uint32_t lo = vs ? cut_at(p, vs - 1) : 0, hi = cut_at(p, vs);
-      uint64_t fc, bc, wc;
-      stage_cost<kMode, false>(t, h, p, k, ti, base, bq_in, bq_nic, lo, hi, vs == 0, vs == NV - 1, fc, bc, wc);
+      uint64_t fc, bc;
+      stage_cost<kMode, false>(t, h, p, k, ti, base, bq_in, bq_nic, lo, hi, vs == 0, vs == NV - 1, fc, bc);
       f[vs] = (V)fc;
       b[vs] = (V)bc;
     }
@@ -1909,9 +1932,13 @@ __device__ __forceinline__ void il_tile(const Tab& t, const Hot<kMode>& h, const
 // pipelines (shared layout; sorted ids [sstart[16], sstart[16 + 21]), so a
 // tile mostly holds one (S, v) and one micro-batch count), then the
 // deferred S-stage pipelines at [sstart[16 - S], + ctr[1 + 16 - S]), tile q
-// located by walking the sixteen list lengths (16 stages first).
+// located by walking the sixteen list lengths (16 stages first).  The Tab
+// is read from its copy in device memory: this kernel holds every pipeline
+// kind's code, and with the Tab as a by-value argument the compiler copied
+// the whole argument block to private memory in every wave.
 template <int kMode, bool kHet>
-__global__ void __launch_bounds__(kEvalThreads) k_deferred(Tab t, EvalBufs e) {
+__global__ void __launch_bounds__(kEvalThreads) k_deferred(const Tab* __restrict__ tp, EvalBufs e) {
+  const Tab& t = *tp;
   extern __shared__ uint4 lds[];
   fill_lds<kMode>(t, lds);
   const Hot<kMode> h(t, lds);
@@ -1955,19 +1982,18 @@ __global__ void __launch_bounds__(kEvalThreads) k_deferred(Tab t, EvalBufs e) {
 }
 
 // Pipelines whose fp64 time reached 2^53 ps, again in u64 (exact below 2^64).
-// wz: the weight-gradient parts of a zero-bubble pipeline, else nullptr.
+// zb: the zero-bubble order.
 template <int S>
-__device__ __forceinline__ uint64_t redo_one(const StageRec& R, const uint64_t* wz, uint32_t M) {
-  uint64_t f[S], b[S], c[S], w[S], last[S];
+__device__ __forceinline__ uint64_t redo_one(const StageRec& R, bool zb, uint32_t M) {
+  uint64_t f[S], b[S], c[S], last[S];
 #pragma unroll
   for (int s = 0; s < S; ++s) {
     f[s] = R[s][0];
-    w[s] = wz ? wz[s] : 0;
-    b[s] = R[s][1] - w[s];
+    b[s] = R[s][1];
     c[s] = R[s][2];
   }
   int skipped;
-  if (wz) pipe_zb<S, uint64_t, false>(f, b, w, c, M, skipped, last);
+  if (zb) pipe_zb<S, uint64_t, false>(f, b, c, M, skipped, last);
   else pipe<S, uint64_t, false>(f, b, c, M, skipped, last);
   uint64_t T = 0;
 #pragma unroll
@@ -1999,9 +2025,8 @@ __global__ void __launch_bounds__(64) k_redo_u64(Tab t, EvalBufs e) {
       continue;
     }
     StageRec R;
-    uint64_t wz[kMaxStages];
-    const uint64_t* w = !kHet && p.zb ? wz : nullptr;
-    RecSink sink{R, !kHet && p.zb ? wz : nullptr};
+    const bool w = !kHet && p.zb;
+    RecSink sink{R};
     class_setup<2, kHet>(t, h, p, slot & 3, sink, kHet ? e.pcut + (slot & ~3u) : nullptr);
     uint64_t r;
     switch (S) {
@@ -2186,7 +2211,7 @@ int eval_grids(Tab* t) {
 
 static EvalBufs bufs(const EvalArgs& a) {
   return {a.packed, (const uint4*)a.pcut, a.hdp, a.meta, a.ids, a.sstart, a.out, a.ctr, a.ctr + kEvalCounters, a.deferred,
-          (unsigned long long*)a.skipped_ops};
+          (unsigned long long*)a.skipped_ops, a.dtab};
 }
 
 // first pass of one stage-count group (g = 0..3) over a chunk
@@ -2237,9 +2262,9 @@ static void launch_deferred_het(const Tab& t, const EvalBufs& e, uint32_t max_ta
   int g = blocks_for(max_tasks, kEvalThreads);
   const size_t lds = t.mode < 2 ? t.lds_bytes : 0;
   g = g < 1 ? 1 : (g > (int)t.grid_deferred ? (int)t.grid_deferred : g);
-  if (t.mode == 0) k_deferred<0, kHet><<<g, kEvalThreads, lds, s>>>(t, e);
-  else if (t.mode == 1) k_deferred<1, kHet><<<g, kEvalThreads, lds, s>>>(t, e);
-  else k_deferred<2, kHet><<<g, kEvalThreads, 0, s>>>(t, e);
+  if (t.mode == 0) k_deferred<0, kHet><<<g, kEvalThreads, lds, s>>>(e.dtab, e);
+  else if (t.mode == 1) k_deferred<1, kHet><<<g, kEvalThreads, lds, s>>>(e.dtab, e);
+  else k_deferred<2, kHet><<<g, kEvalThreads, 0, s>>>(e.dtab, e);
   k_redo_u64<kHet><<<32, 64, 0, s>>>(t, e);
 }
 
