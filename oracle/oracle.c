@@ -103,6 +103,7 @@ typedef struct {
   int mem_check;         /* 0: capacities not given, memory not checked */
   int rail_only;         /* 1: rail-only inter-node network (R47) */
   int ccl_tree;          /* 1: all-reduces take the faster of ring and tree (R48) */
+  int contention;        /* 1: concurrent segment syncs of a stage share its links (R49) */
   uint32_t* nic_dev;    /* NULL or per-device NIC MB/s, pool order */
   uint32_t* intra_node; /* NULL or per-node intra MB/s, pool order */
 } or_cluster;
@@ -650,6 +651,25 @@ static uint64_t dp_sync_cl(const or_ctx* x, uint64_t p, uint64_t zero, uint64_t 
   return r;
 }
 
+/* R49: the same sync split into its latency steps and the time its bytes
+ * take on the link (the part concurrent collectives on one link share); the
+ * tree is taken only when strictly faster, as above */
+static void dp_parts(const or_ctx* x, uint64_t p, uint64_t zero, uint64_t grads, uint64_t params, uint64_t alpha,
+                     uint64_t bq, uint64_t* lat, uint64_t* bw) {
+  *lat = 0;
+  *bw = 0;
+  if (p <= 1) return;
+  *lat = mul(2 * (p - 1), alpha);
+  if (!zero) *bw = link_time(mul(2 * (p - 1), cdiv(grads, p)), bq);
+  else *bw = add(link_time(mul(p - 1, cdiv(grads, p)), bq), link_time(mul(p - 1, cdiv(params, p)), bq));
+  if (x->c.ccl_tree && !zero) {
+    uint64_t lg = 0;
+    while ((1ull << lg) < p) ++lg;
+    uint64_t tl = mul(2 * lg, alpha), tb = link_time(mul(2, grads), bq);
+    if (add(tl, tb) < add(*lat, *bw)) { *lat = tl; *bw = tb; }
+  }
+}
+
 /* parameters of layers [a, b) held by one rank at TP t, EP ep: non-expert
  * part (with the embedding if a = 0 and the head if b = L) and expert part */
 static void span_params(const or_ctx* x, uint64_t a, uint64_t b, uint64_t t, uint64_t ep, uint64_t* pd,
@@ -919,6 +939,9 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
     }
   for (uint64_t g = 0; g < G; ++g) for (uint64_t s = 0; s < OR_MAXS; ++s) d->tdp[g][s] = 0;
   uint64_t seg_alpha[OR_MAXG * OR_MAXS], seg_bq[OR_MAXG * OR_MAXS];
+  uint64_t seg_lat[OR_MAXG][OR_MAXS], seg_bw[OR_MAXG][OR_MAXS];
+  memset(seg_lat, 0, sizeof(seg_lat));
+  memset(seg_bw, 0, sizeof(seg_bw));
   for (uint64_t j = 0; j + 1 < nb; ++j) {
     uint64_t a = bnd[j], e = bnd[j + 1];
     uint64_t sg[OR_MAXG];
@@ -940,18 +963,34 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
      * each TP group: a ring all-gather over tp/tp_min members of the
      * class's own gradient shard, on the group's node fabric; classes
      * reshard at the same time, so the slowest counts */
-    uint64_t rs = 0;
+    uint64_t rs = 0, rs_lat = 0, rs_bw = 0;
     for (uint64_t g = 0; g < G; ++g) {
       if (p->tp[g] == tp_min) continue;
       uint64_t qd, qe;
       span_params(x, a, e, p->tp[g], ep, &qd, &qe);
       int k = p->type[g][sg[g]];
-      uint64_t r = ring(p->tp[g] / tp_min - 1, mul(m->grad_bytes, add(qd, qe)), cl->a_intra[k],
-                        intra_max(x, k, base[g][sg[g]], p->reps[g] * p->tp[g]));
-      rs = umax(rs, r);
+      uint64_t steps = p->tp[g] / tp_min - 1, chunk = mul(m->grad_bytes, add(qd, qe));
+      uint64_t bqi = intra_max(x, k, base[g][sg[g]], p->reps[g] * p->tp[g]);
+      uint64_t r = ring(steps, chunk, cl->a_intra[k], bqi);
+      if (r > rs) { rs = r; rs_lat = mul(steps, cl->a_intra[k]); rs_bw = link_time(mul(steps, chunk), bqi); }
     }
     t = add(t, rs);
-    for (uint64_t g = 0; g < G; ++g) d->tdp[g][sg[g]] = umax(d->tdp[g][sg[g]], t);
+    if (!cl->contention) {
+      for (uint64_t g = 0; g < G; ++g) d->tdp[g][sg[g]] = umax(d->tdp[g][sg[g]], t);
+    } else {
+      /* R49: the segments a stage holds sync at the same time over the same
+       * devices, so their link times add up while their latencies overlap */
+      uint64_t ld, bd, le = 0, be = 0;
+      dp_parts(x, p_all, p->zero, mul(m->grad_bytes, pd), mul(m->param_bytes, pd), alpha, bq, &ld, &bd);
+      if (m->E) dp_parts(x, p_all / ep, p->zero, mul(m->grad_bytes, pe), mul(m->param_bytes, pe), alpha, bq, &le, &be);
+      uint64_t lat = add(add(ld, le), rs_lat), bw = add(add(bd, be), rs_bw);
+      if (add(lat, bw) != t) or_die("contention: split does not add up");
+      for (uint64_t g = 0; g < G; ++g) {
+        seg_lat[g][sg[g]] = umax(seg_lat[g][sg[g]], lat);
+        seg_bw[g][sg[g]] = add(seg_bw[g][sg[g]], bw);
+        d->tdp[g][sg[g]] = add(seg_lat[g][sg[g]], seg_bw[g][sg[g]]);
+      }
+    }
   }
 
   /* per class pipeline; a segment's sync starts when every stage holding it
@@ -1164,6 +1203,7 @@ or_ctx* oracle_new(const uint64_t* mp, const uint32_t* q, const uint64_t* cp,
   }
   c->rail_only = cp[1 + 11 * c->K] != 0;
   c->ccl_tree = cp[2 + 11 * c->K] != 0;
+  c->contention = cp[3 + 11 * c->K] != 0;
   if (nic_dev) { c->nic_dev = (uint32_t*)malloc(4 * dsum); memcpy(c->nic_dev, nic_dev, 4 * dsum); }
   if (intra_node) { c->intra_node = (uint32_t*)malloc(4 * nsum); memcpy(c->intra_node, intra_node, 4 * nsum); }
   x->Vp = cdiv(m->vocab, 128) * 128;

@@ -108,6 +108,7 @@ def _cluster_words(c):
         w += [t[k] for k in TYPE_KEYS] + [t.get("mem_bytes") or 0]
     w.append(1 if c.get("rail_only") else 0)
     w.append(1 if c.get("ccl_tree") else 0)
+    w.append(1 if c.get("contention") else 0)
     return np.array(w, dtype=np.uint64)
 
 
