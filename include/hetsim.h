@@ -109,6 +109,12 @@ typedef struct {
                                        2 ceil(log2 p) latencies plus twice the gradient bytes at the
                                        ring's slowest rate, as a collective library picks an algorithm
                                        per call (Sec. 4.1 [C3]); 0: rings only */
+  uint32_t contention;              /* 1: with the per-class layout, the syncs of the layer segments a
+                                       stage holds run at the same time over the same devices and share
+                                       their links: the stage waits for the largest latency part plus
+                                       the sum of the link-time parts (each segment: its rings' message
+                                       latencies, then their bytes at the slowest rate, resharding
+                                       included); 0: concurrent syncs do not slow each other */
 } sim_cluster_desc;
 
 /*

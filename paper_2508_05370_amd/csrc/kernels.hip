@@ -90,6 +90,28 @@ __device__ __forceinline__ uint64_t ring_sync(uint32_t p, double rp, uint32_t ze
   return 2 * steps * alpha + link_ps(steps * g, bq) + link_ps(steps * div_up(params, p, rp), bq);
 }
 
+// The same sync as latency steps and link time (the part that concurrent
+// syncs over the same links share); the tree only when strictly faster.
+__device__ __forceinline__ void ring_parts(uint32_t p, double rp, uint32_t zero, uint64_t grads, uint64_t params,
+                                           uint64_t alpha, uint32_t bq, uint32_t tree, uint64_t& lat, uint64_t& bw) {
+  const uint64_t g = div_up(grads, p, rp);
+  lat = 2ull * (p - 1) * alpha;
+  if (!zero) {
+    bw = link_ps(2ull * (p - 1) * g, bq);
+    if (tree && p > 1) {
+      const uint64_t lg = 32 - __builtin_clz(p - 1);
+      const uint64_t tl = 2 * lg * alpha, tb = link_ps(2 * grads, bq);
+      if (tl + tb < lat + bw) {
+        lat = tl;
+        bw = tb;
+      }
+    }
+  } else {
+    const uint64_t steps = p - 1;
+    bw = link_ps(steps * g, bq) + link_ps(steps * div_up(params, p, rp), bq);
+  }
+}
+
 // micro-batch counts: exact up to 64, then steps of 16 up to 1088
 __device__ __forceinline__ uint32_t m_bucket(uint32_t M) {
   if (M <= 64) return M - 1;
@@ -739,7 +761,8 @@ __device__ __forceinline__ uint32_t row_word(const uint4 (&rows)[4], uint32_t c,
 
 template <int kMode>
 __device__ __forceinline__ uint64_t seg_dp(const Tab& t, const Hot<kMode>& h, const Plan& p, const uint4 (&rows)[4],
-                                           uint32_t a, uint32_t e, double rp, double rpe) {
+                                           uint32_t a, uint32_t e, double rp, double rpe, uint64_t& lat,
+                                           uint64_t& bw) {
   const uint32_t G = p.G, epl = p.epl, ns = e - a;
   uint32_t tmin = 3;
 #pragma unroll
@@ -747,7 +770,7 @@ __device__ __forceinline__ uint64_t seg_dp(const Tab& t, const Hot<kMode>& h, co
     if (c2 < G) tmin = cls_tpl(p.chdr, c2) < tmin ? cls_tpl(p.chdr, c2) : tmin;
   bool same = true;
   uint32_t k0 = 0, nmin = 0xffffffffu, nmax = 0, bq_dp = 0;
-  uint64_t a_dp = 0, rs = 0;
+  uint64_t a_dp = 0, rs = 0, rs_l = 0, rs_b = 0;
 #pragma unroll
   for (uint32_t c2 = 0; c2 < 4; ++c2) {
     if (c2 >= G) continue;
@@ -780,8 +803,12 @@ __device__ __forceinline__ uint64_t seg_dp(const Tab& t, const Hot<kMode>& h, co
       const uint64_t sh = (uint64_t)ns * (t.par_layer[tpl2] + t.par_expert[tpl2][epl]) +
                           (a == 0 ? t.par_embed[tpl2] : 0) + (e == t.L ? t.par_head[tpl2] : 0);
       const uint32_t bq_in = range_max(h.rmi(), t.N, l2, h2);
-      const uint64_t r = g1 * t2.a_intra + link_ps(g1 * t.grad_bytes * sh, bq_in);
-      rs = r > rs ? r : rs;
+      const uint64_t rl = g1 * t2.a_intra, rb = link_ps(g1 * t.grad_bytes * sh, bq_in), r = rl + rb;
+      if (r > rs) {
+        rs = r;
+        rs_l = rl;
+        rs_b = rb;
+      }
     }
   }
   const bool intra = same && nmin == nmax;
@@ -789,22 +816,26 @@ __device__ __forceinline__ uint64_t seg_dp(const Tab& t, const Hot<kMode>& h, co
   const uint32_t bq = intra ? h.rmi()[nmin] : bq_dp;
   const uint64_t pd = (uint64_t)ns * t.par_layer[tmin] + (a == 0 ? t.par_embed[tmin] : 0) +
                       (e == t.L ? t.par_head[tmin] : 0);
-  uint64_t tdp = p.psum <= 1 ? 0 : ring_sync(p.psum, rp, p.zero, t.grad_bytes * pd, t.param_bytes * pd, alpha, bq, t.ccl_tree);
+  uint64_t ld = 0, bd = 0, le = 0, be = 0;
+  if (p.psum > 1) ring_parts(p.psum, rp, p.zero, t.grad_bytes * pd, t.param_bytes * pd, alpha, bq, t.ccl_tree, ld, bd);
   const uint32_t pe = p.psum >> epl;
   if (t.E && pe > 1) {
     const uint64_t px = (uint64_t)ns * t.par_expert[tmin][epl];
-    tdp += ring_sync(pe, rpe, p.zero, t.grad_bytes * px, t.param_bytes * px, alpha, bq, t.ccl_tree);
+    ring_parts(pe, rpe, p.zero, t.grad_bytes * px, t.param_bytes * px, alpha, bq, t.ccl_tree, le, be);
   }
-  return tdp + rs;
+  lat = ld + le + rs_l;
+  bw = bd + be + rs_b;
+  return lat + bw;
 }
 
 // The sync a stage [lo, hi) of the pipeline's class waits for: the longest
-// of the segments inside it.
+// of the segments inside it, or with contention the largest latency part
+// plus the sum of the link-time parts.
 template <int kMode>
 __device__ __forceinline__ uint64_t het_stage_dp(const Tab& t, const Hot<kMode>& h, const Plan& p,
                                                  const uint4 (&rows)[4], uint32_t lo, uint32_t hi, double rp,
                                                  double rpe) {
-  uint64_t best = 0;
+  uint64_t best = 0, lmax = 0, bsum = 0;
   for (uint32_t a = lo; a < hi;) {
     uint32_t e = hi;   // the next cut of any class above a
 #pragma unroll
@@ -818,11 +849,14 @@ __device__ __forceinline__ uint64_t het_stage_dp(const Tab& t, const Hot<kMode>&
           e = (v > a && v < e) ? v : e;
         }
       }
-    const uint64_t x = seg_dp(t, h, p, rows, a, e, rp, rpe);
+    uint64_t sl, sb;
+    const uint64_t x = seg_dp(t, h, p, rows, a, e, rp, rpe, sl, sb);
     best = x > best ? x : best;
+    lmax = sl > lmax ? sl : lmax;
+    bsum += sb;
     a = e;
   }
-  return best;
+  return t.contention ? lmax + bsum : best;
 }
 
 __device__ __forceinline__ void load_rows(const uint4* prow, uint4 (&rows)[4]) {
@@ -856,19 +890,22 @@ __device__ __forceinline__ void het_plan_syncs(const Tab& t, const Hot<kMode>& h
   // per class: current stage and its end, and that stage's type, node range,
   // worst NIC/PCIe rate, inter-node latency, node latency, worst node fabric;
   // classes enter their first stage at the walk's first step
+  // cur: the stage's sync so far -- the longest segment, or with contention
+  // the largest latency part (cur) and the summed link times (curb)
   uint32_t stg[4], nxt[4], kk[4], nl[4], nh[4], bx[4], bin[4];
-  uint64_t as2[4], ain[4], cur[4];
+  uint64_t as2[4], ain[4], cur[4], curb[4];
 #pragma unroll
   for (uint32_t c2 = 0; c2 < 4; ++c2) {
     stg[c2] = 0xffffffffu; nxt[c2] = c2 < G ? 0 : 0xffffffffu; kk[c2] = 0; nl[c2] = 0; nh[c2] = 0; bx[c2] = 0;
-    bin[c2] = 0; as2[c2] = 0; ain[c2] = 0; cur[c2] = 0;
+    bin[c2] = 0; as2[c2] = 0; ain[c2] = 0; cur[c2] = 0; curb[c2] = 0;
   }
   for (uint32_t a = 0; a < t.L;) {
 #pragma unroll
     for (uint32_t c2 = 0; c2 < 4; ++c2) {
       if (nxt[c2] == a) {   // the walk crossed one of class c2's cuts (or starts)
-        if (a > 0) drow[c2 * kMaxStages + stg[c2]] = cur[c2];
+        if (a > 0) drow[c2 * kMaxStages + stg[c2]] = cur[c2] + curb[c2];
         cur[c2] = 0;
+        curb[c2] = 0;
         const uint32_t s2 = ++stg[c2], tpl2 = cls_tpl(p.chdr, c2);
         const uint32_t k2 = (uint32_t)(p.tv[c2] >> (4 * s2)) & 15;
         const TypeInfo t2 = h.type(k2);
@@ -894,7 +931,7 @@ __device__ __forceinline__ void het_plan_syncs(const Tab& t, const Hot<kMode>& h
     const uint32_t ns = e - a;
     bool same = true;
     uint32_t nmin = 0xffffffffu, nmax = 0, bq_dp = 0;
-    uint64_t a_dp = 0, rs = 0;
+    uint64_t a_dp = 0, rs = 0, rs_l = 0, rs_b = 0;
 #pragma unroll
     for (uint32_t c2 = 0; c2 < 4; ++c2) {
       if (c2 >= G) continue;
@@ -908,8 +945,12 @@ __device__ __forceinline__ void het_plan_syncs(const Tab& t, const Hot<kMode>& h
         const uint64_t g1 = (1u << (tpl2 - tmin)) - 1;
         const uint64_t sh = (uint64_t)ns * (t.par_layer[tpl2] + t.par_expert[tpl2][epl]) +
                             (a == 0 ? t.par_embed[tpl2] : 0) + (e == t.L ? t.par_head[tpl2] : 0);
-        const uint64_t r = g1 * ain[c2] + link_ps(g1 * t.grad_bytes * sh, bin[c2]);
-        rs = r > rs ? r : rs;
+        const uint64_t rl = g1 * ain[c2], rb = link_ps(g1 * t.grad_bytes * sh, bin[c2]), r = rl + rb;
+        if (r > rs) {
+          rs = r;
+          rs_l = rl;
+          rs_b = rb;
+        }
       }
     }
     const bool intra = same && nmin == nmax;
@@ -917,21 +958,38 @@ __device__ __forceinline__ void het_plan_syncs(const Tab& t, const Hot<kMode>& h
     const uint32_t bq = intra ? h.rmi()[nmin] : bq_dp;
     const uint64_t pd = (uint64_t)ns * t.par_layer[tmin] + (a == 0 ? t.par_embed[tmin] : 0) +
                         (e == t.L ? t.par_head[tmin] : 0);
-    uint64_t x = p.psum <= 1 ? 0 : ring_sync(p.psum, rp, p.zero, t.grad_bytes * pd, t.param_bytes * pd, alpha, bq, t.ccl_tree);
-    const uint32_t pe = p.psum >> epl;
-    if (t.E && pe > 1) {
-      const uint64_t px = (uint64_t)ns * t.par_expert[tmin][epl];
-      x += ring_sync(pe, rpe, p.zero, t.grad_bytes * px, t.param_bytes * px, alpha, bq, t.ccl_tree);
-    }
-    x += rs;
+    if (!t.contention) {
+      uint64_t x = p.psum <= 1 ? 0 : ring_sync(p.psum, rp, p.zero, t.grad_bytes * pd, t.param_bytes * pd, alpha, bq, t.ccl_tree);
+      const uint32_t pe = p.psum >> epl;
+      if (t.E && pe > 1) {
+        const uint64_t px = (uint64_t)ns * t.par_expert[tmin][epl];
+        x += ring_sync(pe, rpe, p.zero, t.grad_bytes * px, t.param_bytes * px, alpha, bq, t.ccl_tree);
+      }
+      x += rs;
 #pragma unroll
-    for (uint32_t c2 = 0; c2 < 4; ++c2)
-      if (c2 < G) cur[c2] = x > cur[c2] ? x : cur[c2];
+      for (uint32_t c2 = 0; c2 < 4; ++c2)
+        if (c2 < G) cur[c2] = x > cur[c2] ? x : cur[c2];
+    } else {
+      uint64_t ld = 0, bd = 0, le = 0, be = 0;
+      if (p.psum > 1) ring_parts(p.psum, rp, p.zero, t.grad_bytes * pd, t.param_bytes * pd, alpha, bq, t.ccl_tree, ld, bd);
+      const uint32_t pe = p.psum >> epl;
+      if (t.E && pe > 1) {
+        const uint64_t px = (uint64_t)ns * t.par_expert[tmin][epl];
+        ring_parts(pe, rpe, p.zero, t.grad_bytes * px, t.param_bytes * px, alpha, bq, t.ccl_tree, le, be);
+      }
+      const uint64_t l = ld + le + rs_l, b = bd + be + rs_b;
+#pragma unroll
+      for (uint32_t c2 = 0; c2 < 4; ++c2)
+        if (c2 < G) {
+          cur[c2] = l > cur[c2] ? l : cur[c2];
+          curb[c2] += b;
+        }
+    }
     a = e;
   }
 #pragma unroll
   for (uint32_t c2 = 0; c2 < 4; ++c2)
-    if (c2 < G) drow[c2 * kMaxStages + stg[c2]] = cur[c2];
+    if (c2 < G) drow[c2 * kMaxStages + stg[c2]] = cur[c2] + curb[c2];
 }
 
 // Forward and backward time of one micro-batch over layers [lo, hi) on the
