@@ -104,6 +104,7 @@ typedef struct {
   int rail_only;         /* 1: rail-only inter-node network (R47) */
   int ccl_tree;          /* 1: all-reduces take the faster of ring and tree (R48) */
   int contention;        /* 1: concurrent segment syncs of a stage share its links (R49) */
+  int ccl_hier;          /* 1: all-reduces over whole nodes may take the two-level algorithm (R50) */
   uint32_t* nic_dev;    /* NULL or per-device NIC MB/s, pool order */
   uint32_t* intra_node; /* NULL or per-node intra MB/s, pool order */
 } or_cluster;
@@ -392,6 +393,7 @@ typedef struct {
   uint64_t overlap;      /* 1: gradient sync overlapped with the last backward pass (R38) */
   uint64_t v;            /* model chunks per device: 1 = plain 1F1B, 2..4 interleaved (R41) */
   uint64_t zb;           /* 1: backward split into input and weight gradients, zero-bubble order (R44) */
+  int het;               /* 1: per-class layout */
   uint64_t tp[OR_MAXG], S[OR_MAXG];
   uint64_t cut[OR_MAXG][OR_MAXS];
   uint64_t reps[OR_MAXG], nmb[OR_MAXG];
@@ -438,6 +440,7 @@ static int decode_rules(const or_ctx* x, const or_planes* q, int64_t i, or_plan*
   if (hdr >> 17) return 0;                                   /* V7 reserved bits */
   p->overlap = (hdr >> 13) & 1;
   p->v = ((hdr >> 14) & 3) + 1;
+  p->het = q->chdr != NULL;
   p->zb = (hdr >> 16) & 1;
   if (p->zb && (p->overlap || p->v > 1)) return 0;           /* V13 (R45) */
   p->ep = 1ull << ((hdr >> 2) & 3);
@@ -819,6 +822,45 @@ static void dp_link(const or_ctx* x, const or_plan* p, uint64_t base[OR_MAXG][OR
   *bq_out = bq;
 }
 
+/* R50: the shape of the DP group of stage sg[g] of every class for the
+ * two-level all-reduce: usable when the classes' devices fill whole nodes
+ * with the same number g > 1 of members (TP groups) in every node, over
+ * N > 1 nodes; a_in, bq_in: the worst node latency and fabric rate. */
+typedef struct { int ok; uint64_t g, N, a_in, bq_in; } or_hier;
+static or_hier hier_shape(const or_ctx* x, const or_plan* p, uint64_t base[OR_MAXG][OR_MAXS], const uint64_t* sg) {
+  const or_cluster* cl = &x->c;
+  or_hier h = {1, 0, 0, 0, 0};
+  for (uint64_t g = 0; g < p->G; ++g) {
+    int k = p->type[g][sg[g]];
+    uint64_t b = base[g][sg[g]], n = p->reps[g] * p->tp[g], d = cl->dpn[k];
+    if (b % d || n % d) { h.ok = 0; return h; }
+    uint64_t gm = d / p->tp[g];
+    if (g > 0 && gm != h.g) { h.ok = 0; return h; }
+    h.g = gm;
+    h.N += n / d;
+    h.a_in = umax(h.a_in, cl->a_intra[k]);
+    h.bq_in = umax(h.bq_in, intra_max(x, k, b, n));
+  }
+  h.ok = h.g > 1 && h.N > 1;
+  return h;
+}
+/* two-level all-reduce: reduce-scatter inside each node (g - 1 steps of a
+ * 1/g shard on the node fabric), ring all-reduce of each shard across the
+ * N nodes on the group's inter-node tier, all-gather inside each node */
+static uint64_t hier_allreduce(const or_hier* h, uint64_t grads, uint64_t alpha, uint64_t bq) {
+  uint64_t sh = cdiv(grads, h->g);
+  return add(add(mul(2 * (h->g - 1), h->a_in), link_time(mul(2 * (h->g - 1), sh), h->bq_in)),
+             add(mul(2 * (h->N - 1), alpha), link_time(mul(2 * (h->N - 1), cdiv(sh, h->N)), bq)));
+}
+/* a dense DP sync with the cluster's algorithms: ring, tree (R48), and
+ * the two-level all-reduce where the group allows it (R50; no ZeRO) */
+static uint64_t dp_sync_h(const or_ctx* x, const or_hier* h, uint64_t p, uint64_t zero, uint64_t grads,
+                          uint64_t params, uint64_t alpha, uint64_t bq) {
+  uint64_t r = dp_sync_cl(x, p, zero, grads, params, alpha, bq);
+  if (x->c.ccl_hier && h && h->ok && !zero && p > 1) r = umin(r, hier_allreduce(h, grads, alpha, bq));
+  return r;
+}
+
 static void eval_plan_interleaved(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t* scratch);
 
 /* R44-R46: zero-bubble order (ZB-H1 of Qi et al. 2024, "Zero Bubble
@@ -940,6 +982,7 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
   for (uint64_t g = 0; g < G; ++g) for (uint64_t s = 0; s < OR_MAXS; ++s) d->tdp[g][s] = 0;
   uint64_t seg_alpha[OR_MAXG * OR_MAXS], seg_bq[OR_MAXG * OR_MAXS];
   uint64_t seg_lat[OR_MAXG][OR_MAXS], seg_bw[OR_MAXG][OR_MAXS];
+  or_hier seg_h[OR_MAXG * OR_MAXS];
   memset(seg_lat, 0, sizeof(seg_lat));
   memset(seg_bw, 0, sizeof(seg_bw));
   for (uint64_t j = 0; j + 1 < nb; ++j) {
@@ -954,10 +997,12 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
     dp_link(x, p, base, sg, &alpha, &bq);
     seg_alpha[j] = alpha;
     seg_bq[j] = bq;
+    seg_h[j] = hier_shape(x, p, base, sg);
     /* R36: the ring runs on the coarsest TP layout among the classes */
     uint64_t pd, pe;
     span_params(x, a, e, tp_min, ep, &pd, &pe);
-    uint64_t t = dp_sync_cl(x, p_all, p->zero, mul(m->grad_bytes, pd), mul(m->param_bytes, pd), alpha, bq);
+    uint64_t t = dp_sync_h(x, p->het ? NULL : &seg_h[j], p_all, p->zero, mul(m->grad_bytes, pd),
+                           mul(m->param_bytes, pd), alpha, bq);
     if (m->E) t = add(t, dp_sync_cl(x, p_all / ep, p->zero, mul(m->grad_bytes, pe), mul(m->param_bytes, pe), alpha, bq));
     /* R36: classes with finer shards first gather the coarse shard inside
      * each TP group: a ring all-gather over tp/tp_min members of the
@@ -1037,8 +1082,8 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
         uint64_t ready = d->end[g][s] - bsum, c = 0;
         for (uint64_t j = 0; j < nbk; ++j) {
           ready = add(ready, comp[j]);
-          uint64_t dj = dp_sync_cl(x, p_all, p->zero, mul(m->grad_bytes, pd[j]), mul(m->param_bytes, pd[j]),
-                                seg_alpha[s], seg_bq[s]);
+          uint64_t dj = dp_sync_h(x, &seg_h[s], p_all, p->zero, mul(m->grad_bytes, pd[j]),
+                                  mul(m->param_bytes, pd[j]), seg_alpha[s], seg_bq[s]);
           if (m->E && pe[j])
             dj = add(dj, dp_sync_cl(x, p_all / ep, p->zero, mul(m->grad_bytes, pe[j]), mul(m->param_bytes, pe[j]),
                                  seg_alpha[s], seg_bq[s]));
@@ -1152,7 +1197,8 @@ static void eval_plan_interleaved(const or_ctx* x, const or_plan* p, or_detail* 
     uint64_t pd = mul(ns, layer_params_dense(x, tp)), pe = mul(ns, layer_params_expert(x, tp, ep));
     if (s == 0) pd = add(pd, embed_params(x, tp));
     if (s == S - 1) pd = add(pd, head_params(x, tp));
-    uint64_t t = dp_sync_cl(x, p_all, p->zero, mul(m->grad_bytes, pd), mul(m->param_bytes, pd), alpha, bq);
+    or_hier hs = hier_shape(x, p, base, sg);
+    uint64_t t = dp_sync_h(x, &hs, p_all, p->zero, mul(m->grad_bytes, pd), mul(m->param_bytes, pd), alpha, bq);
     if (m->E) t = add(t, dp_sync_cl(x, p_all / ep, p->zero, mul(m->grad_bytes, pe), mul(m->param_bytes, pe), alpha, bq));
     tdp[s] = t;
   }
@@ -1204,6 +1250,7 @@ or_ctx* oracle_new(const uint64_t* mp, const uint32_t* q, const uint64_t* cp,
   c->rail_only = cp[1 + 11 * c->K] != 0;
   c->ccl_tree = cp[2 + 11 * c->K] != 0;
   c->contention = cp[3 + 11 * c->K] != 0;
+  c->ccl_hier = cp[4 + 11 * c->K] != 0;
   if (nic_dev) { c->nic_dev = (uint32_t*)malloc(4 * dsum); memcpy(c->nic_dev, nic_dev, 4 * dsum); }
   if (intra_node) { c->intra_node = (uint32_t*)malloc(4 * nsum); memcpy(c->intra_node, intra_node, 4 * nsum); }
   x->Vp = cdiv(m->vocab, 128) * 128;
@@ -1318,6 +1365,11 @@ void oracle_pipeline_interleaved(uint64_t S, uint64_t v, uint64_t M, const uint6
 uint64_t oracle_alpha_ps(uint64_t gbps_unidir) { return cdiv(9200ull * 8 * 1000, gbps_unidir); }
 uint64_t oracle_beta_q(uint64_t MBps) { return beta_q(MBps); }
 uint64_t oracle_link_time(uint64_t bytes, uint64_t bq) { return link_time(bytes, bq); }
+uint64_t oracle_hier_allreduce(uint64_t g, uint64_t N, uint64_t grads, uint64_t a_in, uint64_t MBps_in, uint64_t alpha,
+                               uint64_t MBps) {
+  or_hier h = {1, g, N, a_in, beta_q(MBps_in)};
+  return hier_allreduce(&h, grads, alpha, beta_q(MBps));
+}
 uint64_t oracle_tree_allreduce(uint64_t p, uint64_t grads, uint64_t alpha, uint64_t MBps) {
   return tree_allreduce(p, grads, alpha, beta_q(MBps));
 }

@@ -55,6 +55,8 @@ def lib():
         L.oracle_dp_sync.argtypes = [u64, u64, u64, u64, u64, u64]
         L.oracle_tree_allreduce.argtypes = [u64, u64, u64, u64]
         L.oracle_tree_allreduce.restype = u64
+        L.oracle_hier_allreduce.argtypes = [u64] * 7
+        L.oracle_hier_allreduce.restype = u64
         L.oracle_dp_sync.restype = u64
         L.oracle_layer_time.argtypes = [P, C.c_int, u64, u64, u64, u64, C.c_int]
         L.oracle_layer_time.restype = u64
@@ -109,6 +111,7 @@ def _cluster_words(c):
     w.append(1 if c.get("rail_only") else 0)
     w.append(1 if c.get("ccl_tree") else 0)
     w.append(1 if c.get("contention") else 0)
+    w.append(1 if c.get("ccl_hier") else 0)
     return np.array(w, dtype=np.uint64)
 
 
@@ -265,6 +268,10 @@ def link_time(nbytes, bq):
 
 def dp_sync(p, zero, grads, params, alpha, MBps):
     return lib().oracle_dp_sync(p, zero, grads, params, alpha, MBps)
+
+
+def hier_allreduce(g, N, grads, a_in, MBps_in, alpha, MBps):
+    return lib().oracle_hier_allreduce(g, N, grads, a_in, MBps_in, alpha, MBps)
 
 
 def tree_allreduce(p, grads, alpha, MBps):
