@@ -115,6 +115,11 @@ typedef struct {
                                        the sum of the link-time parts (each segment: its rings' message
                                        latencies, then their bytes at the slowest rate, resharding
                                        included); 0: concurrent syncs do not slow each other */
+  uint32_t ccl_hier;                /* 1: a dense DP all-reduce (shared layout, not ZeRO) whose group fills
+                                       whole nodes with the same number g > 1 of members (TP groups) in
+                                       every node, over N > 1 nodes, may take the two-level algorithm --
+                                       reduce-scatter inside each node, ring all-reduce of each 1/g shard
+                                       across the nodes, all-gather inside each node -- when faster */
 } sim_cluster_desc;
 
 /*

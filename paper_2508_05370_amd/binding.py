@@ -31,7 +31,7 @@ class ClusterDesc(C.Structure):
     _fields_ = [("n_types", C.c_uint32)] + [(k, C.c_void_p) for k in (
         "n_nodes", "dev_per_node", "tflops", "hbm_GBps", "intra_MBps", "pcie_MBps", "nic_MBps", "intra_alpha_ps",
         "pcie_alpha_ps", "nic_alpha_ps", "nic_MBps_dev", "intra_MBps_node", "mem_bytes")] + [
-        ("rail_only", C.c_uint32), ("ccl_tree", C.c_uint32), ("contention", C.c_uint32)]
+        ("rail_only", C.c_uint32), ("ccl_tree", C.c_uint32), ("contention", C.c_uint32), ("ccl_hier", C.c_uint32)]
 
 
 class Plans(C.Structure):
@@ -149,6 +149,7 @@ def cluster_desc(c):
     d.rail_only = 1 if c.get("rail_only") else 0
     d.ccl_tree = 1 if c.get("ccl_tree") else 0
     d.contention = 1 if c.get("contention") else 0
+    d.ccl_hier = 1 if c.get("ccl_hier") else 0
     return d, keep
 
 

@@ -84,6 +84,7 @@ struct Tab {
   uint32_t rail_only;             // 1: rail-only inter-node network (cross-rail hops forwarded in a node)
   uint32_t ccl_tree;              // 1: all-reduces take the faster of ring and tree
   uint32_t contention;            // 1: a stage's concurrent segment syncs share its links
+  uint32_t ccl_hier;              // 1: whole-node DP groups may take the two-level all-reduce
   uint64_t mem_cap[kMaxTypes];    // device memory of type k, bytes
   uint64_t opt_bytes;             // optimizer-state bytes per parameter
   uint64_t act_layer[4][4];       // bytes one layer stores for backward per micro-batch [log2 TP][mbs index]

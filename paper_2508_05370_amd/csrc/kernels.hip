@@ -649,13 +649,25 @@ __device__ __forceinline__ uint32_t dev_before_own(const Plan& p, uint32_t s, ui
 // participating devices, or inside one node when every replica of the stage
 // sits in the same node; MoE models add the expert ring over the EP-sized
 // groups.  The same for every class of the plan.
-template <int kMode>
+// With two-level collectives enabled, hs is the group's shape for them:
+// usable when every class's devices of the stage fill whole nodes with the
+// same number g > 1 of TP groups per node, over N > 1 nodes in all; a_in
+// and bq_in are the worst node latency and fabric rate over them.
+struct HierShape {
+  bool ok;
+  uint32_t g, N, bq_in;
+  uint64_t a_in;
+};
+
+template <int kMode, bool kHier>
 __device__ __forceinline__ void stage_link(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t s,
-                                           uint64_t& alpha, uint32_t& bq) {
+                                           uint64_t& alpha, uint32_t& bq, HierShape& hs) {
   const uint32_t G = p.G, tp = p.tp;
   bool same = true;
   uint32_t k0 = 0, nmin = 0xffffffffu, nmax = 0, bq_dp = 0;
   uint64_t a_dp = 0;
+  hs.ok = kHier && t.ccl_hier != 0;
+  hs.g = 0; hs.N = 0; hs.bq_in = 0; hs.a_in = 0;
 #pragma unroll
   for (uint32_t c2 = 0; c2 < 4; ++c2) {
     if (c2 >= G) continue;
@@ -671,23 +683,52 @@ __device__ __forceinline__ void stage_link(const Tab& t, const Hot<kMode>& h, co
     const uint32_t bx = nic2 > t2.bq_pcie ? nic2 : t2.bq_pcie;
     bq_dp = bx > bq_dp ? bx : bq_dp;
     a_dp = 2 * t2.a_side > a_dp ? 2 * t2.a_side : a_dp;
+    if (kHier && t.ccl_hier) {
+      const uint32_t dm = (1u << d2) - 1, gm = (1u << d2) >> p.tpl;
+      hs.ok = hs.ok && (b2 & dm) == 0 && (n2 & dm) == 0 && (c2 == 0 || gm == hs.g);
+      hs.g = gm;
+      hs.N += n2 >> d2;
+      hs.a_in = t2.a_intra > hs.a_in ? t2.a_intra : hs.a_in;
+      const uint32_t bi = range_max(h.rmi(), t.N, l2, h2);
+      hs.bq_in = bi > hs.bq_in ? bi : hs.bq_in;
+    }
   }
+  hs.ok = hs.ok && hs.g > 1 && hs.N > 1;
   const bool intra = same && nmin == nmax;
   alpha = intra ? h.type(k0).a_intra : a_dp;
   bq = intra ? h.rmi()[nmin] : bq_dp;
 }
 
-template <int kMode>
+// A dense all-reduce of `grads` bytes per member over the group, with the
+// two-level algorithm when the shape allows it and it is faster: the
+// node-local ring over the whole gradient (g members), then the ring
+// across the N nodes over a 1/g shard (g is a power of two).
+__device__ __forceinline__ uint64_t with_hier(uint64_t ring, const HierShape& hs, uint32_t zero, uint64_t grads,
+                                              uint64_t alpha, uint32_t bq) {
+  if (!hs.ok || zero) return ring;
+  const uint32_t lg = __builtin_ctz(hs.g);
+  const uint64_t sh = (grads + hs.g - 1) >> lg;
+  const uint64_t intra = 2ull * (hs.g - 1) * hs.a_in + link_ps(2ull * (hs.g - 1) * sh, hs.bq_in);
+  const uint64_t inter = 2ull * (hs.N - 1) * alpha +
+                         link_ps(2ull * (hs.N - 1) * div_up(sh, hs.N, 1.0 / (double)hs.N), bq);
+  return intra + inter < ring ? intra + inter : ring;
+}
+
+// kHier: the two-level all-reduce is considered (the first-pass kernels,
+// compiled without it, defer every pipeline when it is enabled).
+template <int kMode, bool kHier = true>
 __device__ __forceinline__ uint64_t stage_dp(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t s,
                                              uint32_t ns, double rp, double rpe) {
   if (p.psum <= 1) return 0;
   const uint32_t tpl = p.tpl, epl = p.epl, S = p.S;
   uint64_t alpha;
   uint32_t bq;
-  stage_link(t, h, p, s, alpha, bq);
+  HierShape hs;
+  stage_link<kMode, kHier>(t, h, p, s, alpha, bq, hs);
   const uint64_t pd = (uint64_t)ns * t.par_layer[tpl] + (s == 0 ? t.par_embed[tpl] : 0) +
                       (s == S - 1 ? t.par_head[tpl] : 0);
   uint64_t tdp = ring_sync(p.psum, rp, p.zero, t.grad_bytes * pd, t.param_bytes * pd, alpha, bq, t.ccl_tree);
+  if (kHier) tdp = with_hier(tdp, hs, p.zero, t.grad_bytes * pd, alpha, bq);
   const uint32_t pe = p.psum >> epl;
   if (t.E && pe > 1) {
     const uint64_t px = (uint64_t)ns * t.par_expert[tpl][epl];
@@ -704,16 +745,18 @@ __device__ __forceinline__ uint64_t stage_dp(const Tab& t, const Hot<kMode>& h, 
 // r_j = end - R_j (R_j: backward compute of the buckets after it), so the
 // queue completes at end + max_j (D_j - R_j) (D_j: syncs of bucket j and
 // the later ones); that tail is returned, walked from the last bucket.
-template <int kMode>
+template <int kMode, bool kHier = true>
 __device__ __forceinline__ uint64_t overlap_tail(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t s,
                                                  uint32_t lo, uint32_t hi, uint32_t k, double rp, double rpe) {
   if (p.psum <= 1) return 0;
   const uint32_t tpl = p.tpl, epl = p.epl, mi = p.mi;
   uint64_t alpha;
   uint32_t bq;
-  stage_link(t, h, p, s, alpha, bq);
+  HierShape hs;
+  stage_link<kMode, kHier>(t, h, p, s, alpha, bq, hs);
   const uint64_t gb = t.grad_bytes, pb = t.param_bytes;
   uint64_t dl = ring_sync(p.psum, rp, p.zero, gb * t.par_layer[tpl], pb * t.par_layer[tpl], alpha, bq, t.ccl_tree);
+  dl = with_hier(dl, hs, p.zero, gb * t.par_layer[tpl], alpha, bq);
   const uint32_t pe = p.psum >> epl;
   if (t.E && pe > 1)
     dl += ring_sync(pe, rpe, p.zero, gb * t.par_expert[tpl][epl], pb * t.par_expert[tpl][epl], alpha, bq, t.ccl_tree);
@@ -721,7 +764,9 @@ __device__ __forceinline__ uint64_t overlap_tail(const Tab& t, const Hot<kMode>&
   const uint32_t row = ((k * 4 + tpl) * t.n_mbs + mi) * t.nep + epq;
   int64_t D = 0, R = 0, X = 0;
   if (s == 0) {
-    D += (int64_t)ring_sync(p.psum, rp, p.zero, gb * t.par_embed[tpl], pb * t.par_embed[tpl], alpha, bq, t.ccl_tree);
+    D += (int64_t)with_hier(
+        ring_sync(p.psum, rp, p.zero, gb * t.par_embed[tpl], pb * t.par_embed[tpl], alpha, bq, t.ccl_tree), hs, p.zero,
+        gb * t.par_embed[tpl], alpha, bq);
     X = D;
     R += (int64_t)h.emb(k * t.n_mbs + mi).y;
   }
@@ -731,7 +776,9 @@ __device__ __forceinline__ uint64_t overlap_tail(const Tab& t, const Hot<kMode>&
     R += (int64_t)(t.uniform_layers ? h.pfb(row).y : h.pfb(row * L1 + l + 1).y - h.pfb(row * L1 + l).y);
   }
   if (s == p.S - 1) {
-    D += (int64_t)ring_sync(p.psum, rp, p.zero, gb * t.par_head[tpl], pb * t.par_head[tpl], alpha, bq, t.ccl_tree);
+    D += (int64_t)with_hier(
+        ring_sync(p.psum, rp, p.zero, gb * t.par_head[tpl], pb * t.par_head[tpl], alpha, bq, t.ccl_tree), hs, p.zero,
+        gb * t.par_head[tpl], alpha, bq);
     X = D - R > X ? D - R : X;
   }
   return (uint64_t)X;
@@ -1183,7 +1230,7 @@ struct RegSink {
 // Iteration time from the end of each stage's last op: the max over stages
 // of that end plus the stage's DP sync, walking the stages with the same
 // shift so that no array is indexed at run time.
-template <int S, int kMode, bool kHet, bool kOvl>
+template <int S, int kMode, bool kHet, bool kOvl, bool kHier>
 __device__ __forceinline__ double dp_tail(const Tab& t, const Hot<kMode>& h, const Plan& p, double (&last)[S],
                                           const uint64_t* drow) {
   if constexpr (kHet) {
@@ -1201,8 +1248,8 @@ __device__ __forceinline__ double dp_tail(const Tab& t, const Hot<kMode>& h, con
   uint32_t lo = 0;
   for (uint32_t s = 0; s < (uint32_t)S; ++s) {
     const uint32_t hi = cut_at(p, s);
-    const uint64_t d = kOvl ? overlap_tail(t, h, p, s, lo, hi, (uint32_t)(p.tc >> (4 * s)) & 15, rp, rpe)
-                            : stage_dp(t, h, p, s, hi - lo, rp, rpe);
+    const uint64_t d = kOvl ? overlap_tail<kMode, kHier>(t, h, p, s, lo, hi, (uint32_t)(p.tc >> (4 * s)) & 15, rp, rpe)
+                            : stage_dp<kMode, kHier>(t, h, p, s, hi - lo, rp, rpe);
     const double e = last[0] + (double)d;
     T = e > T ? e : T;
 #pragma unroll
@@ -1615,14 +1662,16 @@ struct EvalBufs {
 // backward pass.  The first pass (kFull false) sends such pipelines straight
 // to the deferred lists, so that its kernels carry no overlap code; the
 // deferred pass runs them with the shortcut (the whole loop where they stay
-// aperiodic) and the overlapped sync.
+// aperiodic) and the overlapped sync.  It does the same with zero-bubble
+// pipelines (kZb), and with every shared-layout pipeline of a context that
+// enables two-level collectives, whose sync code only the deferred pass has.
 template <int S, bool kFull, int kMode, bool kHet, bool kOvl = false, bool kZb = false>
 __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot) {
   RegSink<S> r;
   uint32_t M;
   {
     const Plan p = load_plan<kHet>(e.packed, e.pcut, slot);
-    if (!kFull && !kHet && !kOvl && !kZb && (p.overlap | p.zb)) {
+    if (!kFull && !kHet && !kOvl && !kZb && (p.overlap | p.zb | t.ccl_hier)) {
       e.deferred[e.sstart[kMaxStages - S] + atomicAdd(&e.ctr[1 + kMaxStages - S], 1u)] = slot;
       return;
     }
@@ -1640,7 +1689,7 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
   // shuffle is opaque to the compiler, which would otherwise reuse the
   // first load
   const uint32_t slot2 = __shfl(slot, (int)(threadIdx.x & 63u));
-  const double T = done ? dp_tail<S, kMode, kHet, kOvl>(t, h, load_plan<kHet>(e.packed, e.pcut, slot2), last,
+  const double T = done ? dp_tail<S, kMode, kHet, kOvl, kFull || kOvl || kZb>(t, h, load_plan<kHet>(e.packed, e.pcut, slot2), last,
                                                          kHet ? e.hdp + (size_t)slot2 * kMaxStages : nullptr)
                         : 0;
   if (!done) {

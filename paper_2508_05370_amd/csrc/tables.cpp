@@ -309,6 +309,7 @@ int build_tables(const sim_model_desc* md, const sim_cluster_desc* cd, HostTable
   t.rail_only = cd->rail_only != 0;
   t.ccl_tree = cd->ccl_tree != 0;
   t.contention = cd->contention != 0;
+  t.ccl_hier = cd->ccl_hier != 0;
   u128 mem_max = 0;
   if (cd->mem_bytes) {
     t.mem_check = 1;
