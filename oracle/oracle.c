@@ -656,7 +656,9 @@ static uint64_t dp_sync_cl(const or_ctx* x, uint64_t p, uint64_t zero, uint64_t 
 
 /* R49: the same sync split into its latency steps and the time its bytes
  * take on the link (the part concurrent collectives on one link share); the
- * tree is taken only when strictly faster, as above */
+ * tree is taken only when strictly faster, as above.  A shared-layout plan
+ * also splits the two-level all-reduce (dp_parts_h, after its definition),
+ * so that a stage holding one segment keeps its sync time. */
 static void dp_parts(const or_ctx* x, uint64_t p, uint64_t zero, uint64_t grads, uint64_t params, uint64_t alpha,
                      uint64_t bq, uint64_t* lat, uint64_t* bw) {
   *lat = 0;
@@ -861,6 +863,18 @@ static uint64_t dp_sync_h(const or_ctx* x, const or_hier* h, uint64_t p, uint64_
   return r;
 }
 
+/* the split of dp_sync_h: the two-level all-reduce's latency steps on both
+ * tiers and its bytes on both tiers, taken where it is strictly faster */
+static void dp_parts_h(const or_ctx* x, const or_hier* h, uint64_t p, uint64_t zero, uint64_t grads, uint64_t params,
+                       uint64_t alpha, uint64_t bq, uint64_t* lat, uint64_t* bw) {
+  dp_parts(x, p, zero, grads, params, alpha, bq, lat, bw);
+  if (!(x->c.ccl_hier && h && h->ok && !zero && p > 1)) return;
+  uint64_t sh = cdiv(grads, h->g);
+  uint64_t hl = add(mul(2 * (h->g - 1), h->a_in), mul(2 * (h->N - 1), alpha));
+  uint64_t hb = add(link_time(mul(2 * (h->g - 1), sh), h->bq_in), link_time(mul(2 * (h->N - 1), cdiv(sh, h->N)), bq));
+  if (add(hl, hb) < add(*lat, *bw)) { *lat = hl; *bw = hb; }
+}
+
 static void eval_plan_interleaved(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t* scratch);
 
 /* R44-R46: zero-bubble order (ZB-H1 of Qi et al. 2024, "Zero Bubble
@@ -1026,7 +1040,8 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
       /* R49: the segments a stage holds sync at the same time over the same
        * devices, so their link times add up while their latencies overlap */
       uint64_t ld, bd, le = 0, be = 0;
-      dp_parts(x, p_all, p->zero, mul(m->grad_bytes, pd), mul(m->param_bytes, pd), alpha, bq, &ld, &bd);
+      dp_parts_h(x, p->het ? NULL : &seg_h[j], p_all, p->zero, mul(m->grad_bytes, pd), mul(m->param_bytes, pd),
+                 alpha, bq, &ld, &bd);
       if (m->E) dp_parts(x, p_all / ep, p->zero, mul(m->grad_bytes, pe), mul(m->param_bytes, pe), alpha, bq, &le, &be);
       uint64_t lat = add(add(ld, le), rs_lat), bw = add(add(bd, be), rs_bw);
       if (add(lat, bw) != t) or_die("contention: split does not add up");

@@ -5,7 +5,8 @@ same time over the same devices (R37).  With contention their link times add up 
 latencies overlap: the stage waits for the largest latency part plus the sum of the link-time
 parts.  Pinned: the two parts against the ring closed form (2 (p - 1) latencies, 2 (p - 1)
 chunks of ceil(B / p) bytes on the slowest link) on a hand-built two-class plan; plans whose
-stages hold one segment each (every shared-layout plan) are unchanged; no plan gets faster.
+stages hold one segment each (every shared-layout plan) are unchanged, also with the tree and
+two-level all-reduce enabled; no plan gets faster.
 """
 import numpy as np
 
@@ -70,6 +71,24 @@ def test_one_segment_per_stage_is_unchanged(oracle_mod, workloads):
         assert np.array_equal(a, b)
         h = workloads.as_per_class(p)
         assert np.array_equal(oracle_mod.Oracle(w["model"], dict(w["cluster"], contention=True)).eval(h), a)
+
+
+def test_one_segment_per_stage_with_other_algorithms(oracle_mod, workloads):
+    """With the tree and two-level all-reduce also enabled, a stage that holds one segment keeps
+    the sync the faster algorithm gives: contention changes no shared-layout plan of any kind
+    (plain, overlapped, zero-bubble, interleaved)."""
+    for idx in (2, 3, 4, 5):
+        w = workloads.workload(idx)
+        c = dict(w["cluster"], ccl_tree=True, ccl_hier=True, rail_only=True)
+        p = workloads.plans(w, 0, 3000)
+        p["hdr"][1000:2000] |= np.uint32(1 << 13)
+        p["hdr"][2000:] |= np.uint32(1 << 16)
+        q = workloads.interleaved_plans(w, 0, 1000)
+        for x in (p, q):
+            a = oracle_mod.Oracle(w["model"], c).eval(x)
+            b = oracle_mod.Oracle(w["model"], dict(c, contention=True)).eval(x)
+            assert np.array_equal(a, b), idx
+        assert np.any(a != oracle_mod.Oracle(w["model"], w["cluster"]).eval(q))
 
 
 def test_contention_never_helps(oracle_mod, workloads):
