@@ -112,3 +112,49 @@ def test_all_cluster_options_per_class(torch, B, oracle_mod, workloads, idx):
     say("case: every cluster option, per-class plans, workload %d" % idx)
     got = B.times_u64(B.Sim(w["model"], c).eval_plans(B.device_plans(p)))
     _equal(got, oracle_mod.Oracle(w["model"], c).eval(p), "every option, per-class, workload %d" % idx)
+
+
+@pytest.mark.parametrize("idx", [3, 5])
+@pytest.mark.parametrize("kind", ["plain", "per-class"])
+def test_all_cluster_options_stage_records(torch, B, oracle_mod, workloads, idx, kind):
+    """Per (class, stage) forward/backward/hop times and the sync each stage waits for, with the
+    four cluster options on."""
+    w = workloads.workload(idx)
+    c = dict(w["cluster"], **ALL_FLAGS)
+    n = 1500
+    p = workloads.het_plans(w, 0, n) if kind == "per-class" else workloads.plans(w, 0, n)
+    say("case: every cluster option, %s stage records, workload %d" % (kind, idx))
+    st, cl = B.Sim(w["model"], c).eval_stages(B.device_plans(p))
+    st = st.cpu().numpy().view(np.uint64)
+    cl = cl.cpu().numpy().view(np.uint32)
+    o = oracle_mod.Oracle(w["model"], c)
+    checked = 0
+    for i in range(0, n, 3):
+        d = o.detail(p, i)
+        if d is None:
+            assert np.all(cl[i] == 0)
+            continue
+        for g in range(d["G"]):
+            for s in range(d["S_class"][g]):
+                rec = [int(v) for v in st[i, g, s]]
+                want = [d["f"][g][s], d["b"][g][s], d["c"][g][s], d["tdp"][g][s]]
+                assert rec == want, (idx, i, g, s, rec, want)
+        checked += 1
+    assert checked > 200
+
+
+@pytest.mark.parametrize("idx", [3, 4])
+def test_all_cluster_options_with_memory(torch, B, oracle_mod, workloads, idx):
+    """Per-type device memory and the four cluster options together, over mixed plan kinds."""
+    w = workloads.with_memory(workloads.workload(idx))
+    c = dict(w["cluster"], **ALL_FLAGS)
+    n = 10_007
+    a = workloads.plans(w, 0, 2 * n)
+    a["hdr"][n:] |= np.uint32(1 << 16)
+    b = workloads.interleaved_plans(w, 0, n)
+    p = _concat([a, b], np.random.default_rng(idx + 10).permutation(3 * n))
+    say("case: every cluster option with device memory, workload %d" % idx)
+    got = B.times_u64(B.Sim(w["model"], c).eval_plans(B.device_plans(p)))
+    want = oracle_mod.Oracle(w["model"], c).eval(p)
+    _equal(got, want, "every option with memory, workload %d" % idx)
+    assert 0 < np.count_nonzero(want != MAXU) < 3 * n
