@@ -97,25 +97,25 @@ typedef struct {
   const uint32_t* intra_MBps_node;  /* optional [total nodes] per-node fabric rate (overrides intra_MBps) */
   const uint64_t* mem_bytes;        /* optional [K] device memory in bytes, each >= 1 (Table 5 names
                                        A100 40 GB and H100 80 GB); NULL = memory not checked */
-  uint32_t rail_only;               /* 1: rail-only inter-node network (Fig. 2): the NIC of local rank r
+  uint32_t rail_only;               /* nonzero: rail-only inter-node network (Fig. 2): the NIC of local rank r
                                        of every node joins rail r and rails do not meet, so a pipeline
                                        hop between nodes whose device pairs sit at different local ranks
                                        first crosses a node's fabric to the receiver's rank -- the
                                        sender's node, or the receiver's when the sender's type has one
                                        device per node -- adding that node's latency and the activation
                                        at its slowest fabric rate (Fig. 2c); 0: any NIC reaches any */
-  uint32_t ccl_tree;                /* 1: every DP all-reduce (not the reduce-scatter and all-gather of
+  uint32_t ccl_tree;                /* nonzero: every DP all-reduce (not the reduce-scatter and all-gather of
                                        ZeRO) takes the faster of the ring and a pipelined binary tree,
                                        2 ceil(log2 p) latencies plus twice the gradient bytes at the
                                        ring's slowest rate, as a collective library picks an algorithm
                                        per call (Sec. 4.1 [C3]); 0: rings only */
-  uint32_t contention;              /* 1: with the per-class layout, the syncs of the layer segments a
+  uint32_t contention;              /* nonzero: with the per-class layout, the syncs of the layer segments a
                                        stage holds run at the same time over the same devices and share
                                        their links: the stage waits for the largest latency part plus
                                        the sum of the link-time parts (each segment: its rings' message
                                        latencies, then their bytes at the slowest rate, resharding
                                        included); 0: concurrent syncs do not slow each other */
-  uint32_t ccl_hier;                /* 1: a dense DP all-reduce (shared layout, not ZeRO) whose group fills
+  uint32_t ccl_hier;                /* nonzero: a dense DP all-reduce (shared layout, not ZeRO) whose group fills
                                        whole nodes with the same number g > 1 of members (TP groups) in
                                        every node, over N > 1 nodes, may take the two-level algorithm --
                                        reduce-scatter inside each node, ring all-reduce of each 1/g shard
