@@ -111,3 +111,31 @@ def test_null_arguments(B):
     assert L.sim_best_reduce(None, None, 0, None, None) == B.SIM_EINVAL
     assert L.sim_set_timing(None, 1) == B.SIM_EINVAL
     L.sim_destroy(None)
+
+
+def test_binding_structs_match_the_header(B, tmp_path):
+    """Every descriptor the binding passes has the header's layout: each field's offset and each
+    struct's size, as the C compiler lays them out, equal the ctypes mirror's."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    structs = {"sim_model_desc": B.ModelDesc, "sim_cluster_desc": B.ClusterDesc, "sim_plans": B.Plans,
+               "sim_best": B.Best}
+    lines = ["#include <stddef.h>", "#include <stdio.h>", '#include "hetsim.h"', "int main(void) {"]
+    for cname, py in structs.items():
+        lines.append('  printf("%s size %%zu\\n", sizeof(%s));' % (cname, cname))
+        for f, _ in py._fields_:
+            lines.append('  printf("%s %s %%zu\\n", offsetof(%s, %s));' % (cname, f, cname, f))
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "probe.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "probe"
+    subprocess.run([cc, "-std=c11", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    got = {tuple(x.split()[:2]): int(x.split()[2]) for x in out if x}
+    for cname, py in structs.items():
+        assert got[(cname, "size")] == C.sizeof(py), cname
+        for f, _ in py._fields_:
+            assert got[(cname, f)] == getattr(py, f).offset, (cname, f)
