@@ -1,0 +1,82 @@
+"""Parity over seeded random configurations, between the HIP path, through the C ABI, and the
+oracle.  Bit-exact.
+
+Each case draws a model (the five shapes, with fresh expert loads for the MoE one), a cluster
+of 1-6 device types with 1-8 nodes each, 1, 2, 4 or 8 devices per node, jittered links or not,
+types whose node fabric is PCIe only, mixed latency multipliers, each of the four cluster
+options on or off, device memory or none, and a global batch; then plain, overlapped,
+zero-bubble, interleaved and per-class-layout plans for it.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+OPTIONS = ("rail_only", "ccl_tree", "contention", "ccl_hier")
+MODELS = ("gpt2-small", "llama-7b", "llama-70b", "mixtral-8x7b", "gpt3-175b")
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as T
+    if not T.cuda.is_available():
+        pytest.skip("no GPU")
+    return T
+
+
+@pytest.fixture(scope="module")
+def B():
+    from paper_2508_05370_amd import binding
+    return binding
+
+
+def _config(workloads, seed):
+    rng = np.random.default_rng(0xC0F16000 + seed)
+    name = MODELS[rng.integers(0, len(MODELS))]
+    m = workloads.model(name)
+    if m["experts"]:
+        m["load_q16"] = workloads.dirichlet_q16(m["L"], m["experts"], seed=int(rng.integers(1, 1 << 30)))
+    K = int(rng.integers(1, 7))
+    nodes = [int(rng.integers(1, 9)) for _ in range(K)]
+    dpn = int(rng.choice([1, 2, 4, 8]))
+    c = workloads.cluster_random(int(rng.integers(0, 1000)), nodes, dpn=dpn, jitter=bool(rng.integers(0, 2)),
+                                 pcie_only_types=tuple(k for k in range(K) if rng.integers(0, 4) == 0),
+                                 alpha_mult=bool(rng.integers(0, 2)))
+    for k, on in zip(OPTIONS, rng.integers(0, 2, len(OPTIONS))):
+        c[k] = bool(on)
+    if rng.integers(0, 2):
+        for t in c["types"]:
+            t["mem_bytes"] = int(workloads.MEM_GIB[rng.integers(0, len(workloads.MEM_GIB))]) << 30
+    m["global_batch"] = int(rng.choice([8, 64, 512, 1024]))
+    return name, m, c, int(rng.integers(0, 1 << 30))
+
+
+@pytest.mark.parametrize("seed", range(48))
+def test_random_configuration(torch, B, oracle_mod, workloads, seed):
+    name, m, c, s0 = _config(workloads, seed)
+    n = 4001
+    p = workloads.random_plans(m, c, s0, 0, n)
+    kinds = {"plain": p}
+    for kind, bit in (("overlap", 13), ("zero-bubble", 16)):
+        q = {k: v.copy() for k, v in p.items()}
+        q["hdr"] |= np.uint32(1 << bit)
+        kinds[kind] = q
+    kinds["interleaved"] = workloads.random_plans_il(m, c, s0 + 1, 0, n)
+    kinds["per-class"] = workloads.random_plans_het(m, c, s0 + 2, 0, n)
+    sim, o = B.Sim(m, c), oracle_mod.Oracle(m, c)
+    opts = ",".join(k for k in OPTIONS if c[k]) or "none"
+    for kind, q in kinds.items():
+        say("case: random configuration %d (%s, %d types, options %s), %s plans" % (
+            seed, name, len(c["types"]), opts, kind))
+        got = B.times_u64(sim.eval_plans(B.device_plans(q)))
+        want = o.eval(q)
+        bad = np.nonzero(got != want)[0]
+        assert bad.size == 0, "configuration %d %s: %d mismatches, first %s: gpu %d oracle %d" % (
+            seed, kind, bad.size, bad[:5], int(got[bad[0]]), int(want[bad[0]]))
