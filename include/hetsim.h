@@ -203,7 +203,8 @@ typedef struct {
  * backward, for every TP degree, micro-batch size and EP degree, with layer
  * prefix sums), the link tables and range-maximum structures, and uploads
  * them.  Returns SIM_EINVAL for malformed descriptors, SIM_ERANGE when some
- * plan's time could exceed 2^62 ps or a per-stage quantity 2^52 ps,
+ * plan's time could exceed 2^62 ps, a per-stage quantity 2^52 ps or a
+ * device's memory as sim_eval_memory defines it 2^63 bytes,
  * SIM_ENOMEM or SIM_EHIP on allocation/copy failure.  *out is NULL on error.
  */
 int sim_create(const sim_model_desc* model, const sim_cluster_desc* cluster, sim_ctx** out);

@@ -310,10 +310,14 @@ int build_tables(const sim_model_desc* md, const sim_cluster_desc* cd, HostTable
   t.ccl_tree = cd->ccl_tree != 0;
   t.contention = cd->contention != 0;
   t.ccl_hier = cd->ccl_hier != 0;
+  // The per-device bytes that sim_eval_memory reports are defined with or
+  // without capacities; the capacities only switch the feasibility check on.
   u128 mem_max = 0;
   if (cd->mem_bytes) {
     t.mem_check = 1;
     for (uint32_t k = 0; k < K; ++k) t.mem_cap[k] = cd->mem_bytes[k];
+  }
+  {
     t.opt_bytes = md->opt_bytes;
     for (uint32_t j = 0; j < 4; ++j) {
       if (!(t.tp_ok >> j & 1)) continue;

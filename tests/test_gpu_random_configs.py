@@ -80,3 +80,40 @@ def test_random_configuration(torch, B, oracle_mod, workloads, seed):
         bad = np.nonzero(got != want)[0]
         assert bad.size == 0, "configuration %d %s: %d mismatches, first %s: gpu %d oracle %d" % (
             seed, kind, bad.size, bad[:5], int(got[bad[0]]), int(want[bad[0]]))
+
+
+@pytest.mark.parametrize("seed", range(0, 48, 3))
+def test_random_configuration_records(torch, B, oracle_mod, workloads, seed):
+    """Stage records (forward, backward, hop and sync per class and stage; per virtual stage for
+    interleaved plans) and per-stage device memory of every class against the oracle's detail."""
+    name, m, c, s0 = _config(workloads, seed)
+    n = 600
+    p = workloads.random_plans(m, c, s0, 0, n)
+    z = {k: v.copy() for k, v in p.items()}
+    z["hdr"] |= np.uint32(1 << 16)
+    kinds = {"plain": p, "zero-bubble": z, "interleaved": workloads.random_plans_il(m, c, s0 + 1, 0, n),
+             "per-class": workloads.random_plans_het(m, c, s0 + 2, 0, n)}
+    sim, o = B.Sim(m, c), oracle_mod.Oracle(m, c)
+    for kind, q in kinds.items():
+        say("case: random configuration %d (%s), %s stage records and memory" % (seed, name, kind))
+        dq = B.device_plans(q)
+        st, cl = sim.eval_stages(dq)
+        st = st.cpu().numpy().view(np.uint64)
+        mem = sim.eval_memory(dq, n).cpu().numpy().view(np.uint64)
+        for i in range(0, n, 7):
+            ref = o.stage_mem(q, i)
+            if ref is None:
+                assert np.all(mem[i] == np.uint64(2**64 - 1)), (seed, kind, i)
+            else:
+                assert np.array_equal(mem[i], ref), (seed, kind, i)
+            d = o.detail(q, i)
+            if d is None:
+                continue
+            v = ((int(q["hdr"][i]) >> 14) & 3) + 1
+            for g in range(d["G"]):
+                S = d["S_class"][g] if v == 1 else ((int(q["hdr"][i]) >> 4) & 15) + 1   # devices
+                for vs in range(S * v):
+                    rec = [int(x) for x in st[i, g, vs]]
+                    want = [d["f"][g][vs], d["b"][g][vs], d["c"][g][vs] if vs < S else 0,
+                            d["tdp"][g][vs] if vs < S else 0]
+                    assert rec == want, (seed, kind, i, g, vs, rec, want)
