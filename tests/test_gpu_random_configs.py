@@ -82,17 +82,20 @@ def test_random_configuration(torch, B, oracle_mod, workloads, seed):
             seed, kind, bad.size, bad[:5], int(got[bad[0]]), int(want[bad[0]]))
 
 
-@pytest.mark.parametrize("seed", range(0, 48, 3))
+@pytest.mark.parametrize("seed", range(48))
 def test_random_configuration_records(torch, B, oracle_mod, workloads, seed):
     """Stage records (forward, backward, hop and sync per class and stage; per virtual stage for
     interleaved plans) and per-stage device memory of every class against the oracle's detail."""
     name, m, c, s0 = _config(workloads, seed)
     n = 600
     p = workloads.random_plans(m, c, s0, 0, n)
-    z = {k: v.copy() for k, v in p.items()}
-    z["hdr"] |= np.uint32(1 << 16)
-    kinds = {"plain": p, "zero-bubble": z, "interleaved": workloads.random_plans_il(m, c, s0 + 1, 0, n),
-             "per-class": workloads.random_plans_het(m, c, s0 + 2, 0, n)}
+    kinds = {"plain": p}
+    for kind, bit in (("overlap", 13), ("zero-bubble", 16)):
+        q = {k: v.copy() for k, v in p.items()}
+        q["hdr"] |= np.uint32(1 << bit)
+        kinds[kind] = q
+    kinds["interleaved"] = workloads.random_plans_il(m, c, s0 + 1, 0, n)
+    kinds["per-class"] = workloads.random_plans_het(m, c, s0 + 2, 0, n)
     sim, o = B.Sim(m, c), oracle_mod.Oracle(m, c)
     for kind, q in kinds.items():
         say("case: random configuration %d (%s), %s stage records and memory" % (seed, name, kind))
