@@ -1,7 +1,8 @@
 """Parity over seeded random configurations, between the HIP path, through the C ABI, and the
 oracle.  Bit-exact.
 
-Each case draws a model (the five shapes, with fresh expert loads for the MoE one), a cluster
+Each case draws a model (the five shapes, with fresh expert loads for the MoE one; or, in
+`test_random_model`, a random transformer shape), a cluster
 of 1-6 device types with 1-8 nodes each, 1, 2, 4 or 8 devices per node, jittered links or not,
 types whose node fabric is PCIe only, mixed latency multipliers, each of the four cluster
 options on or off, device memory or none, and a global batch; then plain, overlapped,
@@ -120,3 +121,60 @@ def test_random_configuration_records(torch, B, oracle_mod, workloads, seed):
                     want = [d["f"][g][vs], d["b"][g][vs], d["c"][g][vs] if vs < S else 0,
                             d["tdp"][g][vs] if vs < S else 0]
                     assert rec == want, (seed, kind, i, g, vs, rec, want)
+
+
+def _random_model(workloads, rng):
+    """A transformer shape drawn at random: depth, width, heads and grouped KV heads, MLP width
+    and gating, vocabulary, positions, sequence length, micro-batch size, gradient and
+    optimizer-state bytes, and for a third of them experts with top-k routing."""
+    heads = int(rng.choice([4, 8, 12, 16, 32, 64, 96]))
+    h = heads * int(rng.choice([64, 80, 128]))
+    kvs = [k for k in range(1, heads + 1) if heads % k == 0]
+    seq = int(rng.choice([512, 1024, 2048, 4096, 8192]))
+    mbs = int(rng.choice([1, 2, 4]))
+    m = dict(workloads.model("gpt2-small"), L=int(rng.integers(2, 97)), h=h, heads=heads,
+             kv_heads=int(rng.choice(kvs)), ffn=64 * int(rng.integers(h // 64, 4 * h // 64 + 1)),
+             gated=int(rng.integers(0, 2)), vocab=int(rng.integers(1000, 200_000)),
+             learned_pos=seq if rng.integers(0, 2) else 0, seq=seq, mbs=[mbs],
+             global_batch=mbs * int(rng.choice([8, 32, 128, 512])), grad_bytes=int(rng.choice([2, 4])),
+             opt_bytes=int(rng.choice([0, 8, 12, 16])))
+    if rng.integers(0, 3) == 0:
+        m["experts"] = int(rng.choice([4, 8, 16]))
+        m["topk"] = int(rng.integers(1, 3))
+        m["expert_ffn"] = 64 * int(rng.integers(h // 64, 4 * h // 64 + 1))
+        m["ffn"] = 0
+        m["load_q16"] = workloads.dirichlet_q16(m["L"], m["experts"], seed=int(rng.integers(1, 1 << 30)))
+    return m
+
+
+@pytest.mark.parametrize("seed", range(32))
+def test_random_model(torch, B, oracle_mod, workloads, seed):
+    """Random model shapes on random clusters (with their options and memory): times of every
+    plan kind, then stage records and device memory on sampled plans."""
+    _, _, c, s0 = _config(workloads, 1000 + seed)
+    m = _random_model(workloads, np.random.default_rng(0x30DE1000 + seed))
+    n = 3001
+    p = workloads.random_plans(m, c, s0, 0, n)
+    kinds = {"plain": p}
+    for kind, bit in (("overlap", 13), ("zero-bubble", 16)):
+        q = {k: v.copy() for k, v in p.items()}
+        q["hdr"] |= np.uint32(1 << bit)
+        kinds[kind] = q
+    kinds["interleaved"] = workloads.random_plans_il(m, c, s0 + 1, 0, n)
+    kinds["per-class"] = workloads.random_plans_het(m, c, s0 + 2, 0, n)
+    sim, o = B.Sim(m, c), oracle_mod.Oracle(m, c)
+    for kind, q in kinds.items():
+        say("case: random model %d (L %d, h %d, experts %d), %s plans" % (seed, m["L"], m["h"], m["experts"], kind))
+        dq = B.device_plans(q)
+        got = B.times_u64(sim.eval_plans(dq))
+        want = o.eval(q)
+        bad = np.nonzero(got != want)[0]
+        assert bad.size == 0, "model %d %s: %d mismatches, first %s: gpu %d oracle %d" % (
+            seed, kind, bad.size, bad[:5], int(got[bad[0]]), int(want[bad[0]]))
+        mem = sim.eval_memory(dq, n).cpu().numpy().view(np.uint64)
+        for i in range(0, n, 29):
+            ref = o.stage_mem(q, i)
+            if ref is None:
+                assert np.all(mem[i] == np.uint64(2**64 - 1)), (seed, kind, i)
+            else:
+                assert np.array_equal(mem[i], ref), (seed, kind, i)
