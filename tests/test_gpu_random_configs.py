@@ -178,3 +178,56 @@ def test_random_model(torch, B, oracle_mod, workloads, seed):
                 assert np.all(mem[i] == np.uint64(2**64 - 1)), (seed, kind, i)
             else:
                 assert np.array_equal(mem[i], ref), (seed, kind, i)
+
+
+def _with_mbs(p, mbs, rng):
+    """Move each plan to a random micro-batch size of the list where every class's micro-batch
+    count divides and still gives each replica one: the count shrinks by the size, so the
+    global batch stays the same (header bits 11-12 = the size's index)."""
+    p = {k: v.copy() for k, v in p.items()}
+    n = p["hdr"].shape[0]
+    G = ((p["hdr"] >> 8) & 3) + 1
+    moved = 0
+    for i in range(n):
+        j = int(rng.integers(0, len(mbs)))
+        cls = [(int(p["cls"][g, i]) & 0xFFFF, int(p["cls"][g, i]) >> 16) for g in range(int(G[i]))]
+        if j == 0 or any(nmb % mbs[j] or nmb // mbs[j] < reps for reps, nmb in cls):
+            continue
+        for g, (reps, nmb) in enumerate(cls):
+            p["cls"][g, i] = reps | ((nmb // mbs[j]) << 16)
+        p["hdr"][i] = (int(p["hdr"][i]) & ~(3 << 11)) | (j << 11)
+        moved += 1
+    return p, moved
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_micro_batch_sizes(torch, B, oracle_mod, workloads, seed):
+    """Models with four micro-batch sizes; plans moved to a random one of them (plain,
+    zero-bubble and interleaved), times and device memory."""
+    _, _, c, s0 = _config(workloads, 2000 + seed)
+    rng = np.random.default_rng(0x3B500000 + seed)
+    m = _random_model(workloads, rng)
+    m["mbs"] = [1, 2, 4, 8]
+    m["global_batch"] = int(rng.choice([64, 256, 1024]))
+    n = 3001
+    p = workloads.random_plans(m, c, s0, 0, n)
+    z = {k: v.copy() for k, v in p.items()}
+    z["hdr"] |= np.uint32(1 << 16)
+    sim, o = B.Sim(m, c), oracle_mod.Oracle(m, c)
+    for kind, q0 in (("plain", p), ("zero-bubble", z), ("interleaved", workloads.random_plans_il(m, c, s0 + 1, 0, n))):
+        q, moved = _with_mbs(q0, m["mbs"], rng)
+        assert moved > n // 4
+        say("case: micro-batch sizes %d, %s plans (%d moved)" % (seed, kind, moved))
+        dq = B.device_plans(q)
+        got = B.times_u64(sim.eval_plans(dq))
+        want = o.eval(q)
+        bad = np.nonzero(got != want)[0]
+        assert bad.size == 0, "mbs %d %s: %d mismatches, first %s: gpu %d oracle %d" % (
+            seed, kind, bad.size, bad[:5], int(got[bad[0]]), int(want[bad[0]]))
+        mem = sim.eval_memory(dq, n).cpu().numpy().view(np.uint64)
+        for i in range(0, n, 31):
+            ref = o.stage_mem(q, i)
+            if ref is None:
+                assert np.all(mem[i] == np.uint64(2**64 - 1)), (seed, kind, i)
+            else:
+                assert np.array_equal(mem[i], ref), (seed, kind, i)
