@@ -202,8 +202,8 @@ def _with_mbs(p, mbs, rng):
 
 @pytest.mark.parametrize("seed", range(12))
 def test_random_micro_batch_sizes(torch, B, oracle_mod, workloads, seed):
-    """Models with four micro-batch sizes; plans moved to a random one of them (plain,
-    zero-bubble and interleaved), times and device memory."""
+    """Models with four micro-batch sizes; plans of every kind moved to a random one of them,
+    times and device memory."""
     _, _, c, s0 = _config(workloads, 2000 + seed)
     rng = np.random.default_rng(0x3B500000 + seed)
     m = _random_model(workloads, rng)
@@ -211,10 +211,15 @@ def test_random_micro_batch_sizes(torch, B, oracle_mod, workloads, seed):
     m["global_batch"] = int(rng.choice([64, 256, 1024]))
     n = 3001
     p = workloads.random_plans(m, c, s0, 0, n)
-    z = {k: v.copy() for k, v in p.items()}
-    z["hdr"] |= np.uint32(1 << 16)
+    kinds = {"plain": p}
+    for kind, bit in (("overlap", 13), ("zero-bubble", 16)):
+        q = {k: v.copy() for k, v in p.items()}
+        q["hdr"] |= np.uint32(1 << bit)
+        kinds[kind] = q
+    kinds["interleaved"] = workloads.random_plans_il(m, c, s0 + 1, 0, n)
+    kinds["per-class"] = workloads.random_plans_het(m, c, s0 + 2, 0, n)
     sim, o = B.Sim(m, c), oracle_mod.Oracle(m, c)
-    for kind, q0 in (("plain", p), ("zero-bubble", z), ("interleaved", workloads.random_plans_il(m, c, s0 + 1, 0, n))):
+    for kind, q0 in kinds.items():
         q, moved = _with_mbs(q0, m["mbs"], rng)
         assert moved > n // 4
         say("case: micro-batch sizes %d, %s plans (%d moved)" % (seed, kind, moved))
