@@ -1,4 +1,5 @@
 """Build the HIP library (libhetsim.so, gfx950) and the input generator in-tree."""
+import concurrent.futures
 import os
 import subprocess
 
@@ -16,26 +17,43 @@ HIP_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall",
 # the pipeline recurrence carries integer times in fp64: no NaN/inf ever occurs,
 # which lets max() compile to one v_max_f64 (no reassociation is enabled)
 KERNEL_FLAGS = ["-ffinite-math-only"]
-SOURCES = [("kernels.hip", KERNEL_FLAGS), ("api.cpp", []), ("tables.cpp", [])]
+# (source, object, extra flags): the common kernels, the C ABI, the table
+# builder, and one object per evaluation-pass variant -- table mode (0..2) x
+# plan layout (shared, per class) x pass (first, deferred) -- so that the
+# variants compile in parallel
+SOURCES = [("kernels.hip", "kernels.o", KERNEL_FLAGS), ("api.cpp", "api.o", []), ("tables.cpp", "tables.o", [])]
+SOURCES += [("eval_pass.hip", "eval_pass_m%d_h%d_p%d.o" % (m, h, p),
+             KERNEL_FLAGS + ["-DHETSIM_MODE=%d" % m, "-DHETSIM_HET=%d" % h, "-DHETSIM_PASS=%d" % p])
+            for p in (1, 0) for m in range(3) for h in range(2)]
+
+
+def _jobs():
+    try:
+        return max(1, len(os.sched_getaffinity(0)))
+    except AttributeError:
+        return max(1, os.cpu_count() or 1)
+
+
+def _compile(cmd):
+    proc = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)
+    text = "\n".join(ln for ln in proc.stdout.decode(errors="replace").splitlines() if "packed-fp32-ops" not in ln)
+    return proc.returncode, text
 
 
 def build(force=True, verbose=False):
     if not force and os.path.exists(LIB):
         return LIB
     os.makedirs(BUILD, exist_ok=True)
-    procs, objs = [], []
-    for src, extra in SOURCES:
-        obj = os.path.join(BUILD, src + ".o")
-        objs.append(obj)
-        cmd = ["hipcc", *HIP_FLAGS, *extra, "-I", INCLUDE, "-c", os.path.join(CSRC, src), "-o", obj]
-        procs.append((cmd, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)))
-    for cmd, p in procs:
-        out, _ = p.communicate()
-        text = "\n".join(ln for ln in out.decode(errors="replace").splitlines() if "packed-fp32-ops" not in ln)
-        if p.returncode != 0:
+    cmds = [["hipcc", *HIP_FLAGS, *extra, "-I", INCLUDE, "-c", os.path.join(CSRC, src), "-o", os.path.join(BUILD, obj)]
+            for src, obj, extra in SOURCES]
+    with concurrent.futures.ThreadPoolExecutor(max_workers=_jobs()) as pool:
+        results = list(pool.map(_compile, cmds))
+    for cmd, (rc, text) in zip(cmds, results):
+        if rc != 0:
             raise RuntimeError("hipcc failed: %s\n%s" % (" ".join(cmd), text))
         if verbose and text.strip():
             print(text)
+    objs = [os.path.join(BUILD, obj) for _, obj, _ in SOURCES]
     tmp = LIB + ".tmp"
     subprocess.run(["hipcc", "--offload-arch=" + ARCH, "-shared", "-fPIC", *objs, "-o", tmp], check=True)
     os.replace(tmp, LIB)
