@@ -748,7 +748,10 @@ static void stage_compute(const or_ctx* x, const or_plan* p, uint64_t g, int k, 
   }
   *F = add(add(Fc, tpf), epc);
   *B = add(Bc, epc);
-  if (Wg) *Wg = *B / 2;                                        /* R44: the weight-gradient half of the backward */
+  /* R44: W, the weight gradient, is half of the backward compute (rounded
+   * down); the MoE all-to-all of the backward pass carries the input
+   * gradient between EP ranks, so it stays in B with the other half */
+  if (Wg) *Wg = Bc / 2;
 }
 
 /* PP hop between class g's stage on pool k (devices from b1 on) and its

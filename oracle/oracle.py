@@ -32,7 +32,8 @@ class _Detail(C.Structure):
 def lib():
     global _lib
     if _lib is None:
-        path = _build.LIB
+        # a mutated build of the same source may be named for tests that check the pins catch it
+        path = os.environ.get("HETSIM_ORACLE_LIB") or _build.LIB
         if not os.path.exists(path):
             _build.build(force=False)
         L = C.CDLL(path)

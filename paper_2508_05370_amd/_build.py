@@ -19,12 +19,15 @@ HIP_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall",
 KERNEL_FLAGS = ["-ffinite-math-only"]
 # (source, object, extra flags): the common kernels, the C ABI, the table
 # builder, and one object per evaluation-pass variant -- table mode (0..2) x
-# plan layout (shared, per class) x pass (first, deferred) -- so that the
-# variants compile in parallel
+# plan layout (shared, per class) x pass (first, deferred), and the variant
+# pass (overlap and zero-bubble pipelines, shared layout) per table mode --
+# so that they compile in parallel
 SOURCES = [("kernels.hip", "kernels.o", KERNEL_FLAGS), ("api.cpp", "api.o", []), ("tables.cpp", "tables.o", [])]
 SOURCES += [("eval_pass.hip", "eval_pass_m%d_h%d_p%d.o" % (m, h, p),
              KERNEL_FLAGS + ["-DHETSIM_MODE=%d" % m, "-DHETSIM_HET=%d" % h, "-DHETSIM_PASS=%d" % p])
             for p in (1, 0) for m in range(3) for h in range(2)]
+SOURCES += [("eval_pass.hip", "eval_pass_m%d_h0_p2.o" % m,
+             KERNEL_FLAGS + ["-DHETSIM_MODE=%d" % m, "-DHETSIM_HET=0", "-DHETSIM_PASS=2"]) for m in range(3)]
 
 
 def _jobs():

@@ -23,6 +23,7 @@ hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* sstart,
 hipError_t launch_scatter(const uint16_t* keys, uint32_t nslots, uint32_t* cursor, uint32_t* ids, hipStream_t s);
 hipError_t launch_first(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s);
 hipError_t launch_group(const Tab& t, const EvalArgs& a, uint32_t max_tasks, int g, hipStream_t s);
+hipError_t launch_variant(const Tab& t, const EvalArgs& a, int g, hipStream_t s);
 hipError_t launch_deferred(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s);
 hipError_t launch_argmin(const uint64_t* t, int64_t n, int64_t base, sim_best* b, hipStream_t s);
 hipError_t launch_best_reduce(const sim_best* in, int64_t n, sim_best* out, hipStream_t s);
@@ -53,7 +54,6 @@ struct sim_ctx {
   hipStream_t grp[4];      // first-pass groups of multi-chunk calls, created on first use
 };
 
-static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 constexpr size_t kSkipBytes = (size_t)kSkipSlots * kSkipStride * 8;
 
 extern "C" const char* sim_strerror(int code) {
@@ -144,48 +144,6 @@ static void end_event(sim_ctx* c, int kind, hipStream_t s, EventPair* e) {
   c->ev[kind].push_back(*e);
 }
 
-// Workspace of one chunk: packed plans, pipeline metadata, pipeline ids and
-// the deferred lists, bucket counts followed by the evaluation counters and
-// the overflow list (counts and counters cleared together), bucket cursors,
-// the start of each stage count's pipelines, each pipeline's bucket key
-// (u16, written with the metadata and read by the scatter), and with the
-// per-class layout
-// the plans' class cut rows (64 bytes per plan) and the syncs each pipeline's
-// stages wait for (16 u64 per pipeline slot, 512 bytes per plan).
-constexpr uint32_t kCounters = kBuckets + kEvalCounters;
-struct Work {
-  PackedPlan* packed;
-  uint4* pcut;
-  uint64_t* hdp;
-  uint32_t *meta, *ids, *deferred, *hist, *ctr, *cursor, *sstart;
-  uint16_t* keys;
-};
-static size_t cut_rows_bytes(int64_t ch, bool het) { return het ? align256((size_t)ch * 64) : 0; }
-static size_t het_sync_bytes(int64_t ch, bool het) {
-  return het ? align256((size_t)ch * kMaxClasses * kMaxStages * 8) : 0;
-}
-static size_t work_bytes(int64_t ch, bool het) {
-  return align256((size_t)ch * sizeof(PackedPlan)) + 3 * align256((size_t)ch * 4 * 4) +
-         align256(kCounters * 4 + (size_t)ch * 4 * 4) + align256(kBuckets * 4) + align256(kSstartWords * 4) +
-         align256((size_t)ch * 4 * 2) +
-         cut_rows_bytes(ch, het) + het_sync_bytes(ch, het);
-}
-static Work carve(void* base, int64_t ch, bool het) {
-  Work w;
-  char* p = (char*)base;
-  w.pcut = het ? (uint4*)p : nullptr; p += cut_rows_bytes(ch, het);
-  w.hdp = het ? (uint64_t*)p : nullptr; p += het_sync_bytes(ch, het);
-  w.packed = (PackedPlan*)p; p += align256((size_t)ch * sizeof(PackedPlan));
-  w.meta = (uint32_t*)p; p += align256((size_t)ch * 16);
-  w.ids = (uint32_t*)p; p += align256((size_t)ch * 16);
-  w.deferred = (uint32_t*)p; p += align256((size_t)ch * 16);
-  w.hist = (uint32_t*)p; w.ctr = w.hist + kBuckets; p += align256(kCounters * 4 + (size_t)ch * 16);
-  w.cursor = (uint32_t*)p; p += align256(kBuckets * 4);
-  w.sstart = (uint32_t*)p; p += align256(kSstartWords * 4);
-  w.keys = (uint16_t*)p;
-  return w;
-}
-
 static bool side_streams(sim_ctx* c) {
   std::lock_guard<std::mutex> g(c->mu);
   if (!c->aux && hipStreamCreateWithFlags(&c->aux, hipStreamNonBlocking) != hipSuccess) c->aux = nullptr;
@@ -265,6 +223,7 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
       for (int g = 0; g < 4 && e == hipSuccess; ++g) {
         e = hipStreamWaitEvent(c->grp[g], sorted(b), 0);
         if (e == hipSuccess) e = launch_group(c->tab, a, (uint32_t)(cn * 4), g, c->grp[g]);
+        if (e == hipSuccess) e = launch_variant(c->tab, a, g, c->grp[g]);
         if (e == hipSuccess) e = hipEventRecord(fin(b, g), c->grp[g]);
         if (e == hipSuccess) e = hipStreamWaitEvent(aux, fin(b, g), 0);
       }

@@ -27,6 +27,8 @@
 #pragma once
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "internal.h"
 
 namespace hetsim {
@@ -1045,12 +1047,15 @@ __device__ __forceinline__ void het_plan_syncs(const Tab& t, const Hot<kMode>& h
 // reps * tp devices of the pipeline's class from `base` on in pool k (type
 // ti; bq_in, bq_nic: slowest node fabric and NIC rates over them): the
 // layers, the embedding if `first`, the head if `last`, the TP all-reduces
-// exposed in the forward pass and the MoE all-to-all in both passes.
+// exposed in the forward pass and the MoE all-to-all in both passes.  wc:
+// the weight-gradient pass of the zero-bubble order, half of the backward
+// compute rounded down (the all-to-all carries input gradients: it stays in
+// the input-gradient pass).
 template <int kMode, bool kHet>
 __device__ __forceinline__ void stage_cost(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t k,
                                            const TypeInfo& ti, uint32_t base, uint32_t bq_in, uint32_t bq_nic,
                                            uint32_t lo, uint32_t hi, bool first, bool last, uint64_t& fc,
-                                           uint64_t& bc) {
+                                           uint64_t& bc, uint64_t& wc) {
   const uint32_t tp = p.tp, ep = p.ep, tpl = p.tpl, epl = p.epl, mi = p.mi, ns = hi - lo, dpl = ti.dpl;
   const uint64_t act = t.act[mi], act_tp = (act + tp - 1) >> tpl;
   const uint32_t L1 = t.L + 1, epq = t.E ? p.epl : 0;
@@ -1075,6 +1080,7 @@ __device__ __forceinline__ void stage_cost(const Tab& t, const Hot<kMode>& h, co
     fc += hd.x;
     bc += hd.y;
   }
+  wc = bc >> 1;
   if (tp > 1) {  // TP all-reduces of this stage, exposed in the forward pass
     const uint64_t steps = (uint64_t)(2 * ns + first) * 2 * (tp - 1);
     fc += steps * ti.a_intra + link_ps(steps * act_tp, bq_in);
@@ -1153,8 +1159,8 @@ __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, c
     TypeInfo ti;
     stage_place<kMode, kHet>(t, h, p, s, k, ti, base, bq_in, bq_nic);
     const uint32_t dpl = ti.dpl;
-    uint64_t fc, bc;
-    stage_cost<kMode, kHet>(t, h, p, k, ti, base, bq_in, bq_nic, lo, hi, s == 0, s == S - 1, fc, bc);
+    uint64_t fc, bc, wc;
+    stage_cost<kMode, kHet>(t, h, p, k, ti, base, bq_in, bq_nic, lo, hi, s == 0, s == S - 1, fc, bc, wc);
     uint64_t hop = 0;
     if (s > 0) {  // hop (s-1) -> s
       // same pool means the two ranges are adjacent: intra iff the pair spans one node
@@ -1183,21 +1189,25 @@ __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, c
         tdp = stage_sync(t, h, p, s, lo, hi, rp, rpe);
       }
     }
-    sink.put(s, fc, bc, hop, tdp);
+    sink.put(s, fc, bc, wc, hop, tdp);
     lo = hi;
   }
 }
 
 // Sinks of class_setup.  RecSink stores whole stage records in memory order
-// (the hop of the last stage is 0).
+// (the hop of the last stage is 0), and, given `w`, each stage's
+// weight-gradient pass.
 struct RecSink {
   static constexpr bool kDp = true;
   uint64_t (&rec)[kMaxStages][kRecWords];
-  __device__ __forceinline__ void put(uint32_t s, uint64_t fc, uint64_t bc, uint64_t hop, uint64_t tdp) {
+  uint64_t* w = nullptr;
+  __device__ __forceinline__ void put(uint32_t s, uint64_t fc, uint64_t bc, uint64_t wc, uint64_t hop,
+                                      uint64_t tdp) {
     rec[s][0] = fc;
     rec[s][1] = bc;
     rec[s][2] = 0;
     rec[s][3] = tdp;
+    if (w) w[s] = wc;
     if (s > 0) rec[s - 1][2] = hop;
   }
 };
@@ -1215,7 +1225,7 @@ struct RegSink {
 #pragma unroll
     for (int i = 0; i < S; ++i) f[i] = b[i] = c[i] = 0;
   }
-  __device__ __forceinline__ void put(uint32_t s, uint64_t fc, uint64_t bc, uint64_t hop, uint64_t) {
+  __device__ __forceinline__ void put(uint32_t s, uint64_t fc, uint64_t bc, uint64_t, uint64_t hop, uint64_t) {
 #pragma unroll
     for (int i = 0; i + 1 < S; ++i) {
       f[i] = f[i + 1];
@@ -1224,6 +1234,32 @@ struct RegSink {
     }
     f[S - 1] = (double)fc;
     b[S - 1] = (double)bc;
+    c[S - 1] = 0;
+    if (S > 1 && s > 0) c[S - 2] = (double)hop;
+  }
+};
+
+// ZbSink: the same with the backward split for the zero-bubble order: bi,
+// the input-gradient pass, and w, the weight-gradient pass.
+template <int S>
+struct ZbSink {
+  static constexpr bool kDp = false;
+  double f[S], bi[S], w[S], c[S];
+  __device__ __forceinline__ ZbSink() {
+#pragma unroll
+    for (int i = 0; i < S; ++i) f[i] = bi[i] = w[i] = c[i] = 0;
+  }
+  __device__ __forceinline__ void put(uint32_t s, uint64_t fc, uint64_t bc, uint64_t wc, uint64_t hop, uint64_t) {
+#pragma unroll
+    for (int i = 0; i + 1 < S; ++i) {
+      f[i] = f[i + 1];
+      bi[i] = bi[i + 1];
+      w[i] = w[i + 1];
+      c[i] = c[i + 1];
+    }
+    f[S - 1] = (double)fc;
+    bi[S - 1] = (double)(bc - wc);
+    w[S - 1] = (double)wc;
     c[S - 1] = 0;
     if (S > 1 && s > 0) c[S - 2] = (double)hop;
   }
@@ -1455,49 +1491,38 @@ __device__ __forceinline__ bool pipe(const V (&f)[S], const V (&b)[S], const V (
 }
 
 // Zero-bubble order (ZB-H1, Qi et al. 2024): pipe's evaluation order with a
-// stage's backward pass b split into W = floor(b / 2), the weight gradient,
-// and B = b - W, the input gradient stage s-1 waits for (eb = its end).
-// After B(s, i) stage s runs W(s, i - s) once i >= s -- a pure delay on the
-// stage, its B having run before -- and its last min(s, M) W passes at the
-// end.  From i = S - 1 on every steady iteration runs every stage's W, so
-// the same map repeats and the periodic shortcut applies as in pipe (state
-// out_f[0..S-2], last[0..S-1]; the B end of stage s + 1 is read only by
-// stage s, right after, in the same iteration, so it is one carried value).
-// W is derived from b where it is used, so the recurrence keeps pipe's five
-// per-stage arrays: the empty asm makes the copy of b opaque, so that the
-// derivation is not hoisted out of the loops into a sixth array.  kJump:
+// stage's backward pass split into bi, the input gradient stage s-1 waits
+// for (eb = its end), and w, the weight gradient (half of the backward
+// compute; the MoE all-to-all stays in bi).  After B(s, i) stage s runs
+// W(s, i - s) once i >= s -- a pure delay on the stage, its B having run
+// before -- and its last min(s, M) W passes at the end.  From i = S - 1 on
+// every steady iteration runs every stage's W, so the same map repeats and
+// the periodic shortcut applies as in pipe (state out_f[0..S-2],
+// last[0..S-1]; the B end of stage s + 1 is read only by stage s, right
+// after, in the same iteration, so it is one carried value).  kJump:
 // shortcut pairs within the budget, then the whole loop; otherwise the
 // whole loop.
-__device__ __forceinline__ double half_down(double b) {
-  asm volatile("" : "+v"(b));
-  return __builtin_floor(b * 0.5);
-}
-__device__ __forceinline__ uint64_t half_down(uint64_t b) {
-  asm volatile("" : "+v"(b));
-  return b >> 1;
-}
-
 template <int S, typename V>
-__device__ __forceinline__ void zb_iter(const V (&f)[S], const V (&b)[S], const V (&c)[S], int i, int tr,
-                                        V (&out_f)[S], V (&last)[S]) {
+__device__ __forceinline__ void zb_iter(const V (&f)[S], const V (&bi)[S], const V (&w)[S], const V (&c)[S], int i,
+                                        int tr, V (&out_f)[S], V (&last)[S]) {
   V eb = 0;
 #pragma unroll
   for (int s = S - 1; s >= 0; --s) {
-    const V w = half_down(b[s]);
     if (s > tr) {   // the stage still runs a forward in this iteration
       const V st = s == 0 ? last[0] : vmax(last[s], out_f[s - 1] + c[s - 1]);
       out_f[s] = st + f[s];
       const V sb = s == S - 1 ? out_f[s] : vmax(out_f[s], eb + c[s]);
-      eb = sb + (b[s] - w);
+      eb = sb + bi[s];
     } else {
-      eb = (s == S - 1 ? last[s] : vmax(last[s], eb + c[s])) + (b[s] - w);
+      eb = (s == S - 1 ? last[s] : vmax(last[s], eb + c[s])) + bi[s];
     }
-    last[s] = i >= s ? eb + w : eb;
+    last[s] = i >= s ? eb + w[s] : eb;
   }
 }
 
 template <int S, typename V, bool kJump>
-__device__ __forceinline__ void pipe_zb(const V (&f)[S], const V (&b)[S], const V (&c)[S], uint32_t M, int& skipped,
+__device__ __forceinline__ void pipe_zb(const V (&f)[S], const V (&bi)[S], const V (&w)[S], const V (&c)[S], uint32_t M,
+                                        int& skipped,
                                         V (&last)[S]) {
   V out_f[S];
 #pragma unroll
@@ -1517,24 +1542,23 @@ __device__ __forceinline__ void pipe_zb(const V (&f)[S], const V (&b)[S], const 
   const int left = m_ - (S - 1);
   skipped = 0;
   int i = 0;
-  for (; i < left && i < S - 1; ++i) zb_iter<S, V>(f, b, c, i, -1, out_f, last);
+  for (; i < left && i < S - 1; ++i) zb_iter<S, V>(f, bi, w, c, i, -1, out_f, last);
   int rem = left - i;
   if (kJump) {
     int budget = kPeriodicBudget;
     while (rem >= 2 && budget > 0) {
-      zb_iter<S, V>(f, b, c, S, -1, out_f, last);
+      zb_iter<S, V>(f, bi, w, c, S, -1, out_f, last);
       bool same = true;
       V lam = 0, eb = 0;
 #pragma unroll
       for (int s = S - 1; s >= 0; --s) {
-        const V w = half_down(b[s]);
         const V st = s == 0 ? last[0] : vmax(last[s], out_f[s - 1] + c[s - 1]);
         const V nf = st + f[s];
         if (s < S - 1) same = same && nf - out_f[s] == lam;
         out_f[s] = nf;
         const V sb = s == S - 1 ? nf : vmax(nf, eb + c[s]);
-        eb = sb + (b[s] - w);
-        const V nl = eb + w;
+        eb = sb + bi[s];
+        const V nl = eb + w[s];
         if (s == S - 1) lam = nl - last[s];
         else same = same && nl - last[s] == lam;
         last[s] = nl;
@@ -1553,12 +1577,12 @@ __device__ __forceinline__ void pipe_zb(const V (&f)[S], const V (&b)[S], const 
       }
     }
   }
-  for (; rem > 0; --rem) zb_iter<S, V>(f, b, c, S, -1, out_f, last);
+  for (; rem > 0; --rem) zb_iter<S, V>(f, bi, w, c, S, -1, out_f, last);
 #pragma unroll
   for (int tr = 0; tr < S - 1; ++tr)
-    if (tr >= S - 1 - m_) zb_iter<S, V>(f, b, c, m_ - S + 1 + tr, tr, out_f, last);
+    if (tr >= S - 1 - m_) zb_iter<S, V>(f, bi, w, c, m_ - S + 1 + tr, tr, out_f, last);
 #pragma unroll
-  for (int s = 0; s < S; ++s) last[s] += (V)(s < m_ ? s : m_) * half_down(b[s]);
+  for (int s = 0; s < S; ++s) last[s] += (V)(s < m_ ? s : m_) * w[s];
 }
 
 // Integers below 2^53 are exact in fp64.  Every value the fp64 pass computes
@@ -1576,9 +1600,11 @@ struct EvalBufs {
   const uint32_t* ids;      // pipeline ids sorted by bucket
   const uint32_t* sstart;   // [16 - S]: start of the S-stage pipelines in ids; [16] = total
   uint64_t* out;
-  uint32_t* ctr;            // [0] overflow count, [1 + 16 - S] deferred S-stage pipelines
+  uint32_t* ctr;            // [0] overflow count, [1 + 16 - S] deferred S-stage pipelines,
+                            // [kVariantCtr + 16 - S] S-stage overlap and zero-bubble pipelines
   uint32_t* ovf;            // overflow list (fp64 result reached 2^53)
-  uint32_t* deferred;       // deferred S-stage pipelines at [sstart[16 - S], ...)
+  uint32_t* deferred;       // deferred S-stage pipelines at [sstart[16 - S], ...), the S-stage
+                            // overlap and zero-bubble ones backwards from sstart[17 - S] - 1
   unsigned long long* skipped_ops;   // optional: recurrence ops skipped by the shortcut
   const Tab* dtab;          // the Tab in device memory
 };
@@ -1591,21 +1617,27 @@ struct EvalBufs {
 // takes the periodic shortcut and defers the lanes still aperiodic after the
 // budget; k_deferred runs those through the whole steady loop.
 // kOvl: the pipeline's plan overlaps its gradient sync with the last
-// backward pass.  The first pass (kFull false) sends such pipelines straight
-// to the deferred lists, so that its kernels carry no overlap code; the
-// deferred pass runs them with the shortcut (the whole loop where they stay
-// aperiodic) and the overlapped sync.  It does the same with zero-bubble
-// pipelines (kZb), and with every shared-layout pipeline of a context that
-// enables two-level collectives, whose sync code only the deferred pass has.
+// backward pass; kZb: it runs the zero-bubble order.  The first pass (kFull
+// false) sends both kinds to the variant lists, so that its kernels carry
+// neither; k_variant runs them with the shortcut (the whole loop where they
+// stay aperiodic).  With a context that enables two-level collectives, whose
+// sync code the first pass lacks, it sends every other shared-layout
+// pipeline to the deferred lists.
 template <int S, bool kFull, int kMode, bool kHet, bool kOvl = false, bool kZb = false>
 __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot) {
-  RegSink<S> r;
+  typename std::conditional<kZb, ZbSink<S>, RegSink<S>>::type r;
   uint32_t M;
   {
     const Plan p = load_plan<kHet>(e.packed, e.pcut, slot);
-    if (!kFull && !kHet && !kOvl && !kZb && (p.overlap | p.zb | t.ccl_hier)) {
-      e.deferred[e.sstart[kMaxStages - S] + atomicAdd(&e.ctr[1 + kMaxStages - S], 1u)] = slot;
-      return;
+    if (!kFull && !kHet && !kOvl && !kZb) {
+      if (p.overlap | p.zb) {
+        e.deferred[e.sstart[kMaxStages - S + 1] - 1 - atomicAdd(&e.ctr[kVariantCtr + kMaxStages - S], 1u)] = slot;
+        return;
+      }
+      if (t.ccl_hier) {
+        e.deferred[e.sstart[kMaxStages - S] + atomicAdd(&e.ctr[1 + kMaxStages - S], 1u)] = slot;
+        return;
+      }
     }
     M = class_mb(p);
     class_setup<kMode, kHet>(t, h, p, slot & 3, r, nullptr);
@@ -1613,7 +1645,7 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
   int skipped;
   double last[S];
   bool done = true;
-  if constexpr (kZb) pipe_zb<S, double, true>(r.f, r.b, r.c, M, skipped, last);
+  if constexpr (kZb) pipe_zb<S, double, true>(r.f, r.bi, r.w, r.c, M, skipped, last);
   else if constexpr (kOvl) done = pipe<S, double, true, true>(r.f, r.b, r.c, M, skipped, last);
   else done = pipe<S, double, !kFull>(r.f, r.b, r.c, M, skipped, last);
   // the DP tail reads the plan again (an L2 hit) rather than keeping it in
@@ -1638,20 +1670,19 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
               (unsigned long long)skipped * (unsigned long long)(6 * (S - 1) + 2));
 }
 
-// Deferred pass of one pipeline: the whole loop, or for a plan with
-// overlapped gradient sync or the zero-bubble order the shortcut first
-// (shared layout only).  The first pass sends both kinds here at once, so
-// that its kernels carry neither.
+// Deferred pass of one pipeline: the whole loop.
 template <int S, int kMode, bool kHet>
 __device__ __forceinline__ void eval_deferred(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot) {
-  const uint32_t hdr = kHet ? 0 : e.packed[slot >> 2].hdr;
-  if (!kHet && ((hdr >> 13) & 1)) {
-    eval_one<S, false, kMode, kHet, true>(t, h, e, slot);
-  } else if (!kHet && ((hdr >> 16) & 1)) {
-    eval_one<S, false, kMode, kHet, false, true>(t, h, e, slot);
-  } else {
-    eval_one<S, true, kMode, kHet>(t, h, e, slot);
-  }
+  eval_one<S, true, kMode, kHet>(t, h, e, slot);
+}
+
+// Variant pass of one pipeline (shared layout): overlapped gradient sync or
+// the zero-bubble order, the shortcut first and the whole loop where the
+// schedule stays aperiodic.
+template <int S, int kMode>
+__device__ __forceinline__ void eval_variant(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot) {
+  if ((e.packed[slot >> 2].hdr >> 16) & 1) eval_one<S, false, kMode, false, false, true>(t, h, e, slot);
+  else eval_one<S, false, kMode, false, true>(t, h, e, slot);
 }
 
 // ---------------------------------------------------------------- interleaved 1F1B
@@ -1716,8 +1747,8 @@ __device__ __forceinline__ void il_setup(const Tab& t, const Hot<kMode>& h, cons
     for (int j = 0; j < v; ++j) {
       const int vs = j * S + s;
       const uint32_t lo = vs ? cut_at(p, vs - 1) : 0, hi = cut_at(p, vs);
-      uint64_t fc, bc;
-      stage_cost<kMode, false>(t, h, p, k, ti, base, bq_in, bq_nic, lo, hi, vs == 0, vs == NV - 1, fc, bc);
+      uint64_t fc, bc, wc;
+      stage_cost<kMode, false>(t, h, p, k, ti, base, bq_in, bq_nic, lo, hi, vs == 0, vs == NV - 1, fc, bc, wc);
       f[vs] = (V)fc;
       b[vs] = (V)bc;
     }
@@ -2020,19 +2051,58 @@ __global__ void __launch_bounds__(kEvalThreads) k_deferred(const Tab* __restrict
   }
 }
 
+// Overlap and zero-bubble pipelines of the four stage counts of group GRP
+// (as k_eval's groups), taken from the variant lists the first pass filled:
+// the S-stage list runs backwards from sstart[17 - S] - 1 and holds
+// ctr[kVariantCtr + 16 - S] pipelines.  64-pipeline tiles of one stage count,
+// dealt round-robin to the waves of the grid.  The Tab is read from its copy
+// in device memory, as in k_deferred.  A block with no tile returns before
+// touching LDS, so a launch over empty lists costs next to nothing.
+template <int GRP, int kMode>
+__global__ void __launch_bounds__(kEvalThreads) k_variant(const Tab* __restrict__ tp, EvalBufs e) {
+  constexpr int kTop = kMaxStages - 4 * GRP;   // stage counts kTop-3 .. kTop
+  const uint32_t c0 = e.ctr[kVariantCtr + kMaxStages - kTop], c1 = e.ctr[kVariantCtr + kMaxStages - kTop + 1];
+  const uint32_t c2 = e.ctr[kVariantCtr + kMaxStages - kTop + 2], c3 = e.ctr[kVariantCtr + kMaxStages - kTop + 3];
+  // first tile of each list
+  const uint32_t q1 = (c0 + 63) >> 6, q2 = q1 + ((c1 + 63) >> 6), q3 = q2 + ((c2 + 63) >> 6);
+  const uint32_t tiles = q3 + ((c3 + 63) >> 6);
+  const uint32_t wpb = kEvalThreads / 64;
+  if (blockIdx.x * wpb >= tiles) return;   // the whole block, before any barrier
+  const Tab& t = *tp;
+  extern __shared__ uint4 lds[];
+  fill_lds<kMode>(t, lds);
+  const Hot<kMode> h(t, lds);
+  const uint32_t waves = gridDim.x * wpb;
+  for (uint32_t q = blockIdx.x * wpb + (threadIdx.x >> 6); q < tiles; q += waves) {
+    const uint32_t j = (q >= q1) + (q >= q2) + (q >= q3);
+    const uint32_t first = j == 0 ? 0 : j == 1 ? q1 : j == 2 ? q2 : q3;
+    const uint32_t cnt = j == 0 ? c0 : j == 1 ? c1 : j == 2 ? c2 : c3;
+    const uint32_t off = (q - first) * 64u + (threadIdx.x & 63u);
+    if (off >= cnt) continue;
+    const uint32_t S = kTop - j;
+    const uint32_t slot = e.deferred[e.sstart[kMaxStages - S + 1] - 1 - off];
+    if (j == 0) eval_variant<kTop, kMode>(t, h, e, slot);
+    else if (j == 1) eval_variant<kTop - 1, kMode>(t, h, e, slot);
+    else if (j == 2) eval_variant<kTop - 2, kMode>(t, h, e, slot);
+    else eval_variant<kTop - 3, kMode>(t, h, e, slot);
+  }
+}
+
 // Pipelines whose fp64 time reached 2^53 ps, again in u64 (exact below 2^64).
-// zb: the zero-bubble order.
+// zb: the zero-bubble order, W[s] each stage's weight-gradient pass.
 template <int S>
-__device__ __forceinline__ uint64_t redo_one(const StageRec& R, bool zb, uint32_t M) {
-  uint64_t f[S], b[S], c[S], last[S];
+__device__ __forceinline__ uint64_t redo_one(const StageRec& R, const uint64_t (&W)[kMaxStages], bool zb,
+                                             uint32_t M) {
+  uint64_t f[S], b[S], w[S], c[S], last[S];
 #pragma unroll
   for (int s = 0; s < S; ++s) {
     f[s] = R[s][0];
-    b[s] = R[s][1];
+    w[s] = zb ? W[s] : 0;
+    b[s] = R[s][1] - w[s];
     c[s] = R[s][2];
   }
   int skipped;
-  if (zb) pipe_zb<S, uint64_t, false>(f, b, c, M, skipped, last);
+  if (zb) pipe_zb<S, uint64_t, false>(f, b, w, c, M, skipped, last);
   else pipe<S, uint64_t, false>(f, b, c, M, skipped, last);
   uint64_t T = 0;
 #pragma unroll
@@ -2064,27 +2134,28 @@ __global__ void __launch_bounds__(64) k_redo_u64(Tab t, EvalBufs e) {
       continue;
     }
     StageRec R;
+    uint64_t W[kMaxStages];
     const bool w = !kHet && p.zb;
-    RecSink sink{R};
+    RecSink sink{R, W};
     class_setup<2, kHet>(t, h, p, slot & 3, sink, kHet ? e.pcut + (slot & ~3u) : nullptr);
     uint64_t r;
     switch (S) {
-      case 1: r = redo_one<1>(R, w, M); break;
-      case 2: r = redo_one<2>(R, w, M); break;
-      case 3: r = redo_one<3>(R, w, M); break;
-      case 4: r = redo_one<4>(R, w, M); break;
-      case 5: r = redo_one<5>(R, w, M); break;
-      case 6: r = redo_one<6>(R, w, M); break;
-      case 7: r = redo_one<7>(R, w, M); break;
-      case 8: r = redo_one<8>(R, w, M); break;
-      case 9: r = redo_one<9>(R, w, M); break;
-      case 10: r = redo_one<10>(R, w, M); break;
-      case 11: r = redo_one<11>(R, w, M); break;
-      case 12: r = redo_one<12>(R, w, M); break;
-      case 13: r = redo_one<13>(R, w, M); break;
-      case 14: r = redo_one<14>(R, w, M); break;
-      case 15: r = redo_one<15>(R, w, M); break;
-      default: r = redo_one<16>(R, w, M); break;
+      case 1: r = redo_one<1>(R, W, w, M); break;
+      case 2: r = redo_one<2>(R, W, w, M); break;
+      case 3: r = redo_one<3>(R, W, w, M); break;
+      case 4: r = redo_one<4>(R, W, w, M); break;
+      case 5: r = redo_one<5>(R, W, w, M); break;
+      case 6: r = redo_one<6>(R, W, w, M); break;
+      case 7: r = redo_one<7>(R, W, w, M); break;
+      case 8: r = redo_one<8>(R, W, w, M); break;
+      case 9: r = redo_one<9>(R, W, w, M); break;
+      case 10: r = redo_one<10>(R, W, w, M); break;
+      case 11: r = redo_one<11>(R, W, w, M); break;
+      case 12: r = redo_one<12>(R, W, w, M); break;
+      case 13: r = redo_one<13>(R, W, w, M); break;
+      case 14: r = redo_one<14>(R, W, w, M); break;
+      case 15: r = redo_one<15>(R, W, w, M); break;
+      default: r = redo_one<16>(R, W, w, M); break;
     }
     atomicMax((unsigned long long*)&e.out[slot >> 2], (unsigned long long)r);
   }

@@ -1,6 +1,7 @@
 // eval_pass.hip -- one evaluation pass of one variant: table mode HETSIM_MODE
 // (0..2), plan layout HETSIM_HET (0 shared, 1 per class), pass HETSIM_PASS
-// (0 the first pass's k_eval groups, 1 the deferred pass).  The build
+// (0 the first pass's k_eval groups, 1 the deferred pass, 2 the variant pass
+// of overlap and zero-bubble pipelines).  The build
 // compiles this file once per variant; kernels.hip dispatches at run time.
 #include "launch.h"
 
@@ -43,6 +44,36 @@ hipError_t occupancy_first_v(int nb[4], size_t lds) {
 }
 template hipError_t occupancy_first_v<HETSIM_MODE>(int[4], size_t);
 #endif
+
+#elif HETSIM_PASS == 2
+// overlap and zero-bubble pipelines exist in the shared layout only
+#if HETSIM_HET
+#error "the variant pass is built for the shared layout only"
+#endif
+template <int kMode>
+hipError_t launch_variant_v(const Tab& t, const EvalArgs& a, int g, hipStream_t s) {
+  const EvalBufs e = eval_bufs(a);
+  const uint32_t grid = t.grid_variant[g];
+  const size_t lds = kMode < 2 ? t.lds_bytes : 0;
+  if (g == 0) k_variant<0, kMode><<<grid, kEvalThreads, lds, s>>>(e.dtab, e);
+  else if (g == 1) k_variant<1, kMode><<<grid, kEvalThreads, lds, s>>>(e.dtab, e);
+  else if (g == 2) k_variant<2, kMode><<<grid, kEvalThreads, lds, s>>>(e.dtab, e);
+  else k_variant<3, kMode><<<grid, kEvalThreads, lds, s>>>(e.dtab, e);
+  return hipGetLastError();
+}
+template hipError_t launch_variant_v<HETSIM_MODE>(const Tab&, const EvalArgs&, int, hipStream_t);
+
+template <int kMode>
+hipError_t occupancy_variant_v(int nb[4], size_t lds) {
+  const void* k[4] = {(const void*)k_variant<0, kMode>, (const void*)k_variant<1, kMode>,
+                      (const void*)k_variant<2, kMode>, (const void*)k_variant<3, kMode>};
+  for (int i = 0; i < 4; ++i) {
+    hipError_t r = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb[i], k[i], kEvalThreads, lds);
+    if (r != hipSuccess) return r;
+  }
+  return hipSuccess;
+}
+template hipError_t occupancy_variant_v<HETSIM_MODE>(int[4], size_t);
 
 #else
 template <int kMode, bool kHet>

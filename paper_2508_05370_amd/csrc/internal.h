@@ -1,5 +1,6 @@
 // internal.h -- context tables shared by the host builder and the gfx950 kernels.
 #pragma once
+#include <hip/hip_runtime.h>
 #include <stdint.h>
 #include <vector>
 
@@ -97,15 +98,20 @@ struct Tab {
   const void* img;                // the image in device memory (16-byte aligned)
   uint32_t grid_eval[4];          // blocks of each first-pass kernel that fit the device at once
   uint32_t grid_deferred;
+  uint32_t grid_variant[4];       // blocks of each variant-pass kernel that fit the device at once
 };
 
 // Device buffers of one evaluation pass over a chunk, as the host hands them
 // to the launcher.  sstart[16 - S] is the first sorted id of the S-stage
 // pipelines, sstart[16] their total and the first id of the interleaved
 // pipelines (layout above).  ctr[0] counts overflowed pipelines,
-// ctr[1 + 16 - S] the S-stage pipelines deferred to the full-loop pass; the
-// overflow list follows the counters at ctr + kEvalCounters.
-constexpr uint32_t kEvalCounters = 32;
+// ctr[1 + 16 - S] the S-stage pipelines deferred to the full-loop pass,
+// ctr[kVariantCtr + 16 - S] the S-stage overlap and zero-bubble pipelines
+// of the variant pass; the overflow list follows the counters at
+// ctr + kEvalCounters.
+constexpr uint32_t kVariantCtr = 1 + kMaxStages;
+constexpr uint32_t kEvalCounters = 48;
+static_assert(kVariantCtr + kMaxStages <= kEvalCounters, "evaluation counters");
 // The skipped-work counter is spread over slots on separate cache lines so
 // that the waves of a launch do not serialise on one address.
 constexpr uint32_t kSkipSlots = 512, kSkipStride = 16;
@@ -122,6 +128,50 @@ struct EvalArgs {
   uint64_t* skipped_ops;       // optional: kSkipSlots counters, kSkipStride words apart
   const Tab* dtab;             // the context's Tab in device memory (read by the deferred pass)
 };
+
+constexpr size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Workspace of one chunk: packed plans, pipeline metadata, pipeline ids and
+// the deferred lists, bucket counts followed by the evaluation counters and
+// the overflow list (counts and counters cleared together), bucket cursors,
+// the start of each stage count's pipelines, each pipeline's bucket key
+// (u16, written with the metadata and read by the scatter), and with the
+// per-class layout
+// the plans' class cut rows (64 bytes per plan) and the syncs each pipeline's
+// stages wait for (16 u64 per pipeline slot, 512 bytes per plan).
+constexpr uint32_t kCounters = kBuckets + kEvalCounters;
+struct Work {
+  PackedPlan* packed;
+  uint4* pcut;
+  uint64_t* hdp;
+  uint32_t *meta, *ids, *deferred, *hist, *ctr, *cursor, *sstart;
+  uint16_t* keys;
+};
+constexpr size_t cut_rows_bytes(int64_t ch, bool het) { return het ? align256((size_t)ch * 64) : 0; }
+constexpr size_t het_sync_bytes(int64_t ch, bool het) {
+  return het ? align256((size_t)ch * kMaxClasses * kMaxStages * 8) : 0;
+}
+constexpr size_t work_bytes(int64_t ch, bool het) {
+  return align256((size_t)ch * sizeof(PackedPlan)) + 3 * align256((size_t)ch * 4 * 4) +
+         align256(kCounters * 4 + (size_t)ch * 4 * 4) + align256(kBuckets * 4) + align256(kSstartWords * 4) +
+         align256((size_t)ch * 4 * 2) +
+         cut_rows_bytes(ch, het) + het_sync_bytes(ch, het);
+}
+inline Work carve(void* base, int64_t ch, bool het) {
+  Work w;
+  char* p = (char*)base;
+  w.pcut = het ? (uint4*)p : nullptr; p += cut_rows_bytes(ch, het);
+  w.hdp = het ? (uint64_t*)p : nullptr; p += het_sync_bytes(ch, het);
+  w.packed = (PackedPlan*)p; p += align256((size_t)ch * sizeof(PackedPlan));
+  w.meta = (uint32_t*)p; p += align256((size_t)ch * 16);
+  w.ids = (uint32_t*)p; p += align256((size_t)ch * 16);
+  w.deferred = (uint32_t*)p; p += align256((size_t)ch * 16);
+  w.hist = (uint32_t*)p; w.ctr = w.hist + kBuckets; p += align256(kCounters * 4 + (size_t)ch * 16);
+  w.cursor = (uint32_t*)p; p += align256(kBuckets * 4);
+  w.sstart = (uint32_t*)p; p += align256(kSstartWords * 4);
+  w.keys = (uint16_t*)p;
+  return w;
+}
 
 // Host side: validate descriptors and build the tables (host copies).
 struct HostTables {

@@ -209,7 +209,7 @@ int eval_grids(Tab* t) {
   if (r == hipSuccess) r = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (r != hipSuccess) return (int)r;
   const size_t lds = t->mode < 2 ? t->lds_bytes : 0;
-  int nb[5] = {0, 0, 0, 0, 0};
+  int nb[9] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
   if (t->mode == 0) r = occupancy_first_v<0>(nb, lds);
   else if (t->mode == 1) r = occupancy_first_v<1>(nb, lds);
   else r = occupancy_first_v<2>(nb, lds);
@@ -218,9 +218,15 @@ int eval_grids(Tab* t) {
     else if (t->mode == 1) r = occupancy_deferred_v<1>(nb + 4, lds);
     else r = occupancy_deferred_v<2>(nb + 4, lds);
   }
+  if (r == hipSuccess) {
+    if (t->mode == 0) r = occupancy_variant_v<0>(nb + 5, lds);
+    else if (t->mode == 1) r = occupancy_variant_v<1>(nb + 5, lds);
+    else r = occupancy_variant_v<2>(nb + 5, lds);
+  }
   if (r != hipSuccess) return (int)r;
   for (int i = 0; i < 4; ++i) t->grid_eval[i] = (uint32_t)((nb[i] > 0 ? nb[i] : 1) * cus);
   t->grid_deferred = (uint32_t)((nb[4] > 0 ? nb[4] : 1) * cus);
+  for (int i = 0; i < 4; ++i) t->grid_variant[i] = (uint32_t)((nb[5 + i] > 0 ? nb[5 + i] : 1) * cus);
   return 0;
 }
 
@@ -232,10 +238,21 @@ hipError_t launch_group(const Tab& t, const EvalArgs& a, uint32_t max_tasks, int
   return het ? launch_group_v<2, true>(t, a, max_tasks, g, s) : launch_group_v<2, false>(t, a, max_tasks, g, s);
 }
 
-// first pass over a chunk: k_eval of each stage-count group, in order
+// variant pass of one stage-count group: the overlap and zero-bubble
+// pipelines the group's first pass listed (none with the per-class layout)
+hipError_t launch_variant(const Tab& t, const EvalArgs& a, int g, hipStream_t s) {
+  if (a.pcut) return hipSuccess;
+  if (t.mode == 0) return launch_variant_v<0>(t, a, g, s);
+  if (t.mode == 1) return launch_variant_v<1>(t, a, g, s);
+  return launch_variant_v<2>(t, a, g, s);
+}
+
+// first pass over a chunk: k_eval of each stage-count group, in order, then
+// the variant passes
 hipError_t launch_first(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s) {
   hipError_t r = hipSuccess;
   for (int g = 0; g < 4 && r == hipSuccess; ++g) r = launch_group(t, a, max_tasks, g, s);
+  for (int g = 0; g < 4 && r == hipSuccess; ++g) r = launch_variant(t, a, g, s);
   return r;
 }
 

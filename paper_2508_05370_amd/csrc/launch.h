@@ -15,8 +15,13 @@ template <int kMode, bool kHet>
 hipError_t launch_deferred_v(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s);
 // Blocks per CU of the shared-layout first-pass kernels (nb[0..3]) or of the
 // deferred kernel (nb[0]) at the given LDS size.
+// Variant pass of stage-count group g: overlap and zero-bubble pipelines.
+template <int kMode>
+hipError_t launch_variant_v(const Tab& t, const EvalArgs& a, int g, hipStream_t s);
 template <int kMode>
 hipError_t occupancy_first_v(int nb[4], size_t lds);
+template <int kMode>
+hipError_t occupancy_variant_v(int nb[4], size_t lds);
 template <int kMode>
 hipError_t occupancy_deferred_v(int nb[1], size_t lds);
 
@@ -30,6 +35,12 @@ HETSIM_EXTERN_VARIANT(1, true)
 HETSIM_EXTERN_VARIANT(2, false)
 HETSIM_EXTERN_VARIANT(2, true)
 #undef HETSIM_EXTERN_VARIANT
+extern template hipError_t launch_variant_v<0>(const Tab&, const EvalArgs&, int, hipStream_t);
+extern template hipError_t launch_variant_v<1>(const Tab&, const EvalArgs&, int, hipStream_t);
+extern template hipError_t launch_variant_v<2>(const Tab&, const EvalArgs&, int, hipStream_t);
+extern template hipError_t occupancy_variant_v<0>(int[4], size_t);
+extern template hipError_t occupancy_variant_v<1>(int[4], size_t);
+extern template hipError_t occupancy_variant_v<2>(int[4], size_t);
 extern template hipError_t occupancy_first_v<0>(int[4], size_t);
 extern template hipError_t occupancy_first_v<1>(int[4], size_t);
 extern template hipError_t occupancy_first_v<2>(int[4], size_t);

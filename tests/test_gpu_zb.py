@@ -59,6 +59,22 @@ def test_zero_bubble_plans(torch, B, oracle_mod, workloads, idx):
     want = oracle_mod.Oracle(w["model"], w["cluster"]).eval(p)
     _equal(got, want, "zero-bubble workload %d" % idx)
     assert np.count_nonzero(want != MAXU) > n // 4
+    if w["model"].get("experts"):
+        # MoE plans whose backward carries an all-to-all (EP > 1) are among those compared
+        ep_gt1 = ((p["hdr"] >> 2) & 3) > 0
+        assert np.count_nonzero(ep_gt1 & (want != MAXU)) > n // 10
+
+
+def test_zero_bubble_moe_hand_worked(torch, B, oracle_mod, workloads):
+    """The hand-worked MoE plan of the oracle's pins (EP 4, uniform loads, all-to-all on the node
+    fabric, weight-gradient pass half of the backward compute) and its 1F1B twin."""
+    import test_oracle_zb as Z
+    o, p, m, c = Z._moe_zb_setup(oracle_mod, workloads)
+    say("case: hand-worked MoE zero-bubble plan")
+    got = _times(B, B.Sim(m, c), p)
+    want = o.eval(p)
+    _equal(got, want, "hand-worked MoE zero-bubble")
+    assert np.all(want != MAXU) and want[0] < want[1]
 
 
 def test_zero_bubble_mixed(torch, B, oracle_mod, workloads):

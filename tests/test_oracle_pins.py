@@ -328,3 +328,161 @@ def test_moe_all_to_all_closed_form(oracle_mod, workloads):
     T, h, e, topk = 256, 4096, 2, 2
     per_a2a = (ep - 1) * 1000 + (ep - 1) * T * topk * h * e // ep * 40
     assert epf == 2 * 4 * per_a2a
+
+
+# ------------------------------------------------------------------ hand-worked communication and cost terms
+def _one_type(n_nodes, dpn, **kw):
+    t = dict(n_nodes=n_nodes, dev_per_node=dpn, tflops=300, hbm_GBps=2000, intra_MBps=25_000, pcie_MBps=0,
+             nic_MBps=25_000, intra_alpha_ps=1000, pcie_alpha_ps=0, nic_alpha_ps=0)
+    t.update(kw)
+    return t
+
+
+@pytest.mark.parametrize("tp", [2, 4, 8])
+def test_tp_allreduce_closed_form(oracle_mod, workloads, tp):
+    """TP all-reduces are exposed in the forward pass only (Table 1): two per layer (after the
+    attention and after the MLP) and one for the vocabulary-parallel embedding on the first stage,
+    each a ring all-reduce over the tp ranks of a node: 2(tp-1) steps of one latency and of an
+    activation shard Act/tp.  On a 25 GB/s fabric (exactly 40 ps/B) with 1 us per message, a
+    stage holding n layers gets nAR = 2n + [first stage] all-reduces; with 1000 ps per message,
+    TPF = nAR 2(tp-1) 1000 ps + nAR 2(tp-1) (Act/tp) 40 ps.
+    Rejects: (tp-1) steps instead of 2(tp-1); no embedding all-reduce; the whole activation per
+    step; a TP term in the backward pass."""
+    m = workloads.model("llama-7b", L=4, seq=256, global_batch=2)
+    c = dict(types=[_one_type(2, 8)], nic_MBps_dev=None, intra_MBps_node=None)
+    o = oracle_mod.Oracle(m, c)
+    p = _plan()
+    _set(p, 0, tp=tp, cuts=(1, 4), classes=((1, 2, 0x00),))
+    d = o.detail(p, 0)
+    act = 256 * 4096 * 2
+    for s, (layers, first, last) in enumerate(((range(0, 1), 1, 0), (range(1, 4), 0, 1))):
+        comp_f = sum(o.layer_time(0, tp, 1, 1, l) for l in layers)
+        comp_b = sum(o.layer_time(0, tp, 1, 1, l, True) for l in layers)
+        if first:
+            comp_f += o.embed_time(0, 1)
+            comp_b += o.embed_time(0, 1, True)
+        if last:
+            comp_f += o.head_time(0, tp, 1)
+            comp_b += o.head_time(0, tp, 1, True)
+        n_ar = 2 * len(layers) + first
+        steps = n_ar * 2 * (tp - 1)
+        assert d["f"][0][s] - comp_f == steps * 1000 + steps * (act // tp) * 40, (tp, s)
+        assert d["b"][0][s] == comp_b, (tp, s)
+
+
+def _hop_cluster(nodes_a=1, dpn_a=4):
+    # Table 5's delays: A100-like type A with 2 x 287.5 ns PCIe trips, H100-like type B with
+    # 2 x 143.75 ns, NIC processing 368 ns on both
+    A = _one_type(nodes_a, dpn_a, intra_MBps=300_000, intra_alpha_ps=30_670, pcie_MBps=32_000,
+                  pcie_alpha_ps=287_500, nic_MBps=25_000, nic_alpha_ps=368_000)
+    B = _one_type(1, 4, intra_MBps=450_000, intra_alpha_ps=20_440, pcie_MBps=64_000, pcie_alpha_ps=143_750,
+                  nic_MBps=50_000, nic_alpha_ps=368_000)
+    return dict(types=[A, B], nic_MBps_dev=None, intra_MBps_node=None)
+
+
+def test_pp_hop_inter_node_with_pcie(oracle_mod, workloads):
+    """An inter-node pipeline hop goes GPU -> PCIe switch -> NIC on each end (Sec. 5: two PCIe
+    trips per side) plus the NIC's processing delay (Table 5), and both ends pay; the activation
+    crosses at the slowest of the two NICs and the two PCIe links.  Stage 0 on type A, stage 1 on
+    type B: alpha = (2 x 287,500 + 368,000) + (2 x 143,750 + 368,000) ps.  With the NICs slower
+    than PCIe the rate is A's NIC (40 ps/B); with A's PCIe link at 16 GB/s (62.5 ps/B) it is that
+    link.  Rejects: latency of one end only; one PCIe trip per side; the PCIe rate ignored."""
+    m = workloads.model("gpt2-small")
+    act = 1024 * 768 * 2
+    alpha = (2 * 287_500 + 368_000) + (2 * 143_750 + 368_000)
+    for pcie_a, ps_per_byte in ((32_000, 40), (16_000, 62.5)):
+        c = _hop_cluster()
+        c["types"][0]["pcie_MBps"] = pcie_a
+        o = oracle_mod.Oracle(m, c)
+        p = _plan()
+        _set(p, 0, cuts=(6, 12), classes=((4, 8, 0x10),))
+        d = o.detail(p, 0)
+        assert d["c"][0][0] == alpha + int(act * ps_per_byte), pcie_a
+
+
+def test_pp_hop_intra_vs_inter_in_one_pool(oracle_mod, workloads):
+    """Within one pool a hop is intra-node iff every replica's pair of devices shares a node:
+    two replicas per stage on one 4-device node pay one node-fabric message (30.67 ns, and the
+    activation at 300 GB/s with the per-byte rate rounded up in 2^-16 ps units); on 2-device
+    nodes the stages sit on different nodes and the hop pays both ends' inter-node path on
+    type A.  Rejects: the intra/inter decision taken per pool rather than per node."""
+    m = workloads.model("gpt2-small")
+    act = 1024 * 768 * 2
+    bq_intra = -(-65536 * 10**6 // 300_000)                      # ps per byte in 2^-16 units, rounded up
+    o = oracle_mod.Oracle(m, _hop_cluster(1, 4))
+    p = _plan()
+    _set(p, 0, cuts=(6, 12), classes=((2, 8, 0x00),))
+    assert o.detail(p, 0)["c"][0][0] == 30_670 + -(-act * bq_intra // 65536)
+    o2 = oracle_mod.Oracle(m, _hop_cluster(2, 2))
+    assert o2.detail(p, 0)["c"][0][0] == 2 * (2 * 287_500 + 368_000) + act * 40
+
+
+def test_expert_imbalance_takes_busiest_rank(oracle_mod, workloads):
+    """R9: an MoE layer waits for its busiest EP rank.  On a device of 1 TFLOP/s (one flop per ps)
+    whose memory is fast enough that no op's bytes cost more than 1 ps, an expert that receives n
+    tokens costs 2 n h 2f (up and gate) + 1 (the activation) + 2 n f h (down) = 6 n h f + 1 ps
+    forward.  At EP 2, rank 0 hosts experts 0-3 and rank 1 experts 4-7; expert e receives
+    ceil(ep T topk q_e / 2^16) tokens of the ep T routed ones.  Moving load from rank 1 to rank 0
+    changes the layer by the change of the busiest rank's sum, not of the sum or the mean over
+    ranks (those stay put).  Rejects: sum or mean over ranks in place of the max."""
+    L, E, h, f, seq, topk, ep = 1, 8, 64, 128, 16, 2, 2
+    m = dict(L=L, h=h, heads=4, kv_heads=4, ffn=0, gated=1, vocab=128, learned_pos=0, seq=seq, dtype_bytes=2,
+             global_batch=2, mbs=[1], experts=E, topk=topk, expert_ffn=f, grad_bytes=4, param_bytes=2, opt_bytes=12)
+    c = dict(types=[_one_type(1, 4, tflops=1, hbm_GBps=4_000_000_000)], nic_MBps_dev=None, intra_MBps_node=None)
+
+    def expert(n):
+        return 6 * n * h * f + 1 if n else 2          # an idle expert still reads its two weight blocks
+
+    def busiest(q):
+        T = seq
+        tok = [-(-ep * T * topk * int(x) // 65536) for x in q]
+        return max(sum(expert(n) for n in tok[:4]), sum(expert(n) for n in tok[4:]))
+
+    uniform = [8192] * 8
+    skew = [16384, 16384, 8192, 8192, 4096, 4096, 4096, 4096]
+    t = {}
+    for name, q in (("uniform", uniform), ("skew", skew)):
+        mm = dict(m, load_q16=np.array([q], dtype=np.uint32))
+        t[name] = oracle_mod.Oracle(mm, c).layer_time(0, 1, 1, ep, 0)
+    assert busiest(skew) != busiest(uniform)
+    assert t["skew"] - t["uniform"] == busiest(skew) - busiest(uniform)
+
+
+def test_embedding_bytes(oracle_mod, workloads):
+    """The input embedding is a gather, not a GEMM: per token it reads one table row of h elements
+    and writes one output row; with learned positions it also reads a position row and adds it
+    (reading the partial sum and writing the result).  So it moves 2 T h e bytes (4 T h e with
+    learned positions), whatever the vocabulary and the TP degree, at the memory rate:
+    1000 B / hbm ps, i.e. exactly B ps at 1000 GB/s; backward twice that.  Rejects: the whole
+    table read; positions not counted; compute-rate costing."""
+    c = dict(types=[_one_type(1, 4, hbm_GBps=1000, tflops=1)], nic_MBps_dev=None, intra_MBps_node=None)
+    for name, pos in (("gpt2-small", 1), ("llama-7b", 0)):
+        for vocab in (32000, 64000):
+            m = workloads.model(name, vocab=vocab, seq=512)
+            o = oracle_mod.Oracle(m, c)
+            for b in (1, 2):
+                T = b * 512
+                B = T * m["h"] * m["dtype_bytes"] * (4 if pos else 2)
+                assert o.embed_time(0, b) == B, (name, vocab, b)
+                assert o.embed_time(0, b, True) == 2 * B
+
+
+def test_dp_ring_inter_node_latency(oracle_mod, workloads):
+    """A DP ring whose members sit on several nodes crosses the inter-node path at every step:
+    each step pays both ends' latency (two PCIe trips and the NIC on each side, Sec. 5 and
+    Table 5) and moves its chunk at the slowest NIC or PCIe rate; inside one node it pays the node
+    fabric's.  A 4-replica ring all-reduce of the whole model's fp32 gradients (PP 1, TP 1) over
+    type A on two 2-device nodes: 2(p-1) steps of 2 (2 x 287,500 + 368,000) ps and of
+    ceil(G/p) bytes at 40 ps/B (the 25 GB/s NIC; PCIe is 32 GB/s).  Two replicas on one node: the
+    same ring on the fabric (30.67 ns, 300 GB/s).  Rejects: one end's latency per step."""
+    m = workloads.model("gpt2-small")
+    grads = 4 * oracle_mod.Oracle(m, _hop_cluster()).param_count(True)
+    p = _plan()
+    _set(p, 0, cuts=(12,), classes=((4, 8, 0x00),))
+    d = oracle_mod.Oracle(m, _hop_cluster(2, 2)).detail(p, 0)
+    steps = 2 * 3
+    assert d["tdp"][0][0] == steps * 2 * (2 * 287_500 + 368_000) + steps * -(-grads // 4) * 40
+    _set(p, 0, cuts=(12,), classes=((2, 8, 0x00),))
+    d = oracle_mod.Oracle(m, _hop_cluster(1, 2)).detail(p, 0)
+    bq = -(-65536 * 10**6 // 300_000)
+    assert d["tdp"][0][0] == 2 * 30_670 + -(-(2 * -(-grads // 2)) * bq // 65536)

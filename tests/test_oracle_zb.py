@@ -3,7 +3,7 @@
 The backward pass splits into B (input gradient, what the previous stage waits for) and W
 (weight gradient, local); stage s runs the 1F1B order of forwards and B passes and releases
 each W s micro-batches after its B (ZB-H1 of Qi et al. 2024, "Zero Bubble Pipeline
-Parallelism"), W being half of the stage's backward time.  Pinned: that paper's ZB-H1 bubble
+Parallelism"), W being half of the stage's backward compute (the MoE all-to-all stays in B).  Pinned: that paper's ZB-H1 bubble
 (S - 1)(F + B - W) for equal pass costs, an
 event-driven replay of the same op lists (independent code), the reduction to 1F1B when W
 costs nothing, the in-flight count (every stage at most S micro-batches, 1F1B's peak) against a
@@ -86,7 +86,8 @@ def _set(p, i, cuts, classes, tp=1, zero=0, zb=1, overlap=0, v=1):
 
 
 def test_plan_split_and_schedule(oracle_mod, workloads):
-    """W is half of each stage's backward time (rounded down) and B the rest; the stage times
+    """Dense model: W is half of each stage's backward time (rounded down; all of it is compute)
+    and B the rest; the stage times
     equal the plain plan's, the ends are the zero-bubble pipeline over them, and the iteration is
     the latest end plus its sync."""
     m = workloads.model("gpt2-small")
@@ -140,22 +141,55 @@ def test_invalid_zero_bubble_plans(oracle_mod, workloads):
     assert np.all(o.eval(h) == MAXU)
 
 
-def test_split_with_moe_all_to_all(oracle_mod, workloads):
-    """For an MoE model the backward includes the expert all-to-all; W is still half of the
-    whole backward time and the plan's time follows the zero-bubble pipeline over the split."""
-    w = workloads.workload(4)
-    p = workloads.plans(w, 0, 400)
-    p["hdr"] |= np.uint32(1 << 16)
-    o = oracle_mod.Oracle(w["model"], w["cluster"])
-    checked = 0
-    for i in range(0, 400, 7):
-        d = o.detail(p, i)
-        if d is None:
-            continue
-        for g in range(d["G"]):
-            assert d["w"][g] == [x // 2 for x in d["b"][g]]
-            bi = [x - y for x, y in zip(d["b"][g], d["w"][g])]
-            S = d["S"]
-            assert d["end"][g] == oracle_mod.pipeline_zb(S, d["M"][g], d["f"][g], bi, d["w"][g], d["c"][g][:S - 1])
-        checked += 1
-    assert checked > 30
+def _moe_zb_setup(oracle_mod, workloads):
+    """A Mixtral-shaped 4-layer MoE model at uniform expert load on two 4-device nodes of one
+    type: two stages of 4 replicas at EP 4 (each stage's EP group fills one node, so its
+    all-to-all runs on the node fabric), 4 micro-batches per replica; the hop between the stages
+    crosses nodes over 25 GB/s NICs with 1000 ps per NIC side and no PCIe delay."""
+    m = workloads.model("mixtral-8x7b", L=4, seq=256, global_batch=16)
+    m["load_q16"] = np.full((4, 8), 65536 // 8, dtype=np.uint32)
+    c = workloads.cluster_two_type_8()
+    c["types"][0].update(n_nodes=2, dev_per_node=4, intra_MBps=25_000, intra_alpha_ps=1000, nic_MBps=25_000,
+                         nic_alpha_ps=1000, pcie_alpha_ps=0)
+    o = oracle_mod.Oracle(m, c)
+    p = _plan(2)
+    hdr = 2 << 2                                                  # EP 4
+    _set(p, 0, (2, 4), ((4, 16, 0x00),))
+    _set(p, 1, (2, 4), ((4, 16, 0x00),), zb=0)
+    p["hdr"][:] |= np.uint32(hdr)
+    return o, p, m, c
+
+
+def test_moe_split_keeps_all_to_all_in_input_gradient(oracle_mod, workloads):
+    """ZB-H1 splits a layer's backward compute into the input-gradient and the weight-gradient
+    GEMMs; the MoE all-to-all of the backward pass carries input gradients between EP ranks, so it
+    belongs to B.  Hand computation: per stage, Bc = the layers' (and embedding's or head's)
+    backward compute, EPB = 2 all-to-alls per layer, each (ep-1) alpha + (ep-1)/ep T topk h e at
+    40 ps/B (25 GB/s; the pairwise-exchange closed form), W = floor(Bc / 2), B = Bc - W + EPB.
+    The hop between the stages crosses nodes: both NIC sides' 1000 ps and the activation T h e at
+    40 ps/B.  The stage ends are then an event-driven replay of the zero-bubble op lists
+    (independent code) over (F, B, W) and that hop, and the iteration the latest end plus the
+    stage's sync.  Rejects: W taken as
+    half of the whole backward including the all-to-all; the all-to-all moved into W."""
+    o, p, _, _ = _moe_zb_setup(oracle_mod, workloads)
+    ep, T, h, e, topk = 4, 256, 4096, 2, 2
+    per_a2a = (ep - 1) * 1000 + (ep - 1) * T * topk * h * e // ep * 40
+    d = o.detail(p, 0)
+    assert d is not None and d["S"] == 2 and d["M"][0] == 4
+    lay = [(o.layer_time(0, 1, 1, ep, l), o.layer_time(0, 1, 1, ep, l, True)) for l in range(4)]
+    fc = [lay[0][0] + lay[1][0] + o.embed_time(0, 1), lay[2][0] + lay[3][0] + o.head_time(0, 1, 1)]
+    bc = [lay[0][1] + lay[1][1] + o.embed_time(0, 1, True), lay[2][1] + lay[3][1] + o.head_time(0, 1, 1, True)]
+    epb = 2 * 2 * per_a2a                                          # two layers per stage, two all-to-alls each
+    f = [x + epb for x in fc]
+    w = [x // 2 for x in bc]
+    bi = [x - y + epb for x, y in zip(bc, w)]
+    assert d["f"][0][:2] == f
+    assert d["b"][0][:2] == [x + epb for x in bc]
+    assert d["w"][0][:2] == w
+    hop = 2 * 1000 + T * h * e * 40
+    assert d["c"][0][0] == hop
+    end = brute_sim.simulate_zb(2, 4, f, bi, w, [hop, 0])
+    assert d["end"][0][:2] == end
+    assert d["time"] == max(x + t for x, t in zip(end, d["tdp"][0][:2]))
+    # the all-to-all really is there, and half of it is not what W holds
+    assert epb > 0 and all(x != (b + epb) // 2 for x, b in zip(w, bc))
