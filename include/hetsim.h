@@ -36,6 +36,7 @@ extern "C" {
 #define SIM_ERANGE (-2)   /* descriptor could overflow the 64-bit time arithmetic */
 #define SIM_ENOMEM (-3)   /* host or device allocation failed */
 #define SIM_EHIP (-4)     /* a HIP runtime call or kernel launch failed */
+#define SIM_ESIZE (-5)    /* more plans than sim_eval_plans_noalloc's fixed workspace holds */
 
 /* per-plan result of an invalid or infeasible plan */
 #define SIM_TIME_INVALID UINT64_MAX
@@ -223,6 +224,28 @@ int sim_create(const sim_model_desc* model, const sim_cluster_desc* cluster, sim
  * launch fails.
  */
 int sim_eval_plans(sim_ctx* ctx, const sim_plans* plans, int64_t n, uint64_t* out_time_ps, void* stream);
+
+/* Plans per call of sim_eval_plans_noalloc: shared layout, per-class layout. */
+#define SIM_NOALLOC_MAX_PLANS (1 << 18)
+#define SIM_NOALLOC_MAX_PLANS_PER_CLASS (1 << 16)
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * results as sim_eval_plans, computed by the same kernels, with no
+ * hipMalloc, hipFree, pool allocation, stream or event creation.  The
+ * workspace is a static device array of about 46 MiB that every GPU the
+ * library runs on holds from the first sim_create on it until the process
+ * ends.  Every call on one GPU shares that GPU's array: calls that overlap
+ * in time on one GPU (on two streams, from two threads or two contexts)
+ * race and give wrong results; serialize them.  The counters a call needs
+ * are cleared by a fill kernel on `stream` (no memset node), and every other
+ * buffer is rewritten before it is read, so consecutive calls need nothing
+ * in between.  All work runs on `stream` in order.  Returns SIM_ESIZE when n
+ * exceeds SIM_NOALLOC_MAX_PLANS (SIM_NOALLOC_MAX_PLANS_PER_CLASS for the
+ * per-class layout), SIM_EINVAL and SIM_EHIP as sim_eval_plans.
+ */
+int sim_eval_plans_noalloc(sim_ctx* ctx, const sim_plans* plans, int64_t n, uint64_t* out_time_ps, void* stream);
 
 /*
  * Per-stage quantities of plans 0..n-1 (device memory, caller-owned):

@@ -12,7 +12,8 @@ import numpy as np
 
 from . import _build
 
-SIM_OK, SIM_EINVAL, SIM_ERANGE, SIM_ENOMEM, SIM_EHIP = 0, -1, -2, -3, -4
+SIM_OK, SIM_EINVAL, SIM_ERANGE, SIM_ENOMEM, SIM_EHIP, SIM_ESIZE = 0, -1, -2, -3, -4, -5
+SIM_NOALLOC_MAX_PLANS, SIM_NOALLOC_MAX_PLANS_PER_CLASS = 1 << 18, 1 << 16
 TIME_INVALID = 2**64 - 1
 
 _lib = None
@@ -43,7 +44,7 @@ class Best(C.Structure):
     _fields_ = [("time_ps", C.c_uint64), ("index", C.c_int64)]
 
 
-EXPORTS = ("sim_create", "sim_eval_plans", "sim_eval_stages", "sim_eval_memory", "sim_argmin", "sim_best_reduce", "sim_set_timing",
+EXPORTS = ("sim_create", "sim_eval_plans", "sim_eval_plans_noalloc", "sim_eval_stages", "sim_eval_memory", "sim_argmin", "sim_best_reduce", "sim_set_timing",
            "sim_get_timing", "sim_get_skipped_ops", "sim_destroy", "sim_strerror")
 
 
@@ -60,6 +61,8 @@ def lib():
         L.sim_create.restype = C.c_int
         L.sim_eval_plans.argtypes = [P, C.POINTER(Plans), I64, P, P]
         L.sim_eval_plans.restype = C.c_int
+        L.sim_eval_plans_noalloc.argtypes = [P, C.POINTER(Plans), I64, P, P]
+        L.sim_eval_plans_noalloc.restype = C.c_int
         L.sim_eval_stages.argtypes = [P, C.POINTER(Plans), I64, P, P, P]
         L.sim_eval_stages.restype = C.c_int
         L.sim_eval_memory.argtypes = [P, C.POINTER(Plans), I64, P, P]
@@ -227,6 +230,18 @@ class Sim:
             out = torch.empty(n, dtype=torch.int64, device=dp["hdr"].device)
         ps = plans_struct(dp, offset)
         _check(lib().sim_eval_plans(self.h, C.byref(ps), n, out.data_ptr(), _stream(stream)), "sim_eval_plans")
+        return out
+
+    def eval_plans_noalloc(self, dp, n=None, out=None, offset=0, stream=None):
+        """As eval_plans, through the allocation-free entry point (its workspace is the library's static
+        device array; at most SIM_NOALLOC_MAX_PLANS plans per call).  `out` must be given: this call
+        allocates nothing."""
+        if n is None:
+            n = dp["hdr"].shape[0] - offset
+        assert out is not None, "eval_plans_noalloc writes into a caller-provided tensor"
+        ps = plans_struct(dp, offset)
+        _check(lib().sim_eval_plans_noalloc(self.h, C.byref(ps), n, out.data_ptr(), _stream(stream)),
+               "sim_eval_plans_noalloc")
         return out
 
     def eval_stages(self, dp, n=None, stream=None):

@@ -63,6 +63,7 @@ extern "C" const char* sim_strerror(int code) {
     case SIM_ERANGE: return "descriptor could overflow 64-bit picosecond arithmetic";
     case SIM_ENOMEM: return "out of memory";
     case SIM_EHIP: return "HIP runtime error";
+    case SIM_ESIZE: return "more plans than the allocation-free entry point's workspace holds (SIM_NOALLOC_MAX_PLANS)";
     default: return "unknown error";
   }
 }
@@ -83,6 +84,9 @@ extern "C" int sim_create(const sim_model_desc* model, const sim_cluster_desc* c
   c->aux = nullptr;
   for (auto& g : c->grp) g = nullptr;
   if (hipGetDevice(&c->device) != hipSuccess) { delete ht; delete c; return SIM_EHIP; }
+  // this device's copy of the allocation-free workspace (resolved once per device)
+  void* scratch = nullptr;
+  if (noalloc_scratch(c->device, &scratch) != 0) { delete ht; delete c; return SIM_EHIP; }
   // the table image, then the skipped-work counter slots
   const size_t img = align256(ht->img.size());
   if (hipMalloc(&c->tables, img + kSkipBytes + align256(sizeof(Tab))) != hipSuccess) {
@@ -256,6 +260,33 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
   for (auto& x : evs)
     if (x) (void)hipEventDestroy(x);
   if (!ws) return SIM_ENOMEM;
+  return e == hipSuccess ? SIM_OK : SIM_EHIP;
+}
+
+static_assert(SIM_NOALLOC_MAX_PLANS == kNoAllocPlans && SIM_NOALLOC_MAX_PLANS_PER_CLASS == kNoAllocPlansHet,
+              "allocation-free limits");
+
+// One chunk on the caller's stream, with the workspace in the static device
+// array: no allocation, no side streams, no events.
+extern "C" int sim_eval_plans_noalloc(sim_ctx* c, const sim_plans* plans, int64_t n, uint64_t* out, void* stream) {
+  if (!c || !plans_ok(plans, n) || (n > 0 && !out)) return SIM_EINVAL;
+  if (n == 0) return SIM_OK;
+  const bool het = plans->chdr != nullptr;
+  if (n > (het ? kNoAllocPlansHet : kNoAllocPlans)) return SIM_ESIZE;
+  hipStream_t s = (hipStream_t)stream;
+  if (hipSetDevice(c->device) != hipSuccess) return SIM_EHIP;
+  void* ws = nullptr;
+  if (noalloc_scratch(c->device, &ws) != 0) return SIM_EHIP;
+  const Work W = carve(ws, n, het);
+  hipError_t e = launch_fill32(W.hist, kCounters, 0, s);
+  if (e == hipSuccess) e = launch_prep(c->tab, *plans, n, out, W.packed, W.pcut, W.meta, W.hist, W.keys, s);
+  if (e == hipSuccess && het) e = launch_plan_syncs(c->tab, W.packed, W.pcut, W.meta, n, W.hdp, s);
+  if (e == hipSuccess) e = launch_scan(W.hist, W.cursor, W.sstart, s);
+  if (e == hipSuccess) e = launch_scatter(W.keys, (uint32_t)(n * 4), W.cursor, W.ids, s);
+  const EvalArgs a = {W.packed, W.pcut, W.hdp, W.meta, W.ids, W.sstart, out, W.ctr, W.deferred,
+                      c->timing ? c->skipped_ops : nullptr, c->dtab};
+  if (e == hipSuccess) e = launch_first(c->tab, a, (uint32_t)(n * 4), s);
+  if (e == hipSuccess) e = launch_deferred(c->tab, a, (uint32_t)(n * 4), s);
   return e == hipSuccess ? SIM_OK : SIM_EHIP;
 }
 

@@ -173,6 +173,18 @@ inline Work carve(void* base, int64_t ch, bool het) {
   return w;
 }
 
+// The allocation-free entry point's workspace: one chunk of at most
+// kNoAllocPlans plans in the shared layout or kNoAllocPlansHet in the
+// per-class layout, in a static device array (one per GPU).
+constexpr int64_t kNoAllocPlans = 1 << 18;
+constexpr int64_t kNoAllocPlansHet = 1 << 16;
+constexpr size_t kNoAllocBytes = work_bytes(kNoAllocPlans, false) > work_bytes(kNoAllocPlansHet, true)
+                                     ? work_bytes(kNoAllocPlans, false)
+                                     : work_bytes(kNoAllocPlansHet, true);
+// Address of this device's copy of that array (the current device); 0 or a
+// HIP error code.
+int noalloc_scratch(int device, void** ptr);
+
 // Host side: validate descriptors and build the tables (host copies).
 struct HostTables {
   Tab tab;

@@ -2,9 +2,39 @@
 // passes (those are in eval_pass.hip): packing and checking, bucketing,
 // per-stage records, device memory, the u64 redo and the argmin; and the
 // launchers the C ABI calls.  The data flow is described in device.h.
+#include <mutex>
+
 #include "launch.h"
 
 namespace hetsim {
+
+// ---------------------------------------------------------------- allocation-free workspace
+// The workspace of sim_eval_plans_noalloc: one chunk's buffers (kNoAllocBytes,
+// about 46 MiB) in a static device array.  Every GPU the library runs on holds
+// its own copy until the process ends; host code reaches it only through the
+// address hipGetSymbolAddress returns for the current device (the array's
+// name in host code is a host-side stand-in, not a device address).
+static __device__ __align__(256) uint8_t scratch[kNoAllocBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void* scratch_ptr[kMaxDevices];
+}  // namespace
+
+int noalloc_scratch(int device, void** ptr) {
+  if (device < 0 || device >= kMaxDevices || !ptr) return (int)hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> g(scratch_mu);
+  if (!scratch_ptr[device]) {
+    void* p = nullptr;
+    const hipError_t r = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (r != hipSuccess) return (int)r;
+    if (!p) return (int)hipErrorInvalidSymbol;
+    scratch_ptr[device] = p;
+  }
+  *ptr = scratch_ptr[device];
+  return 0;
+}
 
 // ---------------------------------------------------------------- bucketing
 __global__ void k_fill32(uint32_t* p, uint32_t n, uint32_t v) {

@@ -31,8 +31,9 @@ def test_exports_every_declared_symbol(B):
 
 def test_strerror(B):
     L = B.lib()
-    for code in (0, -1, -2, -3, -4):
+    for code in (0, -1, -2, -3, -4, -5):
         assert L.sim_strerror(code)
+    assert b"allocation-free" in L.sim_strerror(B.SIM_ESIZE)
     assert L.sim_strerror(-99) == b"unknown error"
 
 
@@ -105,6 +106,7 @@ def test_null_arguments(B):
     L = B.lib()
     assert L.sim_create(None, None, None) == B.SIM_EINVAL
     assert L.sim_eval_plans(None, None, 0, None, None) == B.SIM_EINVAL
+    assert L.sim_eval_plans_noalloc(None, None, 0, None, None) == B.SIM_EINVAL
     assert L.sim_eval_stages(None, None, 0, None, None, None) == B.SIM_EINVAL
     assert L.sim_eval_memory(None, None, 0, None, None) == B.SIM_EINVAL
     assert L.sim_argmin(None, None, 0, 0, None, None) == B.SIM_EINVAL
