@@ -248,6 +248,17 @@ int sim_eval_plans(sim_ctx* ctx, const sim_plans* plans, int64_t n, uint64_t* ou
 int sim_eval_plans_noalloc(sim_ctx* ctx, const sim_plans* plans, int64_t n, uint64_t* out_time_ps, void* stream);
 
 /*
+ * Measurement helper for roofline reports (no part of an evaluation): the
+ * peak rate, in nodes per second, at which the current device runs the
+ * recurrence's schedule-node operation -- end = max(end, input + hop) +
+ * duration, three fp64 VALU operations -- over independent chains, so that
+ * instruction issue and not latency bounds it.  Blocking: it allocates a
+ * small buffer, launches on `stream`, waits for it and frees the buffer.
+ * Returns SIM_EINVAL for a NULL result, SIM_ENOMEM or SIM_EHIP on failure.
+ */
+int sim_measure_node_rate(double* nodes_per_s, void* stream);
+
+/*
  * Per-stage quantities of plans 0..n-1 (device memory, caller-owned):
  *   out_stage[((i*4 + c)*16 + s)*4 + q], q = 0 forward time of one
  *   micro-batch on stage s of class c, 1 backward time, 2 pipeline hop

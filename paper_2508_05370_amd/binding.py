@@ -45,7 +45,7 @@ class Best(C.Structure):
 
 
 EXPORTS = ("sim_create", "sim_eval_plans", "sim_eval_plans_noalloc", "sim_eval_stages", "sim_eval_memory", "sim_argmin", "sim_best_reduce", "sim_set_timing",
-           "sim_get_timing", "sim_get_skipped_ops", "sim_destroy", "sim_strerror")
+           "sim_get_timing", "sim_get_skipped_ops", "sim_destroy", "sim_strerror", "sim_measure_node_rate")
 
 
 def lib():
@@ -63,6 +63,8 @@ def lib():
         L.sim_eval_plans.restype = C.c_int
         L.sim_eval_plans_noalloc.argtypes = [P, C.POINTER(Plans), I64, P, P]
         L.sim_eval_plans_noalloc.restype = C.c_int
+        L.sim_measure_node_rate.argtypes = [C.POINTER(C.c_double), P]
+        L.sim_measure_node_rate.restype = C.c_int
         L.sim_eval_stages.argtypes = [P, C.POINTER(Plans), I64, P, P, P]
         L.sim_eval_stages.restype = C.c_int
         L.sim_eval_memory.argtypes = [P, C.POINTER(Plans), I64, P, P]
@@ -297,6 +299,13 @@ class Sim:
         v = C.c_uint64()
         _check(lib().sim_get_skipped_ops(self.h, C.byref(v)), "sim_get_skipped_ops")
         return v.value
+
+
+def measure_node_rate(stream=None):
+    """Peak schedule-node rate of the current device (nodes/s; three fp64 VALU ops per node)."""
+    v = C.c_double()
+    _check(lib().sim_measure_node_rate(C.byref(v), _stream(stream)), "sim_measure_node_rate")
+    return v.value
 
 
 def best_tuple(slot_tensor):

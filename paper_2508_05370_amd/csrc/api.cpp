@@ -27,6 +27,7 @@ hipError_t launch_variant(const Tab& t, const EvalArgs& a, int g, hipStream_t s)
 hipError_t launch_deferred(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s);
 hipError_t launch_argmin(const uint64_t* t, int64_t n, int64_t base, sim_best* b, hipStream_t s);
 hipError_t launch_best_reduce(const sim_best* in, int64_t n, sim_best* out, hipStream_t s);
+hipError_t launch_node_probe(double* sink, int blocks, int iters, hipStream_t s);
 }  // namespace hetsim
 
 using namespace hetsim;
@@ -368,4 +369,40 @@ extern "C" int sim_get_timing(sim_ctx* c, int kind, double* total_ms, int64_t* l
   *total_ms = sum;
   *launches = (int64_t)v.size();
   return rc;
+}
+
+// Times the node probe on `stream` (blocking): 32 blocks of 256 threads per
+// CU, 8 chains per thread, 4096 nodes per chain; the faster of two timed runs
+// after one warm-up.
+extern "C" int sim_measure_node_rate(double* nodes_per_s, void* stream) {
+  if (!nodes_per_s) return SIM_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return SIM_EHIP;
+  const int blocks = 32 * cus, iters = 4096;
+  double* sink = nullptr;
+  if (hipMalloc(&sink, (size_t)blocks * 256 * sizeof(double)) != hipSuccess) return SIM_ENOMEM;
+  hipEvent_t a = nullptr, b = nullptr;
+  int rc = SIM_OK;
+  float best = 0;
+  if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) rc = SIM_EHIP;
+  for (int r = 0; r < 3 && rc == SIM_OK; ++r) {
+    if (hipEventRecord(a, s) != hipSuccess || launch_node_probe(sink, blocks, iters, s) != hipSuccess ||
+        hipEventRecord(b, s) != hipSuccess || hipEventSynchronize(b) != hipSuccess) {
+      rc = SIM_EHIP;
+      break;
+    }
+    float ms = 0;
+    if (hipEventElapsedTime(&ms, a, b) != hipSuccess) rc = SIM_EHIP;
+    if (r > 0 && (best == 0 || ms < best)) best = ms;
+  }
+  if (a) (void)hipEventDestroy(a);
+  if (b) (void)hipEventDestroy(b);
+  (void)hipFree(sink);
+  if (rc != SIM_OK) return rc;
+  if (best <= 0) return SIM_EHIP;
+  *nodes_per_s = (double)blocks * 256 * 8 * iters / (best * 1e-3);
+  return SIM_OK;
 }

@@ -226,6 +226,33 @@ hipError_t launch_scatter(const uint16_t* keys, uint32_t nslots, uint32_t* curso
   k_scatter<<<blocks_for(nslots, 256 * kScatterPer), 256, 0, s>>>(keys, nslots, cursor, ids);
   return hipGetLastError();
 }
+// ---------------------------------------------------------------- node-rate probe
+// Peak rate of the recurrence's schedule-node operation on this device:
+// end = max(end, input + hop) + duration, in fp64 (add, max, add), over
+// kProbeChains independent chains per lane so that issue, not latency,
+// bounds it.  The result feeds roofline reports; it is not part of any
+// evaluation.
+constexpr int kProbeChains = 8;
+__global__ void __launch_bounds__(256) k_node_probe(double* __restrict__ sink, int iters, double c, double d) {
+  double a[kProbeChains];
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+#pragma unroll
+  for (int j = 0; j < kProbeChains; ++j) a[j] = (double)(i + j);
+  for (int k = 0; k < iters; ++k) {
+#pragma unroll
+    for (int j = 0; j < kProbeChains; ++j) a[j] = __builtin_fmax(a[j], a[(j + 1) % kProbeChains] + c) + d;
+  }
+  double t = 0;
+#pragma unroll
+  for (int j = 0; j < kProbeChains; ++j) t += a[j];
+  sink[i] = t;
+}
+
+hipError_t launch_node_probe(double* sink, int blocks, int iters, hipStream_t s) {
+  k_node_probe<<<blocks, 256, 0, s>>>(sink, iters, 3.0, 1.0);
+  return hipGetLastError();
+}
+
 // ---------------------------------------------------------------- evaluation passes
 EvalBufs eval_bufs(const EvalArgs& a) {
   return {a.packed, (const uint4*)a.pcut, a.hdp, a.meta, a.ids, a.sstart, a.out, a.ctr, a.ctr + kEvalCounters, a.deferred,
