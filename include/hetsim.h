@@ -270,8 +270,8 @@ int sim_measure_node_rate(double* nodes_per_s, void* stream);
  *   class or an invalid plan).  For an interleaved plan s runs over the
  *   PP*v virtual stages for q = 0, 1; q = 2 and 3 are per device (s < PP;
  *   the hop of device PP-1 is the one back to device 0) and 0 past PP.
- * Entries of absent stages are left untouched.  n is at most 2^21 per call.
- * Same errors as sim_eval_plans.
+ * Entries of absent stages are left untouched.  Plans are worked in chunks
+ * of 2^21 through one temporary workspace.  Same errors as sim_eval_plans.
  */
 int sim_eval_stages(sim_ctx* ctx, const sim_plans* plans, int64_t n, uint64_t* out_stage, uint32_t* out_class,
                     void* stream);
@@ -302,7 +302,7 @@ int sim_eval_stages(sim_ctx* ctx, const sim_plans* plans, int64_t n, uint64_t* o
  * chunk).  Entries of absent classes and stages
  * are 0; all 64 entries of a plan that breaks another rule are
  * SIM_TIME_INVALID.  The memory check itself does not affect this output.
- * n is at most 2^21 per call.  Errors as sim_eval_plans.
+ * Any n; plans are worked in chunks of 2^21.  Errors as sim_eval_plans.
  */
 int sim_eval_memory(sim_ctx* ctx, const sim_plans* plans, int64_t n, uint64_t* out_mem, void* stream);
 
@@ -350,6 +350,13 @@ int sim_get_timing(sim_ctx* ctx, int kind, double* total_ms, int64_t* launches);
  */
 int sim_get_skipped_ops(sim_ctx* ctx, uint64_t* ops);
 
+/*
+ * Release a context.  Waits for the context's own work only: its side
+ * streams and the latest call it was given on each caller stream (up to 16
+ * caller streams are tracked; past that it waits for the whole device).
+ * Calls on a stream under graph capture are not tracked: the caller must
+ * not destroy a context that a graph it has not yet finished still uses.
+ */
 void sim_destroy(sim_ctx* ctx);
 const char* sim_strerror(int code);
 

@@ -43,12 +43,22 @@ def _compile(cmd):
     return proc.returncode, text
 
 
-def build(force=True, verbose=False):
-    if not force and os.path.exists(LIB):
+def _stale(src, obj):
+    """An object is stale when older than its source or any header of the library."""
+    if not os.path.exists(obj):
+        return True
+    deps = [src] + [os.path.join(d, f) for d in (CSRC, INCLUDE) for f in os.listdir(d) if f.endswith(".h")]
+    return os.path.getmtime(obj) < max(os.path.getmtime(x) for x in deps)
+
+
+def build(force=True, verbose=False, incremental=False):
+    """Compile every object and link the library.  incremental: recompile only stale objects."""
+    if not force and not incremental and os.path.exists(LIB):
         return LIB
     os.makedirs(BUILD, exist_ok=True)
     cmds = [["hipcc", *HIP_FLAGS, *extra, "-I", INCLUDE, "-c", os.path.join(CSRC, src), "-o", os.path.join(BUILD, obj)]
-            for src, obj, extra in SOURCES]
+            for src, obj, extra in SOURCES
+            if not incremental or _stale(os.path.join(CSRC, src), os.path.join(BUILD, obj))]
     with concurrent.futures.ThreadPoolExecutor(max_workers=_jobs()) as pool:
         results = list(pool.map(_compile, cmds))
     for cmd, (rc, text) in zip(cmds, results):
@@ -64,4 +74,5 @@ def build(force=True, verbose=False):
 
 
 if __name__ == "__main__":
-    print(build(verbose=True))
+    import sys
+    print(build(verbose=True, incremental="--incremental" in sys.argv))

@@ -41,6 +41,21 @@ struct EventPair {
 };
 }  // namespace
 
+// Side streams of multi-chunk calls made on one caller stream: the four
+// first-pass groups and the deferred pass.  Each caller stream gets its own
+// set, so calls on different caller streams do not queue behind each other.
+struct SideStreams {
+  hipStream_t caller;
+  hipStream_t aux;
+  hipStream_t grp[4];
+};
+
+// Streams this context has launched work on, each with an event recorded
+// after its latest call: sim_destroy waits for these (and the side streams)
+// rather than for the whole device.  The events are created with the
+// context, so that recording one allocates nothing.
+constexpr int kTracked = 16;
+
 struct sim_ctx {
   Tab tab;
   int device;
@@ -51,8 +66,11 @@ struct sim_ctx {
   std::vector<EventPair> ev[4];
   uint64_t* skipped_ops;   // device counter, inside `tables`
   Tab* dtab;               // copy of `tab` in device memory, inside `tables`
-  hipStream_t aux;         // deferred passes of multi-chunk calls, created on first use
-  hipStream_t grp[4];      // first-pass groups of multi-chunk calls, created on first use
+  std::vector<SideStreams> side;   // per caller stream, created on first use
+  hipStream_t seen[kTracked];      // caller streams of calls so far
+  hipEvent_t seen_ev[kTracked];    // recorded after the latest call on seen[j]
+  int nseen;
+  bool untracked;                  // more than kTracked streams were used
 };
 
 constexpr size_t kSkipBytes = (size_t)kSkipSlots * kSkipStride * 8;
@@ -82,49 +100,90 @@ extern "C" int sim_create(const sim_model_desc* model, const sim_cluster_desc* c
   c->timing = false;
   c->tables = nullptr;
   c->pool = nullptr;
-  c->aux = nullptr;
-  for (auto& g : c->grp) g = nullptr;
+  c->nseen = 0;
+  c->untracked = false;
+  for (auto& e : c->seen_ev) e = nullptr;
   if (hipGetDevice(&c->device) != hipSuccess) { delete ht; delete c; return SIM_EHIP; }
+  for (auto& e : c->seen_ev)
+    if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) {
+      for (auto& x : c->seen_ev)
+        if (x) (void)hipEventDestroy(x);
+      delete ht; delete c; return SIM_EHIP;
+    }
   // this device's copy of the allocation-free workspace (resolved once per device)
   void* scratch = nullptr;
-  if (noalloc_scratch(c->device, &scratch) != 0) { delete ht; delete c; return SIM_EHIP; }
+  auto fail = [&](int rc) {
+    for (auto& x : c->seen_ev) (void)hipEventDestroy(x);
+    if (c->tables) (void)hipFree(c->tables);
+    delete ht;
+    delete c;
+    return rc;
+  };
+  if (noalloc_scratch(c->device, &scratch) != 0) return fail(SIM_EHIP);
   // the table image, then the skipped-work counter slots
   const size_t img = align256(ht->img.size());
   if (hipMalloc(&c->tables, img + kSkipBytes + align256(sizeof(Tab))) != hipSuccess) {
-    delete ht; delete c; return SIM_ENOMEM;
+    c->tables = nullptr;
+    return fail(SIM_ENOMEM);
   }
   if (hipMemcpy(c->tables, ht->img.data(), ht->img.size(), hipMemcpyHostToDevice) != hipSuccess ||
-      hipMemset((char*)c->tables + img, 0, kSkipBytes) != hipSuccess) {
-    (void)hipFree(c->tables); delete ht; delete c; return SIM_EHIP;
-  }
+      hipMemset((char*)c->tables + img, 0, kSkipBytes) != hipSuccess)
+    return fail(SIM_EHIP);
   c->tab.img = c->tables;
-  if (eval_grids(&c->tab) != 0) { (void)hipFree(c->tables); delete ht; delete c; return SIM_EHIP; }
+  if (eval_grids(&c->tab) != 0) return fail(SIM_EHIP);
   c->skipped_ops = (uint64_t*)((char*)c->tables + img);
   c->dtab = (Tab*)((char*)c->tables + img + kSkipBytes);
-  if (hipMemcpy(c->dtab, &c->tab, sizeof(Tab), hipMemcpyHostToDevice) != hipSuccess) {
-    (void)hipFree(c->tables); delete ht; delete c; return SIM_EHIP;
-  }
-  delete ht;
+  if (hipMemcpy(c->dtab, &c->tab, sizeof(Tab), hipMemcpyHostToDevice) != hipSuccess) return fail(SIM_EHIP);
   hipMemPoolProps props;
   memset(&props, 0, sizeof(props));
   props.allocType = hipMemAllocationTypePinned;
   props.location.type = hipMemLocationTypeDevice;
   props.location.id = c->device;
-  if (hipMemPoolCreate(&c->pool, &props) != hipSuccess) { (void)hipFree(c->tables); delete c; return SIM_EHIP; }
+  if (hipMemPoolCreate(&c->pool, &props) != hipSuccess) {
+    c->pool = nullptr;
+    return fail(SIM_EHIP);
+  }
+  delete ht;
   uint64_t keep = UINT64_MAX;   // keep workspace memory cached between calls
   (void)hipMemPoolSetAttribute(c->pool, hipMemPoolAttrReleaseThreshold, &keep);
   *out = c;
   return SIM_OK;
 }
 
+// Record that a call has been launched on stream s (after its last launch).
+static void track(sim_ctx* c, hipStream_t s) {
+  std::lock_guard<std::mutex> g(c->mu);
+  int j = 0;
+  while (j < c->nseen && c->seen[j] != s) ++j;
+  if (j == c->nseen) {
+    if (j == kTracked) {
+      c->untracked = true;
+      return;
+    }
+    c->seen[c->nseen++] = s;
+  }
+  (void)hipEventRecord(c->seen_ev[j], s);
+}
+
 extern "C" void sim_destroy(sim_ctx* c) {
   if (!c) return;
+  (void)hipSetDevice(c->device);
+  // wait for this context's work: its side streams and the latest call on
+  // every caller stream it was given (the whole device only if it was given
+  // more streams than it tracks)
+  for (auto& q : c->side) {
+    (void)hipStreamSynchronize(q.aux);
+    for (auto g : q.grp) (void)hipStreamSynchronize(g);
+  }
+  if (c->untracked) (void)hipDeviceSynchronize();
+  for (int j = 0; j < c->nseen; ++j) (void)hipEventSynchronize(c->seen_ev[j]);
   for (auto& v : c->ev)
     for (auto& e : v) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }
-  (void)hipDeviceSynchronize();
-  if (c->aux) (void)hipStreamDestroy(c->aux);
-  for (auto& g : c->grp)
-    if (g) (void)hipStreamDestroy(g);
+  for (auto& e : c->seen_ev) (void)hipEventDestroy(e);
+  for (auto& q : c->side) {
+    (void)hipStreamDestroy(q.aux);
+    for (auto g : q.grp) (void)hipStreamDestroy(g);
+  }
   if (c->pool) (void)hipMemPoolDestroy(c->pool);
   if (c->tables) (void)hipFree(c->tables);
   delete c;
@@ -149,17 +208,29 @@ static void end_event(sim_ctx* c, int kind, hipStream_t s, EventPair* e) {
   c->ev[kind].push_back(*e);
 }
 
-static bool side_streams(sim_ctx* c) {
+// The side streams of caller stream s (created on its first multi-chunk call).
+static bool side_streams(sim_ctx* c, hipStream_t s, SideStreams* out) {
   std::lock_guard<std::mutex> g(c->mu);
-  if (!c->aux && hipStreamCreateWithFlags(&c->aux, hipStreamNonBlocking) != hipSuccess) c->aux = nullptr;
-  for (auto& q : c->grp)
-    if (!q && hipStreamCreateWithFlags(&q, hipStreamNonBlocking) != hipSuccess) q = nullptr;
-  bool ok = c->aux != nullptr;
-  for (auto q : c->grp) ok = ok && q;
-  return ok;
+  for (auto& q : c->side)
+    if (q.caller == s) {
+      *out = q;
+      return true;
+    }
+  SideStreams q = {s, nullptr, {nullptr, nullptr, nullptr, nullptr}};
+  bool ok = hipStreamCreateWithFlags(&q.aux, hipStreamNonBlocking) == hipSuccess;
+  for (auto& x : q.grp) ok = ok && hipStreamCreateWithFlags(&x, hipStreamNonBlocking) == hipSuccess;
+  if (!ok) {
+    if (q.aux) (void)hipStreamDestroy(q.aux);
+    for (auto x : q.grp)
+      if (x) (void)hipStreamDestroy(x);
+    return false;
+  }
+  c->side.push_back(q);
+  *out = q;
+  return true;
 }
 
-// Chunks of kChunk plans.  With more than one chunk, the four stage-count
+// Chunks of kChunk plans (one chunk up to 2 kChunk).  With more than one chunk, the four stage-count
 // groups of chunk i's first pass run on four streams of the context, and its
 // deferred pass on a fifth that waits for the four, while the call's stream
 // packs and sorts chunk i + 1.  The two workspaces alternate; the call's
@@ -170,17 +241,22 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
   if (n == 0) return SIM_OK;
   hipStream_t s = (hipStream_t)stream;
   if (hipSetDevice(c->device) != hipSuccess) return SIM_EHIP;
-  const int64_t ch = n < kChunk ? n : kChunk;
+  // up to two chunks' worth of plans run as one chunk on the caller's stream
+  // alone (so that calls on several caller streams overlap each other);
+  // larger calls are worked in kChunk chunks, double-buffered, with side
+  // streams
+  const int64_t ch = n <= 2 * kChunk ? n : kChunk;
   const int nbuf = n > ch ? 2 : 1;
   hipStream_t aux = s;
+  SideStreams side = {};
   constexpr int kEv = 2 * 6;   // per buffer: sorted, four group ends, deferred end
   hipEvent_t evs[kEv] = {};
   auto sorted = [&](int b) { return evs[b * 6]; };
   auto fin = [&](int b, int g) { return evs[b * 6 + 1 + g]; };
   auto done = [&](int b) { return evs[b * 6 + 5]; };
   if (nbuf == 2) {
-    if (!side_streams(c)) return SIM_EHIP;
-    aux = c->aux;
+    if (!side_streams(c, s, &side)) return SIM_EHIP;
+    aux = side.aux;
     for (int j = 0; j < kEv; ++j)
       if (hipEventCreateWithFlags(&evs[j], hipEventDisableTiming) != hipSuccess) {
         for (auto& x : evs)
@@ -226,10 +302,10 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
       if (e == hipSuccess) e = hipEventRecord(sorted(b), s);
       joined = false;
       for (int g = 0; g < 4 && e == hipSuccess; ++g) {
-        e = hipStreamWaitEvent(c->grp[g], sorted(b), 0);
-        if (e == hipSuccess) e = launch_group(c->tab, a, (uint32_t)(cn * 4), g, c->grp[g]);
-        if (e == hipSuccess) e = launch_variant(c->tab, a, g, c->grp[g]);
-        if (e == hipSuccess) e = hipEventRecord(fin(b, g), c->grp[g]);
+        e = hipStreamWaitEvent(side.grp[g], sorted(b), 0);
+        if (e == hipSuccess) e = launch_group(c->tab, a, (uint32_t)(cn * 4), g, side.grp[g]);
+        if (e == hipSuccess) e = launch_variant(c->tab, a, g, side.grp[g]);
+        if (e == hipSuccess) e = hipEventRecord(fin(b, g), side.grp[g]);
         if (e == hipSuccess) e = hipStreamWaitEvent(aux, fin(b, g), 0);
       }
       if (t0) end_event(c, 0, aux, &e0);
@@ -246,7 +322,7 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
   // the call's stream takes over everything the side streams were given (after
   // a failed launch, drain them before the workspace is released)
   if (nbuf == 2 && e != hipSuccess) {
-    for (auto q : c->grp) (void)hipStreamSynchronize(q);
+    for (auto q : side.grp) (void)hipStreamSynchronize(q);
     (void)hipStreamSynchronize(aux);
   } else if (!joined) {
     for (int g = 0; g < 4; ++g) {
@@ -258,6 +334,7 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
   }
   if (tcall) end_event(c, 2, s, &call);
   if (ws) (void)hipFreeAsync(ws, s);
+  track(c, s);
   for (auto& x : evs)
     if (x) (void)hipEventDestroy(x);
   if (!ws) return SIM_ENOMEM;
@@ -288,6 +365,10 @@ extern "C" int sim_eval_plans_noalloc(sim_ctx* c, const sim_plans* plans, int64_
                       c->timing ? c->skipped_ops : nullptr, c->dtab};
   if (e == hipSuccess) e = launch_first(c->tab, a, (uint32_t)(n * 4), s);
   if (e == hipSuccess) e = launch_deferred(c->tab, a, (uint32_t)(n * 4), s);
+  // a stream under graph capture records nothing here: the launches become
+  // graph nodes, and the caller owns the graph's completion
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(s, &cap) == hipSuccess && cap == hipStreamCaptureStatusNone) track(c, s);
   return e == hipSuccess ? SIM_OK : SIM_EHIP;
 }
 
@@ -295,40 +376,65 @@ extern "C" int sim_eval_stages(sim_ctx* c, const sim_plans* plans, int64_t n, ui
                                uint32_t* out_class, void* stream) {
   if (!c || !plans_ok(plans, n) || (n > 0 && (!out_stage || !out_class))) return SIM_EINVAL;
   if (n == 0) return SIM_OK;
-  if (n > kChunk) return SIM_EINVAL;
   hipStream_t s = (hipStream_t)stream;
   if (hipSetDevice(c->device) != hipSuccess) return SIM_EHIP;
   void* ws = nullptr;
   const bool het = plans->chdr != nullptr;
-  if (hipMallocFromPoolAsync(&ws, align256((size_t)n * sizeof(PackedPlan)) + cut_rows_bytes(n, het), c->pool, s) !=
+  const int64_t ch = n < kChunk ? n : kChunk;
+  if (hipMallocFromPoolAsync(&ws, align256((size_t)ch * sizeof(PackedPlan)) + cut_rows_bytes(ch, het), c->pool, s) !=
       hipSuccess)
     return SIM_ENOMEM;
   PackedPlan* packed = (PackedPlan*)ws;
-  uint4* pcut = het ? (uint4*)((char*)ws + align256((size_t)n * sizeof(PackedPlan))) : nullptr;
-  hipError_t e = launch_prep(c->tab, *plans, n, nullptr, packed, pcut, out_class, nullptr, nullptr, s);
-  if (e == hipSuccess) e = launch_stages(c->tab, packed, pcut, out_class, n, out_stage, s);
+  uint4* pcut = het ? (uint4*)((char*)ws + align256((size_t)ch * sizeof(PackedPlan))) : nullptr;
+  hipError_t e = hipSuccess;
+  // chunks of kChunk plans through one workspace, in order on the stream
+  for (int64_t off = 0; off < n && e == hipSuccess; off += ch) {
+    const int64_t cn = n - off < ch ? n - off : ch;
+    sim_plans p = *plans;
+    p.hdr += off; p.cls += off; p.types += off;
+    if (p.cut) p.cut += off;
+    if (het) { p.chdr += off; p.ccut += off; }
+    e = launch_prep(c->tab, p, cn, nullptr, packed, pcut, out_class + off * 4, nullptr, nullptr, s);
+    if (e == hipSuccess)
+      e = launch_stages(c->tab, packed, pcut, out_class + off * 4, cn, out_stage + off * 4 * kMaxStages * 4, s);
+  }
   (void)hipFreeAsync(ws, s);
+  track(c, s);
   return e == hipSuccess ? SIM_OK : SIM_EHIP;
 }
 
 extern "C" int sim_eval_memory(sim_ctx* c, const sim_plans* plans, int64_t n, uint64_t* out_mem, void* stream) {
   if (!c || !plans_ok(plans, n) || (n > 0 && !out_mem)) return SIM_EINVAL;
   if (n == 0) return SIM_OK;
-  if (n > kChunk) return SIM_EINVAL;
   if (hipSetDevice(c->device) != hipSuccess) return SIM_EHIP;
-  return launch_memory(c->tab, *plans, n, out_mem, (hipStream_t)stream) == hipSuccess ? SIM_OK : SIM_EHIP;
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = hipSuccess;
+  for (int64_t off = 0; off < n && e == hipSuccess; off += kChunk) {
+    const int64_t cn = n - off < kChunk ? n - off : kChunk;
+    sim_plans p = *plans;
+    p.hdr += off; p.cls += off; p.types += off;
+    if (p.cut) p.cut += off;
+    if (p.chdr) { p.chdr += off; p.ccut += off; }
+    e = launch_memory(c->tab, p, cn, out_mem + off * 4 * kMaxStages, s);
+  }
+  track(c, s);
+  return e == hipSuccess ? SIM_OK : SIM_EHIP;
 }
 
 extern "C" int sim_argmin(sim_ctx* c, const uint64_t* t, int64_t n, int64_t base, sim_best* out, void* stream) {
   if (!c || !out || n < 0 || (n > 0 && !t)) return SIM_EINVAL;
   if (hipSetDevice(c->device) != hipSuccess) return SIM_EHIP;
-  return launch_argmin(t, n, base, out, (hipStream_t)stream) == hipSuccess ? SIM_OK : SIM_EHIP;
+  const hipError_t e = launch_argmin(t, n, base, out, (hipStream_t)stream);
+  track(c, (hipStream_t)stream);
+  return e == hipSuccess ? SIM_OK : SIM_EHIP;
 }
 
 extern "C" int sim_best_reduce(sim_ctx* c, const sim_best* in, int64_t n, sim_best* out, void* stream) {
   if (!c || !out || n < 0 || (n > 0 && !in)) return SIM_EINVAL;
   if (hipSetDevice(c->device) != hipSuccess) return SIM_EHIP;
-  return launch_best_reduce(in, n, out, (hipStream_t)stream) == hipSuccess ? SIM_OK : SIM_EHIP;
+  const hipError_t e = launch_best_reduce(in, n, out, (hipStream_t)stream);
+  track(c, (hipStream_t)stream);
+  return e == hipSuccess ? SIM_OK : SIM_EHIP;
 }
 
 extern "C" int sim_set_timing(sim_ctx* c, int enable) {

@@ -175,14 +175,15 @@ def test_interleaved_memory(torch, B, oracle_mod, workloads, idx):
 
 
 def test_interleaved_chunks_and_streams(torch, B, oracle_mod, workloads):
-    """More than one 2M-plan chunk of interleaved plans, checked on samples."""
+    """More than two 2M-plan chunks of interleaved plans (a call above 4M plans is worked in 2M
+    chunks), checked on samples."""
     w = workloads.workload(3)
-    n = (1 << 21) + 40_013
+    n = (1 << 22) + 40_013
     p = workloads.interleaved_plans(w, 0, n)
-    say("case: interleaved, %d plans in two chunks" % n)
+    say("case: interleaved, %d plans in three chunks" % n)
     got = _times(B, B.Sim(w["model"], w["cluster"]), p)
     rng = np.random.default_rng(3)
-    sample = np.unique(np.concatenate([rng.integers(0, n, 30_000), np.arange((1 << 21) - 50, (1 << 21) + 50)]))
+    sample = np.unique(np.concatenate([rng.integers(0, n, 30_000), np.arange((1 << 21) - 50, (1 << 21) + 50), np.arange((1 << 22) - 50, (1 << 22) + 50)]))
     sub = {k: np.ascontiguousarray(x[..., sample]) for k, x in p.items()}
     want = oracle_mod.Oracle(w["model"], w["cluster"]).eval(sub)
     _equal(got[sample], want, "interleaved multi-chunk")

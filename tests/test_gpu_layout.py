@@ -113,11 +113,12 @@ def test_per_class_memory(torch, B, oracle_mod, workloads, idx):
 
 
 def test_per_class_chunks_and_streams(torch, B, oracle_mod, workloads):
-    """More than one 2M-plan chunk: the per-class cut rows follow every chunk's offset."""
+    """More than two 2M-plan chunks (a call above 4M plans is worked in 2M chunks): the per-class
+    cut rows follow every chunk's offset."""
     w = workloads.workload(3)
-    n = (1 << 21) + 40_013
+    n = (1 << 22) + 40_013
     p = workloads.het_plans(w, 0, n)
-    say("case: per-class layout, %d plans in two chunks" % n)
+    say("case: per-class layout, %d plans in three chunks" % n)
     got = B.times_u64(B.Sim(w["model"], w["cluster"]).eval_plans(B.device_plans(p)))
     want = oracle_mod.Oracle(w["model"], w["cluster"]).eval(p)
     _equal(got, want, "per-class multi-chunk")

@@ -162,20 +162,21 @@ def test_all_cluster_options_with_memory(torch, B, oracle_mod, workloads, idx):
 
 @pytest.mark.parametrize("idx", [3, 5])
 def test_all_cluster_options_two_chunks(torch, B, oracle_mod, workloads, idx):
-    """More than one 2M-plan chunk in one call (double-buffered workspaces, side streams) with
-    every cluster option on, over mixed plan kinds; checked on sampled plans."""
+    """More than two 2M-plan chunks in one call (a call above 4M plans is worked in 2M chunks:
+    double-buffered workspaces, side streams) with every cluster option on, over mixed plan kinds;
+    checked on sampled plans."""
     w = workloads.workload(idx)
     c = dict(w["cluster"], **ALL_FLAGS)
-    n = (1 << 21) + 4097
+    n = (1 << 22) + 4097
     a = workloads.plans(w, 0, n)
     a["hdr"][1::5] |= np.uint32(1 << 13)
     a["hdr"][2::5] |= np.uint32(1 << 16)
     b = workloads.interleaved_plans(w, 0, n // 4)
     p = _concat([a, b], np.random.default_rng(idx + 20).permutation(n + n // 4))
-    say("case: every cluster option, two chunks of mixed kinds, workload %d" % idx)
+    say("case: every cluster option, three chunks of mixed kinds, workload %d" % idx)
     got = B.times_u64(B.Sim(w["model"], c).eval_plans(B.device_plans(p)))
     rng = np.random.default_rng(idx + 30)
     sample = np.unique(np.concatenate([rng.integers(0, got.size, 20_000), [0, got.size - 1],
-                                       np.arange((1 << 21) - 50, (1 << 21) + 50)]))
+                                       np.arange((1 << 21) - 50, (1 << 21) + 50), np.arange((1 << 22) - 50, (1 << 22) + 50)]))
     want = oracle_mod.Oracle(w["model"], c).eval(_sub(p, sample))
-    _equal(got[sample], want, "every option, two chunks, workload %d" % idx)
+    _equal(got[sample], want, "every option, three chunks, workload %d" % idx)

@@ -130,7 +130,9 @@ def test_capacity_edges(torch, B, oracle_mod, workloads):
             assert got == (times[i] if delta == 0 else MAXU), (k, delta)
 
 
-def test_memory_empty_and_oversized_calls(torch, B, workloads):
+def test_memory_and_stages_empty_and_chunked_calls(torch, B, workloads):
+    """n = 0 is a no-op; a call over more than 2^21 plans is worked in chunks: the plans around
+    the chunk seam and a sample of the rest equal a small call over the same plans."""
     import ctypes as C
     w = _workload(workloads, 2)
     sim = B.Sim(w["model"], w["cluster"])
@@ -140,5 +142,22 @@ def test_memory_empty_and_oversized_calls(torch, B, workloads):
     out = torch.empty((8, 4, 16), dtype=torch.int64, device="cuda")
     L = B.lib()
     assert L.sim_eval_memory(sim.h, C.byref(ps), 0, out.data_ptr(), B._stream(None)) == B.SIM_OK
-    ps.stride = 1 << 22                      # stride >= n holds; n above 2^21 is rejected
-    assert L.sim_eval_memory(sim.h, C.byref(ps), (1 << 21) + 1, out.data_ptr(), B._stream(None)) == B.SIM_EINVAL
+    n = (1 << 21) + 3001
+    say("case: memory and stage records of %d plans (one call, two chunks)" % n)
+    p = workloads.plans(w, 0, n)
+    dp = B.device_plans(p)
+    mem = sim.eval_memory(dp)
+    st, cl = sim.eval_stages(dp)
+    rng = np.random.default_rng(7)
+    pick = np.unique(np.concatenate([np.arange((1 << 21) - 64, (1 << 21) + 64), rng.integers(0, n, 256),
+                                     np.arange(n - 8, n)]))
+    sub = {k: np.ascontiguousarray(v[..., pick]) for k, v in p.items()}
+    ds = B.device_plans(sub)
+    m2 = sim.eval_memory(ds)
+    s2, c2 = sim.eval_stages(ds)
+    idx = torch.as_tensor(pick, device="cuda")
+    assert torch.equal(mem[idx], m2)
+    assert torch.equal(cl[idx], c2)
+    assert bool((c2[:, 0] != 0).any())
+    # both outputs start at zero, so untouched entries compare too
+    assert torch.equal(st[idx], s2)

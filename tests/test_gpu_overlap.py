@@ -75,12 +75,12 @@ def test_overlap_stage_records(torch, B, oracle_mod, workloads, idx):
 
 
 def test_overlap_with_device_memory_and_chunks(torch, B, oracle_mod, workloads):
-    """Overlap plans over more than one 2M-plan chunk, with device memory checked."""
+    """Overlap plans over more than two 2M-plan chunks, with device memory checked."""
     w = workloads.with_memory(workloads.workload(2), [48, 80, 32])
-    n = (1 << 21) + 20_011
+    n = (1 << 22) + 20_011
     p = workloads.plans(w, 0, n)
     p["hdr"] |= OVERLAP
-    say("case: overlap with memory, %d plans in two chunks" % n)
+    say("case: overlap with memory, %d plans in three chunks" % n)
     got = B.times_u64(B.Sim(w["model"], w["cluster"]).eval_plans(B.device_plans(p)))
     want = oracle_mod.Oracle(w["model"], w["cluster"]).eval(p)
     _equal(got, want, "overlap with memory")
