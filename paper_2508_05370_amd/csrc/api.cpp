@@ -19,8 +19,10 @@ hipError_t launch_plan_syncs(const Tab& t, const PackedPlan* packed, const uint4
                              int64_t n, uint64_t* hdp, hipStream_t s);
 hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint4* pcut, const uint32_t* meta, int64_t n,
                          uint64_t* out_stage, hipStream_t s);
-hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* sstart, hipStream_t s);
-hipError_t launch_scatter(const uint16_t* keys, uint32_t nslots, uint32_t* cursor, uint32_t* ids, hipStream_t s);
+hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* sstart, uint32_t* sbase, bool grouped,
+                       hipStream_t s);
+hipError_t launch_scatter(const uint16_t* keys, uint32_t nslots, uint32_t* cursor, const uint32_t* sbase, bool grouped,
+                          uint32_t* ids, hipStream_t s);
 hipError_t launch_first(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s);
 hipError_t launch_group(const Tab& t, const EvalArgs& a, uint32_t max_tasks, int g, hipStream_t s);
 hipError_t launch_variant(const Tab& t, const EvalArgs& a, int g, hipStream_t s);
@@ -288,8 +290,10 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
     if (e == hipSuccess) e = launch_prep(c->tab, p, cn, out + off, W.packed, W.pcut, W.meta, W.hist, W.keys, s);
     if (t1) end_event(c, 1, s, &ev);
     if (e == hipSuccess && het) e = launch_plan_syncs(c->tab, W.packed, W.pcut, W.meta, cn, W.hdp, s);
-    if (e == hipSuccess) e = launch_scan(W.hist, W.cursor, W.sstart, s);
-    if (e == hipSuccess) e = launch_scatter(W.keys, (uint32_t)(cn * 4), W.cursor, W.ids, s);
+    // shared-layout calls sort long plans by plan, leaving padding lanes
+    if (e == hipSuccess && !het) e = launch_fill32(W.ids, (uint32_t)id_words(cn), kNoSlot, s);
+    if (e == hipSuccess) e = launch_scan(W.hist, W.cursor, W.sstart, W.sbase, !het, s);
+    if (e == hipSuccess) e = launch_scatter(W.keys, (uint32_t)(cn * 4), W.cursor, W.sbase, !het, W.ids, s);
     const EvalArgs a = {W.packed, W.pcut, W.hdp, W.meta, W.ids, W.sstart, out + off, W.ctr, W.deferred,
                         c->timing ? c->skipped_ops : nullptr, c->dtab};
     EventPair e0;
@@ -359,8 +363,9 @@ extern "C" int sim_eval_plans_noalloc(sim_ctx* c, const sim_plans* plans, int64_
   hipError_t e = launch_fill32(W.hist, kCounters, 0, s);
   if (e == hipSuccess) e = launch_prep(c->tab, *plans, n, out, W.packed, W.pcut, W.meta, W.hist, W.keys, s);
   if (e == hipSuccess && het) e = launch_plan_syncs(c->tab, W.packed, W.pcut, W.meta, n, W.hdp, s);
-  if (e == hipSuccess) e = launch_scan(W.hist, W.cursor, W.sstart, s);
-  if (e == hipSuccess) e = launch_scatter(W.keys, (uint32_t)(n * 4), W.cursor, W.ids, s);
+  if (e == hipSuccess && !het) e = launch_fill32(W.ids, (uint32_t)id_words(n), kNoSlot, s);
+  if (e == hipSuccess) e = launch_scan(W.hist, W.cursor, W.sstart, W.sbase, !het, s);
+  if (e == hipSuccess) e = launch_scatter(W.keys, (uint32_t)(n * 4), W.cursor, W.sbase, !het, W.ids, s);
   const EvalArgs a = {W.packed, W.pcut, W.hdp, W.meta, W.ids, W.sstart, out, W.ctr, W.deferred,
                       c->timing ? c->skipped_ops : nullptr, c->dtab};
   if (e == hipSuccess) e = launch_first(c->tab, a, (uint32_t)(n * 4), s);

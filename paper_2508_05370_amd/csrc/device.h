@@ -485,7 +485,7 @@ __global__ void __launch_bounds__(256) k_prep(Tab t, sim_plans pl, int64_t n, ui
         for (int c = 0; c < 4; ++c) pcut[4 * i + c] = make_uint4(r.cw[c][0], r.cw[c][1], r.cw[c][2], r.cw[c][3]);
       }
     }
-    uint32_t m[4], key[4];
+    uint32_t m[4], key[4], Mmax = 0;
 #pragma unroll
     for (uint32_t c = 0; c < 4; ++c) {
       m[c] = 0;
@@ -493,6 +493,16 @@ __global__ void __launch_bounds__(256) k_prep(Tab t, sim_plans pl, int64_t n, ui
       if (ok && c < G) {
         const uint32_t reps = r.cls[c] & 0xffff, M = ((r.cls[c] >> 16) + reps - 1) / reps;
         m[c] = r.S[c] | (G << 5) | (M << 8) | ((r.v - 1) << 24);
+        Mmax = M > Mmax ? M : Mmax;
+      }
+    }
+    // plans sorted by plan (their class 0 carries the key, ranked by the
+    // longest class), the others by pipeline
+    const bool by_plan = !kHet && ok && r.v == 1;
+#pragma unroll
+    for (uint32_t c = 0; c < 4; ++c) {
+      if (ok && c < G && (!by_plan || c == 0)) {
+        const uint32_t M = by_plan ? Mmax : m[c] >> 8 & 0xffff;
         key[c] = r.v > 1 ? il_key(r.S[c], r.v, M) : bucket_key(r.S[c], G, M);
         if (hist) atomicAdd(&lh[key[c]], 1u);
       }
@@ -1623,8 +1633,44 @@ struct EvalBufs {
 // stay aperiodic).  With a context that enables two-level collectives, whose
 // sync code the first pass lacks, it sends every other shared-layout
 // pipeline to the deferred lists.
+// DP tail of a plan-sorted pipeline (first pass, shared layout, G > 1 classes
+// on G adjacent lanes): the lane of class c costs the syncs of stages c,
+// c + G, ... (each the same for every class of the plan) into its plan's row
+// of the wavefront's LDS exchange area, then every lane of the plan reads
+// the whole row.  Every lane of the plan takes part, deferred ones included
+// (the syncs do not depend on the recurrence).
+template <int S, int kMode>
+__device__ __forceinline__ double grouped_tail(const Tab& t, const Hot<kMode>& h, const Plan& p, const double (&last)[S],
+                                               double* xw) {
+  const uint32_t G = p.G, lane = threadIdx.x & 63u;
+  double* x = xw + (lane / G) * xchg_row(S);
+  const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> p.epl);
+  for (uint32_t s = p.c; s < (uint32_t)S; s += G) {
+    const uint32_t lo = s ? cut_at(p, s - 1) : 0;
+    x[s] = (double)stage_dp<kMode, false>(t, h, p, s, cut_at(p, s) - lo, rp, rpe);
+  }
+  // the rows are written and read by the lanes of one wavefront, whose LDS
+  // accesses complete in order; the fences keep the compiler from moving
+  // the reads above the writes of the other lanes
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  double T = 0;
+#pragma unroll
+  for (int s = 0; s < S; ++s) {
+    const double v = last[s] + x[s];
+    T = v > T ? v : T;
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  return T;
+}
+
 template <int S, bool kFull, int kMode, bool kHet, bool kOvl = false, bool kZb = false>
-__device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot) {
+__device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot,
+                                         double* xw = nullptr) {
+  // plan-sorted pipelines: this pass, shared layout, no variant
+  constexpr bool kGrouped = !kFull && !kHet && !kOvl && !kZb;
   typename std::conditional<kZb, ZbSink<S>, RegSink<S>>::type r;
   uint32_t M;
   {
@@ -1653,9 +1699,15 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
   // shuffle is opaque to the compiler, which would otherwise reuse the
   // first load
   const uint32_t slot2 = __shfl(slot, (int)(threadIdx.x & 63u));
-  const double T = done ? dp_tail<S, kMode, kHet, kOvl, kFull || kOvl || kZb>(t, h, load_plan<kHet>(e.packed, e.pcut, slot2), last,
-                                                         kHet ? e.hdp + (size_t)slot2 * kMaxStages : nullptr)
-                        : 0;
+  double T;
+  const Plan p2 = load_plan<kHet>(e.packed, e.pcut, slot2);
+  if (kGrouped && p2.G > 1) {   // G is the same in the whole wavefront
+    T = grouped_tail<S, kMode>(t, h, p2, last, xw);
+  } else {
+    T = done ? dp_tail<S, kMode, kHet, kOvl, kFull || kOvl || kZb>(t, h, p2, last,
+                                                                   kHet ? e.hdp + (size_t)slot2 * kMaxStages : nullptr)
+             : 0;
+  }
   if (!done) {
     e.deferred[e.sstart[kMaxStages - S] + atomicAdd(&e.ctr[1 + kMaxStages - S], 1u)] = slot;
     return;
@@ -1946,10 +1998,15 @@ __global__ void __launch_bounds__(kEvalThreads) k_eval(Tab t, EvalBufs e) {
   fill_lds<kMode>(t, lds);
   const Hot<kMode> h(t, lds);
   const uint32_t stride = gridDim.x * kEvalThreads;
+  // the wavefront's row of the plan-sorted groups' LDS exchange area
+  double* xw = nullptr;
+  if constexpr (!kHet)
+    xw = (double*)((char*)lds + (kMode < 2 ? t.lds_bytes : 0)) + (threadIdx.x >> 6) * (kXchgPlans * kTop);
   for (uint32_t base = lo + blockIdx.x * kEvalThreads + (threadIdx.x & ~63u); base < hi; base += stride) {
     const uint32_t pos = base + (threadIdx.x & 63u);
     bool pending = pos < hi;
     const uint32_t slot = pending ? e.ids[pos] : 0;
+    pending = pending && slot != kNoSlot;   // padding lanes of plan-sorted groups
     const uint32_t S = !pending ? 0 : kHet ? e.meta[slot] & 31 : ((e.packed[slot >> 2].hdr >> 4) & 15) + 1;
     // one pass per distinct stage count present in the wavefront (usually one)
     while (true) {
@@ -1957,10 +2014,10 @@ __global__ void __launch_bounds__(kEvalThreads) k_eval(Tab t, EvalBufs e) {
       if (!live) break;
       const uint32_t S0 = __builtin_amdgcn_readfirstlane(__shfl(S, __ffsll((unsigned long long)live) - 1));
       if (pending && S == S0) {
-        if (S0 == kTop) eval_one<kTop, false, kMode, kHet>(t, h, e, slot);
-        else if (S0 == kTop - 1) eval_one<kTop - 1, false, kMode, kHet>(t, h, e, slot);
-        else if (S0 == kTop - 2) eval_one<kTop - 2, false, kMode, kHet>(t, h, e, slot);
-        else eval_one<kTop - 3, false, kMode, kHet>(t, h, e, slot);
+        if (S0 == kTop) eval_one<kTop, false, kMode, kHet>(t, h, e, slot, xw);
+        else if (S0 == kTop - 1) eval_one<kTop - 1, false, kMode, kHet>(t, h, e, slot, xw);
+        else if (S0 == kTop - 2) eval_one<kTop - 2, false, kMode, kHet>(t, h, e, slot, xw);
+        else eval_one<kTop - 3, false, kMode, kHet>(t, h, e, slot, xw);
         pending = false;
       }
     }

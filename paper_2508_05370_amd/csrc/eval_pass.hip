@@ -19,7 +19,8 @@ hipError_t launch_group_v(const Tab& t, const EvalArgs& a, uint32_t max_tasks, i
   const EvalBufs e = eval_bufs(a);
   const int nb = pass_blocks(max_tasks, kEvalThreads);
   const uint32_t need = nb > 0 ? (uint32_t)nb : 1, grid = 4 * t.grid_eval[g] < need ? 4 * t.grid_eval[g] : need;
-  const size_t lds = kMode < 2 ? t.lds_bytes : 0;
+  // the shared layout's plan-sorted groups add their plans' DP exchange area
+  const size_t lds = (kMode < 2 ? t.lds_bytes : 0) + (!kHet ? xchg_bytes(g) : 0);
   if (g == 0) k_eval<0, kMode, kHet><<<grid, kEvalThreads, lds, s>>>(t, e);
   else if (g == 1) k_eval<1, kMode, kHet><<<grid, kEvalThreads, lds, s>>>(t, e);
   else if (g == 2) k_eval<2, kMode, kHet><<<grid, kEvalThreads, lds, s>>>(t, e);
@@ -37,7 +38,7 @@ hipError_t occupancy_first_v(int nb[4], size_t lds) {
   const void* k[4] = {(const void*)k_eval<0, kMode, false>, (const void*)k_eval<1, kMode, false>,
                       (const void*)k_eval<2, kMode, false>, (const void*)k_eval<3, kMode, false>};
   for (int i = 0; i < 4; ++i) {
-    hipError_t r = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb[i], k[i], kEvalThreads, lds);
+    hipError_t r = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb[i], k[i], kEvalThreads, lds + xchg_bytes(i));
     if (r != hipSuccess) return r;
   }
   return hipSuccess;
@@ -68,7 +69,7 @@ hipError_t occupancy_variant_v(int nb[4], size_t lds) {
   const void* k[4] = {(const void*)k_variant<0, kMode>, (const void*)k_variant<1, kMode>,
                       (const void*)k_variant<2, kMode>, (const void*)k_variant<3, kMode>};
   for (int i = 0; i < 4; ++i) {
-    hipError_t r = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb[i], k[i], kEvalThreads, lds);
+    hipError_t r = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb[i], k[i], kEvalThreads, lds + xchg_bytes(i));
     if (r != hipSuccess) return r;
   }
   return hipSuccess;

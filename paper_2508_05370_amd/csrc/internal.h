@@ -25,6 +25,22 @@ static_assert(kIlGroups * kIlBucketsQ <= 1024, "interleaved buckets");
 // sstart: [16 - S] first sorted id of the S-stage pipelines, [16 + q] first
 // id of interleaved group q, [16 + kIlGroups] the total
 constexpr int kSstartWords = kMaxStages + kIlGroups + 1;
+// Plans of the shared layout with one model chunk per device are sorted by
+// plan: the G pipelines of a plan take G adjacent lanes of one wavefront,
+// every wavefront holds plans of one stage count and one class count (64 / G
+// plans of them, 21 when G = 3), and each (stages, classes) bucket starts on
+// a wavefront boundary.  kGroupPad bounds the padding lanes this adds to a
+// chunk; padding lanes hold kNoSlot.
+constexpr uint32_t kSuperBuckets = kMaxStages * kMaxClasses;
+constexpr uint32_t kGroupPad = 64 * kSuperBuckets;
+constexpr uint32_t kNoSlot = 0xffffffffu;
+__host__ __device__ constexpr uint32_t plans_per_wave(uint32_t G) { return G == 3 ? 21 : 64 / G; }
+// LDS of the first pass over plan-sorted pipelines: per wavefront, a row of
+// DP syncs for each of up to 32 plans (one per stage of the kernel's largest
+// stage count), exchanged between the lanes of each plan
+constexpr uint32_t kXchgPlans = 32;
+__host__ __device__ constexpr uint32_t xchg_row(uint32_t S) { return (S + 3) / 4 * 4; }
+__host__ __device__ constexpr uint32_t xchg_bytes(int group) { return 4 * kXchgPlans * (kMaxStages - 4 * group) * 8; }
 
 // A validated plan packed into 80 contiguous bytes, so that the pipelines of
 // one plan gather it with five 16-byte loads.
@@ -144,17 +160,20 @@ struct Work {
   PackedPlan* packed;
   uint4* pcut;
   uint64_t* hdp;
-  uint32_t *meta, *ids, *deferred, *hist, *ctr, *cursor, *sstart;
+  uint32_t *meta, *ids, *deferred, *hist, *ctr, *cursor, *sstart, *sbase;
   uint16_t* keys;
 };
+// sorted ids (and deferred lists) of a chunk: four lanes per plan at most,
+// plus the padding of the plan-sorted buckets
+constexpr size_t id_words(int64_t ch) { return (size_t)ch * 4 + kGroupPad; }
 constexpr size_t cut_rows_bytes(int64_t ch, bool het) { return het ? align256((size_t)ch * 64) : 0; }
 constexpr size_t het_sync_bytes(int64_t ch, bool het) {
   return het ? align256((size_t)ch * kMaxClasses * kMaxStages * 8) : 0;
 }
 constexpr size_t work_bytes(int64_t ch, bool het) {
-  return align256((size_t)ch * sizeof(PackedPlan)) + 3 * align256((size_t)ch * 4 * 4) +
+  return align256((size_t)ch * sizeof(PackedPlan)) + align256((size_t)ch * 4 * 4) + 2 * align256(id_words(ch) * 4) +
          align256(kCounters * 4 + (size_t)ch * 4 * 4) + align256(kBuckets * 4) + align256(kSstartWords * 4) +
-         align256((size_t)ch * 4 * 2) +
+         align256(kSuperBuckets * 4) + align256((size_t)ch * 4 * 2) +
          cut_rows_bytes(ch, het) + het_sync_bytes(ch, het);
 }
 inline Work carve(void* base, int64_t ch, bool het) {
@@ -164,11 +183,12 @@ inline Work carve(void* base, int64_t ch, bool het) {
   w.hdp = het ? (uint64_t*)p : nullptr; p += het_sync_bytes(ch, het);
   w.packed = (PackedPlan*)p; p += align256((size_t)ch * sizeof(PackedPlan));
   w.meta = (uint32_t*)p; p += align256((size_t)ch * 16);
-  w.ids = (uint32_t*)p; p += align256((size_t)ch * 16);
-  w.deferred = (uint32_t*)p; p += align256((size_t)ch * 16);
+  w.ids = (uint32_t*)p; p += align256(id_words(ch) * 4);
+  w.deferred = (uint32_t*)p; p += align256(id_words(ch) * 4);
   w.hist = (uint32_t*)p; w.ctr = w.hist + kBuckets; p += align256(kCounters * 4 + (size_t)ch * 16);
   w.cursor = (uint32_t*)p; p += align256(kBuckets * 4);
   w.sstart = (uint32_t*)p; p += align256(kSstartWords * 4);
+  w.sbase = (uint32_t*)p; p += align256(kSuperBuckets * 4);
   w.keys = (uint16_t*)p;
   return w;
 }

@@ -41,16 +41,28 @@ __global__ void k_fill32(uint32_t* p, uint32_t n, uint32_t v) {
   for (uint32_t j = blockIdx.x * blockDim.x + threadIdx.x; j < n; j += gridDim.x * blockDim.x) p[j] = v;
 }
 
-// exclusive scan of the bucket counts; sstart[16 - S] = first id of the
-// S-stage pipelines, sstart[16 + q] = first id of interleaved group q,
-// sstart[16 + kIlGroups] = number of pipelines.  Thread tid takes plain
-// buckets [8 tid, 8 tid + 8) and interleaved bucket kPlainBuckets + tid; one
-// scan of (plain, interleaved) pairs, the interleaved ones after all plain.
+// Bucket offsets.  Plain buckets come in 64 groups of kBucketsM (one group
+// per (stages, classes), more stages first, then more classes), the
+// interleaved buckets after them.  With `grouped` (a shared-layout call),
+// the plain groups count plans, not pipelines: a group of G classes then
+// takes ceil(plans / plans_per_wave(G)) whole wavefronts of lanes, its
+// buckets' cursors count plans from the group's start, and sbase[group] is
+// the group's first lane.  Otherwise (per-class layout) they count pipelines
+// and their cursors are lanes.  sstart[16 - S] = first lane of
+// the S-stage pipelines, sstart[16 + q] = first lane of interleaved group q,
+// sstart[16 + kIlGroups] = all lanes.  Thread tid takes plain buckets
+// [8 tid, 8 tid + 8) (sixteen threads per group) and interleaved bucket
+// kPlainBuckets + tid; one block scan of (plain, interleaved) pairs, then one
+// of the 64 groups' lane counts.
 __global__ void __launch_bounds__(1024) k_scan(const uint32_t* __restrict__ hist, uint32_t* __restrict__ cursor,
-                                               uint32_t* __restrict__ sstart) {
+                                               uint32_t* __restrict__ sstart, uint32_t* __restrict__ sbase,
+                                               uint32_t grouped) {
   constexpr int kPer = kPlainBuckets / 1024;
+  constexpr int kThreadsPerGroup = kBucketsM / kPer;
   static_assert(kPlainBuckets % 1024 == 0 && kBuckets - kPlainBuckets == 1024, "bucket count");
+  static_assert(kThreadsPerGroup * kSuperBuckets == 1024, "sixteen threads per (stages, classes) group");
   __shared__ uint2 part[1024];
+  __shared__ uint32_t lanes[kSuperBuckets + 1];
   uint32_t v[kPer], sum = 0;
   const uint32_t tid = threadIdx.x;
 #pragma unroll
@@ -65,20 +77,48 @@ __global__ void __launch_bounds__(1024) k_scan(const uint32_t* __restrict__ hist
     part[tid].y += x.y;
     __syncthreads();
   }
-  uint32_t run = part[tid].x - sum;
-  // pipelines of S stages start at bucket (16 - S) * kPlainBuckets / 16
-  if ((tid * kPer) % (kPlainBuckets / kMaxStages) == 0) sstart[(tid * kPer) / (kPlainBuckets / kMaxStages)] = run;
+  // the group of this thread's buckets, its entries before this thread's
+  const uint32_t grp = tid / kThreadsPerGroup, g0 = grp * kThreadsPerGroup;
+  const uint32_t before_grp = g0 ? part[g0 - 1].x : 0;
+  const bool by_plan = grouped != 0;
+  if (tid < kSuperBuckets) {
+    // lanes of group tid
+    const uint32_t a = tid * kThreadsPerGroup;
+    const uint32_t n = part[a + kThreadsPerGroup - 1].x - (a ? part[a - 1].x : 0);
+    const uint32_t pw = plans_per_wave(kMaxClasses - tid % kMaxClasses);
+    lanes[tid] = grouped ? (n + pw - 1) / pw * 64u : n;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    uint32_t run = 0;
+    for (uint32_t q = 0; q < kSuperBuckets; ++q) {
+      const uint32_t x = lanes[q];
+      lanes[q] = run;
+      run += x;
+    }
+    lanes[kSuperBuckets] = run;
+  }
+  __syncthreads();
+  if (tid < kSuperBuckets) sbase[tid] = lanes[tid];
+  // pipelines of S stages start at group (16 - S) * 4 (four classes first)
+  if (tid < kMaxStages) sstart[tid] = lanes[tid * kMaxClasses];
+  uint32_t run = part[tid].x - sum - before_grp;
+  if (!by_plan) run += lanes[grp];
 #pragma unroll
   for (int j = 0; j < kPer; ++j) { cursor[tid * kPer + j] = run; run += v[j]; }
-  const uint32_t irun = part[1023].x + part[tid].y - vi;
+  const uint32_t irun = lanes[kSuperBuckets] + part[tid].y - vi;
   if (tid % kIlBucketsQ == 0 && tid / kIlBucketsQ <= (uint32_t)kIlGroups) sstart[kMaxStages + tid / kIlBucketsQ] = irun;
   cursor[kPlainBuckets + tid] = irun;
 }
 
-// place every pipeline id at its bucket's next free position
+// Place every pipeline id at its bucket's next free lane.  A plain key of a
+// grouped call sits on the plan's class-0 slot and stands for the whole plan: the plan's rank r in its
+// group puts its G pipeline ids on lanes sbase[group] + 64 (r / P) + G (r % P)
+// onward (P = plans_per_wave(G)); the lanes left over stay kNoSlot.
 constexpr int kScatterPer = 64;
 __global__ void __launch_bounds__(256) k_scatter(const uint16_t* __restrict__ keys, uint32_t nslots,
-                                                 uint32_t* __restrict__ cursor, uint32_t* __restrict__ ids) {
+                                                 uint32_t* __restrict__ cursor, const uint32_t* __restrict__ sbase,
+                                                 uint32_t grouped, uint32_t* __restrict__ ids) {
   constexpr int kPer = kScatterPer;
   __shared__ uint32_t lc[kBuckets];
   for (uint32_t j = threadIdx.x; j < kBuckets; j += blockDim.x) lc[j] = 0;
@@ -103,8 +143,17 @@ __global__ void __launch_bounds__(256) k_scatter(const uint16_t* __restrict__ ke
     if (lc[j]) lc[j] = atomicAdd(&cursor[j], lc[j]);
   __syncthreads();
 #pragma unroll
-  for (int j = 0; j < kPer; ++j)
-    if (key[j] != 0xffffffffu) ids[lc[key[j]] + rank[j]] = first + j * blockDim.x;
+  for (int j = 0; j < kPer; ++j) {
+    if (key[j] == 0xffffffffu) continue;
+    const uint32_t slot = first + j * blockDim.x, pos = lc[key[j]] + rank[j];
+    const uint32_t grp = key[j] / kBucketsM, G = kMaxClasses - grp % kMaxClasses;
+    if (grouped && key[j] < kPlainBuckets) {
+      const uint32_t pw = plans_per_wave(G), lane = sbase[grp] + pos / pw * 64u + pos % pw * G;
+      for (uint32_t c = 0; c < G; ++c) ids[lane + c] = slot + c;
+    } else {
+      ids[pos] = slot;
+    }
+  }
 }
 
 // ---------------------------------------------------------------- argmin
@@ -218,12 +267,14 @@ hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint4* pc
   else k_stages<false><<<blocks_for(n * 4, 256), 256, 0, s>>>(t, packed, pcut, meta, n, out_stage);
   return hipGetLastError();
 }
-hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* sstart, hipStream_t s) {
-  k_scan<<<1, 1024, 0, s>>>(hist, cursor, sstart);
+hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* sstart, uint32_t* sbase, bool grouped,
+                       hipStream_t s) {
+  k_scan<<<1, 1024, 0, s>>>(hist, cursor, sstart, sbase, grouped ? 1u : 0u);
   return hipGetLastError();
 }
-hipError_t launch_scatter(const uint16_t* keys, uint32_t nslots, uint32_t* cursor, uint32_t* ids, hipStream_t s) {
-  k_scatter<<<blocks_for(nslots, 256 * kScatterPer), 256, 0, s>>>(keys, nslots, cursor, ids);
+hipError_t launch_scatter(const uint16_t* keys, uint32_t nslots, uint32_t* cursor, const uint32_t* sbase, bool grouped,
+                          uint32_t* ids, hipStream_t s) {
+  k_scatter<<<blocks_for(nslots, 256 * kScatterPer), 256, 0, s>>>(keys, nslots, cursor, sbase, grouped ? 1u : 0u, ids);
   return hipGetLastError();
 }
 // ---------------------------------------------------------------- node-rate probe
