@@ -1393,7 +1393,7 @@ __device__ __forceinline__ uint64_t vmax(uint64_t a, uint64_t b) { return a > b 
 // micro-batches.  A wave waits at most kPeriodicBudget steady iterations for
 // its lanes; a lane still aperiodic by then is deferred to a full-loop pass,
 // so one aperiodic schedule does not hold 63 periodic ones.
-constexpr int kPeriodicBudget = 32;
+constexpr int kPeriodicBudget = 48;
 
 template <int S, typename V>
 __device__ __forceinline__ void steady_iter(const V (&f)[S], const V (&b)[S], const V (&c)[S], V (&out_f)[S],
@@ -1673,8 +1673,8 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
   constexpr bool kGrouped = !kFull && !kHet && !kOvl && !kZb;
   typename std::conditional<kZb, ZbSink<S>, RegSink<S>>::type r;
   uint32_t M;
+  const Plan p = load_plan<kHet>(e.packed, e.pcut, slot);
   {
-    const Plan p = load_plan<kHet>(e.packed, e.pcut, slot);
     if (!kFull && !kHet && !kOvl && !kZb) {
       if (p.overlap | p.zb) {
         e.deferred[e.sstart[kMaxStages - S + 1] - 1 - atomicAdd(&e.ctr[kVariantCtr + kMaxStages - S], 1u)] = slot;
@@ -1694,13 +1694,15 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
   if constexpr (kZb) pipe_zb<S, double, true>(r.f, r.bi, r.w, r.c, M, skipped, last);
   else if constexpr (kOvl) done = pipe<S, double, true, true>(r.f, r.b, r.c, M, skipped, last);
   else done = pipe<S, double, !kFull>(r.f, r.b, r.c, M, skipped, last);
-  // the DP tail reads the plan again (an L2 hit) rather than keeping it in
-  // registers through the recurrence; the lane's own slot passed through a
-  // shuffle is opaque to the compiler, which would otherwise reuse the
-  // first load
-  const uint32_t slot2 = __shfl(slot, (int)(threadIdx.x & 63u));
+  // With up to kKeepPlanS stages the plan stays in registers through the
+  // recurrence (whose state is small); longer pipelines read it again for
+  // the DP tail (an L2 hit) rather than hold it: the lane's own slot passed
+  // through a shuffle is opaque to the compiler, which would otherwise reuse
+  // the first load
+  constexpr int kKeepPlanS = 8;
+  const uint32_t slot2 = S <= kKeepPlanS ? slot : __shfl(slot, (int)(threadIdx.x & 63u));
   double T;
-  const Plan p2 = load_plan<kHet>(e.packed, e.pcut, slot2);
+  const Plan p2 = S <= kKeepPlanS ? p : load_plan<kHet>(e.packed, e.pcut, slot2);
   if (kGrouped && p2.G > 1) {   // G is the same in the whole wavefront
     T = grouped_tail<S, kMode>(t, h, p2, last, xw);
   } else {
