@@ -160,21 +160,27 @@ typedef struct {
  *   types[c*stride+i]   u64, device type of stage s of class c in bits [4s, 4s+4)
  * Entries past PP stages or past the class count are ignored.
  *
- * Per-class layout (chdr != NULL): device groups may differ in TP degree and
- * in how many layers each stage takes (Sec. 3 "Non-uniform workload
- * partitioning": TP=1 next to TP=3 groups, more layers on faster devices).
- * Then hdr's TP and PP fields must be 0, `cut` is not read (may be NULL),
- * and
+ * Per-class layout (chdr != NULL): device groups may differ in TP degree,
+ * in how many layers each stage takes and in micro-batch size (Sec. 3
+ * "Non-uniform workload partitioning": TP=1 next to TP=3 groups, more
+ * layers on faster devices, non-uniform batches).  Then hdr's TP, PP and
+ * micro-batch size fields must be 0, `cut` is not read (may be NULL), and
  *   chdr[i]                 byte c (class c): bits 0-1 log2 TP, 2-5 PP-1,
- *                           6-7 zero
+ *                           6-7 micro-batch size index (into mbs[])
  *   ccut[(c*16+s)*stride+i] u8, last layer (exclusive) of stage s of class
  *                           c: 1 <= ... < ccut[(c*16+PP_c-1)*stride+i] = L
- * The gradient sync of the layers between two consecutive cuts of any
- * class runs as one ring over every replica on the coarsest TP layout among
- * the classes, after the classes with finer shards gather it inside their
- * TP groups (resharding, Sec. 3 "Resharding", Sec. 4.1 [C2]); a stage's
- * sync waits for its own backward passes and those of the other classes'
- * stages that hold the same layers.  The rules above apply per class.
+ * The classes' micro-batches times their micro-batch sizes sum to the
+ * global batch.  The gradient sync of the layers between two consecutive
+ * cuts of any class runs as one ring over every replica on the coarsest TP
+ * layout among the classes.  Before it each class reshards its gradients
+ * (Sec. 3 "Resharding", both conditions; Sec. 4.1 [C2]): when the classes
+ * holding those layers differ in micro-batch size, each weights its shard
+ * by its share of the batch (one elementwise pass: a multiply per element,
+ * the fp32 shard read and written at its devices' HBM rate), and a class
+ * with a finer shard gathers the coarse one inside its TP groups; the
+ * classes do this at once and the slowest counts.  A stage's sync waits for
+ * its own backward passes and those of the other classes' stages that hold
+ * the same layers.  The rules above apply per class.
  * A plan that breaks any rule (ranges, divisibility of heads/widths by TP,
  * TP within a node, EP dividing every class's replicas, capacity of every
  * device pool, micro-batches summing to the global batch, at least one

@@ -25,10 +25,10 @@
  *   - parallelism exists to fit the model within device memory (Sec. 2),
  *     and device types differ in capacity (Sec. 3 example, Table 5: A100
  *     40 GB, H100 80 GB): a plan that overflows a device is infeasible;
- *   - device groups may differ in TP degree and layer split (Sec. 3); then
- *     the gradient sync is preceded by resharding (Sec. 3 "Resharding",
- *     Sec. 4.1 [C2]).
- * Where the paper is silent the reading used is named R1..R43 in comments;
+ *   - device groups may differ in TP degree, layer split and micro-batch
+ *     size (Sec. 3); then the gradient sync is preceded by resharding
+ *     (Sec. 3 "Resharding", both of its conditions; Sec. 4.1 [C2]).
+ * Where the paper is silent the reading used is named R1..R51 in comments;
  * the design notes of the repository list every reading.
  *
  * Parity notes: the recurrence, the collective formulas, the interconnect
@@ -49,7 +49,12 @@
  * per-virtual-stage costs of a plain plan over the same cuts and the ring
  * closed form of its per-device sync; its in-flight activation count (each
  * pass counted at the device's largest chunk) is a bound of this reading,
- * pinned only by its own differences.
+ * pinned only by its own differences.  Per-class micro-batch sizes and the
+ * gradient weighting they trigger (R51) are pinned by Sec. 3's worked example
+ * composed by hand from pinned pieces; the weighting's cost itself is a
+ * reading with no printed value: parity unpinned beyond that.  Whole plans of
+ * the exhaustive 8-device workload are checked against a second, independent
+ * evaluator (brute_plan.py).
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -390,6 +395,7 @@ static void pipeline(uint64_t S, uint64_t M, const uint64_t* f, const uint64_t* 
  * devices, TP degrees that follow each device group's size; R35). */
 typedef struct {
   uint64_t ep, G, zero, mi;
+  uint64_t mi_c[OR_MAXG];  /* micro-batch size index of each class (R51; the plan's mi in the shared layout) */
   uint64_t overlap;      /* 1: gradient sync overlapped with the last backward pass (R38) */
   uint64_t v;            /* model chunks per device: 1 = plain 1F1B, 2..4 interleaved (R41) */
   uint64_t zb;           /* 1: backward split into input and weight gradients, zero-bubble order (R44) */
@@ -449,21 +455,23 @@ static int decode_rules(const or_ctx* x, const or_planes* q, int64_t i, or_plan*
   p->mi = (hdr >> 11) & 3;
   if (p->mi >= m->n_mbs) return 0;                           /* V8 */
   if (q->chdr) {
-    if (hdr & 0xf3) return 0;                                /* V10 the header's TP and PP are unused (0) */
+    if (hdr & 0x18f3) return 0;                              /* V10 the header's TP, PP and micro-batch size are unused (0) */
     if (p->overlap) return 0;                                /* V11 overlap needs the shared layout */
     if (p->v > 1) return 0;                                  /* V12 interleaving needs the shared layout */
     if (p->zb) return 0;                                     /* V13 so does the zero-bubble order */
     uint32_t w = q->chdr[i];
     for (uint64_t g = 0; g < p->G; ++g) {
       uint32_t bt = (w >> (8 * g)) & 0xff;
-      if (bt >> 6) return 0;                                 /* V10 reserved class bits */
       p->tp[g] = 1ull << (bt & 3);
       p->S[g] = ((bt >> 2) & 15) + 1;
+      p->mi_c[g] = bt >> 6;                                  /* R51 the class's own micro-batch size */
+      if (p->mi_c[g] >= m->n_mbs) return 0;                  /* V8 */
     }
   } else {
     for (uint64_t g = 0; g < p->G; ++g) {
       p->tp[g] = 1ull << (hdr & 3);
       p->S[g] = ((hdr >> 4) & 15) + 1;
+      p->mi_c[g] = p->mi;
     }
   }
   if (p->v > 1 && (p->overlap || p->S[0] < 2 || p->S[0] * p->v > OR_MAXS)) return 0;   /* V12 */
@@ -483,7 +491,7 @@ static int decode_rules(const or_ctx* x, const or_planes* q, int64_t i, or_plan*
     p->nmb[g] = w >> 16;
     if (p->reps[g] == 0) return 0;                           /* V1 */
     if (p->nmb[g] < p->reps[g]) return 0;                    /* V4 every replica gets work */
-    batch += p->nmb[g] * m->mbs[p->mi];
+    batch += p->nmb[g] * m->mbs[p->mi_c[g]];
     uint64_t tv = q->types[g * stride + i];
     for (uint64_t s = 0; s < p->S[g]; ++s) {
       p->type[g][s] = (int)((tv >> (4 * s)) & 15);
@@ -600,7 +608,7 @@ static uint64_t stage_mem(const or_ctx* x, const or_plan* p, uint64_t g, uint64_
   else opt = mul(m->opt_bytes, add(pd, pe));
   uint64_t M = cdiv(p->nmb[g], p->reps[g]);
   uint64_t fly = p->zb ? in_flight_zb(p->S[g], M, s) : in_flight(p->S[g], M, s);
-  uint64_t act = mul(mul(ns, layer_act_bytes(x, tp, m->mbs[p->mi])), fly);
+  uint64_t act = mul(mul(ns, layer_act_bytes(x, tp, m->mbs[p->mi_c[g]])), fly);
   return add(add(wg, opt), act);
 }
 
@@ -709,12 +717,12 @@ static void stage_compute(const or_ctx* x, const or_plan* p, uint64_t g, int k, 
   const or_model* m = &x->m;
   const or_cluster* cl = &x->c;
   uint64_t ep = p->ep, epl = log2u(ep), tp = p->tp[g], tpl = log2u(tp);
-  uint64_t b = m->mbs[p->mi], T = b * m->seq, ns = hi - lo, n = p->reps[g] * tp;
+  uint64_t mi = p->mi_c[g], b = m->mbs[mi], T = b * m->seq, ns = hi - lo, n = p->reps[g] * tp;
   uint64_t act = mul(T, mul(m->h, m->e));                      /* one micro-batch activation (Table 1, R10) */
   uint64_t Fc = 0, Bc = 0;
   for (uint64_t l = lo; l < hi; ++l) {
-    Fc = add(Fc, LF(x, k, tpl, p->mi, epl)[l]);
-    Bc = add(Bc, LB(x, k, tpl, p->mi, epl)[l]);
+    Fc = add(Fc, LF(x, k, tpl, mi, epl)[l]);
+    Bc = add(Bc, LB(x, k, tpl, mi, epl)[l]);
   }
   if (first) { Fc = add(Fc, embed_time(x, k, b, 0)); Bc = add(Bc, embed_time(x, k, b, 1)); }
   if (last) { Fc = add(Fc, head_time(x, k, tp, b, 0)); Bc = add(Bc, head_time(x, k, tp, b, 1)); }
@@ -762,7 +770,7 @@ static uint64_t hop_cost(const or_ctx* x, const or_plan* p, uint64_t g, int k, u
   const or_model* m = &x->m;
   const or_cluster* cl = &x->c;
   uint64_t tp = p->tp[g], n = p->reps[g] * tp;
-  uint64_t act = mul(m->mbs[p->mi] * m->seq, mul(m->h, m->e));
+  uint64_t act = mul(m->mbs[p->mi_c[g]] * m->seq, mul(m->h, m->e));
   int intra = (k == k2);
   for (uint64_t r = 0; intra && r < p->reps[g]; ++r)
     if ((b1 + r * tp) / cl->dpn[k] != (b2 + r * tp) / cl->dpn[k]) intra = 0;
@@ -1021,20 +1029,28 @@ static void eval_plan(const or_ctx* x, const or_plan* p, or_detail* d, uint64_t*
     uint64_t t = dp_sync_h(x, p->het ? NULL : &seg_h[j], p_all, p->zero, mul(m->grad_bytes, pd),
                            mul(m->param_bytes, pd), alpha, bq);
     if (m->E) t = add(t, dp_sync_cl(x, p_all / ep, p->zero, mul(m->grad_bytes, pe), mul(m->param_bytes, pe), alpha, bq));
-    /* R36: classes with finer shards first gather the coarse shard inside
+    /* R51: when the classes holding the segment run different micro-batch
+     * sizes, each class first weights its gradient shard by its share of
+     * the global batch (one elementwise pass: a multiply per element, the
+     * shard read and written at the device's HBM rate).
+     * R36: classes with finer shards then gather the coarse shard inside
      * each TP group: a ring all-gather over tp/tp_min members of the
-     * class's own gradient shard, on the group's node fabric; classes
-     * reshard at the same time, so the slowest counts */
+     * class's own gradient shard, on the group's node fabric.  Classes
+     * reshard at the same time, so the slowest class counts. */
+    int mixed = 0;
+    for (uint64_t g = 1; g < G; ++g) if (p->mi_c[g] != p->mi_c[0]) mixed = 1;
     uint64_t rs = 0, rs_lat = 0, rs_bw = 0;
     for (uint64_t g = 0; g < G; ++g) {
-      if (p->tp[g] == tp_min) continue;
+      if (p->tp[g] == tp_min && !mixed) continue;
       uint64_t qd, qe;
       span_params(x, a, e, p->tp[g], ep, &qd, &qe);
       int k = p->type[g][sg[g]];
-      uint64_t steps = p->tp[g] / tp_min - 1, chunk = mul(m->grad_bytes, add(qd, qe));
+      uint64_t elems = add(qd, qe);
+      uint64_t sc = mixed ? op_time(x, k, elems, mul(2 * m->grad_bytes, elems)) : 0;
+      uint64_t steps = p->tp[g] / tp_min - 1, chunk = mul(m->grad_bytes, elems);
       uint64_t bqi = intra_max(x, k, base[g][sg[g]], p->reps[g] * p->tp[g]);
-      uint64_t r = ring(steps, chunk, cl->a_intra[k], bqi);
-      if (r > rs) { rs = r; rs_lat = mul(steps, cl->a_intra[k]); rs_bw = link_time(mul(steps, chunk), bqi); }
+      uint64_t r = add(sc, ring(steps, chunk, cl->a_intra[k], bqi));
+      if (r > rs) { rs = r; rs_lat = add(sc, mul(steps, cl->a_intra[k])); rs_bw = link_time(mul(steps, chunk), bqi); }
     }
     t = add(t, rs);
     if (!cl->contention) {

@@ -159,14 +159,16 @@ struct Plan {
   // private memory).
   uint32_t c, rc, nc;
   uint64_t tc;
-  // per-class layout: byte c = log2 TP | (PP - 1) << 2 of class c (0 with
-  // the shared layout, where tpl, S and the cuts above hold for every class;
-  // with the per-class layout they are the pipeline's own class's)
+  // per-class layout: byte c = log2 TP | (PP - 1) << 2 | micro-batch size
+  // index << 6 of class c (0 with the shared layout, where tpl, S, mi and
+  // the cuts above hold for every class; with the per-class layout they are
+  // the pipeline's own class's)
   uint32_t chdr;
 };
 
 __device__ __forceinline__ uint32_t cls_tpl(uint32_t chdr, uint32_t c) { return (chdr >> (8 * c)) & 3; }
 __device__ __forceinline__ uint32_t cls_S(uint32_t chdr, uint32_t c) { return ((chdr >> (8 * c + 2)) & 15) + 1; }
+__device__ __forceinline__ uint32_t cls_mi(uint32_t chdr, uint32_t c) { return (chdr >> (8 * c + 6)) & 3; }
 __device__ __forceinline__ uint64_t stage_sel(uint32_t S) { return S == 16 ? ~0ull : ((1ull << (4 * S)) - 1); }
 
 // cut of stage s (a run-time index): mask arithmetic rather than a select,
@@ -214,6 +216,7 @@ __device__ __forceinline__ Plan load_plan(const PackedPlan* packed, const uint4*
     p.tpl = cls_tpl(p.chdr, p.c);
     p.tp = 1u << p.tpl;
     p.S = cls_S(p.chdr, p.c);
+    p.mi = cls_mi(p.chdr, p.c);
     const uint4 r = pcut[slot];
     p.cut_lo = (uint64_t)r.y << 32 | r.x;
     p.cut_hi = (uint64_t)r.w << 32 | r.z;
@@ -259,7 +262,7 @@ __device__ __forceinline__ Checked check_plan(const Tab& t, const sim_plans& pl,
   bool ok = (hdr >> 17) == 0 && mi < t.n_mbs && ((t.ep_ok >> epl) & 1);
   // the per-class layout leaves the header's TP and PP fields unused (0) and
   // has no overlap, interleaving or zero-bubble order
-  if (kHet) ok = ok && (hdr & 0x1e0f3) == 0;
+  if (kHet) ok = ok && (hdr & 0x1f8f3) == 0;   // and its micro-batch size: every class has its own
   // the zero-bubble order goes with neither overlap nor interleaving
   if (!kHet && ((hdr >> 16) & 1)) ok = ok && (hdr & 0xe000) == 0;
   // interleaving: no overlap, at least two devices, at most 16 virtual stages
@@ -277,7 +280,8 @@ __device__ __forceinline__ Checked check_plan(const Tab& t, const sim_plans& pl,
 #pragma unroll
     for (int j = 0; j < 4; ++j) r.cw[c][j] = 0;
     if (c < G) {
-      if (kHet) ok = ok && (lay >> 6) == 0;
+      const uint32_t mic = kHet ? lay >> 6 : mi;   // the class's micro-batch size index
+      if (kHet) ok = ok && mic < t.n_mbs;
       if (kHet || c == 0) {   // the shared layout's cuts are checked once
         ok = ok && ((t.tp_ok >> tpl) & 1);
         const uint32_t ncut = kHet ? S : S * v;
@@ -303,7 +307,7 @@ __device__ __forceinline__ Checked check_plan(const Tab& t, const sim_plans& pl,
         const uint32_t M = (nmb + reps - 1) / reps;
         ok = M % S == 0 && M >= 2 * S;
       }
-      batch += nmb * t.mbs[mi];
+      batch += nmb * t.mbs[mic];
       psum += reps;
       // every stage's type exists and holds whole TP groups in a node
       const uint32_t okm = t.type_ok[tpl];
@@ -373,7 +377,8 @@ __device__ __forceinline__ uint64_t class_state_bytes(const Tab& t, const Checke
 // micro-batch's activations stay until its weight-gradient pass).
 __device__ __forceinline__ uint64_t class_stage_bytes(const Tab& t, const Checked& r, uint32_t c, uint32_t s,
                                                       uint32_t ns, uint64_t state) {
-  const uint32_t mi = (r.hdr >> 11) & 3, S = r.S[c];
+  // the micro-batch size: the header's (shared layout) or the class's (per-class layout, header field 0)
+  const uint32_t mi = ((r.hdr >> 11) & 3) | cls_mi(r.chdr, c), S = r.S[c];
   const uint32_t reps = r.cls[c] & 0xffff, M = ((r.cls[c] >> 16) + reps - 1) / reps;
   const uint32_t held = ((r.hdr >> 16) & 1) ? S : S - s;
   const uint32_t fly = held < M ? held : M;
@@ -820,6 +825,15 @@ __device__ __forceinline__ uint32_t row_word(const uint4 (&rows)[4], uint32_t c,
   return j == 0 ? v.x : j == 1 ? v.y : j == 2 ? v.z : v.w;
 }
 
+// Weighting of a gradient shard of n elements by the class's share of the
+// global batch, on a device of type k: one multiply per element, the fp32
+// shard read and written (the roofline time of one elementwise op)
+__device__ __forceinline__ uint64_t weigh_ps(const Tab& t, uint32_t k, uint64_t n) {
+  const uint64_t tf = t.tflops[k], hb = t.hbm[k], by = 2000 * t.grad_bytes * n;
+  const uint64_t tc = n / tf + (n % tf != 0), tm = by / hb + (by % hb != 0);
+  return tc > tm ? tc : tm;
+}
+
 template <int kMode>
 __device__ __forceinline__ uint64_t seg_dp(const Tab& t, const Hot<kMode>& h, const Plan& p, const uint4 (&rows)[4],
                                            uint32_t a, uint32_t e, double rp, double rpe, uint64_t& lat,
@@ -829,6 +843,11 @@ __device__ __forceinline__ uint64_t seg_dp(const Tab& t, const Hot<kMode>& h, co
 #pragma unroll
   for (uint32_t c2 = 0; c2 < 4; ++c2)
     if (c2 < G) tmin = cls_tpl(p.chdr, c2) < tmin ? cls_tpl(p.chdr, c2) : tmin;
+  // classes at different micro-batch sizes weight their gradients first
+  bool mixed = false;
+#pragma unroll
+  for (uint32_t c2 = 1; c2 < 4; ++c2)
+    if (c2 < G) mixed = mixed || cls_mi(p.chdr, c2) != cls_mi(p.chdr, 0);
   bool same = true;
   uint32_t k0 = 0, nmin = 0xffffffffu, nmax = 0, bq_dp = 0;
   uint64_t a_dp = 0, rs = 0, rs_l = 0, rs_b = 0;
@@ -859,12 +878,16 @@ __device__ __forceinline__ uint64_t seg_dp(const Tab& t, const Hot<kMode>& h, co
     const uint32_t bx = nic2 > t2.bq_pcie ? nic2 : t2.bq_pcie;
     bq_dp = bx > bq_dp ? bx : bq_dp;
     a_dp = 2 * t2.a_side > a_dp ? 2 * t2.a_side : a_dp;
-    if (tpl2 > tmin) {
+    if (tpl2 > tmin || mixed) {
+      // the class's shard: weighted (one multiply per element, read and
+      // written at the device's HBM rate) when micro-batch sizes differ,
+      // then gathered to the coarsest TP layout inside each TP group
       const uint64_t g1 = (1u << (tpl2 - tmin)) - 1;
       const uint64_t sh = (uint64_t)ns * (t.par_layer[tpl2] + t.par_expert[tpl2][epl]) +
                           (a == 0 ? t.par_embed[tpl2] : 0) + (e == t.L ? t.par_head[tpl2] : 0);
+      const uint64_t sc = mixed ? weigh_ps(t, k2, sh) : 0;
       const uint32_t bq_in = range_max(h.rmi(), t.N, l2, h2);
-      const uint64_t rl = g1 * t2.a_intra, rb = link_ps(g1 * t.grad_bytes * sh, bq_in), r = rl + rb;
+      const uint64_t rl = sc + g1 * t2.a_intra, rb = link_ps(g1 * t.grad_bytes * sh, bq_in), r = rl + rb;
       if (r > rs) {
         rs = r;
         rs_l = rl;
@@ -945,9 +968,13 @@ __device__ __forceinline__ void het_plan_syncs(const Tab& t, const Hot<kMode>& h
   const uint32_t G = p.G, epl = p.epl;
   const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> epl);
   uint32_t tmin = 3;
+  bool mixed = false;   // classes at different micro-batch sizes weight their gradients first
 #pragma unroll
   for (uint32_t c2 = 0; c2 < 4; ++c2)
-    if (c2 < G) tmin = cls_tpl(p.chdr, c2) < tmin ? cls_tpl(p.chdr, c2) : tmin;
+    if (c2 < G) {
+      tmin = cls_tpl(p.chdr, c2) < tmin ? cls_tpl(p.chdr, c2) : tmin;
+      mixed = mixed || cls_mi(p.chdr, c2) != cls_mi(p.chdr, 0);
+    }
   // per class: current stage and its end, and that stage's type, node range,
   // worst NIC/PCIe rate, inter-node latency, node latency, worst node fabric;
   // classes enter their first stage at the walk's first step
@@ -1002,11 +1029,12 @@ __device__ __forceinline__ void het_plan_syncs(const Tab& t, const Hot<kMode>& h
       bq_dp = bx[c2] > bq_dp ? bx[c2] : bq_dp;
       a_dp = as2[c2] > a_dp ? as2[c2] : a_dp;
       const uint32_t tpl2 = cls_tpl(p.chdr, c2);
-      if (tpl2 > tmin) {
+      if (tpl2 > tmin || mixed) {
         const uint64_t g1 = (1u << (tpl2 - tmin)) - 1;
         const uint64_t sh = (uint64_t)ns * (t.par_layer[tpl2] + t.par_expert[tpl2][epl]) +
                             (a == 0 ? t.par_embed[tpl2] : 0) + (e == t.L ? t.par_head[tpl2] : 0);
-        const uint64_t rl = g1 * ain[c2], rb = link_ps(g1 * t.grad_bytes * sh, bin[c2]), r = rl + rb;
+        const uint64_t rl = (mixed ? weigh_ps(t, kk[c2], sh) : 0) + g1 * ain[c2];
+        const uint64_t rb = link_ps(g1 * t.grad_bytes * sh, bin[c2]), r = rl + rb;
         if (r > rs) {
           rs = r;
           rs_l = rl;

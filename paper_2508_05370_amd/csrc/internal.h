@@ -92,6 +92,8 @@ struct Tab {
   uint32_t bq_pcie[kMaxTypes];    // PCIe ps/byte in 2^-16 units, 0 = absent
   uint64_t a_intra[kMaxTypes];    // intra-node message latency
   uint64_t a_side[kMaxTypes];     // one end of an inter-node path: two PCIe trips + NIC
+  uint32_t tflops[kMaxTypes];     // device speed of pool k (TFLOP/s, GB/s of HBM): the gradient
+  uint32_t hbm[kMaxTypes];        // weighting of classes with different micro-batch sizes
   uint64_t act[4];                // bytes of one micro-batch activation per mbs index
   uint64_t grad_bytes, param_bytes;
   uint64_t par_layer[4];          // non-expert parameters of one layer on one TP rank, by log2 TP

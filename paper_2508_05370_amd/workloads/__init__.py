@@ -152,6 +152,18 @@ def cluster_two_type_8():
     return dict(types=[A, B], nic_MBps_dev=None, intra_MBps_node=None)
 
 
+def cluster_fig3():
+    """The two nodes of Sec. 3's worked example (Fig. 3): type 0 = node A, 4 x H100 80 GB; type 1 = node
+    B, 4 x A100 40 GB.  Links and delays from Table 5 (its NVLink and PCIe rates are bidirectional
+    totals, so half of each per direction; NIC 200 Gb/s with 368 ns processing; PCIe trips of 143.75
+    and 287.5 ns).  The paper gives no device speeds: these are the public dense bf16 TFLOP/s and HBM
+    GB/s of the two parts.  Memory capacities are not set (the example's Llama-2 70B does not fit
+    four of these devices; give mem_bytes to check it)."""
+    H100 = _type(1, 4, 989, 3350, 450_000, 64_000, nic_MBps(200), alpha_from_gbps(3600), 143_750, 368_000)
+    A100 = _type(1, 4, 312, 1555, 300_000, 32_000, nic_MBps(200), alpha_from_gbps(2400), 287_500, 368_000)
+    return dict(types=[H100, A100], nic_MBps_dev=None, intra_MBps_node=None)
+
+
 def cluster_random(cfg, nodes, dpn=8, nic_choices=(100, 200, 400), pcie=True, jitter=False, pcie_only_types=(),
                    alpha_mult=False):
     st = Stream(0xC1A50000 + cfg)
@@ -275,20 +287,21 @@ def interleaved_plans(w, first=0, n=None, nthreads=None):
 
 
 def as_per_class(p):
-    """The per-class-layout encoding of shared-layout plans: every class gets the plan's TP degree, depth and
-    cuts (header TP and PP fields cleared)."""
+    """The per-class-layout encoding of shared-layout plans: every class gets the plan's TP degree, depth,
+    micro-batch size and cuts (header TP, PP and micro-batch size fields cleared)."""
     n = p["hdr"].shape[0]
     hdr = p["hdr"].astype(np.uint32)
     tpl = hdr & 3
     pp1 = (hdr >> 4) & 15
     G = ((hdr >> 8) & 3) + 1
+    mi = (hdr >> 11) & 3
     chdr = np.zeros(n, np.uint32)
     ccut = np.zeros((64, n), np.uint8)
     for c in range(4):
         has = G > c
-        chdr |= np.where(has, (tpl | (pp1 << 2)) << (8 * c), 0).astype(np.uint32)
+        chdr |= np.where(has, (tpl | (pp1 << 2) | (mi << 6)) << (8 * c), 0).astype(np.uint32)
         ccut[c * 16:(c + 1) * 16] = np.where(has[None, :], p["cut"][:, :n], 0)
-    return dict(hdr=hdr & ~np.uint32(0xF3), cls=np.ascontiguousarray(p["cls"][:, :n]),
+    return dict(hdr=hdr & ~np.uint32(0x18F3), cls=np.ascontiguousarray(p["cls"][:, :n]),
                 types=np.ascontiguousarray(p["types"][:, :n]), chdr=chdr, ccut=ccut)
 
 

@@ -183,14 +183,27 @@ def test_random_model(torch, B, oracle_mod, workloads, seed):
 def _with_mbs(p, mbs, rng):
     """Move each plan to a random micro-batch size of the list where every class's micro-batch
     count divides and still gives each replica one: the count shrinks by the size, so the
-    global batch stays the same (header bits 11-12 = the size's index)."""
+    global batch stays the same (header bits 11-12 = the size's index).  Per-class-layout plans
+    move each class on its own (class byte bits 6-7), so their classes mix micro-batch sizes."""
     p = {k: v.copy() for k, v in p.items()}
     n = p["hdr"].shape[0]
     G = ((p["hdr"] >> 8) & 3) + 1
+    het = "chdr" in p
     moved = 0
     for i in range(n):
-        j = int(rng.integers(0, len(mbs)))
         cls = [(int(p["cls"][g, i]) & 0xFFFF, int(p["cls"][g, i]) >> 16) for g in range(int(G[i]))]
+        if het:
+            any_moved = False
+            for g, (reps, nmb) in enumerate(cls):
+                j = int(rng.integers(0, len(mbs)))
+                if j == 0 or nmb % mbs[j] or nmb // mbs[j] < reps:
+                    continue
+                p["cls"][g, i] = reps | ((nmb // mbs[j]) << 16)
+                p["chdr"][i] = (int(p["chdr"][i]) & ~(3 << (8 * g + 6))) | (j << (8 * g + 6))
+                any_moved = True
+            moved += any_moved
+            continue
+        j = int(rng.integers(0, len(mbs)))
         if j == 0 or any(nmb % mbs[j] or nmb // mbs[j] < reps for reps, nmb in cls):
             continue
         for g, (reps, nmb) in enumerate(cls):

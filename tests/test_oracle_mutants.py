@@ -19,6 +19,7 @@ SRC = os.path.join(ROOT, "oracle", "oracle.c")
 
 PINS = "tests/test_oracle_pins.py::"
 ZB = "tests/test_oracle_zb.py::"
+FIG3 = "tests/test_oracle_fig3.py::"
 
 # name: (text in oracle.c, the mistake, pins that must fail)
 MUTANTS = {
@@ -90,6 +91,27 @@ MUTANTS = {
         "bytes = add(bytes, cdiv(mul(mul(ep - 1, T), mul(m->topk, mul(wmax, mul(m->h, m->e)))), 65536));",
         "bytes = add(bytes, cdiv(mul(mul(ep, T), mul(m->topk, mul(wmax, mul(m->h, m->e)))), 65536));",
         [PINS + "test_moe_all_to_all_closed_form"]),
+    # R51 and the Fig. 3 composition (per-class micro-batch sizes)
+    "weighting_reads_only": (
+        "      uint64_t sc = mixed ? op_time(x, k, elems, mul(2 * m->grad_bytes, elems)) : 0;",
+        "      uint64_t sc = mixed ? op_time(x, k, elems, mul(m->grad_bytes, elems)) : 0;",
+        [FIG3 + "test_fig3_worked_example"]),
+    "weighting_always": (
+        "      uint64_t sc = mixed ? op_time(x, k, elems, mul(2 * m->grad_bytes, elems)) : 0;",
+        "      uint64_t sc = op_time(x, k, elems, mul(2 * m->grad_bytes, elems));",
+        [FIG3 + "test_fig3_worked_example"]),
+    "weighting_at_coarse_shard": (
+        "      span_params(x, a, e, p->tp[g], ep, &qd, &qe);\n      int k = p->type[g][sg[g]];\n      uint64_t elems",
+        "      span_params(x, a, e, tp_min, ep, &qd, &qe);\n      int k = p->type[g][sg[g]];\n      uint64_t elems",
+        [FIG3 + "test_fig3_worked_example"]),
+    "hop_at_plan_micro_batch": (
+        "  uint64_t act = mul(m->mbs[p->mi_c[g]] * m->seq, mul(m->h, m->e));\n  int intra = (k == k2);",
+        "  uint64_t act = mul(m->mbs[p->mi] * m->seq, mul(m->h, m->e));\n  int intra = (k == k2);",
+        [FIG3 + "test_fig3_worked_example"]),
+    "reshard_gather_not_before_ring": (
+        "    t = add(t, rs);\n    if (!cl->contention) {",
+        "    if (!cl->contention) {",
+        [FIG3 + "test_fig3_worked_example"]),
 }
 
 
