@@ -290,11 +290,13 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
     if (e == hipSuccess) e = launch_prep(c->tab, p, cn, out + off, W.packed, W.pcut, W.meta, W.hist, W.keys, s);
     if (t1) end_event(c, 1, s, &ev);
     if (e == hipSuccess && het) e = launch_plan_syncs(c->tab, W.packed, W.pcut, W.meta, cn, W.hdp, s);
-    // shared-layout calls sort long plans by plan, leaving padding lanes
+    // shared-layout calls sort plans by plan, leaving padding lanes; the
+    // variant tiles start empty
     if (e == hipSuccess && !het) e = launch_fill32(W.ids, (uint32_t)id_words(cn), kNoSlot, s);
+    if (e == hipSuccess && !het) e = launch_fill32(W.vlist, (uint32_t)id_words(cn), kNoSlot, s);
     if (e == hipSuccess) e = launch_scan(W.hist, W.cursor, W.sstart, W.sbase, !het, s);
     if (e == hipSuccess) e = launch_scatter(W.keys, (uint32_t)(cn * 4), W.cursor, W.sbase, !het, W.ids, s);
-    const EvalArgs a = {W.packed, W.pcut, W.hdp, W.meta, W.ids, W.sstart, out + off, W.ctr, W.deferred,
+    const EvalArgs a = {W.packed, W.pcut, W.hdp, W.meta, W.ids, W.sstart, out + off, W.ctr, W.deferred, W.vlist,
                         c->timing ? c->skipped_ops : nullptr, c->dtab};
     EventPair e0;
     bool t0 = e == hipSuccess && begin_event(c, 0, s, &e0);
@@ -364,9 +366,10 @@ extern "C" int sim_eval_plans_noalloc(sim_ctx* c, const sim_plans* plans, int64_
   if (e == hipSuccess) e = launch_prep(c->tab, *plans, n, out, W.packed, W.pcut, W.meta, W.hist, W.keys, s);
   if (e == hipSuccess && het) e = launch_plan_syncs(c->tab, W.packed, W.pcut, W.meta, n, W.hdp, s);
   if (e == hipSuccess && !het) e = launch_fill32(W.ids, (uint32_t)id_words(n), kNoSlot, s);
+  if (e == hipSuccess && !het) e = launch_fill32(W.vlist, (uint32_t)id_words(n), kNoSlot, s);
   if (e == hipSuccess) e = launch_scan(W.hist, W.cursor, W.sstart, W.sbase, !het, s);
   if (e == hipSuccess) e = launch_scatter(W.keys, (uint32_t)(n * 4), W.cursor, W.sbase, !het, W.ids, s);
-  const EvalArgs a = {W.packed, W.pcut, W.hdp, W.meta, W.ids, W.sstart, out, W.ctr, W.deferred,
+  const EvalArgs a = {W.packed, W.pcut, W.hdp, W.meta, W.ids, W.sstart, out, W.ctr, W.deferred, W.vlist,
                       c->timing ? c->skipped_ops : nullptr, c->dtab};
   if (e == hipSuccess) e = launch_first(c->tab, a, (uint32_t)(n * 4), s);
   if (e == hipSuccess) e = launch_deferred(c->tab, a, (uint32_t)(n * 4), s);

@@ -1559,7 +1559,7 @@ __device__ __forceinline__ void zb_iter(const V (&f)[S], const V (&bi)[S], const
 }
 
 template <int S, typename V, bool kJump>
-__device__ __forceinline__ void pipe_zb(const V (&f)[S], const V (&bi)[S], const V (&w)[S], const V (&c)[S], uint32_t M,
+__device__ __forceinline__ bool pipe_zb(const V (&f)[S], const V (&bi)[S], const V (&w)[S], const V (&c)[S], uint32_t M,
                                         int& skipped,
                                         V (&last)[S]) {
   V out_f[S];
@@ -1614,6 +1614,14 @@ __device__ __forceinline__ void pipe_zb(const V (&f)[S], const V (&bi)[S], const
         rem = 0;
       }
     }
+    if (rem == 1) {
+      zb_iter<S, V>(f, bi, w, c, S, -1, out_f, last);
+      rem = 0;
+    }
+    if (rem > 0) {   // still aperiodic: the deferred pass runs the whole loop
+      skipped = -1;
+      return false;
+    }
   }
   for (; rem > 0; --rem) zb_iter<S, V>(f, bi, w, c, S, -1, out_f, last);
 #pragma unroll
@@ -1621,6 +1629,7 @@ __device__ __forceinline__ void pipe_zb(const V (&f)[S], const V (&bi)[S], const
     if (tr >= S - 1 - m_) zb_iter<S, V>(f, bi, w, c, m_ - S + 1 + tr, tr, out_f, last);
 #pragma unroll
   for (int s = 0; s < S; ++s) last[s] += (V)(s < m_ ? s : m_) * w[s];
+  return true;
 }
 
 // Integers below 2^53 are exact in fp64.  Every value the fp64 pass computes
@@ -1641,8 +1650,9 @@ struct EvalBufs {
   uint32_t* ctr;            // [0] overflow count, [1 + 16 - S] deferred S-stage pipelines,
                             // [kVariantCtr + 16 - S] S-stage overlap and zero-bubble pipelines
   uint32_t* ovf;            // overflow list (fp64 result reached 2^53)
-  uint32_t* deferred;       // deferred S-stage pipelines at [sstart[16 - S], ...), the S-stage
-                            // overlap and zero-bubble ones backwards from sstart[17 - S] - 1
+  uint32_t* deferred;       // deferred S-stage pipelines at [sstart[16 - S], ...)
+  uint32_t* vlist;          // S-stage overlap and zero-bubble tiles at [sstart[16 - S], ...): each a
+                            // first-pass wavefront's lanes as they were (kNoSlot elsewhere)
   unsigned long long* skipped_ops;   // optional: recurrence ops skipped by the shortcut
   const Tab* dtab;          // the Tab in device memory
 };
@@ -1704,9 +1714,20 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
   const Plan p = load_plan<kHet>(e.packed, e.pcut, slot);
   {
     if (!kFull && !kHet && !kOvl && !kZb) {
-      if (p.overlap | p.zb) {
-        e.deferred[e.sstart[kMaxStages - S + 1] - 1 - atomicAdd(&e.ctr[kVariantCtr + kMaxStages - S], 1u)] = slot;
-        return;
+      // overlap and zero-bubble plans go to the variant pass: the wavefront
+      // takes one 64-slot tile and puts them on the lanes they hold here, so
+      // that the tile keeps its plans' lanes together; the first active lane
+      // takes the tile and the same lane's value is broadcast
+      const bool var = p.overlap | p.zb;
+      if (__ballot(var)) {
+        uint32_t tile = 0;
+        if (threadIdx.x % 64u == (uint32_t)(__ffsll((unsigned long long)__ballot(1)) - 1))
+          tile = atomicAdd(&e.ctr[kVariantCtr + kMaxStages - S], 64u);
+        tile = __builtin_amdgcn_readfirstlane(tile);
+        if (var) {
+          e.vlist[e.sstart[kMaxStages - S] + tile + (threadIdx.x & 63u)] = slot;
+          return;
+        }
       }
       if (t.ccl_hier) {
         e.deferred[e.sstart[kMaxStages - S] + atomicAdd(&e.ctr[1 + kMaxStages - S], 1u)] = slot;
@@ -1719,8 +1740,9 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
   int skipped;
   double last[S];
   bool done = true;
-  if constexpr (kZb) pipe_zb<S, double, true>(r.f, r.bi, r.w, r.c, M, skipped, last);
-  else if constexpr (kOvl) done = pipe<S, double, true, true>(r.f, r.b, r.c, M, skipped, last);
+  // the first and variant passes take the periodic shortcut and defer the
+  // lanes still aperiodic after the budget; the deferred pass runs the whole loop
+  if constexpr (kZb) done = pipe_zb<S, double, !kFull>(r.f, r.bi, r.w, r.c, M, skipped, last);
   else done = pipe<S, double, !kFull>(r.f, r.b, r.c, M, skipped, last);
   // With up to kKeepPlanS stages the plan stays in registers through the
   // recurrence (whose state is small); longer pipelines read it again for
@@ -1752,15 +1774,19 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
               (unsigned long long)skipped * (unsigned long long)(6 * (S - 1) + 2));
 }
 
-// Deferred pass of one pipeline: the whole loop.
+// Deferred pass of one pipeline: the whole loop (plain, overlap or zero-bubble, by its header).
 template <int S, int kMode, bool kHet>
 __device__ __forceinline__ void eval_deferred(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot) {
-  eval_one<S, true, kMode, kHet>(t, h, e, slot);
+  const uint32_t hdr = kHet ? 0 : e.packed[slot >> 2].hdr;
+  if (!kHet && ((hdr >> 16) & 1)) eval_one<S, true, kMode, false, false, true>(t, h, e, slot);
+  else if (!kHet && ((hdr >> 13) & 1)) eval_one<S, true, kMode, false, true, false>(t, h, e, slot);
+  else eval_one<S, true, kMode, kHet>(t, h, e, slot);
 }
 
 // Variant pass of one pipeline (shared layout): overlapped gradient sync or
-// the zero-bubble order, the shortcut first and the whole loop where the
-// schedule stays aperiodic.
+// the zero-bubble order, with the periodic shortcut; lanes still aperiodic
+// after the budget go to the deferred lists (the deferred pass runs them
+// through the whole loop).
 template <int S, int kMode>
 __device__ __forceinline__ void eval_variant(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot) {
   if ((e.packed[slot >> 2].hdr >> 16) & 1) eval_one<S, false, kMode, false, false, true>(t, h, e, slot);
@@ -2139,10 +2165,10 @@ __global__ void __launch_bounds__(kEvalThreads) k_deferred(const Tab* __restrict
 }
 
 // Overlap and zero-bubble pipelines of the four stage counts of group GRP
-// (as k_eval's groups), taken from the variant lists the first pass filled:
-// the S-stage list runs backwards from sstart[17 - S] - 1 and holds
-// ctr[kVariantCtr + 16 - S] pipelines.  64-pipeline tiles of one stage count,
-// dealt round-robin to the waves of the grid.  The Tab is read from its copy
+// (as k_eval's groups), taken from the tiles the first pass filled: the
+// S-stage tiles start at sstart[16 - S] and take ctr[kVariantCtr + 16 - S]
+// slots, each tile one first-pass wavefront's lanes (plans whole, kNoSlot
+// elsewhere), dealt round-robin to the waves of the grid.  The Tab is read from its copy
 // in device memory, as in k_deferred.  A block with no tile returns before
 // touching LDS, so a launch over empty lists costs next to nothing.
 template <int GRP, int kMode>
@@ -2167,7 +2193,8 @@ __global__ void __launch_bounds__(kEvalThreads) k_variant(const Tab* __restrict_
     const uint32_t off = (q - first) * 64u + (threadIdx.x & 63u);
     if (off >= cnt) continue;
     const uint32_t S = kTop - j;
-    const uint32_t slot = e.deferred[e.sstart[kMaxStages - S + 1] - 1 - off];
+    const uint32_t slot = e.vlist[e.sstart[kMaxStages - S] + off];
+    if (slot == kNoSlot) continue;
     if (j == 0) eval_variant<kTop, kMode>(t, h, e, slot);
     else if (j == 1) eval_variant<kTop - 1, kMode>(t, h, e, slot);
     else if (j == 2) eval_variant<kTop - 2, kMode>(t, h, e, slot);

@@ -124,8 +124,8 @@ struct Tab {
 // pipelines, sstart[16] their total and the first id of the interleaved
 // pipelines (layout above).  ctr[0] counts overflowed pipelines,
 // ctr[1 + 16 - S] the S-stage pipelines deferred to the full-loop pass,
-// ctr[kVariantCtr + 16 - S] the S-stage overlap and zero-bubble pipelines
-// of the variant pass; the overflow list follows the counters at
+// ctr[kVariantCtr + 16 - S] the slots of the S-stage overlap and zero-bubble
+// tiles of the variant pass (64 per tile); the overflow list follows the counters at
 // ctr + kEvalCounters.
 constexpr uint32_t kVariantCtr = 1 + kMaxStages;
 constexpr uint32_t kEvalCounters = 48;
@@ -143,6 +143,7 @@ struct EvalArgs {
   uint64_t* out;
   uint32_t* ctr;
   uint32_t* deferred;          // as long as ids
+  uint32_t* vlist;             // as long as ids: overlap and zero-bubble tiles (kNoSlot where empty)
   uint64_t* skipped_ops;       // optional: kSkipSlots counters, kSkipStride words apart
   const Tab* dtab;             // the context's Tab in device memory (read by the deferred pass)
 };
@@ -162,7 +163,7 @@ struct Work {
   PackedPlan* packed;
   uint4* pcut;
   uint64_t* hdp;
-  uint32_t *meta, *ids, *deferred, *hist, *ctr, *cursor, *sstart, *sbase;
+  uint32_t *meta, *ids, *deferred, *vlist, *hist, *ctr, *cursor, *sstart, *sbase;
   uint16_t* keys;
 };
 // sorted ids (and deferred lists) of a chunk: four lanes per plan at most,
@@ -173,7 +174,7 @@ constexpr size_t het_sync_bytes(int64_t ch, bool het) {
   return het ? align256((size_t)ch * kMaxClasses * kMaxStages * 8) : 0;
 }
 constexpr size_t work_bytes(int64_t ch, bool het) {
-  return align256((size_t)ch * sizeof(PackedPlan)) + align256((size_t)ch * 4 * 4) + 2 * align256(id_words(ch) * 4) +
+  return align256((size_t)ch * sizeof(PackedPlan)) + align256((size_t)ch * 4 * 4) + 3 * align256(id_words(ch) * 4) +
          align256(kCounters * 4 + (size_t)ch * 4 * 4) + align256(kBuckets * 4) + align256(kSstartWords * 4) +
          align256(kSuperBuckets * 4) + align256((size_t)ch * 4 * 2) +
          cut_rows_bytes(ch, het) + het_sync_bytes(ch, het);
@@ -187,6 +188,7 @@ inline Work carve(void* base, int64_t ch, bool het) {
   w.meta = (uint32_t*)p; p += align256((size_t)ch * 16);
   w.ids = (uint32_t*)p; p += align256(id_words(ch) * 4);
   w.deferred = (uint32_t*)p; p += align256(id_words(ch) * 4);
+  w.vlist = (uint32_t*)p; p += align256(id_words(ch) * 4);
   w.hist = (uint32_t*)p; w.ctr = w.hist + kBuckets; p += align256(kCounters * 4 + (size_t)ch * 16);
   w.cursor = (uint32_t*)p; p += align256(kBuckets * 4);
   w.sstart = (uint32_t*)p; p += align256(kSstartWords * 4);

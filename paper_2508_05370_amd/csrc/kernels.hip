@@ -307,7 +307,7 @@ hipError_t launch_node_probe(double* sink, int blocks, int iters, hipStream_t s)
 // ---------------------------------------------------------------- evaluation passes
 EvalBufs eval_bufs(const EvalArgs& a) {
   return {a.packed, (const uint4*)a.pcut, a.hdp, a.meta, a.ids, a.sstart, a.out, a.ctr, a.ctr + kEvalCounters, a.deferred,
-          (unsigned long long*)a.skipped_ops, a.dtab};
+          a.vlist, (unsigned long long*)a.skipped_ops, a.dtab};
 }
 
 // Blocks of each evaluation kernel that fit the device at once.
