@@ -1677,7 +1677,7 @@ struct EvalBufs {
 // of the wavefront's LDS exchange area, then every lane of the plan reads
 // the whole row.  Every lane of the plan takes part, deferred ones included
 // (the syncs do not depend on the recurrence).
-template <int S, int kMode>
+template <int S, int kMode, bool kHier>
 __device__ __forceinline__ double grouped_tail(const Tab& t, const Hot<kMode>& h, const Plan& p, const double (&last)[S],
                                                double* xw) {
   const uint32_t G = p.G, lane = threadIdx.x & 63u;
@@ -1685,7 +1685,7 @@ __device__ __forceinline__ double grouped_tail(const Tab& t, const Hot<kMode>& h
   const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> p.epl);
   for (uint32_t s = p.c; s < (uint32_t)S; s += G) {
     const uint32_t lo = s ? cut_at(p, s - 1) : 0;
-    x[s] = (double)stage_dp<kMode, false>(t, h, p, s, cut_at(p, s) - lo, rp, rpe);
+    x[s] = (double)stage_dp<kMode, kHier>(t, h, p, s, cut_at(p, s) - lo, rp, rpe);
   }
   // the rows are written and read by the lanes of one wavefront, whose LDS
   // accesses complete in order; the fences keep the compiler from moving
@@ -1707,8 +1707,9 @@ __device__ __forceinline__ double grouped_tail(const Tab& t, const Hot<kMode>& h
 template <int S, bool kFull, int kMode, bool kHet, bool kOvl = false, bool kZb = false>
 __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot,
                                          double* xw = nullptr) {
-  // plan-sorted pipelines: this pass, shared layout, no variant
-  constexpr bool kGrouped = !kFull && !kHet && !kOvl && !kZb;
+  // plan-sorted pipelines of the first or the variant pass (shared layout;
+  // the overlap's tail is per class)
+  constexpr bool kGrouped = !kFull && !kHet && !kOvl;
   typename std::conditional<kZb, ZbSink<S>, RegSink<S>>::type r;
   uint32_t M;
   const Plan p = load_plan<kHet>(e.packed, e.pcut, slot);
@@ -1754,7 +1755,7 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
   double T;
   const Plan p2 = S <= kKeepPlanS ? p : load_plan<kHet>(e.packed, e.pcut, slot2);
   if (kGrouped && p2.G > 1) {   // G is the same in the whole wavefront
-    T = grouped_tail<S, kMode>(t, h, p2, last, xw);
+    T = grouped_tail<S, kMode, kZb>(t, h, p2, last, xw);
   } else {
     T = done ? dp_tail<S, kMode, kHet, kOvl, kFull || kOvl || kZb>(t, h, p2, last,
                                                                    kHet ? e.hdp + (size_t)slot2 * kMaxStages : nullptr)
@@ -1788,8 +1789,9 @@ __device__ __forceinline__ void eval_deferred(const Tab& t, const Hot<kMode>& h,
 // after the budget go to the deferred lists (the deferred pass runs them
 // through the whole loop).
 template <int S, int kMode>
-__device__ __forceinline__ void eval_variant(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot) {
-  if ((e.packed[slot >> 2].hdr >> 16) & 1) eval_one<S, false, kMode, false, false, true>(t, h, e, slot);
+__device__ __forceinline__ void eval_variant(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot,
+                                             double* xw) {
+  if ((e.packed[slot >> 2].hdr >> 16) & 1) eval_one<S, false, kMode, false, false, true>(t, h, e, slot, xw);
   else eval_one<S, false, kMode, false, true>(t, h, e, slot);
 }
 
@@ -2186,6 +2188,8 @@ __global__ void __launch_bounds__(kEvalThreads) k_variant(const Tab* __restrict_
   fill_lds<kMode>(t, lds);
   const Hot<kMode> h(t, lds);
   const uint32_t waves = gridDim.x * wpb;
+  // the wavefront's row of the zero-bubble plans' DP exchange area (as k_eval's)
+  double* xw = (double*)((char*)lds + (kMode < 2 ? t.lds_bytes : 0)) + (threadIdx.x >> 6) * (kXchgPlans * kTop);
   for (uint32_t q = blockIdx.x * wpb + (threadIdx.x >> 6); q < tiles; q += waves) {
     const uint32_t j = (q >= q1) + (q >= q2) + (q >= q3);
     const uint32_t first = j == 0 ? 0 : j == 1 ? q1 : j == 2 ? q2 : q3;
@@ -2195,10 +2199,10 @@ __global__ void __launch_bounds__(kEvalThreads) k_variant(const Tab* __restrict_
     const uint32_t S = kTop - j;
     const uint32_t slot = e.vlist[e.sstart[kMaxStages - S] + off];
     if (slot == kNoSlot) continue;
-    if (j == 0) eval_variant<kTop, kMode>(t, h, e, slot);
-    else if (j == 1) eval_variant<kTop - 1, kMode>(t, h, e, slot);
-    else if (j == 2) eval_variant<kTop - 2, kMode>(t, h, e, slot);
-    else eval_variant<kTop - 3, kMode>(t, h, e, slot);
+    if (j == 0) eval_variant<kTop, kMode>(t, h, e, slot, xw);
+    else if (j == 1) eval_variant<kTop - 1, kMode>(t, h, e, slot, xw);
+    else if (j == 2) eval_variant<kTop - 2, kMode>(t, h, e, slot, xw);
+    else eval_variant<kTop - 3, kMode>(t, h, e, slot, xw);
   }
 }
 

@@ -55,7 +55,7 @@ template <int kMode>
 hipError_t launch_variant_v(const Tab& t, const EvalArgs& a, int g, hipStream_t s) {
   const EvalBufs e = eval_bufs(a);
   const uint32_t grid = t.grid_variant[g];
-  const size_t lds = kMode < 2 ? t.lds_bytes : 0;
+  const size_t lds = (kMode < 2 ? t.lds_bytes : 0) + xchg_bytes(g);
   if (g == 0) k_variant<0, kMode><<<grid, kEvalThreads, lds, s>>>(e.dtab, e);
   else if (g == 1) k_variant<1, kMode><<<grid, kEvalThreads, lds, s>>>(e.dtab, e);
   else if (g == 2) k_variant<2, kMode><<<grid, kEvalThreads, lds, s>>>(e.dtab, e);
