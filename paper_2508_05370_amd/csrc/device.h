@@ -764,11 +764,18 @@ __device__ __forceinline__ uint64_t stage_dp(const Tab& t, const Hot<kMode>& h, 
 // r_j = end - R_j (R_j: backward compute of the buckets after it), so the
 // queue completes at end + max_j (D_j - R_j) (D_j: syncs of bucket j and
 // the later ones); that tail is returned, walked from the last bucket.
-template <int kMode, bool kHier = true>
-__device__ __forceinline__ uint64_t overlap_tail(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t s,
-                                                 uint32_t lo, uint32_t hi, uint32_t k, double rp, double rpe) {
-  if (p.psum <= 1) return 0;
-  const uint32_t tpl = p.tpl, epl = p.epl, mi = p.mi;
+// The plan-level part of stage s's overlapped sync: the sync of one layer's
+// bucket (dl; every layer bucket of the stage has the same size) and, on
+// the first and last stages, of the embedding's and the head's buckets.
+struct OvlSyncs {
+  uint64_t dl, demb, dhead;
+};
+template <int kMode, bool kHier>
+__device__ __forceinline__ OvlSyncs overlap_syncs(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t s,
+                                                  double rp, double rpe) {
+  OvlSyncs r = {0, 0, 0};
+  if (p.psum <= 1) return r;
+  const uint32_t tpl = p.tpl, epl = p.epl;
   uint64_t alpha;
   uint32_t bq;
   HierShape hs;
@@ -779,28 +786,49 @@ __device__ __forceinline__ uint64_t overlap_tail(const Tab& t, const Hot<kMode>&
   const uint32_t pe = p.psum >> epl;
   if (t.E && pe > 1)
     dl += ring_sync(pe, rpe, p.zero, gb * t.par_expert[tpl][epl], pb * t.par_expert[tpl][epl], alpha, bq, t.ccl_tree);
-  const uint32_t L1 = t.L + 1, epq = t.E ? epl : 0;
+  r.dl = dl;
+  if (s == 0)
+    r.demb = with_hier(
+        ring_sync(p.psum, rp, p.zero, gb * t.par_embed[tpl], pb * t.par_embed[tpl], alpha, bq, t.ccl_tree), hs, p.zero,
+        gb * t.par_embed[tpl], alpha, bq);
+  if (s == p.S - 1)
+    r.dhead = with_hier(
+        ring_sync(p.psum, rp, p.zero, gb * t.par_head[tpl], pb * t.par_head[tpl], alpha, bq, t.ccl_tree), hs, p.zero,
+        gb * t.par_head[tpl], alpha, bq);
+  return r;
+}
+
+// The class's part: its buckets' readiness from its own backward compute on
+// device type k, walked against the syncs.
+template <int kMode>
+__device__ __forceinline__ uint64_t overlap_walk(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t s,
+                                                 uint32_t lo, uint32_t hi, uint32_t k, const OvlSyncs& y) {
+  if (p.psum <= 1) return 0;
+  const uint32_t tpl = p.tpl, mi = p.mi;
+  const uint32_t L1 = t.L + 1, epq = t.E ? p.epl : 0;
   const uint32_t row = ((k * 4 + tpl) * t.n_mbs + mi) * t.nep + epq;
   int64_t D = 0, R = 0, X = 0;
   if (s == 0) {
-    D += (int64_t)with_hier(
-        ring_sync(p.psum, rp, p.zero, gb * t.par_embed[tpl], pb * t.par_embed[tpl], alpha, bq, t.ccl_tree), hs, p.zero,
-        gb * t.par_embed[tpl], alpha, bq);
+    D += (int64_t)y.demb;
     X = D;
     R += (int64_t)h.emb(k * t.n_mbs + mi).y;
   }
   for (uint32_t l = lo; l < hi; ++l) {
-    D += (int64_t)dl;
+    D += (int64_t)y.dl;
     X = D - R > X ? D - R : X;
     R += (int64_t)(t.uniform_layers ? h.pfb(row).y : h.pfb(row * L1 + l + 1).y - h.pfb(row * L1 + l).y);
   }
   if (s == p.S - 1) {
-    D += (int64_t)with_hier(
-        ring_sync(p.psum, rp, p.zero, gb * t.par_head[tpl], pb * t.par_head[tpl], alpha, bq, t.ccl_tree), hs, p.zero,
-        gb * t.par_head[tpl], alpha, bq);
+    D += (int64_t)y.dhead;
     X = D - R > X ? D - R : X;
   }
   return (uint64_t)X;
+}
+
+template <int kMode, bool kHier = true>
+__device__ __forceinline__ uint64_t overlap_tail(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t s,
+                                                 uint32_t lo, uint32_t hi, uint32_t k, double rp, double rpe) {
+  return overlap_walk<kMode>(t, h, p, s, lo, hi, k, overlap_syncs<kMode, kHier>(t, h, p, s, rp, rpe));
 }
 
 // The sync that follows stage s of the pipeline's class (shared layout):
@@ -1704,12 +1732,47 @@ __device__ __forceinline__ double grouped_tail(const Tab& t, const Hot<kMode>& h
   return T;
 }
 
+// The same for an overlapped plan (variant pass): the lane of class c costs
+// the syncs of stages c, c + G, ... (one layer's bucket per stage, the
+// embedding's and the head's) into its plan's row, then every lane walks its
+// own buckets' readiness against them.
+template <int S, int kMode>
+__device__ __forceinline__ double grouped_overlap_tail(const Tab& t, const Hot<kMode>& h, const Plan& p,
+                                                       double (&last)[S], double* xw) {
+  const uint32_t G = p.G, lane = threadIdx.x & 63u;
+  double* x = xw + (lane / G) * xchg_row(S);
+  const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> p.epl);
+  for (uint32_t s = p.c; s < (uint32_t)S; s += G) {
+    const OvlSyncs y = overlap_syncs<kMode, true>(t, h, p, s, rp, rpe);
+    x[s] = (double)y.dl;
+    if (s == 0) x[xchg_row(S) - 2] = (double)y.demb;
+    if (s == (uint32_t)S - 1) x[xchg_row(S) - 1] = (double)y.dhead;
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  const OvlSyncs ends = {0, (uint64_t)x[xchg_row(S) - 2], (uint64_t)x[xchg_row(S) - 1]};
+  double T = 0;
+  uint32_t lo = 0;
+  for (uint32_t s = 0; s < (uint32_t)S; ++s) {
+    const uint32_t hi = cut_at(p, s);
+    const OvlSyncs y = {(uint64_t)x[s], ends.demb, ends.dhead};
+    const double e = last[0] + (double)overlap_walk<kMode>(t, h, p, s, lo, hi, (uint32_t)(p.tc >> (4 * s)) & 15, y);
+    T = e > T ? e : T;
+#pragma unroll
+    for (int i = 0; i + 1 < S; ++i) last[i] = last[i + 1];
+    lo = hi;
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  return T;
+}
+
 template <int S, bool kFull, int kMode, bool kHet, bool kOvl = false, bool kZb = false>
 __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot,
                                          double* xw = nullptr) {
-  // plan-sorted pipelines of the first or the variant pass (shared layout;
-  // the overlap's tail is per class)
-  constexpr bool kGrouped = !kFull && !kHet && !kOvl;
+  // plan-sorted pipelines of the first or the variant pass (shared layout)
+  constexpr bool kGrouped = !kFull && !kHet;
   typename std::conditional<kZb, ZbSink<S>, RegSink<S>>::type r;
   uint32_t M;
   const Plan p = load_plan<kHet>(e.packed, e.pcut, slot);
@@ -1755,7 +1818,8 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
   double T;
   const Plan p2 = S <= kKeepPlanS ? p : load_plan<kHet>(e.packed, e.pcut, slot2);
   if (kGrouped && p2.G > 1) {   // G is the same in the whole wavefront
-    T = grouped_tail<S, kMode, kZb>(t, h, p2, last, xw);
+    if constexpr (kOvl) T = grouped_overlap_tail<S, kMode>(t, h, p2, last, xw);
+    else T = grouped_tail<S, kMode, kZb>(t, h, p2, last, xw);
   } else {
     T = done ? dp_tail<S, kMode, kHet, kOvl, kFull || kOvl || kZb>(t, h, p2, last,
                                                                    kHet ? e.hdp + (size_t)slot2 * kMaxStages : nullptr)
@@ -1792,7 +1856,7 @@ template <int S, int kMode>
 __device__ __forceinline__ void eval_variant(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot,
                                              double* xw) {
   if ((e.packed[slot >> 2].hdr >> 16) & 1) eval_one<S, false, kMode, false, false, true>(t, h, e, slot, xw);
-  else eval_one<S, false, kMode, false, true>(t, h, e, slot);
+  else eval_one<S, false, kMode, false, true>(t, h, e, slot, xw);
 }
 
 // ---------------------------------------------------------------- interleaved 1F1B
@@ -2059,7 +2123,7 @@ __global__ void __launch_bounds__(kEvalThreads) k_eval(Tab t, EvalBufs e) {
   // the wavefront's row of the plan-sorted groups' LDS exchange area
   double* xw = nullptr;
   if constexpr (!kHet)
-    xw = (double*)((char*)lds + (kMode < 2 ? t.lds_bytes : 0)) + (threadIdx.x >> 6) * (kXchgPlans * kTop);
+    xw = (double*)((char*)lds + (kMode < 2 ? t.lds_bytes : 0)) + (threadIdx.x >> 6) * xchg_wave(GRP);
   for (uint32_t base = lo + blockIdx.x * kEvalThreads + (threadIdx.x & ~63u); base < hi; base += stride) {
     const uint32_t pos = base + (threadIdx.x & 63u);
     bool pending = pos < hi;
@@ -2189,7 +2253,7 @@ __global__ void __launch_bounds__(kEvalThreads) k_variant(const Tab* __restrict_
   const Hot<kMode> h(t, lds);
   const uint32_t waves = gridDim.x * wpb;
   // the wavefront's row of the zero-bubble plans' DP exchange area (as k_eval's)
-  double* xw = (double*)((char*)lds + (kMode < 2 ? t.lds_bytes : 0)) + (threadIdx.x >> 6) * (kXchgPlans * kTop);
+  double* xw = (double*)((char*)lds + (kMode < 2 ? t.lds_bytes : 0)) + (threadIdx.x >> 6) * xchg_wave(GRP);
   for (uint32_t q = blockIdx.x * wpb + (threadIdx.x >> 6); q < tiles; q += waves) {
     const uint32_t j = (q >= q1) + (q >= q2) + (q >= q3);
     const uint32_t first = j == 0 ? 0 : j == 1 ? q1 : j == 2 ? q2 : q3;

@@ -35,12 +35,15 @@ constexpr uint32_t kSuperBuckets = kMaxStages * kMaxClasses;
 constexpr uint32_t kGroupPad = 64 * kSuperBuckets;
 constexpr uint32_t kNoSlot = 0xffffffffu;
 __host__ __device__ constexpr uint32_t plans_per_wave(uint32_t G) { return G == 3 ? 21 : 64 / G; }
-// LDS of the first pass over plan-sorted pipelines: per wavefront, a row of
-// DP syncs for each of up to 32 plans (one per stage of the kernel's largest
-// stage count), exchanged between the lanes of each plan
+// LDS of the first and variant passes over plan-sorted pipelines: per
+// wavefront, a row of DP syncs for each of up to 32 plans (one per stage of
+// the kernel's largest stage count, and two more for the embedding's and the
+// head's buckets of an overlapped sync), exchanged between the lanes of each
+// plan
 constexpr uint32_t kXchgPlans = 32;
-__host__ __device__ constexpr uint32_t xchg_row(uint32_t S) { return (S + 3) / 4 * 4; }
-__host__ __device__ constexpr uint32_t xchg_bytes(int group) { return 4 * kXchgPlans * (kMaxStages - 4 * group) * 8; }
+__host__ __device__ constexpr uint32_t xchg_row(uint32_t S) { return (S + 3) / 4 * 4 + 2; }
+__host__ __device__ constexpr uint32_t xchg_wave(int group) { return kXchgPlans * xchg_row(kMaxStages - 4 * group); }
+__host__ __device__ constexpr uint32_t xchg_bytes(int group) { return 4 * xchg_wave(group) * 8; }
 
 // A validated plan packed into 80 contiguous bytes, so that the pipelines of
 // one plan gather it with five 16-byte loads.
