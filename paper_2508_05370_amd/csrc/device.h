@@ -813,10 +813,22 @@ __device__ __forceinline__ uint64_t overlap_walk(const Tab& t, const Hot<kMode>&
     X = D;
     R += (int64_t)h.emb(k * t.n_mbs + mi).y;
   }
-  for (uint32_t l = lo; l < hi; ++l) {
-    D += (int64_t)y.dl;
-    X = D - R > X ? D - R : X;
-    R += (int64_t)(t.uniform_layers ? h.pfb(row).y : h.pfb(row * L1 + l + 1).y - h.pfb(row * L1 + l).y);
+  if (t.uniform_layers) {
+    // every layer's backward costs the same r: after layer i of the n the
+    // value D - R is (D + dl - R) + i (dl - r), linear in i, so its largest
+    // is at the first or the last layer
+    const int64_t n = (int64_t)(hi - lo), dl = (int64_t)y.dl, r = (int64_t)h.pfb(row).y;
+    const int64_t v0 = D + dl - R, v1 = v0 + (n - 1) * (dl - r);
+    X = v0 > X ? v0 : X;
+    X = v1 > X ? v1 : X;
+    D += n * dl;
+    R += n * r;
+  } else {
+    for (uint32_t l = lo; l < hi; ++l) {
+      D += (int64_t)y.dl;
+      X = D - R > X ? D - R : X;
+      R += (int64_t)(h.pfb(row * L1 + l + 1).y - h.pfb(row * L1 + l).y);
+    }
   }
   if (s == p.S - 1) {
     D += (int64_t)y.dhead;
