@@ -2220,7 +2220,7 @@ __global__ void __launch_bounds__(kEvalThreads) k_deferred(const Tab* __restrict
     if (j == kMaxStages) return;
     const uint32_t off = (q - before) * 64u + (threadIdx.x & 63u);
     if (off >= e.ctr[1 + j]) continue;
-    const uint32_t slot = e.deferred[e.sstart[j] + off];
+    const uint32_t slot = e.vlist[e.sstart[j] + off];   // the deferred list, sorted
     switch (kMaxStages - j) {
       case 1: eval_deferred<1, kMode, kHet>(t, h, e, slot); break;
       case 2: eval_deferred<2, kMode, kHet>(t, h, e, slot); break;

@@ -131,8 +131,14 @@ struct Tab {
 // tiles of the variant pass (64 per tile); the overflow list follows the counters at
 // ctr + kEvalCounters.
 constexpr uint32_t kVariantCtr = 1 + kMaxStages;
-constexpr uint32_t kEvalCounters = 48;
-static_assert(kVariantCtr + kMaxStages <= kEvalCounters, "evaluation counters");
+// The deferred lists are sorted by micro-batch count before the deferred
+// pass (longest first, kSortBuckets buckets per stage count): their counts
+// at ctr[kSortCtr + 32 j + b], cursors at ctr[kSortCtr + 512 + 32 j + b] for
+// the list of 16 - j stages.
+constexpr uint32_t kSortBuckets = 32;
+constexpr uint32_t kSortCtr = 48;
+constexpr uint32_t kEvalCounters = kSortCtr + 2 * kMaxStages * kSortBuckets;
+static_assert(kVariantCtr + kMaxStages <= kSortCtr, "evaluation counters");
 // The skipped-work counter is spread over slots on separate cache lines so
 // that the waves of a launch do not serialise on one address.
 constexpr uint32_t kSkipSlots = 512, kSkipStride = 16;

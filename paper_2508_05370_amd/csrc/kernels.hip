@@ -156,6 +156,76 @@ __global__ void __launch_bounds__(256) k_scatter(const uint16_t* __restrict__ ke
   }
 }
 
+// ---------------------------------------------------------------- deferred lists
+// Counting sort of the deferred lists by micro-batch count (bucket
+// min(31, M / 16), largest first) into vlist, which the variant pass has
+// finished with: the deferred pass then runs wavefronts of similar trip
+// counts rather than waiting in every wavefront for its longest chain.
+__device__ __forceinline__ uint32_t defer_bucket(uint32_t meta) {
+  const uint32_t M = (meta >> 8) & 0xffff, b = M >> 4;
+  return b < kSortBuckets - 1 ? b : kSortBuckets - 1;
+}
+// entry idx of the concatenated lists -> (list j, position k in it)
+__device__ __forceinline__ bool defer_entry(const EvalBufs& e, uint32_t idx, uint32_t& j, uint32_t& k) {
+  uint32_t before = 0;
+  for (j = 0; j < (uint32_t)kMaxStages; ++j) {
+    const uint32_t n = e.ctr[1 + j];
+    if (idx < before + n) {
+      k = idx - before;
+      return true;
+    }
+    before += n;
+  }
+  return false;
+}
+__global__ void __launch_bounds__(256) k_defer_hist(EvalBufs e) {
+  __shared__ uint32_t hs[kMaxStages * kSortBuckets];
+  for (uint32_t i = threadIdx.x; i < kMaxStages * kSortBuckets; i += blockDim.x) hs[i] = 0;
+  __syncthreads();
+  uint32_t total = 0;
+  for (uint32_t j = 0; j < (uint32_t)kMaxStages; ++j) total += e.ctr[1 + j];
+  for (uint32_t idx = blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += gridDim.x * blockDim.x) {
+    uint32_t j, k;
+    if (!defer_entry(e, idx, j, k)) break;
+    atomicAdd(&hs[j * kSortBuckets + defer_bucket(e.meta[e.deferred[e.sstart[j] + k]])], 1u);
+  }
+  __syncthreads();
+  for (uint32_t i = threadIdx.x; i < kMaxStages * kSortBuckets; i += blockDim.x)
+    if (hs[i]) atomicAdd(&e.ctr[kSortCtr + i], hs[i]);
+}
+__global__ void __launch_bounds__(256) k_defer_sort(EvalBufs e) {
+  constexpr uint32_t kN = kMaxStages * kSortBuckets;
+  __shared__ uint32_t base[kN], lc[kN];
+  if (threadIdx.x < (uint32_t)kMaxStages) {   // list j's buckets, largest micro-batch counts first
+    uint32_t run = 0;
+    for (int b = kSortBuckets - 1; b >= 0; --b) {
+      base[threadIdx.x * kSortBuckets + b] = run;
+      run += e.ctr[kSortCtr + threadIdx.x * kSortBuckets + b];
+    }
+  }
+  uint32_t total = 0;
+  for (uint32_t j = 0; j < (uint32_t)kMaxStages; ++j) total += e.ctr[1 + j];
+  // one entry per thread per round; ranks within the block from LDS counters,
+  // then one global cursor update per (round, bucket)
+  for (uint32_t r0 = blockIdx.x * blockDim.x; r0 < total; r0 += gridDim.x * blockDim.x) {
+    for (uint32_t i = threadIdx.x; i < kN; i += blockDim.x) lc[i] = 0;
+    __syncthreads();
+    uint32_t j = 0, k = 0, slot = 0, b = 0, rank = 0;
+    const bool has = r0 + threadIdx.x < total && defer_entry(e, r0 + threadIdx.x, j, k);
+    if (has) {
+      slot = e.deferred[e.sstart[j] + k];
+      b = j * kSortBuckets + defer_bucket(e.meta[slot]);
+      rank = atomicAdd(&lc[b], 1u);
+    }
+    __syncthreads();
+    for (uint32_t i = threadIdx.x; i < kN; i += blockDim.x)
+      if (lc[i]) lc[i] = atomicAdd(&e.ctr[kSortCtr + kN + i], lc[i]);
+    __syncthreads();
+    if (has) e.vlist[e.sstart[j] + base[b] + lc[b] + rank] = slot;
+    __syncthreads();
+  }
+}
+
 // ---------------------------------------------------------------- argmin
 __global__ void k_best_init(sim_best* b) {
   b->time_ps = kInvalid;
@@ -369,6 +439,13 @@ hipError_t launch_first(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hip
 hipError_t launch_deferred(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s) {
   const bool het = a.pcut != nullptr;
   hipError_t r;
+  {
+    // the deferred lists, sorted by micro-batch count into vlist
+    const EvalBufs e = eval_bufs(a);
+    k_defer_hist<<<64, 256, 0, s>>>(e);
+    k_defer_sort<<<64, 256, 0, s>>>(e);
+    if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;
+  }
   if (t.mode == 0) r = het ? launch_deferred_v<0, true>(t, a, max_tasks, s) : launch_deferred_v<0, false>(t, a, max_tasks, s);
   else if (t.mode == 1) r = het ? launch_deferred_v<1, true>(t, a, max_tasks, s) : launch_deferred_v<1, false>(t, a, max_tasks, s);
   else r = het ? launch_deferred_v<2, true>(t, a, max_tasks, s) : launch_deferred_v<2, false>(t, a, max_tasks, s);
