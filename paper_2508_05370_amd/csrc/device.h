@@ -1461,7 +1461,7 @@ __device__ __forceinline__ uint64_t vmax(uint64_t a, uint64_t b) { return a > b 
 // micro-batches.  A wave waits at most kPeriodicBudget steady iterations for
 // its lanes; a lane still aperiodic by then is deferred to a full-loop pass,
 // so one aperiodic schedule does not hold 63 periodic ones.
-constexpr int kPeriodicBudget = 48;
+constexpr int kPeriodicBudget = 40;
 
 template <int S, typename V>
 __device__ __forceinline__ void steady_iter(const V (&f)[S], const V (&b)[S], const V (&c)[S], V (&out_f)[S],
