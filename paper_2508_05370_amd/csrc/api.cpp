@@ -20,7 +20,7 @@ hipError_t launch_plan_syncs(const Tab& t, const PackedPlan* packed, const uint4
 hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint4* pcut, const uint32_t* meta, int64_t n,
                          uint64_t* out_stage, hipStream_t s);
 hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* sstart, uint32_t* sbase, bool grouped,
-                       hipStream_t s);
+                       uint32_t* ids, hipStream_t s);
 hipError_t launch_scatter(const uint16_t* keys, uint32_t nslots, uint32_t* cursor, const uint32_t* sbase, bool grouped,
                           uint32_t* ids, hipStream_t s);
 hipError_t launch_first(const Tab& t, const EvalArgs& a, uint32_t max_tasks, hipStream_t s);
@@ -290,11 +290,9 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
     if (e == hipSuccess) e = launch_prep(c->tab, p, cn, out + off, W.packed, W.pcut, W.meta, W.hist, W.keys, s);
     if (t1) end_event(c, 1, s, &ev);
     if (e == hipSuccess && het) e = launch_plan_syncs(c->tab, W.packed, W.pcut, W.meta, cn, W.hdp, s);
-    // shared-layout calls sort plans by plan, leaving padding lanes; the
-    // variant tiles start empty
-    if (e == hipSuccess && !het) e = launch_fill32(W.ids, (uint32_t)id_words(cn), kNoSlot, s);
-    if (e == hipSuccess && !het) e = launch_fill32(W.vlist, (uint32_t)id_words(cn), kNoSlot, s);
-    if (e == hipSuccess) e = launch_scan(W.hist, W.cursor, W.sstart, W.sbase, !het, s);
+    // shared-layout calls sort plans by plan: the scan and the scatter mark
+    // the padding lanes
+    if (e == hipSuccess) e = launch_scan(W.hist, W.cursor, W.sstart, W.sbase, !het, W.ids, s);
     if (e == hipSuccess) e = launch_scatter(W.keys, (uint32_t)(cn * 4), W.cursor, W.sbase, !het, W.ids, s);
     const EvalArgs a = {W.packed, W.pcut, W.hdp, W.meta, W.ids, W.sstart, out + off, W.ctr, W.deferred, W.vlist,
                         c->timing ? c->skipped_ops : nullptr, c->dtab};
@@ -365,9 +363,7 @@ extern "C" int sim_eval_plans_noalloc(sim_ctx* c, const sim_plans* plans, int64_
   hipError_t e = launch_fill32(W.hist, kCounters, 0, s);
   if (e == hipSuccess) e = launch_prep(c->tab, *plans, n, out, W.packed, W.pcut, W.meta, W.hist, W.keys, s);
   if (e == hipSuccess && het) e = launch_plan_syncs(c->tab, W.packed, W.pcut, W.meta, n, W.hdp, s);
-  if (e == hipSuccess && !het) e = launch_fill32(W.ids, (uint32_t)id_words(n), kNoSlot, s);
-  if (e == hipSuccess && !het) e = launch_fill32(W.vlist, (uint32_t)id_words(n), kNoSlot, s);
-  if (e == hipSuccess) e = launch_scan(W.hist, W.cursor, W.sstart, W.sbase, !het, s);
+  if (e == hipSuccess) e = launch_scan(W.hist, W.cursor, W.sstart, W.sbase, !het, W.ids, s);
   if (e == hipSuccess) e = launch_scatter(W.keys, (uint32_t)(n * 4), W.cursor, W.sbase, !het, W.ids, s);
   const EvalArgs a = {W.packed, W.pcut, W.hdp, W.meta, W.ids, W.sstart, out, W.ctr, W.deferred, W.vlist,
                       c->timing ? c->skipped_ops : nullptr, c->dtab};

@@ -460,7 +460,8 @@ __device__ __forceinline__ bool fits_memory(const Tab& t, const Checked& r) {
 // class's cut row to pcut[4 i + c]).  Writes out[i] (0 = valid, to be raised
 // by the pipelines; else invalid) and the per-pipeline metadata
 // S | G << 5 | M << 8 | (v - 1) << 24 with the class's own S (0 = no pipeline),
-// and (keys, when given) each pipeline's bucket (kNoKey = no pipeline).
+// and (keys, when given) each pipeline's bucket (kNoKey = no pipeline); with
+// keys, valid plans sorted by plan get no metadata.
 template <bool kHet>
 __global__ void __launch_bounds__(256) k_prep(Tab t, sim_plans pl, int64_t n, uint64_t* __restrict__ out,
                                               PackedPlan* __restrict__ packed, uint4* __restrict__ pcut,
@@ -513,12 +514,16 @@ __global__ void __launch_bounds__(256) k_prep(Tab t, sim_plans pl, int64_t n, ui
       }
     }
     // one 16-byte and one 8-byte store per plan (the workspace is 256-byte
-    // aligned; a caller's class array may be aligned to 4 bytes only)
-    if (((uintptr_t)meta & 15) == 0) {
-      reinterpret_cast<uint4*>(meta)[i] = make_uint4(m[0], m[1], m[2], m[3]);
-    } else {
+    // aligned; a caller's class array may be aligned to 4 bytes only).  An
+    // evaluation call (keys given) reads no metadata of the plans it sorts by
+    // plan: only its other pipelines get it
+    if (!keys || !by_plan) {
+      if (((uintptr_t)meta & 15) == 0) {
+        reinterpret_cast<uint4*>(meta)[i] = make_uint4(m[0], m[1], m[2], m[3]);
+      } else {
 #pragma unroll
-      for (int c = 0; c < 4; ++c) meta[i * 4 + c] = m[c];
+        for (int c = 0; c < 4; ++c) meta[i * 4 + c] = m[c];
+      }
     }
     if (keys) reinterpret_cast<uint2*>(keys)[i] = make_uint2(key[0] | key[1] << 16, key[2] | key[3] << 16);
   }
@@ -1224,12 +1229,14 @@ __device__ __forceinline__ uint64_t rail_extra(uint32_t n, const TypeInfo& ts, u
 template <int kMode, bool kHet, typename Sink>
 __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t c,
                                             Sink& sink, const uint4* prow) {
-  const uint32_t S = p.S, tp = p.tp, epl = p.epl;
+  // register sinks fix the stage count at compile time (the plan's S equals it)
+  const uint32_t S = Sink::kS ? (uint32_t)Sink::kS : p.S, tp = p.tp, epl = p.epl;
   const uint64_t act = t.act[p.mi];
   const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> epl);
   const uint32_t reps = p.rc;
   uint32_t pk = 0, pbase = 0, pnic = 0, pin = 0, lo = 0;
   TypeInfo pti = {};
+#pragma unroll Sink::kUnroll
   for (uint32_t s = 0; s < S; ++s) {
     const uint32_t hi = cut_at(p, s);
     // ---- this class: compute, TP, EP, hop from the previous stage
@@ -1277,6 +1284,7 @@ __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, c
 // weight-gradient pass.
 struct RecSink {
   static constexpr bool kDp = true;
+  static constexpr int kS = 0, kUnroll = 1;   // stage count taken from the plan
   uint64_t (&rec)[kMaxStages][kRecWords];
   uint64_t* w = nullptr;
   __device__ __forceinline__ void put(uint32_t s, uint64_t fc, uint64_t bc, uint64_t wc, uint64_t hop,
@@ -1294,10 +1302,16 @@ struct RecSink {
 // registers as fp64 (every stage quantity is below 2^52, so exact): each
 // stage shifts the arrays down by one and appends, so after S stages stage s
 // sits at index s; a runtime-indexed array would go through private memory.
-// The DP sync is left to dp_tail, after the recurrence.
+// The stage loop runs S (a compile-time count) times, unrolled by
+// kSetupUnroll: within an unrolled body the shifts are register renames, so
+// the copies are paid once per kSetupUnroll stages.  The DP sync is left to
+// dp_tail, after the recurrence.
+constexpr int kSetupUnroll = 4;
+
 template <int S>
 struct RegSink {
   static constexpr bool kDp = false;
+  static constexpr int kS = S, kUnroll = kSetupUnroll;
   double f[S], b[S], c[S];
   __device__ __forceinline__ RegSink() {
 #pragma unroll
@@ -1322,6 +1336,7 @@ struct RegSink {
 template <int S>
 struct ZbSink {
   static constexpr bool kDp = false;
+  static constexpr int kS = S, kUnroll = kSetupUnroll;
   double f[S], bi[S], w[S], c[S];
   __device__ __forceinline__ ZbSink() {
 #pragma unroll
@@ -1790,21 +1805,7 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
   const Plan p = load_plan<kHet>(e.packed, e.pcut, slot);
   {
     if (!kFull && !kHet && !kOvl && !kZb) {
-      // overlap and zero-bubble plans go to the variant pass: the wavefront
-      // takes one 64-slot tile and puts them on the lanes they hold here, so
-      // that the tile keeps its plans' lanes together; the first active lane
-      // takes the tile and the same lane's value is broadcast
-      const bool var = p.overlap | p.zb;
-      if (__ballot(var)) {
-        uint32_t tile = 0;
-        if (threadIdx.x % 64u == (uint32_t)(__ffsll((unsigned long long)__ballot(1)) - 1))
-          tile = atomicAdd(&e.ctr[kVariantCtr + kMaxStages - S], 64u);
-        tile = __builtin_amdgcn_readfirstlane(tile);
-        if (var) {
-          e.vlist[e.sstart[kMaxStages - S] + tile + (threadIdx.x & 63u)] = slot;
-          return;
-        }
-      }
+      // (overlap and zero-bubble plans left for the variant pass in k_eval)
       if (t.ccl_hier) {
         e.deferred[e.sstart[kMaxStages - S] + atomicAdd(&e.ctr[1 + kMaxStages - S], 1u)] = slot;
         return;
@@ -1837,14 +1838,34 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
                                                                    kHet ? e.hdp + (size_t)slot2 * kMaxStages : nullptr)
              : 0;
   }
-  if (!done) {
-    e.deferred[e.sstart[kMaxStages - S] + atomicAdd(&e.ctr[1 + kMaxStages - S], 1u)] = slot;
-    return;
-  }
-  if (T < kExact) {
-    atomicMax((unsigned long long*)&e.out[slot >> 2], (unsigned long long)T);
+  if constexpr (kGrouped) {
+    // the plan's G pipelines sit on adjacent lanes from a multiple of G, all
+    // of them here: the first one stores the largest result of the finished
+    // ones (one store per plan; the deferred and the u64 passes, later in
+    // stream order, raise it with atomicMax)
+    const uint32_t G = p2.G, lane = threadIdx.x & 63u, lead = lane - lane % G;
+    const bool mine = done && T < kExact;
+    double v = mine ? T : 0;
+    for (uint32_t c = 1; c < G; ++c) {
+      const double u = __shfl(v, (int)(lead + c));
+      if (lane == lead) v = u > v ? u : v;
+    }
+    if (lane == lead && v > 0) e.out[slot >> 2] = (uint64_t)v;
+    if (!done) {
+      e.deferred[e.sstart[kMaxStages - S] + atomicAdd(&e.ctr[1 + kMaxStages - S], 1u)] = slot;
+      return;
+    }
+    if (!mine) e.ovf[atomicAdd(&e.ctr[0], 1u)] = slot;
   } else {
-    e.ovf[atomicAdd(&e.ctr[0], 1u)] = slot;
+    if (!done) {
+      e.deferred[e.sstart[kMaxStages - S] + atomicAdd(&e.ctr[1 + kMaxStages - S], 1u)] = slot;
+      return;
+    }
+    if (T < kExact) {
+      atomicMax((unsigned long long*)&e.out[slot >> 2], (unsigned long long)T);
+    } else {
+      e.ovf[atomicAdd(&e.ctr[0], 1u)] = slot;
+    }
   }
   if (e.skipped_ops && skipped > 0)
     atomicAdd(e.skipped_ops + ((blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) % kSkipSlots) * kSkipStride,
@@ -2141,7 +2162,27 @@ __global__ void __launch_bounds__(kEvalThreads) k_eval(Tab t, EvalBufs e) {
     bool pending = pos < hi;
     const uint32_t slot = pending ? e.ids[pos] : 0;
     pending = pending && slot != kNoSlot;   // padding lanes of plan-sorted groups
-    const uint32_t S = !pending ? 0 : kHet ? e.meta[slot] & 31 : ((e.packed[slot >> 2].hdr >> 4) & 15) + 1;
+    const uint32_t hdr = !pending || kHet ? 0 : e.packed[slot >> 2].hdr;
+    const uint32_t S = !pending ? 0 : kHet ? e.meta[slot] & 31 : ((hdr >> 4) & 15) + 1;
+    if constexpr (!kHet) {
+      // overlap and zero-bubble plans go to the variant pass: the wavefront
+      // (one stage count: the plan-sorted groups are padded to whole
+      // wavefronts) takes one 64-slot tile and every lane writes its own
+      // position, the slot of an overlap or zero-bubble plan or kNoSlot, so
+      // that the tile keeps its plans' lanes together.  Every lane is active
+      // here; the lane that takes the tile is the one readfirstlane reads.
+      const bool var = pending && (((hdr >> 13) & 1) | ((hdr >> 16) & 1));
+      const uint64_t vb = __ballot(var);
+      if (vb) {
+        const uint32_t Sv = __builtin_amdgcn_readfirstlane(__shfl(S, __ffsll((unsigned long long)vb) - 1));
+        uint32_t tile = 0;
+        if ((threadIdx.x & 63u) == (uint32_t)(__ffsll((unsigned long long)__ballot(1)) - 1))
+          tile = atomicAdd(&e.ctr[kVariantCtr + kMaxStages - Sv], 64u);
+        tile = __builtin_amdgcn_readfirstlane(tile);
+        e.vlist[e.sstart[kMaxStages - Sv] + tile + (threadIdx.x & 63u)] = var ? slot : kNoSlot;
+        pending = pending && !var;
+      }
+    }
     // one pass per distinct stage count present in the wavefront (usually one)
     while (true) {
       const uint64_t live = __ballot(pending);

@@ -11,7 +11,7 @@
 
 namespace hetsim {
 
-static int pass_blocks(uint32_t n, uint32_t per) { return (int)((n + per - 1) / per); }
+[[maybe_unused]] static int pass_blocks(uint32_t n, uint32_t per) { return (int)((n + per - 1) / per); }
 
 #if HETSIM_PASS == 0
 template <int kMode, bool kHet>

@@ -56,7 +56,7 @@ __global__ void k_fill32(uint32_t* p, uint32_t n, uint32_t v) {
 // of the 64 groups' lane counts.
 __global__ void __launch_bounds__(1024) k_scan(const uint32_t* __restrict__ hist, uint32_t* __restrict__ cursor,
                                                uint32_t* __restrict__ sstart, uint32_t* __restrict__ sbase,
-                                               uint32_t grouped) {
+                                               uint32_t grouped, uint32_t* __restrict__ ids) {
   constexpr int kPer = kPlainBuckets / 1024;
   constexpr int kThreadsPerGroup = kBucketsM / kPer;
   static_assert(kPlainBuckets % 1024 == 0 && kBuckets - kPlainBuckets == 1024, "bucket count");
@@ -81,12 +81,13 @@ __global__ void __launch_bounds__(1024) k_scan(const uint32_t* __restrict__ hist
   const uint32_t grp = tid / kThreadsPerGroup, g0 = grp * kThreadsPerGroup;
   const uint32_t before_grp = g0 ? part[g0 - 1].x : 0;
   const bool by_plan = grouped != 0;
+  uint32_t ngrp = 0;
   if (tid < kSuperBuckets) {
     // lanes of group tid
     const uint32_t a = tid * kThreadsPerGroup;
-    const uint32_t n = part[a + kThreadsPerGroup - 1].x - (a ? part[a - 1].x : 0);
+    ngrp = part[a + kThreadsPerGroup - 1].x - (a ? part[a - 1].x : 0);
     const uint32_t pw = plans_per_wave(kMaxClasses - tid % kMaxClasses);
-    lanes[tid] = grouped ? (n + pw - 1) / pw * 64u : n;
+    lanes[tid] = grouped ? (ngrp + pw - 1) / pw * 64u : ngrp;
   }
   __syncthreads();
   if (tid == 0) {
@@ -100,6 +101,14 @@ __global__ void __launch_bounds__(1024) k_scan(const uint32_t* __restrict__ hist
   }
   __syncthreads();
   if (tid < kSuperBuckets) sbase[tid] = lanes[tid];
+  // a plan-sorted group's last wavefront, when partly filled: its lanes past
+  // the plans hold no pipeline (k_scatter marks the unused lanes of the full ones)
+  if (grouped && tid < kSuperBuckets) {
+    const uint32_t G = kMaxClasses - tid % kMaxClasses, pw = plans_per_wave(G), r = ngrp % pw;
+    const uint32_t w0 = lanes[tid] + ngrp / pw * 64u;
+    if (r)
+      for (uint32_t q = G * r; q < 64u; ++q) ids[w0 + q] = kNoSlot;
+  }
   // pipelines of S stages start at group (16 - S) * 4 (four classes first)
   if (tid < kMaxStages) sstart[tid] = lanes[tid * kMaxClasses];
   uint32_t run = part[tid].x - sum - before_grp;
@@ -114,7 +123,8 @@ __global__ void __launch_bounds__(1024) k_scan(const uint32_t* __restrict__ hist
 // Place every pipeline id at its bucket's next free lane.  A plain key of a
 // grouped call sits on the plan's class-0 slot and stands for the whole plan: the plan's rank r in its
 // group puts its G pipeline ids on lanes sbase[group] + 64 (r / P) + G (r % P)
-// onward (P = plans_per_wave(G)); the lanes left over stay kNoSlot.
+// onward (P = plans_per_wave(G)); the lanes no plan fills are set to kNoSlot
+// here (64 mod G per full wavefront) and by k_scan (a group's last one).
 constexpr int kScatterPer = 64;
 __global__ void __launch_bounds__(256) k_scatter(const uint16_t* __restrict__ keys, uint32_t nslots,
                                                  uint32_t* __restrict__ cursor, const uint32_t* __restrict__ sbase,
@@ -150,6 +160,9 @@ __global__ void __launch_bounds__(256) k_scatter(const uint16_t* __restrict__ ke
     if (grouped && key[j] < kPlainBuckets) {
       const uint32_t pw = plans_per_wave(G), lane = sbase[grp] + pos / pw * 64u + pos % pw * G;
       for (uint32_t c = 0; c < G; ++c) ids[lane + c] = slot + c;
+      // the wavefront's last plan marks the lanes that no plan fills (64 mod G)
+      if (pos % pw == pw - 1)
+        for (uint32_t q = G * pw; q < 64u; ++q) ids[lane - (pw - 1) * G + q] = kNoSlot;
     } else {
       ids[pos] = slot;
     }
@@ -161,8 +174,9 @@ __global__ void __launch_bounds__(256) k_scatter(const uint16_t* __restrict__ ke
 // min(31, M / 16), largest first) into vlist, which the variant pass has
 // finished with: the deferred pass then runs wavefronts of similar trip
 // counts rather than waiting in every wavefront for its longest chain.
-__device__ __forceinline__ uint32_t defer_bucket(uint32_t meta) {
-  const uint32_t M = (meta >> 8) & 0xffff, b = M >> 4;
+__device__ __forceinline__ uint32_t defer_bucket(const EvalBufs& e, uint32_t slot) {
+  const uint32_t w = e.packed[slot >> 2].cls[slot & 3], reps = w & 0xffff, M = ((w >> 16) + reps - 1) / reps;
+  const uint32_t b = M >> 4;
   return b < kSortBuckets - 1 ? b : kSortBuckets - 1;
 }
 // entry idx of the concatenated lists -> (list j, position k in it)
@@ -187,7 +201,7 @@ __global__ void __launch_bounds__(256) k_defer_hist(EvalBufs e) {
   for (uint32_t idx = blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += gridDim.x * blockDim.x) {
     uint32_t j, k;
     if (!defer_entry(e, idx, j, k)) break;
-    atomicAdd(&hs[j * kSortBuckets + defer_bucket(e.meta[e.deferred[e.sstart[j] + k]])], 1u);
+    atomicAdd(&hs[j * kSortBuckets + defer_bucket(e, e.deferred[e.sstart[j] + k])], 1u);
   }
   __syncthreads();
   for (uint32_t i = threadIdx.x; i < kMaxStages * kSortBuckets; i += blockDim.x)
@@ -214,7 +228,7 @@ __global__ void __launch_bounds__(256) k_defer_sort(EvalBufs e) {
     const bool has = r0 + threadIdx.x < total && defer_entry(e, r0 + threadIdx.x, j, k);
     if (has) {
       slot = e.deferred[e.sstart[j] + k];
-      b = j * kSortBuckets + defer_bucket(e.meta[slot]);
+      b = j * kSortBuckets + defer_bucket(e, slot);
       rank = atomicAdd(&lc[b], 1u);
     }
     __syncthreads();
@@ -338,8 +352,8 @@ hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint4* pc
   return hipGetLastError();
 }
 hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* sstart, uint32_t* sbase, bool grouped,
-                       hipStream_t s) {
-  k_scan<<<1, 1024, 0, s>>>(hist, cursor, sstart, sbase, grouped ? 1u : 0u);
+                       uint32_t* ids, hipStream_t s) {
+  k_scan<<<1, 1024, 0, s>>>(hist, cursor, sstart, sbase, grouped ? 1u : 0u, ids);
   return hipGetLastError();
 }
 hipError_t launch_scatter(const uint16_t* keys, uint32_t nslots, uint32_t* cursor, const uint32_t* sbase, bool grouped,
