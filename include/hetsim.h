@@ -333,10 +333,11 @@ int sim_best_reduce(sim_ctx* ctx, const sim_best* bests, int64_t n, sim_best* ou
  * kind 0 = first evaluation pass (per-pipeline setup and 1F1B recurrence
  * with the periodic shortcut), 1 = plan check/pack kernel, 2 = whole
  * sim_eval_plans call, 3 = deferred pass (full-loop pipelines and the u64
- * redo).  A call of more than 2^21 plans works in chunks of 2^21 and runs
- * each chunk's deferred pass on a second stream of the context, overlapped
- * with the next chunk; the call's stream waits for it before the call's
- * work is complete, so kinds 0 and 3 may overlap in time.
+ * redo).  A call of more than 2^22 plans works in chunks of 2^21 and runs
+ * each chunk's first pass on two side streams of the context and its
+ * deferred pass on a third, overlapped with the next chunk; the call's
+ * stream waits for them before the call's work is complete, so kinds 0 and
+ * 3 may overlap in time.
  */
 int sim_set_timing(sim_ctx* ctx, int enable);
 int sim_get_timing(sim_ctx* ctx, int kind, double* total_ms, int64_t* launches);

@@ -43,13 +43,19 @@ struct EventPair {
 };
 }  // namespace
 
-// Side streams of multi-chunk calls made on one caller stream: the four
-// first-pass groups and the deferred pass.  Each caller stream gets its own
-// set, so calls on different caller streams do not queue behind each other.
+// Side streams of multi-chunk calls made on one caller stream: two for the
+// four first-pass groups and one for the deferred pass.  Each caller stream
+// gets its own set, so calls on different caller streams do not queue behind
+// each other.  The groups pair up long with short -- 13-16 with 1-4 stages,
+// 9-12 with 5-8 -- so two evaluation kernels run at once: measured on the
+// 16M-plan sweep, four at once (one stream each, with enough hardware
+// queues) ran 13 % slower, and the other pairings 2-6 % slower.
+constexpr int kGroupStreams = 2;
+constexpr int kGroupStream[4] = {0, 1, 1, 0};
 struct SideStreams {
   hipStream_t caller;
   hipStream_t aux;
-  hipStream_t grp[4];
+  hipStream_t grp[kGroupStreams];
 };
 
 // Streams this context has launched work on, each with an event recorded
@@ -218,7 +224,7 @@ static bool side_streams(sim_ctx* c, hipStream_t s, SideStreams* out) {
       *out = q;
       return true;
     }
-  SideStreams q = {s, nullptr, {nullptr, nullptr, nullptr, nullptr}};
+  SideStreams q = {s, nullptr, {nullptr, nullptr}};
   bool ok = hipStreamCreateWithFlags(&q.aux, hipStreamNonBlocking) == hipSuccess;
   for (auto& x : q.grp) ok = ok && hipStreamCreateWithFlags(&x, hipStreamNonBlocking) == hipSuccess;
   if (!ok) {
@@ -233,9 +239,9 @@ static bool side_streams(sim_ctx* c, hipStream_t s, SideStreams* out) {
 }
 
 // Chunks of kChunk plans (one chunk up to 2 kChunk).  With more than one chunk, the four stage-count
-// groups of chunk i's first pass run on four streams of the context, and its
-// deferred pass on a fifth that waits for the four, while the call's stream
-// packs and sorts chunk i + 1.  The two workspaces alternate; the call's
+// groups of chunk i's first pass run on two side streams (paired as
+// kGroupStream says), and its deferred pass on a third that waits for them,
+// while the call's stream packs and sorts chunk i + 1.  The two workspaces alternate; the call's
 // stream waits for chunk i's deferred pass before reusing its workspace for
 // chunk i + 2 and, at the end, for the last one.
 extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uint64_t* out, void* stream) {
@@ -306,10 +312,11 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
       if (e == hipSuccess) e = hipEventRecord(sorted(b), s);
       joined = false;
       for (int g = 0; g < 4 && e == hipSuccess; ++g) {
-        e = hipStreamWaitEvent(side.grp[g], sorted(b), 0);
-        if (e == hipSuccess) e = launch_group(c->tab, a, (uint32_t)(cn * 4), g, side.grp[g]);
-        if (e == hipSuccess) e = launch_variant(c->tab, a, g, side.grp[g]);
-        if (e == hipSuccess) e = hipEventRecord(fin(b, g), side.grp[g]);
+        const hipStream_t gs = side.grp[kGroupStream[g]];
+        e = hipStreamWaitEvent(gs, sorted(b), 0);
+        if (e == hipSuccess) e = launch_group(c->tab, a, (uint32_t)(cn * 4), g, gs);
+        if (e == hipSuccess) e = launch_variant(c->tab, a, g, gs);
+        if (e == hipSuccess) e = hipEventRecord(fin(b, g), gs);
         if (e == hipSuccess) e = hipStreamWaitEvent(aux, fin(b, g), 0);
       }
       if (t0) end_event(c, 0, aux, &e0);
