@@ -2157,24 +2157,13 @@ __global__ void __launch_bounds__(kEvalThreads) k_eval(Tab t, EvalBufs e) {
   double* xw = nullptr;
   if constexpr (!kHet)
     xw = (double*)((char*)lds + (kMode < 2 ? t.lds_bytes : 0)) + (threadIdx.x >> 6) * xchg_wave(GRP);
-  // The wavefront's tiles are software-pipelined: while one is evaluated,
-  // the next tile's ids and its plans' header words (or metadata) are held
-  // in registers -- loads that also bring the plan records' first lines into
-  // the caches, one more touching each record's last word -- and the ids of
-  // the tile after that are on their way, so the record loads in eval_one
-  // hit the L2 rather than wait for memory.
-  const uint32_t lane = threadIdx.x & 63u;
-  auto id_at = [&](uint32_t b) { return b + lane < hi ? e.ids[b + lane] : kNoSlot; };
-  auto key_at = [&](uint32_t sl) -> uint32_t { return sl == kNoSlot ? 0 : kHet ? e.meta[sl] : e.packed[sl >> 2].hdr; };
-  uint32_t base = lo + blockIdx.x * kEvalThreads + (threadIdx.x & ~63u);
-  uint32_t slot = id_at(base), nslot = id_at(base + stride), key = key_at(slot);
-  for (; base < hi; base += stride) {
-    const uint32_t nkey = key_at(nslot);
-    const uint32_t ntail = nslot == kNoSlot ? 0 : reinterpret_cast<const uint32_t*>(e.packed + (nslot >> 2))[19];
-    const uint32_t nnslot = id_at(base + 2 * stride);
-    bool pending = slot != kNoSlot;   // past the group, or a padding lane of a plan-sorted group
-    const uint32_t hdr = kHet ? 0 : key;
-    const uint32_t S = !pending ? 0 : kHet ? key & 31 : ((hdr >> 4) & 15) + 1;
+  for (uint32_t base = lo + blockIdx.x * kEvalThreads + (threadIdx.x & ~63u); base < hi; base += stride) {
+    const uint32_t pos = base + (threadIdx.x & 63u);
+    bool pending = pos < hi;
+    const uint32_t slot = pending ? e.ids[pos] : 0;
+    pending = pending && slot != kNoSlot;   // padding lanes of plan-sorted groups
+    const uint32_t hdr = !pending || kHet ? 0 : e.packed[slot >> 2].hdr;
+    const uint32_t S = !pending ? 0 : kHet ? e.meta[slot] & 31 : ((hdr >> 4) & 15) + 1;
     if constexpr (!kHet) {
       // overlap and zero-bubble plans go to the variant pass: the wavefront
       // (one stage count: the plan-sorted groups are padded to whole
@@ -2207,10 +2196,6 @@ __global__ void __launch_bounds__(kEvalThreads) k_eval(Tab t, EvalBufs e) {
         pending = false;
       }
     }
-    asm volatile("" ::"v"(ntail));   // keeps the touching load
-    slot = nslot;
-    nslot = nnslot;
-    key = nkey;
   }
 }
 

@@ -53,7 +53,6 @@ struct __attribute__((aligned(16))) PackedPlan {
   uint32_t cls[4];
   uint64_t types[4];
 };
-static_assert(sizeof(PackedPlan) == 80, "an 80-byte plan record: word 19 is its last");
 
 // Per-device-type fields a kernel reads together (32 bytes, two loads).
 struct TypeInfo {
