@@ -16,7 +16,7 @@ hipError_t launch_prep(const Tab& t, const sim_plans& p, int64_t n, uint64_t* ou
                        uint32_t* meta, uint32_t* hist, uint16_t* keys, hipStream_t s);
 hipError_t launch_memory(const Tab& t, const sim_plans& p, int64_t n, uint64_t* out, hipStream_t s);
 hipError_t launch_plan_syncs(const Tab& t, const PackedPlan* packed, const uint4* pcut, const uint32_t* meta,
-                             int64_t n, uint64_t* hdp, hipStream_t s);
+                             int64_t n, uint64_t* hdp, uint32_t* pc, uint32_t* perm, hipStream_t s);
 hipError_t launch_stages(const Tab& t, const PackedPlan* packed, const uint4* pcut, const uint32_t* meta, int64_t n,
                          uint64_t* out_stage, hipStream_t s);
 hipError_t launch_scan(const uint32_t* hist, uint32_t* cursor, uint32_t* sstart, uint32_t* sbase, bool grouped,
@@ -295,7 +295,9 @@ extern "C" int sim_eval_plans(sim_ctx* c, const sim_plans* plans, int64_t n, uin
     bool t1 = e == hipSuccess && begin_event(c, 1, s, &ev);
     if (e == hipSuccess) e = launch_prep(c->tab, p, cn, out + off, W.packed, W.pcut, W.meta, W.hist, W.keys, s);
     if (t1) end_event(c, 1, s, &ev);
-    if (e == hipSuccess && het) e = launch_plan_syncs(c->tab, W.packed, W.pcut, W.meta, cn, W.hdp, s);
+    // (the plan order goes to the variant-tile array, unused in this layout until the deferred sort)
+    if (e == hipSuccess && het)
+      e = launch_plan_syncs(c->tab, W.packed, W.pcut, W.meta, cn, W.hdp, W.ctr + kEvalCounters, W.vlist, s);
     // shared-layout calls sort plans by plan: the scan and the scatter mark
     // the padding lanes
     if (e == hipSuccess) e = launch_scan(W.hist, W.cursor, W.sstart, W.sbase, !het, W.ids, s);
@@ -369,7 +371,8 @@ extern "C" int sim_eval_plans_noalloc(sim_ctx* c, const sim_plans* plans, int64_
   const Work W = carve(ws, n, het);
   hipError_t e = launch_fill32(W.hist, kCounters, 0, s);
   if (e == hipSuccess) e = launch_prep(c->tab, *plans, n, out, W.packed, W.pcut, W.meta, W.hist, W.keys, s);
-  if (e == hipSuccess && het) e = launch_plan_syncs(c->tab, W.packed, W.pcut, W.meta, n, W.hdp, s);
+  if (e == hipSuccess && het)
+    e = launch_plan_syncs(c->tab, W.packed, W.pcut, W.meta, n, W.hdp, W.ctr + kEvalCounters, W.vlist, s);
   if (e == hipSuccess) e = launch_scan(W.hist, W.cursor, W.sstart, W.sbase, !het, W.ids, s);
   if (e == hipSuccess) e = launch_scatter(W.keys, (uint32_t)(n * 4), W.cursor, W.sbase, !het, W.ids, s);
   const EvalArgs a = {W.packed, W.pcut, W.hdp, W.meta, W.ids, W.sstart, out, W.ctr, W.deferred, W.vlist,

@@ -72,6 +72,14 @@ __device__ __forceinline__ uint64_t div_up(uint64_t x, uint64_t p, double rp) {
   return q + (r != 0);
 }
 
+// ceil(x / p) for any x: div_up below 2^53, the integer division above
+// (never on the workloads here; a branch the wavefront skips when no lane
+// takes it)
+__device__ __forceinline__ uint64_t div_up_u64(uint64_t x, uint64_t p, double rp) {
+  if (x < (1ull << 53)) return div_up(x, p, rp);
+  return x / p + (x % p != 0);
+}
+
 // DP gradient sync of one stage over a ring of p members.  tree: an
 // all-reduce takes the faster of the ring and a pipelined binary tree
 // (reduce up, broadcast down: 2 ceil(log2 p) latencies, each member's
@@ -873,9 +881,11 @@ __device__ __forceinline__ uint32_t row_word(const uint4 (&rows)[4], uint32_t c,
 // Weighting of a gradient shard of n elements by the class's share of the
 // global batch, on a device of type k: one multiply per element, the fp32
 // shard read and written (the roofline time of one elementwise op)
+// (the ceilings through fp64 reciprocals: a 64-bit integer division is a
+// long instruction loop on this ISA)
 __device__ __forceinline__ uint64_t weigh_ps(const Tab& t, uint32_t k, uint64_t n) {
-  const uint64_t tf = t.tflops[k], hb = t.hbm[k], by = 2000 * t.grad_bytes * n;
-  const uint64_t tc = n / tf + (n % tf != 0), tm = by / hb + (by % hb != 0);
+  const uint64_t by = 2000 * t.grad_bytes * n;
+  const uint64_t tc = div_up_u64(n, t.tflops[k], t.rtflops[k]), tm = div_up_u64(by, t.hbm[k], t.rhbm[k]);
   return tc > tm ? tc : tm;
 }
 
@@ -1428,19 +1438,23 @@ __global__ void __launch_bounds__(256) k_stages(Tab t, const PackedPlan* __restr
 }
 
 // Per-class layout: the syncs of every (class, stage) of every valid plan
-// (one plan per lane), once per plan rather than once per pipeline.
+// (one plan per lane), once per plan rather than once per pipeline; lane j
+// takes plan perm[j] of the pc[512] valid plans (sorted by the length of
+// their walks).
 template <int kMode>
 __global__ void __launch_bounds__(256) k_plan_syncs(Tab t, const PackedPlan* __restrict__ packed,
-                                                    const uint4* __restrict__ pcut, const uint32_t* __restrict__ meta,
-                                                    int64_t n, uint64_t* __restrict__ hdp) {
+                                                    const uint4* __restrict__ pcut, const uint32_t* __restrict__ perm,
+                                                    const uint32_t* __restrict__ pc, int64_t n,
+                                                    uint64_t* __restrict__ hdp) {
   extern __shared__ uint4 lds[];
   fill_lds<kMode>(t, lds);
   const Hot<kMode> h(t, lds);
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n || meta[4 * i] == 0) return;
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= n || j >= (int64_t)pc[2 * kPlanBuckets]) return;
+  const uint32_t i = perm[j];
   const Plan p = unpack(packed[i], 0);
   uint4 rows[4];
-  load_rows(pcut + 4 * i, rows);
+  load_rows(pcut + 4 * (size_t)i, rows);
   het_plan_syncs(t, h, p, rows, hdp + (size_t)i * (kMaxClasses * kMaxStages));
 }
 

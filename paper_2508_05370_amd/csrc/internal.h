@@ -97,6 +97,8 @@ struct Tab {
   uint64_t a_side[kMaxTypes];     // one end of an inter-node path: two PCIe trips + NIC
   uint32_t tflops[kMaxTypes];     // device speed of pool k (TFLOP/s, GB/s of HBM): the gradient
   uint32_t hbm[kMaxTypes];        // weighting of classes with different micro-batch sizes
+  double rtflops[kMaxTypes];      // their reciprocals, rounded to nearest (for exact ceilings)
+  double rhbm[kMaxTypes];
   uint64_t act[4];                // bytes of one micro-batch activation per mbs index
   uint64_t grad_bytes, param_bytes;
   uint64_t par_layer[4];          // non-expert parameters of one layer on one TP rank, by log2 TP
@@ -128,8 +130,10 @@ struct Tab {
 // pipelines (layout above).  ctr[0] counts overflowed pipelines,
 // ctr[1 + 16 - S] the S-stage pipelines deferred to the full-loop pass,
 // ctr[kVariantCtr + 16 - S] the slots of the S-stage overlap and zero-bubble
-// tiles of the variant pass (64 per tile); the overflow list follows the counters at
-// ctr + kEvalCounters.
+// tiles of the variant pass (64 per tile); the per-class layout's plan-order
+// counters (kPlanSortWords) follow the evaluation counters at ctr +
+// kEvalCounters, and the overflow list follows them at ctr + kEvalCounters +
+// kPlanSortWords.
 constexpr uint32_t kVariantCtr = 1 + kMaxStages;
 // The deferred lists are sorted by micro-batch count before the deferred
 // pass (longest first, kSortBuckets buckets per stage count): their counts
@@ -138,6 +142,11 @@ constexpr uint32_t kVariantCtr = 1 + kMaxStages;
 constexpr uint32_t kSortBuckets = 32;
 constexpr uint32_t kSortCtr = 48;
 constexpr uint32_t kEvalCounters = kSortCtr + 2 * kMaxStages * kSortBuckets;
+// Per-class layout: plans counting-sorted by (classes, total stages) before
+// the plan-level sync pass -- counts [0, 256), cursors [256, 512), the
+// number of valid plans at 512.
+constexpr uint32_t kPlanBuckets = 256;
+constexpr uint32_t kPlanSortWords = 2 * kPlanBuckets + 1;
 static_assert(kVariantCtr + kMaxStages <= kSortCtr, "evaluation counters");
 // The skipped-work counter is spread over slots on separate cache lines so
 // that the waves of a launch do not serialise on one address.
@@ -167,7 +176,7 @@ constexpr size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // per-class layout
 // the plans' class cut rows (64 bytes per plan) and the syncs each pipeline's
 // stages wait for (16 u64 per pipeline slot, 512 bytes per plan).
-constexpr uint32_t kCounters = kBuckets + kEvalCounters;
+constexpr uint32_t kCounters = kBuckets + kEvalCounters + kPlanSortWords;
 struct Work {
   PackedPlan* packed;
   uint4* pcut;

@@ -169,6 +169,69 @@ __global__ void __launch_bounds__(256) k_scatter(const uint16_t* __restrict__ ke
   }
 }
 
+// ---------------------------------------------------------------- per-class layout: plan order
+// k_plan_syncs walks each plan's layer segments, one plan per lane, so a
+// wavefront lasts as long as its longest walk.  The valid plans are first
+// counting-sorted by (classes, total stages over the classes), a close proxy
+// for the number of segments (the union of the classes' cuts), into perm;
+// pc as kPlanSortWords describes.  The key comes from the pipeline metadata
+// k_prep wrote (S | G << 5 | ..., per class; zero past the classes and for
+// invalid plans).
+__device__ __forceinline__ uint32_t plan_key(uint4 m) {
+  const uint32_t G = (m.x >> 5) & 7, st = (m.x & 31) + (m.y & 31) + (m.z & 31) + (m.w & 31);
+  return (G - 1) * 64 + st - 1;
+}
+constexpr int kPlanPer = 8;   // plans per thread of the plan-order kernels
+__global__ void __launch_bounds__(256) k_plan_hist(const uint4* __restrict__ meta, uint32_t n, uint32_t* __restrict__ pc) {
+  __shared__ uint32_t lh[kPlanBuckets];
+  lh[threadIdx.x] = 0;
+  __syncthreads();
+  for (int j = 0; j < kPlanPer; ++j) {
+    const uint32_t i = (blockIdx.x * kPlanPer + j) * 256 + threadIdx.x;
+    if (i >= n) break;
+    const uint4 m = meta[i];
+    if (m.x) atomicAdd(&lh[plan_key(m)], 1u);
+  }
+  __syncthreads();
+  if (lh[threadIdx.x]) atomicAdd(&pc[threadIdx.x], lh[threadIdx.x]);
+}
+__global__ void __launch_bounds__(256) k_plan_scatter(const uint4* __restrict__ meta, uint32_t n,
+                                                      uint32_t* __restrict__ pc, uint32_t* __restrict__ perm) {
+  static_assert(kPlanBuckets == 256, "one bucket per thread");
+  __shared__ uint32_t base[kPlanBuckets], lc[kPlanBuckets];
+  const uint32_t b = threadIdx.x;
+  base[b] = pc[b];
+  lc[b] = 0;
+  __syncthreads();
+  for (uint32_t off = 1; off < kPlanBuckets; off <<= 1) {   // inclusive scan of the counts
+    const uint32_t x = b >= off ? base[b - off] : 0;
+    __syncthreads();
+    base[b] += x;
+    __syncthreads();
+  }
+  if (blockIdx.x == 0 && b == kPlanBuckets - 1) pc[2 * kPlanBuckets] = base[b];   // valid plans
+  const uint32_t excl = base[b] - pc[b];
+  __syncthreads();
+  base[b] = excl;
+  uint32_t key[kPlanPer], rank[kPlanPer];
+  for (int j = 0; j < kPlanPer; ++j) {
+    const uint32_t i = (blockIdx.x * kPlanPer + j) * 256 + threadIdx.x;
+    key[j] = kNoSlot;
+    if (i < n) {
+      const uint4 m = meta[i];
+      if (m.x) {
+        key[j] = plan_key(m);
+        rank[j] = atomicAdd(&lc[key[j]], 1u);
+      }
+    }
+  }
+  __syncthreads();
+  if (lc[b]) lc[b] = atomicAdd(&pc[kPlanBuckets + b], lc[b]);
+  __syncthreads();
+  for (int j = 0; j < kPlanPer; ++j)
+    if (key[j] != kNoSlot) perm[base[key[j]] + lc[key[j]] + rank[j]] = (blockIdx.x * kPlanPer + j) * 256 + threadIdx.x;
+}
+
 // ---------------------------------------------------------------- deferred lists
 // Counting sort of the deferred lists by micro-batch count (bucket
 // min(31, M / 16), largest first) into vlist, which the variant pass has
@@ -335,13 +398,17 @@ hipError_t launch_memory(const Tab& t, const sim_plans& p, int64_t n, uint64_t* 
   return hipGetLastError();
 }
 
+// pc: the plan-order counters (zero on entry); perm: n words
 hipError_t launch_plan_syncs(const Tab& t, const PackedPlan* packed, const uint4* pcut, const uint32_t* meta,
-                             int64_t n, uint64_t* hdp, hipStream_t s) {
+                             int64_t n, uint64_t* hdp, uint32_t* pc, uint32_t* perm, hipStream_t s) {
+  const int go = blocks_for(n, 256 * kPlanPer);
+  k_plan_hist<<<go, 256, 0, s>>>((const uint4*)meta, (uint32_t)n, pc);
+  k_plan_scatter<<<go, 256, 0, s>>>((const uint4*)meta, (uint32_t)n, pc, perm);
   const int g = blocks_for(n, 256);
   const size_t lds = t.mode < 2 ? t.lds_bytes : 0;
-  if (t.mode == 0) k_plan_syncs<0><<<g, 256, lds, s>>>(t, packed, pcut, meta, n, hdp);
-  else if (t.mode == 1) k_plan_syncs<1><<<g, 256, lds, s>>>(t, packed, pcut, meta, n, hdp);
-  else k_plan_syncs<2><<<g, 256, 0, s>>>(t, packed, pcut, meta, n, hdp);
+  if (t.mode == 0) k_plan_syncs<0><<<g, 256, lds, s>>>(t, packed, pcut, perm, pc, n, hdp);
+  else if (t.mode == 1) k_plan_syncs<1><<<g, 256, lds, s>>>(t, packed, pcut, perm, pc, n, hdp);
+  else k_plan_syncs<2><<<g, 256, 0, s>>>(t, packed, pcut, perm, pc, n, hdp);
   return hipGetLastError();
 }
 
@@ -390,7 +457,8 @@ hipError_t launch_node_probe(double* sink, int blocks, int iters, hipStream_t s)
 
 // ---------------------------------------------------------------- evaluation passes
 EvalBufs eval_bufs(const EvalArgs& a) {
-  return {a.packed, (const uint4*)a.pcut, a.hdp, a.meta, a.ids, a.sstart, a.out, a.ctr, a.ctr + kEvalCounters, a.deferred,
+  return {a.packed, (const uint4*)a.pcut, a.hdp, a.meta, a.ids, a.sstart, a.out, a.ctr,
+          a.ctr + kEvalCounters + kPlanSortWords, a.deferred,
           a.vlist, (unsigned long long*)a.skipped_ops, a.dtab};
 }
 

@@ -254,6 +254,8 @@ int build_tables(const sim_model_desc* md, const sim_cluster_desc* cd, HostTable
     t.cap[k] = cd->n_nodes[k] * cd->dev_per_node[k];
     t.tflops[k] = cd->tflops[k];
     t.hbm[k] = cd->hbm_GBps[k];
+    t.rtflops[k] = 1.0 / (double)cd->tflops[k];
+    t.rhbm[k] = 1.0 / (double)cd->hbm_GBps[k];
     t.dev_off[k] = (uint32_t)d0;
     t.node_off[k] = (uint32_t)n0;
     t.bq_pcie[k] = (uint32_t)beta_q(cd->pcie_MBps[k]);
