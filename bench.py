@@ -436,8 +436,8 @@ def main():
         roof = {"bound": "alu", "achieved": round(achieved / 1e12, 3), "peak": round(peak / 1e12, 3),
                 "unit": "TOP/s", "frac": round(achieved / peak, 4),
                 "traffic": None if a.plans else measured_traffic(a.workload, a.chunk),
-                "kernel": "one sim_eval_plans call: k_prep, k_scan, k_scatter, k_eval x4 groups, k_variant x4, "
-                          "k_deferred, k_redo_u64 per 2M-plan chunk",
+                "kernel": "one sim_eval_plans call: k_fill32, k_prep, k_scan, k_scatter, k_eval x4 groups, "
+                          "k_variant x4, k_defer_hist, k_defer_sort, k_deferred, k_redo_u64 per 2M-plan chunk",
                 "avg_launch_ms": round(avg_ms, 4), "launches": call_n,
                 "work_per_launch": work,
                 "recurrence_ops_per_launch": rec_per_launch, "setup_ops_per_launch": setup_per_launch,

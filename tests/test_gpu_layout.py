@@ -181,3 +181,23 @@ def test_per_class_empty_call(torch, B, workloads):
     sim.eval_plans(B.device_plans(p), n=0, out=out)
     torch.cuda.synchronize()
     assert torch.all(out == 7)
+
+
+def test_per_class_chunk_without_valid_plans(torch, B, oracle_mod, workloads):
+    """A per-class chunk whose plans are all invalid (a nonzero header micro-batch field): the
+    plan-order sort counts no plan, the plan-level sync pass and the pipelines do nothing, and
+    every time is the invalid marker.  Then valid plans again on the same context: the counters
+    start from zero in every call."""
+    w = workloads.workload(3)
+    n = 20_000 + 11
+    p = workloads.het_plans(w, 0, n)
+    q = {k: v.copy() for k, v in p.items()}
+    q["hdr"] |= np.uint32(1 << 11)
+    sim = B.Sim(w["model"], w["cluster"])
+    say("case: per-class layout, %d plans, none valid" % n)
+    got = B.times_u64(sim.eval_plans(B.device_plans(q)))
+    assert np.all(got == MAXU)
+    _equal(got, oracle_mod.Oracle(w["model"], w["cluster"]).eval(q), "no valid per-class plan")
+    say("case: per-class layout, the same plans valid, same context")
+    got = B.times_u64(sim.eval_plans(B.device_plans(p)))
+    _equal(got, oracle_mod.Oracle(w["model"], w["cluster"]).eval(p), "per-class after an empty order")
