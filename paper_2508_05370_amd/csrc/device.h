@@ -1627,7 +1627,7 @@ __device__ __forceinline__ void zb_iter(const V (&f)[S], const V (&bi)[S], const
   }
 }
 
-template <int S, typename V, bool kJump>
+template <int S, typename V, bool kJump, bool kFallback = false>
 __device__ __forceinline__ bool pipe_zb(const V (&f)[S], const V (&bi)[S], const V (&w)[S], const V (&c)[S], uint32_t M,
                                         int& skipped,
                                         V (&last)[S]) {
@@ -1687,7 +1687,7 @@ __device__ __forceinline__ bool pipe_zb(const V (&f)[S], const V (&bi)[S], const
       zb_iter<S, V>(f, bi, w, c, S, -1, out_f, last);
       rem = 0;
     }
-    if (rem > 0) {   // still aperiodic: the deferred pass runs the whole loop
+    if (rem > 0 && !kFallback) {   // still aperiodic: the deferred pass runs the whole loop
       skipped = -1;
       return false;
     }
@@ -2350,9 +2350,11 @@ __device__ __forceinline__ uint64_t redo_one(const StageRec& R, const uint64_t (
     b[s] = R[s][1] - w[s];
     c[s] = R[s][2];
   }
+  // the periodic shortcut holds in any exact arithmetic: pairs within the
+  // budget, then the rest of the loop in place
   int skipped;
-  if (zb) pipe_zb<S, uint64_t, false>(f, b, w, c, M, skipped, last);
-  else pipe<S, uint64_t, false>(f, b, c, M, skipped, last);
+  if (zb) pipe_zb<S, uint64_t, true, true>(f, b, w, c, M, skipped, last);
+  else pipe<S, uint64_t, true, true>(f, b, c, M, skipped, last);
   uint64_t T = 0;
 #pragma unroll
   for (int s = 0; s < S; ++s) T = vmax(T, last[s] + R[s][3]);
