@@ -2375,7 +2375,7 @@ __global__ void __launch_bounds__(64) k_redo_u64(Tab t, EvalBufs e) {
       switch (il_shape(S, p.v)) {
 #define X(S_, V_)                                                    \
   case S_ | (V_ - 1) << 5:                                           \
-    r = il_time<S_, V_, 2, uint64_t, false>(t, h, p, skipped);       \
+    r = il_time<S_, V_, 2, uint64_t, true>(t, h, p, skipped);        \
     break;
         HETSIM_IL_SHAPES(X)
 #undef X
