@@ -3,27 +3,37 @@
 //
 // Data flow of one chunk of plans (all in HBM):
 //   k_prep     one plan per lane: decode and check the plan, pack it into 80
-//              contiguous bytes, and count its pipelines (one per replica
-//              class) per (stages, classes, micro-batches) bucket.
-//   k_scan     one block: bucket offsets, longest pipelines first.
-//   k_scatter  groups pipeline ids by bucket, so that a wavefront runs
-//              pipelines of one stage count, one class count and similar
-//              micro-batch counts.
+//              contiguous bytes, and count it per bucket: in the shared
+//              layout the whole plan by (stages, classes, longest
+//              micro-batch count), otherwise each pipeline (one per replica
+//              class) by its own.
+//   k_scan     one block: bucket offsets, longest pipelines first; a
+//              plan-sorted (stages, classes) group takes whole wavefronts.
+//   k_scatter  places the ids: a plan-sorted plan's G pipelines on adjacent
+//              lanes of one wavefront, so that a wavefront runs one stage
+//              count, one class count and similar micro-batch counts.
+//   k_plan_hist, k_plan_scatter, k_plan_syncs (per-class layout only) the
+//              syncs of every (class, stage), once per plan, plans sorted by
+//              the length of their segment walks.
 //   k_eval     one pipeline per lane, one launch per group of four stage
-//              counts.  Setup: place the class on its device pools, read
-//              stage compute from the layer prefix tables, find each group's
-//              slowest link with range-max tables, and cost the TP/EP/PP/DP
-//              collectives.  Then the 1F1B recurrence, unrolled per stage
-//              count so that all per-stage state stays in VGPRs; times are
-//              integers carried exactly in fp64 (3 VALU ops per schedule
+//              counts.  Overlap and zero-bubble plans are handed to the
+//              variant pass first.  Setup: place the class on its device
+//              pools, read stage compute from the layer prefix tables, find
+//              each group's slowest link with range-max tables, and cost the
+//              TP/EP/PP collectives.  Then the 1F1B recurrence, unrolled per
+//              stage count so that all per-stage state stays in VGPRs; times
+//              are integers carried exactly in fp64 (3 VALU ops per schedule
 //              node).  Once a steady iteration advances the whole schedule
 //              state by one constant, the remaining steady iterations are
 //              added in one step (periodic shortcut); lanes still aperiodic
-//              after a fixed budget are deferred.
+//              after a fixed budget are deferred.  Then the DP syncs, shared
+//              over a plan's lanes, and one store of the plan's time.
+//   k_variant  the overlap and zero-bubble plans of each group, the same way.
+//   k_defer_hist, k_defer_sort  the deferred lists sorted by micro-batch count.
 //   k_deferred the interleaved-1F1B pipelines, then the deferred pipelines of
 //              all stage counts (full steady loop).
 //   k_redo_u64 pipelines whose time reached 2^53 ps, again in u64.
-//              The plan's time is the max over its classes (atomic max).
+//              Later passes raise a plan's time with atomic max.
 #pragma once
 #include <hip/hip_runtime.h>
 
