@@ -2193,17 +2193,24 @@ __global__ void __launch_bounds__(kEvalThreads) k_eval(Tab t, EvalBufs e) {
       // (one stage count: the plan-sorted groups are padded to whole
       // wavefronts) takes one 64-slot tile and every lane writes its own
       // position, the slot of an overlap or zero-bubble plan or kNoSlot, so
-      // that the tile keeps its plans' lanes together.  Every lane is active
-      // here; the lane that takes the tile is the one readfirstlane reads.
+      // that the tile keeps its plans' lanes together; the lane that takes
+      // the tile is the one readfirstlane reads.  That needs every lane of
+      // the wavefront here, which the loop's single uniform latch gives; if
+      // a compiler ever split the wavefront at this point, the tile would
+      // have holes, so a partial wavefront hands such lanes to the deferred
+      // lists instead (whole loop per lane, plans need not stay whole there).
       const bool var = pending && (((hdr >> 13) & 1) | ((hdr >> 16) & 1));
       const uint64_t vb = __ballot(var);
       if (vb) {
-        const uint32_t Sv = __builtin_amdgcn_readfirstlane(__shfl(S, __ffsll((unsigned long long)vb) - 1));
-        uint32_t tile = 0;
-        if ((threadIdx.x & 63u) == (uint32_t)(__ffsll((unsigned long long)__ballot(1)) - 1))
-          tile = atomicAdd(&e.ctr[kVariantCtr + kMaxStages - Sv], 64u);
-        tile = __builtin_amdgcn_readfirstlane(tile);
-        e.vlist[e.sstart[kMaxStages - Sv] + tile + (threadIdx.x & 63u)] = var ? slot : kNoSlot;
+        if (__ballot(1) == ~0ull) {
+          const uint32_t Sv = __builtin_amdgcn_readfirstlane(__shfl(S, __ffsll((unsigned long long)vb) - 1));
+          uint32_t tile = 0;
+          if ((threadIdx.x & 63u) == 0) tile = atomicAdd(&e.ctr[kVariantCtr + kMaxStages - Sv], 64u);
+          tile = __builtin_amdgcn_readfirstlane(tile);
+          e.vlist[e.sstart[kMaxStages - Sv] + tile + (threadIdx.x & 63u)] = var ? slot : kNoSlot;
+        } else if (var) {
+          e.deferred[e.sstart[kMaxStages - S] + atomicAdd(&e.ctr[1 + kMaxStages - S], 1u)] = slot;
+        }
         pending = pending && !var;
       }
     }
