@@ -703,7 +703,8 @@ struct HierShape {
 
 template <int kMode, bool kHier>
 __device__ __forceinline__ void stage_link(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t s,
-                                           uint64_t& alpha, uint32_t& bq, HierShape& hs) {
+                                           uint64_t& alpha, uint32_t& bq, HierShape& hs,
+                                           const uint32_t* __restrict__ bl = nullptr) {
   const uint32_t G = p.G, tp = p.tp;
   bool same = true;
   uint32_t k0 = 0, nmin = 0xffffffffu, nmax = 0, bq_dp = 0;
@@ -715,7 +716,8 @@ __device__ __forceinline__ void stage_link(const Tab& t, const Hot<kMode>& h, co
     if (c2 >= G) continue;
     const uint32_t k2 = (uint32_t)(p.tv[c2] >> (4 * s)) & 15;
     const TypeInfo t2 = h.type(k2);
-    const uint32_t b2 = placed_before(p, c2, s, k2) * tp, n2 = p.reps[c2] * tp, d2 = t2.dpl;
+    // (bl: the plan's lanes' stage placements, class-major, p.S per class)
+    const uint32_t b2 = bl ? bl[c2 * p.S + s] : placed_before(p, c2, s, k2) * tp, n2 = p.reps[c2] * tp, d2 = t2.dpl;
     const uint32_t l2 = t2.node_off + (b2 >> d2), h2 = t2.node_off + ((b2 + n2 - 1) >> d2);
     const uint32_t dl2 = t2.dev_off + b2;
     const uint32_t nic2 = range_max(h.rmn, t.D, dl2, dl2 + n2 - 1);
@@ -760,13 +762,13 @@ __device__ __forceinline__ uint64_t with_hier(uint64_t ring, const HierShape& hs
 // compiled without it, defer every pipeline when it is enabled).
 template <int kMode, bool kHier = true>
 __device__ __forceinline__ uint64_t stage_dp(const Tab& t, const Hot<kMode>& h, const Plan& p, uint32_t s,
-                                             uint32_t ns, double rp, double rpe) {
+                                             uint32_t ns, double rp, double rpe, const uint32_t* bl = nullptr) {
   if (p.psum <= 1) return 0;
   const uint32_t tpl = p.tpl, epl = p.epl, S = p.S;
   uint64_t alpha;
   uint32_t bq;
   HierShape hs;
-  stage_link<kMode, kHier>(t, h, p, s, alpha, bq, hs);
+  stage_link<kMode, kHier>(t, h, p, s, alpha, bq, hs, bl);
   const uint64_t pd = (uint64_t)ns * t.par_layer[tpl] + (s == 0 ? t.par_embed[tpl] : 0) +
                       (s == S - 1 ? t.par_head[tpl] : 0);
   uint64_t tdp = ring_sync(p.psum, rp, p.zero, t.grad_bytes * pd, t.param_bytes * pd, alpha, bq, t.ccl_tree);
@@ -1263,6 +1265,7 @@ __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, c
     uint32_t k, base, bq_in, bq_nic;
     TypeInfo ti;
     stage_place<kMode, kHet>(t, h, p, s, k, ti, base, bq_in, bq_nic);
+    sink.base(s, base);
     const uint32_t dpl = ti.dpl;
     uint64_t fc, bc, wc;
     stage_cost<kMode, kHet>(t, h, p, k, ti, base, bq_in, bq_nic, lo, hi, s == 0, s == S - 1, fc, bc, wc);
@@ -1305,6 +1308,7 @@ __device__ __forceinline__ void class_setup(const Tab& t, const Hot<kMode>& h, c
 struct RecSink {
   static constexpr bool kDp = true;
   static constexpr int kS = 0, kUnroll = 1;   // stage count taken from the plan
+  __device__ __forceinline__ void base(uint32_t, uint32_t) {}
   uint64_t (&rec)[kMaxStages][kRecWords];
   uint64_t* w = nullptr;
   __device__ __forceinline__ void put(uint32_t s, uint64_t fc, uint64_t bc, uint64_t wc, uint64_t hop,
@@ -1333,6 +1337,10 @@ struct RegSink {
   static constexpr bool kDp = false;
   static constexpr int kS = S, kUnroll = kSetupUnroll;
   double f[S], b[S], c[S];
+  uint32_t* bs = nullptr;   // optional: each stage's first device in its pool (LDS)
+  __device__ __forceinline__ void base(uint32_t s, uint32_t b0) {
+    if (bs) bs[s] = b0;
+  }
   __device__ __forceinline__ RegSink() {
 #pragma unroll
     for (int i = 0; i < S; ++i) f[i] = b[i] = c[i] = 0;
@@ -1357,6 +1365,7 @@ template <int S>
 struct ZbSink {
   static constexpr bool kDp = false;
   static constexpr int kS = S, kUnroll = kSetupUnroll;
+  __device__ __forceinline__ void base(uint32_t, uint32_t) {}
   double f[S], bi[S], w[S], c[S];
   __device__ __forceinline__ ZbSink() {
 #pragma unroll
@@ -1758,13 +1767,21 @@ struct EvalBufs {
 // (the syncs do not depend on the recurrence).
 template <int S, int kMode, bool kHier>
 __device__ __forceinline__ double grouped_tail(const Tab& t, const Hot<kMode>& h, const Plan& p, const double (&last)[S],
-                                               double* xw) {
+                                               double* xw, const uint32_t* bw = nullptr) {
   const uint32_t G = p.G, lane = threadIdx.x & 63u;
   double* x = xw + (lane / G) * xchg_row(S);
   const double rp = 1.0 / (double)p.psum, rpe = 1.0 / (double)(p.psum >> p.epl);
+  // bw: every lane's stage placements from its setup (S per lane); the
+  // plan's G lanes start at lane - c
+  const uint32_t* bl = bw ? bw + (lane - p.c) * S : nullptr;
+  if (bw) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
   for (uint32_t s = p.c; s < (uint32_t)S; s += G) {
     const uint32_t lo = s ? cut_at(p, s - 1) : 0;
-    x[s] = (double)stage_dp<kMode, kHier>(t, h, p, s, cut_at(p, s) - lo, rp, rpe);
+    x[s] = (double)stage_dp<kMode, kHier>(t, h, p, s, cut_at(p, s) - lo, rp, rpe, bl);
   }
   // the rows are written and read by the lanes of one wavefront, whose LDS
   // accesses complete in order; the fences keep the compiler from moving
@@ -1821,7 +1838,7 @@ __device__ __forceinline__ double grouped_overlap_tail(const Tab& t, const Hot<k
 
 template <int S, bool kFull, int kMode, bool kHet, bool kOvl = false, bool kZb = false>
 __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, const EvalBufs& e, uint32_t slot,
-                                         double* xw = nullptr) {
+                                         double* xw = nullptr, uint32_t* bw = nullptr) {
   // plan-sorted pipelines of the first or the variant pass (shared layout)
   constexpr bool kGrouped = !kFull && !kHet;
   typename std::conditional<kZb, ZbSink<S>, RegSink<S>>::type r;
@@ -1836,6 +1853,8 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
       }
     }
     M = class_mb(p);
+    if constexpr (kGrouped && !kZb)
+      if (bw) r.bs = bw + (threadIdx.x & 63u) * S;
     class_setup<kMode, kHet>(t, h, p, slot & 3, r, nullptr);
   }
   int skipped;
@@ -1856,7 +1875,7 @@ __device__ __forceinline__ void eval_one(const Tab& t, const Hot<kMode>& h, cons
   const Plan p2 = S <= kKeepPlanS ? p : load_plan<kHet>(e.packed, e.pcut, slot2);
   if (kGrouped && p2.G > 1) {   // G is the same in the whole wavefront
     if constexpr (kOvl) T = grouped_overlap_tail<S, kMode>(t, h, p2, last, xw);
-    else T = grouped_tail<S, kMode, kZb>(t, h, p2, last, xw);
+    else T = grouped_tail<S, kMode, kZb>(t, h, p2, last, xw, kZb ? nullptr : bw);
   } else {
     T = done ? dp_tail<S, kMode, kHet, kOvl, kFull || kOvl || kZb>(t, h, p2, last,
                                                                    kHet ? e.hdp + (size_t)slot2 * kMaxStages : nullptr)
@@ -2179,8 +2198,13 @@ __global__ void __launch_bounds__(kEvalThreads) k_eval(Tab t, EvalBufs e) {
   const uint32_t stride = gridDim.x * kEvalThreads;
   // the wavefront's row of the plan-sorted groups' LDS exchange area
   double* xw = nullptr;
-  if constexpr (!kHet)
-    xw = (double*)((char*)lds + (kMode < 2 ? t.lds_bytes : 0)) + (threadIdx.x >> 6) * xchg_wave(GRP);
+  uint32_t* bw = nullptr;   // and its stage-placement cache, when the group has one
+  if constexpr (!kHet) {
+    char* const x0 = (char*)lds + (kMode < 2 ? t.lds_bytes : 0);
+    xw = (double*)x0 + (threadIdx.x >> 6) * xchg_wave(GRP);
+    if (GRP < 2 && ((t.bcache >> GRP) & 1))
+      bw = (uint32_t*)(x0 + xchg_bytes(GRP)) + (threadIdx.x >> 6) * bcache_words(GRP);
+  }
   for (uint32_t base = lo + blockIdx.x * kEvalThreads + (threadIdx.x & ~63u); base < hi; base += stride) {
     const uint32_t pos = base + (threadIdx.x & 63u);
     bool pending = pos < hi;
@@ -2220,10 +2244,10 @@ __global__ void __launch_bounds__(kEvalThreads) k_eval(Tab t, EvalBufs e) {
       if (!live) break;
       const uint32_t S0 = __builtin_amdgcn_readfirstlane(__shfl(S, __ffsll((unsigned long long)live) - 1));
       if (pending && S == S0) {
-        if (S0 == kTop) eval_one<kTop, false, kMode, kHet>(t, h, e, slot, xw);
-        else if (S0 == kTop - 1) eval_one<kTop - 1, false, kMode, kHet>(t, h, e, slot, xw);
-        else if (S0 == kTop - 2) eval_one<kTop - 2, false, kMode, kHet>(t, h, e, slot, xw);
-        else eval_one<kTop - 3, false, kMode, kHet>(t, h, e, slot, xw);
+        if (S0 == kTop) eval_one<kTop, false, kMode, kHet>(t, h, e, slot, xw, bw);
+        else if (S0 == kTop - 1) eval_one<kTop - 1, false, kMode, kHet>(t, h, e, slot, xw, bw);
+        else if (S0 == kTop - 2) eval_one<kTop - 2, false, kMode, kHet>(t, h, e, slot, xw, bw);
+        else eval_one<kTop - 3, false, kMode, kHet>(t, h, e, slot, xw, bw);
         pending = false;
       }
     }

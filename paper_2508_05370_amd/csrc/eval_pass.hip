@@ -20,7 +20,8 @@ hipError_t launch_group_v(const Tab& t, const EvalArgs& a, uint32_t max_tasks, i
   const int nb = pass_blocks(max_tasks, kEvalThreads);
   const uint32_t need = nb > 0 ? (uint32_t)nb : 1, grid = 4 * t.grid_eval[g] < need ? 4 * t.grid_eval[g] : need;
   // the shared layout's plan-sorted groups add their plans' DP exchange area
-  const size_t lds = (kMode < 2 ? t.lds_bytes : 0) + (!kHet ? xchg_bytes(g) : 0);
+  const size_t lds = (kMode < 2 ? t.lds_bytes : 0) +
+                    (!kHet ? xchg_bytes(g) + (((t.bcache >> g) & 1) ? bcache_bytes(g) : 0) : 0);
   if (g == 0) k_eval<0, kMode, kHet><<<grid, kEvalThreads, lds, s>>>(t, e);
   else if (g == 1) k_eval<1, kMode, kHet><<<grid, kEvalThreads, lds, s>>>(t, e);
   else if (g == 2) k_eval<2, kMode, kHet><<<grid, kEvalThreads, lds, s>>>(t, e);
@@ -33,17 +34,19 @@ template hipError_t launch_group_v<HETSIM_MODE, (bool)HETSIM_HET>(const Tab&, co
 #if !HETSIM_HET
 // Grid caps come from the shared-layout kernels; the per-class-layout ones
 // take the same caps (their fixed-stride loops cover any grid).
+// bcache: the groups whose stage-placement cache is counted (bit g)
 template <int kMode>
-hipError_t occupancy_first_v(int nb[4], size_t lds) {
+hipError_t occupancy_first_v(int nb[4], size_t lds, uint32_t bcache) {
   const void* k[4] = {(const void*)k_eval<0, kMode, false>, (const void*)k_eval<1, kMode, false>,
                       (const void*)k_eval<2, kMode, false>, (const void*)k_eval<3, kMode, false>};
   for (int i = 0; i < 4; ++i) {
-    hipError_t r = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb[i], k[i], kEvalThreads, lds + xchg_bytes(i));
+    const size_t b = lds + xchg_bytes(i) + (((bcache >> i) & 1) ? bcache_bytes(i) : 0);
+    hipError_t r = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb[i], k[i], kEvalThreads, b);
     if (r != hipSuccess) return r;
   }
   return hipSuccess;
 }
-template hipError_t occupancy_first_v<HETSIM_MODE>(int[4], size_t);
+template hipError_t occupancy_first_v<HETSIM_MODE>(int[4], size_t, uint32_t);
 #endif
 
 #elif HETSIM_PASS == 2

@@ -44,6 +44,12 @@ constexpr uint32_t kXchgPlans = 32;
 __host__ __device__ constexpr uint32_t xchg_row(uint32_t S) { return (S + 3) / 4 * 4 + 2; }
 __host__ __device__ constexpr uint32_t xchg_wave(int group) { return kXchgPlans * xchg_row(kMaxStages - 4 * group); }
 __host__ __device__ constexpr uint32_t xchg_bytes(int group) { return 4 * xchg_wave(group) * 8; }
+// The first pass of the two long stage-count groups keeps each lane's stage
+// placements (first device in the pool, u32 per stage) in LDS from setup to
+// the DP tail, where the plan's lanes read each other's instead of counting
+// them again: 64 lanes x the group's longest stage count per wavefront.
+__host__ __device__ constexpr uint32_t bcache_words(int group) { return group < 2 ? 64u * (kMaxStages - 4 * group) : 0u; }
+__host__ __device__ constexpr uint32_t bcache_bytes(int group) { return 4 * bcache_words(group) * 4; }
 
 // A validated plan packed into 80 contiguous bytes, so that the pipelines of
 // one plan gather it with five 16-byte loads.
@@ -122,6 +128,8 @@ struct Tab {
   uint32_t grid_eval[4];          // blocks of each first-pass kernel that fit the device at once
   uint32_t grid_deferred;
   uint32_t grid_variant[4];       // blocks of each variant-pass kernel that fit the device at once
+  uint32_t bcache;                // bit g: first-pass group g keeps stage placements in LDS (when that
+                                  // costs no occupancy)
 };
 
 // Device buffers of one evaluation pass over a chunk, as the host hands them

@@ -469,10 +469,19 @@ int eval_grids(Tab* t) {
   if (r == hipSuccess) r = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (r != hipSuccess) return (int)r;
   const size_t lds = t->mode < 2 ? t->lds_bytes : 0;
-  int nb[9] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
-  if (t->mode == 0) r = occupancy_first_v<0>(nb, lds);
-  else if (t->mode == 1) r = occupancy_first_v<1>(nb, lds);
-  else r = occupancy_first_v<2>(nb, lds);
+  int nb[9] = {0, 0, 0, 0, 0, 0, 0, 0, 0}, nbc[4] = {0, 0, 0, 0};
+  if (t->mode == 0) r = occupancy_first_v<0>(nb, lds, 0);
+  else if (t->mode == 1) r = occupancy_first_v<1>(nb, lds, 0);
+  else r = occupancy_first_v<2>(nb, lds, 0);
+  // the stage-placement cache of the first pass's long groups, where it costs no blocks
+  if (r == hipSuccess) {
+    if (t->mode == 0) r = occupancy_first_v<0>(nbc, lds, 3u);
+    else if (t->mode == 1) r = occupancy_first_v<1>(nbc, lds, 3u);
+    else r = occupancy_first_v<2>(nbc, lds, 3u);
+  }
+  t->bcache = 0;
+  for (int i = 0; i < 2; ++i)
+    if (nbc[i] == nb[i]) t->bcache |= 1u << i;
   if (r == hipSuccess) {
     if (t->mode == 0) r = occupancy_deferred_v<0>(nb + 4, lds);
     else if (t->mode == 1) r = occupancy_deferred_v<1>(nb + 4, lds);

@@ -19,7 +19,7 @@ hipError_t launch_deferred_v(const Tab& t, const EvalArgs& a, uint32_t max_tasks
 template <int kMode>
 hipError_t launch_variant_v(const Tab& t, const EvalArgs& a, int g, hipStream_t s);
 template <int kMode>
-hipError_t occupancy_first_v(int nb[4], size_t lds);
+hipError_t occupancy_first_v(int nb[4], size_t lds, uint32_t bcache);
 template <int kMode>
 hipError_t occupancy_variant_v(int nb[4], size_t lds);
 template <int kMode>
@@ -41,9 +41,9 @@ extern template hipError_t launch_variant_v<2>(const Tab&, const EvalArgs&, int,
 extern template hipError_t occupancy_variant_v<0>(int[4], size_t);
 extern template hipError_t occupancy_variant_v<1>(int[4], size_t);
 extern template hipError_t occupancy_variant_v<2>(int[4], size_t);
-extern template hipError_t occupancy_first_v<0>(int[4], size_t);
-extern template hipError_t occupancy_first_v<1>(int[4], size_t);
-extern template hipError_t occupancy_first_v<2>(int[4], size_t);
+extern template hipError_t occupancy_first_v<0>(int[4], size_t, uint32_t);
+extern template hipError_t occupancy_first_v<1>(int[4], size_t, uint32_t);
+extern template hipError_t occupancy_first_v<2>(int[4], size_t, uint32_t);
 extern template hipError_t occupancy_deferred_v<0>(int[1], size_t);
 extern template hipError_t occupancy_deferred_v<1>(int[1], size_t);
 extern template hipError_t occupancy_deferred_v<2>(int[1], size_t);
