@@ -6,11 +6,10 @@ of every replica class, the DP sync, and the argmin over all plans.  Plans are
 resident in HBM before timing starts.
 
 Prints one JSON line.  Roofline: the evaluation is bound by VALU issue.  The
-work of one call is counted from the plans themselves (the design doc states the
-unit): every schedule node the evaluation executes -- all nodes of the 1F1B
-recurrence (3 fp64 VALU ops per node with a cross-stage input, 1 without),
-less those the periodic shortcut skips, which the library counts on the
-device -- plus the cost model's per-stage and per-plan setup arithmetic priced
+work of one call is counted from the plans themselves: every schedule node
+the evaluation executes -- all nodes of the 1F1B recurrence (3 fp64 VALU
+ops per node with a cross-stage input, 1 without), less those the periodic
+shortcut skips, which the library counts on the device -- plus the cost model's per-stage and per-plan setup arithmetic priced
 by formula.  The peak is the lower of the chip's issue rate (256 CUs x 64
 lanes x 2.4 GHz) and the node probe's measured rate times 3, measured in the
 same run.
@@ -337,7 +336,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if a.gpus != 1 or world != 1:
         print("bench.py evaluates on exactly one GPU: plans shard by index across GPUs with one 16-byte "
-              "argmin exchange, which this build does not run; use --gpus 1", file=sys.stderr)
+              "argmin exchange, which this benchmark does not run; use --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import torch
